@@ -1,0 +1,481 @@
+/*
+ * e2fo.c -- fp64 CPU oracle of the Wigner-6j convolution (E2Former,
+ * arXiv 2501.19216).  TEST INFRASTRUCTURE ONLY: nothing in the product
+ * library links, loads or calls this file; it is used by the tests, the
+ * smoke check and the CPU-baseline leg of the benchmark.
+ *
+ * It is plain, slow and written to be checked against the paper by eye:
+ *   - Wigner 3j symbol by Racah's closed form (App. C.1);
+ *   - complex Clebsch-Gordan coefficients from the 3j symbol (Condon-Shortley);
+ *   - real-basis CG (Def. 2.2) by the unitary complex->real change of basis
+ *     of the real spherical harmonics of Def. 2.1 (sin for m<0, cos for m>0,
+ *     no Condon-Shortley sign in the real functions);
+ *   - real regular solid harmonics R^(l) as the stretched power
+ *     R^(l) = [R^(l-1) (x) R^(1)]^(l), R^(1)(v) = (y, z, x) (Def. 2.1 and the
+ *     projection identity of Thm. 3.2);
+ *   - Wigner 6j symbol by Racah's single-sum formula (App. C.2; the four-3j
+ *     sum printed there has inconsistent m indices and is not used);
+ *   - the recoupling weights X of Def. 2.3 as an overlap of coupling trees;
+ *   - the radius graph: every ordered pair i != j of one graph with
+ *     |r_i - r_j| < cutoff, evaluated exactly on the 2^-16 A grid;
+ *   - the layer by its definition (Def. 3.1 with attention weights, App. D.2
+ *     setup): y_i = sum_j alpha_ij sum_{a,f} w_afo [h_j^(a) (x) R^(f)(r_i - r_j)]^(o);
+ *   - the layer by the node factorisation of Thm. 3.3 / Alg. 1 (for the
+ *     equality check of the two forms only);
+ *   - the per-irrep linear channel mix of App. F.
+ *
+ * Accumulation is in double; the row loops are parallel (OpenMP) over
+ * receivers, each row summed in ascending sender order.
+ */
+#include <complex.h>
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define MAXL 12 /* largest degree any table here is asked for */
+
+static int iabs_(int x) { return x < 0 ? -x : x; }
+static int imin_(int a, int b) { return a < b ? a : b; }
+static int imax_(int a, int b) { return a > b ? a : b; }
+static double sgn_pow(int k) { return (k % 2 == 0) ? 1.0 : -1.0; } /* (-1)^k, k may be < 0 */
+
+static long double fact(int n) {
+    long double r = 1.0L;
+    for (int k = 2; k <= n; ++k) r *= (long double)k;
+    return r;
+}
+
+static int triangle(int a, int b, int c) { return c >= iabs_(a - b) && c <= a + b; }
+
+/* ---------- Wigner 3j: Racah's closed form (App. C.1) ---------- */
+double e2fo_wigner3j(int j1, int j2, int j3, int m1, int m2, int m3) {
+    if (m1 + m2 + m3 != 0) return 0.0;
+    if (!triangle(j1, j2, j3)) return 0.0;
+    if (iabs_(m1) > j1 || iabs_(m2) > j2 || iabs_(m3) > j3) return 0.0;
+    long double tri = fact(j1 + j2 - j3) * fact(j1 - j2 + j3) * fact(-j1 + j2 + j3) / fact(j1 + j2 + j3 + 1);
+    long double mm = fact(j1 + m1) * fact(j1 - m1) * fact(j2 + m2) * fact(j2 - m2) * fact(j3 + m3) * fact(j3 - m3);
+    int zmin = imax_(0, imax_(j2 - j3 - m1, j1 - j3 + m2));
+    int zmax = imin_(j1 + j2 - j3, imin_(j1 - m1, j2 + m2));
+    long double s = 0.0L;
+    for (int z = zmin; z <= zmax; ++z) {
+        long double den = fact(z) * fact(j1 + j2 - j3 - z) * fact(j1 - m1 - z) * fact(j2 + m2 - z) *
+                          fact(j3 - j2 + m1 + z) * fact(j3 - j1 - m2 + z);
+        s += ((z % 2) ? -1.0L : 1.0L) / den;
+    }
+    return (double)(sgn_pow(j1 - j2 - m3) * sqrtl(tri) * sqrtl(mm) * s);
+}
+
+/* Complex (Condon-Shortley) CG <l1 m1; l2 m2 | l3 m3> from the 3j symbol. */
+double e2fo_cg_complex(int l1, int m1, int l2, int m2, int l3, int m3) {
+    return sgn_pow(l1 - l2 + m3) * sqrt(2.0 * l3 + 1.0) * e2fo_wigner3j(l1, l2, l3, m1, m2, -m3);
+}
+
+/* Row m' (real function index) of the complex->real map S = U Y for degree l:
+ * m'>0: S = ((-1)^m' Y^m' + Y^-m')/sqrt2 ; m'<0: S = i (Y^-|m'| - (-1)^|m'| Y^|m'|)/sqrt2. */
+static double complex umat(int l, int mp, int m) {
+    (void)l;
+    const double r = 1.0 / sqrt(2.0);
+    if (mp == 0) return (m == 0) ? 1.0 : 0.0;
+    if (mp > 0) {
+        if (m == mp) return sgn_pow(mp) * r;
+        if (m == -mp) return r;
+        return 0.0;
+    }
+    int mu = -mp;
+    if (m == -mu) return I * r;
+    if (m == mu) return -I * sgn_pow(mu) * r;
+    return 0.0;
+}
+
+/* Real-basis CG for (l1,l2,l3): out[(m1+l1)][(m2+l2)][(m3+l3)] such that
+ * [A (x) B]^(l3)_m3 = sum C[m1][m2][m3] A_m1 B_m2 for real-basis irreps A, B.
+ * The transformed coefficients are purely real when l1+l2+l3 is even and
+ * purely imaginary when odd; the real part (even) or the imaginary part
+ * (odd) is returned.  Returns 0 on success, 1 if the discarded part was not
+ * negligible (a convention error), 2 if the triangle rule fails. */
+int e2fo_cg_real(int l1, int l2, int l3, double *out) {
+    int n1 = 2 * l1 + 1, n2 = 2 * l2 + 1, n3 = 2 * l3 + 1;
+    memset(out, 0, sizeof(double) * n1 * n2 * n3);
+    if (!triangle(l1, l2, l3)) return 2;
+    int odd = (l1 + l2 + l3) % 2;
+    double worst = 0.0;
+    for (int p1 = -l1; p1 <= l1; ++p1)
+        for (int p2 = -l2; p2 <= l2; ++p2)
+            for (int p3 = -l3; p3 <= l3; ++p3) {
+                double complex acc = 0.0;
+                for (int m1 = -l1; m1 <= l1; ++m1) {
+                    double complex u1 = conj(umat(l1, p1, m1));
+                    if (u1 == 0.0) continue;
+                    for (int m2 = -l2; m2 <= l2; ++m2) {
+                        double complex u2 = conj(umat(l2, p2, m2));
+                        if (u2 == 0.0) continue;
+                        int m3 = m1 + m2;
+                        if (iabs_(m3) > l3) continue;
+                        double complex u3 = umat(l3, p3, m3);
+                        if (u3 == 0.0) continue;
+                        acc += u3 * e2fo_cg_complex(l1, m1, l2, m2, l3, m3) * u1 * u2;
+                    }
+                }
+                double keep = odd ? cimag(acc) : creal(acc);
+                double drop = odd ? creal(acc) : cimag(acc);
+                if (fabs(drop) > worst) worst = fabs(drop);
+                out[((p1 + l1) * n2 + (p2 + l2)) * n3 + (p3 + l3)] = keep;
+            }
+    return worst > 1e-12 ? 1 : 0;
+}
+
+/* ---------- cached real CG tables for degrees <= MAXL ---------- */
+static double *g_cg[MAXL + 1][MAXL + 1][2 * MAXL + 1];
+
+static const double *cg(int l1, int l2, int l3) {
+    if (!g_cg[l1][l2][l3]) {
+        int n = (2 * l1 + 1) * (2 * l2 + 1) * (2 * l3 + 1);
+        double *t = (double *)malloc(sizeof(double) * n);
+        e2fo_cg_real(l1, l2, l3, t);
+        g_cg[l1][l2][l3] = t;
+    }
+    return g_cg[l1][l2][l3];
+}
+
+/* Fill every table up to the given degrees before threads read them. */
+static void warm_cg(int lmax_in, int lmax_out) {
+    for (int a = 0; a <= lmax_in; ++a)
+        for (int b = 0; b <= lmax_in; ++b)
+            for (int c = iabs_(a - b); c <= imin_(a + b, lmax_out); ++c) cg(a, b, c);
+}
+
+/* CG coupling of two real irreps: out[m3] = sum C[m1][m2][m3] x[m1] y[m2]. */
+static void couple(int l1, const double *x, int l2, const double *y, int l3, double *out) {
+    const double *c = cg(l1, l2, l3);
+    int n2 = 2 * l2 + 1, n3 = 2 * l3 + 1;
+    for (int k = 0; k < n3; ++k) out[k] = 0.0;
+    for (int i = 0; i < 2 * l1 + 1; ++i)
+        for (int j = 0; j < n2; ++j) {
+            double xy = x[i] * y[j];
+            if (xy == 0.0) continue;
+            for (int k = 0; k < n3; ++k) out[k] += c[(i * n2 + j) * n3 + k] * xy;
+        }
+}
+
+/* ---------- real regular solid harmonics (Def. 2.1), stretched power ---------- */
+void e2fo_solid_harmonics(int lmax, const double *v, double *out) {
+    out[0] = 1.0;
+    if (lmax < 1) return;
+    double r1[3] = {v[1], v[2], v[0]}; /* m = -1, 0, +1  <->  y, z, x */
+    out[1] = r1[0]; out[2] = r1[1]; out[3] = r1[2];
+    for (int l = 2; l <= lmax; ++l) couple(l - 1, out + (l - 1) * (l - 1), 1, r1, l, out + l * l);
+}
+
+/* ---------- Wigner 6j: Racah's single-sum formula ---------- */
+static long double delta_tri(int a, int b, int c) {
+    return sqrtl(fact(a + b - c) * fact(a - b + c) * fact(-a + b + c) / fact(a + b + c + 1));
+}
+
+double e2fo_wigner6j(int j1, int j2, int j3, int j4, int j5, int j6) {
+    if (!triangle(j1, j2, j3) || !triangle(j1, j5, j6) || !triangle(j4, j2, j6) || !triangle(j4, j5, j3)) return 0.0;
+    int a1 = j1 + j2 + j3, a2 = j1 + j5 + j6, a3 = j4 + j2 + j6, a4 = j4 + j5 + j3;
+    int b1 = j1 + j2 + j4 + j5, b2 = j2 + j3 + j5 + j6, b3 = j3 + j1 + j6 + j4;
+    int tmin = imax_(imax_(a1, a2), imax_(a3, a4));
+    int tmax = imin_(b1, imin_(b2, b3));
+    long double s = 0.0L;
+    for (int t = tmin; t <= tmax; ++t) {
+        long double den = fact(t - a1) * fact(t - a2) * fact(t - a3) * fact(t - a4) * fact(b1 - t) * fact(b2 - t) * fact(b3 - t);
+        s += ((t % 2) ? -1.0L : 1.0L) * fact(t + 1) / den;
+    }
+    return (double)(delta_tri(j1, j2, j3) * delta_tri(j1, j5, j6) * delta_tri(j4, j2, j6) * delta_tri(j4, j5, j3) * s);
+}
+
+/* ---------- recoupling weights (Def. 2.3) as an overlap of coupling trees ----------
+ * With A of degree a, B of degree b, C of degree u and f = b + u:
+ *   [A (x) [C (x) B]^(f)]^(o) = sum_d X_d [C (x) [A (x) B]^(d)]^(o).
+ * T2[al,be,ga,M]   = sum_ka C^{f ka}_{u ga, b be} C^{o M}_{a al, f ka}   (left tree)
+ * T1_d[al,be,ga,M] = sum_de C^{d de}_{a al, b be} C^{o M}_{u ga, d de}   (right tree)
+ * The right trees are orthogonal with squared norm 2o+1 (CG orthogonality,
+ * App. C.1), so X_d = <T2, T1_d> / (2o+1). */
+double e2fo_recoupling_x(int a, int b, int u, int o, int d) {
+    int f = b + u;
+    if (!triangle(a, f, o) || !triangle(a, b, d) || !triangle(u, d, o)) return 0.0;
+    const double *cub_f = cg(u, b, f), *caf_o = cg(a, f, o), *cab_d = cg(a, b, d), *cud_o = cg(u, d, o);
+    int na = 2 * a + 1, nb = 2 * b + 1, nu = 2 * u + 1, no = 2 * o + 1, nf = 2 * f + 1, nd = 2 * d + 1;
+    double acc = 0.0;
+    for (int al = 0; al < na; ++al)
+        for (int be = 0; be < nb; ++be)
+            for (int ga = 0; ga < nu; ++ga)
+                for (int M = 0; M < no; ++M) {
+                    double t2 = 0.0, t1 = 0.0;
+                    for (int ka = 0; ka < nf; ++ka)
+                        t2 += cub_f[(ga * nb + be) * nf + ka] * caf_o[(al * nf + ka) * no + M];
+                    for (int de = 0; de < nd; ++de)
+                        t1 += cab_d[(al * nb + be) * nd + de] * cud_o[(ga * nd + de) * no + M];
+                    acc += t2 * t1;
+                }
+    return acc / (double)no;
+}
+
+/* ---------- radius graph (Alg. 1 step 2), exact on the 2^-16 grid ---------- */
+static int in_range(const float *pos, int i, int j, double r2) {
+    double d2 = 0.0;
+    for (int k = 0; k < 3; ++k) {
+        int64_t xi = llrint((double)pos[3 * i + k] * 65536.0), xj = llrint((double)pos[3 * j + k] * 65536.0);
+        int64_t dx = xi - xj;
+        d2 += (double)(dx * dx); /* integers below 2^53: exact */
+    }
+    return d2 < r2;
+}
+
+/* Every ordered pair (i, j), i != j, of one graph with |r_i - r_j| < cutoff.
+ * Rows ascending in j.  Returns E; col_idx is written only if E <= cap. */
+int64_t e2fo_neighbor_list(const float *pos, const int32_t *graph_id, int n, float cutoff, int64_t *row_ptr,
+                           int32_t *col_idx, int64_t cap) {
+    double rc = (double)cutoff * 65536.0;
+    double r2 = rc * rc;
+    int64_t *cnt = (int64_t *)calloc((size_t)n, sizeof(int64_t));
+#pragma omp parallel for schedule(dynamic, 64)
+    for (int i = 0; i < n; ++i) {
+        int64_t c = 0;
+        for (int j = 0; j < n; ++j)
+            if (j != i && (!graph_id || graph_id[i] == graph_id[j]) && in_range(pos, i, j, r2)) ++c;
+        cnt[i] = c;
+    }
+    row_ptr[0] = 0;
+    for (int i = 0; i < n; ++i) row_ptr[i + 1] = row_ptr[i] + cnt[i];
+    int64_t E = row_ptr[n];
+    free(cnt);
+    if (!col_idx || E > cap) return E;
+#pragma omp parallel for schedule(dynamic, 64)
+    for (int i = 0; i < n; ++i) {
+        int64_t e = row_ptr[i];
+        for (int j = 0; j < n; ++j)
+            if (j != i && (!graph_id || graph_id[i] == graph_id[j]) && in_range(pos, i, j, r2)) col_idx[e++] = j;
+    }
+    return E;
+}
+
+/* The same graph through a uniform cell grid (cell side >= cutoff), for
+ * systems where the all-pairs loop is too slow.  Same predicate, same
+ * ascending rows (each row is sorted after collection). */
+static int cmp_i32(const void *x, const void *y) {
+    int32_t a = *(const int32_t *)x, b = *(const int32_t *)y;
+    return (a > b) - (a < b);
+}
+
+int64_t e2fo_neighbor_list_cells(const float *pos, const int32_t *graph_id, int n, float cutoff, int64_t *row_ptr,
+                                 int32_t *col_idx, int64_t cap) {
+    double rc = (double)cutoff * 65536.0, r2 = rc * rc;
+    double lo[3] = {1e300, 1e300, 1e300}, hi[3] = {-1e300, -1e300, -1e300};
+    for (int i = 0; i < n; ++i)
+        for (int k = 0; k < 3; ++k) {
+            double x = pos[3 * i + k];
+            if (x < lo[k]) lo[k] = x;
+            if (x > hi[k]) hi[k] = x;
+        }
+    int dim[3];
+    for (int k = 0; k < 3; ++k) {
+        dim[k] = (int)floor((hi[k] - lo[k]) / (double)cutoff) + 1;
+        if (dim[k] < 1) dim[k] = 1;
+    }
+    int64_t ncell = (int64_t)dim[0] * dim[1] * dim[2];
+    int *cell = (int *)malloc(sizeof(int) * (size_t)n);
+    int64_t *start = (int64_t *)calloc((size_t)ncell + 1, sizeof(int64_t));
+    int *members = (int *)malloc(sizeof(int) * (size_t)n);
+    for (int i = 0; i < n; ++i) {
+        int c[3];
+        for (int k = 0; k < 3; ++k) {
+            c[k] = (int)floor(((double)pos[3 * i + k] - lo[k]) / (double)cutoff);
+            if (c[k] >= dim[k]) c[k] = dim[k] - 1;
+        }
+        cell[i] = (c[2] * dim[1] + c[1]) * dim[0] + c[0];
+        start[cell[i] + 1]++;
+    }
+    for (int64_t c = 0; c < ncell; ++c) start[c + 1] += start[c];
+    int64_t *fillp = (int64_t *)malloc(sizeof(int64_t) * (size_t)ncell);
+    memcpy(fillp, start, sizeof(int64_t) * (size_t)ncell);
+    for (int i = 0; i < n; ++i) members[fillp[cell[i]]++] = i;
+    free(fillp);
+    int64_t *cnt = (int64_t *)calloc((size_t)n, sizeof(int64_t));
+    for (int pass = 0; pass < 2; ++pass) {
+        if (pass == 1) {
+            row_ptr[0] = 0;
+            for (int i = 0; i < n; ++i) row_ptr[i + 1] = row_ptr[i] + cnt[i];
+            if (!col_idx || row_ptr[n] > cap) break;
+        }
+#pragma omp parallel for schedule(dynamic, 64)
+        for (int i = 0; i < n; ++i) {
+            int ci = cell[i];
+            int cx = ci % dim[0], cy = (ci / dim[0]) % dim[1], cz = ci / (dim[0] * dim[1]);
+            int64_t c = 0, e = pass ? row_ptr[i] : 0;
+            for (int dz = -1; dz <= 1; ++dz)
+                for (int dy = -1; dy <= 1; ++dy)
+                    for (int dx = -1; dx <= 1; ++dx) {
+                        int x = cx + dx, y = cy + dy, z = cz + dz;
+                        if (x < 0 || y < 0 || z < 0 || x >= dim[0] || y >= dim[1] || z >= dim[2]) continue;
+                        int64_t cc = ((int64_t)z * dim[1] + y) * dim[0] + x;
+                        for (int64_t q = start[cc]; q < start[cc + 1]; ++q) {
+                            int j = members[q];
+                            if (j != i && (!graph_id || graph_id[i] == graph_id[j]) && in_range(pos, i, j, r2)) {
+                                if (pass) col_idx[e++] = j;
+                                else ++c;
+                            }
+                        }
+                    }
+            if (pass) qsort(col_idx + row_ptr[i], (size_t)(row_ptr[i + 1] - row_ptr[i]), sizeof(int32_t), cmp_i32);
+            else cnt[i] = c;
+        }
+    }
+    int64_t E = row_ptr[n];
+    free(cnt); free(cell); free(start); free(members);
+    return E;
+}
+
+/* ---------- the layer by its definition (Def. 3.1 with attention weights) ----------
+ * y_i^(o)[m,c] = sum_{j in N(i)} alpha[e(i,j), c/dh] sum_{a,f} w[a][f][o]
+ *                  sum_{ma,mf} C^{o m}_{a ma, f mf} h_j^(a)[ma,c] R^(f)_mf(r_i - r_j)
+ * Only the listed rows are evaluated (the definition is separable per row).
+ * out: [n_rows][(L+1)^2][C]. */
+int e2fo_conv_edge(int L, int C, int H, const float *pos, const float *feat, int n, const int64_t *row_ptr,
+                   const int32_t *col_idx, const float *alpha, const double *path_w, const int32_t *rows, int n_rows,
+                   double *out) {
+    if (L < 0 || L > 6 || C < 1 || H < 1 || C % H) return 1;
+    (void)n;
+    int nk = (L + 1) * (L + 1), dh = C / H;
+    warm_cg(L, L);
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int r = 0; r < n_rows; ++r) {
+        int i = rows[r];
+        double *y = out + (size_t)r * nk * C;
+        memset(y, 0, sizeof(double) * (size_t)nk * C);
+        double R[49];
+        for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+            int j = col_idx[e];
+            double v[3] = {(double)pos[3 * i] - pos[3 * j], (double)pos[3 * i + 1] - pos[3 * j + 1],
+                           (double)pos[3 * i + 2] - pos[3 * j + 2]};
+            e2fo_solid_harmonics(L, v, R);
+            const float *hj = feat + (size_t)j * nk * C;
+            for (int a = 0; a <= L; ++a)
+                for (int f = 0; f <= L; ++f)
+                    for (int o = iabs_(a - f); o <= imin_(a + f, L); ++o) {
+                        double w = path_w[(a * (L + 1) + f) * (L + 1) + o];
+                        if (w == 0.0) continue;
+                        const double *c3 = cg(a, f, o);
+                        for (int ma = 0; ma < 2 * a + 1; ++ma)
+                            for (int mf = 0; mf < 2 * f + 1; ++mf)
+                                for (int m = 0; m < 2 * o + 1; ++m) {
+                                    double cgv = c3[(ma * (2 * f + 1) + mf) * (2 * o + 1) + m];
+                                    if (cgv == 0.0) continue;
+                                    double k = w * cgv * R[f * f + mf];
+                                    const float *hrow = hj + (size_t)(a * a + ma) * C;
+                                    double *yrow = y + (size_t)(o * o + m) * C;
+                                    for (int c = 0; c < C; ++c)
+                                        yrow[c] += (double)alpha[e * H + c / dh] * k * (double)hrow[c];
+                                }
+                    }
+        }
+    }
+    return 0;
+}
+
+/* ---------- the layer by node factorisation (Thm. 3.3, Alg. 1) ----------
+ * p = r - origin.  T_j^(a,b,d) = [h_j^(a) (x) R^(b)(p_j)]^(d) for every
+ * triangle-valid (a,b,d);  S_i = sum_j alpha_ij T_j;
+ * y_i^(o) = sum_{a,f} w_afo sum_{u=0}^{f} (-1)^(f-u) binom(f,u)
+ *           sum_d X(a, f-u, u, o; d) [R^(u)(p_i) (x) S_i^(a,f-u,d)]^(o).
+ * Dense scratch of size n * (L+1)^2 * (2L+1) * (4L+1) * C doubles: tiny
+ * graphs only.  out: [n][(L+1)^2][C]. */
+static double binom_(int n, int k) {
+    double r = 1.0;
+    for (int t = 1; t <= k; ++t) r = r * (n - k + t) / t;
+    return r;
+}
+
+int e2fo_conv_factorised(int L, int C, int H, const float *pos, const float *feat, int n, const int64_t *row_ptr,
+                         const int32_t *col_idx, const float *alpha, const double *path_w, const double *origin,
+                         double *out) {
+    if (L < 0 || L > 6 || C < 1 || H < 1 || C % H) return 1;
+    int nk = (L + 1) * (L + 1), dh = C / H, L1 = L + 1, DM = 4 * L + 1;
+    warm_cg(2 * L, 2 * L);
+    /* T index: [node][a][b][d][delta][c] with d in 0..2L, delta < 4L+1 */
+    size_t per_node = (size_t)L1 * L1 * (2 * L + 1) * DM * C;
+    double *T = (double *)calloc((size_t)n * per_node, sizeof(double));
+    double *S = (double *)calloc((size_t)n * per_node, sizeof(double));
+    double *Rp = (double *)malloc(sizeof(double) * (size_t)n * nk);
+    if (!T || !S || !Rp) { free(T); free(S); free(Rp); return 2; }
+#define TIDX(node, a, b, d, de, c) ((((((size_t)(node) * L1 + (a)) * L1 + (b)) * (2 * L + 1) + (d)) * DM + (de)) * C + (c))
+    for (int i = 0; i < n; ++i) {
+        double p[3] = {(double)pos[3 * i] - origin[0], (double)pos[3 * i + 1] - origin[1], (double)pos[3 * i + 2] - origin[2]};
+        e2fo_solid_harmonics(L, p, Rp + (size_t)i * nk);
+    }
+    /* j-side tensor products (red box of Thm. 3.3; T_k of Alg. 1) */
+    for (int j = 0; j < n; ++j)
+        for (int a = 0; a <= L; ++a)
+            for (int b = 0; b <= L; ++b)
+                for (int d = iabs_(a - b); d <= a + b; ++d) {
+                    const double *c3 = cg(a, b, d);
+                    const double *Rb = Rp + (size_t)j * nk + b * b;
+                    for (int al = 0; al < 2 * a + 1; ++al)
+                        for (int be = 0; be < 2 * b + 1; ++be)
+                            for (int de = 0; de < 2 * d + 1; ++de) {
+                                double k = c3[(al * (2 * b + 1) + be) * (2 * d + 1) + de] * Rb[be];
+                                if (k == 0.0) continue;
+                                for (int c = 0; c < C; ++c)
+                                    T[TIDX(j, a, b, d, de, c)] += k * (double)feat[((size_t)j * nk + a * a + al) * C + c];
+                            }
+                }
+    /* attention-weighted aggregation (einsum "ijh,jhds->ihds" of Alg. 1) */
+    for (int i = 0; i < n; ++i)
+        for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+            int j = col_idx[e];
+            for (size_t q = 0; q < per_node; ++q) {
+                int c = (int)(q % (size_t)C);
+                S[(size_t)i * per_node + q] += (double)alpha[e * H + c / dh] * T[(size_t)j * per_node + q];
+            }
+        }
+    /* i-side recoupling (blue box of Thm. 3.3; Wigner6jTP of Alg. 1) */
+    memset(out, 0, sizeof(double) * (size_t)n * nk * C);
+    for (int i = 0; i < n; ++i)
+        for (int a = 0; a <= L; ++a)
+            for (int f = 0; f <= L; ++f)
+                for (int o = iabs_(a - f); o <= imin_(a + f, L); ++o) {
+                    double w = path_w[(a * L1 + f) * L1 + o];
+                    if (w == 0.0) continue;
+                    for (int u = 0; u <= f; ++u) {
+                        int b = f - u;
+                        double coef = w * sgn_pow(f - u) * binom_(f, u);
+                        for (int d = iabs_(a - b); d <= a + b; ++d) {
+                            double x = e2fo_recoupling_x(a, b, u, o, d);
+                            if (x == 0.0) continue;
+                            const double *c3 = cg(u, d, o);
+                            const double *Ru = Rp + (size_t)i * nk + u * u;
+                            for (int ga = 0; ga < 2 * u + 1; ++ga)
+                                for (int de = 0; de < 2 * d + 1; ++de)
+                                    for (int m = 0; m < 2 * o + 1; ++m) {
+                                        double k = coef * x * c3[(ga * (2 * d + 1) + de) * (2 * o + 1) + m] * Ru[ga];
+                                        if (k == 0.0) continue;
+                                        double *yrow = out + ((size_t)i * nk + o * o + m) * C;
+                                        for (int c = 0; c < C; ++c) yrow[c] += k * S[TIDX(i, a, b, d, de, c)];
+                                    }
+                        }
+                    }
+                }
+#undef TIDX
+    free(T); free(S); free(Rp);
+    return 0;
+}
+
+/* ---------- per-irrep linear self-mix (App. F) ----------
+ * out[i][(o,m)][c'] = sum_c W[o][c'][c] y[i][(o,m)][c]. */
+void e2fo_mix(int L, int C, int n_rows, const double *y, const float *W, double *out) {
+    int nk = (L + 1) * (L + 1);
+#pragma omp parallel for schedule(static)
+    for (int r = 0; r < n_rows; ++r)
+        for (int o = 0; o <= L; ++o)
+            for (int m = 0; m < 2 * o + 1; ++m) {
+                const double *yrow = y + ((size_t)r * nk + o * o + m) * C;
+                double *orow = out + ((size_t)r * nk + o * o + m) * C;
+                for (int cp = 0; cp < C; ++cp) {
+                    double s = 0.0;
+                    for (int c = 0; c < C; ++c) s += (double)W[((size_t)o * C + cp) * C + c] * yrow[c];
+                    orow[cp] = s;
+                }
+            }
+}

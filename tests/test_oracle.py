@@ -1,0 +1,447 @@
+"""Pins of the fp64 oracle against closed forms and invariants (CPU only).
+
+Each test names the passage of arXiv 2501.19216 (or the textbook identity)
+that fixes the expected value.  A plausible mistake anywhere in the oracle
+(a dropped term, a wrong sign or index, a transposed operand) fails one of
+them.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+from scipy.special import lpmv
+
+import e2f_synth as syn
+import oracle as o
+
+
+def tri(a, b, c):
+    return abs(a - b) <= c <= a + b
+
+
+# ---------------------------------------------------------------- 3j / CG
+def test_3j_textbook_values():
+    # standard tabulated values (e.g. Edmonds, Table 2)
+    assert o.wigner3j(1, 1, 0, 0, 0, 0) == pytest.approx(-1 / math.sqrt(3), abs=1e-15)
+    assert o.wigner3j(1, 1, 2, 0, 0, 0) == pytest.approx(math.sqrt(2 / 15), abs=1e-15)
+    assert o.wigner3j(2, 2, 2, 0, 0, 0) == pytest.approx(-math.sqrt(2 / 35), abs=1e-15)
+    assert o.wigner3j(1, 1, 1, 1, -1, 0) == pytest.approx(1 / math.sqrt(6), abs=1e-15)
+    assert o.cg_complex(1, 0, 1, 0, 0, 0) == pytest.approx(-1 / math.sqrt(3), abs=1e-15)
+    assert o.cg_complex(1, 1, 1, 0, 2, 1) == pytest.approx(1 / math.sqrt(2), abs=1e-15)
+    # selection rules (App. C.1)
+    assert o.wigner3j(1, 1, 1, 1, 0, 0) == 0.0
+    assert o.wigner3j(1, 1, 3, 0, 0, 0) == 0.0
+
+
+def test_3j_special_closed_forms():
+    for j in range(0, 9):
+        for m in range(-j, j + 1):
+            # (j j 0; m -m 0) = (-1)^(j-m)/sqrt(2j+1)
+            assert o.wigner3j(j, j, 0, m, -m, 0) == pytest.approx((-1) ** (j - m) / math.sqrt(2 * j + 1), abs=1e-14)
+    f = math.factorial
+    for j1, j2 in itertools.product(range(5), range(5)):
+        J = j1 + j2
+        for m1 in range(-j1, j1 + 1):
+            for m2 in range(-j2, j2 + 1):
+                M = m1 + m2
+                # stretched coupling, closed form
+                v = (-1) ** (j1 - j2 + M) * math.sqrt(f(2 * j1) * f(2 * j2) * f(J + M) * f(J - M) /
+                                                     (f(2 * J + 1) * f(j1 + m1) * f(j1 - m1) * f(j2 + m2) * f(j2 - m2)))
+                assert o.wigner3j(j1, j2, J, m1, m2, -M) == pytest.approx(v, abs=1e-14)
+    # coupling with j2 = 1, m2 = 0 (Condon-Shortley closed forms)
+    for j in range(1, 9):
+        for m in range(-j, j + 1):
+            assert o.cg_complex(j, m, 1, 0, j + 1, m) == pytest.approx(
+                math.sqrt((j - m + 1) * (j + m + 1) / ((2 * j + 1) * (j + 1))), abs=1e-14)
+            assert o.cg_complex(j, m, 1, 0, j, m) == pytest.approx(m / math.sqrt(j * (j + 1)), abs=1e-14)
+            assert o.cg_complex(j, m, 1, 0, j - 1, m) == pytest.approx(
+                -math.sqrt((j - m) * (j + m) / (j * (2 * j + 1))), abs=1e-14)
+
+
+def test_3j_symmetries_and_orthogonality():
+    # App. C.1: column permutations, m reversal, both orthogonality sums
+    for j1, j2, j3 in itertools.product(range(5), repeat=3):
+        if not tri(j1, j2, j3):
+            continue
+        ph = (-1) ** (j1 + j2 + j3)
+        for m1 in range(-j1, j1 + 1):
+            for m2 in range(-j2, j2 + 1):
+                m3 = -m1 - m2
+                if abs(m3) > j3:
+                    continue
+                v = o.wigner3j(j1, j2, j3, m1, m2, m3)
+                assert o.wigner3j(j2, j3, j1, m2, m3, m1) == pytest.approx(v, abs=1e-14)
+                assert o.wigner3j(j2, j1, j3, m2, m1, m3) == pytest.approx(ph * v, abs=1e-14)
+                assert o.wigner3j(j1, j2, j3, -m1, -m2, -m3) == pytest.approx(ph * v, abs=1e-14)
+    for j1, j2 in itertools.product(range(4), repeat=2):
+        for j3 in range(abs(j1 - j2), j1 + j2 + 1):
+            for j3p in range(abs(j1 - j2), j1 + j2 + 1):
+                for m3 in range(-j3, j3 + 1):
+                    for m3p in range(-j3p, j3p + 1):
+                        s = sum((2 * j3 + 1) * o.wigner3j(j1, j2, j3, m1, m2, m3) * o.wigner3j(j1, j2, j3p, m1, m2, m3p)
+                                for m1 in range(-j1, j1 + 1) for m2 in range(-j2, j2 + 1))
+                        assert s == pytest.approx(float(j3 == j3p and m3 == m3p), abs=1e-13)
+        for m1, m2, m1p, m2p in itertools.product(range(-j1, j1 + 1), range(-j2, j2 + 1), range(-j1, j1 + 1), range(-j2, j2 + 1)):
+            s = sum((2 * j3 + 1) * o.wigner3j(j1, j2, j3, m1, m2, m3) * o.wigner3j(j1, j2, j3, m1p, m2p, m3)
+                    for j3 in range(abs(j1 - j2), j1 + j2 + 1) for m3 in range(-j3, j3 + 1))
+            assert s == pytest.approx(float(m1 == m1p and m2 == m2p), abs=1e-13)
+
+
+# ---------------------------------------------------------------- solid harmonics
+def sh_closed_form(lmax, v):
+    """Real regular solid harmonics from associated Legendre functions
+    (Def. 2.1 case formula): R^(l)_m = sqrt(l!/(2l-1)!!) * C_lm with the
+    Racah-normalised C_lm = sqrt(4pi/(2l+1)) r^l Y_lm, sin for m<0, cos
+    for m>0, and no Condon-Shortley sign."""
+    x, y, z = v
+    r = math.sqrt(x * x + y * y + z * z)
+    ct = z / r
+    phi = math.atan2(y, x)
+    out = []
+    for l in range(lmax + 1):
+        dfact = 1
+        for k in range(2 * l - 1, 0, -2):
+            dfact *= k
+        s = math.sqrt(math.factorial(l) / dfact)
+        for m in range(-l, l + 1):
+            am = abs(m)
+            P = (-1) ** am * lpmv(am, l, ct)  # remove scipy's Condon-Shortley phase
+            if m == 0:
+                c = r ** l * P
+            else:
+                nrm = math.sqrt(2.0 * math.factorial(l - am) / math.factorial(l + am))
+                c = nrm * r ** l * P * (math.cos(am * phi) if m > 0 else math.sin(am * phi))
+            out.append(s * c)
+    return np.array(out)
+
+
+def test_solid_harmonics_closed_form():
+    rng = np.random.default_rng(11)
+    for _ in range(20):
+        v = rng.standard_normal(3) * rng.uniform(0.3, 3.0)
+        got = o.solid_harmonics(6, v)
+        ref = sh_closed_form(6, v)
+        assert np.max(np.abs(got - ref)) <= 1e-11 * max(1.0, np.max(np.abs(ref)))
+
+
+def test_solid_harmonics_paper_shapes():
+    # Def. 2.1: R^(1)(v) proportional to (y, z, x); R^(2) proportional to
+    # (xy, yz, 3z^2 - r^2, xz, x^2 - y^2), m = -2..2
+    v = np.array([0.37, -1.21, 0.83])
+    x, y, z = v
+    r2 = v @ v
+    R = o.solid_harmonics(2, v)
+    assert np.allclose(R[1:4], [y, z, x], atol=1e-15)
+    shapes = np.array([x * y, y * z, 3 * z * z - r2, x * z, x * x - y * y])
+    scale = np.array([math.sqrt(2), math.sqrt(2), 1 / math.sqrt(6), math.sqrt(2), 1 / math.sqrt(2)])
+    assert np.allclose(R[4:9], scale * shapes, atol=1e-14)
+    # value on the z axis: R^(l)_0(z) = sqrt(l!/(2l-1)!!)
+    Rz = o.solid_harmonics(6, np.array([0.0, 0.0, 1.0]))
+    for l in range(7):
+        dfact = 1
+        for k in range(2 * l - 1, 0, -2):
+            dfact *= k
+        assert Rz[l * l + l] == pytest.approx(math.sqrt(math.factorial(l) / dfact), abs=1e-14)
+    assert Rz[2 * 2 + 2] == pytest.approx(math.sqrt(2.0 / 3.0), abs=1e-15)
+
+
+def test_solid_harmonics_invariants():
+    rng = np.random.default_rng(5)
+    p, q = rng.standard_normal(3), rng.standard_normal(3)
+    # R^(1) is linear: R1(p - q) = R1(p) - R1(q) (Def. 2.1), and only l = 1 is
+    Rp, Rq, Rpq = o.solid_harmonics(3, p), o.solid_harmonics(3, q), o.solid_harmonics(3, p - q)
+    assert np.allclose(Rpq[1:4], Rp[1:4] - Rq[1:4], atol=1e-14)
+    assert not np.allclose(Rpq[4:9], Rp[4:9] - Rq[4:9], atol=1e-3)
+    v = rng.standard_normal(3)
+    R = o.solid_harmonics(6, v)
+    for l in range(7):
+        s = slice(l * l, (l + 1) ** 2)
+        # homogeneity and parity
+        assert np.allclose(o.solid_harmonics(6, 1.7 * v)[s], 1.7 ** l * R[s], rtol=1e-13, atol=1e-13)
+        assert np.allclose(o.solid_harmonics(6, -v)[s], (-1) ** l * R[s], atol=1e-13)
+        # squared norm = l!/(2l-1)!! |v|^(2l)
+        dfact = 1
+        for k in range(2 * l - 1, 0, -2):
+            dfact *= k
+        assert np.sum(R[s] ** 2) == pytest.approx(math.factorial(l) / dfact * (v @ v) ** l, rel=1e-13)
+    # harmonic: the Laplacian vanishes (central differences, fp64)
+    h = 1e-3
+    lap = -6 * R
+    for k in range(3):
+        e = np.zeros(3)
+        e[k] = h
+        lap = lap + o.solid_harmonics(6, v + e) + o.solid_harmonics(6, v - e)
+    assert np.max(np.abs(lap / (h * h))) < 1e-4
+
+
+def test_binomial_local_expansion():
+    # Thm. 3.2: R^(l)(p - q) = sum_u (-1)^(l-u) binom(l,u) [R^(u)(p) (x) R^(l-u)(q)]^(l)
+    rng = np.random.default_rng(2)
+    for l in range(7):
+        for _ in range(3):
+            p, q = rng.standard_normal(3) * 2, rng.standard_normal(3) * 2
+            Rp, Rq = o.solid_harmonics(6, p), o.solid_harmonics(6, q)
+            acc = np.zeros(2 * l + 1)
+            for u in range(l + 1):
+                c = o.cg_real(u, l - u, l)
+                acc += (-1) ** (l - u) * math.comb(l, u) * np.einsum(
+                    "abc,a,b->c", c, Rp[u * u:(u + 1) ** 2], Rq[(l - u) ** 2:(l - u + 1) ** 2])
+            ref = o.solid_harmonics(l, p - q)[l * l:]
+            assert np.max(np.abs(acc - ref)) <= 1e-12 * max(1.0, np.max(np.abs(ref)))
+
+
+# ---------------------------------------------------------------- real CG
+def closed_form_d(lmax, Q):
+    """Wigner D^(l)(Q) fitted from the Legendre closed-form harmonics
+    (independent of the oracle's CG tables)."""
+    rng = np.random.default_rng(3)
+    v = rng.standard_normal((40, 3))
+    A = np.array([sh_closed_form(lmax, x) for x in v])
+    B = np.array([sh_closed_form(lmax, Q @ x) for x in v])
+    Ds = []
+    for l in range(lmax + 1):
+        s = slice(l * l, (l + 1) ** 2)
+        Dt, *_ = np.linalg.lstsq(A[:, s], B[:, s], rcond=None)
+        Ds.append(Dt.T)
+    return Ds
+
+
+def test_real_cg_orthogonal_and_equivariant():
+    Q = o.random_rotation(17)
+    D = closed_form_d(4, Q)
+    # l = 1 is the rotation matrix itself in (y, z, x) order
+    P = np.array([[0, 1, 0], [0, 0, 1], [1, 0, 0]])
+    assert np.allclose(D[1], P @ Q @ P.T, atol=1e-12)
+    for l1, l2 in itertools.product(range(5), repeat=2):
+        blocks = []
+        for l3 in range(abs(l1 - l2), l1 + l2 + 1):
+            c = o.cg_real(l1, l2, l3)  # raises if the real/imaginary split fails
+            M = c.reshape(-1, 2 * l3 + 1)
+            assert np.allclose(M.T @ M, np.eye(2 * l3 + 1), atol=1e-13)
+            blocks.append(M)
+            if l3 <= 4:
+                # coupling commutes with rotation: C(D1 x, D2 y) = D3 C(x, y)
+                lhs = np.einsum("ia,jb,ijk->abk", D[l1], D[l2], c)
+                rhs = np.einsum("kq,abq->abk", D[l3], c)
+                assert np.max(np.abs(lhs - rhs)) < 1e-10, (l1, l2, l3)
+        full = np.concatenate(blocks, axis=1)  # completeness: square orthogonal
+        assert np.allclose(full @ full.T, np.eye(full.shape[0]), atol=1e-13)
+    for l1, l2, l3 in itertools.product(range(4), repeat=3):
+        if tri(l1, l2, l3):
+            # swap symmetry inherited from the complex basis
+            a, b = o.cg_real(l1, l2, l3), o.cg_real(l2, l1, l3)
+            assert np.allclose(a, (-1) ** (l1 + l2 - l3) * b.transpose(1, 0, 2), atol=1e-14)
+
+
+# ---------------------------------------------------------------- 6j and X
+def sixj_from_3j(j1, j2, j3, j4, j5, j6):
+    """6j as the contraction of four 3j symbols (standard form)."""
+    s = 0.0
+    for m1, m2, m4, m5 in itertools.product(range(-j1, j1 + 1), range(-j2, j2 + 1), range(-j4, j4 + 1), range(-j5, j5 + 1)):
+        m3 = -m1 - m2  # from the first symbol (-m1 -m2 -m3)
+        m6 = m5 - m1   # from (j1 j5 j6; m1 -m5 m6)
+        if abs(m3) > j3 or abs(m6) > j6:
+            continue
+        ph = (-1) ** (j1 + j2 + j3 + j4 + j5 + j6 - m1 - m2 - m3 - m4 - m5 - m6)
+        s += ph * (o.wigner3j(j1, j2, j3, -m1, -m2, -m3) * o.wigner3j(j1, j5, j6, m1, -m5, m6) *
+                   o.wigner3j(j4, j2, j6, m4, m2, -m6) * o.wigner3j(j4, j5, j3, -m4, m5, m3))
+    return s
+
+
+def test_6j_against_four_3j_sum():
+    for js in [(1, 1, 1, 1, 1, 1), (2, 1, 1, 1, 2, 2), (2, 2, 2, 2, 2, 2), (3, 2, 1, 2, 3, 2), (1, 2, 3, 3, 2, 1),
+               (2, 3, 3, 1, 2, 2), (4, 2, 2, 2, 4, 2), (3, 3, 2, 2, 1, 3)]:
+        assert o.wigner6j(*js) == pytest.approx(sixj_from_3j(*js), abs=1e-13), js
+
+
+def test_6j_special_value_symmetries_orthogonality():
+    for a, b, c in itertools.product(range(5), repeat=3):
+        if tri(a, b, c):
+            # {a b c; 0 c b} = (-1)^(a+b+c) / sqrt((2b+1)(2c+1))
+            assert o.wigner6j(a, b, c, 0, c, b) == pytest.approx((-1) ** (a + b + c) / math.sqrt((2 * b + 1) * (2 * c + 1)), abs=1e-14)
+    # App. C.2: the 24 tetrahedral symmetries
+    rng = np.random.default_rng(0)
+    for _ in range(30):
+        j = [int(x) for x in rng.integers(0, 5, size=6)]
+        v = o.wigner6j(*j)
+        cols = [(j[0], j[3]), (j[1], j[4]), (j[2], j[5])]
+        for perm in itertools.permutations(range(3)):
+            pc = [cols[k] for k in perm]
+            for flip in [(), (0, 1), (0, 2), (1, 2)]:
+                cc = [(c[1], c[0]) if k in flip else c for k, c in enumerate(pc)]
+                assert o.wigner6j(cc[0][0], cc[1][0], cc[2][0], cc[0][1], cc[1][1], cc[2][1]) == pytest.approx(v, abs=1e-14)
+    # App. C.2 orthogonality
+    for j1, j2, j4, j5 in itertools.product(range(4), repeat=4):
+        for j6 in range(0, 7):
+            for j6p in range(0, 7):
+                s = sum((2 * j3 + 1) * (2 * j6 + 1) * o.wigner6j(j1, j2, j3, j4, j5, j6) * o.wigner6j(j1, j2, j3, j4, j5, j6p)
+                        for j3 in range(0, 8))
+                want = float(j6 == j6p and tri(j1, j5, j6) and tri(j4, j2, j6))
+                assert s == pytest.approx(want, abs=1e-12)
+
+
+def test_recoupling_weights():
+    rng = np.random.default_rng(9)
+    L = 4
+    for a, b, u in itertools.product(range(L + 1), repeat=3):
+        f = b + u
+        if f > L:
+            continue
+        for oo in range(abs(a - f), min(a + f, L) + 1):
+            xs = {d: o.recoupling_x(a, b, u, oo, d) for d in range(abs(a - b), a + b + 1)}
+            for d, x in xs.items():
+                # closed form of Def. 2.3 with the standard phase (-1)^(a+b+d)
+                # (the printed (-1)^(a+b+c+d) is a misprint), times -1 in the
+                # real basis when a+b+d and u+d+o are both odd
+                cf = (-1) ** (a + b + d) * math.sqrt((2 * d + 1) * (2 * f + 1)) * o.wigner6j(a, b, d, u, oo, f)
+                if (a + b + d) % 2 and (u + d + oo) % 2:
+                    cf = -cf
+                assert x == pytest.approx(cf, abs=1e-12)
+                if u == 0:
+                    assert x == pytest.approx(float(d == oo), abs=1e-13)
+                if b == 0:
+                    assert x == pytest.approx(float(d == a) * (-1) ** (a + u - oo), abs=1e-13)
+            # the recoupling identity on random tensors
+            A, B, C = rng.standard_normal(2 * a + 1), rng.standard_normal(2 * b + 1), rng.standard_normal(2 * u + 1)
+            cb = np.einsum("gbk,g,b->k", o.cg_real(u, b, f), C, B)
+            lhs = np.einsum("ako,a,k->o", o.cg_real(a, f, oo), A, cb)
+            rhs = np.zeros(2 * oo + 1)
+            for d, x in xs.items():
+                if tri(u, d, oo):
+                    ab = np.einsum("abd,a,b->d", o.cg_real(a, b, d), A, B)
+                    rhs += x * np.einsum("gdo,g,d->o", o.cg_real(u, d, oo), C, ab)
+            assert np.allclose(lhs, rhs, atol=1e-12)
+
+
+# ---------------------------------------------------------------- radius graph
+def test_neighbor_list_exact_predicate_and_cells():
+    rng = np.random.default_rng(4)
+    pos = syn.quantize(rng.uniform(0, 12, size=(300, 3)))
+    gid = rng.integers(0, 3, size=300).astype(np.int32)
+    for g in [None, gid]:
+        rp1, c1 = o.neighbor_list(pos, 3.0, g, method="brute")
+        rp2, c2 = o.neighbor_list(pos, 3.0, g, method="cells")
+        assert np.array_equal(rp1, rp2) and np.array_equal(c1, c2)
+        pairs = set()
+        for i in range(300):
+            row = c1[rp1[i]:rp1[i + 1]]
+            assert np.all(np.diff(row) > 0) and i not in row
+            for j in row:
+                pairs.add((i, int(j)))
+                if g is not None:
+                    assert g[i] == g[j]
+        assert all((j, i) in pairs for (i, j) in pairs)
+        # brute force in float64 on the grid agrees
+        d2 = np.sum((pos[:, None, :].astype(np.float64) - pos[None, :, :]) ** 2, axis=2)
+        want = (d2 < 9.0) & ~np.eye(300, dtype=bool)
+        if g is not None:
+            want &= g[:, None] == g[None, :]
+        assert len(pairs) == int(want.sum())
+    # strict inequality exactly at the cutoff on the grid
+    two = np.array([[0, 0, 0], [0, 0, 3.0], [0, 3.0 - 2.0 ** -16, 0]], dtype=np.float32)
+    rp, c = o.neighbor_list(two, 3.0)
+    assert list(c[rp[0]:rp[1]]) == [2]
+
+
+# ---------------------------------------------------------------- the layer
+def small_graph(L, n, C, H, seed, box=4.0, cutoff=3.0):
+    rng = np.random.default_rng(seed)
+    pos = syn.quantize(rng.uniform(0, box, size=(n, 3)))
+    rp, ci = o.neighbor_list(pos, cutoff)
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    alpha = rng.uniform(0.1, 1.0, size=(len(ci), H)).astype(np.float32)
+    w = rng.uniform(0.5, 1.5, size=(L + 1) ** 3)
+    return pos, rp, ci, feat, alpha, w
+
+
+@pytest.mark.parametrize("L", [0, 1, 2, 3, 4])
+def test_factorised_equals_definition(L):
+    # Thm. 3.3 and Sec. 4.1: the node-factorised layer gives identical outputs
+    n = 8 if L < 4 else 5
+    pos, rp, ci, feat, alpha, w = small_graph(L, n, 4, 2, seed=10 + L)
+    y1 = o.conv_edge(L, 2, pos, feat, rp, ci, alpha, w)
+    for origin in ([0, 0, 0], [-3.1, 2.2, 7.5], pos[0].astype(np.float64)):
+        y2 = o.conv_factorised(L, 2, pos, feat, rp, ci, alpha, w, np.array(origin, dtype=np.float64))
+        # the binomial expansion cancels terms of size |p|^f down to |r_ij|^f,
+        # so fp64 rounding grows like (max|p| / cutoff)^L
+        maxp = np.max(np.linalg.norm(pos.astype(np.float64) - np.array(origin), axis=1))
+        tol = 1e-13 * max(1.0, maxp / 3.0) ** L
+        assert np.max(np.abs(y1 - y2)) <= tol * np.max(np.abs(y1))
+
+
+def test_layer_equivariance_and_translation():
+    # Lemma (equivariance, App. E): rotating positions and features rotates
+    # every output irrep by D^(o); a translation changes nothing.
+    L, H, C = 3, 2, 4
+    pos, rp, ci, feat, alpha, w = small_graph(L, 9, C, H, seed=21)
+    W = np.random.default_rng(1).standard_normal((L + 1, C, C)).astype(np.float32)
+    y = o.layer(L, H, pos, feat, rp, ci, alpha, w, W)
+    Q = o.random_rotation(5)
+    D = o.wigner_d(L, Q)
+    for l in range(L + 1):
+        assert np.allclose(D[l] @ D[l].T, np.eye(2 * l + 1), atol=1e-12)
+    center = np.array([1.0, 2.0, -0.5])
+    pos_r = ((pos.astype(np.float64) - center) @ Q.T + center).astype(np.float32)
+    feat_r = feat.astype(np.float64).copy()
+    for l in range(L + 1):
+        s = slice(l * l, (l + 1) ** 2)
+        feat_r[:, s, :] = np.einsum("mk,nkc->nmc", D[l], feat[:, s, :])
+    y_r = o.layer(L, H, pos_r, feat_r.astype(np.float32), rp, ci, alpha, w, W)
+    want = y.copy()
+    for l in range(L + 1):
+        s = slice(l * l, (l + 1) ** 2)
+        want[:, s, :] = np.einsum("mk,nkc->nmc", D[l], y[:, s, :])
+    # float32 rounding of the rotated inputs bounds the agreement
+    assert np.max(np.abs(y_r - want)) <= 2e-5 * np.max(np.abs(want))
+    shift = np.array([3.0, -1.25, 0.5], dtype=np.float32)  # a grid vector
+    y_t = o.layer(L, H, pos + shift, feat, rp, ci, alpha, w, W)
+    assert np.array_equal(y_t, y)
+
+
+def test_layer_special_cases():
+    rng = np.random.default_rng(8)
+    L, H, C = 2, 2, 4
+    pos, rp, ci, feat, alpha, _ = small_graph(L, 10, C, H, seed=31)
+    n = pos.shape[0]
+    recv = np.repeat(np.arange(n), np.diff(rp))
+    head = np.arange(C) // (C // H)
+    a_full = alpha[:, head]  # [E, C]
+    # only the f = 0 paths (a, 0, a): y^(a) = sum_j alpha_ij h_j^(a), a plain SpMM
+    w = np.zeros((L + 1,) * 3)
+    for a in range(L + 1):
+        w[a, 0, a] = 1.0
+    y = o.conv_edge(L, H, pos, feat, rp, ci, alpha, w.reshape(-1))
+    want = np.zeros((n, (L + 1) ** 2, C))
+    np.add.at(want, recv, a_full[:, None, :] * feat[ci].astype(np.float64))
+    assert np.allclose(y, want, atol=1e-12)
+    # only (0, 1, 1): y^(1) = sum_j alpha_ij h_j^(0) (r_i - r_j) in (y, z, x) order
+    w = np.zeros((L + 1,) * 3)
+    w[0, 1, 1] = 1.0
+    y = o.conv_edge(L, H, pos, feat, rp, ci, alpha, w.reshape(-1))
+    rij = pos[recv].astype(np.float64) - pos[ci]
+    vec = rij[:, [1, 2, 0]]
+    want = np.zeros((n, 3, C))
+    np.add.at(want, recv, vec[:, :, None] * (a_full * feat[ci, 0, :])[:, None, :])
+    assert np.allclose(y[:, 1:4, :], want, atol=1e-12)
+    assert np.all(y[:, 0, :] == 0) and np.all(y[:, 4:, :] == 0)
+    # isolated atom: zero row
+    lonely = np.concatenate([pos, np.array([[40.0, 40.0, 40.0]], dtype=np.float32)])
+    rp2, ci2 = o.neighbor_list(lonely, 3.0)
+    f2 = rng.standard_normal((n + 1, (L + 1) ** 2, C)).astype(np.float32)
+    a2 = rng.uniform(size=(len(ci2), H)).astype(np.float32)
+    y2 = o.conv_edge(L, H, lonely, f2, rp2, ci2, a2, rng.uniform(size=(L + 1) ** 3))
+    assert np.all(y2[n] == 0)
+
+
+def test_row_subset_and_mixing():
+    L, H, C = 2, 2, 4
+    pos, rp, ci, feat, alpha, w = small_graph(L, 10, C, H, seed=41)
+    y = o.conv_edge(L, H, pos, feat, rp, ci, alpha, w)
+    rows = np.array([7, 2, 9], dtype=np.int32)
+    assert np.array_equal(o.conv_edge(L, H, pos, feat, rp, ci, alpha, w, rows), y[rows])
+    W = np.random.default_rng(2).standard_normal((L + 1, C, C)).astype(np.float32)
+    out = o.mix(L, y, W)
+    for l in range(L + 1):
+        s = slice(l * l, (l + 1) ** 2)
+        assert np.allclose(out[:, s, :], np.einsum("pc,nmc->nmp", W[l].astype(np.float64), y[:, s, :]), atol=1e-13)
