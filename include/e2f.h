@@ -1,0 +1,145 @@
+/*
+ * e2f.h -- C ABI of libe2f: the Wigner-6j convolution of E2Former
+ * (arXiv 2501.19216) on AMD MI355X (gfx950).
+ *
+ * The layer (Def. 3.1 with attention weights, App. D.2 setup; Alg. 1 I/O):
+ *   y_i^(o)[m,c] = sum_{j in N(i)} alpha[e(i,j), c / (C/H)] sum_{a,f} w[a][f][o]
+ *                  [h_j^(a) (x) R^(f)(r_i - r_j)]^(o)_m [c]
+ *   out_i^(o)[m,c'] = sum_c W[o][c'][c] y_i^(o)[m,c]              (App. F self-mix)
+ * with real regular solid harmonics R^(f) (Def. 2.1), real-basis
+ * Clebsch-Gordan coupling [.](o) (Def. 2.2), a, f, o <= L.
+ *
+ * Conventions:
+ *   - irrep features are float32 [N][(L+1)^2][C], index l*l+l+m, m = -l..l,
+ *     real basis with m<0 <-> sin(|m| phi), m>0 <-> cos(m phi), no
+ *     Condon-Shortley sign; R^(1)(v) = (v_y, v_z, v_x) and
+ *     R^(l) = [R^(l-1) (x) R^(1)]^(l) (stretched power);
+ *   - channel c belongs to head c / (C/H);
+ *   - positions are float32 [N][3] in Angstrom; the radius graph compares
+ *     squared distances exactly on the 2^-16 A grid (positions are rounded
+ *     to it for that comparison only);
+ *   - the graph is CSR: row_ptr int64 [N+1], col_idx int32 [E]; row i holds
+ *     the senders j of receiver i in ascending order; attention weights are
+ *     float32 [E][H] in the same order.
+ *
+ * Memory: every pointer argument is HIP device memory owned by the caller
+ * unless it is marked "host".  The library never frees caller memory.  A
+ * context owns its coefficient tables and an internal workspace that grows
+ * on demand (hipMalloc) and is released by e2f_destroy.
+ *
+ * Streams: `stream` is a hipStream_t passed as void* (NULL = null stream).
+ * Work is enqueued on it; calls marked (sync) also wait for it.
+ *
+ * Errors: functions return e2f_status and never throw.  Arguments are
+ * checked on the host before any device work; on E2F_EINVAL no output is
+ * written.  e2f_last_error() gives the message of the last failing call on
+ * the calling thread.  A context is not safe for concurrent use from two
+ * threads, and calls on one context must not overlap on two streams.
+ */
+#ifndef E2F_H
+#define E2F_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  E2F_OK = 0,
+  E2F_EINVAL = 1,       /* bad argument (null pointer, bad size, non-finite) */
+  E2F_ECAPACITY = 2,    /* output buffer too small; the needed size is returned */
+  E2F_ENOMEM = 3,       /* device allocation failed */
+  E2F_EDEVICE = 4,      /* HIP error, or a context without a device */
+  E2F_EUNSUPPORTED = 5  /* L, C or problem size outside what is compiled in */
+} e2f_status;
+
+typedef enum { E2F_F32 = 0, E2F_BF16 = 1 } e2f_dtype;
+
+typedef struct e2f_ctx e2f_ctx;
+
+/* Create a context for degrees up to lmax_max (0..6) on HIP device `device`.
+ * device = -1 makes a host-only context (tables and argument checks only;
+ * every device call then returns E2F_EDEVICE).  (sync) */
+e2f_status e2f_create(int lmax_max, int device, e2f_ctx** out);
+void e2f_destroy(e2f_ctx* ctx);
+/* Message of the last failing call on this thread ("" if none). */
+const char* e2f_last_error(void);
+
+/* Number of rows of the j-side node tensor product T_j for degree L: the
+ * blocks [h^(a) (x) R^(b)]^(d), a,b <= L, |a-b| <= d <= a+b, that some
+ * i-side degree u <= L-b and output o <= L use (Thm. 3.3).  -1 if L is out
+ * of range.  58 / 183 / 454 / 1767 for L = 2 / 3 / 4 / 6. */
+int64_t e2f_node_tp_dim(int lmax);
+
+/* Host utilities (host memory, no context). */
+/* Real-basis CG tensor for (l1,l2,l3), l <= 12: out[(2l1+1)][(2l2+1)][(2l3+1)] (Def. 2.2). */
+e2f_status e2f_real_cg(int l1, int l2, int l3, double* out /* host */);
+/* Recoupling weight X_d of [A (x) [C (x) B]^(b+u)]^(o) = sum_d X_d [C (x) [A (x) B]^(d)]^(o)
+ * for A, B, C of degrees a, b, u (Def. 2.3). */
+double e2f_recoupling_weight(int a, int b, int u, int o, int d);
+
+/* Radius graph (Alg. 1 step 2): every ordered pair (i, j), i != j, with
+ * |r_i - r_j| < cutoff (strict, exact on the 2^-16 A grid) and, if graph_id
+ * is given, graph_id[i] == graph_id[j].  Rows are sorted ascending.
+ * graph_id: [N] or NULL.  row_ptr: [N+1] (always written).  col_idx:
+ * [capacity] or NULL.  *n_edges (host) receives E.  If col_idx is NULL or
+ * E > capacity, returns E2F_ECAPACITY after writing row_ptr and *n_edges
+ * (a size query).  Positions must satisfy |x| < 16384 A.  (sync) */
+e2f_status e2f_neighbor_list(e2f_ctx* ctx, const float* pos, const int32_t* graph_id, int32_t n, float cutoff,
+                             int64_t* row_ptr, int32_t* col_idx, int64_t capacity, int64_t* n_edges,
+                             void* stream);
+
+/* Real regular solid harmonics (Def. 2.1) of p_i = pos_i - origins[origin_id[i]]
+ * (origin 0 if origin_id is NULL; the zero vector if origins is NULL),
+ * evaluated in float64 and rounded: out [N][(lmax+1)^2] float32. */
+e2f_status e2f_solid_harmonics(e2f_ctx* ctx, const float* pos, const float* origins, const int32_t* origin_id,
+                               int32_t n, int lmax, float* out, void* stream);
+
+/* j-side node tensor product (Alg. 1 clebsch_gorden_tp; red box of Thm. 3.3):
+ * out[i][row][c] = [h_i^(a) (x) R^(b)(p_i)]^(d)_delta [c] for the rows of
+ * e2f_node_tp_dim(lmax) blocks, ordered by (a, b, d), then delta.
+ * p_i as in e2f_solid_harmonics.  feat [N][(L+1)^2][C], out [N][dimT][C].
+ * C must be a multiple of 4. */
+e2f_status e2f_node_tp(e2f_ctx* ctx, const float* pos, const float* origins, const int32_t* origin_id,
+                       const float* feat, int32_t n, int32_t channels, int lmax, float* out, void* stream);
+
+typedef struct {
+  int lmax;              /* L, 0..6 */
+  int32_t channels;      /* C, a multiple of 4, <= 1024 */
+  int32_t heads;         /* H, C % H == 0 and (C/H) % 4 == 0 */
+  float cutoff;          /* r_c of the graph, used for default weights and tiles */
+  const double* path_w;  /* host [(L+1)^3] w[a][f][o]; NULL => cutoff^-f on triangle-valid paths */
+  const void* mix_w;     /* device [(L+1)][C][C] W[o][c_out][c_in] of mix_dtype; NULL => no mixing */
+  e2f_dtype mix_dtype;   /* E2F_F32, or E2F_BF16 (mixing inputs rounded to bf16, fp32 accumulate) */
+  float tile_side;       /* side of the receiver tiles whose centres serve as local origins; 0 => 5*cutoff */
+} e2f_conv_params;
+
+/* Wigner-6j convolution forward (Thm. 3.3, Alg. 1): the layer above computed
+ * by node factorisation.  Per receiver tile t (a cube of side tile_side per
+ * graph) with centre o_t:  T_j = [h_j (x) R^(b)(r_j - o_t)]^(d) for the
+ * senders of t's receivers,  S_i = sum_j alpha_ij T_j,
+ * y_i = sum K(a,b,d,u,o) [R^(u)(r_i - o_t) (x) S_i^(a,b,d)]^(o), then mixing.
+ * graph_id: [N] or NULL (must match the graph's).  alpha: [E][H] or NULL
+ * (all ones).  out: [N][(L+1)^2][C].  Isolated atoms get zero rows.
+ * Deterministic: no floating-point atomics.  (sync: one small device->host
+ * read of the tile plan size) */
+e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
+                                     const int32_t* graph_id, const float* feat, int32_t n, const int64_t* row_ptr,
+                                     const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,
+                                     void* stream);
+
+/* The conventional per-edge SO(3) convolution (Def. 3.1): the same layer
+ * computed edge by edge with R^(f)(r_i - r_j) and the CG product per edge.
+ * Same arguments and output as e2f_wigner6j_conv_forward; graph_id unused. */
+e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
+                                    const int32_t* graph_id, const float* feat, int32_t n, const int64_t* row_ptr,
+                                    const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,
+                                    void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* E2F_H */

@@ -1,0 +1,239 @@
+"""Python binding of libe2f, the MI355X Wigner-6j convolution (E2Former,
+arXiv 2501.19216).
+
+Argument marshalling only: every step of the layer runs in the HIP kernels
+of ``libe2f.so`` through its C ABI (``include/e2f.h``); torch tensors are
+used for device memory and the current stream.  The functions carry the
+names of the C entry points.  If the library is not built, importing this
+package raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libe2f.so")
+
+E2F_OK, E2F_EINVAL, E2F_ECAPACITY, E2F_ENOMEM, E2F_EDEVICE, E2F_EUNSUPPORTED = range(6)
+E2F_F32, E2F_BF16 = 0, 1
+_STATUS = {0: "E2F_OK", 1: "E2F_EINVAL", 2: "E2F_ECAPACITY", 3: "E2F_ENOMEM", 4: "E2F_EDEVICE", 5: "E2F_EUNSUPPORTED"}
+
+# every function declared in include/e2f.h
+EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg",
+            "e2f_recoupling_weight", "e2f_neighbor_list", "e2f_solid_harmonics", "e2f_node_tp",
+            "e2f_wigner6j_conv_forward", "e2f_edge_tp_conv_forward"]
+
+
+class E2FError(RuntimeError):
+    def __init__(self, status: int, where: str, msg: str):
+        super().__init__("%s: %s (%s)" % (where, _STATUS.get(status, status), msg))
+        self.status = status
+
+
+class ConvParams(ctypes.Structure):
+    _fields_ = [("lmax", ctypes.c_int), ("channels", ctypes.c_int32), ("heads", ctypes.c_int32),
+                ("cutoff", ctypes.c_float), ("path_w", ctypes.c_void_p), ("mix_w", ctypes.c_void_p),
+                ("mix_dtype", ctypes.c_int), ("tile_side", ctypes.c_float)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libe2f.so is not built; run `python -m paper_2501_19216_amd.build_lib` "
+                          "(or __graft_entry__.build())")
+    L = ctypes.CDLL(LIB_PATH)
+    i, i32, i64, p, f = ctypes.c_int, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_float
+    L.e2f_create.argtypes = [i, i, ctypes.POINTER(p)]
+    L.e2f_create.restype = i
+    L.e2f_destroy.argtypes = [p]
+    L.e2f_destroy.restype = None
+    L.e2f_last_error.argtypes = []
+    L.e2f_last_error.restype = ctypes.c_char_p
+    L.e2f_node_tp_dim.argtypes = [i]
+    L.e2f_node_tp_dim.restype = i64
+    L.e2f_real_cg.argtypes = [i, i, i, p]
+    L.e2f_real_cg.restype = i
+    L.e2f_recoupling_weight.argtypes = [i, i, i, i, i]
+    L.e2f_recoupling_weight.restype = ctypes.c_double
+    L.e2f_neighbor_list.argtypes = [p, p, p, i32, f, p, p, i64, ctypes.POINTER(i64), p]
+    L.e2f_neighbor_list.restype = i
+    L.e2f_solid_harmonics.argtypes = [p, p, p, p, i32, i, p, p]
+    L.e2f_solid_harmonics.restype = i
+    L.e2f_node_tp.argtypes = [p, p, p, p, p, i32, i32, i, p, p]
+    L.e2f_node_tp.restype = i
+    for name in ("e2f_wigner6j_conv_forward", "e2f_edge_tp_conv_forward"):
+        fn = getattr(L, name)
+        fn.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, i32, p, p, i64, p, p, p]
+        fn.restype = i
+    return L
+
+
+lib = _load()
+
+
+def _check(st: int, where: str, allow=()):
+    if st != E2F_OK and st not in allow:
+        raise E2FError(st, where, lib.e2f_last_error().decode())
+    return st
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device=None):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _dev(t, dtype, name):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if t.dtype != dtype or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous %s tensor" % (name, dtype))
+    return t
+
+
+class Context:
+    """Owns an e2f_ctx (coefficient tables and workspace) on one device."""
+
+    def __init__(self, lmax_max: int = 6, device: int | None = 0):
+        h = ctypes.c_void_p()
+        dev = -1 if device is None else int(device)
+        _check(lib.e2f_create(lmax_max, dev, ctypes.byref(h)), "e2f_create")
+        self.handle = h
+        self.device = dev
+        self.lmax_max = lmax_max
+
+    def close(self):
+        if self.handle:
+            lib.e2f_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def e2f_create(lmax_max: int = 6, device: int | None = 0) -> Context:
+    return Context(lmax_max, device)
+
+
+def e2f_destroy(ctx: Context) -> None:
+    ctx.close()
+
+
+def e2f_node_tp_dim(lmax: int) -> int:
+    return int(lib.e2f_node_tp_dim(lmax))
+
+
+def e2f_real_cg(l1: int, l2: int, l3: int):
+    import numpy as np
+    out = np.zeros((2 * l1 + 1, 2 * l2 + 1, 2 * l3 + 1))
+    _check(lib.e2f_real_cg(l1, l2, l3, out.ctypes.data_as(ctypes.c_void_p)), "e2f_real_cg")
+    return out
+
+
+def e2f_recoupling_weight(a: int, b: int, u: int, o: int, d: int) -> float:
+    return float(lib.e2f_recoupling_weight(a, b, u, o, d))
+
+
+def e2f_neighbor_list(ctx: Context, pos: torch.Tensor, cutoff: float, graph_id: torch.Tensor | None = None):
+    """Radius graph as device CSR (row_ptr int64 [N+1], col_idx int32 [E])."""
+    _dev(pos, torch.float32, "pos")
+    _dev(graph_id, torch.int32, "graph_id")
+    n = pos.shape[0]
+    row_ptr = torch.empty(n + 1, dtype=torch.int64, device=pos.device)
+    E = ctypes.c_int64(0)
+    _check(lib.e2f_neighbor_list(ctx.handle, _ptr(pos), _ptr(graph_id), n, cutoff, _ptr(row_ptr), None, 0,
+                                 ctypes.byref(E), _stream(pos.device)), "e2f_neighbor_list", allow=(E2F_ECAPACITY,))
+    col = torch.empty(max(E.value, 1), dtype=torch.int32, device=pos.device)
+    _check(lib.e2f_neighbor_list(ctx.handle, _ptr(pos), _ptr(graph_id), n, cutoff, _ptr(row_ptr), _ptr(col),
+                                 col.numel(), ctypes.byref(E), _stream(pos.device)), "e2f_neighbor_list")
+    return row_ptr, col[:E.value]
+
+
+def e2f_solid_harmonics(ctx: Context, pos: torch.Tensor, lmax: int, origins: torch.Tensor | None = None,
+                        origin_id: torch.Tensor | None = None) -> torch.Tensor:
+    _dev(pos, torch.float32, "pos")
+    _dev(origins, torch.float32, "origins")
+    _dev(origin_id, torch.int32, "origin_id")
+    out = torch.empty(pos.shape[0], (lmax + 1) ** 2, dtype=torch.float32, device=pos.device)
+    _check(lib.e2f_solid_harmonics(ctx.handle, _ptr(pos), _ptr(origins), _ptr(origin_id), pos.shape[0], lmax,
+                                   _ptr(out), _stream(pos.device)), "e2f_solid_harmonics")
+    return out
+
+
+def e2f_node_tp(ctx: Context, pos: torch.Tensor, feat: torch.Tensor, lmax: int, origins: torch.Tensor | None = None,
+                origin_id: torch.Tensor | None = None) -> torch.Tensor:
+    _dev(pos, torch.float32, "pos")
+    _dev(feat, torch.float32, "feat")
+    _dev(origins, torch.float32, "origins")
+    _dev(origin_id, torch.int32, "origin_id")
+    n, nk, C = feat.shape
+    out = torch.empty(n, e2f_node_tp_dim(lmax), C, dtype=torch.float32, device=feat.device)
+    _check(lib.e2f_node_tp(ctx.handle, _ptr(pos), _ptr(origins), _ptr(origin_id), _ptr(feat), n, C, lmax, _ptr(out),
+                           _stream(feat.device)), "e2f_node_tp")
+    return out
+
+
+def _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side):
+    import numpy as np
+    keep = None
+    pw = None
+    if path_w is not None:
+        keep = np.ascontiguousarray(path_w, dtype=np.float64)
+        if keep.size != (lmax + 1) ** 3:
+            raise ValueError("path_w must have (lmax+1)^3 entries")
+        pw = keep.ctypes.data_as(ctypes.c_void_p)
+    mix_dtype = E2F_F32
+    if mix_w is not None:
+        if mix_w.dtype == torch.bfloat16:
+            mix_dtype = E2F_BF16
+        else:
+            _dev(mix_w, torch.float32, "mix_w")
+        if not mix_w.is_cuda or not mix_w.is_contiguous():
+            raise ValueError("mix_w must be a contiguous device tensor")
+    prm = ConvParams(lmax, channels, heads, cutoff, pw, None if mix_w is None else mix_w.data_ptr(), mix_dtype,
+                     float(tile_side))
+    return prm, keep
+
+
+def _conv(fn_name, ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w, mix_w, graph_id,
+          tile_side, out):
+    _dev(pos, torch.float32, "pos")
+    _dev(feat, torch.float32, "feat")
+    _dev(row_ptr, torch.int64, "row_ptr")
+    _dev(col_idx, torch.int32, "col_idx")
+    _dev(alpha, torch.float32, "alpha")
+    _dev(graph_id, torch.int32, "graph_id")
+    n, nk, C = feat.shape
+    if out is None:
+        out = torch.empty_like(feat)
+    _dev(out, torch.float32, "out")
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side)
+    st = getattr(lib, fn_name)(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(graph_id), _ptr(feat), n,
+                               _ptr(row_ptr), _ptr(col_idx), col_idx.numel(), _ptr(alpha), _ptr(out),
+                               _stream(feat.device))
+    del keep
+    _check(st, fn_name)
+    return out
+
+
+def e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None, mix_w=None,
+                              graph_id=None, tile_side=0.0, out=None):
+    """Wigner-6j convolution forward; returns out [N,(L+1)^2,C] float32."""
+    return _conv("e2f_wigner6j_conv_forward", ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w,
+                 mix_w, graph_id, tile_side, out)
+
+
+def e2f_edge_tp_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None, mix_w=None,
+                             graph_id=None, tile_side=0.0, out=None):
+    """Per-edge SO(3) convolution baseline; same output as the 6j forward."""
+    return _conv("e2f_edge_tp_conv_forward", ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w,
+                 mix_w, graph_id, tile_side, out)

@@ -1,0 +1,558 @@
+// C ABI of libe2f (declared in include/e2f.h): argument checks on the host,
+// the context with its coefficient tables and workspace, and the order of
+// kernel launches for each entry point.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <limits>
+#include <string>
+#include <vector>
+
+#include "../../include/e2f.h"
+#include "e2f_internal.h"
+#include "e2f_launch.h"
+
+using namespace e2f;
+
+namespace {
+
+thread_local std::string g_err;
+
+e2f_status fail(e2f_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+struct Buf {
+  void* p = nullptr;
+  size_t n = 0;
+};
+
+}  // namespace
+
+struct e2f_ctx {
+  int device = -1;
+  int lmax_max = 0;
+  std::vector<LayerTables> host;
+  std::vector<DevTables> dev;
+  std::vector<void*> table_mem;            // structure arrays per L
+  std::vector<void*> coef_mem;             // weighted coefficients per L
+  std::vector<std::vector<double>> coef_w; // path weights of the uploaded coefficients
+  int* stats = nullptr;                    // device, kStatsInts ints
+  int64_t* pinned = nullptr;               // host, 16 int64
+  std::vector<double> origins_host;
+  Buf a, b, c;
+};
+
+namespace {
+
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = false;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+#define E2F_HIP(call)                                                                        \
+  do {                                                                                       \
+    hipError_t e_ = (call);                                                                  \
+    if (e_ != hipSuccess) return fail(E2F_EDEVICE, "%s: %s", #call, hipGetErrorString(e_));  \
+  } while (0)
+
+size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+
+e2f_status ensure(e2f_ctx* ctx, Buf& b, size_t bytes, hipStream_t s) {
+  if (bytes <= b.n) return E2F_OK;
+  if (b.p) {
+    E2F_HIP(hipStreamSynchronize(s));
+    E2F_HIP(hipFree(b.p));
+    b.p = nullptr;
+    b.n = 0;
+  }
+  size_t want = al256(bytes + bytes / 8);
+  if (hipMalloc(&b.p, want) != hipSuccess) {
+    (void)hipGetLastError();
+    b.p = nullptr;
+    return fail(E2F_ENOMEM, "workspace allocation of %zu bytes failed", want);
+  }
+  b.n = want;
+  (void)ctx;
+  return E2F_OK;
+}
+
+// Carves aligned sub-buffers out of one workspace.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  template <typename T>
+  T* take(size_t count) {
+    T* p = (T*)(base + off);
+    off += al256(sizeof(T) * count);
+    return p;
+  }
+};
+
+template <typename T>
+void push_array(std::vector<char>& blob, std::vector<size_t>& offs, const std::vector<T>& v) {
+  size_t off = al256(blob.size());
+  blob.resize(off + sizeof(T) * std::max<size_t>(v.size(), 1), 0);
+  if (!v.empty()) std::memcpy(blob.data() + off, v.data(), sizeof(T) * v.size());
+  offs.push_back(off);
+}
+
+e2f_status upload_tables(e2f_ctx* ctx, int L) {
+  const LayerTables& t = ctx->host[L];
+  std::vector<char> blob;
+  std::vector<size_t> o;
+  push_array(blob, o, t.a_row_start);  // 0
+  push_array(blob, o, t.sh_ptr);       // 1
+  push_array(blob, o, t.sh_pow);       // 2
+  push_array(blob, o, t.sh_coef);      // 3
+  push_array(blob, o, t.m_rowoff);     // 4
+  push_array(blob, o, t.m_ptr);        // 5
+  push_array(blob, o, t.m_ridx);       // 6
+  push_array(blob, o, t.m_coef);       // 7
+  push_array(blob, o, t.q_ncol);       // 8
+  push_array(blob, o, t.q_coloff);     // 9
+  push_array(blob, o, t.q_cols);       // 10
+  push_array(blob, o, t.q_slotoff);    // 11
+  push_array(blob, o, t.q_ptr);        // 12
+  push_array(blob, o, t.q_ridx);       // 13
+  push_array(blob, o, t.k_ptr);        // 14
+  push_array(blob, o, t.k_ridx);       // 15
+  void* mem = nullptr;
+  E2F_HIP(hipMalloc(&mem, blob.size()));
+  ctx->table_mem[L] = mem;
+  E2F_HIP(hipMemcpy(mem, blob.data(), blob.size(), hipMemcpyHostToDevice));
+  char* b = (char*)mem;
+  DevTables d{};
+  d.L = L;
+  d.nk = t.nk;
+  d.dimT = t.dimT;
+  d.a_row_start = (const int*)(b + o[0]);
+  d.sh_ptr = (const int*)(b + o[1]);
+  d.sh_pow = (const int*)(b + o[2]);
+  d.sh_coef = (const double*)(b + o[3]);
+  d.m_rowoff = (const int*)(b + o[4]);
+  d.m_ptr = (const int*)(b + o[5]);
+  d.m_ridx = (const int*)(b + o[6]);
+  d.m_coef = (const double*)(b + o[7]);
+  d.q_ncol = (const int*)(b + o[8]);
+  d.q_coloff = (const int*)(b + o[9]);
+  d.q_cols = (const int*)(b + o[10]);
+  d.q_slotoff = (const int*)(b + o[11]);
+  d.q_ptr = (const int*)(b + o[12]);
+  d.q_ridx = (const int*)(b + o[13]);
+  d.k_ptr = (const int*)(b + o[14]);
+  d.k_ridx = (const int*)(b + o[15]);
+  d.q_coef = nullptr;
+  d.k_coef = nullptr;
+  d.max_qslots = t.max_qslots;
+  d.m_slots = t.m_slots();
+  ctx->dev[L] = d;
+  return E2F_OK;
+}
+
+std::vector<double> path_weights(const e2f_conv_params* p) {
+  const int L1 = p->lmax + 1;
+  std::vector<double> w((size_t)L1 * L1 * L1, 0.0);
+  if (p->path_w) {
+    std::memcpy(w.data(), p->path_w, sizeof(double) * w.size());
+  } else {
+    for (int a = 0; a < L1; ++a)
+      for (int f = 0; f < L1; ++f)
+        for (int o = std::abs(a - f); o <= std::min(a + f, p->lmax); ++o)
+          w[((size_t)a * L1 + f) * L1 + o] = std::pow((double)p->cutoff, -(double)f);
+  }
+  return w;
+}
+
+// Refresh the path-weighted coefficient arrays of degree L when the weights change.
+e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStream_t s) {
+  if (ctx->coef_mem[L] && ctx->coef_w[L] == w) return E2F_OK;
+  const LayerTables& t = ctx->host[L];
+  std::vector<double> q(t.q_unit.size());
+  for (size_t e = 0; e < q.size(); ++e) q[e] = t.q_unit[e] * w[t.q_path[e]];
+  std::vector<float> k(t.k_unit.size());
+  for (size_t e = 0; e < k.size(); ++e) k[e] = (float)(t.k_unit[e] * w[t.k_path[e]]);
+  std::vector<char> blob;
+  std::vector<size_t> o;
+  push_array(blob, o, q);
+  push_array(blob, o, k);
+  E2F_HIP(hipStreamSynchronize(s));  // earlier work may still read the old coefficients
+  if (ctx->coef_mem[L]) E2F_HIP(hipFree(ctx->coef_mem[L]));
+  ctx->coef_mem[L] = nullptr;
+  void* mem = nullptr;
+  E2F_HIP(hipMalloc(&mem, blob.size()));
+  E2F_HIP(hipMemcpy(mem, blob.data(), blob.size(), hipMemcpyHostToDevice));
+  ctx->coef_mem[L] = mem;
+  ctx->coef_w[L] = w;
+  ctx->dev[L].q_coef = (const double*)((char*)mem + o[0]);
+  ctx->dev[L].k_coef = (const float*)((char*)mem + o[1]);
+  return E2F_OK;
+}
+
+bool finite_pos(float x) { return std::isfinite(x) && x > 0.0f; }
+
+e2f_status check_conv(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos, const float* feat, int32_t n,
+                      const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges, float* out) {
+  if (!ctx) return fail(E2F_EINVAL, "ctx is NULL");
+  if (!p) return fail(E2F_EINVAL, "params is NULL");
+  if (p->lmax < 0 || p->lmax > kMaxL) return fail(E2F_EUNSUPPORTED, "lmax %d outside 0..%d", p->lmax, kMaxL);
+  if (p->lmax > ctx->lmax_max) return fail(E2F_EINVAL, "lmax %d above the context's %d", p->lmax, ctx->lmax_max);
+  if (p->channels < 1 || p->heads < 1) return fail(E2F_EINVAL, "channels and heads must be positive");
+  if (p->channels % p->heads) return fail(E2F_EINVAL, "channels %d not divisible by heads %d", p->channels, p->heads);
+  if (p->channels % 4 || (p->channels / p->heads) % 4 || p->channels > 1024)
+    return fail(E2F_EUNSUPPORTED, "channels %d / head width %d must be multiples of 4 (channels <= 1024)",
+                p->channels, p->channels / p->heads);
+  if (!finite_pos(p->cutoff) || p->cutoff > 64.0f) return fail(E2F_EINVAL, "cutoff must be finite, in (0, 64]");
+  if (!std::isfinite(p->tile_side) || p->tile_side < 0.0f) return fail(E2F_EINVAL, "tile_side must be finite and >= 0");
+  if (p->mix_dtype != E2F_F32 && p->mix_dtype != E2F_BF16) return fail(E2F_EINVAL, "unknown mix_dtype");
+  if (p->path_w) {
+    const int L1 = p->lmax + 1;
+    for (int q = 0; q < L1 * L1 * L1; ++q)
+      if (!std::isfinite(p->path_w[q])) return fail(E2F_EINVAL, "path_w[%d] is not finite", q);
+  }
+  if (n < 0) return fail(E2F_EINVAL, "n < 0");
+  if (n_edges < 0) return fail(E2F_EINVAL, "n_edges < 0");
+  if (n_edges > std::numeric_limits<int32_t>::max()) return fail(E2F_EUNSUPPORTED, "more than 2^31-1 edges");
+  if (n > 0 && (!pos || !feat || !out || !row_ptr)) return fail(E2F_EINVAL, "pos, feat, out and row_ptr are required");
+  if (n_edges > 0 && !col_idx) return fail(E2F_EINVAL, "col_idx is NULL with n_edges > 0");
+  const double elems = (double)n * nk_of(p->lmax) * p->channels;
+  if (elems > 4.0e18) return fail(E2F_EINVAL, "feature index space overflows int64");
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  return E2F_OK;
+}
+
+// Tile plan: bounding box on the device, then the tile grid on the host.
+struct TilePlan {
+  int lo[3];
+  int dim[3];
+  int64_t span[3];
+  int ncell = 1;
+  int64_t n_graphs = 1;
+};
+
+e2f_status run_bbox(e2f_ctx* ctx, const float* pos, const int32_t* graph_id, int n, hipStream_t s, int st[kStatsInts]) {
+  E2F_HIP(launch_bbox(pos, graph_id, n, ctx->stats, s));
+  E2F_HIP(hipMemcpyAsync(ctx->pinned, ctx->stats, sizeof(int) * kStatsInts, hipMemcpyDeviceToHost, s));
+  E2F_HIP(hipStreamSynchronize(s));
+  std::memcpy(st, ctx->pinned, sizeof(int) * kStatsInts);
+  if (st[7] & 1) return fail(E2F_EINVAL, "a position is not finite or has |x| >= 16384 A");
+  if (st[7] & 2) return fail(E2F_EINVAL, "a graph id is negative");
+  return E2F_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+e2f_status e2f_create(int lmax_max, int device, e2f_ctx** out) {
+  if (!out) return fail(E2F_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (lmax_max < 0 || lmax_max > kMaxL) return fail(E2F_EINVAL, "lmax_max %d outside 0..%d", lmax_max, kMaxL);
+  if (device < -1) return fail(E2F_EINVAL, "device %d", device);
+  e2f_ctx* ctx = new e2f_ctx();
+  ctx->device = device;
+  ctx->lmax_max = lmax_max;
+  for (int L = 0; L <= lmax_max; ++L) ctx->host.push_back(build_layer_tables(L));
+  ctx->dev.assign(lmax_max + 1, DevTables{});
+  ctx->table_mem.assign(lmax_max + 1, nullptr);
+  ctx->coef_mem.assign(lmax_max + 1, nullptr);
+  ctx->coef_w.assign(lmax_max + 1, {});
+  if (device >= 0) {
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess || device >= count) {
+      (void)hipGetLastError();
+      delete ctx;
+      return fail(E2F_EDEVICE, "HIP device %d not available", device);
+    }
+    DeviceGuard g(device);
+    if (!g.ok) {
+      delete ctx;
+      return fail(E2F_EDEVICE, "hipSetDevice(%d) failed", device);
+    }
+    e2f_status st = E2F_OK;
+    for (int L = 0; L <= lmax_max && st == E2F_OK; ++L) st = upload_tables(ctx, L);
+    if (st == E2F_OK && hipMalloc((void**)&ctx->stats, sizeof(int) * 64) != hipSuccess)
+      st = fail(E2F_ENOMEM, "stats allocation failed");
+    if (st == E2F_OK && hipHostMalloc((void**)&ctx->pinned, sizeof(int64_t) * 16, hipHostMallocDefault) != hipSuccess)
+      st = fail(E2F_ENOMEM, "pinned allocation failed");
+    if (st != E2F_OK) {
+      e2f_destroy(ctx);
+      return st;
+    }
+  }
+  *out = ctx;
+  return E2F_OK;
+}
+
+void e2f_destroy(e2f_ctx* ctx) {
+  if (!ctx) return;
+  if (ctx->device >= 0) {
+    DeviceGuard g(ctx->device);
+    (void)hipDeviceSynchronize();
+    for (void* p : ctx->table_mem)
+      if (p) (void)hipFree(p);
+    for (void* p : ctx->coef_mem)
+      if (p) (void)hipFree(p);
+    for (Buf* b : {&ctx->a, &ctx->b, &ctx->c})
+      if (b->p) (void)hipFree(b->p);
+    if (ctx->stats) (void)hipFree(ctx->stats);
+    if (ctx->pinned) (void)hipHostFree(ctx->pinned);
+  }
+  delete ctx;
+}
+
+const char* e2f_last_error(void) { return g_err.c_str(); }
+
+int64_t e2f_node_tp_dim(int lmax) { return node_tp_dim(lmax); }
+
+e2f_status e2f_real_cg(int l1, int l2, int l3, double* out) {
+  if (!out) return fail(E2F_EINVAL, "out is NULL");
+  if (l1 < 0 || l2 < 0 || l3 < 0 || l1 > 12 || l2 > 12 || l3 > 12) return fail(E2F_EINVAL, "degrees must be in 0..12");
+  if (l3 < std::abs(l1 - l2) || l3 > l1 + l2) return fail(E2F_EINVAL, "(%d,%d,%d) violates the triangle rule", l1, l2, l3);
+  std::vector<double> c = real_cg(l1, l2, l3);
+  std::memcpy(out, c.data(), sizeof(double) * c.size());
+  return E2F_OK;
+}
+
+double e2f_recoupling_weight(int a, int b, int u, int o, int d) {
+  if (a < 0 || b < 0 || u < 0 || o < 0 || d < 0 || a > 12 || b > 12 || u > 12 || o > 12 || d > 24) return 0.0;
+  return recoupling_weight(a, b, u, o, d);
+}
+
+e2f_status e2f_neighbor_list(e2f_ctx* ctx, const float* pos, const int32_t* graph_id, int32_t n, float cutoff,
+                             int64_t* row_ptr, int32_t* col_idx, int64_t capacity, int64_t* n_edges, void* stream) {
+  if (!ctx) return fail(E2F_EINVAL, "ctx is NULL");
+  if (!row_ptr || !n_edges) return fail(E2F_EINVAL, "row_ptr and n_edges are required");
+  if (n < 0) return fail(E2F_EINVAL, "n < 0");
+  if (n > 0 && !pos) return fail(E2F_EINVAL, "pos is NULL");
+  if (!finite_pos(cutoff) || cutoff > 64.0f) return fail(E2F_EINVAL, "cutoff must be finite, in (0, 64]");
+  if (capacity < 0) return fail(E2F_EINVAL, "capacity < 0");
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  if (n == 0) {
+    E2F_HIP(hipMemsetAsync(row_ptr, 0, sizeof(int64_t), s));
+    E2F_HIP(hipStreamSynchronize(s));
+    *n_edges = 0;
+    return col_idx ? E2F_OK : fail(E2F_ECAPACITY, "size query: 0 edges");
+  }
+  int st[kStatsInts];
+  e2f_status rs = run_bbox(ctx, pos, graph_id, n, s, st);
+  if (rs != E2F_OK) return rs;
+  CellGrid cg;
+  const double rc = (double)cutoff * kGrid;
+  cg.side = (int64_t)std::ceil(rc);
+  const int64_t limit = std::max<int64_t>(8 * (int64_t)n, 4096);
+  for (;;) {
+    cg.ncell = 1;
+    for (int k = 0; k < 3; ++k) {
+      cg.lo[k] = st[k];
+      cg.dim[k] = (int)(((int64_t)st[3 + k] - st[k]) / cg.side + 1);
+      cg.ncell *= cg.dim[k];
+    }
+    if (cg.ncell <= limit) break;
+    cg.side *= 2;
+  }
+  rs = ensure(ctx, ctx->a, nl_scratch_bytes(n, cg), s);
+  if (rs != E2F_OK) return rs;
+  E2F_HIP(launch_nl_count(pos, graph_id, n, rc * rc, cg, ctx->a.p, row_ptr, s));
+  E2F_HIP(hipMemcpyAsync(ctx->pinned, row_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  E2F_HIP(hipStreamSynchronize(s));
+  const int64_t E = ctx->pinned[0];
+  *n_edges = E;
+  if (!col_idx || E > capacity) return fail(E2F_ECAPACITY, "the graph has %lld edges", (long long)E);
+  if (E > std::numeric_limits<int32_t>::max()) return fail(E2F_EUNSUPPORTED, "more than 2^31-1 edges");
+  if (E == 0) return E2F_OK;
+  const size_t sort_b = nl_sort_tmp_bytes(n, E);
+  rs = ensure(ctx, ctx->b, al256(sizeof(int32_t) * (size_t)E) + al256(sort_b), s);
+  if (rs != E2F_OK) return rs;
+  Carver cv{(char*)ctx->b.p};
+  int32_t* unsorted = cv.take<int32_t>((size_t)E);
+  void* sort_tmp = cv.take<char>(sort_b);
+  E2F_HIP(launch_nl_fill(pos, graph_id, n, rc * rc, cg, ctx->a.p, row_ptr, unsorted, col_idx, E, sort_tmp, sort_b, s));
+  return E2F_OK;
+}
+
+e2f_status e2f_solid_harmonics(e2f_ctx* ctx, const float* pos, const float* origins, const int32_t* origin_id,
+                               int32_t n, int lmax, float* out, void* stream) {
+  if (!ctx) return fail(E2F_EINVAL, "ctx is NULL");
+  if (lmax < 0 || lmax > ctx->lmax_max) return fail(E2F_EINVAL, "lmax %d outside 0..%d", lmax, ctx->lmax_max);
+  if (n < 0) return fail(E2F_EINVAL, "n < 0");
+  if (n > 0 && (!pos || !out)) return fail(E2F_EINVAL, "pos and out are required");
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  if (n == 0) return E2F_OK;
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  E2F_HIP(launch_sh(ctx->dev[lmax], pos, nullptr, nullptr, origins, origin_id, std::numeric_limits<int>::max(), n,
+                    nullptr, out, s));
+  return E2F_OK;
+}
+
+e2f_status e2f_node_tp(e2f_ctx* ctx, const float* pos, const float* origins, const int32_t* origin_id,
+                       const float* feat, int32_t n, int32_t channels, int lmax, float* out, void* stream) {
+  if (!ctx) return fail(E2F_EINVAL, "ctx is NULL");
+  if (lmax < 0 || lmax > ctx->lmax_max) return fail(E2F_EINVAL, "lmax %d outside 0..%d", lmax, ctx->lmax_max);
+  if (n < 0) return fail(E2F_EINVAL, "n < 0");
+  if (channels < 4 || channels % 4 || channels > 1024)
+    return fail(E2F_EUNSUPPORTED, "channels %d must be a multiple of 4 in 4..1024", channels);
+  if (n > 0 && (!pos || !feat || !out)) return fail(E2F_EINVAL, "pos, feat and out are required");
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  if (n == 0) return E2F_OK;
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  const DevTables& t = ctx->dev[lmax];
+  e2f_status rs = ensure(ctx, ctx->c, sizeof(double) * (size_t)n * t.nk, s);
+  if (rs != E2F_OK) return rs;
+  double* R = (double*)ctx->c.p;
+  E2F_HIP(launch_sh(t, pos, nullptr, nullptr, origins, origin_id, std::numeric_limits<int>::max(), n, R, nullptr, s));
+  E2F_HIP(launch_node_tp(t, R, nullptr, feat, n, channels, out, s));
+  return E2F_OK;
+}
+
+e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos,
+                                     const int32_t* graph_id, const float* feat, int32_t n, const int64_t* row_ptr,
+                                     const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,
+                                     void* stream) {
+  e2f_status rs = check_conv(ctx, p, pos, feat, n, row_ptr, col_idx, n_edges, out);
+  if (rs != E2F_OK) return rs;
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  const int L = p->lmax, C = p->channels, nk = nk_of(L);
+  rs = set_weights(ctx, L, path_weights(p), s);
+  if (rs != E2F_OK) return rs;
+  if (n == 0) return E2F_OK;
+  if (n_edges == 0) {
+    E2F_HIP(hipMemsetAsync(out, 0, sizeof(float) * (size_t)n * nk * C, s));
+    return E2F_OK;
+  }
+  const DevTables& t = ctx->dev[L];
+  int st[kStatsInts];
+  rs = run_bbox(ctx, pos, graph_id, n, s, st);
+  if (rs != E2F_OK) return rs;
+  // ---- tile grid (local origins; precision of the binomial expansion)
+  TilePlan tp;
+  const double side = (p->tile_side > 0.0f ? (double)p->tile_side : 5.0 * (double)p->cutoff) * kGrid;
+  tp.ncell = 1;
+  for (int k = 0; k < 3; ++k) {
+    tp.lo[k] = st[k];
+    tp.span[k] = (int64_t)st[3 + k] - st[k] + 1;
+    int64_t d = (int64_t)std::ceil((double)tp.span[k] / side);
+    d = std::max<int64_t>(1, std::min<int64_t>(d, 64));
+    tp.dim[k] = (int)d;
+    tp.ncell *= tp.dim[k];
+  }
+  tp.n_graphs = graph_id ? (int64_t)st[6] + 1 : 1;
+  const int64_t keys = tp.n_graphs * tp.ncell;
+  const int64_t count = keys * (int64_t)n;
+  if (count > std::numeric_limits<int32_t>::max() - 1)
+    return fail(E2F_EUNSUPPORTED, "tile plan of %lld graph-tiles x %d atoms exceeds 2^31", (long long)keys, n);
+  ctx->origins_host.assign((size_t)3 * tp.ncell, 0.0);
+  for (int cz = 0; cz < tp.dim[2]; ++cz)
+    for (int cy = 0; cy < tp.dim[1]; ++cy)
+      for (int cx = 0; cx < tp.dim[0]; ++cx) {
+        const int c[3] = {cx, cy, cz};
+        const int cell = (cz * tp.dim[1] + cy) * tp.dim[0] + cx;
+        for (int k = 0; k < 3; ++k) {
+          const int64_t og = tp.lo[k] + ((2 * (int64_t)c[k] + 1) * tp.span[k]) / (2 * (int64_t)tp.dim[k]);
+          ctx->origins_host[3 * cell + k] = (double)og / kGrid;
+        }
+      }
+  const size_t scan_b = scan_tmp_bytes(count);
+  size_t need_a = al256(sizeof(int32_t) * (size_t)n) + 2 * al256(sizeof(int32_t) * (size_t)count) + al256(scan_b) +
+                  al256(sizeof(double) * ctx->origins_host.size());
+  rs = ensure(ctx, ctx->a, need_a, s);
+  if (rs != E2F_OK) return rs;
+  Carver ca{(char*)ctx->a.p};
+  int32_t* tile_of = ca.take<int32_t>(n);
+  int32_t* flags = ca.take<int32_t>((size_t)count);
+  int32_t* pidx = ca.take<int32_t>((size_t)count);
+  void* scan_tmp = ca.take<char>(scan_b);
+  double* origins = ca.take<double>(ctx->origins_host.size());
+  E2F_HIP(hipMemcpyAsync(origins, ctx->origins_host.data(), sizeof(double) * ctx->origins_host.size(),
+                         hipMemcpyHostToDevice, s));
+  E2F_HIP(launch_tile_keys(pos, graph_id, n, tp.lo, tp.dim, tp.span, tp.ncell, tile_of, s));
+  E2F_HIP(hipMemsetAsync(flags, 0, sizeof(int32_t) * (size_t)count, s));
+  E2F_HIP(launch_pair_flags(row_ptr, col_idx, tile_of, n, flags, s));
+  E2F_HIP(launch_scan_i32(flags, pidx, count, scan_tmp, scan_b, s));
+  E2F_HIP(hipMemcpyAsync(ctx->pinned, pidx + count - 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  E2F_HIP(hipMemcpyAsync((char*)ctx->pinned + 8, flags + count - 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  E2F_HIP(hipStreamSynchronize(s));
+  int32_t last_idx, last_flag;
+  std::memcpy(&last_idx, ctx->pinned, 4);
+  std::memcpy(&last_flag, (char*)ctx->pinned + 8, 4);
+  const int64_t P = (int64_t)last_idx + last_flag;
+  // ---- phase 2 buffers
+  const bool mixing = p->mix_w != nullptr;
+  const size_t tbytes = sizeof(float) * (size_t)P * t.dimT * C;
+  const size_t sbytes = sizeof(float) * (size_t)n * t.dimT * C;
+  const size_t need_b = 2 * al256(sizeof(int32_t) * (size_t)P) + al256(sizeof(int32_t) * (size_t)n_edges) +
+                        al256(sizeof(double) * (size_t)P * nk) + al256(sizeof(double) * (size_t)n * nk) +
+                        al256(tbytes) + al256(sbytes) + (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
+  rs = ensure(ctx, ctx->b, need_b, s);
+  if (rs != E2F_OK) return rs;
+  Carver cb{(char*)ctx->b.p};
+  int32_t* pair_node = cb.take<int32_t>((size_t)P);
+  int32_t* pair_tile = cb.take<int32_t>((size_t)P);
+  int32_t* col_pair = cb.take<int32_t>((size_t)n_edges);
+  double* Rp = cb.take<double>((size_t)P * nk);
+  double* Rr = cb.take<double>((size_t)n * nk);
+  float* T = cb.take<float>((size_t)P * t.dimT * C);
+  float* S = cb.take<float>((size_t)n * t.dimT * C);
+  float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
+  E2F_HIP(launch_pairs(flags, pidx, count, n, pair_node, pair_tile, s));
+  E2F_HIP(launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
+  E2F_HIP(launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, nullptr, s));
+  E2F_HIP(launch_sh(t, pos, nullptr, origins, nullptr, tile_of, tp.ncell, n, Rr, nullptr, s));
+  E2F_HIP(launch_node_tp(t, Rp, pair_node, feat, (int)P, C, T, s));
+  E2F_HIP(launch_aggregate(T, row_ptr, col_pair, alpha, n, t.dimT, C, p->heads, S, s));
+  E2F_HIP(launch_recouple(t, Rr, S, n, C, y, s));
+  if (mixing) E2F_HIP(launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
+  return E2F_OK;
+}
+
+e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos,
+                                    const int32_t* graph_id, const float* feat, int32_t n, const int64_t* row_ptr,
+                                    const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,
+                                    void* stream) {
+  (void)graph_id;
+  e2f_status rs = check_conv(ctx, p, pos, feat, n, row_ptr, col_idx, n_edges, out);
+  if (rs != E2F_OK) return rs;
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  const int L = p->lmax, C = p->channels, nk = nk_of(L);
+  rs = set_weights(ctx, L, path_weights(p), s);
+  if (rs != E2F_OK) return rs;
+  if (n == 0) return E2F_OK;
+  if (n_edges == 0) {
+    E2F_HIP(hipMemsetAsync(out, 0, sizeof(float) * (size_t)n * nk * C, s));
+    return E2F_OK;
+  }
+  const bool mixing = p->mix_w != nullptr;
+  float* y = out;
+  if (mixing) {
+    rs = ensure(ctx, ctx->c, sizeof(float) * (size_t)n * nk * C, s);
+    if (rs != E2F_OK) return rs;
+    y = (float*)ctx->c.p;
+  }
+  E2F_HIP(launch_edge_tp(ctx->dev[L], pos, feat, row_ptr, col_idx, alpha, n, C, p->heads, y, s));
+  if (mixing) E2F_HIP(launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
+  return E2F_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,529 @@
+// HIP kernels of the Wigner-6j convolution (Thm. 3.3, Alg. 1) and of the
+// per-edge baseline (Def. 3.1) for gfx950.
+//
+// Data layout (HBM):
+//   feat  [N][nk][C]        float32, nk = (L+1)^2
+//   R     [items][nk]       float64 solid harmonics of p = r - origin
+//   T     [pairs][dimT][C]  float32 j-side products, one row per (tile, sender)
+//   S     [N][dimT][C]      float32 aggregated products per receiver
+//   y/out [N][nk][C]        float32
+// Channels are innermost everywhere, so every row gather in the aggregation
+// and every per-node product reads contiguous, coalesced channel vectors.
+// No floating-point atomics anywhere: each output element has one writer.
+#include <hip/hip_runtime.h>
+#include <hip/hip_bf16.h>
+#include <hipcub/hipcub.hpp>
+
+#include <utility>
+
+#include "e2f_launch.h"
+
+namespace e2f {
+namespace {
+
+// ------------------------------------------------------------ solid harmonics
+// Component k of R(p) as the explicit polynomial sum_t coef_t x^ex y^ey z^ez.
+template <typename F>
+__device__ __forceinline__ F sh_poly(const DevTables& t, int k, F x, F y, F z) {
+  F acc = 0;
+  for (int e = t.sh_ptr[k]; e < t.sh_ptr[k + 1]; ++e) {
+    const int pw = t.sh_pow[e];
+    F m = (F)t.sh_coef[e];
+    for (int q = 0; q < (pw & 15); ++q) m *= x;
+    for (int q = 0; q < ((pw >> 4) & 15); ++q) m *= y;
+    for (int q = 0; q < ((pw >> 8) & 15); ++q) m *= z;
+    acc += m;
+  }
+  return acc;
+}
+
+__global__ void k_sh(DevTables t, const float* __restrict__ pos, const int32_t* __restrict__ node_of,
+                     const double* __restrict__ origins_d, const float* __restrict__ origins_f,
+                     const int32_t* __restrict__ origin_id, int origin_mod, int n, double* __restrict__ out_d,
+                     float* __restrict__ out_f) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= (int64_t)n * t.nk) return;
+  const int item = (int)(gid / t.nk), k = (int)(gid % t.nk);
+  const int node = node_of ? node_of[item] : item;
+  double ox = 0.0, oy = 0.0, oz = 0.0;
+  const int oi = origin_id ? origin_id[item] % origin_mod : 0;
+  if (origins_d) {
+    ox = origins_d[3 * oi];
+    oy = origins_d[3 * oi + 1];
+    oz = origins_d[3 * oi + 2];
+  } else if (origins_f) {
+    ox = origins_f[3 * oi];
+    oy = origins_f[3 * oi + 1];
+    oz = origins_f[3 * oi + 2];
+  }
+  const double v = sh_poly<double>(t, k, (double)pos[3 * node] - ox, (double)pos[3 * node + 1] - oy,
+                                   (double)pos[3 * node + 2] - oz);
+  if (out_d) out_d[gid] = v;
+  else out_f[gid] = (float)v;
+}
+
+// ------------------------------------------------------------ tile plan
+struct TileGrid {
+  int lo[3];
+  int dim[3];
+  int64_t span[3];
+  int ncell;
+};
+
+__global__ void k_tile_keys(const float* __restrict__ pos, const int32_t* __restrict__ gid, int n, TileGrid g,
+                            int32_t* __restrict__ tile_of) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  int c[3];
+  for (int k = 0; k < 3; ++k) {
+    const int64_t X = __float2int_rn(pos[3 * i + k] * 65536.0f);
+    const int64_t q = (X - g.lo[k]) * g.dim[k] / g.span[k];
+    c[k] = (int)(q < g.dim[k] - 1 ? q : g.dim[k] - 1);
+  }
+  const int cell = (c[2] * g.dim[1] + c[1]) * g.dim[0] + c[0];
+  tile_of[i] = (gid ? gid[i] : 0) * g.ncell + cell;
+}
+
+__global__ void k_pair_flags(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ col,
+                             const int32_t* __restrict__ tile_of, int n, int32_t* __restrict__ flags) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int64_t base = (int64_t)tile_of[i] * n;
+  for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) flags[base + col[e]] = 1;
+}
+
+__global__ void k_pairs(const int32_t* __restrict__ flags, const int32_t* __restrict__ pidx, int64_t count, int n,
+                        int32_t* __restrict__ pair_node, int32_t* __restrict__ pair_tile) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= count || !flags[q]) return;
+  const int p = pidx[q];
+  pair_node[p] = (int)(q % n);
+  pair_tile[p] = (int)(q / n);
+}
+
+__global__ void k_col_pair(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ col,
+                           const int32_t* __restrict__ tile_of, const int32_t* __restrict__ pidx, int n,
+                           int32_t* __restrict__ col_pair) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int64_t base = (int64_t)tile_of[i] * n;
+  for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) col_pair[e] = pidx[base + col[e]];
+}
+
+// ------------------------------------------------------------ j-side node TP
+// T[item][r][c] = sum_al M[r][al] h_node^(a)[al][c], with the per-node matrix
+// M[r][al] = sum_be C^{d de}_{a al, b be} R^(b)_be(p) built once per item in
+// float64 and kept in LDS (cost independent of C).
+template <int L>
+__global__ __launch_bounds__(256) void k_node_tp(DevTables t, const double* __restrict__ R,
+                                                 const int32_t* __restrict__ node_of, const float* __restrict__ feat,
+                                                 int C, float* __restrict__ T) {
+  constexpr int NK = (L + 1) * (L + 1);
+  extern __shared__ float smem[];
+  __shared__ double Rl[NK];
+  const int item = blockIdx.x;
+  const int node = node_of ? node_of[item] : item;
+  const int CB = C < 256 ? C : 256;
+  const int G = blockDim.x / CB;
+  float* Ml = smem;
+  float* hl = smem + t.m_slots;
+  if (threadIdx.x < NK) Rl[threadIdx.x] = R[(size_t)item * NK + threadIdx.x];
+  __syncthreads();
+  for (int s = threadIdx.x; s < t.m_slots; s += blockDim.x) {
+    double v = 0.0;
+    for (int e = t.m_ptr[s]; e < t.m_ptr[s + 1]; ++e) v += t.m_coef[e] * Rl[t.m_ridx[e]];
+    Ml[s] = (float)v;
+  }
+  const int cl = threadIdx.x % CB, g = threadIdx.x / CB;
+  const float* hsrc = feat + (size_t)node * NK * C;
+  float* Tdst = T + (size_t)item * t.dimT * C;
+  for (int c0 = 0; c0 < C; c0 += CB) {
+    const int cw = (C - c0) < CB ? (C - c0) : CB;
+    __syncthreads();
+    for (int q = threadIdx.x; q < NK * CB; q += blockDim.x) {
+      const int k = q / CB, cc = q % CB;
+      hl[q] = cc < cw ? hsrc[(size_t)k * C + c0 + cc] : 0.0f;
+    }
+    __syncthreads();
+    if (g < G && cl < cw) {
+#pragma unroll
+      for (int a = 0; a <= L; ++a) {
+        const int r1 = t.a_row_start[a + 1];
+        for (int r = t.a_row_start[a] + g; r < r1; r += G) {
+          const float* mrow = Ml + t.m_rowoff[r];
+          float acc = 0.0f;
+#pragma unroll
+          for (int al = 0; al < 2 * a + 1; ++al) acc += mrow[al] * hl[(a * a + al) * CB + cl];
+          Tdst[(size_t)r * C + c0 + cl] = acc;
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------ aggregation
+// S[i][q] = sum_{e in row i} alpha[e][head(q)] T[col_pair[e]][q], q over the
+// flattened (row, channel) vector of width W = dimT*C.  One block per
+// (receiver, 4096-float column chunk); float4 loads, four per thread per edge.
+constexpr int kAggThreads = 256;
+constexpr int kAggUnroll = 4;
+
+__global__ __launch_bounds__(kAggThreads) void k_aggregate(const float4* __restrict__ T,
+                                                           const int64_t* __restrict__ row_ptr,
+                                                           const int32_t* __restrict__ col_pair,
+                                                           const float* __restrict__ alpha, int W4, int C, int dh,
+                                                           int H, float4* __restrict__ S) {
+  const int i = blockIdx.x;
+  const int base = blockIdx.y * (kAggThreads * kAggUnroll) + threadIdx.x;
+  float4 acc[kAggUnroll];
+  int head[kAggUnroll];
+#pragma unroll
+  for (int u = 0; u < kAggUnroll; ++u) {
+    acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    head[u] = (((base + u * kAggThreads) * 4) % C) / dh;
+  }
+  const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+  for (int64_t e = e0; e < e1; ++e) {
+    const float4* trow = T + (size_t)col_pair[e] * W4;
+#pragma unroll
+    for (int u = 0; u < kAggUnroll; ++u) {
+      const int q = base + u * kAggThreads;
+      if (q < W4) {
+        const float a = alpha ? alpha[e * H + head[u]] : 1.0f;
+        const float4 v = trow[q];
+        acc[u].x += a * v.x;
+        acc[u].y += a * v.y;
+        acc[u].z += a * v.z;
+        acc[u].w += a * v.w;
+      }
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kAggUnroll; ++u) {
+    const int q = base + u * kAggThreads;
+    if (q < W4) S[(size_t)i * W4 + q] = acc[u];
+  }
+}
+
+// ------------------------------------------------------------ i-side recouple
+// y_i^(o)[m][c] = sum_col Q_o[m][col] S_i[col][c], with the per-node matrix
+// Q_o[m][(a,b,d,de)] = sum_u K(a,b,d,u,o) sum_ga C^{o m}_{u ga, d de} R^(u)_ga(p_i)
+// built in float64 per receiver and kept in LDS, one output degree at a time.
+template <int L, int O>
+__device__ __forceinline__ void recouple_one(const DevTables& t, const double* Rl, float* Ql, const float* Si,
+                                             int C, float* yi) {
+  constexpr int NM = 2 * O + 1;
+  const int ncol = t.q_ncol[O], s0 = t.q_slotoff[O];
+  __syncthreads();
+  for (int s = threadIdx.x; s < NM * ncol; s += blockDim.x) {
+    double v = 0.0;
+    for (int e = t.q_ptr[s0 + s]; e < t.q_ptr[s0 + s + 1]; ++e) v += t.q_coef[e] * Rl[t.q_ridx[e]];
+    Ql[s] = (float)v;
+  }
+  __syncthreads();
+  const int* cols = t.q_cols + t.q_coloff[O];
+  for (int c = threadIdx.x; c < C; c += blockDim.x) {
+    float acc[NM];
+#pragma unroll
+    for (int m = 0; m < NM; ++m) acc[m] = 0.0f;
+    for (int col = 0; col < ncol; ++col) {
+      const float s = Si[(size_t)cols[col] * C + c];
+#pragma unroll
+      for (int m = 0; m < NM; ++m) acc[m] += Ql[m * ncol + col] * s;
+    }
+#pragma unroll
+    for (int m = 0; m < NM; ++m) yi[(size_t)(O * O + m) * C + c] = acc[m];
+  }
+}
+
+template <int L, int... Os>
+__device__ __forceinline__ void recouple_all(std::integer_sequence<int, Os...>, const DevTables& t, const double* Rl,
+                                             float* Ql, const float* Si, int C, float* yi) {
+  (recouple_one<L, Os>(t, Rl, Ql, Si, C, yi), ...);
+}
+
+template <int L>
+__global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __restrict__ R,
+                                                  const float* __restrict__ S, int C, float* __restrict__ y) {
+  constexpr int NK = (L + 1) * (L + 1);
+  extern __shared__ float Ql[];
+  __shared__ double Rl[NK];
+  const int i = blockIdx.x;
+  if (threadIdx.x < NK) Rl[threadIdx.x] = R[(size_t)i * NK + threadIdx.x];
+  recouple_all<L>(std::make_integer_sequence<int, L + 1>{}, t, Rl, Ql, S + (size_t)i * t.dimT * C, C,
+                  y + (size_t)i * NK * C);
+}
+
+// ------------------------------------------------------------ channel mixing
+// out[row][c'] = sum_c W[o][c'][c] y[row][c] for the rows (i, m) of degree o:
+// a tiled GEMM per degree, 64 rows x 64 output channels per block, 4x4
+// outputs per thread.  With bf16 weights the inputs are rounded to bf16 and
+// the products accumulate in fp32.
+__device__ __forceinline__ float bf16_round(float x) { return __bfloat162float(__float2bfloat16(x)); }
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_mix(const float* __restrict__ y, const void* __restrict__ Wv, int n, int nk,
+                                             int o, int C, float* __restrict__ out) {
+  __shared__ float Ys[16][64 + 1];
+  __shared__ float Ws[16][64 + 1];
+  const int nm = 2 * o + 1;
+  const int64_t rows = (int64_t)n * nm;
+  const int64_t r0 = (int64_t)blockIdx.x * 64;
+  const int n0 = blockIdx.y * 64;
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  float acc[4][4] = {};
+  auto row_addr = [&](int64_t r) -> int64_t {
+    const int64_t i = r / nm, m = r % nm;
+    return (i * nk + o * o + m) * (int64_t)C;
+  };
+  for (int k0 = 0; k0 < C; k0 += 16) {
+    for (int q = threadIdx.x; q < 16 * 64; q += 256) {
+      const int rr = q / 16, kk = q % 16;  // Y tile: 64 rows x 16 k
+      const int64_t r = r0 + rr;
+      float v = 0.0f;
+      if (r < rows && k0 + kk < C) v = y[row_addr(r) + k0 + kk];
+      Ys[kk][rr] = BF16 ? bf16_round(v) : v;
+      const int nn = q / 16;  // W tile: 64 out channels x 16 k
+      float w = 0.0f;
+      if (n0 + nn < C && k0 + kk < C) {
+        const size_t wi = ((size_t)o * C + n0 + nn) * C + k0 + kk;
+        w = BF16 ? __bfloat162float(((const __hip_bfloat16*)Wv)[wi]) : ((const float*)Wv)[wi];
+      }
+      Ws[kk][nn] = w;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        a[u] = Ys[kk][ty * 4 + u];
+        b[u] = Ws[kk][tx * 4 + u];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[u][v] += a[u] * b[v];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int64_t r = r0 + ty * 4 + u;
+    if (r >= rows) continue;
+    const int64_t base = row_addr(r);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int cn = n0 + tx * 4 + v;
+      if (cn < C) out[base + cn] = acc[u][v];
+    }
+  }
+}
+
+// ------------------------------------------------------------ edge baseline
+// Per receiver block: edges in batches of EB; for each edge the filter
+// K[k][q] = sum_f w_afo sum_mf C^{o m}_{a al, f mf} R^(f)_mf(r_i - r_j) is built
+// once in LDS (cost independent of C), then every channel applies it to h_j.
+template <int L>
+__global__ __launch_bounds__(128) void k_edge_tp(DevTables t, const float* __restrict__ pos,
+                                                 const float* __restrict__ feat, const int64_t* __restrict__ row_ptr,
+                                                 const int32_t* __restrict__ col, const float* __restrict__ alpha,
+                                                 int C, int H, float* __restrict__ y) {
+  constexpr int NK = (L + 1) * (L + 1);
+  constexpr int EB = 4;
+  extern __shared__ float sm[];
+  float* Kl = sm;                 // [EB][NK*NK]
+  float* Rl = sm + EB * NK * NK;  // [EB][NK]
+  const int i = blockIdx.x;
+  const int dh = C / H;
+  const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+  const float xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
+  for (int c0 = 0; c0 < C; c0 += blockDim.x) {
+    const int c = c0 + threadIdx.x;
+    const bool live = c < C;
+    float acc[NK];
+#pragma unroll
+    for (int k = 0; k < NK; ++k) acc[k] = 0.0f;
+    for (int64_t eb = e0; eb < e1; eb += EB) {
+      const int nb = (e1 - eb) < EB ? (int)(e1 - eb) : EB;
+      __syncthreads();
+      for (int q = threadIdx.x; q < nb * NK; q += blockDim.x) {
+        const int b = q / NK, k = q % NK;
+        const int j = col[eb + b];
+        Rl[q] = sh_poly<float>(t, k, xi - pos[3 * j], yi - pos[3 * j + 1], zi - pos[3 * j + 2]);
+      }
+      __syncthreads();
+      for (int q = threadIdx.x; q < nb * NK * NK; q += blockDim.x) {
+        const int b = q / (NK * NK), s = q % (NK * NK);
+        float v = 0.0f;
+        for (int e = t.k_ptr[s]; e < t.k_ptr[s + 1]; ++e) v += t.k_coef[e] * Rl[b * NK + t.k_ridx[e]];
+        Kl[q] = v;
+      }
+      __syncthreads();
+      if (live) {
+        for (int b = 0; b < nb; ++b) {
+          const int j = col[eb + b];
+          const float a = alpha ? alpha[(eb + b) * H + c / dh] : 1.0f;
+          float h[NK];
+#pragma unroll
+          for (int q = 0; q < NK; ++q) h[q] = a * feat[((size_t)j * NK + q) * C + c];
+          const float* Kb = Kl + b * NK * NK;
+#pragma unroll
+          for (int k = 0; k < NK; ++k) {
+            float s = 0.0f;
+#pragma unroll
+            for (int q = 0; q < NK; ++q) s += Kb[k * NK + q] * h[q];
+            acc[k] += s;
+          }
+        }
+      }
+    }
+    if (live) {
+#pragma unroll
+      for (int k = 0; k < NK; ++k) y[((size_t)i * NK + k) * C + c] = acc[k];
+    }
+  }
+}
+
+// Kernels whose dynamic LDS exceeds the 64 KB default must opt in (gfx950
+// has 160 KB per CU).
+template <typename K>
+hipError_t allow_lds(K kernel, size_t bytes) {
+  if (bytes <= 65536) return hipSuccess;
+  return hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
+}  // namespace
+
+// ============================================================ launchers
+hipError_t launch_sh(const DevTables& t, const float* pos, const int32_t* node_of, const double* origins_d,
+                     const float* origins_f, const int32_t* origin_id, int origin_mod, int n, double* out_d,
+                     float* out_f, hipStream_t s) {
+  const int64_t total = (int64_t)n * t.nk;
+  if (total == 0) return hipSuccess;
+  k_sh<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(t, pos, node_of, origins_d, origins_f, origin_id, origin_mod,
+                                                        n, out_d, out_f);
+  return hipGetLastError();
+}
+
+hipError_t launch_tile_keys(const float* pos, const int32_t* graph_id, int n, const int* lo, const int* dim,
+                            const int64_t* span, int ncell, int32_t* tile_of, hipStream_t s) {
+  TileGrid g;
+  for (int k = 0; k < 3; ++k) {
+    g.lo[k] = lo[k];
+    g.dim[k] = dim[k];
+    g.span[k] = span[k];
+  }
+  g.ncell = ncell;
+  if (n > 0) k_tile_keys<<<(n + 255) / 256, 256, 0, s>>>(pos, graph_id, n, g, tile_of);
+  return hipGetLastError();
+}
+
+hipError_t launch_pair_flags(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of, int n,
+                             int32_t* flags, hipStream_t s) {
+  if (n > 0) k_pair_flags<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, col_idx, tile_of, n, flags);
+  return hipGetLastError();
+}
+
+size_t scan_tmp_bytes(int64_t count) {
+  size_t b = 0;
+  hipcub::DeviceScan::ExclusiveSum(nullptr, b, (const int32_t*)nullptr, (int32_t*)nullptr, (int)count);
+  return b;
+}
+
+hipError_t launch_scan_i32(const int32_t* in, int32_t* out, int64_t count, void* tmp, size_t tmp_bytes,
+                           hipStream_t s) {
+  size_t b = tmp_bytes;
+  return hipcub::DeviceScan::ExclusiveSum(tmp, b, in, out, (int)count, s);
+}
+
+hipError_t launch_pairs(const int32_t* flags, const int32_t* pidx, int64_t count, int n, int32_t* pair_node,
+                        int32_t* pair_tile, hipStream_t s) {
+  if (count > 0)
+    k_pairs<<<(unsigned)((count + 255) / 256), 256, 0, s>>>(flags, pidx, count, n, pair_node, pair_tile);
+  return hipGetLastError();
+}
+
+hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of,
+                           const int32_t* pidx, int n, int32_t* col_pair, hipStream_t s) {
+  if (n > 0) k_col_pair<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, col_idx, tile_of, pidx, n, col_pair);
+  return hipGetLastError();
+}
+
+hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* node_of, const float* feat,
+                          int n_items, int C, float* T, hipStream_t s) {
+  if (n_items == 0) return hipSuccess;
+  const int CB = C < 256 ? C : 256;
+  const size_t lds = sizeof(float) * ((size_t)t.m_slots + (size_t)t.nk * CB);
+  switch (t.L) {
+#define E2F_CASE(LL)                                                                                        \
+  case LL:                                                                                                  \
+    if (hipError_t e = allow_lds(k_node_tp<LL>, lds); e != hipSuccess) return e;                            \
+    k_node_tp<LL><<<n_items, 256, lds, s>>>(t, R, node_of, feat, C, T);                                     \
+    break;
+    E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
+#undef E2F_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_t* col_pair, const float* alpha,
+                            int n, int dimT, int C, int H, float* S, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int64_t W4 = (int64_t)dimT * C / 4;
+  dim3 grid(n, (unsigned)((W4 + kAggThreads * kAggUnroll - 1) / (kAggThreads * kAggUnroll)));
+  k_aggregate<<<grid, kAggThreads, 0, s>>>((const float4*)T, row_ptr, col_pair, alpha, (int)W4, C, C / H, H,
+                                           (float4*)S);
+  return hipGetLastError();
+}
+
+hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, int n, int C, float* y,
+                           hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int threads = C <= 64 ? 64 : (C <= 128 ? 128 : 256);
+  const size_t lds = sizeof(float) * (size_t)t.max_qslots;
+  switch (t.L) {
+#define E2F_CASE(LL)                                                                                        \
+  case LL:                                                                                                  \
+    if (hipError_t e = allow_lds(k_recouple<LL>, lds); e != hipSuccess) return e;                           \
+    k_recouple<LL><<<n, threads, lds, s>>>(t, R, S, C, y);                                                  \
+    break;
+    E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
+#undef E2F_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_mix(int L, const float* y, const void* W, bool w_bf16, int n, int C, float* out, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int nk = (L + 1) * (L + 1);
+  for (int o = 0; o <= L; ++o) {
+    const int64_t rows = (int64_t)n * (2 * o + 1);
+    dim3 grid((unsigned)((rows + 63) / 64), (unsigned)((C + 63) / 64));
+    if (w_bf16) k_mix<true><<<grid, 256, 0, s>>>(y, W, n, nk, o, C, out);
+    else k_mix<false><<<grid, 256, 0, s>>>(y, W, n, nk, o, C, out);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_tp(const DevTables& t, const float* pos, const float* feat, const int64_t* row_ptr,
+                          const int32_t* col_idx, const float* alpha, int n, int C, int H, float* y, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int threads = C <= 64 ? 64 : 128;
+  const size_t lds = sizeof(float) * ((size_t)4 * t.nk * t.nk + (size_t)4 * t.nk);
+  switch (t.L) {
+#define E2F_CASE(LL)                                                                                        \
+  case LL:                                                                                                  \
+    if (hipError_t e = allow_lds(k_edge_tp<LL>, lds); e != hipSuccess) return e;                            \
+    k_edge_tp<LL><<<n, threads, lds, s>>>(t, pos, feat, row_ptr, col_idx, alpha, C, H, y);                  \
+    break;
+    E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
+#undef E2F_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace e2f

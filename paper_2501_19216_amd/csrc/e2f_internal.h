@@ -1,0 +1,80 @@
+// Internal declarations shared by the host code (tables, C ABI) and the HIP
+// kernels of libe2f.  Nothing here is part of the public ABI (include/e2f.h).
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+namespace e2f {
+
+constexpr int kMaxL = 6;          // largest supported degree L
+constexpr double kGrid = 65536.0; // positions are compared on a 2^-16 A grid
+
+inline int nk_of(int L) { return (L + 1) * (L + 1); }
+
+// ---------------------------------------------------------------- host tables
+// Real-basis Clebsch-Gordan tensor C[m1][m2][m3] for (l1,l2,l3), row-major,
+// built from the explicit CG formula and the real change of basis (tables.cpp).
+std::vector<double> real_cg(int l1, int l2, int l3);
+// Recoupling weight X(a,b,u,o;d) of [A (x) [C (x) B]^(b+u)]^(o) onto
+// [C (x) [A (x) B]^(d)]^(o) (Def. 2.3), closed form from the Wigner 6j symbol.
+double recoupling_weight(int a, int b, int u, int o, int d);
+double wigner6j(int j1, int j2, int j3, int j4, int j5, int j6);
+
+// Structure of the factorised layer for one L: every table is independent of
+// the path weights except the *_coef arrays, which the context refreshes when
+// the caller's path weights change.
+struct Block {
+  int a, b, d, toff;  // T_j^(a,b,d) occupies rows toff .. toff+2d
+};
+
+struct LayerTables {
+  int L = 0, nk = 0, dimT = 0;
+  std::vector<Block> blocks;        // sorted by (a, b, d)
+  std::vector<int> a_row_start;     // [L+2] first T row of each a
+  // solid harmonics as polynomials: component k = sum_t coef_t x^ex y^ey z^ez
+  std::vector<int> sh_ptr;          // [nk+1]
+  std::vector<int> sh_pow;          // packed ex | ey<<4 | ez<<8
+  std::vector<double> sh_coef;
+  // j-side per-node matrix M: row r of T has (2a+1) slots starting at m_rowoff[r]
+  std::vector<int> m_rowoff;        // [dimT+1]
+  std::vector<int> m_ptr;           // [nslots+1] entries of each slot
+  std::vector<int> m_ridx;          // index into R (l*l + l + m)
+  std::vector<double> m_coef;       // CG value
+  // i-side per-node matrix Q_o, (2o+1) x ncol[o], for each output degree o
+  std::vector<int> q_ncol;          // [L+1]
+  std::vector<int> q_coloff;        // [L+2] offset of o's column list in q_cols
+  std::vector<int> q_cols;          // T row index of each column
+  std::vector<int> q_slotoff;       // [L+2] offset of o's slots
+  std::vector<int> q_ptr;           // [nslots+1]
+  std::vector<int> q_ridx;
+  std::vector<int> q_path;          // (a*(L+1)+f)*(L+1)+o of the path weight
+  std::vector<double> q_unit;       // coefficient without the path weight
+  // edge tensor product filter K[k][q] (dense nk x nk)
+  std::vector<int> k_ptr;           // [nk*nk+1]
+  std::vector<int> k_ridx;
+  std::vector<int> k_path;
+  std::vector<double> k_unit;
+  int max_qslots = 0;               // largest (2o+1)*ncol[o]
+  int m_slots() const { return m_rowoff.back(); }
+};
+
+LayerTables build_layer_tables(int L);
+int64_t node_tp_dim(int L);
+
+// ---------------------------------------------------------------- device side
+// Device copies of one LayerTables (pointers into one allocation).
+struct DevTables {
+  int L, nk, dimT;
+  const int* a_row_start;
+  const int* sh_ptr; const int* sh_pow; const double* sh_coef;
+  const int* m_rowoff; const int* m_ptr; const int* m_ridx; const double* m_coef;
+  const int* q_ncol; const int* q_coloff; const int* q_cols; const int* q_slotoff;
+  const int* q_ptr; const int* q_ridx; const double* q_coef; // q_coef includes path weights
+  const int* k_ptr; const int* k_ridx; const float* k_coef;  // k_coef includes path weights
+  int max_qslots, m_slots;
+};
+
+}  // namespace e2f

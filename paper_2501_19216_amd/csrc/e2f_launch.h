@@ -1,0 +1,63 @@
+// Kernel launchers of libe2f (implemented in neighbor.hip and conv.hip).
+// All sizes are checked by the callers in abi.cpp before these run.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "e2f_internal.h"
+
+namespace e2f {
+
+// stats[0..2] = min grid coordinate, stats[3..5] = max, stats[6] = max
+// graph id, stats[7] = error bits (1: bad position, 2: negative graph id).
+constexpr int kStatsInts = 8;
+hipError_t launch_bbox(const float* pos, const int32_t* graph_id, int n, int* stats, hipStream_t s);
+
+// ---- radius graph
+struct CellGrid {
+  int lo[3];
+  int64_t side;   // cell side in grid units (>= cutoff)
+  int dim[3];
+  int64_t ncell;
+};
+size_t nl_scratch_bytes(int n, const CellGrid& g);  // cell tables and counts
+hipError_t launch_nl_count(const float* pos, const int32_t* graph_id, int n, double r2, const CellGrid& g,
+                           void* scratch, int64_t* row_ptr, hipStream_t s);
+// After the count: sorts n+1 counts into row_ptr (exclusive scan).  Part of launch_nl_count.
+hipError_t launch_nl_fill(const float* pos, const int32_t* graph_id, int n, double r2, const CellGrid& g,
+                          void* scratch, const int64_t* row_ptr, int32_t* unsorted, int32_t* col_idx, int64_t E,
+                          void* sort_tmp, size_t sort_tmp_bytes, hipStream_t s);
+size_t nl_sort_tmp_bytes(int n, int64_t E);
+
+// ---- solid harmonics: out[item][k], item -> node node_of[item] (or item),
+// origin origins[origin_id[item] % origin_mod] (or 0 / zero vector)
+hipError_t launch_sh(const DevTables& t, const float* pos, const int32_t* node_of, const double* origins_d,
+                     const float* origins_f, const int32_t* origin_id, int origin_mod, int n, double* out_d,
+                     float* out_f, hipStream_t s);
+
+// ---- tile plan of the factorised forward
+hipError_t launch_tile_keys(const float* pos, const int32_t* graph_id, int n, const int* lo, const int* dim,
+                            const int64_t* span, int ncell, int32_t* tile_of, hipStream_t s);
+hipError_t launch_pair_flags(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of, int n,
+                             int32_t* flags, hipStream_t s);
+size_t scan_tmp_bytes(int64_t count);
+hipError_t launch_scan_i32(const int32_t* in, int32_t* out, int64_t count, void* tmp, size_t tmp_bytes, hipStream_t s);
+hipError_t launch_pairs(const int32_t* flags, const int32_t* pidx, int64_t count, int n, int32_t* pair_node,
+                        int32_t* pair_tile, hipStream_t s);
+hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of,
+                           const int32_t* pidx, int n, int32_t* col_pair, hipStream_t s);
+
+// ---- factorised layer
+hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* node_of, const float* feat,
+                          int n_items, int C, float* T, hipStream_t s);
+hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_t* col_pair, const float* alpha,
+                            int n, int dimT, int C, int H, float* S, hipStream_t s);
+hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, int n, int C, float* y,
+                           hipStream_t s);
+
+// ---- per-irrep channel mixing and the edge baseline
+hipError_t launch_mix(int L, const float* y, const void* W, bool w_bf16, int n, int C, float* out, hipStream_t s);
+hipError_t launch_edge_tp(const DevTables& t, const float* pos, const float* feat, const int64_t* row_ptr,
+                          const int32_t* col_idx, const float* alpha, int n, int C, int H, float* y, hipStream_t s);
+
+}  // namespace e2f

@@ -1,0 +1,226 @@
+// Radius graph on gfx950 (Alg. 1 step 2: D_ij = |r_i - r_j|, kept below the
+// cutoff).  Cell list with integer cell coordinates on the 2^-16 A grid:
+//   bbox (atomic min/max) -> cell counts -> exclusive scan -> cell members ->
+//   per-atom neighbour count over the 27 cells (exact integer predicate) ->
+//   exclusive scan into row_ptr -> fill -> segmented sort of every row.
+// Only integer atomics are used, and the rows are sorted at the end, so the
+// CSR is bitwise deterministic.
+#include <hip/hip_runtime.h>
+#include <hipcub/hipcub.hpp>
+
+#include "e2f_launch.h"
+
+namespace e2f {
+namespace {
+
+__device__ __forceinline__ int grid_coord(float x) { return __float2int_rn(x * 65536.0f); }
+
+__global__ void k_bbox(const float* __restrict__ pos, const int32_t* __restrict__ gid, int n, int* __restrict__ st) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  for (int k = 0; k < 3; ++k) {
+    const float x = pos[3 * i + k];
+    if (!(fabsf(x) < 16384.0f)) {  // also catches NaN
+      atomicOr(&st[7], 1);
+      return;
+    }
+    const int X = grid_coord(x);
+    atomicMin(&st[k], X);
+    atomicMax(&st[3 + k], X);
+  }
+  if (gid) {
+    const int g = gid[i];
+    if (g < 0) atomicOr(&st[7], 2);
+    else atomicMax(&st[6], g);
+  }
+}
+
+__global__ void k_stats_init(int* st) {
+  if (threadIdx.x < 3) st[threadIdx.x] = INT_MAX;
+  else if (threadIdx.x < 6) st[threadIdx.x] = INT_MIN;
+  else if (threadIdx.x < kStatsInts) st[threadIdx.x] = 0;
+}
+
+struct Grid {
+  int lo0, lo1, lo2;
+  int d0, d1, d2;
+  int64_t side;
+};
+
+__device__ __forceinline__ int cell_axis(int X, int lo, int64_t side, int d) {
+  int64_t c = ((int64_t)X - lo) / side;
+  return (int)(c < d - 1 ? c : d - 1);
+}
+
+__global__ void k_cell_count(const float* __restrict__ pos, int n, Grid g, int* __restrict__ cell_of,
+                             int* __restrict__ cell_cnt) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int cx = cell_axis(grid_coord(pos[3 * i]), g.lo0, g.side, g.d0);
+  const int cy = cell_axis(grid_coord(pos[3 * i + 1]), g.lo1, g.side, g.d1);
+  const int cz = cell_axis(grid_coord(pos[3 * i + 2]), g.lo2, g.side, g.d2);
+  const int c = (cz * g.d1 + cy) * g.d0 + cx;
+  cell_of[i] = c;
+  atomicAdd(&cell_cnt[c], 1);
+}
+
+__global__ void k_cell_place(int n, const int* __restrict__ cell_of, const int* __restrict__ cell_start,
+                             int* __restrict__ cell_fill, int* __restrict__ members) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int c = cell_of[i];
+  members[cell_start[c] + atomicAdd(&cell_fill[c], 1)] = i;
+}
+
+// Count (out == nullptr) or write the neighbours of atom i.
+template <bool WRITE>
+__global__ void k_neighbors(const float* __restrict__ pos, const int32_t* __restrict__ gid, int n, double r2, Grid g,
+                            const int* __restrict__ cell_of, const int* __restrict__ cell_start,
+                            const int* __restrict__ members, int64_t* __restrict__ counts,
+                            const int64_t* __restrict__ row_ptr, int32_t* __restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int xi = grid_coord(pos[3 * i]), yi = grid_coord(pos[3 * i + 1]), zi = grid_coord(pos[3 * i + 2]);
+  const int gi = gid ? gid[i] : 0;
+  const int c = cell_of[i];
+  const int cx = c % g.d0, cy = (c / g.d0) % g.d1, cz = c / (g.d0 * g.d1);
+  int64_t cnt = 0;
+  int64_t w = WRITE ? row_ptr[i] : 0;
+  for (int dz = -1; dz <= 1; ++dz) {
+    const int z = cz + dz;
+    if (z < 0 || z >= g.d2) continue;
+    for (int dy = -1; dy <= 1; ++dy) {
+      const int y = cy + dy;
+      if (y < 0 || y >= g.d1) continue;
+      for (int dx = -1; dx <= 1; ++dx) {
+        const int x = cx + dx;
+        if (x < 0 || x >= g.d0) continue;
+        const int cc = (z * g.d1 + y) * g.d0 + x;
+        for (int q = cell_start[cc]; q < cell_start[cc + 1]; ++q) {
+          const int j = members[q];
+          if (j == i) continue;
+          if (gid && gid[j] != gi) continue;
+          const int64_t ddx = (int64_t)grid_coord(pos[3 * j]) - xi;
+          const int64_t ddy = (int64_t)grid_coord(pos[3 * j + 1]) - yi;
+          const int64_t ddz = (int64_t)grid_coord(pos[3 * j + 2]) - zi;
+          const int64_t d2 = ddx * ddx + ddy * ddy + ddz * ddz;  // < 2^53 for cutoff <= 64 A
+          if ((double)d2 < r2) {
+            if (WRITE) out[w++] = j;
+            else ++cnt;
+          }
+        }
+      }
+    }
+  }
+  if (!WRITE) counts[i] = cnt;
+}
+
+__global__ void k_zero_last(int64_t* counts, int n) { counts[n] = 0; }
+
+Grid to_grid(const CellGrid& cg) {
+  return Grid{cg.lo[0], cg.lo[1], cg.lo[2], cg.dim[0], cg.dim[1], cg.dim[2], cg.side};
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct NlScratch {
+  int* cell_of;
+  int* cell_cnt;    // ncell + 1 (becomes the fill cursor)
+  int* cell_start;  // ncell + 1
+  int* members;
+  int64_t* counts;  // n + 1
+  void* scan_tmp;
+  size_t scan_bytes;
+};
+
+size_t scan_bytes_cells(int64_t ncell) {
+  size_t b = 0;
+  hipcub::DeviceScan::ExclusiveSum(nullptr, b, (int*)nullptr, (int*)nullptr, (int)(ncell + 1));
+  return b;
+}
+size_t scan_bytes_counts(int n) {
+  size_t b = 0;
+  hipcub::DeviceScan::ExclusiveSum(nullptr, b, (int64_t*)nullptr, (int64_t*)nullptr, n + 1);
+  return b;
+}
+
+NlScratch carve(void* base, int n, const CellGrid& g) {
+  char* p = (char*)base;
+  NlScratch s;
+  s.cell_of = (int*)p; p += align256(sizeof(int) * (size_t)n);
+  s.cell_cnt = (int*)p; p += align256(sizeof(int) * (size_t)(g.ncell + 1));
+  s.cell_start = (int*)p; p += align256(sizeof(int) * (size_t)(g.ncell + 1));
+  s.members = (int*)p; p += align256(sizeof(int) * (size_t)n);
+  s.counts = (int64_t*)p; p += align256(sizeof(int64_t) * (size_t)(n + 1));
+  s.scan_bytes = std::max(scan_bytes_cells(g.ncell), scan_bytes_counts(n));
+  s.scan_tmp = p;
+  return s;
+}
+
+}  // namespace
+
+hipError_t launch_bbox(const float* pos, const int32_t* graph_id, int n, int* stats, hipStream_t s) {
+  k_stats_init<<<1, 64, 0, s>>>(stats);
+  if (n > 0) k_bbox<<<(n + 255) / 256, 256, 0, s>>>(pos, graph_id, n, stats);
+  return hipGetLastError();
+}
+
+size_t nl_scratch_bytes(int n, const CellGrid& g) {
+  size_t b = 0;
+  b += align256(sizeof(int) * (size_t)n);
+  b += 2 * align256(sizeof(int) * (size_t)(g.ncell + 1));
+  b += align256(sizeof(int) * (size_t)n);
+  b += align256(sizeof(int64_t) * (size_t)(n + 1));
+  b += align256(std::max(scan_bytes_cells(g.ncell), scan_bytes_counts(n)));
+  return b;
+}
+
+hipError_t launch_nl_count(const float* pos, const int32_t* graph_id, int n, double r2, const CellGrid& cg,
+                           void* scratch, int64_t* row_ptr, hipStream_t st) {
+  NlScratch s = carve(scratch, n, cg);
+  Grid g = to_grid(cg);
+  hipError_t e = hipMemsetAsync(s.cell_cnt, 0, sizeof(int) * (size_t)(cg.ncell + 1), st);
+  if (e != hipSuccess) return e;
+  const int blocks = (n + 255) / 256;
+  k_cell_count<<<blocks, 256, 0, st>>>(pos, n, g, s.cell_of, s.cell_cnt);
+  size_t tb = s.scan_bytes;
+  e = hipcub::DeviceScan::ExclusiveSum(s.scan_tmp, tb, s.cell_cnt, s.cell_start, (int)(cg.ncell + 1), st);
+  if (e != hipSuccess) return e;
+  e = hipMemsetAsync(s.cell_cnt, 0, sizeof(int) * (size_t)(cg.ncell + 1), st);
+  if (e != hipSuccess) return e;
+  k_cell_place<<<blocks, 256, 0, st>>>(n, s.cell_of, s.cell_start, s.cell_cnt, s.members);
+  k_neighbors<false><<<blocks, 256, 0, st>>>(pos, graph_id, n, r2, g, s.cell_of, s.cell_start, s.members, s.counts,
+                                            nullptr, nullptr);
+  k_zero_last<<<1, 1, 0, st>>>(s.counts, n);
+  tb = s.scan_bytes;
+  e = hipcub::DeviceScan::ExclusiveSum(s.scan_tmp, tb, s.counts, row_ptr, n + 1, st);
+  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+size_t nl_sort_tmp_bytes(int n, int64_t E) {
+  size_t b = 0;
+  hipcub::DeviceSegmentedRadixSort::SortKeys(nullptr, b, (const int32_t*)nullptr, (int32_t*)nullptr, (int)E, n,
+                                             (const int64_t*)nullptr, (const int64_t*)nullptr, 0, 32);
+  return b;
+}
+
+hipError_t launch_nl_fill(const float* pos, const int32_t* graph_id, int n, double r2, const CellGrid& cg,
+                          void* scratch, const int64_t* row_ptr, int32_t* unsorted, int32_t* col_idx, int64_t E,
+                          void* sort_tmp, size_t sort_tmp_bytes, hipStream_t st) {
+  NlScratch s = carve(scratch, n, cg);
+  Grid g = to_grid(cg);
+  k_neighbors<true><<<(n + 255) / 256, 256, 0, st>>>(pos, graph_id, n, r2, g, s.cell_of, s.cell_start, s.members,
+                                                    nullptr, row_ptr, unsorted);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  int bits = 1;
+  while ((1LL << bits) < (int64_t)n) ++bits;
+  size_t tb = sort_tmp_bytes;
+  e = hipcub::DeviceSegmentedRadixSort::SortKeys(sort_tmp, tb, unsorted, col_idx, (int)E, n, row_ptr, row_ptr + 1, 0,
+                                                 bits, st);
+  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+}  // namespace e2f

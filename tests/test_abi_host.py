@@ -1,0 +1,114 @@
+"""CPU-only checks of the C ABI boundary: the library loads without a GPU,
+exports every symbol include/e2f.h declares, rejects bad arguments before
+any device work, and its independently generated coefficient tables agree
+with the oracle's."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as o
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def e2f():
+    import paper_2501_19216_amd as e
+    return e
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "e2f.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(e2f_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(e2f):
+    names = declared_functions()
+    assert len(names) >= 11
+    assert sorted(e2f.EXPORTED) == names
+    lib = ctypes.CDLL(e2f.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_node_tp_dim(e2f):
+    assert [e2f.e2f_node_tp_dim(L) for L in (2, 3, 4, 6)] == [58, 183, 454, 1767]
+    assert e2f.e2f_node_tp_dim(-1) == -1 and e2f.e2f_node_tp_dim(7) == -1
+
+
+def test_tables_agree_with_oracle(e2f):
+    for l1 in range(7):
+        for l2 in range(7):
+            for l3 in range(abs(l1 - l2), l1 + l2 + 1):
+                assert np.max(np.abs(e2f.e2f_real_cg(l1, l2, l3) - o.cg_real(l1, l2, l3))) < 1e-13
+    for a in range(5):
+        for b in range(5):
+            for u in range(5 - b):
+                for oo in range(5):
+                    for d in range(9):
+                        assert abs(e2f.e2f_recoupling_weight(a, b, u, oo, d) - o.recoupling_x(a, b, u, oo, d)) < 1e-12
+    with pytest.raises(e2f.E2FError):
+        e2f.e2f_real_cg(1, 1, 3)
+
+
+def _params(e2f, **kw):
+    base = dict(lmax=2, channels=16, heads=4, cutoff=5.0, path_w=None, mix_w=None, mix_dtype=0, tile_side=0.0)
+    base.update(kw)
+    return e2f.ConvParams(**base)
+
+
+FAKE = ctypes.c_void_p(256)  # never dereferenced: every call below fails before device work
+
+
+@pytest.mark.parametrize("fn", ["e2f_wigner6j_conv_forward", "e2f_edge_tp_conv_forward"])
+def test_conv_argument_checks(e2f, fn):
+    ctx = e2f.e2f_create(4, None)
+    f = getattr(e2f.lib, fn)
+
+    def call(prm, n=8, E=20, pos=FAKE, feat=FAKE, rp=FAKE, ci=FAKE, out=FAKE, handle=ctx.handle):
+        return f(handle, ctypes.byref(prm) if prm is not None else None, pos, None, feat, n, rp, ci, E, None, out, None)
+
+    EINVAL, EUNS, EDEV = e2f.E2F_EINVAL, e2f.E2F_EUNSUPPORTED, e2f.E2F_EDEVICE
+    assert call(_params(e2f)) == EDEV  # valid, but the context has no device
+    assert call(None) == EINVAL
+    assert call(_params(e2f), handle=None) == EINVAL
+    assert call(_params(e2f, lmax=5)) == EINVAL      # above the context's lmax_max
+    assert call(_params(e2f, lmax=7)) == EUNS
+    assert call(_params(e2f, heads=3)) == EINVAL     # 16 % 3
+    assert call(_params(e2f, channels=18, heads=2)) == EUNS
+    assert call(_params(e2f, cutoff=0.0)) == EINVAL
+    assert call(_params(e2f, cutoff=float("nan"))) == EINVAL
+    assert call(_params(e2f, tile_side=-1.0)) == EINVAL
+    assert call(_params(e2f, mix_dtype=7)) == EINVAL
+    assert call(_params(e2f), n=-1) == EINVAL
+    assert call(_params(e2f), E=-1) == EINVAL
+    assert call(_params(e2f), E=2 ** 31) == EUNS
+    assert call(_params(e2f), pos=None) == EINVAL
+    assert call(_params(e2f), ci=None) == EINVAL
+    w = np.full(27, np.inf)
+    assert call(_params(e2f, path_w=w.ctypes.data_as(ctypes.c_void_p))) == EINVAL
+    assert "path_w" in e2f.lib.e2f_last_error().decode()
+    ctx.close()
+
+
+def test_other_argument_checks(e2f):
+    ctx = e2f.e2f_create(6, None)
+    lib = e2f.lib
+    E = ctypes.c_int64(0)
+    assert lib.e2f_neighbor_list(ctx.handle, FAKE, None, 10, 5.0, FAKE, None, 0, ctypes.byref(E), None) == e2f.E2F_EDEVICE
+    assert lib.e2f_neighbor_list(ctx.handle, FAKE, None, 10, -5.0, FAKE, None, 0, ctypes.byref(E), None) == e2f.E2F_EINVAL
+    assert lib.e2f_neighbor_list(ctx.handle, FAKE, None, 10, 65.0, FAKE, None, 0, ctypes.byref(E), None) == e2f.E2F_EINVAL
+    assert lib.e2f_neighbor_list(ctx.handle, FAKE, None, 10, 5.0, None, None, 0, ctypes.byref(E), None) == e2f.E2F_EINVAL
+    assert lib.e2f_neighbor_list(None, FAKE, None, 10, 5.0, FAKE, None, 0, ctypes.byref(E), None) == e2f.E2F_EINVAL
+    assert lib.e2f_solid_harmonics(ctx.handle, FAKE, None, None, 10, 7, FAKE, None) == e2f.E2F_EINVAL
+    assert lib.e2f_solid_harmonics(ctx.handle, FAKE, None, None, 10, 3, FAKE, None) == e2f.E2F_EDEVICE
+    assert lib.e2f_node_tp(ctx.handle, FAKE, None, None, FAKE, 10, 6, 3, FAKE, None) == e2f.E2F_EUNSUPPORTED
+    assert lib.e2f_node_tp(ctx.handle, FAKE, None, None, FAKE, 10, 8, 3, FAKE, None) == e2f.E2F_EDEVICE
+    h = ctypes.c_void_p()
+    assert lib.e2f_create(7, -1, ctypes.byref(h)) == e2f.E2F_EINVAL
+    assert lib.e2f_create(3, -2, ctypes.byref(h)) == e2f.E2F_EINVAL
+    ctx.close()

@@ -1,0 +1,186 @@
+"""GPU parity of every step of the hot path against the fp64 oracle.
+
+Calls go through the C ABI (the ctypes binding of libe2f.so).  Bars:
+radius graph bit-exact; float32 layer max relative error <= 1e-4 per output
+irrep block; bf16 channel mixing <= 1e-2.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as o
+import e2f_synth as syn
+from cases import TOL_BF16, TOL_F32, case, sample_rows
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module")
+def e2f():
+    import paper_2501_19216_amd as e
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    return e
+
+
+@pytest.fixture(scope="module")
+def ctx(e2f):
+    c = e2f.e2f_create(6, 0)
+    yield c
+    c.close()
+
+
+def gpu(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.to(DEV)
+
+
+def run_both(e2f, ctx, inp, rp, ci, alpha, L, H, cutoff, mix=None, mix_bf16=False, tile_side=0.0):
+    pos, feat = gpu(inp.pos), gpu(inp.feat)
+    row_ptr, col = gpu(rp), gpu(ci)
+    al = gpu(alpha)
+    gid = None if inp.graph_id is None else gpu(inp.graph_id)
+    mw = None
+    if mix is not None:
+        mw = gpu(mix).to(torch.bfloat16) if mix_bf16 else gpu(mix)
+    y6 = e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col, al, L, H, cutoff, mix_w=mw, graph_id=gid,
+                                       tile_side=tile_side)
+    ye = e2f.e2f_edge_tp_conv_forward(ctx, pos, feat, row_ptr, col, al, L, H, cutoff, mix_w=mw, graph_id=gid)
+    torch.cuda.synchronize()
+    return y6.cpu().numpy(), ye.cpu().numpy()
+
+
+# ------------------------------------------------------------ radius graph
+@pytest.mark.parametrize("name", ["cluster32_L2", "molecules256x30_L3", "water2000_L4", "protein20k_L4"])
+def test_neighbor_list_bit_exact(e2f, ctx, name):
+    inp, rp, ci, _ = case(name)
+    wl = inp.workload
+    gid = None if inp.graph_id is None else gpu(inp.graph_id)
+    g_rp, g_ci = e2f.e2f_neighbor_list(ctx, gpu(inp.pos), wl.cutoff, gid)
+    assert torch.equal(g_rp.cpu(), torch.from_numpy(rp))
+    assert torch.equal(g_ci.cpu(), torch.from_numpy(ci))
+
+
+def test_neighbor_list_edge_cases(e2f, ctx):
+    # strict inequality on the grid, a single atom, isolated atoms
+    pts = np.array([[0, 0, 0], [0, 0, 3.0], [0, 3.0 - 2.0 ** -16, 0], [50, 50, 50]], dtype=np.float32)
+    rp, ci = e2f.e2f_neighbor_list(ctx, gpu(pts), 3.0)
+    orp, oci = o.neighbor_list(pts, 3.0)
+    assert np.array_equal(rp.cpu().numpy(), orp) and np.array_equal(ci.cpu().numpy(), oci)
+    rp, ci = e2f.e2f_neighbor_list(ctx, gpu(pts[:1]), 3.0)
+    assert rp.cpu().tolist() == [0, 0] and ci.numel() == 0
+    with pytest.raises(e2f.E2FError):
+        bad = pts.copy()
+        bad[1, 2] = np.nan
+        e2f.e2f_neighbor_list(ctx, gpu(bad), 3.0)
+
+
+# ------------------------------------------------------------ per-node steps
+def test_solid_harmonics(e2f, ctx):
+    rng = np.random.default_rng(3)
+    pos = syn.quantize(rng.uniform(-20, 20, size=(300, 3)))
+    origins = syn.quantize(rng.uniform(-5, 5, size=(4, 3)))
+    oid = rng.integers(0, 4, size=300).astype(np.int32)
+    for L in [0, 1, 2, 4, 6]:
+        got = e2f.e2f_solid_harmonics(ctx, gpu(pos), L, gpu(origins), gpu(oid)).cpu().numpy()
+        ref = o.solid_harmonics(L, pos.astype(np.float64) - origins[oid].astype(np.float64))
+        for l in range(L + 1):
+            s = slice(l * l, (l + 1) ** 2)
+            assert np.max(np.abs(got[:, s] - ref[:, s])) <= 1e-6 * np.max(np.abs(ref[:, s]))
+
+
+def node_tp_reference(L, pos, feat):
+    """[h^(a) (x) R^(b)(p)]^(d) over the blocks used by the factorised layer
+    (some u <= L-b and o <= L can reach them), ordered (a, b, d, delta)."""
+    tri = lambda a, b, c: abs(a - b) <= c <= a + b
+    R = o.solid_harmonics(L, pos.astype(np.float64))
+    rows = []
+    for a in range(L + 1):
+        for b in range(L + 1):
+            for d in range(abs(a - b), a + b + 1):
+                if not any(tri(a, b + u, oo) and tri(u, d, oo) for u in range(L - b + 1) for oo in range(L + 1)):
+                    continue
+                c = o.cg_real(a, b, d)
+                rows.append(np.einsum("xyz,nxc,ny->nzc", c, feat[:, a * a:(a + 1) ** 2, :].astype(np.float64),
+                                      R[:, b * b:(b + 1) ** 2]))
+    return np.concatenate(rows, axis=1)
+
+
+@pytest.mark.parametrize("L,C", [(2, 16), (3, 64), (4, 128), (6, 8)])
+def test_node_tp(e2f, ctx, L, C):
+    rng = np.random.default_rng(L)
+    pos = syn.quantize(rng.uniform(-6, 6, size=(37, 3)))
+    feat = rng.standard_normal((37, (L + 1) ** 2, C)).astype(np.float32)
+    got = e2f.e2f_node_tp(ctx, gpu(pos), gpu(feat), L).cpu().numpy()
+    ref = node_tp_reference(L, pos, feat)
+    assert got.shape == ref.shape == (37, e2f.e2f_node_tp_dim(L), C)
+    assert np.max(np.abs(got - ref)) <= 1e-5 * np.max(np.abs(ref))
+
+
+# ------------------------------------------------------------ the layer
+@pytest.mark.parametrize("name,rows", [("cluster32_L2", None), ("molecules256x30_L3", 512), ("water2000_L4", 96)])
+def test_conv_parity(e2f, ctx, name, rows):
+    inp, rp, ci, alpha = case(name)
+    wl = inp.workload
+    y6, ye = run_both(e2f, ctx, inp, rp, ci, alpha, wl.lmax, wl.heads, wl.cutoff, mix=inp.mix_w)
+    r = sample_rows(inp.pos.shape[0], rows or inp.pos.shape[0])
+    ref = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, inp.mix_w, rows=r)
+    e6 = o.max_rel_err(y6[r], ref, wl.lmax)
+    ee = o.max_rel_err(ye[r], ref, wl.lmax)
+    print("%s: 6j err %.3e  edge err %.3e" % (name, e6, ee))
+    assert e6 <= TOL_F32 and ee <= TOL_F32
+
+
+def test_conv_parity_protein_fp32_and_bf16(e2f, ctx):
+    inp, rp, ci, alpha = case("protein20k_L4")
+    wl = inp.workload
+    r = sample_rows(inp.pos.shape[0], 48, seed=1)
+    y = o.conv_edge(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, rows=r)
+    ref = o.mix(wl.lmax, y, inp.mix_w)
+    y6, ye = run_both(e2f, ctx, inp, rp, ci, alpha, wl.lmax, wl.heads, wl.cutoff, mix=inp.mix_w)
+    e6, ee = o.max_rel_err(y6[r], ref, wl.lmax), o.max_rel_err(ye[r], ref, wl.lmax)
+    print("protein fp32: 6j err %.3e  edge err %.3e" % (e6, ee))
+    assert e6 <= TOL_F32 and ee <= TOL_F32
+    y6, ye = run_both(e2f, ctx, inp, rp, ci, alpha, wl.lmax, wl.heads, wl.cutoff, mix=inp.mix_w, mix_bf16=True)
+    e6, ee = o.max_rel_err(y6[r], ref, wl.lmax), o.max_rel_err(ye[r], ref, wl.lmax)
+    print("protein bf16 mix: 6j err %.3e  edge err %.3e" % (e6, ee))
+    assert e6 <= TOL_BF16 and ee <= TOL_BF16
+
+
+def test_conv_edge_cases(e2f, ctx):
+    rng = np.random.default_rng(12)
+    # ragged sizes, L = 0, isolated atoms, explicit path weights, no alpha
+    for L, n, C, H in [(0, 13, 4, 1), (1, 29, 12, 3), (3, 57, 8, 2)]:
+        pos = syn.quantize(rng.uniform(0, 9, size=(n, 3)))
+        pos[-1] = [60.0, 60.0, 60.0]  # isolated
+        rp, ci = o.neighbor_list(pos, 4.0)
+        feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+        w = rng.uniform(0.2, 1.0, size=(L + 1) ** 3)
+        ones = np.ones((len(ci), H), dtype=np.float32)
+        ref = o.conv_edge(L, H, pos, feat, rp, ci, ones, w)
+        for fn in (e2f.e2f_wigner6j_conv_forward, e2f.e2f_edge_tp_conv_forward):
+            got = fn(ctx, gpu(pos), gpu(feat), gpu(rp), gpu(ci), None, L, H, 4.0, path_w=w).cpu().numpy()
+            assert o.max_rel_err(got, ref, L) <= TOL_F32
+            assert np.all(got[-1] == 0)
+    # no edges at all
+    pos = np.array([[0, 0, 0], [10, 0, 0]], dtype=np.float32)
+    feat = rng.standard_normal((2, 4, 4)).astype(np.float32)
+    rp = np.zeros(3, dtype=np.int64)
+    ci = np.zeros(0, dtype=np.int32)
+    for fn in (e2f.e2f_wigner6j_conv_forward, e2f.e2f_edge_tp_conv_forward):
+        got = fn(ctx, gpu(pos), gpu(feat), gpu(rp), gpu(ci), None, 1, 1, 4.0).cpu().numpy()
+        assert np.all(got == 0)
+
+
+def test_determinism_and_translation(e2f, ctx):
+    inp, rp, ci, alpha = case("water2000_L4")
+    wl = inp.workload
+    a1, b1 = run_both(e2f, ctx, inp, rp, ci, alpha, wl.lmax, wl.heads, wl.cutoff)
+    a2, b2 = run_both(e2f, ctx, inp, rp, ci, alpha, wl.lmax, wl.heads, wl.cutoff)
+    assert np.array_equal(a1, a2) and np.array_equal(b1, b2)
+    shifted = type(inp)(inp.pos + np.float32(37.5), inp.graph_id, inp.species, inp.feat, inp.mix_w, inp.path_w, wl)
+    a3, b3 = run_both(e2f, ctx, shifted, rp, ci, alpha, wl.lmax, wl.heads, wl.cutoff)
+    assert o.max_rel_err(a3, a1, wl.lmax) <= TOL_F32 and o.max_rel_err(b3, b1, wl.lmax) <= TOL_F32
