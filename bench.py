@@ -1,0 +1,232 @@
+#!/usr/bin/env python3
+"""Benchmark of the Wigner-6j convolution forward on one MI355X.
+
+One step = the whole hot path over one synthetic input already resident in
+HBM: the radius graph (CSR) followed by the Wigner-6j convolution forward
+(tile plan, solid harmonics, j-side node products, CSR attention-weighted
+aggregation, i-side 6j recoupling, per-irrep fp32 channel mixing).
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+
+Prints ONE JSON line.  Besides the step throughput it reports the forward
+alone (atoms/s, edges/s), the per-edge tensor-product baseline on the same
+inputs and GPU, the per-kernel times (HIP events on the launch stream,
+recorded during the timed steps), the roofline of the dominant kernel, the
+fp64 oracle timed on the host cores on a bounded row sample, and the parity
+of the timed output on those rows.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "Wigner-6j conv fwd atoms/s + edges/s at Lmax=4, C=128; speedup vs edge-TP"
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+FP32_VECTOR_PEAK_TFS = 157.3  # MI355X fp32 vector (packed) peak
+
+
+def tri(a, b, c):
+    return abs(a - b) <= c <= a + b
+
+
+def layer_counts(L):
+    """Index-structure counts of the factorised layer (per channel): rows of
+    T, j-side matrix entries, i-side matrix entries, edge filter entries."""
+    blocks = [(a, b, d) for a in range(L + 1) for b in range(L + 1) for d in range(abs(a - b), a + b + 1)
+              if any(tri(a, b + u, o) and tri(u, d, o) for u in range(L - b + 1) for o in range(L + 1))]
+    dimT = sum(2 * d + 1 for a, b, d in blocks)
+    m_slots = sum((2 * d + 1) * (2 * a + 1) for a, b, d in blocks)
+    q_slots = sum((2 * o + 1) * (2 * d + 1) for a, b, d in blocks for o in range(L + 1)
+                  if any(tri(a, b + u, o) and tri(u, d, o) for u in range(L - b + 1)))
+    return dict(dimT=dimT, m_slots=m_slots, q_slots=q_slots, k_slots=(L + 1) ** 4)
+
+
+def file_sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="protein20k_L4")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--cpu-rows", type=int, default=2048)
+    ap.add_argument("--copy-calib", action="store_true", help="also run a 1 GiB device copy (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path (no sharding, no collectives).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import e2f_synth as syn
+    import paper_2501_19216_amd as e2f
+
+    wl = syn.WORKLOADS[args.workload]
+    inp = syn.make_inputs(wl)
+    n, L, C, H = inp.pos.shape[0], wl.lmax, wl.channels, wl.heads
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    ctx = e2f.e2f_create(L, 0)
+    pos = torch.from_numpy(inp.pos).to(dev)
+    feat = torch.from_numpy(inp.feat).to(dev)
+    mix_w = torch.from_numpy(inp.mix_w).to(dev)
+    gid = None if inp.graph_id is None else torch.from_numpy(inp.graph_id).to(dev)
+
+    # the graph once, to size buffers and draw the attention weights
+    row_ptr, col = e2f.e2f_neighbor_list(ctx, pos, wl.cutoff, gid)
+    E = col.numel()
+    rp_h, ci_h = row_ptr.cpu().numpy(), col.cpu().numpy()
+    alpha_h = syn.attention_weights(inp.pos, inp.species, rp_h, ci_h, H, wl.cutoff, wl.species, wl.seed)
+    alpha = torch.from_numpy(alpha_h).to(dev)
+    rp_buf = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    col_buf = torch.empty(E, dtype=torch.int32, device=dev)
+    out = torch.empty_like(feat)
+
+    def step():
+        rp, ci = e2f.e2f_neighbor_list(ctx, pos, wl.cutoff, gid, rp_buf, col_buf)
+        e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, rp, ci, alpha, L, H, wl.cutoff, mix_w=mix_w, graph_id=gid,
+                                      out=out)
+
+    def fwd_only():
+        e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col, alpha, L, H, wl.cutoff, mix_w=mix_w,
+                                      graph_id=gid, out=out)
+
+    out_e = torch.empty_like(feat)
+
+    def edge_only():
+        e2f.e2f_edge_tp_conv_forward(ctx, pos, feat, row_ptr, col, alpha, L, H, wl.cutoff, mix_w=mix_w, out=out_e)
+
+    def nl_only():
+        e2f.e2f_neighbor_list(ctx, pos, wl.cutoff, gid, rp_buf, col_buf)
+
+    def timed(fn, k):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(k):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / k
+
+    for _ in range(args.warmup):
+        step()
+    # ---- the timed steps, with per-kernel event timing on the launch stream
+    e2f.e2f_profile(ctx, True)
+    ms_step = timed(step, args.steps)
+    prof = e2f.e2f_profile_read(ctx)
+    e2f.e2f_profile(ctx, False)
+    print("[bench] %s: %d atoms, %d edges, step %.3f ms" % (wl.name, n, E, ms_step), file=sys.stderr, flush=True)
+    out_step = out.cpu().numpy()
+    # ---- the forward alone, the baseline, the graph alone
+    for _ in range(2):
+        fwd_only(), edge_only()
+    ms_fwd = timed(fwd_only, args.steps)
+    ms_edge = timed(edge_only, args.steps)
+    ms_nl = timed(nl_only, args.steps)
+    pairs, tiles = e2f.e2f_last_plan(ctx)
+    print("[bench] fwd %.3f ms, edge-TP %.3f ms, graph %.3f ms" % (ms_fwd, ms_edge, ms_nl), file=sys.stderr,
+          flush=True)
+
+    kernels = {k: dict(launches=v[0] // args.steps, ms=v[1] / args.steps) for k, v in prof.items()}
+    cnt = layer_counts(L)
+    dimT = cnt["dimT"]
+    # algorithmic bytes / flops per launch of each kernel of the forward
+    alg = {
+        "aggregate": dict(bytes=4.0 * dimT * C * (pairs + n) + 4.0 * E * (1 + H) + 8.0 * (n + 1),
+                          flops=2.0 * E * dimT * C),
+        "node_tp": dict(bytes=4.0 * C * (n * (L + 1) ** 2 + pairs * dimT), flops=2.0 * pairs * cnt["m_slots"] * C),
+        "recouple": dict(bytes=4.0 * C * n * (dimT + (L + 1) ** 2), flops=2.0 * n * cnt["q_slots"] * C),
+        "mix": dict(bytes=8.0 * n * (L + 1) ** 2 * C + 4.0 * (L + 1) * C * C, flops=2.0 * n * (L + 1) ** 2 * C * C),
+    }
+    dom = max((k for k in kernels if k in alg), key=lambda k: kernels[k]["ms"])
+    t_dom = kernels[dom]["ms"] / max(1, kernels[dom]["launches"])
+    ai = alg[dom]["flops"] / alg[dom]["bytes"]
+    ridge = FP32_VECTOR_PEAK_TFS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if ai < ridge:
+        achieved = alg[dom]["bytes"] / (t_dom * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s", frac=achieved / HBM_PEAK_GBS)
+    else:
+        achieved = alg[dom]["flops"] / (t_dom * 1e-3) / 1e12
+        roof = dict(bound="alu", achieved=achieved, peak=FP32_VECTOR_PEAK_TFS, unit="TFLOP/s",
+                    frac=achieved / FP32_VECTOR_PEAK_TFS)
+    roof["kernel"] = dom
+    roof["traffic"] = None
+    tr_path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (dom, wl.name))
+    if os.path.exists(tr_path):
+        tr = json.load(open(tr_path))
+        src = os.path.join(ROOT, "paper_2501_19216_amd", "csrc", "conv.hip")
+        if tr.get("conv_sha256") == file_sha(src):
+            roof["traffic"] = tr["bytes_per_launch"]
+    for k, v in kernels.items():
+        if k in alg:
+            tk = v["ms"] / max(1, v["launches"]) * 1e-3
+            v["alg_GBps"] = alg[k]["bytes"] / tk / 1e9
+            v["alg_TFLOPs"] = alg[k]["flops"] / tk / 1e12
+
+    if args.copy_calib:
+        x = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        y = torch.empty_like(x)
+        y.copy_(x)
+        torch.cuda.synchronize()
+
+    # ---- oracle on the host cores, bounded row sample; parity of the timed output
+    cpu = None
+    parity = None
+    if not args.no_cpu:
+        import oracle
+        orp, oci = oracle.neighbor_list(inp.pos, wl.cutoff, inp.graph_id)
+        graph_equal = bool(np.array_equal(orp, rp_h) and np.array_equal(oci, ci_h))
+        k = min(args.cpu_rows, n)
+        rows = np.linspace(0, n - 1, k).astype(np.int32)
+        cores = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
+        t0 = time.perf_counter()
+        ref = oracle.layer(L, H, inp.pos, inp.feat, orp, oci, alpha_h, inp.path_w, inp.mix_w, rows=rows)
+        dt = time.perf_counter() - t0
+        cpu = dict(value=k / dt, unit="atoms/s", cores=cores, kind="oracle",
+                   sample="%d of %d receiver rows (evenly spaced), fp64 layer definition + mixing, %.1f s" % (k, n, dt))
+        parity = dict(rows=k, max_rel_err=oracle.max_rel_err(out_step[rows], ref, L), graph_bit_exact=graph_equal)
+
+    res = {
+        "metric": METRIC,
+        "value": n / (ms_step * 1e-3),
+        "unit": "atoms/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "atoms": n, "edges": E, "lmax": L, "channels": C, "heads": H,
+                   "cutoff": wl.cutoff, "mix": "fp32", "pairs": pairs, "tiles": tiles,
+                   "step": "radius graph + Wigner-6j conv forward"},
+        "edges_per_s": E / (ms_step * 1e-3),
+        "fwd": {"ms": ms_fwd, "atoms_per_s": n / (ms_fwd * 1e-3), "edges_per_s": E / (ms_fwd * 1e-3)},
+        "edge_tp": {"ms": ms_edge, "atoms_per_s": n / (ms_edge * 1e-3), "edges_per_s": E / (ms_edge * 1e-3)},
+        "speedup_vs_edge_tp": ms_edge / ms_fwd,
+        "neighbor_list_ms": ms_nl,
+        "kernels": kernels,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "parity": parity,
+    }
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

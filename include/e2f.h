@@ -138,6 +138,20 @@ e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* params,
                                     const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,
                                     void* stream);
 
+/* Size of the tile plan of the last e2f_wigner6j_conv_forward on this
+ * context: *pairs = number of (tile, sender) rows of T it computed, *tiles =
+ * number of graph x cell tile keys.  Host outputs. */
+e2f_status e2f_last_plan(const e2f_ctx* ctx, int64_t* pairs /* host */, int64_t* tiles /* host */);
+
+/* Kernel timing.  e2f_profile(ctx, 1) waits for the device, clears the
+ * records and starts bracketing every launch group of this context with HIP
+ * events on its stream (bbox, nl_count, nl_fill, tile_plan, sh, node_tp,
+ * aggregate, recouple, mix, edge_tp); e2f_profile(ctx, 0) stops.  (sync) */
+e2f_status e2f_profile(e2f_ctx* ctx, int enable);
+/* Text "name launches total_ms" per line for the records so far, into buf
+ * (host, `bytes` long, NUL-terminated); E2F_ECAPACITY if too small.  (sync) */
+e2f_status e2f_profile_read(e2f_ctx* ctx, char* buf /* host */, size_t bytes);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,7 +24,7 @@ _STATUS = {0: "E2F_OK", 1: "E2F_EINVAL", 2: "E2F_ECAPACITY", 3: "E2F_ENOMEM", 4:
 # every function declared in include/e2f.h
 EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg",
             "e2f_recoupling_weight", "e2f_neighbor_list", "e2f_solid_harmonics", "e2f_node_tp",
-            "e2f_wigner6j_conv_forward", "e2f_edge_tp_conv_forward"]
+            "e2f_wigner6j_conv_forward", "e2f_edge_tp_conv_forward", "e2f_profile", "e2f_profile_read", "e2f_last_plan"]
 
 
 class E2FError(RuntimeError):
@@ -41,7 +41,7 @@ class ConvParams(ctypes.Structure):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError("libe2f.so is not built; run `python -m paper_2501_19216_amd.build_lib` "
+        raise ImportError("libe2f.so is not built; run `python paper_2501_19216_amd/build_lib.py` "
                           "(or __graft_entry__.build())")
     L = ctypes.CDLL(LIB_PATH)
     i, i32, i64, p, f = ctypes.c_int, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_float
@@ -63,6 +63,12 @@ def _load():
     L.e2f_solid_harmonics.restype = i
     L.e2f_node_tp.argtypes = [p, p, p, p, p, i32, i32, i, p, p]
     L.e2f_node_tp.restype = i
+    L.e2f_last_plan.argtypes = [p, ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    L.e2f_last_plan.restype = i
+    L.e2f_profile.argtypes = [p, i]
+    L.e2f_profile.restype = i
+    L.e2f_profile_read.argtypes = [p, ctypes.c_char_p, ctypes.c_size_t]
+    L.e2f_profile_read.restype = i
     for name in ("e2f_wigner6j_conv_forward", "e2f_edge_tp_conv_forward"):
         fn = getattr(L, name)
         fn.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, i32, p, p, i64, p, p, p]
@@ -143,13 +149,25 @@ def e2f_recoupling_weight(a: int, b: int, u: int, o: int, d: int) -> float:
     return float(lib.e2f_recoupling_weight(a, b, u, o, d))
 
 
-def e2f_neighbor_list(ctx: Context, pos: torch.Tensor, cutoff: float, graph_id: torch.Tensor | None = None):
-    """Radius graph as device CSR (row_ptr int64 [N+1], col_idx int32 [E])."""
+def e2f_neighbor_list(ctx: Context, pos: torch.Tensor, cutoff: float, graph_id: torch.Tensor | None = None,
+                      row_ptr: torch.Tensor | None = None, col_idx: torch.Tensor | None = None):
+    """Radius graph as device CSR (row_ptr int64 [N+1], col_idx int32 [E]).
+
+    With preallocated row_ptr/col_idx large enough, one library call; else a
+    size query first."""
     _dev(pos, torch.float32, "pos")
     _dev(graph_id, torch.int32, "graph_id")
     n = pos.shape[0]
-    row_ptr = torch.empty(n + 1, dtype=torch.int64, device=pos.device)
     E = ctypes.c_int64(0)
+    if row_ptr is not None and col_idx is not None:
+        _dev(row_ptr, torch.int64, "row_ptr")
+        _dev(col_idx, torch.int32, "col_idx")
+        st = _check(lib.e2f_neighbor_list(ctx.handle, _ptr(pos), _ptr(graph_id), n, cutoff, _ptr(row_ptr),
+                                          _ptr(col_idx), col_idx.numel(), ctypes.byref(E), _stream(pos.device)),
+                    "e2f_neighbor_list", allow=(E2F_ECAPACITY,))
+        if st == E2F_OK:
+            return row_ptr, col_idx[:E.value]
+    row_ptr = torch.empty(n + 1, dtype=torch.int64, device=pos.device)
     _check(lib.e2f_neighbor_list(ctx.handle, _ptr(pos), _ptr(graph_id), n, cutoff, _ptr(row_ptr), None, 0,
                                  ctypes.byref(E), _stream(pos.device)), "e2f_neighbor_list", allow=(E2F_ECAPACITY,))
     col = torch.empty(max(E.value, 1), dtype=torch.int32, device=pos.device)
@@ -237,3 +255,26 @@ def e2f_edge_tp_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, head
     """Per-edge SO(3) convolution baseline; same output as the 6j forward."""
     return _conv("e2f_edge_tp_conv_forward", ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w,
                  mix_w, graph_id, tile_side, out)
+
+
+def e2f_profile(ctx: Context, enable: bool) -> None:
+    """Start (clearing earlier records) or stop event timing of every launch group."""
+    _check(lib.e2f_profile(ctx.handle, 1 if enable else 0), "e2f_profile")
+
+
+def e2f_profile_read(ctx: Context) -> dict:
+    """{step name: (launch groups, total ms)} recorded since e2f_profile(ctx, True)."""
+    buf = ctypes.create_string_buffer(1 << 16)
+    _check(lib.e2f_profile_read(ctx.handle, buf, len(buf)), "e2f_profile_read")
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, cnt, ms = line.split()
+        out[name] = (int(cnt), float(ms))
+    return out
+
+
+def e2f_last_plan(ctx: Context) -> tuple:
+    """(pairs, tiles) of the last factorised forward on this context."""
+    P, T = ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(lib.e2f_last_plan(ctx.handle, ctypes.byref(P), ctypes.byref(T)), "e2f_last_plan")
+    return P.value, T.value

@@ -1,6 +1,6 @@
 """Build libe2f.so (HIP for gfx950) in-tree with hipcc.
 
-    python -m paper_2501_19216_amd.build_lib
+    python paper_2501_19216_amd/build_lib.py
 
 Every translation unit is compiled to an object in parallel, then linked.
 Packed fp32 instructions are disabled (-packed-fp32-ops) in device code.

@@ -50,6 +50,15 @@ struct e2f_ctx {
   int64_t* pinned = nullptr;               // host, 16 int64
   std::vector<double> origins_host;
   Buf a, b, c;
+  int64_t last_pairs = 0, last_tiles = 0;  // plan size of the last factorised forward
+  // kernel timing (e2f_profile): events recorded on the launch stream
+  bool prof = false;
+  struct Rec {
+    const char* name;
+    hipEvent_t start, stop;
+  };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
 };
 
 namespace {
@@ -73,6 +82,42 @@ struct DeviceGuard {
   } while (0)
 
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+
+hipEvent_t take_event(e2f_ctx* ctx) {
+  if (!ctx->pool.empty()) {
+    hipEvent_t e = ctx->pool.back();
+    ctx->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Brackets the launches of one named step with events when profiling is on.
+struct Timed {
+  e2f_ctx* ctx;
+  hipStream_t s;
+  e2f_ctx::Rec rec{};
+  Timed(e2f_ctx* c, const char* name, hipStream_t st) : ctx(c), s(st) {
+    if (!ctx->prof) return;
+    rec.name = name;
+    rec.start = take_event(ctx);
+    rec.stop = take_event(ctx);
+    if (rec.start) (void)hipEventRecord(rec.start, s);
+  }
+  ~Timed() {
+    if (!ctx->prof || !rec.start || !rec.stop) return;
+    (void)hipEventRecord(rec.stop, s);
+    ctx->recs.push_back(rec);
+  }
+};
+
+#define E2F_TIMED(name, call)            \
+  do {                                   \
+    Timed tm_(ctx, name, s);             \
+    E2F_HIP(call);                       \
+  } while (0)
 
 e2f_status ensure(e2f_ctx* ctx, Buf& b, size_t bytes, hipStream_t s) {
   if (bytes <= b.n) return E2F_OK;
@@ -247,7 +292,7 @@ struct TilePlan {
 };
 
 e2f_status run_bbox(e2f_ctx* ctx, const float* pos, const int32_t* graph_id, int n, hipStream_t s, int st[kStatsInts]) {
-  E2F_HIP(launch_bbox(pos, graph_id, n, ctx->stats, s));
+  E2F_TIMED("bbox", launch_bbox(pos, graph_id, n, ctx->stats, s));
   E2F_HIP(hipMemcpyAsync(ctx->pinned, ctx->stats, sizeof(int) * kStatsInts, hipMemcpyDeviceToHost, s));
   E2F_HIP(hipStreamSynchronize(s));
   std::memcpy(st, ctx->pinned, sizeof(int) * kStatsInts);
@@ -311,6 +356,11 @@ void e2f_destroy(e2f_ctx* ctx) {
       if (p) (void)hipFree(p);
     for (Buf* b : {&ctx->a, &ctx->b, &ctx->c})
       if (b->p) (void)hipFree(b->p);
+    for (auto& r : ctx->recs) {
+      ctx->pool.push_back(r.start);
+      ctx->pool.push_back(r.stop);
+    }
+    for (hipEvent_t e : ctx->pool) (void)hipEventDestroy(e);
     if (ctx->stats) (void)hipFree(ctx->stats);
     if (ctx->pinned) (void)hipHostFree(ctx->pinned);
   }
@@ -371,7 +421,7 @@ e2f_status e2f_neighbor_list(e2f_ctx* ctx, const float* pos, const int32_t* grap
   }
   rs = ensure(ctx, ctx->a, nl_scratch_bytes(n, cg), s);
   if (rs != E2F_OK) return rs;
-  E2F_HIP(launch_nl_count(pos, graph_id, n, rc * rc, cg, ctx->a.p, row_ptr, s));
+  E2F_TIMED("nl_count", launch_nl_count(pos, graph_id, n, rc * rc, cg, ctx->a.p, row_ptr, s));
   E2F_HIP(hipMemcpyAsync(ctx->pinned, row_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
   E2F_HIP(hipStreamSynchronize(s));
   const int64_t E = ctx->pinned[0];
@@ -385,7 +435,7 @@ e2f_status e2f_neighbor_list(e2f_ctx* ctx, const float* pos, const int32_t* grap
   Carver cv{(char*)ctx->b.p};
   int32_t* unsorted = cv.take<int32_t>((size_t)E);
   void* sort_tmp = cv.take<char>(sort_b);
-  E2F_HIP(launch_nl_fill(pos, graph_id, n, rc * rc, cg, ctx->a.p, row_ptr, unsorted, col_idx, E, sort_tmp, sort_b, s));
+  E2F_TIMED("nl_fill", launch_nl_fill(pos, graph_id, n, rc * rc, cg, ctx->a.p, row_ptr, unsorted, col_idx, E, sort_tmp, sort_b, s));
   return E2F_OK;
 }
 
@@ -474,8 +524,10 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
         }
       }
   const size_t scan_b = scan_tmp_bytes(count);
+  const size_t sort_b = recv_sort_tmp_bytes(n);
   size_t need_a = al256(sizeof(int32_t) * (size_t)n) + 2 * al256(sizeof(int32_t) * (size_t)count) + al256(scan_b) +
-                  al256(sizeof(double) * ctx->origins_host.size());
+                  al256(sizeof(double) * ctx->origins_host.size()) + 2 * al256(sizeof(uint64_t) * (size_t)n) +
+                  2 * al256(sizeof(int32_t) * (size_t)n) + al256(sort_b);
   rs = ensure(ctx, ctx->a, need_a, s);
   if (rs != E2F_OK) return rs;
   Carver ca{(char*)ctx->a.p};
@@ -484,12 +536,20 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   int32_t* pidx = ca.take<int32_t>((size_t)count);
   void* scan_tmp = ca.take<char>(scan_b);
   double* origins = ca.take<double>(ctx->origins_host.size());
+  uint64_t* rkeys = ca.take<uint64_t>(n);
+  uint64_t* rkeys_out = ca.take<uint64_t>(n);
+  int32_t* rvals = ca.take<int32_t>(n);
+  int32_t* order = ca.take<int32_t>(n);
+  void* sort_tmp = ca.take<char>(sort_b);
   E2F_HIP(hipMemcpyAsync(origins, ctx->origins_host.data(), sizeof(double) * ctx->origins_host.size(),
                          hipMemcpyHostToDevice, s));
-  E2F_HIP(launch_tile_keys(pos, graph_id, n, tp.lo, tp.dim, tp.span, tp.ncell, tile_of, s));
+  E2F_TIMED("tile_plan", launch_tile_keys(pos, graph_id, n, tp.lo, tp.dim, tp.span, tp.ncell, tile_of, s));
   E2F_HIP(hipMemsetAsync(flags, 0, sizeof(int32_t) * (size_t)count, s));
-  E2F_HIP(launch_pair_flags(row_ptr, col_idx, tile_of, n, flags, s));
-  E2F_HIP(launch_scan_i32(flags, pidx, count, scan_tmp, scan_b, s));
+  E2F_TIMED("tile_plan", launch_pair_flags(row_ptr, col_idx, tile_of, n, flags, s));
+  // receivers in spatial order (fine cells of 4 A) for L2 reuse in the aggregation
+  E2F_TIMED("tile_plan", launch_sort_receivers(pos, tile_of, n, tp.lo, (int64_t)(4.0 * kGrid), rkeys, rkeys_out,
+                                               rvals, order, sort_tmp, sort_b, s));
+  E2F_TIMED("tile_plan", launch_scan_i32(flags, pidx, count, scan_tmp, scan_b, s));
   E2F_HIP(hipMemcpyAsync(ctx->pinned, pidx + count - 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
   E2F_HIP(hipMemcpyAsync((char*)ctx->pinned + 8, flags + count - 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
   E2F_HIP(hipStreamSynchronize(s));
@@ -497,6 +557,8 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   std::memcpy(&last_idx, ctx->pinned, 4);
   std::memcpy(&last_flag, (char*)ctx->pinned + 8, 4);
   const int64_t P = (int64_t)last_idx + last_flag;
+  ctx->last_pairs = P;
+  ctx->last_tiles = keys;
   // ---- phase 2 buffers
   const bool mixing = p->mix_w != nullptr;
   const size_t tbytes = sizeof(float) * (size_t)P * t.dimT * C;
@@ -515,14 +577,14 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   float* T = cb.take<float>((size_t)P * t.dimT * C);
   float* S = cb.take<float>((size_t)n * t.dimT * C);
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
-  E2F_HIP(launch_pairs(flags, pidx, count, n, pair_node, pair_tile, s));
-  E2F_HIP(launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
-  E2F_HIP(launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, nullptr, s));
-  E2F_HIP(launch_sh(t, pos, nullptr, origins, nullptr, tile_of, tp.ncell, n, Rr, nullptr, s));
-  E2F_HIP(launch_node_tp(t, Rp, pair_node, feat, (int)P, C, T, s));
-  E2F_HIP(launch_aggregate(T, row_ptr, col_pair, alpha, n, t.dimT, C, p->heads, S, s));
-  E2F_HIP(launch_recouple(t, Rr, S, n, C, y, s));
-  if (mixing) E2F_HIP(launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
+  E2F_TIMED("tile_plan", launch_pairs(flags, pidx, count, n, pair_node, pair_tile, s));
+  E2F_TIMED("tile_plan", launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
+  E2F_TIMED("sh", launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, nullptr, s));
+  E2F_TIMED("sh", launch_sh(t, pos, nullptr, origins, nullptr, tile_of, tp.ncell, n, Rr, nullptr, s));
+  E2F_TIMED("node_tp", launch_node_tp(t, Rp, pair_node, feat, (int)P, C, T, s));
+  E2F_TIMED("aggregate", launch_aggregate(T, row_ptr, col_pair, alpha, order, n, t.dimT, C, p->heads, S, s));
+  E2F_TIMED("recouple", launch_recouple(t, Rr, S, n, C, y, s));
+  if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
   return E2F_OK;
 }
 
@@ -550,8 +612,61 @@ e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, cons
     if (rs != E2F_OK) return rs;
     y = (float*)ctx->c.p;
   }
-  E2F_HIP(launch_edge_tp(ctx->dev[L], pos, feat, row_ptr, col_idx, alpha, n, C, p->heads, y, s));
-  if (mixing) E2F_HIP(launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
+  E2F_TIMED("edge_tp", launch_edge_tp(ctx->dev[L], pos, feat, row_ptr, col_idx, alpha, n, C, p->heads, y, s));
+  if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
+  return E2F_OK;
+}
+
+e2f_status e2f_last_plan(const e2f_ctx* ctx, int64_t* pairs, int64_t* tiles) {
+  if (!ctx || !pairs || !tiles) return fail(E2F_EINVAL, "ctx, pairs and tiles are required");
+  *pairs = ctx->last_pairs;
+  *tiles = ctx->last_tiles;
+  return E2F_OK;
+}
+
+e2f_status e2f_profile(e2f_ctx* ctx, int enable) {
+  if (!ctx) return fail(E2F_EINVAL, "ctx is NULL");
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  DeviceGuard g(ctx->device);
+  E2F_HIP(hipDeviceSynchronize());
+  for (auto& r : ctx->recs) {
+    ctx->pool.push_back(r.start);
+    ctx->pool.push_back(r.stop);
+  }
+  ctx->recs.clear();
+  ctx->prof = enable != 0;
+  return E2F_OK;
+}
+
+e2f_status e2f_profile_read(e2f_ctx* ctx, char* buf, size_t bytes) {
+  if (!ctx || !buf || bytes == 0) return fail(E2F_EINVAL, "ctx and buf are required");
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  DeviceGuard g(ctx->device);
+  std::vector<std::string> names;
+  std::vector<double> ms;
+  std::vector<long> cnt;
+  for (auto& r : ctx->recs) {
+    E2F_HIP(hipEventSynchronize(r.stop));
+    float t = 0.0f;
+    E2F_HIP(hipEventElapsedTime(&t, r.start, r.stop));
+    size_t k = 0;
+    while (k < names.size() && names[k] != r.name) ++k;
+    if (k == names.size()) {
+      names.emplace_back(r.name);
+      ms.push_back(0.0);
+      cnt.push_back(0);
+    }
+    ms[k] += t;
+    cnt[k] += 1;
+  }
+  std::string out;
+  char line[128];
+  for (size_t k = 0; k < names.size(); ++k) {
+    snprintf(line, sizeof(line), "%s %ld %.6f\n", names[k].c_str(), cnt[k], ms[k]);
+    out += line;
+  }
+  if (out.size() + 1 > bytes) return fail(E2F_ECAPACITY, "profile text needs %zu bytes", out.size() + 1);
+  std::memcpy(buf, out.c_str(), out.size() + 1);
   return E2F_OK;
 }
 

@@ -161,48 +161,75 @@ __global__ __launch_bounds__(256) void k_node_tp(DevTables t, const double* __re
   }
 }
 
+// ------------------------------------------------------------ receiver order
+// Receivers sorted by (tile, Morton index of a fine spatial cell): groups of
+// consecutive receivers then share most of their senders, so their T rows
+// are reused from L2.
+__device__ __forceinline__ uint32_t spread3(uint32_t v) {
+  v &= 0x3ff;
+  v = (v | (v << 16)) & 0x030000ff;
+  v = (v | (v << 8)) & 0x0300f00f;
+  v = (v | (v << 4)) & 0x030c30c3;
+  v = (v | (v << 2)) & 0x09249249;
+  return v;
+}
+
+__global__ void k_recv_keys(const float* __restrict__ pos, const int32_t* __restrict__ tile_of, int n, int lo0,
+                            int lo1, int lo2, int64_t fine, uint64_t* __restrict__ keys, int32_t* __restrict__ vals) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int lo[3] = {lo0, lo1, lo2};
+  uint32_t m = 0;
+  for (int k = 0; k < 3; ++k) {
+    int64_t c = ((int64_t)__float2int_rn(pos[3 * i + k] * 65536.0f) - lo[k]) / fine;
+    c = c < 0 ? 0 : (c > 1023 ? 1023 : c);
+    m |= spread3((uint32_t)c) << k;
+  }
+  keys[i] = ((uint64_t)(uint32_t)tile_of[i] << 32) | m;
+  vals[i] = i;
+}
+
 // ------------------------------------------------------------ aggregation
 // S[i][q] = sum_{e in row i} alpha[e][head(q)] T[col_pair[e]][q], q over the
-// flattened (row, channel) vector of width W = dimT*C.  One block per
-// (receiver, 4096-float column chunk); float4 loads, four per thread per edge.
-constexpr int kAggThreads = 256;
-constexpr int kAggUnroll = 4;
+// flattened (row, channel) vector of width W = dimT*C, read as float4.
+// A block holds kAggRecv spatially consecutive receivers (one wave each) and
+// one column chunk of 64 float4 (1 KB of every T row it touches).  The flat
+// block id is mapped so that each of the 8 XCDs walks its own contiguous
+// range of receiver groups, chunk by chunk: the groups in flight on one XCD
+// share their senders' chunk in that XCD's L2.
+constexpr int kAggRecv = 4;
+constexpr int kAggChunk4 = 64;
+constexpr int kXcds = 8;
 
-__global__ __launch_bounds__(kAggThreads) void k_aggregate(const float4* __restrict__ T,
-                                                           const int64_t* __restrict__ row_ptr,
-                                                           const int32_t* __restrict__ col_pair,
-                                                           const float* __restrict__ alpha, int W4, int C, int dh,
-                                                           int H, float4* __restrict__ S) {
-  const int i = blockIdx.x;
-  const int base = blockIdx.y * (kAggThreads * kAggUnroll) + threadIdx.x;
-  float4 acc[kAggUnroll];
-  int head[kAggUnroll];
-#pragma unroll
-  for (int u = 0; u < kAggUnroll; ++u) {
-    acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-    head[u] = (((base + u * kAggThreads) * 4) % C) / dh;
-  }
+__global__ __launch_bounds__(64 * kAggRecv) void k_aggregate(const float4* __restrict__ T,
+                                                             const int64_t* __restrict__ row_ptr,
+                                                             const int32_t* __restrict__ col_pair,
+                                                             const float* __restrict__ alpha,
+                                                             const int32_t* __restrict__ order, int n, int W4,
+                                                             int nchunk, int ngroups, int gpx, int C, int dh, int H,
+                                                             float4* __restrict__ S) {
+  const int bid = blockIdx.x;
+  const int xcd = bid % kXcds, local = bid / kXcds;
+  const int group = xcd * gpx + local % gpx;
+  const int chunk = local / gpx;
+  if (group >= ngroups || chunk >= nchunk) return;
+  const int r = group * kAggRecv + (int)(threadIdx.x >> 6);
+  const int q = chunk * kAggChunk4 + (int)(threadIdx.x & 63);
+  if (r >= n || q >= W4) return;
+  const int i = order[r];
+  const int head = ((q * 4) % C) / dh;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+#pragma unroll 4
   for (int64_t e = e0; e < e1; ++e) {
-    const float4* trow = T + (size_t)col_pair[e] * W4;
-#pragma unroll
-    for (int u = 0; u < kAggUnroll; ++u) {
-      const int q = base + u * kAggThreads;
-      if (q < W4) {
-        const float a = alpha ? alpha[e * H + head[u]] : 1.0f;
-        const float4 v = trow[q];
-        acc[u].x += a * v.x;
-        acc[u].y += a * v.y;
-        acc[u].z += a * v.z;
-        acc[u].w += a * v.w;
-      }
-    }
+    const float a = alpha ? alpha[e * H + head] : 1.0f;
+    const float4 v = T[(size_t)col_pair[e] * W4 + q];
+    acc.x += a * v.x;
+    acc.y += a * v.y;
+    acc.z += a * v.z;
+    acc.w += a * v.w;
   }
-#pragma unroll
-  for (int u = 0; u < kAggUnroll; ++u) {
-    const int q = base + u * kAggThreads;
-    if (q < W4) S[(size_t)i * W4 + q] = acc[u];
-  }
+  S[(size_t)i * W4 + q] = acc;
 }
 
 // ------------------------------------------------------------ i-side recouple
@@ -468,13 +495,33 @@ hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* no
   return hipGetLastError();
 }
 
+size_t recv_sort_tmp_bytes(int n) {
+  size_t b = 0;
+  hipcub::DeviceRadixSort::SortPairs(nullptr, b, (const uint64_t*)nullptr, (uint64_t*)nullptr,
+                                     (const int32_t*)nullptr, (int32_t*)nullptr, n);
+  return b;
+}
+
+hipError_t launch_sort_receivers(const float* pos, const int32_t* tile_of, int n, const int* lo, int64_t fine,
+                                 uint64_t* keys, uint64_t* keys_out, int32_t* vals, int32_t* order, void* tmp,
+                                 size_t tmp_bytes, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  k_recv_keys<<<(n + 255) / 256, 256, 0, s>>>(pos, tile_of, n, lo[0], lo[1], lo[2], fine, keys, vals);
+  size_t b = tmp_bytes;
+  return hipcub::DeviceRadixSort::SortPairs(tmp, b, keys, keys_out, vals, order, n, 0, 64, s);
+}
+
 hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_t* col_pair, const float* alpha,
-                            int n, int dimT, int C, int H, float* S, hipStream_t s) {
+                            const int32_t* order, int n, int dimT, int C, int H, float* S, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int64_t W4 = (int64_t)dimT * C / 4;
-  dim3 grid(n, (unsigned)((W4 + kAggThreads * kAggUnroll - 1) / (kAggThreads * kAggUnroll)));
-  k_aggregate<<<grid, kAggThreads, 0, s>>>((const float4*)T, row_ptr, col_pair, alpha, (int)W4, C, C / H, H,
-                                           (float4*)S);
+  const int nchunk = (int)((W4 + kAggChunk4 - 1) / kAggChunk4);
+  const int ngroups = (n + kAggRecv - 1) / kAggRecv;
+  const int gpx = (ngroups + kXcds - 1) / kXcds;
+  const int64_t blocks = (int64_t)kXcds * gpx * nchunk;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  k_aggregate<<<(unsigned)blocks, 64 * kAggRecv, 0, s>>>((const float4*)T, row_ptr, col_pair, alpha, order, n,
+                                                         (int)W4, nchunk, ngroups, gpx, C, C / H, H, (float4*)S);
   return hipGetLastError();
 }
 

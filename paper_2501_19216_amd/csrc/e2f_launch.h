@@ -50,8 +50,13 @@ hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const
 // ---- factorised layer
 hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* node_of, const float* feat,
                           int n_items, int C, float* T, hipStream_t s);
+size_t recv_sort_tmp_bytes(int n);
+// order = receivers sorted by (tile, Morton index of fine cells of side `fine` grid units)
+hipError_t launch_sort_receivers(const float* pos, const int32_t* tile_of, int n, const int* lo, int64_t fine,
+                                 uint64_t* keys, uint64_t* keys_out, int32_t* vals, int32_t* order, void* tmp,
+                                 size_t tmp_bytes, hipStream_t s);
 hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_t* col_pair, const float* alpha,
-                            int n, int dimT, int C, int H, float* S, hipStream_t s);
+                            const int32_t* order, int n, int dimT, int C, int H, float* S, hipStream_t s);
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, int n, int C, float* y,
                            hipStream_t s);
 
