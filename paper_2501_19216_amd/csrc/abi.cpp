@@ -471,7 +471,7 @@ e2f_status e2f_node_tp(e2f_ctx* ctx, const float* pos, const float* origins, con
   if (rs != E2F_OK) return rs;
   double* R = (double*)ctx->c.p;
   E2F_HIP(launch_sh(t, pos, nullptr, nullptr, origins, origin_id, std::numeric_limits<int>::max(), n, R, nullptr, s));
-  E2F_HIP(launch_node_tp(t, R, nullptr, feat, n, channels, out, s));
+  E2F_HIP(launch_node_tp(t, R, nullptr, feat, n, channels, channels, out, s));
   return E2F_OK;
 }
 
@@ -545,17 +545,23 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
                          hipMemcpyHostToDevice, s));
   E2F_TIMED("tile_plan", launch_tile_keys(pos, graph_id, n, tp.lo, tp.dim, tp.span, tp.ncell, tile_of, s));
   E2F_HIP(hipMemsetAsync(flags, 0, sizeof(int32_t) * (size_t)count, s));
-  E2F_TIMED("tile_plan", launch_pair_flags(row_ptr, col_idx, tile_of, n, flags, s));
+  E2F_TIMED("tile_plan", launch_pair_flags(row_ptr, col_idx, tile_of, n, flags, ctx->stats + 8, s));
   // receivers in spatial order (fine cells of 4 A) for L2 reuse in the aggregation
   E2F_TIMED("tile_plan", launch_sort_receivers(pos, tile_of, n, tp.lo, (int64_t)(4.0 * kGrid), rkeys, rkeys_out,
                                                rvals, order, sort_tmp, sort_b, s));
   E2F_TIMED("tile_plan", launch_scan_i32(flags, pidx, count, scan_tmp, scan_b, s));
   E2F_HIP(hipMemcpyAsync(ctx->pinned, pidx + count - 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
   E2F_HIP(hipMemcpyAsync((char*)ctx->pinned + 8, flags + count - 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  E2F_HIP(hipMemcpyAsync((char*)ctx->pinned + 16, ctx->stats + 8, sizeof(int32_t), hipMemcpyDeviceToHost, s));
   E2F_HIP(hipStreamSynchronize(s));
-  int32_t last_idx, last_flag;
+  int32_t last_idx, last_flag, max_degree;
   std::memcpy(&last_idx, ctx->pinned, 4);
   std::memcpy(&last_flag, (char*)ctx->pinned + 8, 4);
+  std::memcpy(&max_degree, (char*)ctx->pinned + 16, 4);
+  // the MFMA aggregation over receiver blocks of 16 needs 16 * degree <= 8192
+  const bool use_blocks = max_degree <= kBlockMaxDegree;
+  const int nblk = (n + 15) / 16;
+  const size_t blk_tmp_b = blocks_tmp_bytes(nblk);
   const int64_t P = (int64_t)last_idx + last_flag;
   ctx->last_pairs = P;
   ctx->last_tiles = keys;
@@ -563,7 +569,11 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   const bool mixing = p->mix_w != nullptr;
   const size_t tbytes = sizeof(float) * (size_t)P * t.dimT * C;
   const size_t sbytes = sizeof(float) * (size_t)n * t.dimT * C;
-  const size_t need_b = 2 * al256(sizeof(int32_t) * (size_t)P) + al256(sizeof(int32_t) * (size_t)n_edges) +
+  // the union has at most as many rows as the block has edges
+  const int64_t edge_of_cap = use_blocks ? 16 * n_edges : 1;
+  const size_t need_b = 2 * al256(sizeof(int32_t) * (size_t)P) + 3 * al256(sizeof(int32_t) * (size_t)n_edges) +
+                        4 * al256(sizeof(int32_t) * (size_t)(nblk + 1)) + al256(blk_tmp_b) +
+                        al256(sizeof(int32_t) * (size_t)edge_of_cap) +
                         al256(sizeof(double) * (size_t)P * nk) + al256(sizeof(double) * (size_t)n * nk) +
                         al256(tbytes) + al256(sbytes) + (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
   rs = ensure(ctx, ctx->b, need_b, s);
@@ -572,6 +582,14 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   int32_t* pair_node = cb.take<int32_t>((size_t)P);
   int32_t* pair_tile = cb.take<int32_t>((size_t)P);
   int32_t* col_pair = cb.take<int32_t>((size_t)n_edges);
+  int32_t* uni = cb.take<int32_t>((size_t)n_edges);
+  int32_t* edge_slot = cb.take<int32_t>((size_t)n_edges);
+  int32_t* blk_count = cb.take<int32_t>((size_t)nblk + 1);
+  int32_t* blk_off = cb.take<int32_t>((size_t)nblk + 1);
+  int32_t* ucount = cb.take<int32_t>((size_t)nblk + 1);
+  int32_t* uoff = cb.take<int32_t>((size_t)nblk + 1);
+  int32_t* edge_of = cb.take<int32_t>((size_t)edge_of_cap);
+  void* blk_tmp = cb.take<char>(blk_tmp_b);
   double* Rp = cb.take<double>((size_t)P * nk);
   double* Rr = cb.take<double>((size_t)n * nk);
   float* T = cb.take<float>((size_t)P * t.dimT * C);
@@ -579,11 +597,15 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
   E2F_TIMED("tile_plan", launch_pairs(flags, pidx, count, n, pair_node, pair_tile, s));
   E2F_TIMED("tile_plan", launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
+  if (use_blocks)
+    E2F_TIMED("tile_plan", launch_block_plan(row_ptr, col_pair, order, n, blk_count, blk_off, uni, ucount, uoff,
+                                             edge_slot, edge_of, edge_of_cap, blk_tmp, blk_tmp_b, s));
   E2F_TIMED("sh", launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, nullptr, s));
   E2F_TIMED("sh", launch_sh(t, pos, nullptr, origins, nullptr, tile_of, tp.ncell, n, Rr, nullptr, s));
-  E2F_TIMED("node_tp", launch_node_tp(t, Rp, pair_node, feat, (int)P, C, T, s));
-  E2F_TIMED("aggregate", launch_aggregate(T, row_ptr, col_pair, alpha, order, n, t.dimT, C, p->heads, S, s));
-  E2F_TIMED("recouple", launch_recouple(t, Rr, S, n, C, y, s));
+  E2F_TIMED("node_tp", launch_node_tp(t, Rp, pair_node, feat, (int)P, C, C / p->heads, T, s));
+  E2F_TIMED("aggregate", launch_aggregate(T, row_ptr, col_pair, alpha, order, uni, blk_off, uoff, ucount, edge_of,
+                                          use_blocks, n, t.dimT, C, p->heads, S, s));
+  E2F_TIMED("recouple", launch_recouple(t, Rr, S, n, C, C / p->heads, y, s));
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
   return E2F_OK;
 }

@@ -85,9 +85,11 @@ __global__ void k_tile_keys(const float* __restrict__ pos, const int32_t* __rest
 }
 
 __global__ void k_pair_flags(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ col,
-                             const int32_t* __restrict__ tile_of, int n, int32_t* __restrict__ flags) {
+                             const int32_t* __restrict__ tile_of, int n, int32_t* __restrict__ flags,
+                             int32_t* __restrict__ max_degree) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
+  atomicMax(max_degree, (int32_t)(row_ptr[i + 1] - row_ptr[i]));
   const int64_t base = (int64_t)tile_of[i] * n;
   for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) flags[base + col[e]] = 1;
 }
@@ -111,13 +113,14 @@ __global__ void k_col_pair(const int64_t* __restrict__ row_ptr, const int32_t* _
 }
 
 // ------------------------------------------------------------ j-side node TP
-// T[item][r][c] = sum_al M[r][al] h_node^(a)[al][c], with the per-node matrix
+// T[item][r][c] = sum_al M[r][al] h_node^(a)[al][c], stored head-major as
+// T[item][c / dh][r][c % dh] (dh = C gives the plain [r][c] layout), with the per-node matrix
 // M[r][al] = sum_be C^{d de}_{a al, b be} R^(b)_be(p) built once per item in
 // float64 and kept in LDS (cost independent of C).
 template <int L>
 __global__ __launch_bounds__(256) void k_node_tp(DevTables t, const double* __restrict__ R,
                                                  const int32_t* __restrict__ node_of, const float* __restrict__ feat,
-                                                 int C, float* __restrict__ T) {
+                                                 int C, int dh, float* __restrict__ T) {
   constexpr int NK = (L + 1) * (L + 1);
   extern __shared__ float smem[];
   __shared__ double Rl[NK];
@@ -154,7 +157,8 @@ __global__ __launch_bounds__(256) void k_node_tp(DevTables t, const double* __re
           float acc = 0.0f;
 #pragma unroll
           for (int al = 0; al < 2 * a + 1; ++al) acc += mrow[al] * hl[(a * a + al) * CB + cl];
-          Tdst[(size_t)r * C + c0 + cl] = acc;
+          const int cc = c0 + cl;
+          Tdst[(size_t)(cc / dh) * t.dimT * dh + (size_t)r * dh + cc % dh] = acc;
         }
       }
     }
@@ -189,25 +193,228 @@ __global__ void k_recv_keys(const float* __restrict__ pos, const int32_t* __rest
   vals[i] = i;
 }
 
+// ------------------------------------------------------------ receiver blocks
+// Receivers are cut into blocks of G consecutive entries of the spatial
+// order.  For each block the plan lists the union U_b of the T rows its
+// edges read (sorted, unique) and, for every edge, the position of its T row
+// in U_b.  Rows are sorted by sender and the pairs of a tile are numbered by
+// ascending sender, so every receiver's edges are in ascending U_b position.
+constexpr int kUnionMax = 8192;  // G * (largest degree) must fit
+
+__global__ void k_block_edges(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ order, int n, int G,
+                              int nblk, int32_t* __restrict__ blk_count) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nblk) return;
+  int64_t c = 0;
+  for (int r = b * G; r < min(n, (b + 1) * G); ++r) c += row_ptr[order[r] + 1] - row_ptr[order[r]];
+  blk_count[b] = (int32_t)c;
+}
+
+__global__ __launch_bounds__(256) void k_block_union(const int64_t* __restrict__ row_ptr,
+                                                     const int32_t* __restrict__ col_pair,
+                                                     const int32_t* __restrict__ order, int n, int G,
+                                                     const int32_t* __restrict__ blk_off,
+                                                     int32_t* __restrict__ uni, int32_t* __restrict__ ucount,
+                                                     int32_t* __restrict__ edge_slot) {
+  extern __shared__ int32_t ush[];
+  int32_t* keys = ush;               // [kUnionMax]
+  int32_t* ukeys = ush + kUnionMax;  // [kUnionMax]
+  __shared__ int32_t off[65];
+  __shared__ int32_t part[256];
+  const int b = blockIdx.x;
+  const int r0 = b * G, nr = min(G, n - r0);
+  if (threadIdx.x == 0) {
+    int32_t o = 0;
+    for (int r = 0; r < nr; ++r) {
+      off[r] = o;
+      const int i = order[r0 + r];
+      o += (int32_t)(row_ptr[i + 1] - row_ptr[i]);
+    }
+    off[nr] = o;
+  }
+  __syncthreads();
+  const int total = off[nr];  // <= kUnionMax, guaranteed by the host's choice of G
+  int p2 = 1;
+  while (p2 < total) p2 <<= 1;
+  for (int r = 0; r < nr; ++r) {
+    const int64_t rs = row_ptr[order[r0 + r]];
+    for (int t = threadIdx.x; t < off[r + 1] - off[r]; t += blockDim.x) keys[off[r] + t] = col_pair[rs + t];
+  }
+  for (int k = total + threadIdx.x; k < p2; k += blockDim.x) keys[k] = 0x7fffffff;
+  __syncthreads();
+  // bitonic sort of keys[0, p2)
+  for (int size = 2; size <= p2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int k = threadIdx.x; k < p2 / 2; k += blockDim.x) {
+        const int lo = 2 * k - (k & (stride - 1));
+        const int hi = lo + stride;
+        const bool up = (lo & size) == 0;
+        const int32_t x = keys[lo], y = keys[hi];
+        if ((x > y) == up) {
+          keys[lo] = y;
+          keys[hi] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // unique: each thread owns a contiguous run of `per` sorted keys
+  const int per = (total + blockDim.x - 1) / blockDim.x;
+  const int k0 = threadIdx.x * per, k1 = min(total, k0 + per);
+  int cnt = 0;
+  for (int k = k0; k < k1; ++k) cnt += (k == 0 || keys[k] != keys[k - 1]);
+  part[threadIdx.x] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t s = 0;
+    for (int t = 0; t < (int)blockDim.x; ++t) {
+      const int32_t v = part[t];
+      part[t] = s;
+      s += v;
+    }
+    ucount[b] = s;
+    off[64] = s;
+  }
+  __syncthreads();
+  int w = part[threadIdx.x];
+  for (int k = k0; k < k1; ++k)
+    if (k == 0 || keys[k] != keys[k - 1]) {
+      ukeys[w] = keys[k];
+      uni[blk_off[b] + w] = keys[k];
+      ++w;
+    }
+  __syncthreads();
+  const int nu = off[64];
+  // position of every edge's T row in the union
+  for (int r = 0; r < nr; ++r) {
+    const int64_t rs = row_ptr[order[r0 + r]];
+    for (int t = threadIdx.x; t < off[r + 1] - off[r]; t += blockDim.x) {
+      const int32_t key = col_pair[rs + t];
+      int lo = 0, hi = nu;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (ukeys[mid] < key) lo = mid + 1;
+        else hi = mid;
+      }
+      edge_slot[rs + t] = lo;
+    }
+  }
+}
+
+// Dense index of a block's edges: edge_of[(uoff[b] + slot) * 16 + r] = edge of
+// receiver r (0..15) of block b whose T row is union entry `slot`, else -1.
+__global__ void k_block_index(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ order, int n,
+                              const int32_t* __restrict__ uoff, const int32_t* __restrict__ edge_slot,
+                              int32_t* __restrict__ edge_of) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= n) return;
+  const int i = order[r];
+  const int64_t base = (int64_t)uoff[r / 16] * 16 + (r % 16);
+  for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) edge_of[base + (int64_t)edge_slot[e] * 16] = (int32_t)e;
+}
+
 // ------------------------------------------------------------ aggregation
-// S[i][q] = sum_{e in row i} alpha[e][head(q)] T[col_pair[e]][q], q over the
-// flattened (row, channel) vector of width W = dimT*C, read as float4.
-// A block holds kAggRecv spatially consecutive receivers (one wave each) and
-// one column chunk of 64 float4 (1 KB of every T row it touches).  The flat
-// block id is mapped so that each of the 8 XCDs walks its own contiguous
-// range of receiver groups, chunk by chunk: the groups in flight on one XCD
-// share their senders' chunk in that XCD's L2.
+// S[i][q] = sum_{e in row i} alpha[e][head(q)] T[col_pair[e]][q].
+//
+// MFMA form.  For a block of 16 spatially consecutive receivers and the union
+// U_b of their T rows, and for one head h:
+//     S_b,h [16 x cols] = A_b,h [16 x |U_b|] . T_{U_b},h [|U_b| x cols],
+// where A_b,h[r][u] is the attention weight of the edge (receiver r, union row
+// u) or 0.  v_mfma_f32_16x16x4f32 takes A as 16 receivers x 4 union rows and
+// B as 4 union rows x 16 columns of head h, so every T element loaded from
+// L2 is used by all 16 receivers inside the matrix core instead of being
+// gathered once per edge.  The columns of head h are enumerated as
+// m = delta*dh + t (t < dh) and cut into groups of 16; T and S are stored
+// head-major ([row][head][delta][t]), so one head's columns are contiguous
+// and a wave's 8 groups read 512 contiguous bytes of each T row.  A wave owns
+// kAggGroups groups of one head of one block and walks U_b four rows at a time.
+// Accumulation order is fixed (deterministic).
+constexpr int kAggGroups = 8;
+constexpr int kXcds = 8;
+constexpr int kPiece = 512;  // union rows staged in LDS at a time
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict__ T, const float* __restrict__ alpha,
+                                                        const int32_t* __restrict__ order,
+                                                        const int32_t* __restrict__ uni,
+                                                        const int32_t* __restrict__ blk_off,
+                                                        const int32_t* __restrict__ uoff,
+                                                        const int32_t* __restrict__ ucount,
+                                                        const int32_t* __restrict__ edge_of, int n, int nblk, int bpx,
+                                                        int ntg, int ntg4, int dimT, int C, int dh, int H,
+                                                        float* __restrict__ S) {
+  __shared__ int32_t ubl[kPiece];
+  __shared__ float Al[kPiece * 16];  // Al[slot][receiver]: A operand of head h
+  const int bid = blockIdx.x;
+  const int xcd = bid % kXcds, local = bid / kXcds;
+  const int b = xcd * bpx + local % bpx;
+  const int wtask = local / bpx;
+  if (b >= nblk || wtask >= H * ntg4) return;  // uniform over the workgroup
+  const int h = wtask / ntg4;
+  const int tg = (wtask % ntg4) * 4 + (int)(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int j = lane & 15, k = lane >> 4;
+  const int64_t W = (int64_t)dimT * C;
+  const int hcols = dimT * dh;
+  int64_t col[kAggGroups];
+#pragma unroll
+  for (int g = 0; g < kAggGroups; ++g) {
+    const int m = (tg * kAggGroups + g) * 16 + j;
+    col[g] = (tg < ntg && m < hcols) ? (int64_t)h * hcols + m : -1;
+  }
+  v4f acc[kAggGroups];
+#pragma unroll
+  for (int g = 0; g < kAggGroups; ++g) acc[g] = (v4f){0.f, 0.f, 0.f, 0.f};
+  const int nu = ucount[b];
+  const int32_t* ub = uni + blk_off[b];
+  const int32_t* eb = edge_of + (int64_t)uoff[b] * 16;
+  for (int p0 = 0; p0 < nu; p0 += kPiece) {
+    const int np = min(nu - p0, kPiece);
+    __syncthreads();
+    for (int t = threadIdx.x; t < np; t += blockDim.x) ubl[t] = ub[p0 + t];
+    for (int t = threadIdx.x; t < np * 16; t += blockDim.x) {
+      const int idx = eb[(int64_t)p0 * 16 + t];
+      Al[t] = idx >= 0 ? (alpha ? alpha[(int64_t)idx * H + h] : 1.0f) : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll 2
+    for (int s0 = 0; s0 < np; s0 += 4) {
+      const int s = s0 + k;
+      const bool valid = s < np;
+      const float a = valid ? Al[s * 16 + j] : 0.0f;
+      const float* trow = T + (int64_t)(valid ? ubl[s] : 0) * W;
+      float bv[kAggGroups];
+#pragma unroll
+      for (int g = 0; g < kAggGroups; ++g) bv[g] = (valid && col[g] >= 0) ? trow[col[g]] : 0.0f;
+#pragma unroll
+      for (int g = 0; g < kAggGroups; ++g) acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[g], acc[g], 0, 0, 0);
+    }
+  }
+  // acc[g][v] = S[receiver 4k+v][column j of group g]
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int r = b * 16 + 4 * k + v;
+    if (r >= n) continue;
+    float* srow = S + (int64_t)order[r] * W;
+#pragma unroll
+    for (int g = 0; g < kAggGroups; ++g)
+      if (col[g] >= 0) srow[col[g]] = acc[g][v];
+  }
+}
+
+// Fallback for receivers with more than 512 neighbours: one wave per
+// receiver and 1 KB column chunk, rows read from L2 (receivers in spatial
+// order, XCD-contiguous mapping).
 constexpr int kAggRecv = 4;
 constexpr int kAggChunk4 = 64;
-constexpr int kXcds = 8;
 
-__global__ __launch_bounds__(64 * kAggRecv) void k_aggregate(const float4* __restrict__ T,
-                                                             const int64_t* __restrict__ row_ptr,
-                                                             const int32_t* __restrict__ col_pair,
-                                                             const float* __restrict__ alpha,
-                                                             const int32_t* __restrict__ order, int n, int W4,
-                                                             int nchunk, int ngroups, int gpx, int C, int dh, int H,
-                                                             float4* __restrict__ S) {
+__global__ __launch_bounds__(64 * kAggRecv) void k_aggregate_rows(const float4* __restrict__ T,
+                                                                  const int64_t* __restrict__ row_ptr,
+                                                                  const int32_t* __restrict__ col_pair,
+                                                                  const float* __restrict__ alpha,
+                                                                  const int32_t* __restrict__ order, int n, int W4,
+                                                                  int nchunk, int ngroups, int gpx, int C, int dh,
+                                                                  int H, float4* __restrict__ S) {
   const int bid = blockIdx.x;
   const int xcd = bid % kXcds, local = bid / kXcds;
   const int group = xcd * gpx + local % gpx;
@@ -217,7 +424,7 @@ __global__ __launch_bounds__(64 * kAggRecv) void k_aggregate(const float4* __res
   const int q = chunk * kAggChunk4 + (int)(threadIdx.x & 63);
   if (r >= n || q >= W4) return;
   const int i = order[r];
-  const int head = ((q * 4) % C) / dh;
+  const int head = (int)(((int64_t)q * 4) / ((int64_t)W4 * 4 / H));  // head-major rows
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
 #pragma unroll 4
@@ -238,7 +445,7 @@ __global__ __launch_bounds__(64 * kAggRecv) void k_aggregate(const float4* __res
 // built in float64 per receiver and kept in LDS, one output degree at a time.
 template <int L, int O>
 __device__ __forceinline__ void recouple_one(const DevTables& t, const double* Rl, float* Ql, const float* Si,
-                                             int C, float* yi) {
+                                             int C, int dh, float* yi) {
   constexpr int NM = 2 * O + 1;
   const int ncol = t.q_ncol[O], s0 = t.q_slotoff[O];
   __syncthreads();
@@ -254,7 +461,7 @@ __device__ __forceinline__ void recouple_one(const DevTables& t, const double* R
 #pragma unroll
     for (int m = 0; m < NM; ++m) acc[m] = 0.0f;
     for (int col = 0; col < ncol; ++col) {
-      const float s = Si[(size_t)cols[col] * C + c];
+      const float s = Si[(size_t)(c / dh) * t.dimT * dh + (size_t)cols[col] * dh + c % dh];
 #pragma unroll
       for (int m = 0; m < NM; ++m) acc[m] += Ql[m * ncol + col] * s;
     }
@@ -265,19 +472,19 @@ __device__ __forceinline__ void recouple_one(const DevTables& t, const double* R
 
 template <int L, int... Os>
 __device__ __forceinline__ void recouple_all(std::integer_sequence<int, Os...>, const DevTables& t, const double* Rl,
-                                             float* Ql, const float* Si, int C, float* yi) {
-  (recouple_one<L, Os>(t, Rl, Ql, Si, C, yi), ...);
+                                             float* Ql, const float* Si, int C, int dh, float* yi) {
+  (recouple_one<L, Os>(t, Rl, Ql, Si, C, dh, yi), ...);
 }
 
 template <int L>
 __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __restrict__ R,
-                                                  const float* __restrict__ S, int C, float* __restrict__ y) {
+                                                  const float* __restrict__ S, int C, int dh, float* __restrict__ y) {
   constexpr int NK = (L + 1) * (L + 1);
   extern __shared__ float Ql[];
   __shared__ double Rl[NK];
   const int i = blockIdx.x;
   if (threadIdx.x < NK) Rl[threadIdx.x] = R[(size_t)i * NK + threadIdx.x];
-  recouple_all<L>(std::make_integer_sequence<int, L + 1>{}, t, Rl, Ql, S + (size_t)i * t.dimT * C, C,
+  recouple_all<L>(std::make_integer_sequence<int, L + 1>{}, t, Rl, Ql, S + (size_t)i * t.dimT * C, C, dh,
                   y + (size_t)i * NK * C);
 }
 
@@ -416,7 +623,7 @@ __global__ __launch_bounds__(128) void k_edge_tp(DevTables t, const float* __res
 // has 160 KB per CU).
 template <typename K>
 hipError_t allow_lds(K kernel, size_t bytes) {
-  if (bytes <= 65536) return hipSuccess;
+  if (bytes <= 32768) return hipSuccess;
   return hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
@@ -447,8 +654,10 @@ hipError_t launch_tile_keys(const float* pos, const int32_t* graph_id, int n, co
 }
 
 hipError_t launch_pair_flags(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of, int n,
-                             int32_t* flags, hipStream_t s) {
-  if (n > 0) k_pair_flags<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, col_idx, tile_of, n, flags);
+                             int32_t* flags, int32_t* max_degree, hipStream_t s) {
+  hipError_t e = hipMemsetAsync(max_degree, 0, sizeof(int32_t), s);
+  if (e != hipSuccess) return e;
+  if (n > 0) k_pair_flags<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, col_idx, tile_of, n, flags, max_degree);
   return hipGetLastError();
 }
 
@@ -478,7 +687,7 @@ hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const
 }
 
 hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* node_of, const float* feat,
-                          int n_items, int C, float* T, hipStream_t s) {
+                          int n_items, int C, int dh, float* T, hipStream_t s) {
   if (n_items == 0) return hipSuccess;
   const int CB = C < 256 ? C : 256;
   const size_t lds = sizeof(float) * ((size_t)t.m_slots + (size_t)t.nk * CB);
@@ -486,7 +695,7 @@ hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* no
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
     if (hipError_t e = allow_lds(k_node_tp<LL>, lds); e != hipSuccess) return e;                            \
-    k_node_tp<LL><<<n_items, 256, lds, s>>>(t, R, node_of, feat, C, T);                                     \
+    k_node_tp<LL><<<n_items, 256, lds, s>>>(t, R, node_of, feat, C, dh, T);                                     \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
 #undef E2F_CASE
@@ -511,21 +720,65 @@ hipError_t launch_sort_receivers(const float* pos, const int32_t* tile_of, int n
   return hipcub::DeviceRadixSort::SortPairs(tmp, b, keys, keys_out, vals, order, n, 0, 64, s);
 }
 
-hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_t* col_pair, const float* alpha,
-                            const int32_t* order, int n, int dimT, int C, int H, float* S, hipStream_t s) {
+size_t blocks_tmp_bytes(int nblk) {
+  size_t b = 0;
+  hipcub::DeviceScan::ExclusiveSum(nullptr, b, (const int32_t*)nullptr, (int32_t*)nullptr, nblk + 1);
+  return b;
+}
+
+hipError_t launch_block_plan(const int64_t* row_ptr, const int32_t* col_pair, const int32_t* order, int n,
+                             int32_t* blk_count, int32_t* blk_off, int32_t* uni, int32_t* ucount, int32_t* uoff,
+                             int32_t* edge_slot, int32_t* edge_of, int64_t edge_of_cap, void* tmp, size_t tmp_bytes,
+                             hipStream_t s) {
   if (n == 0) return hipSuccess;
+  const int G = 16;
+  const int nblk = (n + G - 1) / G;
+  hipError_t e = hipMemsetAsync(blk_count + nblk, 0, sizeof(int32_t), s);
+  if (e != hipSuccess) return e;
+  if ((e = hipMemsetAsync(ucount + nblk, 0, sizeof(int32_t), s)) != hipSuccess) return e;
+  k_block_edges<<<(nblk + 255) / 256, 256, 0, s>>>(row_ptr, order, n, G, nblk, blk_count);
+  size_t b = tmp_bytes;
+  if ((e = hipcub::DeviceScan::ExclusiveSum(tmp, b, blk_count, blk_off, nblk + 1, s)) != hipSuccess) return e;
+  const size_t lds = 2 * sizeof(int32_t) * kUnionMax;
+  if ((e = allow_lds(k_block_union, lds)) != hipSuccess) return e;
+  k_block_union<<<nblk, 256, lds, s>>>(row_ptr, col_pair, order, n, G, blk_off, uni, ucount, edge_slot);
+  b = tmp_bytes;
+  if ((e = hipcub::DeviceScan::ExclusiveSum(tmp, b, ucount, uoff, nblk + 1, s)) != hipSuccess) return e;
+  // edge_of holds at most E*16 entries (every union row belongs to an edge)
+  if ((e = hipMemsetAsync(edge_of, 0xff, sizeof(int32_t) * (size_t)edge_of_cap, s)) != hipSuccess) return e;
+  k_block_index<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, order, n, uoff, edge_slot, edge_of);
+  return hipGetLastError();
+}
+
+hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_t* col_pair, const float* alpha,
+                            const int32_t* order, const int32_t* uni, const int32_t* blk_off, const int32_t* uoff,
+                            const int32_t* ucount, const int32_t* edge_of, bool use_blocks, int n, int dimT, int C,
+                            int H, float* S, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int dh = C / H;
+  if (use_blocks) {
+    const int nblk = (n + 15) / 16;
+    const int ntg = (dimT * dh + 16 * kAggGroups - 1) / (16 * kAggGroups);
+    const int ntg4 = (ntg + 3) / 4;
+    const int bpx = (nblk + kXcds - 1) / kXcds;
+    const int64_t blocks = (int64_t)kXcds * bpx * H * ntg4;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    k_aggregate_mfma<<<(unsigned)blocks, 256, 0, s>>>(T, alpha, order, uni, blk_off, uoff, ucount, edge_of, n, nblk,
+                                                      bpx, ntg, ntg4, dimT, C, dh, H, S);
+    return hipGetLastError();
+  }
   const int64_t W4 = (int64_t)dimT * C / 4;
   const int nchunk = (int)((W4 + kAggChunk4 - 1) / kAggChunk4);
   const int ngroups = (n + kAggRecv - 1) / kAggRecv;
   const int gpx = (ngroups + kXcds - 1) / kXcds;
   const int64_t blocks = (int64_t)kXcds * gpx * nchunk;
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  k_aggregate<<<(unsigned)blocks, 64 * kAggRecv, 0, s>>>((const float4*)T, row_ptr, col_pair, alpha, order, n,
-                                                         (int)W4, nchunk, ngroups, gpx, C, C / H, H, (float4*)S);
+  k_aggregate_rows<<<(unsigned)blocks, 64 * kAggRecv, 0, s>>>((const float4*)T, row_ptr, col_pair, alpha, order, n,
+                                                              (int)W4, nchunk, ngroups, gpx, C, dh, H, (float4*)S);
   return hipGetLastError();
 }
 
-hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, int n, int C, float* y,
+hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, int n, int C, int dh, float* y,
                            hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int threads = C <= 64 ? 64 : (C <= 128 ? 128 : 256);
@@ -534,7 +787,7 @@ hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, 
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
     if (hipError_t e = allow_lds(k_recouple<LL>, lds); e != hipSuccess) return e;                           \
-    k_recouple<LL><<<n, threads, lds, s>>>(t, R, S, C, y);                                                  \
+    k_recouple<LL><<<n, threads, lds, s>>>(t, R, S, C, dh, y);                                                  \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
 #undef E2F_CASE

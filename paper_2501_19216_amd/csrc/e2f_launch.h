@@ -39,7 +39,7 @@ hipError_t launch_sh(const DevTables& t, const float* pos, const int32_t* node_o
 hipError_t launch_tile_keys(const float* pos, const int32_t* graph_id, int n, const int* lo, const int* dim,
                             const int64_t* span, int ncell, int32_t* tile_of, hipStream_t s);
 hipError_t launch_pair_flags(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of, int n,
-                             int32_t* flags, hipStream_t s);
+                             int32_t* flags, int32_t* max_degree, hipStream_t s);
 size_t scan_tmp_bytes(int64_t count);
 hipError_t launch_scan_i32(const int32_t* in, int32_t* out, int64_t count, void* tmp, size_t tmp_bytes, hipStream_t s);
 hipError_t launch_pairs(const int32_t* flags, const int32_t* pidx, int64_t count, int n, int32_t* pair_node,
@@ -48,16 +48,33 @@ hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const
                            const int32_t* pidx, int n, int32_t* col_pair, hipStream_t s);
 
 // ---- factorised layer
+// T stored head-major: T[item][c / dh][row][c % dh] (dh = C: plain [row][c])
 hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* node_of, const float* feat,
-                          int n_items, int C, float* T, hipStream_t s);
+                          int n_items, int C, int dh, float* T, hipStream_t s);
 size_t recv_sort_tmp_bytes(int n);
 // order = receivers sorted by (tile, Morton index of fine cells of side `fine` grid units)
 hipError_t launch_sort_receivers(const float* pos, const int32_t* tile_of, int n, const int* lo, int64_t fine,
                                  uint64_t* keys, uint64_t* keys_out, int32_t* vals, int32_t* order, void* tmp,
                                  size_t tmp_bytes, hipStream_t s);
+// Receiver blocks of 16 consecutive entries of `order`: block edge counts
+// (blk_count [nblk+1]) and offsets (blk_off [nblk+1]), the sorted union of the
+// T rows each block reads (uni [E], block b at blk_off[b]), union sizes
+// (ucount [nblk+1]) and offsets (uoff [nblk+1]), the union position of every
+// edge (edge_slot [E]) and the dense edge index edge_of [edge_of_cap >= 16*E].
+// Requires 16 * (largest degree) <= 8192.
+constexpr int kBlockMaxDegree = 512;
+size_t blocks_tmp_bytes(int nblk);
+hipError_t launch_block_plan(const int64_t* row_ptr, const int32_t* col_pair, const int32_t* order, int n,
+                             int32_t* blk_count, int32_t* blk_off, int32_t* uni, int32_t* ucount, int32_t* uoff,
+                             int32_t* edge_slot, int32_t* edge_of, int64_t edge_of_cap, void* tmp, size_t tmp_bytes,
+                             hipStream_t s);
+// use_blocks: MFMA form over the block plan; else per-receiver rows from L2.
 hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_t* col_pair, const float* alpha,
-                            const int32_t* order, int n, int dimT, int C, int H, float* S, hipStream_t s);
-hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, int n, int C, float* y,
+                            const int32_t* order, const int32_t* uni, const int32_t* blk_off, const int32_t* uoff,
+                            const int32_t* ucount, const int32_t* edge_of, bool use_blocks, int n, int dimT, int C,
+                            int H, float* S, hipStream_t s);
+// S read head-major like T
+hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, int n, int C, int dh, float* y,
                            hipStream_t s);
 
 // ---- per-irrep channel mixing and the edge baseline
