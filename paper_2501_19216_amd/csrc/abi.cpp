@@ -569,11 +569,8 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   const bool mixing = p->mix_w != nullptr;
   const size_t tbytes = sizeof(float) * (size_t)P * t.dimT * C;
   const size_t sbytes = sizeof(float) * (size_t)n * t.dimT * C;
-  // the union has at most as many rows as the block has edges
-  const int64_t edge_of_cap = use_blocks ? 16 * n_edges : 1;
   const size_t need_b = 2 * al256(sizeof(int32_t) * (size_t)P) + 3 * al256(sizeof(int32_t) * (size_t)n_edges) +
                         4 * al256(sizeof(int32_t) * (size_t)(nblk + 1)) + al256(blk_tmp_b) +
-                        al256(sizeof(int32_t) * (size_t)edge_of_cap) +
                         al256(sizeof(double) * (size_t)P * nk) + al256(sizeof(double) * (size_t)n * nk) +
                         al256(tbytes) + al256(sbytes) + (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
   rs = ensure(ctx, ctx->b, need_b, s);
@@ -588,7 +585,6 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   int32_t* blk_off = cb.take<int32_t>((size_t)nblk + 1);
   int32_t* ucount = cb.take<int32_t>((size_t)nblk + 1);
   int32_t* uoff = cb.take<int32_t>((size_t)nblk + 1);
-  int32_t* edge_of = cb.take<int32_t>((size_t)edge_of_cap);
   void* blk_tmp = cb.take<char>(blk_tmp_b);
   double* Rp = cb.take<double>((size_t)P * nk);
   double* Rr = cb.take<double>((size_t)n * nk);
@@ -597,13 +593,24 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
   E2F_TIMED("tile_plan", launch_pairs(flags, pidx, count, n, pair_node, pair_tile, s));
   E2F_TIMED("tile_plan", launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
-  if (use_blocks)
-    E2F_TIMED("tile_plan", launch_block_plan(row_ptr, col_pair, order, n, blk_count, blk_off, uni, ucount, uoff,
-                                             edge_slot, edge_of, edge_of_cap, blk_tmp, blk_tmp_b, s));
+  float* alpha_blk = nullptr;
+  if (use_blocks) {
+    E2F_TIMED("tile_plan", launch_block_union(row_ptr, col_pair, order, n, blk_count, blk_off, uni, ucount, uoff,
+                                              edge_slot, blk_tmp, blk_tmp_b, s));
+    E2F_HIP(hipMemcpyAsync(ctx->pinned, uoff + nblk, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    E2F_HIP(hipStreamSynchronize(s));
+    int32_t union_rows;
+    std::memcpy(&union_rows, ctx->pinned, 4);
+    rs = ensure(ctx, ctx->c, sizeof(float) * (size_t)union_rows * p->heads * 16 + 256, s);
+    if (rs != E2F_OK) return rs;
+    alpha_blk = (float*)ctx->c.p;
+    E2F_TIMED("tile_plan", launch_block_alpha(row_ptr, order, n, uoff, edge_slot, alpha, p->heads, union_rows,
+                                              alpha_blk, s));
+  }
   E2F_TIMED("sh", launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, nullptr, s));
   E2F_TIMED("sh", launch_sh(t, pos, nullptr, origins, nullptr, tile_of, tp.ncell, n, Rr, nullptr, s));
   E2F_TIMED("node_tp", launch_node_tp(t, Rp, pair_node, feat, (int)P, C, C / p->heads, T, s));
-  E2F_TIMED("aggregate", launch_aggregate(T, row_ptr, col_pair, alpha, order, uni, blk_off, uoff, ucount, edge_of,
+  E2F_TIMED("aggregate", launch_aggregate(T, row_ptr, col_pair, alpha, order, uni, blk_off, uoff, ucount, alpha_blk,
                                           use_blocks, n, t.dimT, C, p->heads, S, s));
   E2F_TIMED("recouple", launch_recouple(t, Rr, S, n, C, C / p->heads, y, s));
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));

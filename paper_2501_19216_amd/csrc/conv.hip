@@ -14,6 +14,8 @@
 #include <hip/hip_bf16.h>
 #include <hipcub/hipcub.hpp>
 
+#include <cstdio>
+#include <cstdlib>
 #include <utility>
 
 #include "e2f_launch.h"
@@ -301,16 +303,21 @@ __global__ __launch_bounds__(256) void k_block_union(const int64_t* __restrict__
   }
 }
 
-// Dense index of a block's edges: edge_of[(uoff[b] + slot) * 16 + r] = edge of
-// receiver r (0..15) of block b whose T row is union entry `slot`, else -1.
-__global__ void k_block_index(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ order, int n,
+// Dense A operand of the block aggregation:
+//   alpha_blk[((uoff[b] + slot) * H + h) * 16 + r] = alpha[e][h]
+// for the edge e of receiver r (0..15) of block b whose T row is union entry
+// `slot`; entries without an edge stay 0 (the buffer is cleared first).
+__global__ void k_block_alpha(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ order, int n,
                               const int32_t* __restrict__ uoff, const int32_t* __restrict__ edge_slot,
-                              int32_t* __restrict__ edge_of) {
+                              const float* __restrict__ alpha, int H, float* __restrict__ alpha_blk) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= n) return;
   const int i = order[r];
-  const int64_t base = (int64_t)uoff[r / 16] * 16 + (r % 16);
-  for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) edge_of[base + (int64_t)edge_slot[e] * 16] = (int32_t)e;
+  const int64_t base = (int64_t)uoff[r / 16] * H * 16 + (r % 16);
+  for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+    const int64_t at = base + (int64_t)edge_slot[e] * H * 16;
+    for (int h = 0; h < H; ++h) alpha_blk[at + h * 16] = alpha ? alpha[e * H + h] : 1.0f;
+  }
 }
 
 // ------------------------------------------------------------ aggregation
@@ -329,18 +336,18 @@ __global__ void k_block_index(const int64_t* __restrict__ row_ptr, const int32_t
 // and a wave's 8 groups read 512 contiguous bytes of each T row.  A wave owns
 // kAggGroups groups of one head of one block and walks U_b four rows at a time.
 // Accumulation order is fixed (deterministic).
-constexpr int kAggGroups = 8;
 constexpr int kXcds = 8;
 constexpr int kPiece = 512;  // union rows staged in LDS at a time
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict__ T, const float* __restrict__ alpha,
+template <int NQ, int UNROLL>
+__global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict__ T,
                                                         const int32_t* __restrict__ order,
                                                         const int32_t* __restrict__ uni,
                                                         const int32_t* __restrict__ blk_off,
                                                         const int32_t* __restrict__ uoff,
                                                         const int32_t* __restrict__ ucount,
-                                                        const int32_t* __restrict__ edge_of, int n, int nblk, int bpx,
+                                                        const float* __restrict__ alpha_blk, int n, int nblk, int bpx,
                                                         int ntg, int ntg4, int dimT, int C, int dh, int H,
                                                         float* __restrict__ S) {
   __shared__ int32_t ubl[kPiece];
@@ -356,49 +363,57 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
   const int j = lane & 15, k = lane >> 4;
   const int64_t W = (int64_t)dimT * C;
   const int hcols = dimT * dh;
-  int64_t col[kAggGroups];
+  // MFMA group g = 4q + u reads column m = (tg*NQ + q)*64 + 4j + u of head h,
+  // so lane j loads the float4 at 4j covering its four groups.
+  constexpr int kAggGroups = 4 * NQ;
+  int64_t col4[NQ];
 #pragma unroll
-  for (int g = 0; g < kAggGroups; ++g) {
-    const int m = (tg * kAggGroups + g) * 16 + j;
-    col[g] = (tg < ntg && m < hcols) ? (int64_t)h * hcols + m : -1;
+  for (int q = 0; q < NQ; ++q) {
+    const int m0 = (tg * NQ + q) * 64 + 4 * j;
+    col4[q] = (tg < ntg && m0 < hcols) ? (int64_t)h * hcols + m0 : -1;
   }
   v4f acc[kAggGroups];
 #pragma unroll
   for (int g = 0; g < kAggGroups; ++g) acc[g] = (v4f){0.f, 0.f, 0.f, 0.f};
   const int nu = ucount[b];
   const int32_t* ub = uni + blk_off[b];
-  const int32_t* eb = edge_of + (int64_t)uoff[b] * 16;
+  const float* ab = alpha_blk + ((int64_t)uoff[b] * H + h) * 16;
   for (int p0 = 0; p0 < nu; p0 += kPiece) {
     const int np = min(nu - p0, kPiece);
     __syncthreads();
     for (int t = threadIdx.x; t < np; t += blockDim.x) ubl[t] = ub[p0 + t];
-    for (int t = threadIdx.x; t < np * 16; t += blockDim.x) {
-      const int idx = eb[(int64_t)p0 * 16 + t];
-      Al[t] = idx >= 0 ? (alpha ? alpha[(int64_t)idx * H + h] : 1.0f) : 0.0f;
-    }
+    for (int t = threadIdx.x; t < np * 16; t += blockDim.x)
+      Al[t] = ab[((int64_t)(p0 + t / 16) * H) * 16 + (t % 16)];
     __syncthreads();
-#pragma unroll 2
+#pragma unroll UNROLL
     for (int s0 = 0; s0 < np; s0 += 4) {
       const int s = s0 + k;
       const bool valid = s < np;
       const float a = valid ? Al[s * 16 + j] : 0.0f;
-      const float* trow = T + (int64_t)(valid ? ubl[s] : 0) * W;
-      float bv[kAggGroups];
+      const float4* trow = (const float4*)(T + (int64_t)(valid ? ubl[s] : 0) * W);
+      float4 bv[NQ];
 #pragma unroll
-      for (int g = 0; g < kAggGroups; ++g) bv[g] = (valid && col[g] >= 0) ? trow[col[g]] : 0.0f;
+      for (int q = 0; q < NQ; ++q)
+        bv[q] = (valid && col4[q] >= 0) ? trow[col4[q] / 4] : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-      for (int g = 0; g < kAggGroups; ++g) acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[g], acc[g], 0, 0, 0);
+      for (int q = 0; q < NQ; ++q) {
+        acc[4 * q + 0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].x, acc[4 * q + 0], 0, 0, 0);
+        acc[4 * q + 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].y, acc[4 * q + 1], 0, 0, 0);
+        acc[4 * q + 2] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].z, acc[4 * q + 2], 0, 0, 0);
+        acc[4 * q + 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].w, acc[4 * q + 3], 0, 0, 0);
+      }
     }
   }
-  // acc[g][v] = S[receiver 4k+v][column j of group g]
+  // acc[4q+u][v] = S[receiver 4k+v][column (tg*NQ+q)*64 + 4j + u]
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const int r = b * 16 + 4 * k + v;
     if (r >= n) continue;
-    float* srow = S + (int64_t)order[r] * W;
+    float4* srow = (float4*)(S + (int64_t)order[r] * W);
 #pragma unroll
-    for (int g = 0; g < kAggGroups; ++g)
-      if (col[g] >= 0) srow[col[g]] = acc[g][v];
+    for (int q = 0; q < NQ; ++q)
+      if (col4[q] >= 0)
+        srow[col4[q] / 4] = make_float4(acc[4 * q][v], acc[4 * q + 1][v], acc[4 * q + 2][v], acc[4 * q + 3][v]);
   }
 }
 
@@ -726,10 +741,9 @@ size_t blocks_tmp_bytes(int nblk) {
   return b;
 }
 
-hipError_t launch_block_plan(const int64_t* row_ptr, const int32_t* col_pair, const int32_t* order, int n,
-                             int32_t* blk_count, int32_t* blk_off, int32_t* uni, int32_t* ucount, int32_t* uoff,
-                             int32_t* edge_slot, int32_t* edge_of, int64_t edge_of_cap, void* tmp, size_t tmp_bytes,
-                             hipStream_t s) {
+hipError_t launch_block_union(const int64_t* row_ptr, const int32_t* col_pair, const int32_t* order, int n,
+                              int32_t* blk_count, int32_t* blk_off, int32_t* uni, int32_t* ucount, int32_t* uoff,
+                              int32_t* edge_slot, void* tmp, size_t tmp_bytes, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int G = 16;
   const int nblk = (n + G - 1) / G;
@@ -744,28 +758,44 @@ hipError_t launch_block_plan(const int64_t* row_ptr, const int32_t* col_pair, co
   k_block_union<<<nblk, 256, lds, s>>>(row_ptr, col_pair, order, n, G, blk_off, uni, ucount, edge_slot);
   b = tmp_bytes;
   if ((e = hipcub::DeviceScan::ExclusiveSum(tmp, b, ucount, uoff, nblk + 1, s)) != hipSuccess) return e;
-  // edge_of holds at most E*16 entries (every union row belongs to an edge)
-  if ((e = hipMemsetAsync(edge_of, 0xff, sizeof(int32_t) * (size_t)edge_of_cap, s)) != hipSuccess) return e;
-  k_block_index<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, order, n, uoff, edge_slot, edge_of);
+  return hipGetLastError();
+}
+
+hipError_t launch_block_alpha(const int64_t* row_ptr, const int32_t* order, int n, const int32_t* uoff,
+                              const int32_t* edge_slot, const float* alpha, int H, int64_t union_rows,
+                              float* alpha_blk, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipError_t e = hipMemsetAsync(alpha_blk, 0, sizeof(float) * (size_t)union_rows * H * 16, s);
+  if (e != hipSuccess) return e;
+  k_block_alpha<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, order, n, uoff, edge_slot, alpha, H, alpha_blk);
   return hipGetLastError();
 }
 
 hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_t* col_pair, const float* alpha,
                             const int32_t* order, const int32_t* uni, const int32_t* blk_off, const int32_t* uoff,
-                            const int32_t* ucount, const int32_t* edge_of, bool use_blocks, int n, int dimT, int C,
+                            const int32_t* ucount, const float* alpha_blk, bool use_blocks, int n, int dimT, int C,
                             int H, float* S, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int dh = C / H;
   if (use_blocks) {
+    // columns per wave (64*NQ) and slot-loop unroll; E2F_AGG_CFG="NQ,UNROLL" overrides (tuning)
+    int nq = 6, un = 1;
+    if (const char* cfg = getenv("E2F_AGG_CFG")) sscanf(cfg, "%d,%d", &nq, &un);
     const int nblk = (n + 15) / 16;
-    const int ntg = (dimT * dh + 16 * kAggGroups - 1) / (16 * kAggGroups);
+    const int ntg = (dimT * dh + 64 * nq - 1) / (64 * nq);
     const int ntg4 = (ntg + 3) / 4;
     const int bpx = (nblk + kXcds - 1) / kXcds;
     const int64_t blocks = (int64_t)kXcds * bpx * H * ntg4;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    k_aggregate_mfma<<<(unsigned)blocks, 256, 0, s>>>(T, alpha, order, uni, blk_off, uoff, ucount, edge_of, n, nblk,
-                                                      bpx, ntg, ntg4, dimT, C, dh, H, S);
-    return hipGetLastError();
+#define E2F_AGG(NQ_, U_)                                                                                   \
+  if (nq == NQ_ && un == U_) {                                                                            \
+    k_aggregate_mfma<NQ_, U_><<<(unsigned)blocks, 256, 0, s>>>(T, order, uni, blk_off, uoff, ucount, alpha_blk, n, \
+                                                             nblk, bpx, ntg, ntg4, dimT, C, dh, H, S);     \
+    return hipGetLastError();                                                                             \
+  }
+    E2F_AGG(2, 1) E2F_AGG(4, 1) E2F_AGG(6, 1) E2F_AGG(8, 1)
+#undef E2F_AGG
+    return hipErrorInvalidValue;
   }
   const int64_t W4 = (int64_t)dimT * C / 4;
   const int nchunk = (int)((W4 + kAggChunk4 - 1) / kAggChunk4);
