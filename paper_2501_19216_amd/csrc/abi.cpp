@@ -178,6 +178,14 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
   push_array(blob, o, t.q_ridx);       // 13
   push_array(blob, o, t.k_ptr);        // 14
   push_array(blob, o, t.k_ridx);       // 15
+  std::vector<double> tpc(t.tp_sched.unit);
+  push_array(blob, o, t.tp_sched.k);     // 16
+  push_array(blob, o, t.tp_sched.off);   // 17
+  push_array(blob, o, t.tp_sched.meta);  // 18
+  push_array(blob, o, tpc);              // 19
+  push_array(blob, o, t.rc_sched.k);     // 20
+  push_array(blob, o, t.rc_sched.off);   // 21
+  push_array(blob, o, t.rc_sched.meta);  // 22
   void* mem = nullptr;
   E2F_HIP(hipMalloc(&mem, blob.size()));
   ctx->table_mem[L] = mem;
@@ -203,6 +211,14 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
   d.q_ridx = (const int*)(b + o[13]);
   d.k_ptr = (const int*)(b + o[14]);
   d.k_ridx = (const int*)(b + o[15]);
+  d.tp_k = (const int*)(b + o[16]);
+  d.tp_off = (const int*)(b + o[17]);
+  d.tp_meta = (const int*)(b + o[18]);
+  d.tp_coef = (const double*)(b + o[19]);
+  d.rc_k = (const int*)(b + o[20]);
+  d.rc_off = (const int*)(b + o[21]);
+  d.rc_meta = (const int*)(b + o[22]);
+  d.rc_coef = nullptr;
   d.q_coef = nullptr;
   d.k_coef = nullptr;
   d.max_qslots = t.max_qslots;
@@ -233,10 +249,13 @@ e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStr
   for (size_t e = 0; e < q.size(); ++e) q[e] = t.q_unit[e] * w[t.q_path[e]];
   std::vector<float> k(t.k_unit.size());
   for (size_t e = 0; e < k.size(); ++e) k[e] = (float)(t.k_unit[e] * w[t.k_path[e]]);
+  std::vector<double> rc(t.rc_sched.unit.size());
+  for (size_t e = 0; e < rc.size(); ++e) rc[e] = t.rc_sched.path[e] < 0 ? 0.0 : t.rc_sched.unit[e] * w[t.rc_sched.path[e]];
   std::vector<char> blob;
   std::vector<size_t> o;
   push_array(blob, o, q);
   push_array(blob, o, k);
+  push_array(blob, o, rc);
   E2F_HIP(hipStreamSynchronize(s));  // earlier work may still read the old coefficients
   if (ctx->coef_mem[L]) E2F_HIP(hipFree(ctx->coef_mem[L]));
   ctx->coef_mem[L] = nullptr;
@@ -247,6 +266,7 @@ e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStr
   ctx->coef_w[L] = w;
   ctx->dev[L].q_coef = (const double*)((char*)mem + o[0]);
   ctx->dev[L].k_coef = (const float*)((char*)mem + o[1]);
+  ctx->dev[L].rc_coef = (const double*)((char*)mem + o[2]);
   return E2F_OK;
 }
 

@@ -115,56 +115,95 @@ __global__ void k_col_pair(const int64_t* __restrict__ row_ptr, const int32_t* _
 }
 
 // ------------------------------------------------------------ j-side node TP
-// T[item][r][c] = sum_al M[r][al] h_node^(a)[al][c], stored head-major as
-// T[item][c / dh][r][c % dh] (dh = C gives the plain [r][c] layout), with the per-node matrix
-// M[r][al] = sum_be C^{d de}_{a al, b be} R^(b)_be(p) built once per item in
-// float64 and kept in LDS (cost independent of C).
+// T[item][r][c] = sum_al M[r][al] h_node^(a)[al][c] for the rows r of degree a,
+// with the per-node matrix M[r][al] = sum_be C^{d de}_{a al, b be} R^(b)_be(p)
+// built once per item in float64 (cost independent of C).  The product runs on
+// v_mfma_f32_16x16x4f32: tiles of 16 rows of one degree a (so they share the
+// K operand h^(a), 2a+1 values padded to a multiple of 4) by 16 channels.
+// T is stored head-major, T[item][c / dh][r][c % dh] (dh = C: plain [r][c]).
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+// Build one chunk of a per-node matrix into LDS from its schedule (see
+// Schedule): coalesced, independent loads; each thread sums its slots.
+__device__ __forceinline__ void run_schedule(const int* __restrict__ meta, const double* __restrict__ coef, int K,
+                                             const double* Rl, float* dst) {
+  double acc = 0.0;
+  const int t = threadIdx.x;
+#pragma unroll 4
+  for (int k = 0; k < K; ++k) {
+    const int m = meta[k * kSchedThreads + t];
+    acc += coef[k * kSchedThreads + t] * Rl[(m >> 20) & 127];
+    if (m < 0) {
+      dst[m & 0xfffff] = (float)acc;
+      acc = 0.0;
+    }
+  }
+}
+
+template <int L, int A>
+__device__ __forceinline__ void node_tp_degree(const DevTables& t, const double* Rl, float* Ml, const float* h, int C,
+                                               int dh, float* Tp, int& chunk) {
+  constexpr int NK = (L + 1) * (L + 1);
+  constexpr int KA = 2 * A + 1;
+  constexpr int KP = (KA + 3) & ~3;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int j = lane & 15, k4 = lane >> 4;
+  const int ra0 = t.a_row_start[A], ra1 = t.a_row_start[A + 1];
+  const int NT = (C + 15) / 16;
+  for (int c0 = ra0; c0 < ra1; c0 += kTpRows) {
+    const int rc = min(kTpRows, ra1 - c0);
+    __syncthreads();
+    for (int q = threadIdx.x; q < rc * KP; q += blockDim.x) Ml[q] = 0.0f;
+    __syncthreads();
+    run_schedule(t.tp_meta + t.tp_off[chunk], t.tp_coef + t.tp_off[chunk], t.tp_k[chunk], Rl, Ml);
+    ++chunk;
+    __syncthreads();
+    const int nrt = (rc + 15) / 16;
+#pragma unroll 4
+    for (int task = wave; task < nrt * NT; task += (int)(blockDim.x >> 6)) {
+      const int rt = task / NT, nt = task % NT;
+      const int c = nt * 16 + j;
+      v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KP / 4; ++ks) {
+        const int kk = ks * 4 + k4;
+        const float a = (rt * 16 + j < rc) ? Ml[(rt * 16 + j) * KP + kk] : 0.0f;
+        const float b = (kk < KA && c < C) ? h[(size_t)(A * A + kk) * C + c] : 0.0f;
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+      }
+      if (c < C) {
+        float* dst = Tp + (size_t)(c / dh) * t.dimT * dh + c % dh;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int rl = rt * 16 + 4 * k4 + v;
+          if (rl < rc) dst[(size_t)(c0 + rl) * dh] = acc[v];
+        }
+      }
+    }
+  }
+  (void)NK;
+}
+
+template <int L, int... As>
+__device__ __forceinline__ void node_tp_all(std::integer_sequence<int, As...>, const DevTables& t, const double* Rl,
+                                            float* Ml, const float* h, int C, int dh, float* Tp) {
+  int chunk = 0;
+  (node_tp_degree<L, As>(t, Rl, Ml, h, C, dh, Tp, chunk), ...);
+}
+
 template <int L>
 __global__ __launch_bounds__(256) void k_node_tp(DevTables t, const double* __restrict__ R,
                                                  const int32_t* __restrict__ node_of, const float* __restrict__ feat,
                                                  int C, int dh, float* __restrict__ T) {
   constexpr int NK = (L + 1) * (L + 1);
-  extern __shared__ float smem[];
+  constexpr int KPMAX = ((2 * L + 1) + 3) & ~3;
+  __shared__ float Ml[kTpRows * KPMAX];
   __shared__ double Rl[NK];
   const int item = blockIdx.x;
   const int node = node_of ? node_of[item] : item;
-  const int CB = C < 256 ? C : 256;
-  const int G = blockDim.x / CB;
-  float* Ml = smem;
-  float* hl = smem + t.m_slots;
   if (threadIdx.x < NK) Rl[threadIdx.x] = R[(size_t)item * NK + threadIdx.x];
-  __syncthreads();
-  for (int s = threadIdx.x; s < t.m_slots; s += blockDim.x) {
-    double v = 0.0;
-    for (int e = t.m_ptr[s]; e < t.m_ptr[s + 1]; ++e) v += t.m_coef[e] * Rl[t.m_ridx[e]];
-    Ml[s] = (float)v;
-  }
-  const int cl = threadIdx.x % CB, g = threadIdx.x / CB;
-  const float* hsrc = feat + (size_t)node * NK * C;
-  float* Tdst = T + (size_t)item * t.dimT * C;
-  for (int c0 = 0; c0 < C; c0 += CB) {
-    const int cw = (C - c0) < CB ? (C - c0) : CB;
-    __syncthreads();
-    for (int q = threadIdx.x; q < NK * CB; q += blockDim.x) {
-      const int k = q / CB, cc = q % CB;
-      hl[q] = cc < cw ? hsrc[(size_t)k * C + c0 + cc] : 0.0f;
-    }
-    __syncthreads();
-    if (g < G && cl < cw) {
-#pragma unroll
-      for (int a = 0; a <= L; ++a) {
-        const int r1 = t.a_row_start[a + 1];
-        for (int r = t.a_row_start[a] + g; r < r1; r += G) {
-          const float* mrow = Ml + t.m_rowoff[r];
-          float acc = 0.0f;
-#pragma unroll
-          for (int al = 0; al < 2 * a + 1; ++al) acc += mrow[al] * hl[(a * a + al) * CB + cl];
-          const int cc = c0 + cl;
-          Tdst[(size_t)(cc / dh) * t.dimT * dh + (size_t)r * dh + cc % dh] = acc;
-        }
-      }
-    }
-  }
+  node_tp_all<L>(std::make_integer_sequence<int, L + 1>{}, t, Rl, Ml, feat + (size_t)node * NK * C, C, dh,
+                 T + (size_t)item * t.dimT * C);
 }
 
 // ------------------------------------------------------------ receiver order
@@ -338,7 +377,6 @@ __global__ void k_block_alpha(const int64_t* __restrict__ row_ptr, const int32_t
 // Accumulation order is fixed (deterministic).
 constexpr int kXcds = 8;
 constexpr int kPiece = 512;  // union rows staged in LDS at a time
-typedef float v4f __attribute__((ext_vector_type(4)));
 
 template <int NQ, int UNROLL>
 __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict__ T,
@@ -455,52 +493,72 @@ __global__ __launch_bounds__(64 * kAggRecv) void k_aggregate_rows(const float4* 
 }
 
 // ------------------------------------------------------------ i-side recouple
-// y_i^(o)[m][c] = sum_col Q_o[m][col] S_i[col][c], with the per-node matrix
-// Q_o[m][(a,b,d,de)] = sum_u K(a,b,d,u,o) sum_ga C^{o m}_{u ga, d de} R^(u)_ga(p_i)
-// built in float64 per receiver and kept in LDS, one output degree at a time.
-template <int L, int O>
-__device__ __forceinline__ void recouple_one(const DevTables& t, const double* Rl, float* Ql, const float* Si,
-                                             int C, int dh, float* yi) {
-  constexpr int NM = 2 * O + 1;
-  const int ncol = t.q_ncol[O], s0 = t.q_slotoff[O];
-  __syncthreads();
-  for (int s = threadIdx.x; s < NM * ncol; s += blockDim.x) {
-    double v = 0.0;
-    for (int e = t.q_ptr[s0 + s]; e < t.q_ptr[s0 + s + 1]; ++e) v += t.q_coef[e] * Rl[t.q_ridx[e]];
-    Ql[s] = (float)v;
-  }
-  __syncthreads();
-  const int* cols = t.q_cols + t.q_coloff[O];
-  for (int c = threadIdx.x; c < C; c += blockDim.x) {
-    float acc[NM];
-#pragma unroll
-    for (int m = 0; m < NM; ++m) acc[m] = 0.0f;
-    for (int col = 0; col < ncol; ++col) {
-      const float s = Si[(size_t)(c / dh) * t.dimT * dh + (size_t)cols[col] * dh + c % dh];
-#pragma unroll
-      for (int m = 0; m < NM; ++m) acc[m] += Ql[m * ncol + col] * s;
-    }
-#pragma unroll
-    for (int m = 0; m < NM; ++m) yi[(size_t)(O * O + m) * C + c] = acc[m];
-  }
-}
+// y_i[k][c] = sum_r Q_i[k][r] S_i[r][c] over the T rows r, with the per-node
+// matrix Q_i[(o,m)][(a,b,d,de)] = sum_u K(a,b,d,u,o) sum_ga C^{o m}_{u ga, d de}
+// R^(u)_ga(p_i) built in float64 in LDS (256 T rows at a time, from a fixed
+// schedule) and the product on v_mfma_f32_16x16x4f32: 16 output rows x 16
+// channels per tile, S_i read from HBM exactly once.
 
-template <int L, int... Os>
-__device__ __forceinline__ void recouple_all(std::integer_sequence<int, Os...>, const DevTables& t, const double* Rl,
-                                             float* Ql, const float* Si, int C, int dh, float* yi) {
-  (recouple_one<L, Os>(t, Rl, Ql, Si, C, dh, yi), ...);
-}
-
-template <int L>
+template <int L, int NTW>
 __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __restrict__ R,
                                                   const float* __restrict__ S, int C, int dh, float* __restrict__ y) {
   constexpr int NK = (L + 1) * (L + 1);
-  extern __shared__ float Ql[];
+  constexpr int MT = (NK + 15) / 16;  // NTW: channel tiles per wave and pass
+  __shared__ float Qt[kRcRows * 16 * MT];  // Qt[r][k]
   __shared__ double Rl[NK];
   const int i = blockIdx.x;
   if (threadIdx.x < NK) Rl[threadIdx.x] = R[(size_t)i * NK + threadIdx.x];
-  recouple_all<L>(std::make_integer_sequence<int, L + 1>{}, t, Rl, Ql, S + (size_t)i * t.dimT * C, C, dh,
-                  y + (size_t)i * NK * C);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int j = lane & 15, k4 = lane >> 4;
+  const int dimT = t.dimT;
+  const float* Si = S + (size_t)i * dimT * C;
+  const int NT = (C + 15) / 16;
+  for (int ns = 0; ns < NT; ns += 4 * NTW) {
+    v4f acc[NTW][MT];
+#pragma unroll
+    for (int q = 0; q < NTW; ++q)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[q][mt] = (v4f){0.f, 0.f, 0.f, 0.f};
+    for (int r0 = 0; r0 < dimT; r0 += kRcRows) {
+      const int rc = min(kRcRows, dimT - r0);
+      __syncthreads();
+      for (int q = threadIdx.x; q < kRcRows * 16 * MT; q += blockDim.x) Qt[q] = 0.0f;
+      __syncthreads();
+      const int ch = r0 / kRcRows;
+      run_schedule(t.rc_meta + t.rc_off[ch], t.rc_coef + t.rc_off[ch], t.rc_k[ch], Rl, Qt);
+      __syncthreads();
+#pragma unroll 8
+      for (int kk = 0; kk < rc; kk += 4) {
+        const int rl = kk + k4;
+        float a[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) a[mt] = Qt[rl * 16 * MT + mt * 16 + j];
+#pragma unroll
+        for (int q = 0; q < NTW; ++q) {
+          const int nt = ns + wave + 4 * q;
+          const int c = nt * 16 + j;
+          const float b = (rl < rc && nt < NT && c < C)
+                              ? Si[(size_t)(c / dh) * dimT * dh + (size_t)(r0 + rl) * dh + c % dh]
+                              : 0.0f;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) acc[q][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], b, acc[q][mt], 0, 0, 0);
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < NTW; ++q) {
+      const int nt = ns + wave + 4 * q;
+      const int c = nt * 16 + j;
+      if (nt >= NT || c >= C) continue;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = mt * 16 + 4 * k4 + v;
+          if (row < NK) y[((size_t)i * NK + row) * C + c] = acc[q][mt][v];
+        }
+    }
+  }
 }
 
 // ------------------------------------------------------------ channel mixing
@@ -704,13 +762,10 @@ hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const
 hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* node_of, const float* feat,
                           int n_items, int C, int dh, float* T, hipStream_t s) {
   if (n_items == 0) return hipSuccess;
-  const int CB = C < 256 ? C : 256;
-  const size_t lds = sizeof(float) * ((size_t)t.m_slots + (size_t)t.nk * CB);
   switch (t.L) {
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
-    if (hipError_t e = allow_lds(k_node_tp<LL>, lds); e != hipSuccess) return e;                            \
-    k_node_tp<LL><<<n_items, 256, lds, s>>>(t, R, node_of, feat, C, dh, T);                                     \
+    k_node_tp<LL><<<n_items, 256, 0, s>>>(t, R, node_of, feat, C, dh, T);                                   \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
 #undef E2F_CASE
@@ -811,13 +866,14 @@ hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, int n, int C, int dh, float* y,
                            hipStream_t s) {
   if (n == 0) return hipSuccess;
-  const int threads = C <= 64 ? 64 : (C <= 128 ? 128 : 256);
-  const size_t lds = sizeof(float) * (size_t)t.max_qslots;
+  const int nt = (C + 15) / 16;  // channel tiles; 4 waves
+  const int ntw = nt <= 4 ? 1 : (nt <= 8 ? 2 : 4);
   switch (t.L) {
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
-    if (hipError_t e = allow_lds(k_recouple<LL>, lds); e != hipSuccess) return e;                           \
-    k_recouple<LL><<<n, threads, lds, s>>>(t, R, S, C, dh, y);                                                  \
+    if (ntw == 1) k_recouple<LL, 1><<<n, 256, 0, s>>>(t, R, S, C, dh, y);                                   \
+    else if (ntw == 2) k_recouple<LL, 2><<<n, 256, 0, s>>>(t, R, S, C, dh, y);                              \
+    else k_recouple<LL, 4><<<n, 256, 0, s>>>(t, R, S, C, dh, y);                                            \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
 #undef E2F_CASE

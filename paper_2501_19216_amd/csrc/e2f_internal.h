@@ -26,6 +26,23 @@ double wigner6j(int j1, int j2, int j3, int j4, int j5, int j6);
 // Structure of the factorised layer for one L: every table is independent of
 // the path weights except the *_coef arrays, which the context refreshes when
 // the caller's path weights change.
+// Row chunks of the per-node matrices staged in LDS by the node TP and the
+// recouple kernels, and their thread count.
+constexpr int kSchedThreads = 256;
+constexpr int kTpRows = 256;
+constexpr int kRcRows = 256;
+
+// A per-node matrix built by 256 threads from a fixed schedule: in chunk c,
+// thread t walks entries k = 0..k[c]-1 at index off[c] + k*256 + t, each
+// adding coef * R[ridx] and, on the last entry of a slot, storing the sum to
+// LDS position dest.  meta packs dest (bits 0-19), ridx (20-26), last (31).
+struct Schedule {
+  std::vector<int> k, off;
+  std::vector<int> meta;
+  std::vector<int> path;      // path-weight index of each entry (-1: none)
+  std::vector<double> unit;   // coefficient without the path weight
+};
+
 struct Block {
   int a, b, d, toff;  // T_j^(a,b,d) occupies rows toff .. toff+2d
 };
@@ -57,6 +74,8 @@ struct LayerTables {
   std::vector<int> k_ridx;
   std::vector<int> k_path;
   std::vector<double> k_unit;
+  Schedule tp_sched;                // node TP: chunks (degree a, 256 rows), dest = row*KP(a) + al
+  Schedule rc_sched;                // recouple: chunks of 256 T rows, dest = row*16*MT + (o*o+m)
   int max_qslots = 0;               // largest (2o+1)*ncol[o]
   int m_slots() const { return m_rowoff.back(); }
 };
@@ -74,6 +93,8 @@ struct DevTables {
   const int* q_ncol; const int* q_coloff; const int* q_cols; const int* q_slotoff;
   const int* q_ptr; const int* q_ridx; const double* q_coef; // q_coef includes path weights
   const int* k_ptr; const int* k_ridx; const float* k_coef;  // k_coef includes path weights
+  const int* tp_k; const int* tp_off; const int* tp_meta; const double* tp_coef;
+  const int* rc_k; const int* rc_off; const int* rc_meta; const double* rc_coef;  // rc_coef includes path weights
   int max_qslots, m_slots;
 };
 

@@ -18,6 +18,7 @@
 //   i-side degree u <= L-b and output o <= L can use them, and the i-side
 //   coefficient K = w_{a,b+u,o} (-1)^b binom(b+u,u) X(a,b,u,o;d) of the binomial
 //   expansion (Thm. 3.2) recoupled by Def. 2.3.
+#include <algorithm>
 #include <cmath>
 #include <complex>
 #include <cstdlib>
@@ -121,6 +122,62 @@ double recoupling_weight(int a, int b, int u, int o, int d) {
   if (((a + b + d) & 1) && ((u + d + o) & 1)) x = -x;
   return x;
 }
+
+namespace {
+
+struct Entry {
+  int ridx, path;
+  double unit;
+};
+struct Slot {
+  int dest;
+  std::vector<Entry> e;
+};
+
+// Balance the slots of every chunk over the threads (largest first to the
+// least loaded thread) and lay the entries out transposed.
+Schedule make_schedule(const std::vector<std::vector<Slot>>& chunks) {
+  Schedule s;
+  const int T = kSchedThreads;
+  for (const auto& slots : chunks) {
+    std::vector<int> order(slots.size());
+    for (size_t q = 0; q < slots.size(); ++q) order[q] = (int)q;
+    std::stable_sort(order.begin(), order.end(),
+                     [&](int x, int y) { return slots[x].e.size() > slots[y].e.size(); });
+    std::vector<std::vector<const Slot*>> per(T);
+    std::vector<size_t> load(T, 0);
+    for (int q : order) {
+      if (slots[q].e.empty()) continue;
+      int best = 0;
+      for (int th = 1; th < T; ++th)
+        if (load[th] < load[best]) best = th;
+      per[best].push_back(&slots[q]);
+      load[best] += slots[q].e.size();
+    }
+    size_t K = 0;
+    for (int th = 0; th < T; ++th) K = std::max(K, load[th]);
+    s.off.push_back((int)s.meta.size());
+    s.k.push_back((int)K);
+    const size_t base = s.meta.size();
+    s.meta.resize(base + K * T, 0);
+    s.path.resize(base + K * T, -1);
+    s.unit.resize(base + K * T, 0.0);
+    for (int th = 0; th < T; ++th) {
+      size_t k = 0;
+      for (const Slot* sl : per[th])
+        for (size_t q = 0; q < sl->e.size(); ++q, ++k) {
+          const size_t at = base + k * T + th;
+          const bool last = q + 1 == sl->e.size();
+          s.meta[at] = sl->dest | (sl->e[q].ridx << 20) | (last ? (int)0x80000000u : 0);
+          s.path[at] = sl->e[q].path;
+          s.unit[at] = sl->e[q].unit;
+        }
+    }
+  }
+  return s;
+}
+
+}  // namespace
 
 static bool block_used(int L, int a, int b, int d) {
   for (int u = 0; u <= L - b; ++u)
@@ -266,6 +323,42 @@ LayerTables build_layer_tables(int L) {
   }
   t.q_coloff[L1] = (int)t.q_cols.size();
   t.q_slotoff[L1] = (int)t.q_ptr.size() - 1;
+  // ---- build schedules of the per-node matrices
+  {
+    // node TP: chunks in kernel order (degree a, then 256-row chunks of its rows)
+    std::vector<std::vector<Slot>> chunks;
+    for (int a = 0; a <= L; ++a) {
+      const int KP = (2 * a + 1 + 3) & ~3;
+      for (int c0 = t.a_row_start[a]; c0 < t.a_row_start[a + 1]; c0 += kTpRows) {
+        std::vector<Slot> slots;
+        const int c1 = std::min(t.a_row_start[a + 1], c0 + kTpRows);
+        for (int r = c0; r < c1; ++r)
+          for (int al = 0; al < 2 * a + 1; ++al) {
+            const int s = t.m_rowoff[r] + al;
+            Slot sl{(r - c0) * KP + al, {}};
+            for (int e = t.m_ptr[s]; e < t.m_ptr[s + 1]; ++e) sl.e.push_back({t.m_ridx[e], -1, t.m_coef[e]});
+            slots.push_back(std::move(sl));
+          }
+        chunks.push_back(std::move(slots));
+      }
+    }
+    t.tp_sched = make_schedule(chunks);
+    // recouple: chunks of 256 T rows; Q rows padded to 16*MT
+    const int MT = (t.nk + 15) / 16;
+    std::vector<std::vector<Slot>> rchunks((t.dimT + kRcRows - 1) / kRcRows);
+    for (int o = 0; o <= L; ++o) {
+      const int ncol = t.q_ncol[o];
+      for (int m = 0; m < 2 * o + 1; ++m)
+        for (int col = 0; col < ncol; ++col) {
+          const int s = t.q_slotoff[o] + m * ncol + col;
+          const int row = t.q_cols[t.q_coloff[o] + col];
+          Slot sl{(row % kRcRows) * 16 * MT + o * o + m, {}};
+          for (int e = t.q_ptr[s]; e < t.q_ptr[s + 1]; ++e) sl.e.push_back({t.q_ridx[e], t.q_path[e], t.q_unit[e]});
+          rchunks[row / kRcRows].push_back(std::move(sl));
+        }
+    }
+    t.rc_sched = make_schedule(rchunks);
+  }
 
   // ---- edge filter K[k][q] = sum_f w_afo sum_mf C^{o m}_{a al, f mf} R^(f)_mf(r_ij)
   t.k_ptr.push_back(0);
