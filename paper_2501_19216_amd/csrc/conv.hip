@@ -141,8 +141,8 @@ __device__ __forceinline__ void run_schedule(const int* __restrict__ meta, const
 }
 
 template <int L, int A>
-__device__ __forceinline__ void node_tp_degree(const DevTables& t, const double* Rl, float* Ml, const float* h, int C,
-                                               int dh, float* Tp, int& chunk) {
+__device__ __forceinline__ void node_tp_degree(const DevTables& t, const double* Rl, float* Ml, const float* h,
+                                               int hstride, int C, int dh, float* Tp, int& chunk) {
   constexpr int NK = (L + 1) * (L + 1);
   constexpr int KA = 2 * A + 1;
   constexpr int KP = (KA + 3) & ~3;
@@ -168,7 +168,7 @@ __device__ __forceinline__ void node_tp_degree(const DevTables& t, const double*
       for (int ks = 0; ks < KP / 4; ++ks) {
         const int kk = ks * 4 + k4;
         const float a = (rt * 16 + j < rc) ? Ml[(rt * 16 + j) * KP + kk] : 0.0f;
-        const float b = (kk < KA && c < C) ? h[(size_t)(A * A + kk) * C + c] : 0.0f;
+        const float b = (kk < KA && c < C) ? h[(A * A + kk) * hstride + c] : 0.0f;
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
       }
       if (c < C) {
@@ -186,24 +186,29 @@ __device__ __forceinline__ void node_tp_degree(const DevTables& t, const double*
 
 template <int L, int... As>
 __device__ __forceinline__ void node_tp_all(std::integer_sequence<int, As...>, const DevTables& t, const double* Rl,
-                                            float* Ml, const float* h, int C, int dh, float* Tp) {
+                                            float* Ml, const float* h, int hstride, int C, int dh, float* Tp) {
   int chunk = 0;
-  (node_tp_degree<L, As>(t, Rl, Ml, h, C, dh, Tp, chunk), ...);
+  (node_tp_degree<L, As>(t, Rl, Ml, h, hstride, C, dh, Tp, chunk), ...);
 }
 
 template <int L>
 __global__ __launch_bounds__(256) void k_node_tp(DevTables t, const double* __restrict__ R,
                                                  const int32_t* __restrict__ node_of, const float* __restrict__ feat,
-                                                 int C, int dh, float* __restrict__ T) {
+                                                 int C, int dh, bool stage_h, float* __restrict__ T) {
   constexpr int NK = (L + 1) * (L + 1);
   constexpr int KPMAX = ((2 * L + 1) + 3) & ~3;
   __shared__ float Ml[kTpRows * KPMAX];
   __shared__ double Rl[NK];
+  extern __shared__ float hl[];  // h_node staged in LDS when it fits (dynamic size > 0)
   const int item = blockIdx.x;
   const int node = node_of ? node_of[item] : item;
   if (threadIdx.x < NK) Rl[threadIdx.x] = R[(size_t)item * NK + threadIdx.x];
-  node_tp_all<L>(std::make_integer_sequence<int, L + 1>{}, t, Rl, Ml, feat + (size_t)node * NK * C, C, dh,
-                 T + (size_t)item * t.dimT * C);
+  const float* h = feat + (size_t)node * NK * C;
+  if (stage_h) {
+    for (int q = threadIdx.x; q < NK * C / 4; q += blockDim.x) ((float4*)hl)[q] = ((const float4*)h)[q];
+    h = hl;
+  }
+  node_tp_all<L>(std::make_integer_sequence<int, L + 1>{}, t, Rl, Ml, h, C, C, dh, T + (size_t)item * t.dimT * C);
 }
 
 // ------------------------------------------------------------ receiver order
@@ -762,10 +767,12 @@ hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const
 hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* node_of, const float* feat,
                           int n_items, int C, int dh, float* T, hipStream_t s) {
   if (n_items == 0) return hipSuccess;
+  const size_t hbytes = sizeof(float) * (size_t)t.nk * C;
+  const size_t lds = hbytes <= 32768 ? hbytes : 0;  // stage h_node in LDS when small
   switch (t.L) {
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
-    k_node_tp<LL><<<n_items, 256, 0, s>>>(t, R, node_of, feat, C, dh, T);                                   \
+    k_node_tp<LL><<<n_items, 256, lds, s>>>(t, R, node_of, feat, C, dh, lds > 0, T);                       \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
 #undef E2F_CASE
