@@ -113,7 +113,8 @@ typedef struct {
   const double* path_w;  /* host [(L+1)^3] w[a][f][o]; NULL => cutoff^-f on triangle-valid paths */
   const void* mix_w;     /* device [(L+1)][C][C] W[o][c_out][c_in] of mix_dtype; NULL => no mixing */
   e2f_dtype mix_dtype;   /* E2F_F32, or E2F_BF16 (mixing inputs rounded to bf16, fp32 accumulate) */
-  float tile_side;       /* side of the receiver tiles whose centres serve as local origins; 0 => 5*cutoff */
+  float tile_side;       /* side of the receiver tiles whose centres serve as local origins;
+                            0 => cutoff * (8, 8, 8, 6, 4, 3, 2) for L = 0..6 */
 } e2f_conv_params;
 
 /* Wigner-6j convolution forward (Thm. 3.3, Alg. 1): the layer above computed
@@ -123,8 +124,11 @@ typedef struct {
  * y_i = sum K(a,b,d,u,o) [R^(u)(r_i - o_t) (x) S_i^(a,b,d)]^(o), then mixing.
  * graph_id: [N] or NULL (must match the graph's).  alpha: [E][H] or NULL
  * (all ones).  out: [N][(L+1)^2][C].  Isolated atoms get zero rows.
- * Deterministic: no floating-point atomics.  (sync: one small device->host
- * read of the tile plan size) */
+ * Tiles are processed in batches whose T and S fit a memory budget (60% of
+ * the free device memory, at most 96 GiB; the environment variable
+ * E2F_TILE_BUDGET_MB overrides it), so the workspace stays bounded for large
+ * systems.  Deterministic: no floating-point atomics.  (sync: small
+ * device->host reads of the plan sizes) */
 e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
                                      const int32_t* graph_id, const float* feat, int32_t n, const int64_t* row_ptr,
                                      const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,

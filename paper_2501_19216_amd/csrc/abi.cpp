@@ -6,6 +6,8 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
+#include <algorithm>
 #include <cstring>
 #include <limits>
 #include <string>
@@ -51,6 +53,7 @@ struct e2f_ctx {
   std::vector<double> origins_host;
   Buf a, b, c;
   int64_t last_pairs = 0, last_tiles = 0;  // plan size of the last factorised forward
+  int64_t last_batches = 0;
   // kernel timing (e2f_profile): events recorded on the launch stream
   bool prof = false;
   struct Rec {
@@ -517,7 +520,10 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   if (rs != E2F_OK) return rs;
   // ---- tile grid (local origins; precision of the binomial expansion)
   TilePlan tp;
-  const double side = (p->tile_side > 0.0f ? (double)p->tile_side : 5.0 * (double)p->cutoff) * kGrid;
+  // fp32 T and S lose about eps * (|p| / cutoff)^L in the binomial expansion, so
+  // the default tile (whose centre is the local origin) shrinks with L
+  static const double kTileCutoffs[kMaxL + 1] = {8.0, 8.0, 8.0, 6.0, 4.0, 3.0, 2.0};
+  const double side = (p->tile_side > 0.0f ? (double)p->tile_side : kTileCutoffs[L] * (double)p->cutoff) * kGrid;
   tp.ncell = 1;
   for (int k = 0; k < 3; ++k) {
     tp.lo[k] = st[k];
@@ -543,11 +549,11 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
           ctx->origins_host[3 * cell + k] = (double)og / kGrid;
         }
       }
-  const size_t scan_b = scan_tmp_bytes(count);
+  const size_t scan_b = std::max(scan_tmp_bytes(count), blocks_tmp_bytes((int)keys + 1));
   const size_t sort_b = recv_sort_tmp_bytes(n);
   size_t need_a = al256(sizeof(int32_t) * (size_t)n) + 2 * al256(sizeof(int32_t) * (size_t)count) + al256(scan_b) +
                   al256(sizeof(double) * ctx->origins_host.size()) + 2 * al256(sizeof(uint64_t) * (size_t)n) +
-                  2 * al256(sizeof(int32_t) * (size_t)n) + al256(sort_b);
+                  2 * al256(sizeof(int32_t) * (size_t)n) + al256(sort_b) + 3 * al256(sizeof(int32_t) * (keys + 1));
   rs = ensure(ctx, ctx->a, need_a, s);
   if (rs != E2F_OK) return rs;
   Carver ca{(char*)ctx->a.p};
@@ -561,38 +567,68 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   int32_t* rvals = ca.take<int32_t>(n);
   int32_t* order = ca.take<int32_t>(n);
   void* sort_tmp = ca.take<char>(sort_b);
+  int32_t* key_count = ca.take<int32_t>(keys + 1);
+  int32_t* rstart_d = ca.take<int32_t>(keys + 1);
+  int32_t* pstart_d = ca.take<int32_t>(keys + 1);
   E2F_HIP(hipMemcpyAsync(origins, ctx->origins_host.data(), sizeof(double) * ctx->origins_host.size(),
                          hipMemcpyHostToDevice, s));
   E2F_TIMED("tile_plan", launch_tile_keys(pos, graph_id, n, tp.lo, tp.dim, tp.span, tp.ncell, tile_of, s));
   E2F_HIP(hipMemsetAsync(flags, 0, sizeof(int32_t) * (size_t)count, s));
   E2F_TIMED("tile_plan", launch_pair_flags(row_ptr, col_idx, tile_of, n, flags, ctx->stats + 8, s));
-  // receivers in spatial order (fine cells of 4 A) for L2 reuse in the aggregation
+  // receivers in (tile, spatial) order: fine cells of 4 A give the L2 reuse of the aggregation
   E2F_TIMED("tile_plan", launch_sort_receivers(pos, tile_of, n, tp.lo, (int64_t)(4.0 * kGrid), rkeys, rkeys_out,
                                                rvals, order, sort_tmp, sort_b, s));
   E2F_TIMED("tile_plan", launch_scan_i32(flags, pidx, count, scan_tmp, scan_b, s));
+  E2F_TIMED("tile_plan", launch_tile_ranges(tile_of, pidx, n, (int)keys, key_count, rstart_d, pstart_d, scan_tmp,
+                                            scan_b, s));
+  std::vector<int32_t> rstart((size_t)keys + 1), pstart((size_t)keys + 1);
   E2F_HIP(hipMemcpyAsync(ctx->pinned, pidx + count - 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
   E2F_HIP(hipMemcpyAsync((char*)ctx->pinned + 8, flags + count - 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
   E2F_HIP(hipMemcpyAsync((char*)ctx->pinned + 16, ctx->stats + 8, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  E2F_HIP(hipMemcpyAsync(rstart.data(), rstart_d, sizeof(int32_t) * (keys + 1), hipMemcpyDeviceToHost, s));
+  E2F_HIP(hipMemcpyAsync(pstart.data(), pstart_d, sizeof(int32_t) * keys, hipMemcpyDeviceToHost, s));
   E2F_HIP(hipStreamSynchronize(s));
   int32_t last_idx, last_flag, max_degree;
   std::memcpy(&last_idx, ctx->pinned, 4);
   std::memcpy(&last_flag, (char*)ctx->pinned + 8, 4);
   std::memcpy(&max_degree, (char*)ctx->pinned + 16, 4);
-  // the MFMA aggregation over receiver blocks of 16 needs 16 * degree <= 8192
-  const bool use_blocks = max_degree <= kBlockMaxDegree;
-  const int nblk = (n + 15) / 16;
-  const size_t blk_tmp_b = blocks_tmp_bytes(nblk);
   const int64_t P = (int64_t)last_idx + last_flag;
+  pstart[keys] = (int32_t)P;
   ctx->last_pairs = P;
   ctx->last_tiles = keys;
+  // the MFMA aggregation over receiver blocks of 16 needs 16 * degree <= 8192
+  const bool use_blocks = max_degree <= kBlockMaxDegree;
+  // ---- tile batches: T and S of a batch must fit the memory budget
+  const size_t row_bytes = sizeof(float) * (size_t)t.dimT * C;
+  size_t free_b = 0, total_b = 0;
+  E2F_HIP(hipMemGetInfo(&free_b, &total_b));
+  size_t budget = std::min<size_t>((size_t)96 << 30, (free_b + ctx->b.n + ctx->c.n) / 10 * 6);
+  if (const char* cap = getenv("E2F_TILE_BUDGET_MB")) budget = (size_t)atoll(cap) << 20;
+  struct Batch {
+    int t0, t1;
+  };
+  std::vector<Batch> batches;
+  int64_t max_pairs = 0, max_recv = 0;
+  for (int t0 = 0; t0 < (int)keys;) {
+    int t1 = t0 + 1;
+    auto cost = [&](int a, int b) {
+      return (size_t)((int64_t)(pstart[b] - pstart[a]) + (rstart[b] - rstart[a])) * row_bytes;
+    };
+    while (t1 < (int)keys && cost(t0, t1 + 1) <= budget) ++t1;
+    batches.push_back({t0, t1});
+    max_pairs = std::max<int64_t>(max_pairs, pstart[t1] - pstart[t0]);
+    max_recv = std::max<int64_t>(max_recv, rstart[t1] - rstart[t0]);
+    t0 = t1;
+  }
+  const int nblk = (int)((max_recv + 15) / 16);
+  const size_t blk_tmp_b = blocks_tmp_bytes(nblk);
   // ---- phase 2 buffers
   const bool mixing = p->mix_w != nullptr;
-  const size_t tbytes = sizeof(float) * (size_t)P * t.dimT * C;
-  const size_t sbytes = sizeof(float) * (size_t)n * t.dimT * C;
   const size_t need_b = 2 * al256(sizeof(int32_t) * (size_t)P) + 3 * al256(sizeof(int32_t) * (size_t)n_edges) +
                         4 * al256(sizeof(int32_t) * (size_t)(nblk + 1)) + al256(blk_tmp_b) +
                         al256(sizeof(double) * (size_t)P * nk) + al256(sizeof(double) * (size_t)n * nk) +
-                        al256(tbytes) + al256(sbytes) + (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
+                        al256(row_bytes * (size_t)max_pairs) + al256(row_bytes * (size_t)max_recv) +
+                        (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
   rs = ensure(ctx, ctx->b, need_b, s);
   if (rs != E2F_OK) return rs;
   Carver cb{(char*)ctx->b.p};
@@ -608,32 +644,41 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   void* blk_tmp = cb.take<char>(blk_tmp_b);
   double* Rp = cb.take<double>((size_t)P * nk);
   double* Rr = cb.take<double>((size_t)n * nk);
-  float* T = cb.take<float>((size_t)P * t.dimT * C);
-  float* S = cb.take<float>((size_t)n * t.dimT * C);
+  float* T = cb.take<float>((size_t)max_pairs * t.dimT * C);
+  float* S = cb.take<float>((size_t)max_recv * t.dimT * C);
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
   E2F_TIMED("tile_plan", launch_pairs(flags, pidx, count, n, pair_node, pair_tile, s));
   E2F_TIMED("tile_plan", launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
-  float* alpha_blk = nullptr;
-  if (use_blocks) {
-    E2F_TIMED("tile_plan", launch_block_union(row_ptr, col_pair, order, n, blk_count, blk_off, uni, ucount, uoff,
-                                              edge_slot, blk_tmp, blk_tmp_b, s));
-    E2F_HIP(hipMemcpyAsync(ctx->pinned, uoff + nblk, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-    E2F_HIP(hipStreamSynchronize(s));
-    int32_t union_rows;
-    std::memcpy(&union_rows, ctx->pinned, 4);
-    rs = ensure(ctx, ctx->c, sizeof(float) * (size_t)union_rows * p->heads * 16 + 256, s);
-    if (rs != E2F_OK) return rs;
-    alpha_blk = (float*)ctx->c.p;
-    E2F_TIMED("tile_plan", launch_block_alpha(row_ptr, order, n, uoff, edge_slot, alpha, p->heads, union_rows,
-                                              alpha_blk, s));
-  }
   E2F_TIMED("sh", launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, nullptr, s));
   E2F_TIMED("sh", launch_sh(t, pos, nullptr, origins, nullptr, tile_of, tp.ncell, n, Rr, nullptr, s));
-  E2F_TIMED("node_tp", launch_node_tp(t, Rp, pair_node, feat, (int)P, C, C / p->heads, T, s));
-  E2F_TIMED("aggregate", launch_aggregate(T, row_ptr, col_pair, alpha, order, uni, blk_off, uoff, ucount, alpha_blk,
-                                          use_blocks, n, t.dimT, C, p->heads, S, s));
-  E2F_TIMED("recouple", launch_recouple(t, Rr, S, n, C, C / p->heads, y, s));
+  const int dh = C / p->heads;
+  for (const Batch& bt : batches) {
+    const int p0 = pstart[bt.t0], q0 = rstart[bt.t0];
+    const int pb = pstart[bt.t1] - p0, nb = rstart[bt.t1] - q0;
+    if (nb == 0) continue;
+    const int32_t* ord = order + q0;
+    E2F_TIMED("node_tp", launch_node_tp(t, Rp + (size_t)p0 * nk, pair_node + p0, feat, pb, C, dh, T, s));
+    float* alpha_blk = nullptr;
+    if (use_blocks) {
+      const int nblk_b = (nb + 15) / 16;
+      E2F_TIMED("tile_plan", launch_block_union(row_ptr, col_pair, ord, nb, blk_count, blk_off, uni, ucount, uoff,
+                                                edge_slot, blk_tmp, blk_tmp_b, s));
+      E2F_HIP(hipMemcpyAsync(ctx->pinned, uoff + nblk_b, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+      E2F_HIP(hipStreamSynchronize(s));
+      int32_t union_rows;
+      std::memcpy(&union_rows, ctx->pinned, 4);
+      rs = ensure(ctx, ctx->c, sizeof(float) * (size_t)union_rows * p->heads * 16 + 256, s);
+      if (rs != E2F_OK) return rs;
+      alpha_blk = (float*)ctx->c.p;
+      E2F_TIMED("tile_plan", launch_block_alpha(row_ptr, ord, nb, uoff, edge_slot, alpha, p->heads, union_rows,
+                                                alpha_blk, s));
+    }
+    E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, alpha, ord, uni, blk_off, uoff, ucount,
+                                            alpha_blk, use_blocks, nb, t.dimT, C, p->heads, S, s));
+    E2F_TIMED("recouple", launch_recouple(t, Rr, S, ord, nb, C, dh, y, s));
+  }
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
+  ctx->last_batches = (int64_t)batches.size();
   return E2F_OK;
 }
 

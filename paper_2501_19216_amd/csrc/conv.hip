@@ -114,6 +114,18 @@ __global__ void k_col_pair(const int64_t* __restrict__ row_ptr, const int32_t* _
   for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) col_pair[e] = pidx[base + col[e]];
 }
 
+// Per tile key: number of receivers (for their range in the receiver order)
+// and first pair index (pidx at the key's first flag).
+__global__ void k_key_counts(const int32_t* __restrict__ tile_of, int n, int32_t* __restrict__ counts) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) atomicAdd(&counts[tile_of[i]], 1);
+}
+
+__global__ void k_key_pstart(const int32_t* __restrict__ pidx, int keys, int n, int32_t* __restrict__ pstart) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < keys) pstart[t] = pidx[(int64_t)t * n];
+}
+
 // ------------------------------------------------------------ j-side node TP
 // T[item][r][c] = sum_al M[r][al] h_node^(a)[al][c] for the rows r of degree a,
 // with the per-node matrix M[r][al] = sum_be C^{d de}_{a al, b be} R^(b)_be(p)
@@ -384,8 +396,7 @@ constexpr int kXcds = 8;
 constexpr int kPiece = 512;  // union rows staged in LDS at a time
 
 template <int NQ, int UNROLL>
-__global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict__ T,
-                                                        const int32_t* __restrict__ order,
+__global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict__ T, int pair_base,
                                                         const int32_t* __restrict__ uni,
                                                         const int32_t* __restrict__ blk_off,
                                                         const int32_t* __restrict__ uoff,
@@ -424,7 +435,7 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
   for (int p0 = 0; p0 < nu; p0 += kPiece) {
     const int np = min(nu - p0, kPiece);
     __syncthreads();
-    for (int t = threadIdx.x; t < np; t += blockDim.x) ubl[t] = ub[p0 + t];
+    for (int t = threadIdx.x; t < np; t += blockDim.x) ubl[t] = ub[p0 + t] - pair_base;
     for (int t = threadIdx.x; t < np * 16; t += blockDim.x)
       Al[t] = ab[((int64_t)(p0 + t / 16) * H) * 16 + (t % 16)];
     __syncthreads();
@@ -447,12 +458,12 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
       }
     }
   }
-  // acc[4q+u][v] = S[receiver 4k+v][column (tg*NQ+q)*64 + 4j + u]
+  // acc[4q+u][v] = S[receiver 4k+v of the block][column (tg*NQ+q)*64 + 4j + u]
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const int r = b * 16 + 4 * k + v;
     if (r >= n) continue;
-    float4* srow = (float4*)(S + (int64_t)order[r] * W);
+    float4* srow = (float4*)(S + (int64_t)r * W);  // S rows follow the receiver order
 #pragma unroll
     for (int q = 0; q < NQ; ++q)
       if (col4[q] >= 0)
@@ -466,7 +477,7 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
 constexpr int kAggRecv = 4;
 constexpr int kAggChunk4 = 64;
 
-__global__ __launch_bounds__(64 * kAggRecv) void k_aggregate_rows(const float4* __restrict__ T,
+__global__ __launch_bounds__(64 * kAggRecv) void k_aggregate_rows(const float4* __restrict__ T, int pair_base,
                                                                   const int64_t* __restrict__ row_ptr,
                                                                   const int32_t* __restrict__ col_pair,
                                                                   const float* __restrict__ alpha,
@@ -488,13 +499,13 @@ __global__ __launch_bounds__(64 * kAggRecv) void k_aggregate_rows(const float4* 
 #pragma unroll 4
   for (int64_t e = e0; e < e1; ++e) {
     const float a = alpha ? alpha[e * H + head] : 1.0f;
-    const float4 v = T[(size_t)col_pair[e] * W4 + q];
+    const float4 v = T[(size_t)(col_pair[e] - pair_base) * W4 + q];
     acc.x += a * v.x;
     acc.y += a * v.y;
     acc.z += a * v.z;
     acc.w += a * v.w;
   }
-  S[(size_t)i * W4 + q] = acc;
+  S[(size_t)r * W4 + q] = acc;  // S rows follow the receiver order
 }
 
 // ------------------------------------------------------------ i-side recouple
@@ -506,17 +517,18 @@ __global__ __launch_bounds__(64 * kAggRecv) void k_aggregate_rows(const float4* 
 
 template <int L, int NTW>
 __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __restrict__ R,
-                                                  const float* __restrict__ S, int C, int dh, float* __restrict__ y) {
+                                                  const float* __restrict__ S, const int32_t* __restrict__ order,
+                                                  int C, int dh, float* __restrict__ y) {
   constexpr int NK = (L + 1) * (L + 1);
   constexpr int MT = (NK + 15) / 16;  // NTW: channel tiles per wave and pass
   __shared__ float Qt[kRcRows * 16 * MT];  // Qt[r][k]
   __shared__ double Rl[NK];
-  const int i = blockIdx.x;
+  const int i = order[blockIdx.x];  // S row blockIdx.x belongs to receiver i
   if (threadIdx.x < NK) Rl[threadIdx.x] = R[(size_t)i * NK + threadIdx.x];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int j = lane & 15, k4 = lane >> 4;
   const int dimT = t.dimT;
-  const float* Si = S + (size_t)i * dimT * C;
+  const float* Si = S + (size_t)blockIdx.x * dimT * C;
   const int NT = (C + 15) / 16;
   for (int ns = 0; ns < NT; ns += 4 * NTW) {
     v4f acc[NTW][MT];
@@ -781,6 +793,17 @@ hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* no
   return hipGetLastError();
 }
 
+hipError_t launch_tile_ranges(const int32_t* tile_of, const int32_t* pidx, int n, int keys, int32_t* counts,
+                              int32_t* rstart, int32_t* pstart, void* tmp, size_t tmp_bytes, hipStream_t s) {
+  hipError_t e = hipMemsetAsync(counts, 0, sizeof(int32_t) * (size_t)(keys + 1), s);
+  if (e != hipSuccess) return e;
+  if (n > 0) k_key_counts<<<(n + 255) / 256, 256, 0, s>>>(tile_of, n, counts);
+  size_t b = tmp_bytes;
+  if ((e = hipcub::DeviceScan::ExclusiveSum(tmp, b, counts, rstart, keys + 1, s)) != hipSuccess) return e;
+  k_key_pstart<<<(keys + 255) / 256, 256, 0, s>>>(pidx, keys, n, pstart);
+  return hipGetLastError();
+}
+
 size_t recv_sort_tmp_bytes(int n) {
   size_t b = 0;
   hipcub::DeviceRadixSort::SortPairs(nullptr, b, (const uint64_t*)nullptr, (uint64_t*)nullptr,
@@ -833,10 +856,10 @@ hipError_t launch_block_alpha(const int64_t* row_ptr, const int32_t* order, int 
   return hipGetLastError();
 }
 
-hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_t* col_pair, const float* alpha,
-                            const int32_t* order, const int32_t* uni, const int32_t* blk_off, const int32_t* uoff,
-                            const int32_t* ucount, const float* alpha_blk, bool use_blocks, int n, int dimT, int C,
-                            int H, float* S, hipStream_t s) {
+hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_ptr, const int32_t* col_pair,
+                            const float* alpha, const int32_t* order, const int32_t* uni, const int32_t* blk_off,
+                            const int32_t* uoff, const int32_t* ucount, const float* alpha_blk, bool use_blocks, int n,
+                            int dimT, int C, int H, float* S, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int dh = C / H;
   if (use_blocks) {
@@ -851,8 +874,8 @@ hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
 #define E2F_AGG(NQ_, U_)                                                                                   \
   if (nq == NQ_ && un == U_) {                                                                            \
-    k_aggregate_mfma<NQ_, U_><<<(unsigned)blocks, 256, 0, s>>>(T, order, uni, blk_off, uoff, ucount, alpha_blk, n, \
-                                                             nblk, bpx, ntg, ntg4, dimT, C, dh, H, S);     \
+    k_aggregate_mfma<NQ_, U_><<<(unsigned)blocks, 256, 0, s>>>(T, pair_base, uni, blk_off, uoff, ucount, alpha_blk, \
+                                                             n, nblk, bpx, ntg, ntg4, dimT, C, dh, H, S);  \
     return hipGetLastError();                                                                             \
   }
     E2F_AGG(2, 1) E2F_AGG(4, 1) E2F_AGG(6, 1) E2F_AGG(8, 1)
@@ -865,22 +888,23 @@ hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_
   const int gpx = (ngroups + kXcds - 1) / kXcds;
   const int64_t blocks = (int64_t)kXcds * gpx * nchunk;
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  k_aggregate_rows<<<(unsigned)blocks, 64 * kAggRecv, 0, s>>>((const float4*)T, row_ptr, col_pair, alpha, order, n,
+  k_aggregate_rows<<<(unsigned)blocks, 64 * kAggRecv, 0, s>>>((const float4*)T, pair_base, row_ptr, col_pair, alpha,
+                                                              order, n,
                                                               (int)W4, nchunk, ngroups, gpx, C, dh, H, (float4*)S);
   return hipGetLastError();
 }
 
-hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, int n, int C, int dh, float* y,
-                           hipStream_t s) {
+hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, const int32_t* order, int n, int C,
+                           int dh, float* y, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int nt = (C + 15) / 16;  // channel tiles; 4 waves
   const int ntw = nt <= 4 ? 1 : (nt <= 8 ? 2 : 4);
   switch (t.L) {
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
-    if (ntw == 1) k_recouple<LL, 1><<<n, 256, 0, s>>>(t, R, S, C, dh, y);                                   \
-    else if (ntw == 2) k_recouple<LL, 2><<<n, 256, 0, s>>>(t, R, S, C, dh, y);                              \
-    else k_recouple<LL, 4><<<n, 256, 0, s>>>(t, R, S, C, dh, y);                                            \
+    if (ntw == 1) k_recouple<LL, 1><<<n, 256, 0, s>>>(t, R, S, order, C, dh, y);                            \
+    else if (ntw == 2) k_recouple<LL, 2><<<n, 256, 0, s>>>(t, R, S, order, C, dh, y);                       \
+    else k_recouple<LL, 4><<<n, 256, 0, s>>>(t, R, S, order, C, dh, y);                                     \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
 #undef E2F_CASE

@@ -51,6 +51,10 @@ hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const
 // T stored head-major: T[item][c / dh][row][c % dh] (dh = C: plain [row][c])
 hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* node_of, const float* feat,
                           int n_items, int C, int dh, float* T, hipStream_t s);
+// receivers per tile key (counts [keys+1]), their first position in the
+// receiver order (rstart [keys+1]) and the first pair of each key (pstart [keys])
+hipError_t launch_tile_ranges(const int32_t* tile_of, const int32_t* pidx, int n, int keys, int32_t* counts,
+                              int32_t* rstart, int32_t* pstart, void* tmp, size_t tmp_bytes, hipStream_t s);
 size_t recv_sort_tmp_bytes(int n);
 // order = receivers sorted by (tile, Morton index of fine cells of side `fine` grid units)
 hipError_t launch_sort_receivers(const float* pos, const int32_t* tile_of, int n, const int* lo, int64_t fine,
@@ -71,13 +75,16 @@ hipError_t launch_block_union(const int64_t* row_ptr, const int32_t* col_pair, c
 hipError_t launch_block_alpha(const int64_t* row_ptr, const int32_t* order, int n, const int32_t* uoff,
                               const int32_t* edge_slot, const float* alpha, int H, int64_t union_rows,
                               float* alpha_blk, hipStream_t s);
-// use_blocks: MFMA form over the block plan; else per-receiver rows from L2.
-hipError_t launch_aggregate(const float* T, const int64_t* row_ptr, const int32_t* col_pair, const float* alpha,
-                            const int32_t* order, const int32_t* uni, const int32_t* blk_off, const int32_t* uoff,
-                            const int32_t* ucount, const float* alpha_blk, bool use_blocks, int n, int dimT, int C,
-                            int H, float* S, hipStream_t s);
-hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, int n, int C, int dh, float* y,
-                           hipStream_t s);
+// S[r] for the n receivers order[0..n) (S rows follow that order); T holds the
+// pairs from pair_base on.  use_blocks: MFMA form over the block plan (built
+// for the same n receivers); else per-receiver rows from L2.
+hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_ptr, const int32_t* col_pair,
+                            const float* alpha, const int32_t* order, const int32_t* uni, const int32_t* blk_off,
+                            const int32_t* uoff, const int32_t* ucount, const float* alpha_blk, bool use_blocks, int n,
+                            int dimT, int C, int H, float* S, hipStream_t s);
+// y[order[r]] from S row r (head-major like T), r < n
+hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, const int32_t* order, int n, int C,
+                           int dh, float* y, hipStream_t s);
 
 // ---- per-irrep channel mixing and the edge baseline
 hipError_t launch_mix(int L, const float* y, const void* W, bool w_bf16, int n, int C, float* out, hipStream_t s);

@@ -184,3 +184,36 @@ def test_determinism_and_translation(e2f, ctx):
     shifted = type(inp)(inp.pos + np.float32(37.5), inp.graph_id, inp.species, inp.feat, inp.mix_w, inp.path_w, wl)
     a3, b3 = run_both(e2f, ctx, shifted, rp, ci, alpha, wl.lmax, wl.heads, wl.cutoff)
     assert o.max_rel_err(a3, a1, wl.lmax) <= TOL_F32 and o.max_rel_err(b3, b1, wl.lmax) <= TOL_F32
+
+
+def test_conv_tile_batches(e2f, ctx, monkeypatch):
+    # small tiles and a tiny memory budget force many tiles and several batches
+    inp, rp, ci, alpha = case("water2000_L4")
+    wl = inp.workload
+    r = sample_rows(inp.pos.shape[0], 64, seed=3)
+    ref = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, inp.mix_w, rows=r)
+    monkeypatch.setenv("E2F_TILE_BUDGET_MB", "150")
+    y6, _ = run_both(e2f, ctx, inp, rp, ci, alpha, wl.lmax, wl.heads, wl.cutoff, mix=inp.mix_w, tile_side=10.0)
+    pairs, tiles = e2f.e2f_last_plan(ctx)
+    assert tiles == 27 and pairs > inp.pos.shape[0]
+    err = o.max_rel_err(y6[r], ref, wl.lmax)
+    print("water2000 in batches of 10 A tiles: err %.3e" % err)
+    assert err <= TOL_F32
+
+
+def test_conv_stress_200k_sampled(e2f, ctx):
+    # 200,000 atoms, cutoff 8 A, L = 6, C = 64: the factorised path only, checked
+    # on sampled receiver rows (the definition is separable per row)
+    inp, rp, ci, alpha = case("stress200k_L6")
+    wl = inp.workload
+    pos, feat = gpu(inp.pos), gpu(inp.feat)
+    g_rp, g_ci = e2f.e2f_neighbor_list(ctx, pos, wl.cutoff)
+    assert torch.equal(g_rp.cpu(), torch.from_numpy(rp)) and torch.equal(g_ci.cpu(), torch.from_numpy(ci))
+    out = e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, g_rp, g_ci, gpu(alpha), wl.lmax, wl.heads, wl.cutoff,
+                                        mix_w=gpu(inp.mix_w))
+    torch.cuda.synchronize()
+    r = sample_rows(inp.pos.shape[0], 24, seed=5)
+    ref = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, inp.mix_w, rows=r)
+    err = o.max_rel_err(out.cpu().numpy()[r], ref, wl.lmax)
+    print("stress200k: %d edges, err %.3e" % (len(ci), err))
+    assert err <= TOL_F32
