@@ -56,6 +56,84 @@ def file_sha(path):
         return hashlib.sha256(f.read()).hexdigest()
 
 
+def central_crop(pos, side):
+    """Atoms inside the central cube of the given side (re-indexed)."""
+    lo, hi = pos.min(0), pos.max(0)
+    c = (lo + hi) / 2
+    keep = np.all(np.abs(pos - c) < side / 2, axis=1)
+    return np.nonzero(keep)[0]
+
+
+def sweep_one(name, steps, warmup):
+    """6j forward and edge-TP baseline on one workload (the 200k-atom system's
+    baseline runs on its central 58.48 A crop, with the 6j path timed there too)."""
+    import torch
+    import e2f_synth as syn
+    import paper_2501_19216_amd as e2f
+
+    wl = syn.WORKLOADS[name]
+    inp = syn.make_inputs(wl)
+    dev = torch.device("cuda:0")
+    ctx = e2f.e2f_create(wl.lmax, 0)
+
+    def setup(idx):
+        pos_h = inp.pos if idx is None else np.ascontiguousarray(inp.pos[idx])
+        feat_h = inp.feat if idx is None else np.ascontiguousarray(inp.feat[idx])
+        gid_h = inp.graph_id if (inp.graph_id is None or idx is None) else inp.graph_id[idx]
+        spc = inp.species if idx is None else inp.species[idx]
+        pos = torch.from_numpy(pos_h).to(dev)
+        gid = None if gid_h is None else torch.from_numpy(np.ascontiguousarray(gid_h)).to(dev)
+        rp, ci = e2f.e2f_neighbor_list(ctx, pos, wl.cutoff, gid)
+        al = syn.attention_weights(pos_h, spc, rp.cpu().numpy(), ci.cpu().numpy(), wl.heads, wl.cutoff, wl.species,
+                                   wl.seed)
+        return pos, torch.from_numpy(feat_h).to(dev), gid, rp, ci, torch.from_numpy(al).to(dev)
+
+    mix_w = torch.from_numpy(inp.mix_w).to(dev)
+
+    def time_fn(fn, k):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(k):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / k
+
+    res = {"workload": name, "lmax": wl.lmax, "channels": wl.channels, "heads": wl.heads, "cutoff": wl.cutoff}
+    pos, feat, gid, rp, ci, al = setup(None)
+    out = torch.empty_like(feat)
+    n, E = feat.shape[0], ci.numel()
+    k6 = max(2, steps // 4) if n > 50000 else steps
+    f6 = lambda: e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, rp, ci, al, wl.lmax, wl.heads, wl.cutoff,
+                                               mix_w=mix_w, graph_id=gid, out=out)
+    e2f.e2f_profile(ctx, True)
+    ms6 = time_fn(f6, k6)
+    prof = e2f.e2f_profile_read(ctx)
+    e2f.e2f_profile(ctx, False)
+    pairs, tiles = e2f.e2f_last_plan(ctx)
+    res.update(atoms=n, edges=E, pairs=pairs, tiles=tiles, fwd_ms=ms6, atoms_per_s=n / ms6 * 1e3,
+               edges_per_s=E / ms6 * 1e3,
+               kernels_ms={k: v[1] / (warmup + k6) for k, v in prof.items()})
+    if n > 50000:
+        idx = central_crop(inp.pos, syn._cube_side(20000))
+        del out
+        pos, feat, gid, rp, ci, al = setup(idx)
+        out = torch.empty_like(feat)
+        res["crop"] = {"atoms": feat.shape[0], "edges": ci.numel()}
+        res["crop"]["fwd_ms"] = time_fn(lambda: e2f.e2f_wigner6j_conv_forward(
+            ctx, pos, feat, rp, ci, al, wl.lmax, wl.heads, wl.cutoff, mix_w=mix_w, graph_id=gid, out=out), steps)
+        base = res["crop"]
+    else:
+        base = res
+    oute = torch.empty_like(feat)
+    base["edge_tp_ms"] = time_fn(lambda: e2f.e2f_edge_tp_conv_forward(
+        ctx, pos, feat, rp, ci, al, wl.lmax, wl.heads, wl.cutoff, mix_w=mix_w, out=oute), steps)
+    base["speedup_vs_edge_tp"] = base["edge_tp_ms"] / base["fwd_ms"]
+    ctx.close()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -65,6 +143,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-rows", type=int, default=6144)
     ap.add_argument("--copy-calib", action="store_true", help="also run a 1 GiB device copy (counter calibration)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead: one JSON line per workload (6j forward and edge-TP baseline times and speedup)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (no sharding, no collectives).",
@@ -74,6 +154,11 @@ def main():
     import torch
     import e2f_synth as syn
     import paper_2501_19216_amd as e2f
+
+    if args.sweep:
+        for name in syn.WORKLOADS:
+            print(json.dumps(sweep_one(name, args.steps, args.warmup)), flush=True)
+        return
 
     wl = syn.WORKLOADS[args.workload]
     inp = syn.make_inputs(wl)
