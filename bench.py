@@ -31,8 +31,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "Wigner-6j conv fwd atoms/s + edges/s at Lmax=4, C=128; speedup vs edge-TP"
-HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
-FP32_VECTOR_PEAK_TFS = 157.3  # MI355X fp32 vector (packed) peak
+HBM_PEAK_GBS = 8000.0         # MI355X HBM3E
+FP32_MFMA_PEAK_TFS = 157.3    # MI355X dense fp32 MFMA
+BF16_MFMA_PEAK_TFS = 2500.0   # MI355X dense bf16 MFMA
 
 
 def tri(a, b, c):
@@ -236,30 +237,58 @@ def main():
         "recouple": dict(bytes=4.0 * C * n * (dimT + (L + 1) ** 2), flops=2.0 * n * cnt["q_slots"] * C),
         "mix": dict(bytes=8.0 * n * (L + 1) ** 2 * C + 4.0 * (L + 1) * C * C, flops=2.0 * n * (L + 1) ** 2 * C * C),
     }
+    peaks = {k: FP32_MFMA_PEAK_TFS for k in alg}  # all four run on fp32 MFMA
+
+    def roof_of(bytes_, flops, t_ms, peak_tf):
+        """Roofline position of one launch: the binding resource is the one
+        whose lower-bound time is larger."""
+        t_b, t_f = bytes_ / (HBM_PEAK_GBS * 1e9), flops / (peak_tf * 1e12)
+        if t_b >= t_f:
+            a = bytes_ / (t_ms * 1e-3) / 1e9
+            return dict(bound="hbm", achieved=a, peak=HBM_PEAK_GBS, unit="GB/s", frac=a / HBM_PEAK_GBS)
+        a = flops / (t_ms * 1e-3) / 1e12
+        return dict(bound="mfma", achieved=a, peak=peak_tf, unit="TFLOP/s", frac=a / peak_tf)
+
+    for k, v in kernels.items():
+        if k in alg:
+            tk = v["ms"] / max(1, v["launches"])
+            v["alg_GBps"] = alg[k]["bytes"] / (tk * 1e-3) / 1e9
+            v["alg_TFLOPs"] = alg[k]["flops"] / (tk * 1e-3) / 1e12
+            r = roof_of(alg[k]["bytes"], alg[k]["flops"], tk, peaks[k])
+            v["bound"], v["frac"] = r["bound"], r["frac"]
     dom = max((k for k in kernels if k in alg), key=lambda k: kernels[k]["ms"])
     t_dom = kernels[dom]["ms"] / max(1, kernels[dom]["launches"])
-    ai = alg[dom]["flops"] / alg[dom]["bytes"]
-    ridge = FP32_VECTOR_PEAK_TFS * 1e12 / (HBM_PEAK_GBS * 1e9)
-    if ai < ridge:
-        achieved = alg[dom]["bytes"] / (t_dom * 1e-3) / 1e9
-        roof = dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s", frac=achieved / HBM_PEAK_GBS)
-    else:
-        achieved = alg[dom]["flops"] / (t_dom * 1e-3) / 1e12
-        roof = dict(bound="alu", achieved=achieved, peak=FP32_VECTOR_PEAK_TFS, unit="TFLOP/s",
-                    frac=achieved / FP32_VECTOR_PEAK_TFS)
-    roof["kernel"] = dom
+    roof = roof_of(alg[dom]["bytes"], alg[dom]["flops"], t_dom, peaks[dom])
     roof["traffic"] = None
+    roof["kernel"] = dom
     tr_path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (dom, wl.name))
     if os.path.exists(tr_path):
         tr = json.load(open(tr_path))
         src = os.path.join(ROOT, "paper_2501_19216_amd", "csrc", "conv.hip")
         if tr.get("conv_sha256") == file_sha(src):
             roof["traffic"] = tr["bytes_per_launch"]
-    for k, v in kernels.items():
-        if k in alg:
-            tk = v["ms"] / max(1, v["launches"]) * 1e-3
-            v["alg_GBps"] = alg[k]["bytes"] / tk / 1e9
-            v["alg_TFLOPs"] = alg[k]["flops"] / tk / 1e12
+
+    # ---- the bf16 channel-mixing variant of the same forward
+    mix_bf16 = mix_w.to(torch.bfloat16)
+
+    def fwd_bf16():
+        e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col, alpha, L, H, wl.cutoff, mix_w=mix_bf16,
+                                      graph_id=gid, out=out)
+
+    for _ in range(2):
+        fwd_bf16()
+    e2f.e2f_profile(ctx, True)
+    ms_fwd_bf16 = timed(fwd_bf16, args.steps)
+    prof16 = e2f.e2f_profile_read(ctx)
+    e2f.e2f_profile(ctx, False)
+    mix16_ms = prof16["mix"][1] / prof16["mix"][0] if "mix" in prof16 else None
+    bf16_res = {"ms": ms_fwd_bf16, "atoms_per_s": n / (ms_fwd_bf16 * 1e-3), "mix_ms": mix16_ms}
+    if mix16_ms:
+        mb = 8.0 * n * (L + 1) ** 2 * C + 2.0 * (L + 1) * C * C
+        r = roof_of(mb, alg["mix"]["flops"], mix16_ms, BF16_MFMA_PEAK_TFS)
+        bf16_res.update(mix_alg_GBps=mb / (mix16_ms * 1e-3) / 1e9,
+                        mix_alg_TFLOPs=alg["mix"]["flops"] / (mix16_ms * 1e-3) / 1e12,
+                        mix_bound=r["bound"], mix_frac=r["frac"])
 
     if args.copy_calib:
         x = torch.empty(1 << 28, dtype=torch.float32, device=dev)
@@ -304,6 +333,7 @@ def main():
         "fwd": {"ms": ms_fwd, "atoms_per_s": n / (ms_fwd * 1e-3), "edges_per_s": E / (ms_fwd * 1e-3)},
         "edge_tp": {"ms": ms_edge, "atoms_per_s": n / (ms_edge * 1e-3), "edges_per_s": E / (ms_edge * 1e-3)},
         "speedup_vs_edge_tp": ms_edge / ms_fwd,
+        "fwd_bf16_mix": bf16_res,
         "neighbor_list_ms": ms_nl,
         "kernels": kernels,
         "roofline": roof,

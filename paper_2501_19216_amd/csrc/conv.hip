@@ -644,6 +644,93 @@ __global__ __launch_bounds__(256) void k_mix(const float* __restrict__ y, const 
   }
 }
 
+// MFMA channel mixing, used when C is a multiple of 16 up to 128.
+// One workgroup of kMixWaves waves holds W^(o) in LDS (padded rows, so the
+// 16-byte operand reads of 16 consecutive lanes hit distinct banks) and
+// streams kMixGroups groups of 16*kMixWaves rows of irrep o. Each wave takes
+// 16 rows and loads them once into registers as the B operand: lane (j, q)
+// holds row j, channels 16s+4q..16s+4q+3. W^(o) rows are the A operand, read
+// from LDS for every 16-channel output block; the reduction visits channel
+// 16s+4q+u at step (s, u) on both operands. fp32: v_mfma_f32_16x16x4f32;
+// bf16: y rounded to bf16 (nearest even) and v_mfma_f32_16x16x16bf16_1k,
+// fp32 accumulation either way.
+typedef short v4s __attribute__((ext_vector_type(4)));
+struct MixGrid {
+  int wg_start[kMaxL + 2];  // first workgroup of each irrep o, and the total
+};
+constexpr int kMixWaves = 8;
+constexpr int kMixGroups = 4;
+constexpr int kMixRowsPerWg = 16 * kMixWaves * kMixGroups;
+
+__device__ __forceinline__ short bf16_bits(float x) {
+  return (short)__bfloat16_as_ushort(__float2bfloat16(x));
+}
+
+template <bool BF16, int C16>
+__global__ __launch_bounds__(64 * kMixWaves) void k_mix_mfma(const float* __restrict__ y, const void* __restrict__ Wv,
+                                                            int n, int nk, int L, MixGrid g,
+                                                            float* __restrict__ out) {
+  constexpr int C = 16 * C16;
+  constexpr int WS = BF16 ? C + 8 : C + 4;  // LDS row stride in elements
+  extern __shared__ float mix_lds[];
+  int o = 0;
+  while (o < L && (int)blockIdx.x >= g.wg_start[o + 1]) ++o;
+  const int nm = 2 * o + 1;
+  const int64_t rows = (int64_t)n * nm;
+  if (BF16) {
+    uint16_t* Wl = (uint16_t*)mix_lds;
+    const uint16_t* W = (const uint16_t*)Wv + (size_t)o * C * C;
+    for (int q = threadIdx.x; q < C * C; q += blockDim.x) Wl[(q / C) * WS + q % C] = W[q];
+  } else {
+    const float* W = (const float*)Wv + (size_t)o * C * C;
+    for (int q = threadIdx.x; q < C * C; q += blockDim.x) mix_lds[(q / C) * WS + q % C] = W[q];
+  }
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int j = lane & 15, q4 = lane >> 4;
+  const int64_t first = (int64_t)(blockIdx.x - g.wg_start[o]) * kMixRowsPerWg;
+  for (int gi = 0; gi < kMixGroups; ++gi) {
+    const int64_t r0 = first + (int64_t)(gi * kMixWaves + wave) * 16;
+    if (r0 >= rows) break;  // uniform over the wave
+    const int64_t r = r0 + j;
+    const bool valid = r < rows;
+    int64_t base = 0;
+    if (valid) {
+      const int64_t i = r / nm;
+      base = (i * nk + o * o + (r - i * nm)) * C;
+    }
+    float4 yv[C16];
+#pragma unroll
+    for (int s = 0; s < C16; ++s)
+      yv[s] = valid ? *(const float4*)(y + base + 16 * s + 4 * q4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    v4s yb[BF16 ? C16 : 1];
+    if (BF16) {
+#pragma unroll
+      for (int s = 0; s < C16; ++s)
+        yb[s] = (v4s){bf16_bits(yv[s].x), bf16_bits(yv[s].y), bf16_bits(yv[s].z), bf16_bits(yv[s].w)};
+    }
+#pragma unroll 2
+    for (int cb = 0; cb < C16; ++cb) {
+      v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < C16; ++s) {
+        if (BF16) {
+          const v4s a = *(const v4s*)((const uint16_t*)mix_lds + (cb * 16 + j) * WS + 16 * s + 4 * q4);
+          acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, yb[s], acc, 0, 0, 0);
+        } else {
+          const float4 a = *(const float4*)(mix_lds + (cb * 16 + j) * WS + 16 * s + 4 * q4);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, yv[s].x, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, yv[s].y, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, yv[s].z, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, yv[s].w, acc, 0, 0, 0);
+        }
+      }
+      // acc[v] = out[row j][16cb + 4q + v]
+      if (valid) *(float4*)(out + base + 16 * cb + 4 * q4) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    }
+  }
+}
+
 // ------------------------------------------------------------ edge baseline
 // Per receiver block: edges in batches of EB; for each edge the filter
 // K[k][q] = sum_f w_afo sum_mf C^{o m}_{a al, f mf} R^(f)_mf(r_i - r_j) is built
@@ -916,6 +1003,29 @@ hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, 
 hipError_t launch_mix(int L, const float* y, const void* W, bool w_bf16, int n, int C, float* out, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int nk = (L + 1) * (L + 1);
+  if (C % 16 == 0 && C <= 128) {
+    MixGrid g{};
+    for (int o = 0; o <= L; ++o) {
+      const int64_t wgs = ((int64_t)n * (2 * o + 1) + kMixRowsPerWg - 1) / kMixRowsPerWg;
+      if ((int64_t)g.wg_start[o] + wgs > 0x7fffffff) return hipErrorInvalidValue;
+      g.wg_start[o + 1] = g.wg_start[o] + (int)wgs;
+    }
+    const int C16 = C / 16;
+    const size_t lds = (size_t)C * (w_bf16 ? (C + 8) * 2 : (C + 4) * 4);
+#define E2F_MIX(B_, C16_)                                                                                    \
+  if (w_bf16 == B_ && C16 == C16_) {                                                                         \
+    if (hipError_t e = allow_lds(k_mix_mfma<B_, C16_>, lds); e != hipSuccess) return e;                      \
+    k_mix_mfma<B_, C16_><<<g.wg_start[L + 1], 64 * kMixWaves, lds, s>>>(y, W, n, nk, L, g, out);             \
+    return hipGetLastError();                                                                                \
+  }
+    E2F_MIX(false, 1) E2F_MIX(false, 2) E2F_MIX(false, 3) E2F_MIX(false, 4)
+    E2F_MIX(false, 5) E2F_MIX(false, 6) E2F_MIX(false, 7) E2F_MIX(false, 8)
+    E2F_MIX(true, 1) E2F_MIX(true, 2) E2F_MIX(true, 3) E2F_MIX(true, 4)
+    E2F_MIX(true, 5) E2F_MIX(true, 6) E2F_MIX(true, 7) E2F_MIX(true, 8)
+#undef E2F_MIX
+    return hipErrorInvalidValue;
+  }
+  // other channel counts: tiled VALU GEMM per irrep
   for (int o = 0; o <= L; ++o) {
     const int64_t rows = (int64_t)n * (2 * o + 1);
     dim3 grid((unsigned)((rows + 63) / 64), (unsigned)((C + 63) / 64));

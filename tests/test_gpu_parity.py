@@ -150,6 +150,18 @@ def test_conv_parity_protein_fp32_and_bf16(e2f, ctx):
     assert e6 <= TOL_BF16 and ee <= TOL_BF16
 
 
+def test_conv_parity_bf16_mix_c64(e2f, ctx):
+    # bf16 channel mixing at 64 channels (MFMA bf16 path, 4 channel blocks)
+    inp, rp, ci, alpha = case("molecules256x30_L3")
+    wl = inp.workload
+    r = sample_rows(inp.pos.shape[0], 256, seed=3)
+    ref = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, inp.mix_w, rows=r)
+    y6, ye = run_both(e2f, ctx, inp, rp, ci, alpha, wl.lmax, wl.heads, wl.cutoff, mix=inp.mix_w, mix_bf16=True)
+    e6, ee = o.max_rel_err(y6[r], ref, wl.lmax), o.max_rel_err(ye[r], ref, wl.lmax)
+    print("molecules bf16 mix: 6j err %.3e  edge err %.3e" % (e6, ee))
+    assert e6 <= TOL_BF16 and ee <= TOL_BF16
+
+
 def test_conv_edge_cases(e2f, ctx):
     rng = np.random.default_rng(12)
     # ragged sizes, L = 0, isolated atoms, explicit path weights, no alpha
