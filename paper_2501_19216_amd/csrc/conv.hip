@@ -395,7 +395,7 @@ __global__ void k_block_alpha(const int64_t* __restrict__ row_ptr, const int32_t
 constexpr int kXcds = 8;
 constexpr int kPiece = 512;  // union rows staged in LDS at a time
 
-template <int NQ, int UNROLL>
+template <int NQ>
 __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict__ T, int pair_base,
                                                         const int32_t* __restrict__ uni,
                                                         const int32_t* __restrict__ blk_off,
@@ -405,7 +405,11 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
                                                         int ntg, int ntg4, int dimT, int C, int dh, int H,
                                                         float* __restrict__ S) {
   __shared__ int32_t ubl[kPiece];
-  __shared__ float Al[kPiece * 16];  // Al[slot][receiver]: A operand of head h
+  __shared__ float4 Al4[kPiece * 4];  // Al[slot][receiver]: A operand of head h
+  const float* Al = (const float*)Al4;
+  // workgroup = (block b, column task); the blocks of one XCD are contiguous
+  // in space and the column tasks are the slow index, so the workgroups in
+  // flight on an XCD share T rows through its L2
   const int bid = blockIdx.x;
   const int xcd = bid % kXcds, local = bid / kXcds;
   const int b = xcd * bpx + local % bpx;
@@ -415,59 +419,102 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
   const int tg = (wtask % ntg4) * 4 + (int)(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int j = lane & 15, k = lane >> 4;
-  const int64_t W = (int64_t)dimT * C;
+  const int64_t W4 = (int64_t)dimT * C / 4;
   const int hcols = dimT * dh;
   // MFMA group g = 4q + u reads column m = (tg*NQ + q)*64 + 4j + u of head h,
-  // so lane j loads the float4 at 4j covering its four groups.
+  // so lane j loads the float4 at 4j covering its four groups.  Columns past
+  // the head's end load column 0 of the head instead (never stored).
   constexpr int kAggGroups = 4 * NQ;
-  int64_t col4[NQ];
+  int c4[NQ];
+  bool cvalid[NQ];
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     const int m0 = (tg * NQ + q) * 64 + 4 * j;
-    col4[q] = (tg < ntg && m0 < hcols) ? (int64_t)h * hcols + m0 : -1;
+    cvalid[q] = tg < ntg && m0 < hcols;
+    c4[q] = (h * hcols + (cvalid[q] ? m0 : 0)) / 4;
   }
   v4f acc[kAggGroups];
 #pragma unroll
   for (int g = 0; g < kAggGroups; ++g) acc[g] = (v4f){0.f, 0.f, 0.f, 0.f};
   const int nu = ucount[b];
   const int32_t* ub = uni + blk_off[b];
-  const float* ab = alpha_blk + ((int64_t)uoff[b] * H + h) * 16;
+  const float4* ab4 = (const float4*)(alpha_blk + ((int64_t)uoff[b] * H + h) * 16);
+  const float4* T4 = (const float4*)T;
+  const bool active = tg < ntg;  // uniform over the wave
+  // Union rows 4 at a time (lane row k); rows past the piece take weight 0
+  // and re-read the piece's first row.  Two register stages: the loads of
+  // one step are in flight while the MFMAs of the previous one run.
+  float4 b0[NQ], b1[NQ];
+  float a0 = 0.f, a1 = 0.f;
+  auto load = [&](int s0, int np, float4* bv, float& a) {
+    const int sl = s0 + k;
+    const bool valid = sl < np;
+    a = valid ? Al[sl * 16 + j] : 0.0f;
+    const float4* trow = T4 + (int64_t)ubl[valid ? sl : 0] * W4;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) bv[q] = trow[c4[q]];
+  };
+  auto mma = [&](const float4* bv, float a) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      acc[4 * q + 0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].x, acc[4 * q + 0], 0, 0, 0);
+      acc[4 * q + 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].y, acc[4 * q + 1], 0, 0, 0);
+      acc[4 * q + 2] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].z, acc[4 * q + 2], 0, 0, 0);
+      acc[4 * q + 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].w, acc[4 * q + 3], 0, 0, 0);
+    }
+  };
   for (int p0 = 0; p0 < nu; p0 += kPiece) {
     const int np = min(nu - p0, kPiece);
-    __syncthreads();
-    for (int t = threadIdx.x; t < np; t += blockDim.x) ubl[t] = ub[p0 + t] - pair_base;
-    for (int t = threadIdx.x; t < np * 16; t += blockDim.x)
-      Al[t] = ab[((int64_t)(p0 + t / 16) * H) * 16 + (t % 16)];
-    __syncthreads();
-#pragma unroll UNROLL
-    for (int s0 = 0; s0 < np; s0 += 4) {
-      const int s = s0 + k;
-      const bool valid = s < np;
-      const float a = valid ? Al[s * 16 + j] : 0.0f;
-      const float4* trow = (const float4*)(T + (int64_t)(valid ? ubl[s] : 0) * W);
-      float4 bv[NQ];
+    // staging: each thread issues its loads before its stores (clamped
+    // indexes, so there is no branch between them)
+    {
+      static_assert(kPiece == 2 * 256, "staging assumes 256 threads");
+      __syncthreads();
+      const int t = threadIdx.x;
+      const int32_t u0 = ub[p0 + min(t, np - 1)], u1 = ub[p0 + min(t + 256, np - 1)];
+      if (t < np) ubl[t] = u0 - pair_base;
+      if (t + 256 < np) ubl[t + 256] = u1 - pair_base;
 #pragma unroll
-      for (int q = 0; q < NQ; ++q)
-        bv[q] = (valid && col4[q] >= 0) ? trow[col4[q] / 4] : make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int half = 0; half < 2; ++half) {
+        float4 v[4];
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        acc[4 * q + 0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].x, acc[4 * q + 0], 0, 0, 0);
-        acc[4 * q + 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].y, acc[4 * q + 1], 0, 0, 0);
-        acc[4 * q + 2] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].z, acc[4 * q + 2], 0, 0, 0);
-        acc[4 * q + 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[q].w, acc[4 * q + 3], 0, 0, 0);
+        for (int u = 0; u < 4; ++u) {
+          const int q = min(t + 256 * (4 * half + u), 4 * np - 1);
+          v[u] = ab4[(int64_t)(p0 + q / 4) * H * 4 + q % 4];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (t + 256 * (4 * half + u) < 4 * np) Al4[t + 256 * (4 * half + u)] = v[u];
       }
+      __syncthreads();
+    }
+    if (!active) continue;  // no barrier below
+    // Steps of 4 rows in pairs (an odd count ends with a zero-weight step);
+    // the body has no branch, so each wait covers only the older stage, and
+    // sched_barrier keeps the scheduler from sinking a prefetch to its use.
+    const int npair = (np + 7) / 8;
+    load(0, np, b0, a0);
+    for (int it = 0; it < npair; ++it) {
+      load(8 * it + 4, np, b1, a1);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(b0, a0);
+      __builtin_amdgcn_sched_barrier(0);
+      load(8 * it + 8, np, b0, a0);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(b1, a1);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
+  if (!active) return;
   // acc[4q+u][v] = S[receiver 4k+v of the block][column (tg*NQ+q)*64 + 4j + u]
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const int r = b * 16 + 4 * k + v;
     if (r >= n) continue;
-    float4* srow = (float4*)(S + (int64_t)r * W);  // S rows follow the receiver order
+    float4* srow = (float4*)S + (int64_t)r * W4;  // S rows follow the receiver order
 #pragma unroll
     for (int q = 0; q < NQ; ++q)
-      if (col4[q] >= 0)
-        srow[col4[q] / 4] = make_float4(acc[4 * q][v], acc[4 * q + 1][v], acc[4 * q + 2][v], acc[4 * q + 3][v]);
+      if (cvalid[q]) srow[c4[q]] = make_float4(acc[4 * q][v], acc[4 * q + 1][v], acc[4 * q + 2][v], acc[4 * q + 3][v]);
   }
 }
 
@@ -521,7 +568,9 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
                                                   int C, int dh, float* __restrict__ y) {
   constexpr int NK = (L + 1) * (L + 1);
   constexpr int MT = (NK + 15) / 16;  // NTW: channel tiles per wave and pass
-  __shared__ float Qt[kRcRows * 16 * MT];  // Qt[r][k]
+  constexpr int QS = rc_qstride(NK);
+  constexpr int ST = 8;                // 4-row steps per pipeline stage
+  extern __shared__ float Qt[];        // Qt[r][k], kRcRows rows of QS floats
   __shared__ double Rl[NK];
   const int i = order[blockIdx.x];  // S row blockIdx.x belongs to receiver i
   if (threadIdx.x < NK) Rl[threadIdx.x] = R[(size_t)i * NK + threadIdx.x];
@@ -531,6 +580,17 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
   const float* Si = S + (size_t)blockIdx.x * dimT * C;
   const int NT = (C + 15) / 16;
   for (int ns = 0; ns < NT; ns += 4 * NTW) {
+    // B operand: lane (j, k4) reads channel c(q) of row 4s + k4; channels
+    // past C read channel 0 (never stored)
+    const float* sb[NTW];
+    bool cok[NTW];
+#pragma unroll
+    for (int q = 0; q < NTW; ++q) {
+      const int c = (ns + wave + 4 * q) * 16 + j;
+      cok[q] = c < C;
+      const int cc = cok[q] ? c : 0;
+      sb[q] = Si + (size_t)(cc / dh) * dimT * dh + cc % dh;
+    }
     v4f acc[NTW][MT];
 #pragma unroll
     for (int q = 0; q < NTW; ++q)
@@ -539,34 +599,58 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
     for (int r0 = 0; r0 < dimT; r0 += kRcRows) {
       const int rc = min(kRcRows, dimT - r0);
       __syncthreads();
-      for (int q = threadIdx.x; q < kRcRows * 16 * MT; q += blockDim.x) Qt[q] = 0.0f;
+      for (int q = threadIdx.x; q < kRcRows * QS; q += blockDim.x) Qt[q] = 0.0f;
       __syncthreads();
       const int ch = r0 / kRcRows;
       run_schedule(t.rc_meta + t.rc_off[ch], t.rc_coef + t.rc_off[ch], t.rc_k[ch], Rl, Qt);
       __syncthreads();
-#pragma unroll 8
-      for (int kk = 0; kk < rc; kk += 4) {
-        const int rl = kk + k4;
-        float a[MT];
+      // Stages of ST steps in pairs; rows past the chunk read its last row
+      // and take Q = 0.  No branch in the body, so each wait covers only the
+      // older stage; sched_barrier keeps a prefetch from sinking to its use.
+      float bA[ST][NTW], bB[ST][NTW];
+      auto load = [&](int stg, float (*bv)[NTW]) {
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) a[mt] = Qt[rl * 16 * MT + mt * 16 + j];
+        for (int u = 0; u < ST; ++u) {
+          const int rl = min((stg * ST + u) * 4 + k4, rc - 1);
 #pragma unroll
-        for (int q = 0; q < NTW; ++q) {
-          const int nt = ns + wave + 4 * q;
-          const int c = nt * 16 + j;
-          const float b = (rl < rc && nt < NT && c < C)
-                              ? Si[(size_t)(c / dh) * dimT * dh + (size_t)(r0 + rl) * dh + c % dh]
-                              : 0.0f;
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) acc[q][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], b, acc[q][mt], 0, 0, 0);
+          for (int q = 0; q < NTW; ++q) bv[u][q] = sb[q][(size_t)(r0 + rl) * dh];
         }
+      };
+      auto mma = [&](int stg, float (*bv)[NTW]) {
+#pragma unroll
+        for (int u = 0; u < ST; ++u) {
+          const int rl = (stg * ST + u) * 4 + k4;
+          const int rq = min(rl, kRcRows - 1);
+          float a[MT];
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const float qv = Qt[rq * QS + mt * 16 + j];
+            a[mt] = rl < rc ? qv : 0.0f;
+          }
+#pragma unroll
+          for (int q = 0; q < NTW; ++q)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+              acc[q][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv[u][q], acc[q][mt], 0, 0, 0);
+        }
+      };
+      const int nstage = (rc + 4 * ST - 1) / (4 * ST);
+      load(0, bA);
+      for (int sp = 0; sp < nstage; sp += 2) {
+        load(sp + 1, bB);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(sp, bA);
+        __builtin_amdgcn_sched_barrier(0);
+        load(sp + 2, bA);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(sp + 1, bB);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
 #pragma unroll
     for (int q = 0; q < NTW; ++q) {
-      const int nt = ns + wave + 4 * q;
-      const int c = nt * 16 + j;
-      if (nt >= NT || c >= C) continue;
+      const int c = (ns + wave + 4 * q) * 16 + j;
+      if (!cok[q]) continue;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -950,22 +1034,22 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
   if (n == 0) return hipSuccess;
   const int dh = C / H;
   if (use_blocks) {
-    // columns per wave (64*NQ) and slot-loop unroll; E2F_AGG_CFG="NQ,UNROLL" overrides (tuning)
-    int nq = 6, un = 1;
-    if (const char* cfg = getenv("E2F_AGG_CFG")) sscanf(cfg, "%d,%d", &nq, &un);
+    // columns per wave: 64*NQ; E2F_AGG_NQ overrides (tuning)
+    int nq = 2;
+    if (const char* cfg = getenv("E2F_AGG_NQ")) nq = atoi(cfg);
     const int nblk = (n + 15) / 16;
     const int ntg = (dimT * dh + 64 * nq - 1) / (64 * nq);
     const int ntg4 = (ntg + 3) / 4;
     const int bpx = (nblk + kXcds - 1) / kXcds;
     const int64_t blocks = (int64_t)kXcds * bpx * H * ntg4;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-#define E2F_AGG(NQ_, U_)                                                                                   \
-  if (nq == NQ_ && un == U_) {                                                                            \
-    k_aggregate_mfma<NQ_, U_><<<(unsigned)blocks, 256, 0, s>>>(T, pair_base, uni, blk_off, uoff, ucount, alpha_blk, \
-                                                             n, nblk, bpx, ntg, ntg4, dimT, C, dh, H, S);  \
+#define E2F_AGG(NQ_)                                                                                       \
+  if (nq == NQ_) {                                                                                        \
+    k_aggregate_mfma<NQ_><<<(unsigned)blocks, 256, 0, s>>>(T, pair_base, uni, blk_off, uoff, ucount, alpha_blk, \
+                                                         n, nblk, bpx, ntg, ntg4, dimT, C, dh, H, S);      \
     return hipGetLastError();                                                                             \
   }
-    E2F_AGG(2, 1) E2F_AGG(4, 1) E2F_AGG(6, 1) E2F_AGG(8, 1)
+    E2F_AGG(2) E2F_AGG(4) E2F_AGG(6) E2F_AGG(8)
 #undef E2F_AGG
     return hipErrorInvalidValue;
   }
@@ -986,15 +1070,20 @@ hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, 
   if (n == 0) return hipSuccess;
   const int nt = (C + 15) / 16;  // channel tiles; 4 waves
   const int ntw = nt <= 4 ? 1 : (nt <= 8 ? 2 : 4);
+  const size_t lds = sizeof(float) * (size_t)kRcRows * rc_qstride(t.nk);
   switch (t.L) {
+#define E2F_RC(LL, W)                                                                                       \
+  if (ntw == W) {                                                                                           \
+    if (hipError_t e = allow_lds(k_recouple<LL, W>, lds); e != hipSuccess) return e;                        \
+    k_recouple<LL, W><<<n, 256, lds, s>>>(t, R, S, order, C, dh, y);                                        \
+  }
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
-    if (ntw == 1) k_recouple<LL, 1><<<n, 256, 0, s>>>(t, R, S, order, C, dh, y);                            \
-    else if (ntw == 2) k_recouple<LL, 2><<<n, 256, 0, s>>>(t, R, S, order, C, dh, y);                       \
-    else k_recouple<LL, 4><<<n, 256, 0, s>>>(t, R, S, order, C, dh, y);                                     \
+    E2F_RC(LL, 1) E2F_RC(LL, 2) E2F_RC(LL, 4)                                                               \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
 #undef E2F_CASE
+#undef E2F_RC
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -31,6 +31,12 @@ double wigner6j(int j1, int j2, int j3, int j4, int j5, int j6);
 constexpr int kSchedThreads = 256;
 constexpr int kTpRows = 256;
 constexpr int kRcRows = 256;
+// Row stride (floats) of the recouple's per-node matrix tile in LDS: the
+// 16*ceil(nk/16) used columns padded to 16 mod 32, so the MFMA operand reads
+// of 4 rows x 16 columns fall in distinct banks.
+constexpr int rc_qstride(int nk) {
+  return 16 * ((nk + 15) / 16) + (((nk + 15) / 16) % 2 == 0 ? 16 : 0);
+}
 
 // A per-node matrix built by 256 threads from a fixed schedule: in chunk c,
 // thread t walks entries k = 0..k[c]-1 at index off[c] + k*256 + t, each
@@ -75,7 +81,7 @@ struct LayerTables {
   std::vector<int> k_path;
   std::vector<double> k_unit;
   Schedule tp_sched;                // node TP: chunks (degree a, 256 rows), dest = row*KP(a) + al
-  Schedule rc_sched;                // recouple: chunks of 256 T rows, dest = row*16*MT + (o*o+m)
+  Schedule rc_sched;                // recouple: chunks of 256 T rows, dest = row*rc_qstride + (o*o+m)
   int max_qslots = 0;               // largest (2o+1)*ncol[o]
   int m_slots() const { return m_rowoff.back(); }
 };

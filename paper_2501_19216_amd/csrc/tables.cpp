@@ -343,8 +343,8 @@ LayerTables build_layer_tables(int L) {
       }
     }
     t.tp_sched = make_schedule(chunks);
-    // recouple: chunks of 256 T rows; Q rows padded to 16*MT
-    const int MT = (t.nk + 15) / 16;
+    // recouple: chunks of 256 T rows; Q rows padded to rc_qstride
+    const int QS = rc_qstride(t.nk);
     std::vector<std::vector<Slot>> rchunks((t.dimT + kRcRows - 1) / kRcRows);
     for (int o = 0; o <= L; ++o) {
       const int ncol = t.q_ncol[o];
@@ -352,7 +352,7 @@ LayerTables build_layer_tables(int L) {
         for (int col = 0; col < ncol; ++col) {
           const int s = t.q_slotoff[o] + m * ncol + col;
           const int row = t.q_cols[t.q_coloff[o] + col];
-          Slot sl{(row % kRcRows) * 16 * MT + o * o + m, {}};
+          Slot sl{(row % kRcRows) * QS + o * o + m, {}};
           for (int e = t.q_ptr[s]; e < t.q_ptr[s + 1]; ++e) sl.e.push_back({t.q_ridx[e], t.q_path[e], t.q_unit[e]});
           rchunks[row / kRcRows].push_back(std::move(sl));
         }
