@@ -226,6 +226,8 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
   d.k_coef = nullptr;
   d.max_qslots = t.max_qslots;
   d.m_slots = t.m_slots();
+  for (int a = 0; a <= L; ++a) d.tp_rs[a] = t.tp_rs[a];
+  for (int a = 0; a <= L + 1; ++a) d.tp_mo[a] = t.tp_mo[a];
   ctx->dev[L] = d;
   return E2F_OK;
 }

@@ -152,75 +152,72 @@ __device__ __forceinline__ void run_schedule(const int* __restrict__ meta, const
   }
 }
 
-template <int L, int A>
-__device__ __forceinline__ void node_tp_degree(const DevTables& t, const double* Rl, float* Ml, const float* h,
-                                               int hstride, int C, int dh, float* Tp, int& chunk) {
-  constexpr int NK = (L + 1) * (L + 1);
-  constexpr int KA = 2 * A + 1;
-  constexpr int KP = (KA + 3) & ~3;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int j = lane & 15, k4 = lane >> 4;
-  const int ra0 = t.a_row_start[A], ra1 = t.a_row_start[A + 1];
-  const int NT = (C + 15) / 16;
-  for (int c0 = ra0; c0 < ra1; c0 += kTpRows) {
-    const int rc = min(kTpRows, ra1 - c0);
-    __syncthreads();
-    for (int q = threadIdx.x; q < rc * KP; q += blockDim.x) Ml[q] = 0.0f;
-    __syncthreads();
-    run_schedule(t.tp_meta + t.tp_off[chunk], t.tp_coef + t.tp_off[chunk], t.tp_k[chunk], Rl, Ml);
-    ++chunk;
-    __syncthreads();
-    const int nrt = (rc + 15) / 16;
-#pragma unroll 4
-    for (int task = wave; task < nrt * NT; task += (int)(blockDim.x >> 6)) {
-      const int rt = task / NT, nt = task % NT;
-      const int c = nt * 16 + j;
-      v4f acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KP / 4; ++ks) {
-        const int kk = ks * 4 + k4;
-        const float a = (rt * 16 + j < rc) ? Ml[(rt * 16 + j) * KP + kk] : 0.0f;
-        const float b = (kk < KA && c < C) ? h[(A * A + kk) * hstride + c] : 0.0f;
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
-      }
-      if (c < C) {
-        float* dst = Tp + (size_t)(c / dh) * t.dimT * dh + c % dh;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int rl = rt * 16 + 4 * k4 + v;
-          if (rl < rc) dst[(size_t)(c0 + rl) * dh] = acc[v];
-        }
-      }
-    }
-  }
-  (void)NK;
-}
-
-template <int L, int... As>
-__device__ __forceinline__ void node_tp_all(std::integer_sequence<int, As...>, const DevTables& t, const double* Rl,
-                                            float* Ml, const float* h, int hstride, int C, int dh, float* Tp) {
-  int chunk = 0;
-  (node_tp_degree<L, As>(t, Rl, Ml, h, hstride, C, dh, Tp, chunk), ...);
-}
-
+// Per item (a sender under its tile's origin): the whole per-node matrix
+// M^(a)[row][al] = sum_b C^{d de}_{a al, b be} R^(b)_be(p) of every degree a
+// is built once in LDS from one fixed schedule, stored transposed (al-major,
+// rows padded to 16 mod 32 floats), and h is staged in LDS (rows padded the
+// same way) when it fits.  The products then need no global load, so the T
+// stores never hold up a wait:
+//     T[row][c] = sum_al M^(a)[row][al] h^(a)[al][c]
+// on v_mfma_f32_16x16x4f32 with A = h^T (16 channels x 4 al), B = M^T
+// (4 al x 16 rows); each lane ends with 4 consecutive channels of one row,
+// stored as one float4 (a wave writes 16 whole rows of 64 bytes per head).
 template <int L>
 __global__ __launch_bounds__(256) void k_node_tp(DevTables t, const double* __restrict__ R,
                                                  const int32_t* __restrict__ node_of, const float* __restrict__ feat,
-                                                 int C, int dh, bool stage_h, float* __restrict__ T) {
+                                                 int C, int dh, int hs, float* __restrict__ T) {
   constexpr int NK = (L + 1) * (L + 1);
-  constexpr int KPMAX = ((2 * L + 1) + 3) & ~3;
-  __shared__ float Ml[kTpRows * KPMAX];
+  extern __shared__ float sm[];  // M (t.tp_mo[L+1] floats), then h if staged (hs > 0)
   __shared__ double Rl[NK];
-  extern __shared__ float hl[];  // h_node staged in LDS when it fits (dynamic size > 0)
   const int item = blockIdx.x;
   const int node = node_of ? node_of[item] : item;
   if (threadIdx.x < NK) Rl[threadIdx.x] = R[(size_t)item * NK + threadIdx.x];
+  const int msize = t.tp_mo[L + 1];
+  float* Mt = sm;
   const float* h = feat + (size_t)node * NK * C;
-  if (stage_h) {
-    for (int q = threadIdx.x; q < NK * C / 4; q += blockDim.x) ((float4*)hl)[q] = ((const float4*)h)[q];
+  int hstride = C;
+  if (hs > 0) {
+    float* hl = sm + ((msize + 3) & ~3);
+    const int c4 = C / 4;
+    for (int q = threadIdx.x; q < NK * c4; q += blockDim.x)
+      ((float4*)hl)[(q / c4) * (hs / 4) + q % c4] = ((const float4*)h)[q];
     h = hl;
+    hstride = hs;
   }
-  node_tp_all<L>(std::make_integer_sequence<int, L + 1>{}, t, Rl, Ml, h, C, C, dh, T + (size_t)item * t.dimT * C);
+  for (int q = threadIdx.x; q < msize; q += blockDim.x) Mt[q] = 0.0f;
+  __syncthreads();
+  run_schedule(t.tp_meta, t.tp_coef, t.tp_k[0], Rl, Mt);
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int l16 = lane & 15, k4 = lane >> 4;
+  const int NT = (C + 15) / 16;
+  float* Tp = T + (size_t)item * t.dimT * C;
+#pragma unroll
+  for (int a = 0; a <= L; ++a) {
+    const int KA = 2 * a + 1, KP = (KA + 3) & ~3;
+    const int ra0 = t.a_row_start[a], rows = t.a_row_start[a + 1] - ra0;
+    const int rs = t.tp_rs[a];
+    const float* Ma = Mt + t.tp_mo[a];
+    const int nrt = (rows + 15) / 16;
+    for (int task = wave; task < nrt * NT; task += 4) {
+      const int rt = task / NT, nt = task % NT;
+      const int ca = nt * 16 + l16;  // A operand channel
+      const float* hc = h + (ca < C ? ca : 0);
+      v4f acc = {0.f, 0.f, 0.f, 0.f};
+      for (int ks = 0; ks < KP / 4; ++ks) {
+        const int k = 4 * ks + k4;
+        const float hv = hc[(a * a + min(k, KA - 1)) * hstride];
+        const float av = k < KA ? hv : 0.0f;
+        const float bv = Ma[k * rs + rt * 16 + l16];  // rows k >= KA are zero
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
+      }
+      // acc[v] = T[row rt*16 + l16][channel nt*16 + 4*k4 + v]
+      const int row = rt * 16 + l16, c0 = nt * 16 + 4 * k4;
+      if (row < rows && c0 < C)
+        *(float4*)(Tp + (size_t)(c0 / dh) * t.dimT * dh + (size_t)(ra0 + row) * dh + c0 % dh) =
+            make_float4(acc[0], acc[1], acc[2], acc[3]);
+    }
+  }
 }
 
 // ------------------------------------------------------------ receiver order
@@ -950,12 +947,18 @@ hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const
 hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* node_of, const float* feat,
                           int n_items, int C, int dh, float* T, hipStream_t s) {
   if (n_items == 0) return hipSuccess;
-  const size_t hbytes = sizeof(float) * (size_t)t.nk * C;
-  const size_t lds = hbytes <= 32768 ? hbytes : 0;  // stage h_node in LDS when small
+  // h staged in LDS with rows padded to 16 mod 32 floats when it is small
+  int hs = (C + 15) / 16 * 16;
+  if ((hs / 16) % 2 == 0) hs += 16;
+  const size_t mbytes = sizeof(float) * (size_t)((t.tp_mo[t.L + 1] + 3) & ~3);
+  const size_t hbytes = sizeof(float) * (size_t)t.nk * hs;
+  if (hbytes > 32768) hs = 0;
+  const size_t lds = mbytes + (hs > 0 ? hbytes : 0);
   switch (t.L) {
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
-    k_node_tp<LL><<<n_items, 256, lds, s>>>(t, R, node_of, feat, C, dh, lds > 0, T);                       \
+    if (hipError_t e = allow_lds(k_node_tp<LL>, lds); e != hipSuccess) return e;                            \
+    k_node_tp<LL><<<n_items, 256, lds, s>>>(t, R, node_of, feat, C, dh, hs, T);                             \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
 #undef E2F_CASE

@@ -26,10 +26,9 @@ double wigner6j(int j1, int j2, int j3, int j4, int j5, int j6);
 // Structure of the factorised layer for one L: every table is independent of
 // the path weights except the *_coef arrays, which the context refreshes when
 // the caller's path weights change.
-// Row chunks of the per-node matrices staged in LDS by the node TP and the
-// recouple kernels, and their thread count.
+// Thread count of the schedules that build per-node matrices in LDS, and the
+// row chunk of the recouple's matrix.
 constexpr int kSchedThreads = 256;
-constexpr int kTpRows = 256;
 constexpr int kRcRows = 256;
 // Row stride (floats) of the recouple's per-node matrix tile in LDS: the
 // 16*ceil(nk/16) used columns padded to 16 mod 32, so the MFMA operand reads
@@ -80,7 +79,11 @@ struct LayerTables {
   std::vector<int> k_ridx;
   std::vector<int> k_path;
   std::vector<double> k_unit;
-  Schedule tp_sched;                // node TP: chunks (degree a, 256 rows), dest = row*KP(a) + al
+  // node TP: one chunk; the matrix of degree a is stored transposed at
+  // tp_mo[a], entry (al, row) at al*tp_rs[a] + row - a_row_start[a], with
+  // KP(a) = 2a+1 rounded up to 4 rows of tp_rs[a] floats (tp_rs = 16 mod 32)
+  Schedule tp_sched;
+  std::vector<int> tp_rs, tp_mo;    // [L+1], [L+2]
   Schedule rc_sched;                // recouple: chunks of 256 T rows, dest = row*rc_qstride + (o*o+m)
   int max_qslots = 0;               // largest (2o+1)*ncol[o]
   int m_slots() const { return m_rowoff.back(); }
@@ -102,6 +105,7 @@ struct DevTables {
   const int* tp_k; const int* tp_off; const int* tp_meta; const double* tp_coef;
   const int* rc_k; const int* rc_off; const int* rc_meta; const double* rc_coef;  // rc_coef includes path weights
   int max_qslots, m_slots;
+  int tp_rs[kMaxL + 1], tp_mo[kMaxL + 2];
 };
 
 }  // namespace e2f

@@ -325,23 +325,25 @@ LayerTables build_layer_tables(int L) {
   t.q_slotoff[L1] = (int)t.q_ptr.size() - 1;
   // ---- build schedules of the per-node matrices
   {
-    // node TP: chunks in kernel order (degree a, then 256-row chunks of its rows)
-    std::vector<std::vector<Slot>> chunks;
+    // node TP: one chunk over all degrees, transposed per-degree matrices
+    t.tp_rs.assign(L + 1, 0);
+    t.tp_mo.assign(L + 2, 0);
     for (int a = 0; a <= L; ++a) {
       const int KP = (2 * a + 1 + 3) & ~3;
-      for (int c0 = t.a_row_start[a]; c0 < t.a_row_start[a + 1]; c0 += kTpRows) {
-        std::vector<Slot> slots;
-        const int c1 = std::min(t.a_row_start[a + 1], c0 + kTpRows);
-        for (int r = c0; r < c1; ++r)
-          for (int al = 0; al < 2 * a + 1; ++al) {
-            const int s = t.m_rowoff[r] + al;
-            Slot sl{(r - c0) * KP + al, {}};
-            for (int e = t.m_ptr[s]; e < t.m_ptr[s + 1]; ++e) sl.e.push_back({t.m_ridx[e], -1, t.m_coef[e]});
-            slots.push_back(std::move(sl));
-          }
-        chunks.push_back(std::move(slots));
-      }
+      int rs = (t.a_row_start[a + 1] - t.a_row_start[a] + 15) / 16 * 16;
+      if ((rs / 16) % 2 == 0) rs += 16;
+      t.tp_rs[a] = rs;
+      t.tp_mo[a + 1] = t.tp_mo[a] + KP * rs;
     }
+    std::vector<std::vector<Slot>> chunks(1);
+    for (int a = 0; a <= L; ++a)
+      for (int r = t.a_row_start[a]; r < t.a_row_start[a + 1]; ++r)
+        for (int al = 0; al < 2 * a + 1; ++al) {
+          const int s = t.m_rowoff[r] + al;
+          Slot sl{t.tp_mo[a] + al * t.tp_rs[a] + (r - t.a_row_start[a]), {}};
+          for (int e = t.m_ptr[s]; e < t.m_ptr[s + 1]; ++e) sl.e.push_back({t.m_ridx[e], -1, t.m_coef[e]});
+          chunks[0].push_back(std::move(sl));
+        }
     t.tp_sched = make_schedule(chunks);
     // recouple: chunks of 256 T rows; Q rows padded to rc_qstride
     const int QS = rc_qstride(t.nk);
