@@ -146,6 +146,7 @@ def main():
     ap.add_argument("--copy-calib", action="store_true", help="also run a 1 GiB device copy (counter calibration)")
     ap.add_argument("--sweep", action="store_true",
                     help="instead: one JSON line per workload (6j forward and edge-TP baseline times and speedup)")
+    ap.add_argument("--sweep-workloads", default="", help="comma-separated subset of the sweep (default: all)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (no sharding, no collectives).",
@@ -157,7 +158,8 @@ def main():
     import paper_2501_19216_amd as e2f
 
     if args.sweep:
-        for name in syn.WORKLOADS:
+        names = [w for w in args.sweep_workloads.split(",") if w] or list(syn.WORKLOADS)
+        for name in names:
             print(json.dumps(sweep_one(name, args.steps, args.warmup)), flush=True)
         return
 

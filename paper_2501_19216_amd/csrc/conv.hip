@@ -205,10 +205,10 @@ __global__ __launch_bounds__(256) void k_node_tp(DevTables t, const double* __re
       const float* hc = h + (ca < C ? ca : 0);
       v4f acc = {0.f, 0.f, 0.f, 0.f};
       for (int ks = 0; ks < KP / 4; ++ks) {
-        const int k = 4 * ks + k4;
-        const float hv = hc[(a * a + min(k, KA - 1)) * hstride];
+        const int k = 4 * ks + k4, kc = min(k, KA - 1);  // k >= KA: weight 0
+        const float hv = hc[(a * a + kc) * hstride];
         const float av = k < KA ? hv : 0.0f;
-        const float bv = Ma[k * rs + rt * 16 + l16];  // rows k >= KA are zero
+        const float bv = Ma[kc * rs + rt * 16 + l16];
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
       }
       // acc[v] = T[row rt*16 + l16][channel nt*16 + 4*k4 + v]
@@ -555,9 +555,9 @@ __global__ __launch_bounds__(64 * kAggRecv) void k_aggregate_rows(const float4* 
 // ------------------------------------------------------------ i-side recouple
 // y_i[k][c] = sum_r Q_i[k][r] S_i[r][c] over the T rows r, with the per-node
 // matrix Q_i[(o,m)][(a,b,d,de)] = sum_u K(a,b,d,u,o) sum_ga C^{o m}_{u ga, d de}
-// R^(u)_ga(p_i) built in float64 in LDS (256 T rows at a time, from a fixed
-// schedule) and the product on v_mfma_f32_16x16x4f32: 16 output rows x 16
-// channels per tile, S_i read from HBM exactly once.
+// R^(u)_ga(p_i) summed in float64 into an fp32 LDS tile (rc_rows T rows at a
+// time, from a fixed schedule) and the product on v_mfma_f32_16x16x4f32: 16
+// output rows x 16 channels per tile, S_i read from HBM exactly once.
 
 template <int L, int NTW>
 __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __restrict__ R,
@@ -566,8 +566,9 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
   constexpr int NK = (L + 1) * (L + 1);
   constexpr int MT = (NK + 15) / 16;  // NTW: channel tiles per wave and pass
   constexpr int QS = rc_qstride(NK);
+  constexpr int RR = rc_rows(NK);
   constexpr int ST = 8;                // 4-row steps per pipeline stage
-  extern __shared__ float Qt[];        // Qt[r][k], kRcRows rows of QS floats
+  extern __shared__ float Qt[];        // Qt[r][k], RR rows of QS floats
   __shared__ double Rl[NK];
   const int i = order[blockIdx.x];  // S row blockIdx.x belongs to receiver i
   if (threadIdx.x < NK) Rl[threadIdx.x] = R[(size_t)i * NK + threadIdx.x];
@@ -593,12 +594,12 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
     for (int q = 0; q < NTW; ++q)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) acc[q][mt] = (v4f){0.f, 0.f, 0.f, 0.f};
-    for (int r0 = 0; r0 < dimT; r0 += kRcRows) {
-      const int rc = min(kRcRows, dimT - r0);
+    for (int r0 = 0; r0 < dimT; r0 += RR) {
+      const int rc = min(RR, dimT - r0);
       __syncthreads();
-      for (int q = threadIdx.x; q < kRcRows * QS; q += blockDim.x) Qt[q] = 0.0f;
+      for (int q = threadIdx.x; q < RR * QS; q += blockDim.x) Qt[q] = 0.0f;
       __syncthreads();
-      const int ch = r0 / kRcRows;
+      const int ch = r0 / RR;
       run_schedule(t.rc_meta + t.rc_off[ch], t.rc_coef + t.rc_off[ch], t.rc_k[ch], Rl, Qt);
       __syncthreads();
       // Stages of ST steps in pairs; rows past the chunk read its last row
@@ -617,7 +618,7 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
 #pragma unroll
         for (int u = 0; u < ST; ++u) {
           const int rl = (stg * ST + u) * 4 + k4;
-          const int rq = min(rl, kRcRows - 1);
+          const int rq = min(rl, RR - 1);
           float a[MT];
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
@@ -1073,7 +1074,7 @@ hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, 
   if (n == 0) return hipSuccess;
   const int nt = (C + 15) / 16;  // channel tiles; 4 waves
   const int ntw = nt <= 4 ? 1 : (nt <= 8 ? 2 : 4);
-  const size_t lds = sizeof(float) * (size_t)kRcRows * rc_qstride(t.nk);
+  const size_t lds = sizeof(float) * (size_t)rc_rows(t.nk) * rc_qstride(t.nk);
   switch (t.L) {
 #define E2F_RC(LL, W)                                                                                       \
   if (ntw == W) {                                                                                           \

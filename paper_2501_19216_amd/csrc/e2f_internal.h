@@ -26,10 +26,11 @@ double wigner6j(int j1, int j2, int j3, int j4, int j5, int j6);
 // Structure of the factorised layer for one L: every table is independent of
 // the path weights except the *_coef arrays, which the context refreshes when
 // the caller's path weights change.
-// Thread count of the schedules that build per-node matrices in LDS, and the
-// row chunk of the recouple's matrix.
+// Thread count of the schedules that build per-node matrices in LDS.
 constexpr int kSchedThreads = 256;
-constexpr int kRcRows = 256;
+// Rows of T per chunk of the recouple's per-node matrix (fewer at high L so
+// that the LDS tile leaves room for two workgroups per CU).
+constexpr int rc_rows(int nk) { return nk > 25 ? 128 : 256; }
 // Row stride (floats) of the recouple's per-node matrix tile in LDS: the
 // 16*ceil(nk/16) used columns padded to 16 mod 32, so the MFMA operand reads
 // of 4 rows x 16 columns fall in distinct banks.
@@ -81,10 +82,10 @@ struct LayerTables {
   std::vector<double> k_unit;
   // node TP: one chunk; the matrix of degree a is stored transposed at
   // tp_mo[a], entry (al, row) at al*tp_rs[a] + row - a_row_start[a], with
-  // KP(a) = 2a+1 rounded up to 4 rows of tp_rs[a] floats (tp_rs = 16 mod 32)
+  // 2a+1 rows of tp_rs[a] floats (tp_rs = 16 mod 32)
   Schedule tp_sched;
   std::vector<int> tp_rs, tp_mo;    // [L+1], [L+2]
-  Schedule rc_sched;                // recouple: chunks of 256 T rows, dest = row*rc_qstride + (o*o+m)
+  Schedule rc_sched;                // recouple: chunks of rc_rows T rows, dest = row*rc_qstride + (o*o+m)
   int max_qslots = 0;               // largest (2o+1)*ncol[o]
   int m_slots() const { return m_rowoff.back(); }
 };

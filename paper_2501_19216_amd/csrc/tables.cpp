@@ -329,11 +329,10 @@ LayerTables build_layer_tables(int L) {
     t.tp_rs.assign(L + 1, 0);
     t.tp_mo.assign(L + 2, 0);
     for (int a = 0; a <= L; ++a) {
-      const int KP = (2 * a + 1 + 3) & ~3;
       int rs = (t.a_row_start[a + 1] - t.a_row_start[a] + 15) / 16 * 16;
       if ((rs / 16) % 2 == 0) rs += 16;
       t.tp_rs[a] = rs;
-      t.tp_mo[a + 1] = t.tp_mo[a] + KP * rs;
+      t.tp_mo[a + 1] = t.tp_mo[a] + (2 * a + 1) * rs;
     }
     std::vector<std::vector<Slot>> chunks(1);
     for (int a = 0; a <= L; ++a)
@@ -345,18 +344,18 @@ LayerTables build_layer_tables(int L) {
           chunks[0].push_back(std::move(sl));
         }
     t.tp_sched = make_schedule(chunks);
-    // recouple: chunks of 256 T rows; Q rows padded to rc_qstride
-    const int QS = rc_qstride(t.nk);
-    std::vector<std::vector<Slot>> rchunks((t.dimT + kRcRows - 1) / kRcRows);
+    // recouple: chunks of rc_rows T rows; Q rows padded to rc_qstride
+    const int QS = rc_qstride(t.nk), RR = rc_rows(t.nk);
+    std::vector<std::vector<Slot>> rchunks((t.dimT + RR - 1) / RR);
     for (int o = 0; o <= L; ++o) {
       const int ncol = t.q_ncol[o];
       for (int m = 0; m < 2 * o + 1; ++m)
         for (int col = 0; col < ncol; ++col) {
           const int s = t.q_slotoff[o] + m * ncol + col;
           const int row = t.q_cols[t.q_coloff[o] + col];
-          Slot sl{(row % kRcRows) * QS + o * o + m, {}};
+          Slot sl{(row % RR) * QS + o * o + m, {}};
           for (int e = t.q_ptr[s]; e < t.q_ptr[s + 1]; ++e) sl.e.push_back({t.q_ridx[e], t.q_path[e], t.q_unit[e]});
-          rchunks[row / kRcRows].push_back(std::move(sl));
+          rchunks[row / RR].push_back(std::move(sl));
         }
     }
     t.rc_sched = make_schedule(rchunks);
