@@ -392,7 +392,7 @@ __global__ void k_block_alpha(const int64_t* __restrict__ row_ptr, const int32_t
 constexpr int kXcds = 8;
 constexpr int kPiece = 512;  // union rows staged in LDS at a time
 
-template <int NQ>
+template <int NQ, int NS>
 __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict__ T, int pair_base,
                                                         const int32_t* __restrict__ uni,
                                                         const int32_t* __restrict__ blk_off,
@@ -401,7 +401,7 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
                                                         const float* __restrict__ alpha_blk, int n, int nblk, int bpx,
                                                         int ntg, int ntg4, int dimT, int C, int dh, int H,
                                                         float* __restrict__ S) {
-  __shared__ int32_t ubl[kPiece];
+  __shared__ int64_t ubl[kPiece];     // float4 offset of each union row of the piece in T
   __shared__ float4 Al4[kPiece * 4];  // Al[slot][receiver]: A operand of head h
   const float* Al = (const float*)Al4;
   // workgroup = (block b, column task); the blocks of one XCD are contiguous
@@ -439,15 +439,15 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
   const float4* T4 = (const float4*)T;
   const bool active = tg < ntg;  // uniform over the wave
   // Union rows 4 at a time (lane row k); rows past the piece take weight 0
-  // and re-read the piece's first row.  Two register stages: the loads of
-  // one step are in flight while the MFMAs of the previous one run.
-  float4 b0[NQ], b1[NQ];
-  float a0 = 0.f, a1 = 0.f;
+  // and re-read its last row.  NS register stages: while the MFMAs of one
+  // step run, the loads of the next NS-1 steps are in flight.
+  float4 bst[NS][NQ];
+  float ast[NS];
   auto load = [&](int s0, int np, float4* bv, float& a) {
-    const int sl = s0 + k;
-    const bool valid = sl < np;
-    a = valid ? Al[sl * 16 + j] : 0.0f;
-    const float4* trow = T4 + (int64_t)ubl[valid ? sl : 0] * W4;
+    const int sl = s0 + k, sc = min(sl, np - 1);  // clamped reads, no branch
+    const float av = Al[sc * 16 + j];
+    a = sl < np ? av : 0.0f;
+    const float4* trow = T4 + ubl[sc];
 #pragma unroll
     for (int q = 0; q < NQ; ++q) bv[q] = trow[c4[q]];
   };
@@ -462,15 +462,15 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
   };
   for (int p0 = 0; p0 < nu; p0 += kPiece) {
     const int np = min(nu - p0, kPiece);
-    // staging: each thread issues its loads before its stores (clamped
-    // indexes, so there is no branch between them)
+    // staging: every thread issues its loads, then its stores, at clamped
+    // indexes with no branch (slots past the piece hold copies, never read)
     {
       static_assert(kPiece == 2 * 256, "staging assumes 256 threads");
       __syncthreads();
       const int t = threadIdx.x;
       const int32_t u0 = ub[p0 + min(t, np - 1)], u1 = ub[p0 + min(t + 256, np - 1)];
-      if (t < np) ubl[t] = u0 - pair_base;
-      if (t + 256 < np) ubl[t + 256] = u1 - pair_base;
+      ubl[t] = (int64_t)(u0 - pair_base) * W4;
+      ubl[t + 256] = (int64_t)(u1 - pair_base) * W4;
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
         float4 v[4];
@@ -480,26 +480,27 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
           v[u] = ab4[(int64_t)(p0 + q / 4) * H * 4 + q % 4];
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          if (t + 256 * (4 * half + u) < 4 * np) Al4[t + 256 * (4 * half + u)] = v[u];
+        for (int u = 0; u < 4; ++u) Al4[t + 256 * (4 * half + u)] = v[u];
       }
       __syncthreads();
     }
     if (!active) continue;  // no barrier below
-    // Steps of 4 rows in pairs (an odd count ends with a zero-weight step);
-    // the body has no branch, so each wait covers only the older stage, and
-    // sched_barrier keeps the scheduler from sinking a prefetch to its use.
-    const int npair = (np + 7) / 8;
-    load(0, np, b0, a0);
-    for (int it = 0; it < npair; ++it) {
-      load(8 * it + 4, np, b1, a1);
-      __builtin_amdgcn_sched_barrier(0);
-      mma(b0, a0);
-      __builtin_amdgcn_sched_barrier(0);
-      load(8 * it + 8, np, b0, a0);
-      __builtin_amdgcn_sched_barrier(0);
-      mma(b1, a1);
-      __builtin_amdgcn_sched_barrier(0);
+    // Steps of 4 rows, NS per iteration (the last iteration is padded with
+    // zero-weight steps); the body has no branch, so each wait covers only
+    // the oldest stage, and sched_barrier keeps the scheduler from sinking
+    // a prefetch to its use.
+#pragma unroll
+    for (int st = 0; st < NS - 1; ++st) load(4 * st, np, bst[st], ast[st]);
+    const int nit = (np + 4 * NS - 1) / (4 * NS);
+    for (int it = 0; it < nit; ++it) {
+#pragma unroll
+      for (int st = 0; st < NS; ++st) {
+        const int ls = (st + NS - 1) % NS;
+        load(4 * (it * NS + st + NS - 1), np, bst[ls], ast[ls]);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(bst[st], ast[st]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   }
   if (!active) return;
@@ -1038,22 +1039,23 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
   if (n == 0) return hipSuccess;
   const int dh = C / H;
   if (use_blocks) {
-    // columns per wave: 64*NQ; E2F_AGG_NQ overrides (tuning)
-    int nq = 2;
-    if (const char* cfg = getenv("E2F_AGG_NQ")) nq = atoi(cfg);
+    // columns per wave: 64*NQ, register stages NS; E2F_AGG_CFG="NQ,NS" overrides (tuning)
+    int nq = 2, ns = 3;
+    if (const char* cfg = getenv("E2F_AGG_CFG")) sscanf(cfg, "%d,%d", &nq, &ns);
     const int nblk = (n + 15) / 16;
     const int ntg = (dimT * dh + 64 * nq - 1) / (64 * nq);
     const int ntg4 = (ntg + 3) / 4;
     const int bpx = (nblk + kXcds - 1) / kXcds;
     const int64_t blocks = (int64_t)kXcds * bpx * H * ntg4;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-#define E2F_AGG(NQ_)                                                                                       \
-  if (nq == NQ_) {                                                                                        \
-    k_aggregate_mfma<NQ_><<<(unsigned)blocks, 256, 0, s>>>(T, pair_base, uni, blk_off, uoff, ucount, alpha_blk, \
-                                                         n, nblk, bpx, ntg, ntg4, dimT, C, dh, H, S);      \
+#define E2F_AGG(NQ_, NS_)                                                                                  \
+  if (nq == NQ_ && ns == NS_) {                                                                           \
+    k_aggregate_mfma<NQ_, NS_><<<(unsigned)blocks, 256, 0, s>>>(T, pair_base, uni, blk_off, uoff, ucount,  \
+                                                              alpha_blk, n, nblk, bpx, ntg, ntg4, dimT, C, dh, H, S); \
     return hipGetLastError();                                                                             \
   }
-    E2F_AGG(2) E2F_AGG(4) E2F_AGG(6) E2F_AGG(8)
+    E2F_AGG(2, 2) E2F_AGG(2, 3) E2F_AGG(2, 4) E2F_AGG(2, 6) E2F_AGG(4, 2) E2F_AGG(4, 3) E2F_AGG(4, 4)
+    E2F_AGG(6, 2) E2F_AGG(8, 2)
 #undef E2F_AGG
     return hipErrorInvalidValue;
   }
