@@ -108,6 +108,9 @@ def sweep_one(name, steps, warmup):
     k6 = max(2, steps // 4) if n > 50000 else steps
     f6 = lambda: e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, rp, ci, al, wl.lmax, wl.heads, wl.cutoff,
                                                mix_w=mix_w, graph_id=gid, out=out)
+    for _ in range(warmup):  # warm-up outside the profiled window (first call allocates)
+        f6()
+    torch.cuda.synchronize()
     e2f.e2f_profile(ctx, True)
     ms6 = time_fn(f6, k6)
     prof = e2f.e2f_profile_read(ctx)
