@@ -627,7 +627,7 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   // ---- phase 2 buffers
   const bool mixing = p->mix_w != nullptr;
   const size_t need_b = 2 * al256(sizeof(int32_t) * (size_t)P) + 3 * al256(sizeof(int32_t) * (size_t)n_edges) +
-                        4 * al256(sizeof(int32_t) * (size_t)(nblk + 1)) + al256(blk_tmp_b) +
+                        3 * al256(sizeof(int32_t) * (size_t)(nblk + 1)) + al256(blk_tmp_b) +
                         al256(sizeof(double) * (size_t)P * nk) + al256(sizeof(double) * (size_t)n * nk) +
                         al256(row_bytes * (size_t)max_pairs) + al256(row_bytes * (size_t)max_recv) +
                         (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
@@ -642,7 +642,6 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   int32_t* blk_count = cb.take<int32_t>((size_t)nblk + 1);
   int32_t* blk_off = cb.take<int32_t>((size_t)nblk + 1);
   int32_t* ucount = cb.take<int32_t>((size_t)nblk + 1);
-  int32_t* uoff = cb.take<int32_t>((size_t)nblk + 1);
   void* blk_tmp = cb.take<char>(blk_tmp_b);
   double* Rp = cb.take<double>((size_t)P * nk);
   double* Rr = cb.take<double>((size_t)n * nk);
@@ -660,23 +659,12 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
     if (nb == 0) continue;
     const int32_t* ord = order + q0;
     E2F_TIMED("node_tp", launch_node_tp(t, Rp + (size_t)p0 * nk, pair_node + p0, feat, pb, C, dh, T, s));
-    float* alpha_blk = nullptr;
     if (use_blocks) {
-      const int nblk_b = (nb + 15) / 16;
-      E2F_TIMED("tile_plan", launch_block_union(row_ptr, col_pair, ord, nb, blk_count, blk_off, uni, ucount, uoff,
+      E2F_TIMED("tile_plan", launch_block_union(row_ptr, col_pair, ord, nb, blk_count, blk_off, uni, ucount,
                                                 edge_slot, blk_tmp, blk_tmp_b, s));
-      E2F_HIP(hipMemcpyAsync(ctx->pinned, uoff + nblk_b, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-      E2F_HIP(hipStreamSynchronize(s));
-      int32_t union_rows;
-      std::memcpy(&union_rows, ctx->pinned, 4);
-      rs = ensure(ctx, ctx->c, sizeof(float) * (size_t)union_rows * p->heads * 16 + 256, s);
-      if (rs != E2F_OK) return rs;
-      alpha_blk = (float*)ctx->c.p;
-      E2F_TIMED("tile_plan", launch_block_alpha(row_ptr, ord, nb, uoff, edge_slot, alpha, p->heads, union_rows,
-                                                alpha_blk, s));
     }
-    E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, alpha, ord, uni, blk_off, uoff, ucount,
-                                            alpha_blk, use_blocks, nb, t.dimT, C, p->heads, S, s));
+    E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, alpha, ord, uni, blk_off, ucount, edge_slot,
+                                            use_blocks, nb, t.dimT, C, p->heads, S, s));
     E2F_TIMED("recouple", launch_recouple(t, Rr, S, ord, nb, C, dh, y, s));
   }
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));

@@ -356,23 +356,6 @@ __global__ __launch_bounds__(256) void k_block_union(const int64_t* __restrict__
   }
 }
 
-// Dense A operand of the block aggregation:
-//   alpha_blk[((uoff[b] + slot) * H + h) * 16 + r] = alpha[e][h]
-// for the edge e of receiver r (0..15) of block b whose T row is union entry
-// `slot`; entries without an edge stay 0 (the buffer is cleared first).
-__global__ void k_block_alpha(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ order, int n,
-                              const int32_t* __restrict__ uoff, const int32_t* __restrict__ edge_slot,
-                              const float* __restrict__ alpha, int H, float* __restrict__ alpha_blk) {
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= n) return;
-  const int i = order[r];
-  const int64_t base = (int64_t)uoff[r / 16] * H * 16 + (r % 16);
-  for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
-    const int64_t at = base + (int64_t)edge_slot[e] * H * 16;
-    for (int h = 0; h < H; ++h) alpha_blk[at + h * 16] = alpha ? alpha[e * H + h] : 1.0f;
-  }
-}
-
 // ------------------------------------------------------------ aggregation
 // S[i][q] = sum_{e in row i} alpha[e][head(q)] T[col_pair[e]][q].
 //
@@ -380,7 +363,7 @@ __global__ void k_block_alpha(const int64_t* __restrict__ row_ptr, const int32_t
 // U_b of their T rows, and for one head h:
 //     S_b,h [16 x cols] = A_b,h [16 x |U_b|] . T_{U_b},h [|U_b| x cols],
 // where A_b,h[r][u] is the attention weight of the edge (receiver r, union row
-// u) or 0.  v_mfma_f32_16x16x4f32 takes A as 16 receivers x 4 union rows and
+// u) or 0; each workgroup assembles A_b,h in LDS from alpha and edge_slot.  v_mfma_f32_16x16x4f32 takes A as 16 receivers x 4 union rows and
 // B as 4 union rows x 16 columns of head h, so every T element loaded from
 // L2 is used by all 16 receivers inside the matrix core instead of being
 // gathered once per edge.  The columns of head h are enumerated as
@@ -396,9 +379,11 @@ template <int NQ, int NS>
 __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict__ T, int pair_base,
                                                         const int32_t* __restrict__ uni,
                                                         const int32_t* __restrict__ blk_off,
-                                                        const int32_t* __restrict__ uoff,
                                                         const int32_t* __restrict__ ucount,
-                                                        const float* __restrict__ alpha_blk, int n, int nblk, int bpx,
+                                                        const int64_t* __restrict__ row_ptr,
+                                                        const int32_t* __restrict__ order,
+                                                        const int32_t* __restrict__ edge_slot,
+                                                        const float* __restrict__ alpha, int n, int nblk, int bpx,
                                                         int ntg, int ntg4, int dimT, int C, int dh, int H,
                                                         float* __restrict__ S) {
   __shared__ int64_t ubl[kPiece];     // float4 offset of each union row of the piece in T
@@ -435,7 +420,14 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
   for (int g = 0; g < kAggGroups; ++g) acc[g] = (v4f){0.f, 0.f, 0.f, 0.f};
   const int nu = ucount[b];
   const int32_t* ub = uni + blk_off[b];
-  const float4* ab4 = (const float4*)(alpha_blk + ((int64_t)uoff[b] * H + h) * 16);
+  // this thread's receiver for the A operand build: 16 threads per receiver
+  const int rr = threadIdx.x >> 4, rl = threadIdx.x & 15;
+  int64_t e0 = 0, e1 = 0;
+  if (b * 16 + rr < n) {
+    const int i = order[b * 16 + rr];
+    e0 = row_ptr[i];
+    e1 = row_ptr[i + 1];
+  }
   const float4* T4 = (const float4*)T;
   const bool active = tg < ntg;  // uniform over the wave
   // Union rows 4 at a time (lane row k); rows past the piece take weight 0
@@ -462,25 +454,40 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
   };
   for (int p0 = 0; p0 < nu; p0 += kPiece) {
     const int np = min(nu - p0, kPiece);
-    // staging: every thread issues its loads, then its stores, at clamped
-    // indexes with no branch (slots past the piece hold copies, never read)
+    // staging: the piece's 64-bit T row offsets and A = the attention
+    // weights of the block's edges whose union slot falls in the piece,
+    // scattered into a zeroed LDS tile.  All global loads of a batch are
+    // issued (clamped indexes, no branch) before the first store.
     {
       static_assert(kPiece == 2 * 256, "staging assumes 256 threads");
+      constexpr int kEB = 4;  // edges per thread per batch (16 threads per receiver)
       __syncthreads();
       const int t = threadIdx.x;
       const int32_t u0 = ub[p0 + min(t, np - 1)], u1 = ub[p0 + min(t + 256, np - 1)];
+      int sl[kEB];
+      float av[kEB];
+      auto load_edges = [&](int64_t eb) {
+#pragma unroll
+        for (int u = 0; u < kEB; ++u) {
+          const int64_t ec = min(eb + 16 * u, e1 - 1);
+          sl[u] = edge_slot[ec] - p0;
+          av[u] = alpha ? alpha[ec * H + h] : 1.0f;
+        }
+      };
+      auto store_edges = [&](int64_t eb) {
+        float* Alw = (float*)Al4;
+#pragma unroll
+        for (int u = 0; u < kEB; ++u)
+          if (eb + 16 * u < e1 && sl[u] >= 0 && sl[u] < np) Alw[sl[u] * 16 + rr] = av[u];
+      };
+      if (e0 < e1) load_edges(e0 + rl);
       ubl[t] = (int64_t)(u0 - pair_base) * W4;
       ubl[t + 256] = (int64_t)(u1 - pair_base) * W4;
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        float4 v[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int q = min(t + 256 * (4 * half + u), 4 * np - 1);
-          v[u] = ab4[(int64_t)(p0 + q / 4) * H * 4 + q % 4];
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) Al4[t + 256 * (4 * half + u)] = v[u];
+      for (int q = t; q < 4 * np; q += 256) Al4[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+      __syncthreads();
+      for (int64_t eb = e0 + rl; eb < e1; eb += 16 * kEB) {
+        if (eb != e0 + rl) load_edges(eb);
+        store_edges(eb);
       }
       __syncthreads();
     }
@@ -1003,8 +1010,8 @@ size_t blocks_tmp_bytes(int nblk) {
 }
 
 hipError_t launch_block_union(const int64_t* row_ptr, const int32_t* col_pair, const int32_t* order, int n,
-                              int32_t* blk_count, int32_t* blk_off, int32_t* uni, int32_t* ucount, int32_t* uoff,
-                              int32_t* edge_slot, void* tmp, size_t tmp_bytes, hipStream_t s) {
+                              int32_t* blk_count, int32_t* blk_off, int32_t* uni, int32_t* ucount, int32_t* edge_slot,
+                              void* tmp, size_t tmp_bytes, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int G = 16;
   const int nblk = (n + G - 1) / G;
@@ -1017,25 +1024,13 @@ hipError_t launch_block_union(const int64_t* row_ptr, const int32_t* col_pair, c
   const size_t lds = 2 * sizeof(int32_t) * kUnionMax;
   if ((e = allow_lds(k_block_union, lds)) != hipSuccess) return e;
   k_block_union<<<nblk, 256, lds, s>>>(row_ptr, col_pair, order, n, G, blk_off, uni, ucount, edge_slot);
-  b = tmp_bytes;
-  if ((e = hipcub::DeviceScan::ExclusiveSum(tmp, b, ucount, uoff, nblk + 1, s)) != hipSuccess) return e;
-  return hipGetLastError();
-}
-
-hipError_t launch_block_alpha(const int64_t* row_ptr, const int32_t* order, int n, const int32_t* uoff,
-                              const int32_t* edge_slot, const float* alpha, int H, int64_t union_rows,
-                              float* alpha_blk, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  hipError_t e = hipMemsetAsync(alpha_blk, 0, sizeof(float) * (size_t)union_rows * H * 16, s);
-  if (e != hipSuccess) return e;
-  k_block_alpha<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, order, n, uoff, edge_slot, alpha, H, alpha_blk);
   return hipGetLastError();
 }
 
 hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_ptr, const int32_t* col_pair,
                             const float* alpha, const int32_t* order, const int32_t* uni, const int32_t* blk_off,
-                            const int32_t* uoff, const int32_t* ucount, const float* alpha_blk, bool use_blocks, int n,
-                            int dimT, int C, int H, float* S, hipStream_t s) {
+                            const int32_t* ucount, const int32_t* edge_slot, bool use_blocks, int n, int dimT, int C,
+                            int H, float* S, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int dh = C / H;
   if (use_blocks) {
@@ -1050,8 +1045,9 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
 #define E2F_AGG(NQ_, NS_)                                                                                  \
   if (nq == NQ_ && ns == NS_) {                                                                           \
-    k_aggregate_mfma<NQ_, NS_><<<(unsigned)blocks, 256, 0, s>>>(T, pair_base, uni, blk_off, uoff, ucount,  \
-                                                              alpha_blk, n, nblk, bpx, ntg, ntg4, dimT, C, dh, H, S); \
+    k_aggregate_mfma<NQ_, NS_><<<(unsigned)blocks, 256, 0, s>>>(T, pair_base, uni, blk_off, ucount, row_ptr, \
+                                                              order, edge_slot, alpha, n, nblk, bpx, ntg, ntg4,   \
+                                                              dimT, C, dh, H, S);                                \
     return hipGetLastError();                                                                             \
   }
     E2F_AGG(2, 2) E2F_AGG(2, 3) E2F_AGG(2, 4) E2F_AGG(2, 6) E2F_AGG(4, 2) E2F_AGG(4, 3) E2F_AGG(4, 4)

@@ -63,25 +63,21 @@ hipError_t launch_sort_receivers(const float* pos, const int32_t* tile_of, int n
 // Receiver blocks of 16 consecutive entries of `order`: block edge counts
 // (blk_count [nblk+1]) and offsets (blk_off [nblk+1]), the sorted union of the
 // T rows each block reads (uni [E], block b at blk_off[b]), union sizes
-// (ucount [nblk+1]) and offsets (uoff [nblk+1]; uoff[nblk] = union rows) and
-// the union position of every edge (edge_slot [E]).  Requires 16 * (largest
+// (ucount [nblk+1]) and the union position of every edge (edge_slot [E]).  Requires 16 * (largest
 // degree) <= 8192.
 constexpr int kBlockMaxDegree = 512;
 size_t blocks_tmp_bytes(int nblk);
 hipError_t launch_block_union(const int64_t* row_ptr, const int32_t* col_pair, const int32_t* order, int n,
-                              int32_t* blk_count, int32_t* blk_off, int32_t* uni, int32_t* ucount, int32_t* uoff,
-                              int32_t* edge_slot, void* tmp, size_t tmp_bytes, hipStream_t s);
-// alpha_blk [union_rows][H][16]: attention weight of (union row, head, receiver), 0 without an edge
-hipError_t launch_block_alpha(const int64_t* row_ptr, const int32_t* order, int n, const int32_t* uoff,
-                              const int32_t* edge_slot, const float* alpha, int H, int64_t union_rows,
-                              float* alpha_blk, hipStream_t s);
+                              int32_t* blk_count, int32_t* blk_off, int32_t* uni, int32_t* ucount, int32_t* edge_slot,
+                              void* tmp, size_t tmp_bytes, hipStream_t s);
 // S[r] for the n receivers order[0..n) (S rows follow that order); T holds the
 // pairs from pair_base on.  use_blocks: MFMA form over the block plan (built
-// for the same n receivers); else per-receiver rows from L2.
+// for the same n receivers; the attention operand is assembled from alpha and
+// edge_slot); else per-receiver rows from L2.
 hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_ptr, const int32_t* col_pair,
                             const float* alpha, const int32_t* order, const int32_t* uni, const int32_t* blk_off,
-                            const int32_t* uoff, const int32_t* ucount, const float* alpha_blk, bool use_blocks, int n,
-                            int dimT, int C, int H, float* S, hipStream_t s);
+                            const int32_t* ucount, const int32_t* edge_slot, bool use_blocks, int n, int dimT, int C,
+                            int H, float* S, hipStream_t s);
 // y[order[r]] from S row r (head-major like T), r < n
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, const int32_t* order, int n, int C,
                            int dh, float* y, hipStream_t s);

@@ -187,6 +187,28 @@ def test_conv_edge_cases(e2f, ctx):
         assert np.all(got == 0)
 
 
+@pytest.mark.parametrize("C,H", [(12, 3), (48, 4), (256, 8)])
+def test_mixing_channel_counts(e2f, ctx, C, H):
+    # channel mixing on both kernels: MFMA (C a multiple of 16 up to 128) and
+    # the VALU fallback (other C), fp32 and bf16 weights
+    rng = np.random.default_rng(C)
+    L, n = 2, 61
+    pos = syn.quantize(rng.uniform(0, 10, size=(n, 3)))
+    rp, ci = o.neighbor_list(pos, 4.5)
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    alpha = rng.uniform(0.0, 1.0, size=(len(ci), H)).astype(np.float32)
+    mix = (rng.standard_normal((L + 1, C, C)) / np.sqrt(C)).astype(np.float32)
+    w = rng.uniform(0.2, 1.0, size=(L + 1) ** 3)
+    ref = o.layer(L, H, pos, feat, rp, ci, alpha, w, mix)
+    for bf16, tol in ((False, TOL_F32), (True, TOL_BF16)):
+        mw = gpu(mix).to(torch.bfloat16) if bf16 else gpu(mix)
+        for fn in (e2f.e2f_wigner6j_conv_forward, e2f.e2f_edge_tp_conv_forward):
+            got = fn(ctx, gpu(pos), gpu(feat), gpu(rp), gpu(ci), gpu(alpha), L, H, 4.5, path_w=w,
+                     mix_w=mw).cpu().numpy()
+            err = o.max_rel_err(got, ref, L)
+            assert err <= tol, (C, bf16, fn.__name__, err)
+
+
 def test_determinism_and_translation(e2f, ctx):
     inp, rp, ci, alpha = case("water2000_L4")
     wl = inp.workload
