@@ -375,8 +375,8 @@ __global__ __launch_bounds__(256) void k_block_union(const int64_t* __restrict__
 constexpr int kXcds = 8;
 constexpr int kPiece = 512;  // union rows staged in LDS at a time
 
-template <int NQ, int NS>
-__global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict__ T, int pair_base,
+template <int NQ, int NS, int WV>
+__global__ __launch_bounds__(64 * WV) void k_aggregate_mfma(const float* __restrict__ T, int pair_base,
                                                         const int32_t* __restrict__ uni,
                                                         const int32_t* __restrict__ blk_off,
                                                         const int32_t* __restrict__ ucount,
@@ -384,7 +384,7 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
                                                         const int32_t* __restrict__ order,
                                                         const int32_t* __restrict__ edge_slot,
                                                         const float* __restrict__ alpha, int n, int nblk, int bpx,
-                                                        int ntg, int ntg4, int dimT, int C, int dh, int H,
+                                                        int ntg, int ntgw, int dimT, int C, int dh, int H,
                                                         float* __restrict__ S) {
   __shared__ int64_t ubl[kPiece];     // float4 offset of each union row of the piece in T
   __shared__ float4 Al4[kPiece * 4];  // Al[slot][receiver]: A operand of head h
@@ -396,9 +396,9 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
   const int xcd = bid % kXcds, local = bid / kXcds;
   const int b = xcd * bpx + local % bpx;
   const int wtask = local / bpx;
-  if (b >= nblk || wtask >= H * ntg4) return;  // uniform over the workgroup
-  const int h = wtask / ntg4;
-  const int tg = (wtask % ntg4) * 4 + (int)(threadIdx.x >> 6);
+  if (b >= nblk || wtask >= H * ntgw) return;  // uniform over the workgroup
+  const int h = wtask / ntgw;
+  const int tg = (wtask % ntgw) * WV + (int)(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int j = lane & 15, k = lane >> 4;
   const int64_t W4 = (int64_t)dimT * C / 4;
@@ -420,10 +420,10 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
   for (int g = 0; g < kAggGroups; ++g) acc[g] = (v4f){0.f, 0.f, 0.f, 0.f};
   const int nu = ucount[b];
   const int32_t* ub = uni + blk_off[b];
-  // this thread's receiver for the A operand build: 16 threads per receiver
+  // the A operand is built by threads 0..255, 16 per receiver
   const int rr = threadIdx.x >> 4, rl = threadIdx.x & 15;
   int64_t e0 = 0, e1 = 0;
-  if (b * 16 + rr < n) {
+  if (rr < 16 && b * 16 + rr < n) {
     const int i = order[b * 16 + rr];
     e0 = row_ptr[i];
     e1 = row_ptr[i + 1];
@@ -459,11 +459,14 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
     // scattered into a zeroed LDS tile.  All global loads of a batch are
     // issued (clamped indexes, no branch) before the first store.
     {
-      static_assert(kPiece == 2 * 256, "staging assumes 256 threads");
+      constexpr int kNT = 64 * WV, kU = kPiece / kNT;
+      static_assert(kPiece % kNT == 0, "piece must split evenly over the threads");
       constexpr int kEB = 4;  // edges per thread per batch (16 threads per receiver)
       __syncthreads();
       const int t = threadIdx.x;
-      const int32_t u0 = ub[p0 + min(t, np - 1)], u1 = ub[p0 + min(t + 256, np - 1)];
+      int32_t uu[kU];
+#pragma unroll
+      for (int u = 0; u < kU; ++u) uu[u] = ub[p0 + min(t + kNT * u, np - 1)];
       int sl[kEB];
       float av[kEB];
       auto load_edges = [&](int64_t eb) {
@@ -481,9 +484,9 @@ __global__ __launch_bounds__(256) void k_aggregate_mfma(const float* __restrict_
           if (eb + 16 * u < e1 && sl[u] >= 0 && sl[u] < np) Alw[sl[u] * 16 + rr] = av[u];
       };
       if (e0 < e1) load_edges(e0 + rl);
-      ubl[t] = (int64_t)(u0 - pair_base) * W4;
-      ubl[t + 256] = (int64_t)(u1 - pair_base) * W4;
-      for (int q = t; q < 4 * np; q += 256) Al4[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int u = 0; u < kU; ++u) ubl[t + kNT * u] = (int64_t)(uu[u] - pair_base) * W4;
+      for (int q = t; q < 4 * np; q += kNT) Al4[q] = make_float4(0.f, 0.f, 0.f, 0.f);
       __syncthreads();
       for (int64_t eb = e0 + rl; eb < e1; eb += 16 * kEB) {
         if (eb != e0 + rl) load_edges(eb);
@@ -1034,24 +1037,25 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
   if (n == 0) return hipSuccess;
   const int dh = C / H;
   if (use_blocks) {
-    // columns per wave: 64*NQ, register stages NS; E2F_AGG_CFG="NQ,NS" overrides (tuning)
-    int nq = 2, ns = 3;
-    if (const char* cfg = getenv("E2F_AGG_CFG")) sscanf(cfg, "%d,%d", &nq, &ns);
+    // columns per wave: 64*NQ, register stages NS, waves per workgroup WV;
+    // E2F_AGG_CFG="NQ,NS,WV" overrides (tuning)
+    int nq = 2, ns = 3, wv = 4;
+    if (const char* cfg = getenv("E2F_AGG_CFG")) sscanf(cfg, "%d,%d,%d", &nq, &ns, &wv);
     const int nblk = (n + 15) / 16;
     const int ntg = (dimT * dh + 64 * nq - 1) / (64 * nq);
-    const int ntg4 = (ntg + 3) / 4;
+    const int ntgw = (ntg + wv - 1) / wv;
     const int bpx = (nblk + kXcds - 1) / kXcds;
-    const int64_t blocks = (int64_t)kXcds * bpx * H * ntg4;
+    const int64_t blocks = (int64_t)kXcds * bpx * H * ntgw;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-#define E2F_AGG(NQ_, NS_)                                                                                  \
-  if (nq == NQ_ && ns == NS_) {                                                                           \
-    k_aggregate_mfma<NQ_, NS_><<<(unsigned)blocks, 256, 0, s>>>(T, pair_base, uni, blk_off, ucount, row_ptr, \
-                                                              order, edge_slot, alpha, n, nblk, bpx, ntg, ntg4,   \
-                                                              dimT, C, dh, H, S);                                \
+#define E2F_AGG(NQ_, NS_, WV_)                                                                             \
+  if (nq == NQ_ && ns == NS_ && wv == WV_) {                                                              \
+    k_aggregate_mfma<NQ_, NS_, WV_><<<(unsigned)blocks, 64 * WV_, 0, s>>>(                                \
+        T, pair_base, uni, blk_off, ucount, row_ptr, order, edge_slot, alpha, n, nblk, bpx, ntg, ntgw, dimT, C, \
+        dh, H, S);                                                                                        \
     return hipGetLastError();                                                                             \
   }
-    E2F_AGG(2, 2) E2F_AGG(2, 3) E2F_AGG(2, 4) E2F_AGG(2, 6) E2F_AGG(4, 2) E2F_AGG(4, 3) E2F_AGG(4, 4)
-    E2F_AGG(6, 2) E2F_AGG(8, 2)
+    E2F_AGG(2, 2, 4) E2F_AGG(2, 3, 4) E2F_AGG(2, 4, 4) E2F_AGG(2, 3, 8) E2F_AGG(2, 3, 2) E2F_AGG(4, 3, 4)
+    E2F_AGG(4, 3, 8) E2F_AGG(6, 2, 4)
 #undef E2F_AGG
     return hipErrorInvalidValue;
   }
