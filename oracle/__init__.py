@@ -56,6 +56,8 @@ def lib():
             L.e2fo_neighbor_list.argtypes = [p, p, i, ctypes.c_float, p, p, i64]
             L.e2fo_neighbor_list_cells.restype = i64
             L.e2fo_neighbor_list_cells.argtypes = [p, p, i, ctypes.c_float, p, p, i64]
+            L.e2fo_knn_graph.restype = i64
+            L.e2fo_knn_graph.argtypes = [p, p, i, i, p, p, i64]
             L.e2fo_conv_edge.restype = i
             L.e2fo_conv_edge.argtypes = [i, i, i, p, p, i, p, p, p, p, p, i, p]
             L.e2fo_conv_factorised.restype = i
@@ -125,6 +127,21 @@ def neighbor_list(pos, cutoff: float, graph_id=None, method: str = "auto"):
     E = fn(_ptr(pos), _ptr(gid), n, float(cutoff), _ptr(row_ptr), None, 0)
     col = np.zeros(max(E, 1), dtype=np.int32)
     E2 = fn(_ptr(pos), _ptr(gid), n, float(cutoff), _ptr(row_ptr), _ptr(col), E)
+    assert E2 == E
+    return row_ptr, col[:E]
+
+
+def knn_graph(pos, k: int, graph_id=None):
+    """k-nearest-neighbour graph as CSR (Sec. 4.1 sparse graphs): row i holds
+    the min(k, n_g - 1) atoms of i's graph first in (grid distance, index)
+    order, by ascending index."""
+    pos = _c(pos, np.float32)
+    gid = _c(graph_id, np.int32)
+    n = pos.shape[0]
+    row_ptr = np.zeros(n + 1, dtype=np.int64)
+    E = lib().e2fo_knn_graph(_ptr(pos), _ptr(gid), n, int(k), _ptr(row_ptr), None, 0)
+    col = np.zeros(max(E, 1), dtype=np.int32)
+    E2 = lib().e2fo_knn_graph(_ptr(pos), _ptr(gid), n, int(k), _ptr(row_ptr), _ptr(col), E)
     assert E2 == E
     return row_ptr, col[:E]
 

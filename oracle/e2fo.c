@@ -18,6 +18,9 @@
  *   - the recoupling weights X of Def. 2.3 as an overlap of coupling trees;
  *   - the radius graph: every ordered pair i != j of one graph with
  *     |r_i - r_j| < cutoff, evaluated exactly on the 2^-16 A grid;
+ *   - the k-nearest-neighbour graph of the paper's sparse scaling workloads
+ *     (Sec. 4.1, Fig. 2): per atom the k others of its graph that come first
+ *     in (squared grid distance, index) order;
  *   - the layer by its definition (Def. 3.1 with attention weights, App. D.2
  *     setup): y_i = sum_j alpha_ij sum_{a,f} w_afo [h_j^(a) (x) R^(f)(r_i - r_j)]^(o);
  *   - the layer by the node factorisation of Thm. 3.3 / Alg. 1 (for the
@@ -248,6 +251,76 @@ int64_t e2fo_neighbor_list(const float *pos, const int32_t *graph_id, int n, flo
         int64_t e = row_ptr[i];
         for (int j = 0; j < n; ++j)
             if (j != i && (!graph_id || graph_id[i] == graph_id[j]) && in_range(pos, i, j, r2)) col_idx[e++] = j;
+    }
+    return E;
+}
+
+/* ---------- k-nearest-neighbour graph (Sec. 4.1, Fig. 2 sparse graphs) ----------
+ * Row i holds the min(k, n_g - 1) atoms j != i of i's graph (n_g atoms) that
+ * come first in the order of (squared distance on the 2^-16 A grid, then
+ * index j); the row lists them by ascending j.  Distances are exact 64-bit
+ * integers (|x| < 16384 A).  Returns E; col_idx is written only if E <= cap. */
+typedef struct {
+    int64_t d2;
+    int32_t j;
+} knn_cand;
+
+static int cmp_i32_knn(const void *x, const void *y) {
+    int32_t a = *(const int32_t *)x, b = *(const int32_t *)y;
+    return (a > b) - (a < b);
+}
+
+static int cmp_cand(const void *x, const void *y) {
+    const knn_cand *a = (const knn_cand *)x, *b = (const knn_cand *)y;
+    if (a->d2 != b->d2) return (a->d2 > b->d2) - (a->d2 < b->d2);
+    return (a->j > b->j) - (a->j < b->j);
+}
+
+static int64_t grid_d2(const float *pos, int i, int j) {
+    int64_t d2 = 0;
+    for (int k = 0; k < 3; ++k) {
+        int64_t dx = llrint((double)pos[3 * i + k] * 65536.0) - llrint((double)pos[3 * j + k] * 65536.0);
+        d2 += dx * dx;
+    }
+    return d2;
+}
+
+int64_t e2fo_knn_graph(const float *pos, const int32_t *graph_id, int n, int k, int64_t *row_ptr, int32_t *col_idx,
+                       int64_t cap) {
+    int64_t *cnt = (int64_t *)calloc((size_t)n, sizeof(int64_t));
+#pragma omp parallel for schedule(dynamic, 64)
+    for (int i = 0; i < n; ++i) {
+        int64_t c = 0;
+        for (int j = 0; j < n; ++j)
+            if (j != i && (!graph_id || graph_id[i] == graph_id[j])) ++c;
+        cnt[i] = c < k ? c : k;
+    }
+    row_ptr[0] = 0;
+    for (int i = 0; i < n; ++i) row_ptr[i + 1] = row_ptr[i] + cnt[i];
+    const int64_t E = row_ptr[n];
+    free(cnt);
+    if (!col_idx || E > cap) return E;
+#pragma omp parallel
+    {
+        knn_cand *cand = (knn_cand *)malloc(sizeof(knn_cand) * (size_t)(n > 0 ? n : 1));
+        int32_t *row = (int32_t *)malloc(sizeof(int32_t) * (size_t)(k > 0 ? k : 1));
+#pragma omp for schedule(dynamic, 16)
+        for (int i = 0; i < n; ++i) {
+            int m = 0;
+            for (int j = 0; j < n; ++j)
+                if (j != i && (!graph_id || graph_id[i] == graph_id[j])) {
+                    cand[m].d2 = grid_d2(pos, i, j);
+                    cand[m].j = j;
+                    ++m;
+                }
+            qsort(cand, (size_t)m, sizeof(knn_cand), cmp_cand);
+            const int take = m < k ? m : k;
+            for (int q = 0; q < take; ++q) row[q] = cand[q].j;
+            qsort(row, (size_t)take, sizeof(int32_t), cmp_i32_knn);
+            for (int q = 0; q < take; ++q) col_idx[row_ptr[i] + q] = row[q];
+        }
+        free(cand);
+        free(row);
     }
     return E;
 }

@@ -355,6 +355,56 @@ def small_graph(L, n, C, H, seed, box=4.0, cutoff=3.0):
     return pos, rp, ci, feat, alpha, w
 
 
+def test_knn_graph_closed_forms():
+    """kNN graph (Sec. 4.1 sparse workloads): lattice distances are known in
+    closed form (a, a*sqrt2, a*sqrt3), so the selected sets are too, ties
+    included (equal distances are taken in index order)."""
+    a = 1.5  # exact on the 2^-16 grid
+    g = np.array(list(itertools.product(range(5), repeat=3)), dtype=np.float32) * a  # index = 25x + 5y + z
+    idx = lambda x, y, z: 25 * x + 5 * y + z
+    c = idx(2, 2, 2)
+    faces = {idx(2 + dx, 2 + dy, 2 + dz) for dx, dy, dz in itertools.product((-1, 0, 1), repeat=3)
+             if abs(dx) + abs(dy) + abs(dz) == 1}
+    edges = {idx(2 + dx, 2 + dy, 2 + dz) for dx, dy, dz in itertools.product((-1, 0, 1), repeat=3)
+             if abs(dx) + abs(dy) + abs(dz) == 2}
+    corners = {idx(2 + dx, 2 + dy, 2 + dz) for dx, dy, dz in itertools.product((-1, 0, 1), repeat=3)
+               if abs(dx) + abs(dy) + abs(dz) == 3}
+    for k, want in [(6, faces), (7, faces | {min(edges)}), (18, faces | edges), (26, faces | edges | corners),
+                    (20, faces | edges | set(sorted(corners)[:2]))]:
+        rp, ci = o.knn_graph(g, k)
+        row = ci[rp[c]:rp[c + 1]]
+        assert list(row) == sorted(want), k
+        assert np.all(np.diff(rp) == k)
+    # corner atom (0,0,0): 3 at a, 3 at sqrt2 a, then (1,1,1) at sqrt3 a, closer
+    # than the three at 2a
+    rp, ci = o.knn_graph(g, 7)
+    row = set(ci[rp[0]:rp[1]])
+    assert row == {idx(1, 0, 0), idx(0, 1, 0), idx(0, 0, 1), idx(1, 1, 0), idx(1, 0, 1), idx(0, 1, 1), idx(1, 1, 1)}
+
+
+def test_knn_graph_invariants():
+    rng = np.random.default_rng(5)
+    pos = syn.quantize(rng.uniform(0, 12, size=(150, 3)))
+    gid = np.repeat(np.arange(3), 50).astype(np.int32)
+    gid[-1] = 7  # a graph of one atom: empty row
+    for k, graph in [(9, None), (9, gid), (200, None)]:
+        rp, ci = o.knn_graph(pos, k, graph)
+        n = len(pos)
+        for i in range(n):
+            row = ci[rp[i]:rp[i + 1]]
+            same = [j for j in range(n) if j != i and (graph is None or graph[j] == graph[i])]
+            assert len(row) == min(k, len(same))
+            assert np.all(np.diff(row) > 0) and i not in row
+            if k >= len(same):
+                assert list(row) == same  # complete graph of the component
+            else:
+                # every chosen atom precedes every other in (distance, index) order
+                X = np.rint(pos.astype(np.float64) * 65536.0).astype(np.int64)
+                key = lambda j: (int(((X[i] - X[j]) ** 2).sum()), j)
+                worst = max(key(j) for j in row)
+                assert all(key(j) > worst for j in same if j not in set(row))
+
+
 @pytest.mark.parametrize("L", [0, 1, 2, 3, 4])
 def test_factorised_equals_definition(L):
     # Thm. 3.3 and Sec. 4.1: the node-factorised layer gives identical outputs
