@@ -91,6 +91,16 @@ e2f_status e2f_neighbor_list(e2f_ctx* ctx, const float* pos, const int32_t* grap
                              int64_t* row_ptr, int32_t* col_idx, int64_t capacity, int64_t* n_edges,
                              void* stream);
 
+/* k-nearest-neighbour graph (the sparse graphs of the scaling study, Sec. 4.1
+ * and Fig. 2): row i holds the min(k, n_g - 1) atoms j != i of i's graph (n_g
+ * atoms; all atoms if graph_id is NULL) that come first in the order of
+ * (squared distance on the 2^-16 A grid, compared exactly, then index j),
+ * listed by ascending j.  1 <= k <= 512 (E2F_EUNSUPPORTED above).  Arguments,
+ * capacity protocol and errors as for e2f_neighbor_list; graph ids must be
+ * below 2^24.  Every candidate pair is examined (O(N^2) work).  (sync) */
+e2f_status e2f_knn_graph(e2f_ctx* ctx, const float* pos, const int32_t* graph_id, int32_t n, int32_t k,
+                         int64_t* row_ptr, int32_t* col_idx, int64_t capacity, int64_t* n_edges, void* stream);
+
 /* Real regular solid harmonics (Def. 2.1) of p_i = pos_i - origins[origin_id[i]]
  * (origin 0 if origin_id is NULL; the zero vector if origins is NULL),
  * evaluated in float64 and rounded: out [N][(lmax+1)^2] float32. */

@@ -258,10 +258,11 @@ int64_t e2fo_neighbor_list(const float *pos, const int32_t *graph_id, int n, flo
 /* ---------- k-nearest-neighbour graph (Sec. 4.1, Fig. 2 sparse graphs) ----------
  * Row i holds the min(k, n_g - 1) atoms j != i of i's graph (n_g atoms) that
  * come first in the order of (squared distance on the 2^-16 A grid, then
- * index j); the row lists them by ascending j.  Distances are exact 64-bit
- * integers (|x| < 16384 A).  Returns E; col_idx is written only if E <= cap. */
+ * index j); the row lists them by ascending j.  Distances are exact unsigned
+ * 64-bit integers (|x| < 16384 A keeps each of the three squares below 2^62).
+ * Returns E; col_idx is written only if E <= cap. */
 typedef struct {
-    int64_t d2;
+    uint64_t d2;
     int32_t j;
 } knn_cand;
 
@@ -276,11 +277,11 @@ static int cmp_cand(const void *x, const void *y) {
     return (a->j > b->j) - (a->j < b->j);
 }
 
-static int64_t grid_d2(const float *pos, int i, int j) {
-    int64_t d2 = 0;
+static uint64_t grid_d2(const float *pos, int i, int j) {
+    uint64_t d2 = 0;
     for (int k = 0; k < 3; ++k) {
         int64_t dx = llrint((double)pos[3 * i + k] * 65536.0) - llrint((double)pos[3 * j + k] * 65536.0);
-        d2 += dx * dx;
+        d2 += (uint64_t)(dx * dx);
     }
     return d2;
 }

@@ -22,7 +22,7 @@ E2F_F32, E2F_BF16 = 0, 1
 _STATUS = {0: "E2F_OK", 1: "E2F_EINVAL", 2: "E2F_ECAPACITY", 3: "E2F_ENOMEM", 4: "E2F_EDEVICE", 5: "E2F_EUNSUPPORTED"}
 
 # every function declared in include/e2f.h
-EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg",
+EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg", "e2f_knn_graph",
             "e2f_recoupling_weight", "e2f_neighbor_list", "e2f_solid_harmonics", "e2f_node_tp",
             "e2f_wigner6j_conv_forward", "e2f_edge_tp_conv_forward", "e2f_profile", "e2f_profile_read", "e2f_last_plan"]
 
@@ -59,6 +59,8 @@ def _load():
     L.e2f_recoupling_weight.restype = ctypes.c_double
     L.e2f_neighbor_list.argtypes = [p, p, p, i32, f, p, p, i64, ctypes.POINTER(i64), p]
     L.e2f_neighbor_list.restype = i
+    L.e2f_knn_graph.argtypes = [p, p, p, i32, i32, p, p, i64, ctypes.POINTER(i64), p]
+    L.e2f_knn_graph.restype = i
     L.e2f_solid_harmonics.argtypes = [p, p, p, p, i32, i, p, p]
     L.e2f_solid_harmonics.restype = i
     L.e2f_node_tp.argtypes = [p, p, p, p, p, i32, i32, i, p, p]
@@ -173,6 +175,21 @@ def e2f_neighbor_list(ctx: Context, pos: torch.Tensor, cutoff: float, graph_id: 
     col = torch.empty(max(E.value, 1), dtype=torch.int32, device=pos.device)
     _check(lib.e2f_neighbor_list(ctx.handle, _ptr(pos), _ptr(graph_id), n, cutoff, _ptr(row_ptr), _ptr(col),
                                  col.numel(), ctypes.byref(E), _stream(pos.device)), "e2f_neighbor_list")
+    return row_ptr, col[:E.value]
+
+
+def e2f_knn_graph(ctx: Context, pos: torch.Tensor, k: int, graph_id: torch.Tensor | None = None):
+    """k-nearest-neighbour graph as device CSR (row_ptr int64 [N+1], col_idx int32 [E])."""
+    _dev(pos, torch.float32, "pos")
+    _dev(graph_id, torch.int32, "graph_id")
+    n = pos.shape[0]
+    E = ctypes.c_int64(0)
+    row_ptr = torch.empty(n + 1, dtype=torch.int64, device=pos.device)
+    _check(lib.e2f_knn_graph(ctx.handle, _ptr(pos), _ptr(graph_id), n, k, _ptr(row_ptr), None, 0, ctypes.byref(E),
+                             _stream(pos.device)), "e2f_knn_graph", allow=(E2F_ECAPACITY,))
+    col = torch.empty(max(E.value, 1), dtype=torch.int32, device=pos.device)
+    _check(lib.e2f_knn_graph(ctx.handle, _ptr(pos), _ptr(graph_id), n, k, _ptr(row_ptr), _ptr(col), col.numel(),
+                             ctypes.byref(E), _stream(pos.device)), "e2f_knn_graph")
     return row_ptr, col[:E.value]
 
 

@@ -464,6 +464,43 @@ e2f_status e2f_neighbor_list(e2f_ctx* ctx, const float* pos, const int32_t* grap
   return E2F_OK;
 }
 
+e2f_status e2f_knn_graph(e2f_ctx* ctx, const float* pos, const int32_t* graph_id, int32_t n, int32_t k,
+                         int64_t* row_ptr, int32_t* col_idx, int64_t capacity, int64_t* n_edges, void* stream) {
+  if (!ctx) return fail(E2F_EINVAL, "ctx is NULL");
+  if (!row_ptr || !n_edges) return fail(E2F_EINVAL, "row_ptr and n_edges are required");
+  if (n < 0) return fail(E2F_EINVAL, "n < 0");
+  if (n > 0 && !pos) return fail(E2F_EINVAL, "pos is NULL");
+  if (k < 1) return fail(E2F_EINVAL, "k = %d < 1", k);
+  if (k > kKnnMaxK) return fail(E2F_EUNSUPPORTED, "k = %d > %d", k, kKnnMaxK);
+  if (capacity < 0) return fail(E2F_EINVAL, "capacity < 0");
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  if (n == 0) {
+    E2F_HIP(hipMemsetAsync(row_ptr, 0, sizeof(int64_t), s));
+    E2F_HIP(hipStreamSynchronize(s));
+    *n_edges = 0;
+    return col_idx ? E2F_OK : fail(E2F_ECAPACITY, "size query: 0 edges");
+  }
+  int st[kStatsInts];
+  e2f_status rs = run_bbox(ctx, pos, graph_id, n, s, st);
+  if (rs != E2F_OK) return rs;
+  const int64_t ngraph = graph_id ? (int64_t)st[6] + 1 : 1;
+  if (ngraph > (int64_t)1 << 24) return fail(E2F_EUNSUPPORTED, "graph ids above 2^24");
+  rs = ensure(ctx, ctx->a, knn_scratch_bytes(n, (int)ngraph), s);
+  if (rs != E2F_OK) return rs;
+  E2F_TIMED("knn", launch_knn_count(graph_id, n, k, (int)ngraph, ctx->a.p, row_ptr, s));
+  E2F_HIP(hipMemcpyAsync(ctx->pinned, row_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  E2F_HIP(hipStreamSynchronize(s));
+  const int64_t E = ctx->pinned[0];
+  *n_edges = E;
+  if (!col_idx || E > capacity) return fail(E2F_ECAPACITY, "the graph has %lld edges", (long long)E);
+  if (E > std::numeric_limits<int32_t>::max()) return fail(E2F_EUNSUPPORTED, "more than 2^31-1 edges");
+  if (E == 0) return E2F_OK;
+  E2F_TIMED("knn", launch_knn_fill(pos, graph_id, n, k, row_ptr, col_idx, s));
+  return E2F_OK;
+}
+
 e2f_status e2f_solid_harmonics(e2f_ctx* ctx, const float* pos, const float* origins, const int32_t* origin_id,
                                int32_t n, int lmax, float* out, void* stream) {
   if (!ctx) return fail(E2F_EINVAL, "ctx is NULL");

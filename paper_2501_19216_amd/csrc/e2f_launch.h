@@ -28,6 +28,14 @@ hipError_t launch_nl_fill(const float* pos, const int32_t* graph_id, int n, doub
                           void* scratch, const int64_t* row_ptr, int32_t* unsorted, int32_t* col_idx, int64_t E,
                           void* sort_tmp, size_t sort_tmp_bytes, hipStream_t s);
 size_t nl_sort_tmp_bytes(int n, int64_t E);
+// k-nearest-neighbour graph: row sizes min(k, graph size - 1) into row_ptr
+// (graph ids in [0, ngraph)), then the rows (k <= kKnnMaxK).
+constexpr int kKnnMaxK = 512;
+size_t knn_scratch_bytes(int n, int ngraph);
+hipError_t launch_knn_count(const int32_t* graph_id, int n, int k, int ngraph, void* scratch, int64_t* row_ptr,
+                            hipStream_t s);
+hipError_t launch_knn_fill(const float* pos, const int32_t* graph_id, int n, int k, const int64_t* row_ptr,
+                           int32_t* col_idx, hipStream_t s);
 
 // ---- solid harmonics: out[item][k], item -> node node_of[item] (or item),
 // origin origins[origin_id[item] % origin_mod] (or 0 / zero vector)

@@ -117,6 +117,117 @@ __global__ void k_neighbors(const float* __restrict__ pos, const int32_t* __rest
 
 __global__ void k_zero_last(int64_t* counts, int n) { counts[n] = 0; }
 
+// ---------------------------------------------------------------- kNN graph
+// k nearest neighbours (the sparse graphs of the scaling study, Sec. 4.1):
+// row i holds the min(k, n_g - 1) atoms j != i of i's graph that come first
+// in (squared distance on the 2^-16 A grid, index) order, by ascending index.
+// Row sizes follow from the graph sizes alone (integer atomics); the rows
+// are filled by one workgroup per receiver that streams every candidate,
+// keeps those ahead of the current k-th (distance, index) pair in an LDS
+// buffer and cuts the buffer back to k by a bitonic sort when it could
+// overflow.  The result does not depend on the order of arrival.
+constexpr int kKnnBuf = 2048;
+
+__global__ void k_knn_graph_sizes(const int32_t* __restrict__ gid, int n, int* __restrict__ gsize) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) atomicAdd(&gsize[gid ? gid[i] : 0], 1);
+}
+
+__global__ void k_knn_row_sizes(const int32_t* __restrict__ gid, int n, int k, const int* __restrict__ gsize,
+                                int64_t* __restrict__ counts) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) counts[i] = min(k, gsize[gid ? gid[i] : 0] - 1);
+  if (i == 0) counts[n] = 0;
+}
+
+__device__ __forceinline__ bool knn_less(uint64_t da, int ja, uint64_t db, int jb) {
+  return da < db || (da == db && ja < jb);
+}
+
+// bitonic sort of (d, j)[0, m) ascending, m a power of two, 256 threads
+__device__ void knn_sort(uint64_t* d, int32_t* j, int m) {
+  for (int size = 2; size <= m; size <<= 1)
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int t = threadIdx.x; t < m / 2; t += blockDim.x) {
+        const int lo = 2 * t - (t & (stride - 1)), hi = lo + stride;
+        const bool up = (lo & size) == 0;
+        if (knn_less(d[hi], j[hi], d[lo], j[lo]) == up) {
+          const uint64_t td = d[lo];
+          d[lo] = d[hi];
+          d[hi] = td;
+          const int32_t tj = j[lo];
+          j[lo] = j[hi];
+          j[hi] = tj;
+        }
+      }
+      __syncthreads();
+    }
+}
+
+__global__ __launch_bounds__(256) void k_knn_fill(const float* __restrict__ pos, const int32_t* __restrict__ gid,
+                                                  int n, int k, const int64_t* __restrict__ row_ptr,
+                                                  int32_t* __restrict__ col) {
+  __shared__ uint64_t bd[kKnnBuf];
+  __shared__ int32_t bj[kKnnBuf];
+  __shared__ int cnt;
+  __shared__ uint64_t thr_d;
+  __shared__ int thr_j;
+  const int i = blockIdx.x, t = threadIdx.x;
+  const int64_t r0 = row_ptr[i];
+  const int m = (int)(row_ptr[i + 1] - r0);  // min(k, n_g - 1)
+  if (m == 0) return;                          // uniform over the workgroup
+  const int gi = gid ? gid[i] : 0;
+  const int64_t xi = grid_coord(pos[3 * i]), yi = grid_coord(pos[3 * i + 1]), zi = grid_coord(pos[3 * i + 2]);
+  if (t == 0) {
+    cnt = 0;
+    thr_d = ~0ull;
+    thr_j = INT_MAX;
+  }
+  __syncthreads();
+  for (int j0 = 0; j0 < n; j0 += blockDim.x) {
+    const int j = j0 + t;
+    if (j < n && j != i && (!gid || gid[j] == gi)) {
+      const int64_t dx = grid_coord(pos[3 * j]) - xi, dy = grid_coord(pos[3 * j + 1]) - yi,
+                    dz = grid_coord(pos[3 * j + 2]) - zi;
+      const uint64_t d = (uint64_t)(dx * dx) + (uint64_t)(dy * dy) + (uint64_t)(dz * dz);
+      if (knn_less(d, j, thr_d, thr_j)) {
+        const int p = atomicAdd(&cnt, 1);  // < kKnnBuf: the buffer is cut below kKnnBuf - 256
+        bd[p] = d;
+        bj[p] = j;
+      }
+    }
+    __syncthreads();
+    const int c = cnt;  // the same in every thread: nobody appends before the next barrier
+    __syncthreads();
+    if (c > kKnnBuf - (int)blockDim.x || (j0 + (int)blockDim.x >= n && c > 0)) {
+      for (int q = c + t; q < kKnnBuf; q += blockDim.x) {
+        bd[q] = ~0ull;
+        bj[q] = INT_MAX;
+      }
+      __syncthreads();
+      knn_sort(bd, bj, kKnnBuf);
+      if (t == 0) {
+        cnt = min(c, k);
+        if (c >= k) {
+          thr_d = bd[k - 1];
+          thr_j = bj[k - 1];
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // the m nearest are bd/bj[0, m); write them by ascending index
+  int p2 = 1;
+  while (p2 < m) p2 <<= 1;
+  for (int q = t; q < p2; q += blockDim.x) {
+    bd[q] = 0;
+    if (q >= m) bj[q] = INT_MAX;
+  }
+  __syncthreads();
+  knn_sort(bd, bj, p2);
+  for (int q = t; q < m; q += blockDim.x) col[r0 + q] = bj[q];
+}
+
 Grid to_grid(const CellGrid& cg) {
   return Grid{cg.lo[0], cg.lo[1], cg.lo[2], cg.dim[0], cg.dim[1], cg.dim[2], cg.side};
 }
@@ -220,6 +331,35 @@ hipError_t launch_nl_fill(const float* pos, const int32_t* graph_id, int n, doub
   e = hipcub::DeviceSegmentedRadixSort::SortKeys(sort_tmp, tb, unsorted, col_idx, (int)E, n, row_ptr, row_ptr + 1, 0,
                                                  bits, st);
   if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+size_t knn_scratch_bytes(int n, int ngraph) {
+  return align256(sizeof(int) * (size_t)ngraph) + align256(sizeof(int64_t) * (size_t)(n + 1)) +
+         align256(scan_bytes_counts(n));
+}
+
+hipError_t launch_knn_count(const int32_t* graph_id, int n, int k, int ngraph, void* scratch, int64_t* row_ptr,
+                            hipStream_t s) {
+  char* p = (char*)scratch;
+  int* gsize = (int*)p;
+  p += align256(sizeof(int) * (size_t)ngraph);
+  int64_t* counts = (int64_t*)p;
+  p += align256(sizeof(int64_t) * (size_t)(n + 1));
+  void* tmp = p;
+  hipError_t e = hipMemsetAsync(gsize, 0, sizeof(int) * (size_t)ngraph, s);
+  if (e != hipSuccess) return e;
+  k_knn_graph_sizes<<<(n + 255) / 256, 256, 0, s>>>(graph_id, n, gsize);
+  k_knn_row_sizes<<<(n + 256) / 256, 256, 0, s>>>(graph_id, n, k, gsize, counts);
+  size_t b = scan_bytes_counts(n);
+  if ((e = hipcub::DeviceScan::ExclusiveSum(tmp, b, counts, row_ptr, n + 1, s)) != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_knn_fill(const float* pos, const int32_t* graph_id, int n, int k, const int64_t* row_ptr,
+                           int32_t* col_idx, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  k_knn_fill<<<n, 256, 0, s>>>(pos, graph_id, n, k, row_ptr, col_idx);
   return hipGetLastError();
 }
 

@@ -104,6 +104,13 @@ def test_other_argument_checks(e2f):
     assert lib.e2f_neighbor_list(ctx.handle, FAKE, None, 10, 65.0, FAKE, None, 0, ctypes.byref(E), None) == e2f.E2F_EINVAL
     assert lib.e2f_neighbor_list(ctx.handle, FAKE, None, 10, 5.0, None, None, 0, ctypes.byref(E), None) == e2f.E2F_EINVAL
     assert lib.e2f_neighbor_list(None, FAKE, None, 10, 5.0, FAKE, None, 0, ctypes.byref(E), None) == e2f.E2F_EINVAL
+    knn = lambda k, rp=FAKE, handle=ctx.handle: lib.e2f_knn_graph(handle, FAKE, None, 10, k, rp, None, 0,
+                                                                  ctypes.byref(E), None)
+    assert knn(8) == e2f.E2F_EDEVICE
+    assert knn(0) == e2f.E2F_EINVAL
+    assert knn(513) == e2f.E2F_EUNSUPPORTED
+    assert knn(8, rp=None) == e2f.E2F_EINVAL
+    assert knn(8, handle=None) == e2f.E2F_EINVAL
     assert lib.e2f_solid_harmonics(ctx.handle, FAKE, None, None, 10, 7, FAKE, None) == e2f.E2F_EINVAL
     assert lib.e2f_solid_harmonics(ctx.handle, FAKE, None, None, 10, 3, FAKE, None) == e2f.E2F_EDEVICE
     assert lib.e2f_node_tp(ctx.handle, FAKE, None, None, FAKE, 10, 6, 3, FAKE, None) == e2f.E2F_EUNSUPPORTED

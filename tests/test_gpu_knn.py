@@ -1,0 +1,94 @@
+"""GPU k-nearest-neighbour graph (the sparse graphs of the scaling study,
+Sec. 4.1 / Fig. 2) against the oracle, bit-exact, and the Wigner-6j layer on
+kNN graphs against the oracle's definition of the layer.
+
+Run with -m gpu."""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import e2f_synth as syn
+import oracle as o
+from cases import TOL_F32
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def e2f():
+    import paper_2501_19216_amd as m
+    return m
+
+
+@pytest.fixture(scope="module")
+def ctx(e2f):
+    c = e2f.e2f_create(6, 0)
+    yield c
+    c.close()
+
+
+def gpu(a):
+    return None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+
+
+def knn_both(e2f, ctx, pos, k, gid=None):
+    rp, ci = e2f.e2f_knn_graph(ctx, gpu(pos), k, gpu(gid))
+    orp, oci = o.knn_graph(pos, k, gid)
+    return rp.cpu().numpy(), ci.cpu().numpy(), orp, oci
+
+
+@pytest.mark.parametrize("n,k,side", [(1000, 32, 21.5), (1000, 512, 21.5), (3000, 8, 31.0), (257, 300, 12.0)])
+def test_knn_bit_exact_random(e2f, ctx, n, k, side):
+    rng = np.random.default_rng(n + k)
+    pos = syn.quantize(rng.uniform(0, side, size=(n, 3)))
+    rp, ci, orp, oci = knn_both(e2f, ctx, pos, k)
+    print("n %d k %d: %d edges" % (n, k, len(oci)))
+    assert np.array_equal(rp, orp) and np.array_equal(ci, oci)
+
+
+def test_knn_bit_exact_ties_and_graphs(e2f, ctx):
+    # a lattice: many equal distances, taken in index order
+    g = np.array(list(itertools.product(range(6), repeat=3)), dtype=np.float32) * 1.5
+    for k in (6, 7, 18, 20, 26, 64):
+        rp, ci, orp, oci = knn_both(e2f, ctx, g, k)
+        assert np.array_equal(rp, orp) and np.array_equal(ci, oci), k
+    # many small graphs (the 256 x 30 molecules) and a graph of one atom
+    inp = syn.make_inputs(syn.WORKLOADS["molecules256x30_L3"])
+    gid = inp.graph_id.copy()
+    gid[-1] = gid.max() + 1
+    for k in (8, 29, 40):
+        rp, ci, orp, oci = knn_both(e2f, ctx, inp.pos, k, gid)
+        assert np.array_equal(rp, orp) and np.array_equal(ci, oci), k
+    assert rp[-1] == rp[-2]  # the lone atom has no neighbours
+
+
+def knn_inputs(n, k, L, C, H, seed):
+    rng = np.random.default_rng(seed)
+    side = (n / 0.1) ** (1.0 / 3.0)  # 0.1 atoms / A^3, like the other workloads
+    pos = syn.quantize(rng.uniform(0, side, size=(n, 3)))
+    rp, ci = o.knn_graph(pos, k)
+    d = np.linalg.norm(pos[np.repeat(np.arange(n), np.diff(rp))] - pos[ci], axis=1)
+    reach = float(d.max()) * 1.001
+    species = rng.integers(0, 10, size=n)
+    alpha = syn.attention_weights(pos, species, rp, ci, H, reach, 10, seed)
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    return pos, rp, ci, alpha, feat, reach
+
+
+@pytest.mark.parametrize("n,k,L,C,H,rows", [(600, 32, 3, 64, 8, None), (1000, 256, 3, 32, 4, 96),
+                                             (400, 32, 6, 16, 4, 64)])
+def test_layer_on_knn_graphs(e2f, ctx, n, k, L, C, H, rows):
+    pos, rp, ci, alpha, feat, reach = knn_inputs(n, k, L, C, H, seed=n + k + L)
+    w = np.zeros((L + 1) ** 3)
+    for a, f, oo in itertools.product(range(L + 1), repeat=3):
+        if abs(a - f) <= oo <= a + f:
+            w[(a * (L + 1) + f) * (L + 1) + oo] = reach ** (-f)
+    r = np.arange(n) if rows is None else np.linspace(0, n - 1, rows).astype(np.int32)
+    ref = o.conv_edge(L, H, pos, feat, rp, ci, alpha, w, rows=r)
+    for fn in (e2f.e2f_wigner6j_conv_forward, e2f.e2f_edge_tp_conv_forward):
+        got = fn(ctx, gpu(pos), gpu(feat), gpu(rp), gpu(ci), gpu(alpha), L, H, reach).cpu().numpy()
+        err = o.max_rel_err(got[r], ref, L)
+        print("kNN n %d k %d L %d %s: err %.3e" % (n, k, L, fn.__name__, err))
+        assert err <= TOL_F32
