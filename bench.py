@@ -138,6 +138,79 @@ def sweep_one(name, steps, warmup):
     return res
 
 
+# The scaling study of the paper (Sec. 4.1, Fig. 2): (b.i) dense graphs
+# (every atom attends to every other, k = 0 below) at L = 3 against N;
+# k-nearest-neighbour graphs: (b.ii, b.iii) k = 32 at L = 2 and 3 against N,
+# (c) N = 1000, k = 32 against L, (d) N = 1000, L = 3 against k.  Channels
+# and heads are not stated there; 128 channels and 8 heads as in the
+# protein-scale workload.
+FIG2 = ([("b.i", 0, 3, n) for n in (250, 500, 1000, 2000, 4000)] +
+        [("b.ii", 32, 2, n) for n in (1000, 2000, 5000, 10000, 20000, 50000)] +
+        [("b.iii", 32, 3, n) for n in (1000, 2000, 5000, 10000, 20000, 50000)] +
+        [("c", 32, L, 1000) for L in (1, 2, 3, 4, 5, 6)] +
+        [("d", k, 3, 1000) for k in (64, 128, 256, 512)])
+
+
+def fig2_point(panel, k, L, n, steps, warmup, C=128, H=8):
+    """6j forward and edge-TP baseline on a kNN graph of n atoms (uniform at
+    0.1 atoms/A^3, minimum distance 0.9 A), timed on the GPU."""
+    import torch
+    import e2f_synth as syn
+    import paper_2501_19216_amd as e2f
+
+    dev = torch.device("cuda:0")
+    seed = 7000 + 10 * L + n + k
+    pos_h = syn.positions_cube(n, syn._cube_side(n), 0.9, seed)
+    rng = np.random.default_rng(seed)
+    species = rng.integers(0, 10, size=n).astype(np.int32)
+    feat = torch.from_numpy(rng.standard_normal((n, (L + 1) ** 2, C), dtype=np.float32)).to(dev)
+    ctx = e2f.e2f_create(L, 0)
+    pos = torch.from_numpy(pos_h).to(dev)
+    ms_knn = None
+    if k > 0:
+        rp, ci = e2f.e2f_knn_graph(ctx, pos, k)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(3):
+            e2f.e2f_knn_graph(ctx, pos, k)
+        torch.cuda.synchronize()
+        ms_knn = (time.perf_counter() - t0) * 1e3 / 3
+        rph, cih = rp.cpu().numpy(), ci.cpu().numpy()
+    else:  # the complete graph, for the per-edge baseline
+        rph = np.arange(0, n * (n - 1) + 1, n - 1, dtype=np.int64)
+        cih = np.delete(np.tile(np.arange(n, dtype=np.int32), n), np.arange(n) * (n + 1))
+        rp, ci = torch.from_numpy(rph).to(dev), torch.from_numpy(cih).to(dev)
+    d = np.linalg.norm(pos_h[np.repeat(np.arange(n), np.diff(rph))] - pos_h[cih], axis=1)
+    reach = float(d.max()) * 1.001  # the graph's longest edge: envelope, default weights, tiles
+    alpha = torch.from_numpy(syn.attention_weights(pos_h, species, rph, cih, H, reach, 10, seed)).to(dev)
+    out = torch.empty_like(feat)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / steps
+
+    if k > 0:
+        ms6 = timed(lambda: e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, rp, ci, alpha, L, H, reach, out=out))
+        pairs, tiles = e2f.e2f_last_plan(ctx)
+    else:
+        dense = torch.zeros(n, n, H, device=dev)
+        dense[torch.from_numpy(np.repeat(np.arange(n), n - 1)).to(dev), ci.long()] = alpha
+        ms6 = timed(lambda: e2f.e2f_wigner6j_conv_forward_dense(ctx, pos, feat, dense, L, H, reach, out=out))
+        pairs, tiles = n, 1
+        del dense
+    mse = timed(lambda: e2f.e2f_edge_tp_conv_forward(ctx, pos, feat, rp, ci, alpha, L, H, reach, out=out))
+    ctx.close()
+    return {"panel": panel, "graph": "knn" if k > 0 else "dense", "k": k, "lmax": L, "atoms": n, "edges": int(len(cih)), "channels": C,
+            "heads": H, "reach": reach, "tiles": tiles, "pairs": pairs, "knn_ms": ms_knn, "fwd_ms": ms6,
+            "edge_tp_ms": mse, "speedup_vs_edge_tp": mse / ms6, "atoms_per_s": n / ms6 * 1e3}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -150,6 +223,9 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="instead: one JSON line per workload (6j forward and edge-TP baseline times and speedup)")
     ap.add_argument("--sweep-workloads", default="", help="comma-separated subset of the sweep (default: all)")
+    ap.add_argument("--paper-fig2", action="store_true",
+                    help="instead: the scaling study on dense and kNN graphs (6j vs edge-TP), one JSON line per point")
+    ap.add_argument("--fig2-panels", default="", help="comma-separated subset of the panels b.i,b.ii,b.iii,c,d")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (no sharding, no collectives).",
@@ -159,6 +235,14 @@ def main():
     import torch
     import e2f_synth as syn
     import paper_2501_19216_amd as e2f
+
+    if args.paper_fig2:
+        panels = [p for p in args.fig2_panels.split(",") if p]
+        for panel, k, L, n in FIG2:
+            if panels and panel not in panels:
+                continue
+            print(json.dumps(fig2_point(panel, k, L, n, args.steps, args.warmup)), flush=True)
+        return
 
     if args.sweep:
         names = [w for w in args.sweep_workloads.split(",") if w] or list(syn.WORKLOADS)

@@ -144,6 +144,19 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* params
                                      const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,
                                      void* stream);
 
+/* The layer on a dense graph (every atom attends to every other atom; the
+ * dense graphs of the scaling study, Sec. 4.1, and Alg. 1 with its attention
+ * tensor alpha in R^{N x N x H}): the sum runs over all j != i.
+ * alpha [N][N][H] float32 (receiver i, sender j, head); alpha[i][i][*] is
+ * ignored; NULL => 1 for every pair.  One origin, the centre of the bounding
+ * box.  The aggregation S_h = A_h T_h is a dense product per head (rocBLAS
+ * strided-batched SGEMM, fp32).  tile_side and cutoff serve only the default
+ * path weights (cutoff^-f).  N^2 H must stay below 4e9.  Workspace: about
+ * N(2 dimT C + N H) floats.  (sync: one small device->host read) */
+e2f_status e2f_wigner6j_conv_forward_dense(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
+                                           const float* feat, int32_t n, const float* alpha, float* out,
+                                           void* stream);
+
 /* The conventional per-edge SO(3) convolution (Def. 3.1): the same layer
  * computed edge by edge with R^(f)(r_i - r_j) and the CG product per edge.
  * Same arguments and output as e2f_wigner6j_conv_forward; graph_id unused. */

@@ -24,7 +24,7 @@ _STATUS = {0: "E2F_OK", 1: "E2F_EINVAL", 2: "E2F_ECAPACITY", 3: "E2F_ENOMEM", 4:
 # every function declared in include/e2f.h
 EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg", "e2f_knn_graph",
             "e2f_recoupling_weight", "e2f_neighbor_list", "e2f_solid_harmonics", "e2f_node_tp",
-            "e2f_wigner6j_conv_forward", "e2f_edge_tp_conv_forward", "e2f_profile", "e2f_profile_read", "e2f_last_plan"]
+            "e2f_wigner6j_conv_forward", "e2f_wigner6j_conv_forward_dense", "e2f_edge_tp_conv_forward", "e2f_profile", "e2f_profile_read", "e2f_last_plan"]
 
 
 class E2FError(RuntimeError):
@@ -75,6 +75,8 @@ def _load():
         fn = getattr(L, name)
         fn.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, i32, p, p, i64, p, p, p]
         fn.restype = i
+    L.e2f_wigner6j_conv_forward_dense.argtypes = [p, ctypes.POINTER(ConvParams), p, p, i32, p, p, p]
+    L.e2f_wigner6j_conv_forward_dense.restype = i
     return L
 
 
@@ -272,6 +274,26 @@ def e2f_edge_tp_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, head
     """Per-edge SO(3) convolution baseline; same output as the 6j forward."""
     return _conv("e2f_edge_tp_conv_forward", ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w,
                  mix_w, graph_id, tile_side, out)
+
+
+def e2f_wigner6j_conv_forward_dense(ctx, pos, feat, alpha, lmax, heads, cutoff, path_w=None, mix_w=None, out=None):
+    """Dense-graph forward (every atom attends to every other): alpha [N,N,H]
+    float32 (receiver, sender, head) or None; returns out [N,(L+1)^2,C]."""
+    _dev(pos, torch.float32, "pos")
+    _dev(feat, torch.float32, "feat")
+    _dev(alpha, torch.float32, "alpha")
+    n, nk, C = feat.shape
+    if alpha is not None and tuple(alpha.shape) != (n, n, heads):
+        raise ValueError("alpha must be [N, N, heads]")
+    if out is None:
+        out = torch.empty_like(feat)
+    _dev(out, torch.float32, "out")
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, 0.0)
+    st = lib.e2f_wigner6j_conv_forward_dense(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(feat), n, _ptr(alpha),
+                                             _ptr(out), _stream(feat.device))
+    del keep
+    _check(st, "e2f_wigner6j_conv_forward_dense")
+    return out
 
 
 def e2f_profile(ctx: Context, enable: bool) -> None:

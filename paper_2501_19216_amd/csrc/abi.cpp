@@ -14,6 +14,8 @@
 #include <vector>
 
 #include "../../include/e2f.h"
+
+#include <rocblas/rocblas.h>
 #include "e2f_internal.h"
 #include "e2f_launch.h"
 
@@ -62,6 +64,7 @@ struct e2f_ctx {
   };
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
+  rocblas_handle blas = nullptr;  // created on the first dense-graph forward
 };
 
 namespace {
@@ -277,8 +280,7 @@ e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStr
 
 bool finite_pos(float x) { return std::isfinite(x) && x > 0.0f; }
 
-e2f_status check_conv(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos, const float* feat, int32_t n,
-                      const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges, float* out) {
+e2f_status check_params(e2f_ctx* ctx, const e2f_conv_params* p) {
   if (!ctx) return fail(E2F_EINVAL, "ctx is NULL");
   if (!p) return fail(E2F_EINVAL, "params is NULL");
   if (p->lmax < 0 || p->lmax > kMaxL) return fail(E2F_EUNSUPPORTED, "lmax %d outside 0..%d", p->lmax, kMaxL);
@@ -296,6 +298,12 @@ e2f_status check_conv(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos, 
     for (int q = 0; q < L1 * L1 * L1; ++q)
       if (!std::isfinite(p->path_w[q])) return fail(E2F_EINVAL, "path_w[%d] is not finite", q);
   }
+  return E2F_OK;
+}
+
+e2f_status check_conv(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos, const float* feat, int32_t n,
+                      const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges, float* out) {
+  if (e2f_status rs = check_params(ctx, p); rs != E2F_OK) return rs;
   if (n < 0) return fail(E2F_EINVAL, "n < 0");
   if (n_edges < 0) return fail(E2F_EINVAL, "n_edges < 0");
   if (n_edges > std::numeric_limits<int32_t>::max()) return fail(E2F_EUNSUPPORTED, "more than 2^31-1 edges");
@@ -381,6 +389,7 @@ void e2f_destroy(e2f_ctx* ctx) {
       if (p) (void)hipFree(p);
     for (Buf* b : {&ctx->a, &ctx->b, &ctx->c})
       if (b->p) (void)hipFree(b->p);
+    if (ctx->blas) (void)rocblas_destroy_handle(ctx->blas);
     for (auto& r : ctx->recs) {
       ctx->pool.push_back(r.start);
       ctx->pool.push_back(r.stop);
@@ -734,6 +743,73 @@ e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, cons
     y = (float*)ctx->c.p;
   }
   E2F_TIMED("edge_tp", launch_edge_tp(ctx->dev[L], pos, feat, row_ptr, col_idx, alpha, n, C, p->heads, y, s));
+  if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
+  return E2F_OK;
+}
+
+e2f_status e2f_wigner6j_conv_forward_dense(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos,
+                                           const float* feat, int32_t n, const float* alpha, float* out,
+                                           void* stream) {
+  e2f_status rs = check_params(ctx, p);
+  if (rs != E2F_OK) return rs;
+  if (n < 0) return fail(E2F_EINVAL, "n < 0");
+  if (n > 0 && (!pos || !feat || !out)) return fail(E2F_EINVAL, "pos, feat and out are required");
+  if ((double)n * n * p->heads > 4.0e9) return fail(E2F_EUNSUPPORTED, "N^2 H = %.3g attention weights", (double)n * n * p->heads);
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  const int L = p->lmax, C = p->channels, H = p->heads, nk = nk_of(L), dh = C / H;
+  rs = set_weights(ctx, L, path_weights(p), s);
+  if (rs != E2F_OK) return rs;
+  if (n == 0) return E2F_OK;
+  const DevTables& t = ctx->dev[L];
+  int st[kStatsInts];
+  rs = run_bbox(ctx, pos, nullptr, n, s, st);
+  if (rs != E2F_OK) return rs;
+  // one origin, the centre of the bounding box (the products couple every pair)
+  double origin[3];
+  for (int k = 0; k < 3; ++k) origin[k] = (((int64_t)st[k] + st[3 + k]) / 2) / kGrid;
+  const size_t rowb = sizeof(float) * (size_t)t.dimT * C;
+  const bool mixing = p->mix_w != nullptr;
+  const size_t need = al256(sizeof(double) * 3) + al256(sizeof(double) * (size_t)n * nk) +
+                      2 * al256(rowb * (size_t)n) + al256(sizeof(float) * (size_t)n * n * H) +
+                      al256(sizeof(int32_t) * (size_t)n) + (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
+  rs = ensure(ctx, ctx->b, need, s);
+  if (rs != E2F_OK) return rs;
+  Carver cb{(char*)ctx->b.p};
+  double* org = cb.take<double>(3);
+  double* R = cb.take<double>((size_t)n * nk);
+  float* T = cb.take<float>((size_t)n * t.dimT * C);
+  float* S = cb.take<float>((size_t)n * t.dimT * C);
+  float* A = cb.take<float>((size_t)n * n * H);
+  int32_t* order = cb.take<int32_t>((size_t)n);
+  float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
+  ctx->origins_host.assign(origin, origin + 3);
+  E2F_HIP(hipMemcpyAsync(org, ctx->origins_host.data(), sizeof(double) * 3, hipMemcpyHostToDevice, s));
+  E2F_TIMED("sh", launch_sh(t, pos, nullptr, org, nullptr, nullptr, 1, n, R, nullptr, s));
+  E2F_TIMED("node_tp", launch_node_tp(t, R, nullptr, feat, n, C, dh, T, s));
+  E2F_TIMED("tile_plan", launch_dense_alpha(alpha, n, H, A, s));
+  E2F_TIMED("tile_plan", launch_iota(n, order, s));
+  if (!ctx->blas) {
+    if (rocblas_create_handle(&ctx->blas) != rocblas_status_success) {
+      ctx->blas = nullptr;
+      return fail(E2F_EDEVICE, "rocblas_create_handle failed");
+    }
+  }
+  if (rocblas_set_stream(ctx->blas, s) != rocblas_status_success) return fail(E2F_EDEVICE, "rocblas_set_stream failed");
+  // per head: S_h^T (W x N) = T_h^T (W x N) . A_h^T (N x N) in column-major terms,
+  // T_h^T and S_h^T with leading dimension dimT*C, A_h^T = A_h stored row-major
+  const rocblas_int W = t.dimT * dh, ld = t.dimT * C;
+  const float one = 1.0f, zero = 0.0f;
+  {
+    Timed tm_(ctx, "aggregate", s);
+    const rocblas_status bs = rocblas_sgemm_strided_batched(ctx->blas, rocblas_operation_none, rocblas_operation_none,
+                                                            W, n, n, &one, T, ld, W, A, n, (rocblas_stride)n * n,
+                                                            &zero, S, ld, W, H);
+    if (bs != rocblas_status_success)
+      return fail(E2F_EDEVICE, "rocblas_sgemm_strided_batched: %s", rocblas_status_to_string(bs));
+  }
+  E2F_TIMED("recouple", launch_recouple(t, R, S, order, n, C, dh, y, s));
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
   return E2F_OK;
 }

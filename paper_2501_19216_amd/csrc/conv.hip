@@ -824,6 +824,25 @@ __global__ __launch_bounds__(64 * kMixWaves) void k_mix_mfma(const float* __rest
   }
 }
 
+// ------------------------------------------------------------ dense graphs
+// Every atom attends to every other (the dense graphs of the scaling study,
+// Sec. 4.1): the aggregation S_h = A_h T_h is a dense product with
+// A_h[i][j] = alpha[i][j][h] for j != i and 0 on the diagonal.
+__global__ void k_dense_alpha(const float* __restrict__ alpha, int n, int H, float* __restrict__ A) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (h, i, j)
+  const int64_t nn = (int64_t)n * n;
+  if (q >= nn * H) return;
+  const int h = (int)(q / nn);
+  const int64_t ij = q - (int64_t)h * nn;
+  const int i = (int)(ij / n), j = (int)(ij - (int64_t)i * n);
+  A[q] = i == j ? 0.0f : (alpha ? alpha[ij * H + h] : 1.0f);
+}
+
+__global__ void k_iota(int n, int32_t* __restrict__ v) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) v[i] = i;
+}
+
 // ------------------------------------------------------------ edge baseline
 // Per receiver block: edges in batches of EB; for each edge the filter
 // K[k][q] = sum_f w_afo sum_mf C^{o m}_{a al, f mf} R^(f)_mf(r_i - r_j) is built
@@ -1145,6 +1164,20 @@ hipError_t launch_edge_tp(const DevTables& t, const float* pos, const float* fea
 #undef E2F_CASE
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_dense_alpha(const float* alpha, int n, int H, float* A, hipStream_t s) {
+  const int64_t total = (int64_t)n * n * H;
+  if (total == 0) return hipSuccess;
+  if ((total + 255) / 256 > 0x7fffffff) return hipErrorInvalidValue;
+  k_dense_alpha<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(alpha, n, H, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_iota(int n, int32_t* v, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  k_iota<<<(n + 255) / 256, 256, 0, s>>>(n, v);
   return hipGetLastError();
 }
 

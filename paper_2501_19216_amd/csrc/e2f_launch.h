@@ -90,6 +90,10 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, const int32_t* order, int n, int C,
                            int dh, float* y, hipStream_t s);
 
+// ---- dense graphs: A[h][i][j] = alpha[i][j][h] (1 if alpha is NULL), 0 for i == j
+hipError_t launch_dense_alpha(const float* alpha, int n, int H, float* A, hipStream_t s);
+hipError_t launch_iota(int n, int32_t* v, hipStream_t s);
+
 // ---- per-irrep channel mixing and the edge baseline
 hipError_t launch_mix(int L, const float* y, const void* W, bool w_bf16, int n, int C, float* out, hipStream_t s);
 hipError_t launch_edge_tp(const DevTables& t, const float* pos, const float* feat, const int64_t* row_ptr,

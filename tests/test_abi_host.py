@@ -115,6 +115,14 @@ def test_other_argument_checks(e2f):
     assert lib.e2f_solid_harmonics(ctx.handle, FAKE, None, None, 10, 3, FAKE, None) == e2f.E2F_EDEVICE
     assert lib.e2f_node_tp(ctx.handle, FAKE, None, None, FAKE, 10, 6, 3, FAKE, None) == e2f.E2F_EUNSUPPORTED
     assert lib.e2f_node_tp(ctx.handle, FAKE, None, None, FAKE, 10, 8, 3, FAKE, None) == e2f.E2F_EDEVICE
+    dense = lambda prm, n=10, pos=FAKE: lib.e2f_wigner6j_conv_forward_dense(
+        ctx.handle, ctypes.byref(prm) if prm is not None else None, pos, FAKE, n, None, FAKE, None)
+    assert dense(_params(e2f)) == e2f.E2F_EDEVICE
+    assert dense(None) == e2f.E2F_EINVAL
+    assert dense(_params(e2f, heads=3)) == e2f.E2F_EINVAL
+    assert dense(_params(e2f), n=-1) == e2f.E2F_EINVAL
+    assert dense(_params(e2f), pos=None) == e2f.E2F_EINVAL
+    assert dense(_params(e2f), n=40000) == e2f.E2F_EUNSUPPORTED  # N^2 H = 6.4e9
     h = ctypes.c_void_p()
     assert lib.e2f_create(7, -1, ctypes.byref(h)) == e2f.E2F_EINVAL
     assert lib.e2f_create(3, -2, ctypes.byref(h)) == e2f.E2F_EINVAL

@@ -1,6 +1,7 @@
-"""GPU k-nearest-neighbour graph (the sparse graphs of the scaling study,
-Sec. 4.1 / Fig. 2) against the oracle, bit-exact, and the Wigner-6j layer on
-kNN graphs against the oracle's definition of the layer.
+"""The graphs of the scaling study (Sec. 4.1 / Fig. 2): the GPU
+k-nearest-neighbour graph against the oracle, bit-exact; the Wigner-6j layer
+on kNN graphs and on dense graphs (every atom attends to every other) against
+the oracle's definition of the layer.
 
 Run with -m gpu."""
 import itertools
@@ -92,3 +93,49 @@ def test_layer_on_knn_graphs(e2f, ctx, n, k, L, C, H, rows):
         err = o.max_rel_err(got[r], ref, L)
         print("kNN n %d k %d L %d %s: err %.3e" % (n, k, L, fn.__name__, err))
         assert err <= TOL_F32
+
+
+# ------------------------------------------------------------ dense graphs
+def complete_graph(n):
+    rp = np.arange(0, n * (n - 1) + 1, n - 1, dtype=np.int64) if n > 1 else np.zeros(n + 1, dtype=np.int64)
+    ci = np.array([j for i in range(n) for j in range(n) if j != i], dtype=np.int32)
+    return rp, ci
+
+
+@pytest.mark.parametrize("n,L,C,H,rows,mix", [(160, 3, 32, 4, None, False), (700, 4, 64, 8, 48, True),
+                                               (300, 2, 16, 4, None, True)])
+def test_dense_graph_layer(e2f, ctx, n, L, C, H, rows, mix):
+    rng = np.random.default_rng(n + L)
+    side = (n / 0.1) ** (1.0 / 3.0)
+    pos = syn.quantize(rng.uniform(0, side, size=(n, 3)))
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    A = rng.uniform(0.0, 1.0 / n, size=(n, n, H)).astype(np.float32)
+    rp, ci = complete_graph(n)
+    alpha = A[np.repeat(np.arange(n), n - 1), ci]  # [E][H] in CSR order
+    cutoff = 10.0
+    w = np.zeros((L + 1) ** 3)
+    for a, f, oo in itertools.product(range(L + 1), repeat=3):
+        if abs(a - f) <= oo <= a + f:
+            w[(a * (L + 1) + f) * (L + 1) + oo] = cutoff ** (-f)
+    mix_w = (rng.standard_normal((L + 1, C, C)) / np.sqrt(C)).astype(np.float32) if mix else None
+    r = np.arange(n) if rows is None else np.linspace(0, n - 1, rows).astype(np.int32)
+    ref = o.layer(L, H, pos, feat, rp, ci, alpha, w, mix_w, rows=r)
+    got = e2f.e2f_wigner6j_conv_forward_dense(ctx, gpu(pos), gpu(feat), gpu(A), L, H, cutoff,
+                                              mix_w=gpu(mix_w)).cpu().numpy()
+    err = o.max_rel_err(got[r], ref, L)
+    print("dense n %d L %d: err %.3e" % (n, L, err))
+    assert err <= TOL_F32
+    # alpha = None means 1 for every pair
+    ones = np.ones((len(ci), H), dtype=np.float32)
+    r1 = r[:16]
+    ref1 = o.layer(L, H, pos, feat, rp, ci, ones, w, mix_w, rows=r1)
+    got1 = e2f.e2f_wigner6j_conv_forward_dense(ctx, gpu(pos), gpu(feat), None, L, H, cutoff,
+                                               mix_w=gpu(mix_w)).cpu().numpy()
+    assert o.max_rel_err(got1[r1], ref1, L) <= TOL_F32
+
+
+def test_dense_graph_single_atom(e2f, ctx):
+    feat = np.ones((1, 9, 8), dtype=np.float32)
+    got = e2f.e2f_wigner6j_conv_forward_dense(ctx, gpu(np.zeros((1, 3), np.float32)), gpu(feat),
+                                              gpu(np.ones((1, 1, 2), np.float32)), 2, 2, 5.0).cpu().numpy()
+    assert np.all(got == 0)
