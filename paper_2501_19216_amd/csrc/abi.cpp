@@ -52,6 +52,8 @@ struct e2f_ctx {
   std::vector<std::vector<double>> coef_w; // path weights of the uploaded coefficients
   int* stats = nullptr;                    // device, kStatsInts ints
   int64_t* pinned = nullptr;               // host, 16 int64
+  int32_t* pinned_plan = nullptr;          // host, plan sizes read back in one copy
+  size_t pinned_plan_n = 0;
   std::vector<double> origins_host;
   Buf a, b, c;
   int64_t last_pairs = 0, last_tiles = 0;  // plan size of the last factorised forward
@@ -397,6 +399,7 @@ void e2f_destroy(e2f_ctx* ctx) {
     for (hipEvent_t e : ctx->pool) (void)hipEventDestroy(e);
     if (ctx->stats) (void)hipFree(ctx->stats);
     if (ctx->pinned) (void)hipHostFree(ctx->pinned);
+    if (ctx->pinned_plan) (void)hipHostFree(ctx->pinned_plan);
   }
   delete ctx;
 }
@@ -601,7 +604,8 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   const size_t sort_b = recv_sort_tmp_bytes(n);
   size_t need_a = al256(sizeof(int32_t) * (size_t)n) + 2 * al256(sizeof(int32_t) * (size_t)count) + al256(scan_b) +
                   al256(sizeof(double) * ctx->origins_host.size()) + 2 * al256(sizeof(uint64_t) * (size_t)n) +
-                  2 * al256(sizeof(int32_t) * (size_t)n) + al256(sort_b) + 3 * al256(sizeof(int32_t) * (keys + 1));
+                  2 * al256(sizeof(int32_t) * (size_t)n) + al256(sort_b) + 3 * al256(sizeof(int32_t) * (keys + 1)) +
+                  al256(sizeof(int32_t) * (3 + 2 * ((size_t)keys + 1)));
   rs = ensure(ctx, ctx->a, need_a, s);
   if (rs != E2F_OK) return rs;
   Carver ca{(char*)ctx->a.p};
@@ -618,6 +622,7 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   int32_t* key_count = ca.take<int32_t>(keys + 1);
   int32_t* rstart_d = ca.take<int32_t>(keys + 1);
   int32_t* pstart_d = ca.take<int32_t>(keys + 1);
+  int32_t* plan_d = ca.take<int32_t>(3 + 2 * ((size_t)keys + 1));
   E2F_HIP(hipMemcpyAsync(origins, ctx->origins_host.data(), sizeof(double) * ctx->origins_host.size(),
                          hipMemcpyHostToDevice, s));
   E2F_TIMED("tile_plan", launch_tile_keys(pos, graph_id, n, tp.lo, tp.dim, tp.span, tp.ncell, tile_of, s));
@@ -629,17 +634,23 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   E2F_TIMED("tile_plan", launch_scan_i32(flags, pidx, count, scan_tmp, scan_b, s));
   E2F_TIMED("tile_plan", launch_tile_ranges(tile_of, pidx, n, (int)keys, key_count, rstart_d, pstart_d, scan_tmp,
                                             scan_b, s));
-  std::vector<int32_t> rstart((size_t)keys + 1), pstart((size_t)keys + 1);
-  E2F_HIP(hipMemcpyAsync(ctx->pinned, pidx + count - 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-  E2F_HIP(hipMemcpyAsync((char*)ctx->pinned + 8, flags + count - 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-  E2F_HIP(hipMemcpyAsync((char*)ctx->pinned + 16, ctx->stats + 8, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-  E2F_HIP(hipMemcpyAsync(rstart.data(), rstart_d, sizeof(int32_t) * (keys + 1), hipMemcpyDeviceToHost, s));
-  E2F_HIP(hipMemcpyAsync(pstart.data(), pstart_d, sizeof(int32_t) * keys, hipMemcpyDeviceToHost, s));
+  // one read-back of the plan sizes: last pair index and flag, largest degree,
+  // receiver and pair starts of every tile
+  const size_t plan_n = 3 + 2 * ((size_t)keys + 1);
+  if (ctx->pinned_plan_n < plan_n) {
+    if (ctx->pinned_plan) (void)hipHostFree(ctx->pinned_plan);
+    ctx->pinned_plan = nullptr;
+    ctx->pinned_plan_n = 0;
+    if (hipHostMalloc((void**)&ctx->pinned_plan, sizeof(int32_t) * plan_n, hipHostMallocDefault) != hipSuccess)
+      return fail(E2F_ENOMEM, "pinned allocation failed");
+    ctx->pinned_plan_n = plan_n;
+  }
+  E2F_TIMED("tile_plan", launch_plan_pack(pidx, flags, count, ctx->stats + 8, rstart_d, pstart_d, (int)keys, plan_d, s));
+  E2F_HIP(hipMemcpyAsync(ctx->pinned_plan, plan_d, sizeof(int32_t) * plan_n, hipMemcpyDeviceToHost, s));
   E2F_HIP(hipStreamSynchronize(s));
-  int32_t last_idx, last_flag, max_degree;
-  std::memcpy(&last_idx, ctx->pinned, 4);
-  std::memcpy(&last_flag, (char*)ctx->pinned + 8, 4);
-  std::memcpy(&max_degree, (char*)ctx->pinned + 16, 4);
+  const int32_t* pp = ctx->pinned_plan;
+  const int32_t last_idx = pp[0], last_flag = pp[1], max_degree = pp[2];
+  std::vector<int32_t> rstart(pp + 3, pp + 3 + keys + 1), pstart(pp + 4 + keys, pp + 4 + 2 * keys + 1);
   const int64_t P = (int64_t)last_idx + last_flag;
   pstart[keys] = (int32_t)P;
   ctx->last_pairs = P;

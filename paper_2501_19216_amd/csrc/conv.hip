@@ -824,6 +824,22 @@ __global__ __launch_bounds__(64 * kMixWaves) void k_mix_mfma(const float* __rest
   }
 }
 
+// The plan sizes the host needs, gathered for one device->host copy:
+// out = {pidx[count-1], flags[count-1], largest degree, rstart[0..keys],
+// pstart[0..keys]} (pstart[keys] is left for the host).
+__global__ void k_plan_pack(const int32_t* __restrict__ pidx, const int32_t* __restrict__ flags, int64_t count,
+                            const int32_t* __restrict__ max_degree, const int32_t* __restrict__ rstart,
+                            const int32_t* __restrict__ pstart, int keys, int32_t* __restrict__ out) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t == 0) {
+    out[0] = pidx[count - 1];
+    out[1] = flags[count - 1];
+    out[2] = *max_degree;
+  }
+  if (t <= keys) out[3 + t] = rstart[t];
+  if (t < keys) out[4 + keys + t] = pstart[t];
+}
+
 // ------------------------------------------------------------ dense graphs
 // Every atom attends to every other (the dense graphs of the scaling study,
 // Sec. 4.1): the aggregation S_h = A_h T_h is a dense product with
@@ -1178,6 +1194,12 @@ hipError_t launch_dense_alpha(const float* alpha, int n, int H, float* A, hipStr
 hipError_t launch_iota(int n, int32_t* v, hipStream_t s) {
   if (n == 0) return hipSuccess;
   k_iota<<<(n + 255) / 256, 256, 0, s>>>(n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_plan_pack(const int32_t* pidx, const int32_t* flags, int64_t count, const int32_t* max_degree,
+                            const int32_t* rstart, const int32_t* pstart, int keys, int32_t* out, hipStream_t s) {
+  k_plan_pack<<<(keys + 256) / 256, 256, 0, s>>>(pidx, flags, count, max_degree, rstart, pstart, keys, out);
   return hipGetLastError();
 }
 

@@ -63,6 +63,10 @@ hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* no
 // receiver order (rstart [keys+1]) and the first pair of each key (pstart [keys])
 hipError_t launch_tile_ranges(const int32_t* tile_of, const int32_t* pidx, int n, int keys, int32_t* counts,
                               int32_t* rstart, int32_t* pstart, void* tmp, size_t tmp_bytes, hipStream_t s);
+// plan sizes for one read-back: {pidx[count-1], flags[count-1], *max_degree,
+// rstart[0..keys], pstart[0..keys)}, 3 + 2(keys+1) ints
+hipError_t launch_plan_pack(const int32_t* pidx, const int32_t* flags, int64_t count, const int32_t* max_degree,
+                            const int32_t* rstart, const int32_t* pstart, int keys, int32_t* out, hipStream_t s);
 size_t recv_sort_tmp_bytes(int n);
 // order = receivers sorted by (tile, Morton index of fine cells of side `fine` grid units)
 hipError_t launch_sort_receivers(const float* pos, const int32_t* tile_of, int n, const int* lo, int64_t fine,
