@@ -356,6 +356,9 @@ def main():
         src = os.path.join(ROOT, "paper_2501_19216_amd", "csrc", "conv.hip")
         if tr.get("conv_sha256") == file_sha(src):
             roof["traffic"] = tr["bytes_per_launch"]
+            # measured HBM rate: counter bytes over the same launch time
+            roof["traffic_GBps"] = tr["bytes_per_launch"] / (t_dom * 1e-3) / 1e9
+            roof["traffic_frac"] = roof["traffic_GBps"] / HBM_PEAK_GBS
 
     # ---- the bf16 channel-mixing variant of the same forward
     mix_bf16 = mix_w.to(torch.bfloat16)

@@ -58,6 +58,8 @@ def lib():
             L.e2fo_neighbor_list_cells.argtypes = [p, p, i, ctypes.c_float, p, p, i64]
             L.e2fo_knn_graph.restype = i64
             L.e2fo_knn_graph.argtypes = [p, p, i, i, p, p, i64]
+            L.e2fo_attention_weights.restype = None
+            L.e2fo_attention_weights.argtypes = [p, p, p, i, i, i, p, i, ctypes.c_float, p, p, p]
             L.e2fo_conv_edge.restype = i
             L.e2fo_conv_edge.argtypes = [i, i, i, p, p, i, p, p, p, p, p, i, p]
             L.e2fo_conv_factorised.restype = i
@@ -144,6 +146,23 @@ def knn_graph(pos, k: int, graph_id=None):
     E2 = lib().e2fo_knn_graph(_ptr(pos), _ptr(gid), n, int(k), _ptr(row_ptr), _ptr(col), E)
     assert E2 == E
     return row_ptr, col[:E]
+
+
+def attention_weights(pos, q, k, rbf_w, cutoff: float, row_ptr, col_idx) -> np.ndarray:
+    """Attention weights [E, H] float32 (App. E): q.k logits [N,H,dk] plus the
+    radial basis with weights rbf_w [H,R], softmax over each row, cosine
+    envelope."""
+    pos = _c(pos, np.float32)
+    q = _c(q, np.float32)
+    k = _c(k, np.float32)
+    rbf_w = _c(rbf_w, np.float32)
+    row_ptr = _c(row_ptr, np.int64)
+    col_idx = _c(col_idx, np.int32)
+    n, heads, dk = q.shape
+    out = np.zeros((col_idx.shape[0], heads), dtype=np.float32)
+    lib().e2fo_attention_weights(_ptr(pos), _ptr(q), _ptr(k), n, heads, dk, _ptr(rbf_w), rbf_w.shape[1],
+                                 float(cutoff), _ptr(row_ptr), _ptr(col_idx), _ptr(out))
+    return out
 
 
 # ---------------------------------------------------------------- the layer

@@ -18,6 +18,9 @@
  *   - the recoupling weights X of Def. 2.3 as an overlap of coupling trees;
  *   - the radius graph: every ordered pair i != j of one graph with
  *     |r_i - r_j| < cutoff, evaluated exactly on the 2^-16 A grid;
+ *   - the attention weights of the edges (Alg. 1 input alpha; E2Attention
+ *     of App. E): scalar q.k logits plus a radial basis, softmax over each
+ *     receiver's neighbours, cosine envelope;
  *   - the k-nearest-neighbour graph of the paper's sparse scaling workloads
  *     (Sec. 4.1, Fig. 2): per atom the k others of its graph that come first
  *     in (squared grid distance, index) order;
@@ -324,6 +327,53 @@ int64_t e2fo_knn_graph(const float *pos, const int32_t *graph_id, int n, int k, 
         free(row);
     }
     return E;
+}
+
+/* ---------- attention weights (Alg. 1 input alpha; App. E E2Attention) ----------
+ * For the edge e = (i, j) of row i and head h:
+ *   logit = sum_t q[i][h][t] k[j][h][t] + sum_r w[h][r] exp(-((d - mu_r)/sigma)^2),
+ *   mu_r = r cutoff / (R - 1), sigma = cutoff / (R - 1), d = |r_i - r_j|,
+ *   alpha[e][h] = env(d) exp(logit) / sum over the row of exp(logit),
+ *   env(d) = (cos(pi d / cutoff) + 1) / 2 for d < cutoff, else 0. */
+void e2fo_attention_weights(const float *pos, const float *q, const float *k, int n, int heads, int dk,
+                            const float *rbf_w, int n_rbf, float cutoff, const int64_t *row_ptr,
+                            const int32_t *col_idx, float *alpha) {
+    const double rc = cutoff, sigma = rc / (double)(n_rbf - 1);
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int i = 0; i < n; ++i) {
+        const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+        if (e1 == e0) continue;
+        double *lg = (double *)malloc(sizeof(double) * (size_t)(e1 - e0));
+        double *env = (double *)malloc(sizeof(double) * (size_t)(e1 - e0));
+        for (int h = 0; h < heads; ++h) {
+            double mx = -INFINITY;
+            for (int64_t e = e0; e < e1; ++e) {
+                const int j = col_idx[e];
+                double d2 = 0.0;
+                for (int c = 0; c < 3; ++c) {
+                    const double dx = (double)pos[3 * i + c] - (double)pos[3 * j + c];
+                    d2 += dx * dx;
+                }
+                const double d = sqrt(d2);
+                double l = 0.0;
+                for (int t = 0; t < dk; ++t)
+                    l += (double)q[((size_t)i * heads + h) * dk + t] * (double)k[((size_t)j * heads + h) * dk + t];
+                for (int r = 0; r < n_rbf; ++r) {
+                    const double z = (d - r * sigma) / sigma;
+                    l += (double)rbf_w[h * n_rbf + r] * exp(-z * z);
+                }
+                lg[e - e0] = l;
+                env[e - e0] = d < rc ? 0.5 * (cos(acos(-1.0) * d / rc) + 1.0) : 0.0;
+                if (l > mx) mx = l;
+            }
+            double den = 0.0;
+            for (int64_t e = e0; e < e1; ++e) den += exp(lg[e - e0] - mx);
+            for (int64_t e = e0; e < e1; ++e)
+                alpha[e * heads + h] = (float)(env[e - e0] * exp(lg[e - e0] - mx) / den);
+        }
+        free(lg);
+        free(env);
+    }
 }
 
 /* The same graph through a uniform cell grid (cell side >= cutoff), for

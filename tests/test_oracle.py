@@ -355,6 +355,51 @@ def small_graph(L, n, C, H, seed, box=4.0, cutoff=3.0):
     return pos, rp, ci, feat, alpha, w
 
 
+def test_attention_weights_closed_forms():
+    """Attention weights (App. E): softmax over a row times the cosine envelope."""
+    rng = np.random.default_rng(9)
+    n, H, dk, R, rc = 60, 3, 4, 6, 5.0
+    pos = syn.quantize(rng.uniform(0, 9, size=(n, 3)))
+    rp, ci = o.neighbor_list(pos, rc)
+    q = rng.standard_normal((n, H, dk)).astype(np.float32)
+    k = rng.standard_normal((n, H, dk)).astype(np.float32)
+    w = rng.standard_normal((H, R)).astype(np.float32)
+    a = o.attention_weights(pos, q, k, w, rc, rp, ci)
+    recv = np.repeat(np.arange(n), np.diff(rp))
+    d = np.linalg.norm(pos[recv].astype(np.float64) - pos[ci], axis=1)
+    env = 0.5 * (np.cos(np.pi * d / rc) + 1.0)
+    # rows of alpha / envelope sum to one (every edge is inside the cutoff)
+    s = np.zeros((n, H))
+    np.add.at(s, recv, a / env[:, None])
+    has = np.diff(rp) > 0
+    assert np.allclose(s[has], 1.0, atol=2e-6)
+    # equal logits (no q.k, no radial weights): envelope / degree
+    z = o.attention_weights(pos, np.zeros_like(q), k, np.zeros_like(w), rc, rp, ci)
+    assert np.allclose(z, (env / np.diff(rp)[recv])[:, None], rtol=1e-6)
+    # one neighbour per row: the envelope alone
+    rp1 = np.arange(n + 1, dtype=np.int64)
+    ci1 = ((np.arange(n) + 1) % n).astype(np.int32)
+    a1 = o.attention_weights(pos, q, k, w, 50.0, rp1, ci1)
+    d1 = np.linalg.norm(pos.astype(np.float64) - pos[ci1], axis=1)
+    assert np.allclose(a1, (0.5 * (np.cos(np.pi * d1 / 50.0) + 1.0))[:, None], rtol=1e-6)
+    # beyond the cutoff the weight is zero
+    a2 = o.attention_weights(pos, q, k, w, 0.5 * float(d1.min()), rp1, ci1)
+    assert np.all(a2 == 0)
+    # invariant under rotations and translations (logits depend on distances only)
+    Q = o.random_rotation(3)
+    pr = (pos.astype(np.float64) @ Q.T + 11.0).astype(np.float32)
+    assert np.allclose(o.attention_weights(pr, q, k, w, rc, rp, ci), a, atol=1e-5)
+    # the synthetic generator's weights are the case dk = 1, q = k = species embedding
+    species = rng.integers(0, 5, size=n)
+    ref = syn.attention_weights(pos, species, rp, ci, H, rc, 5, 17)
+    g = np.random.default_rng(0xA1FA0000 + 17)
+    emb = g.standard_normal((5, H))
+    rho = g.standard_normal((H, 8)) / math.sqrt(8.0)
+    e = emb[species][:, :, None].astype(np.float32)
+    got = o.attention_weights(pos, e, e, rho.astype(np.float32), rc, rp, ci)
+    assert np.allclose(got, ref, rtol=1e-5, atol=1e-7)
+
+
 def test_knn_graph_closed_forms():
     """kNN graph (Sec. 4.1 sparse workloads): lattice distances are known in
     closed form (a, a*sqrt2, a*sqrt3), so the selected sets are too, ties
