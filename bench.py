@@ -311,6 +311,15 @@ def main():
     ms_fwd = timed(fwd_only, args.steps)
     ms_edge = timed(edge_only, args.steps)
     ms_nl = timed(nl_only, args.steps)
+    # the attention weights of the same graph (q.k over 16 dims per head + 8 radial functions)
+    g = torch.Generator(device=dev).manual_seed(5)
+    q_att = torch.randn(n, H, 16, device=dev, generator=g)
+    k_att = torch.randn(n, H, 16, device=dev, generator=g) / 4.0
+    w_att = torch.randn(H, 8, device=dev, generator=g)
+    a_out = torch.empty(E, H, device=dev)
+    att_only = lambda: e2f.e2f_attention_weights(ctx, pos, row_ptr, col, wl.cutoff, q_att, k_att, w_att, out=a_out)
+    att_only()
+    ms_att = timed(att_only, args.steps)
     pairs, tiles = e2f.e2f_last_plan(ctx)
     print("[bench] fwd %.3f ms, edge-TP %.3f ms, graph %.3f ms" % (ms_fwd, ms_edge, ms_nl), file=sys.stderr,
           flush=True)
@@ -427,6 +436,7 @@ def main():
         "speedup_vs_edge_tp": ms_edge / ms_fwd,
         "fwd_bf16_mix": bf16_res,
         "neighbor_list_ms": ms_nl,
+        "attention": {"ms": ms_att, "dk": 16, "n_rbf": 8, "bytes_GBps": (E * (4 + 4 * H) + 12.0 * n) / (ms_att * 1e-3) / 1e9},
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": cpu,

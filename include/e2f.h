@@ -101,6 +101,21 @@ e2f_status e2f_neighbor_list(e2f_ctx* ctx, const float* pos, const int32_t* grap
 e2f_status e2f_knn_graph(e2f_ctx* ctx, const float* pos, const int32_t* graph_id, int32_t n, int32_t k,
                          int64_t* row_ptr, int32_t* col_idx, int64_t capacity, int64_t* n_edges, void* stream);
 
+/* Attention weights of the graph's edges, the input alpha of Alg. 1 (App. E:
+ * logits from the scalar features and a radial basis, softmax over the
+ * neighbours).  For the edge e = (i, j) of row i and head h:
+ *   logit = sum_t q[i][h][t] k[j][h][t] + sum_r rbf_w[h][r] exp(-((d - mu_r)/sigma)^2),
+ *   mu_r = r cutoff / (n_rbf - 1), sigma = cutoff / (n_rbf - 1), d = |r_i - r_j|,
+ *   alpha[e][h] = (cos(pi d / cutoff) + 1)/2 * exp(logit) / (sum over row i of exp(logit)),
+ * with the envelope 0 for d >= cutoff.  q, k: [N][heads][dk] float32 (unused
+ * if dk = 0); rbf_w: [heads][n_rbf] float32 (n_rbf = 0: no radial term, else
+ * 2..32); CSR as from e2f_neighbor_list / e2f_knn_graph; out alpha [E][heads].
+ * heads <= 64.  fp32, deterministic. */
+e2f_status e2f_attention_weights(e2f_ctx* ctx, const float* pos, const float* q, const float* k, int32_t n,
+                                 int32_t heads, int32_t dk, const float* rbf_w, int32_t n_rbf, float cutoff,
+                                 const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges, float* alpha,
+                                 void* stream);
+
 /* Real regular solid harmonics (Def. 2.1) of p_i = pos_i - origins[origin_id[i]]
  * (origin 0 if origin_id is NULL; the zero vector if origins is NULL),
  * evaluated in float64 and rounded: out [N][(lmax+1)^2] float32. */

@@ -22,7 +22,7 @@ E2F_F32, E2F_BF16 = 0, 1
 _STATUS = {0: "E2F_OK", 1: "E2F_EINVAL", 2: "E2F_ECAPACITY", 3: "E2F_ENOMEM", 4: "E2F_EDEVICE", 5: "E2F_EUNSUPPORTED"}
 
 # every function declared in include/e2f.h
-EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg", "e2f_knn_graph",
+EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg", "e2f_knn_graph", "e2f_attention_weights",
             "e2f_recoupling_weight", "e2f_neighbor_list", "e2f_solid_harmonics", "e2f_node_tp",
             "e2f_wigner6j_conv_forward", "e2f_wigner6j_conv_forward_dense", "e2f_edge_tp_conv_forward", "e2f_profile", "e2f_profile_read", "e2f_last_plan"]
 
@@ -61,6 +61,8 @@ def _load():
     L.e2f_neighbor_list.restype = i
     L.e2f_knn_graph.argtypes = [p, p, p, i32, i32, p, p, i64, ctypes.POINTER(i64), p]
     L.e2f_knn_graph.restype = i
+    L.e2f_attention_weights.argtypes = [p, p, p, p, i32, i32, i32, p, i32, f, p, p, i64, p, p]
+    L.e2f_attention_weights.restype = i
     L.e2f_solid_harmonics.argtypes = [p, p, p, p, i32, i, p, p]
     L.e2f_solid_harmonics.restype = i
     L.e2f_node_tp.argtypes = [p, p, p, p, p, i32, i32, i, p, p]
@@ -193,6 +195,28 @@ def e2f_knn_graph(ctx: Context, pos: torch.Tensor, k: int, graph_id: torch.Tenso
     _check(lib.e2f_knn_graph(ctx.handle, _ptr(pos), _ptr(graph_id), n, k, _ptr(row_ptr), _ptr(col), col.numel(),
                              ctypes.byref(E), _stream(pos.device)), "e2f_knn_graph")
     return row_ptr, col[:E.value]
+
+
+def e2f_attention_weights(ctx: Context, pos, row_ptr, col_idx, cutoff: float, q=None, k=None, rbf_w=None,
+                          heads: int | None = None, out=None):
+    """Attention weights [E, heads] float32: q, k [N, heads, dk] (or None),
+    rbf_w [heads, R] (or None)."""
+    for t, name in ((pos, "pos"), (q, "q"), (k, "k"), (rbf_w, "rbf_w")):
+        _dev(t, torch.float32, name)
+    _dev(row_ptr, torch.int64, "row_ptr")
+    _dev(col_idx, torch.int32, "col_idx")
+    n = pos.shape[0]
+    H = heads if heads is not None else (q.shape[1] if q is not None else rbf_w.shape[0])
+    dk = 0 if q is None else q.shape[2]
+    R = 0 if rbf_w is None else rbf_w.shape[1]
+    E = col_idx.numel()
+    if out is None:
+        out = torch.empty(E, H, dtype=torch.float32, device=pos.device)
+    _dev(out, torch.float32, "out")
+    _check(lib.e2f_attention_weights(ctx.handle, _ptr(pos), _ptr(q), _ptr(k), n, H, dk, _ptr(rbf_w), R, cutoff,
+                                     _ptr(row_ptr), _ptr(col_idx), E, _ptr(out), _stream(pos.device)),
+           "e2f_attention_weights")
+    return out
 
 
 def e2f_solid_harmonics(ctx: Context, pos: torch.Tensor, lmax: int, origins: torch.Tensor | None = None,

@@ -513,6 +513,30 @@ e2f_status e2f_knn_graph(e2f_ctx* ctx, const float* pos, const int32_t* graph_id
   return E2F_OK;
 }
 
+e2f_status e2f_attention_weights(e2f_ctx* ctx, const float* pos, const float* q, const float* k, int32_t n,
+                                 int32_t heads, int32_t dk, const float* rbf_w, int32_t n_rbf, float cutoff,
+                                 const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges, float* alpha,
+                                 void* stream) {
+  if (!ctx) return fail(E2F_EINVAL, "ctx is NULL");
+  if (n < 0 || n_edges < 0) return fail(E2F_EINVAL, "n or n_edges < 0");
+  if (heads < 1) return fail(E2F_EINVAL, "heads = %d < 1", heads);
+  if (heads > 64) return fail(E2F_EUNSUPPORTED, "heads = %d > 64", heads);
+  if (dk < 0 || n_rbf < 0 || n_rbf == 1) return fail(E2F_EINVAL, "dk >= 0 and n_rbf = 0 or >= 2 are required");
+  if (n_rbf > kAttnMaxRbf) return fail(E2F_EUNSUPPORTED, "n_rbf = %d > %d", n_rbf, kAttnMaxRbf);
+  if (!finite_pos(cutoff)) return fail(E2F_EINVAL, "cutoff must be finite and positive");
+  if (n > 0 && (!pos || !row_ptr)) return fail(E2F_EINVAL, "pos and row_ptr are required");
+  if (n > 0 && dk > 0 && (!q || !k)) return fail(E2F_EINVAL, "q and k are required with dk > 0");
+  if (n_rbf > 0 && !rbf_w) return fail(E2F_EINVAL, "rbf_w is required with n_rbf > 0");
+  if (n_edges > 0 && (!col_idx || !alpha)) return fail(E2F_EINVAL, "col_idx and alpha are required");
+  if (n_edges > std::numeric_limits<int32_t>::max()) return fail(E2F_EUNSUPPORTED, "more than 2^31-1 edges");
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  if (n == 0 || n_edges == 0) return E2F_OK;
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  E2F_TIMED("attention", launch_attention(pos, q, k, n, heads, dk, rbf_w, n_rbf, cutoff, row_ptr, col_idx, alpha, s));
+  return E2F_OK;
+}
+
 e2f_status e2f_solid_harmonics(e2f_ctx* ctx, const float* pos, const float* origins, const int32_t* origin_id,
                                int32_t n, int lmax, float* out, void* stream) {
   if (!ctx) return fail(E2F_EINVAL, "ctx is NULL");

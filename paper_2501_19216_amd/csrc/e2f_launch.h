@@ -94,6 +94,12 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, const int32_t* order, int n, int C,
                            int dh, float* y, hipStream_t s);
 
+// ---- attention weights [E][H] (H <= 64, 2 <= R <= kAttnMaxRbf radial functions)
+constexpr int kAttnMaxRbf = 32;
+hipError_t launch_attention(const float* pos, const float* q, const float* k, int n, int H, int dk,
+                            const float* rbf_w, int R, float rc, const int64_t* row_ptr, const int32_t* col_idx,
+                            float* alpha, hipStream_t s);
+
 // ---- dense graphs: A[h][i][j] = alpha[i][j][h] (1 if alpha is NULL), 0 for i == j
 hipError_t launch_dense_alpha(const float* alpha, int n, int H, float* A, hipStream_t s);
 hipError_t launch_iota(int n, int32_t* v, hipStream_t s);

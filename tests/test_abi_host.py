@@ -123,6 +123,17 @@ def test_other_argument_checks(e2f):
     assert dense(_params(e2f), n=-1) == e2f.E2F_EINVAL
     assert dense(_params(e2f), pos=None) == e2f.E2F_EINVAL
     assert dense(_params(e2f), n=40000) == e2f.E2F_EUNSUPPORTED  # N^2 H = 6.4e9
+    att = lambda heads=4, dk=2, R=8, rc=5.0, q=FAKE, w=FAKE: lib.e2f_attention_weights(
+        ctx.handle, FAKE, q, FAKE, 10, heads, dk, w, R, rc, FAKE, FAKE, 30, FAKE, None)
+    assert att() == e2f.E2F_EDEVICE
+    assert att(heads=0) == e2f.E2F_EINVAL
+    assert att(heads=65) == e2f.E2F_EUNSUPPORTED
+    assert att(R=1) == e2f.E2F_EINVAL
+    assert att(R=33) == e2f.E2F_EUNSUPPORTED
+    assert att(rc=0.0) == e2f.E2F_EINVAL
+    assert att(q=None) == e2f.E2F_EINVAL
+    assert att(w=None) == e2f.E2F_EINVAL
+    assert att(dk=0, R=0, q=None, w=None) == e2f.E2F_EDEVICE
     h = ctypes.c_void_p()
     assert lib.e2f_create(7, -1, ctypes.byref(h)) == e2f.E2F_EINVAL
     assert lib.e2f_create(3, -2, ctypes.byref(h)) == e2f.E2F_EINVAL
