@@ -58,6 +58,8 @@ def lib():
             L.e2fo_neighbor_list_cells.argtypes = [p, p, i, ctypes.c_float, p, p, i64]
             L.e2fo_knn_graph.restype = i64
             L.e2fo_knn_graph.argtypes = [p, p, i, i, p, p, i64]
+            L.e2fo_conv_edge_vjp.restype = i
+            L.e2fo_conv_edge_vjp.argtypes = [i, i, i, p, p, p, i, p, p, p, p, p, p]
             L.e2fo_attention_weights.restype = None
             L.e2fo_attention_weights.argtypes = [p, p, p, i, i, i, p, i, ctypes.c_float, p, p, p]
             L.e2fo_conv_edge.restype = i
@@ -182,6 +184,27 @@ def conv_edge(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, rows=None
     if rc:
         raise ValueError("e2fo_conv_edge rejected its arguments")
     return out
+
+
+def conv_edge_vjp(lmax, heads, pos, feat, gy, row_ptr, col_idx, alpha, path_w, want_feat=True, want_alpha=True):
+    """Vector-Jacobian products of the layer (by its definition) for the
+    output gradient gy [n, (L+1)^2, C]: (gfeat [n, (L+1)^2, C], galpha [E, H]),
+    float64; either may be skipped (None)."""
+    pos = _c(pos, np.float32)
+    feat = _c(feat, np.float32)
+    gy = _c(gy, np.float64)
+    row_ptr = _c(row_ptr, np.int64)
+    col_idx = _c(col_idx, np.int32)
+    alpha = _c(alpha, np.float32)
+    path_w = _c(path_w, np.float64)
+    n, nk, C = feat.shape
+    gf = np.zeros((n, nk, C)) if want_feat else None
+    ga = np.zeros((col_idx.shape[0], heads)) if want_alpha else None
+    rc = lib().e2fo_conv_edge_vjp(lmax, C, heads, _ptr(pos), _ptr(feat), _ptr(gy), n, _ptr(row_ptr), _ptr(col_idx),
+                                  _ptr(alpha), _ptr(path_w), _ptr(gf), _ptr(ga))
+    if rc:
+        raise ValueError("e2fo_conv_edge_vjp rejected its arguments")
+    return gf, ga
 
 
 def conv_factorised(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, origin) -> np.ndarray:

@@ -28,7 +28,10 @@
  *     setup): y_i = sum_j alpha_ij sum_{a,f} w_afo [h_j^(a) (x) R^(f)(r_i - r_j)]^(o);
  *   - the layer by the node factorisation of Thm. 3.3 / Alg. 1 (for the
  *     equality check of the two forms only);
- *   - the per-irrep linear channel mix of App. F.
+ *   - the per-irrep linear channel mix of App. F;
+ *   - the vector-Jacobian products of the layer with respect to the features
+ *     and the attention weights, by the definition (the layer is linear in
+ *     both).
  *
  * Accumulation is in double; the row loops are parallel (OpenMP) over
  * receivers, each row summed in ascending sender order.
@@ -495,6 +498,109 @@ int e2fo_conv_edge(int L, int C, int H, const float *pos, const float *feat, int
                                 }
                     }
         }
+    }
+    return 0;
+}
+
+/* ---------- vector-Jacobian products of the layer by its definition ----------
+ * The layer is linear in h and in alpha.  For the output gradient gy
+ * [n][(L+1)^2][C] (double):
+ *   gfeat[j][a al][c] = sum over edges e = (i, j) of alpha[e][c/dh]
+ *       sum_{f,o} w_afo sum_{mf,m} C^{o m}_{a al, f mf} R^(f)_mf(r_i - r_j) gy[i][o m][c],
+ *   galpha[e][h] = sum_{c of head h} sum_{a,f,o} w_afo
+ *       sum_{al,mf,m} C^{o m}_{a al, f mf} R^(f)_mf(r_i - r_j) h_j[a al][c] gy[i][o m][c].
+ * Either output may be NULL.  gfeat is gathered per sender j over a
+ * transposed edge list, so every sum runs in a fixed order. */
+int e2fo_conv_edge_vjp(int L, int C, int H, const float *pos, const float *feat, const double *gy, int n,
+                       const int64_t *row_ptr, const int32_t *col_idx, const float *alpha, const double *path_w,
+                       double *gfeat, double *galpha) {
+    if (L < 0 || L > 6 || C < 1 || H < 1 || C % H) return 1;
+    const int nk = (L + 1) * (L + 1), dh = C / H;
+    const int64_t E = row_ptr[n];
+    warm_cg(L, L);
+    if (galpha) {
+#pragma omp parallel for schedule(dynamic, 4)
+        for (int i = 0; i < n; ++i) {
+            double R[49];
+            const double *gyi = gy + (size_t)i * nk * C;
+            for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+                const int j = col_idx[e];
+                double v[3] = {(double)pos[3 * i] - pos[3 * j], (double)pos[3 * i + 1] - pos[3 * j + 1],
+                               (double)pos[3 * i + 2] - pos[3 * j + 2]};
+                e2fo_solid_harmonics(L, v, R);
+                const float *hj = feat + (size_t)j * nk * C;
+                for (int h = 0; h < H; ++h) galpha[e * H + h] = 0.0;
+                for (int a = 0; a <= L; ++a)
+                    for (int f = 0; f <= L; ++f)
+                        for (int o = iabs_(a - f); o <= imin_(a + f, L); ++o) {
+                            const double w = path_w[(a * (L + 1) + f) * (L + 1) + o];
+                            if (w == 0.0) continue;
+                            const double *c3 = cg(a, f, o);
+                            for (int ma = 0; ma < 2 * a + 1; ++ma)
+                                for (int mf = 0; mf < 2 * f + 1; ++mf)
+                                    for (int m = 0; m < 2 * o + 1; ++m) {
+                                        const double cgv = c3[(ma * (2 * f + 1) + mf) * (2 * o + 1) + m];
+                                        if (cgv == 0.0) continue;
+                                        const double k = w * cgv * R[f * f + mf];
+                                        const float *hrow = hj + (size_t)(a * a + ma) * C;
+                                        const double *grow = gyi + (size_t)(o * o + m) * C;
+                                        for (int c = 0; c < C; ++c) galpha[e * H + c / dh] += k * hrow[c] * grow[c];
+                                    }
+                        }
+            }
+        }
+    }
+    if (gfeat) {
+        /* transposed edge list: for every sender j the edges (i, j), by ascending e */
+        int64_t *tptr = (int64_t *)calloc((size_t)n + 1, sizeof(int64_t));
+        int64_t *tedge = (int64_t *)malloc(sizeof(int64_t) * (size_t)(E > 0 ? E : 1));
+        int32_t *trecv = (int32_t *)malloc(sizeof(int32_t) * (size_t)(E > 0 ? E : 1));
+        for (int64_t e = 0; e < E; ++e) tptr[col_idx[e] + 1]++;
+        for (int j = 0; j < n; ++j) tptr[j + 1] += tptr[j];
+        int64_t *fill = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+        for (int j = 0; j < n; ++j) fill[j] = tptr[j];
+        for (int i = 0; i < n; ++i)
+            for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+                const int64_t t = fill[col_idx[e]]++;
+                tedge[t] = e;
+                trecv[t] = i;
+            }
+        free(fill);
+#pragma omp parallel for schedule(dynamic, 4)
+        for (int j = 0; j < n; ++j) {
+            double R[49];
+            double *g = gfeat + (size_t)j * nk * C;
+            memset(g, 0, sizeof(double) * (size_t)nk * C);
+            for (int64_t t = tptr[j]; t < tptr[j + 1]; ++t) {
+                const int64_t e = tedge[t];
+                const int i = trecv[t];
+                double v[3] = {(double)pos[3 * i] - pos[3 * j], (double)pos[3 * i + 1] - pos[3 * j + 1],
+                               (double)pos[3 * i + 2] - pos[3 * j + 2]};
+                e2fo_solid_harmonics(L, v, R);
+                const double *gyi = gy + (size_t)i * nk * C;
+                for (int a = 0; a <= L; ++a)
+                    for (int f = 0; f <= L; ++f)
+                        for (int o = iabs_(a - f); o <= imin_(a + f, L); ++o) {
+                            const double w = path_w[(a * (L + 1) + f) * (L + 1) + o];
+                            if (w == 0.0) continue;
+                            const double *c3 = cg(a, f, o);
+                            for (int ma = 0; ma < 2 * a + 1; ++ma)
+                                for (int mf = 0; mf < 2 * f + 1; ++mf)
+                                    for (int m = 0; m < 2 * o + 1; ++m) {
+                                        const double cgv = c3[(ma * (2 * f + 1) + mf) * (2 * o + 1) + m];
+                                        if (cgv == 0.0) continue;
+                                        const double k = w * cgv * R[f * f + mf];
+                                        double *grow = g + (size_t)(a * a + ma) * C;
+                                        const double *yrow = gyi + (size_t)(o * o + m) * C;
+                                        for (int c = 0; c < C; ++c)
+                                            grow[c] += (double)alpha[e * H + c / dh] * k * yrow[c];
+                                    }
+                        }
+            }
+        }
+        free(tptr);
+        free(tedge);
+        free(trecv);
     }
     return 0;
 }

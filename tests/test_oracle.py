@@ -400,6 +400,37 @@ def test_attention_weights_closed_forms():
     assert np.allclose(got, ref, rtol=1e-5, atol=1e-7)
 
 
+@pytest.mark.parametrize("L", [0, 2, 3])
+def test_layer_vjp_adjoint_identities(L):
+    """The backward of the layer (with respect to the features and to the
+    attention weights) is pinned by the adjoint identities of a linear map:
+    <gy, y(h, alpha)> = <gfeat(gy), h> = sum_e alpha_e . galpha_e, and the
+    directional derivative in alpha is exact."""
+    rng = np.random.default_rng(30 + L)
+    n, C, H = 40, 8, 2
+    pos = syn.quantize(rng.uniform(0, 7, size=(n, 3)))
+    rp, ci = o.neighbor_list(pos, 4.0)
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    alpha = rng.uniform(0.1, 1.0, size=(len(ci), H)).astype(np.float32)
+    w = rng.uniform(0.2, 1.0, size=(L + 1) ** 3)
+    gy = rng.standard_normal((n, (L + 1) ** 2, C))
+    y = o.conv_edge(L, H, pos, feat, rp, ci, alpha, w)
+    gf, ga = o.conv_edge_vjp(L, H, pos, feat, gy, rp, ci, alpha, w)
+    lhs = float((gy * y).sum())
+    assert abs(float((gf * feat.astype(np.float64)).sum()) - lhs) <= 1e-10 * abs(lhs)
+    assert abs(float((ga * alpha.astype(np.float64)).sum()) - lhs) <= 1e-10 * abs(lhs)
+    d = rng.standard_normal(alpha.shape).astype(np.float32) * np.float32(0.25)
+    y2 = o.conv_edge(L, H, pos, feat, rp, ci, (alpha + d).astype(np.float32), w)
+    dl = float((gy * (y2 - y)).sum())
+    da = (alpha + d).astype(np.float64) - alpha.astype(np.float64)  # the perturbation as stored in float32
+    assert abs(dl - float((ga * da).sum())) <= 1e-9 * max(1.0, abs(dl))
+    # mixing: the adjoint of out = W^(o) y is W^(o)T
+    mix = rng.standard_normal((L + 1, C, C))
+    out = o.mix(L, y, mix)
+    back = o.mix(L, gy, np.transpose(mix, (0, 2, 1)))
+    assert abs(float((gy * out).sum()) - float((back * y).sum())) <= 1e-10 * abs(float((gy * out).sum()))
+
+
 def test_knn_graph_closed_forms():
     """kNN graph (Sec. 4.1 sparse workloads): lattice distances are known in
     closed form (a, a*sqrt2, a*sqrt3), so the selected sets are too, ties
