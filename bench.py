@@ -320,6 +320,17 @@ def main():
     att_only = lambda: e2f.e2f_attention_weights(ctx, pos, row_ptr, col, wl.cutoff, q_att, k_att, w_att, out=a_out)
     att_only()
     ms_att = timed(att_only, args.steps)
+    # the backward of the timed forward (fp32 mixing): both products, then each alone
+    g_out = torch.randn(out.shape, device=dev, generator=g)
+
+    def bwd(wf, wa):
+        return lambda: e2f.e2f_wigner6j_conv_backward(ctx, pos, feat, g_out, row_ptr, col, alpha, L, H, wl.cutoff,
+                                                      mix_w=mix_w, graph_id=gid, want_feat=wf, want_alpha=wa)
+
+    bwd(True, True)()
+    ms_bwd = timed(bwd(True, True), args.steps)
+    ms_bwd_feat = timed(bwd(True, False), args.steps)
+    ms_bwd_alpha = timed(bwd(False, True), args.steps)
     pairs, tiles = e2f.e2f_last_plan(ctx)
     print("[bench] fwd %.3f ms, edge-TP %.3f ms, graph %.3f ms" % (ms_fwd, ms_edge, ms_nl), file=sys.stderr,
           flush=True)
@@ -436,6 +447,7 @@ def main():
         "speedup_vs_edge_tp": ms_edge / ms_fwd,
         "fwd_bf16_mix": bf16_res,
         "neighbor_list_ms": ms_nl,
+        "backward": {"ms": ms_bwd, "grad_feat_ms": ms_bwd_feat, "grad_alpha_ms": ms_bwd_alpha},
         "attention": {"ms": ms_att, "dk": 16, "n_rbf": 8, "bytes_GBps": (E * (4 + 4 * H) + 12.0 * n) / (ms_att * 1e-3) / 1e9},
         "kernels": kernels,
         "roofline": roof,

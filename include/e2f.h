@@ -172,6 +172,23 @@ e2f_status e2f_wigner6j_conv_forward_dense(e2f_ctx* ctx, const e2f_conv_params* 
                                            const float* feat, int32_t n, const float* alpha, float* out,
                                            void* stream);
 
+/* Backward of e2f_wigner6j_conv_forward (same parameters and graph): the
+ * vector-Jacobian products for the output gradient grad_out [N][(L+1)^2][C].
+ * The layer is linear in the features and in the attention weights:
+ *   grad_feat [N][(L+1)^2][C]: the adjoint, itself a Wigner-6j convolution
+ *     (Thm. 3.3) of the unmixed output gradient on the transposed graph (rows
+ *     = senders), with path weights w[a][f][o] kappa(a,f,o) (-1)^f, kappa the
+ *     ratio of the real CG tensors of (a,f,o) and (o,f,a) (computed from the
+ *     tables); the mixing contributes W^(o) transposed;
+ *   grad_alpha [E][H]: per edge and head, the dot product of the unmixed
+ *     output gradient of the receiver with the edge's message (the per-edge
+ *     filter of the baseline); needs feat and C <= 256.
+ * Either output may be NULL (not both).  Positions are not differentiated. */
+e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
+                                      const int32_t* graph_id, const float* feat, const float* grad_out, int32_t n,
+                                      const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges,
+                                      const float* alpha, float* grad_feat, float* grad_alpha, void* stream);
+
 /* The conventional per-edge SO(3) convolution (Def. 3.1): the same layer
  * computed edge by edge with R^(f)(r_i - r_j) and the CG product per edge.
  * Same arguments and output as e2f_wigner6j_conv_forward; graph_id unused. */

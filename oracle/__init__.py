@@ -59,7 +59,7 @@ def lib():
             L.e2fo_knn_graph.restype = i64
             L.e2fo_knn_graph.argtypes = [p, p, i, i, p, p, i64]
             L.e2fo_conv_edge_vjp.restype = i
-            L.e2fo_conv_edge_vjp.argtypes = [i, i, i, p, p, p, i, p, p, p, p, p, p]
+            L.e2fo_conv_edge_vjp.argtypes = [i, i, i, p, p, p, i, p, p, p, p, p, i, p, i, p, p]
             L.e2fo_attention_weights.restype = None
             L.e2fo_attention_weights.argtypes = [p, p, p, i, i, i, p, i, ctypes.c_float, p, p, p]
             L.e2fo_conv_edge.restype = i
@@ -186,10 +186,14 @@ def conv_edge(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, rows=None
     return out
 
 
-def conv_edge_vjp(lmax, heads, pos, feat, gy, row_ptr, col_idx, alpha, path_w, want_feat=True, want_alpha=True):
+def conv_edge_vjp(lmax, heads, pos, feat, gy, row_ptr, col_idx, alpha, path_w, want_feat=True, want_alpha=True,
+                  alpha_rows=None, feat_rows=None):
     """Vector-Jacobian products of the layer (by its definition) for the
     output gradient gy [n, (L+1)^2, C]: (gfeat [n, (L+1)^2, C], galpha [E, H]),
-    float64; either may be skipped (None)."""
+    float64; either may be skipped (None).  alpha_rows: receivers whose edges
+    get galpha; feat_rows: senders that get gfeat (default all; others 0)."""
+    arows = _c(alpha_rows, np.int32)
+    frows = _c(feat_rows, np.int32)
     pos = _c(pos, np.float32)
     feat = _c(feat, np.float32)
     gy = _c(gy, np.float64)
@@ -201,7 +205,8 @@ def conv_edge_vjp(lmax, heads, pos, feat, gy, row_ptr, col_idx, alpha, path_w, w
     gf = np.zeros((n, nk, C)) if want_feat else None
     ga = np.zeros((col_idx.shape[0], heads)) if want_alpha else None
     rc = lib().e2fo_conv_edge_vjp(lmax, C, heads, _ptr(pos), _ptr(feat), _ptr(gy), n, _ptr(row_ptr), _ptr(col_idx),
-                                  _ptr(alpha), _ptr(path_w), _ptr(gf), _ptr(ga))
+                                  _ptr(alpha), _ptr(path_w), _ptr(arows), 0 if arows is None else len(arows),
+                                  _ptr(frows), 0 if frows is None else len(frows), _ptr(gf), _ptr(ga))
     if rc:
         raise ValueError("e2fo_conv_edge_vjp rejected its arguments")
     return gf, ga

@@ -509,18 +509,24 @@ int e2fo_conv_edge(int L, int C, int H, const float *pos, const float *feat, int
  *       sum_{f,o} w_afo sum_{mf,m} C^{o m}_{a al, f mf} R^(f)_mf(r_i - r_j) gy[i][o m][c],
  *   galpha[e][h] = sum_{c of head h} sum_{a,f,o} w_afo
  *       sum_{al,mf,m} C^{o m}_{a al, f mf} R^(f)_mf(r_i - r_j) h_j[a al][c] gy[i][o m][c].
- * Either output may be NULL.  gfeat is gathered per sender j over a
- * transposed edge list, so every sum runs in a fixed order. */
+ * Either output may be NULL.  galpha is computed for the edges of the
+ * receivers arows (all if NULL), gfeat for the senders frows (all if NULL);
+ * the rest stays zero.  gfeat is gathered per sender j over a transposed edge
+ * list, so every sum runs in a fixed order. */
 int e2fo_conv_edge_vjp(int L, int C, int H, const float *pos, const float *feat, const double *gy, int n,
                        const int64_t *row_ptr, const int32_t *col_idx, const float *alpha, const double *path_w,
-                       double *gfeat, double *galpha) {
+                       const int32_t *arows, int n_arows, const int32_t *frows, int n_frows, double *gfeat,
+                       double *galpha) {
     if (L < 0 || L > 6 || C < 1 || H < 1 || C % H) return 1;
     const int nk = (L + 1) * (L + 1), dh = C / H;
     const int64_t E = row_ptr[n];
     warm_cg(L, L);
     if (galpha) {
+        memset(galpha, 0, sizeof(double) * (size_t)E * H);
+        const int na = arows ? n_arows : n;
 #pragma omp parallel for schedule(dynamic, 4)
-        for (int i = 0; i < n; ++i) {
+        for (int r = 0; r < na; ++r) {
+            const int i = arows ? arows[r] : r;
             double R[49];
             const double *gyi = gy + (size_t)i * nk * C;
             for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
@@ -566,11 +572,13 @@ int e2fo_conv_edge_vjp(int L, int C, int H, const float *pos, const float *feat,
                 trecv[t] = i;
             }
         free(fill);
+        memset(gfeat, 0, sizeof(double) * (size_t)n * nk * C);
+        const int nf = frows ? n_frows : n;
 #pragma omp parallel for schedule(dynamic, 4)
-        for (int j = 0; j < n; ++j) {
+        for (int r = 0; r < nf; ++r) {
+            const int j = frows ? frows[r] : r;
             double R[49];
             double *g = gfeat + (size_t)j * nk * C;
-            memset(g, 0, sizeof(double) * (size_t)nk * C);
             for (int64_t t = tptr[j]; t < tptr[j + 1]; ++t) {
                 const int64_t e = tedge[t];
                 const int i = trecv[t];

@@ -24,7 +24,7 @@ _STATUS = {0: "E2F_OK", 1: "E2F_EINVAL", 2: "E2F_ECAPACITY", 3: "E2F_ENOMEM", 4:
 # every function declared in include/e2f.h
 EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg", "e2f_knn_graph", "e2f_attention_weights",
             "e2f_recoupling_weight", "e2f_neighbor_list", "e2f_solid_harmonics", "e2f_node_tp",
-            "e2f_wigner6j_conv_forward", "e2f_wigner6j_conv_forward_dense", "e2f_edge_tp_conv_forward", "e2f_profile", "e2f_profile_read", "e2f_last_plan"]
+            "e2f_wigner6j_conv_forward", "e2f_wigner6j_conv_forward_dense", "e2f_wigner6j_conv_backward", "e2f_edge_tp_conv_forward", "e2f_profile", "e2f_profile_read", "e2f_last_plan"]
 
 
 class E2FError(RuntimeError):
@@ -79,6 +79,8 @@ def _load():
         fn.restype = i
     L.e2f_wigner6j_conv_forward_dense.argtypes = [p, ctypes.POINTER(ConvParams), p, p, i32, p, p, p]
     L.e2f_wigner6j_conv_forward_dense.restype = i
+    L.e2f_wigner6j_conv_backward.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, p, i32, p, p, i64, p, p, p, p]
+    L.e2f_wigner6j_conv_backward.restype = i
     return L
 
 
@@ -318,6 +320,28 @@ def e2f_wigner6j_conv_forward_dense(ctx, pos, feat, alpha, lmax, heads, cutoff, 
     del keep
     _check(st, "e2f_wigner6j_conv_forward_dense")
     return out
+
+
+def e2f_wigner6j_conv_backward(ctx, pos, feat, grad_out, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None,
+                               mix_w=None, graph_id=None, tile_side=0.0, want_feat=True, want_alpha=True):
+    """Vector-Jacobian products of the forward: (grad_feat [N,(L+1)^2,C] or
+    None, grad_alpha [E,H] or None)."""
+    for t, name in ((pos, "pos"), (feat, "feat"), (grad_out, "grad_out"), (alpha, "alpha")):
+        _dev(t, torch.float32, name)
+    _dev(row_ptr, torch.int64, "row_ptr")
+    _dev(col_idx, torch.int32, "col_idx")
+    _dev(graph_id, torch.int32, "graph_id")
+    n, nk, C = grad_out.shape
+    E = col_idx.numel()
+    gf = torch.empty_like(grad_out) if want_feat else None
+    ga = torch.empty(E, heads, dtype=torch.float32, device=grad_out.device) if want_alpha else None
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side)
+    st = lib.e2f_wigner6j_conv_backward(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(graph_id), _ptr(feat),
+                                        _ptr(grad_out), n, _ptr(row_ptr), _ptr(col_idx), E, _ptr(alpha), _ptr(gf),
+                                        _ptr(ga), _stream(grad_out.device))
+    del keep
+    _check(st, "e2f_wigner6j_conv_backward")
+    return gf, ga
 
 
 def e2f_profile(ctx: Context, enable: bool) -> None:

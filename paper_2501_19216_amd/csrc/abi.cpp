@@ -56,6 +56,8 @@ struct e2f_ctx {
   size_t pinned_plan_n = 0;
   std::vector<double> origins_host;
   Buf a, b, c;
+  Buf d;                                   // backward staging (transposed graph, input gradient)
+  std::vector<std::vector<double>> kappa;  // per L: [a][f][o] real CG transpose factors (0 = not computed)
   int64_t last_pairs = 0, last_tiles = 0;  // plan size of the last factorised forward
   int64_t last_batches = 0;
   // kernel timing (e2f_profile): events recorded on the launch stream
@@ -336,6 +338,42 @@ e2f_status run_bbox(e2f_ctx* ctx, const float* pos, const int32_t* graph_id, int
   return E2F_OK;
 }
 
+// Real CG tensors of (a, f, o) and (o, f, a) are proportional with the first
+// and last index swapped: C[a,f,o][al][mf][m] = kappa C[o,f,a][m][mf][al].
+// kappa is read off the library's own tables and the proportionality checked.
+e2f_status transpose_factors(e2f_ctx* ctx, int L, const std::vector<double>*& out) {
+  if ((int)ctx->kappa.size() <= L) ctx->kappa.resize(L + 1);
+  std::vector<double>& k = ctx->kappa[L];
+  const int L1 = L + 1;
+  if (k.empty()) {
+    std::vector<double> v((size_t)L1 * L1 * L1, 0.0);
+    for (int a = 0; a <= L; ++a)
+      for (int f = 0; f <= L; ++f)
+        for (int o = std::abs(a - f); o <= std::min(a + f, L); ++o) {
+          const std::vector<double> A = real_cg(a, f, o), B = real_cg(o, f, a);
+          const int na = 2 * a + 1, nf = 2 * f + 1, no = 2 * o + 1;
+          double num = 0.0, den = 0.0;
+          for (int x = 0; x < na; ++x)
+            for (int y = 0; y < nf; ++y)
+              for (int z = 0; z < no; ++z) {
+                const double bt = B[((size_t)z * nf + y) * na + x];
+                num += A[((size_t)x * nf + y) * no + z] * bt;
+                den += bt * bt;
+              }
+          const double kap = num / den;
+          for (int x = 0; x < na; ++x)
+            for (int y = 0; y < nf; ++y)
+              for (int z = 0; z < no; ++z)
+                if (std::fabs(A[((size_t)x * nf + y) * no + z] - kap * B[((size_t)z * nf + y) * na + x]) > 1e-12)
+                  return fail(E2F_EUNSUPPORTED, "real CG (%d,%d,%d) is not a multiple of its transpose", a, f, o);
+          v[((size_t)a * L1 + f) * L1 + o] = kap;
+        }
+    k.swap(v);
+  }
+  out = &k;
+  return E2F_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -389,7 +427,7 @@ void e2f_destroy(e2f_ctx* ctx) {
       if (p) (void)hipFree(p);
     for (void* p : ctx->coef_mem)
       if (p) (void)hipFree(p);
-    for (Buf* b : {&ctx->a, &ctx->b, &ctx->c})
+    for (Buf* b : {&ctx->a, &ctx->b, &ctx->c, &ctx->d})
       if (b->p) (void)hipFree(b->p);
     if (ctx->blas) (void)rocblas_destroy_handle(ctx->blas);
     for (auto& r : ctx->recs) {
@@ -779,6 +817,85 @@ e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, cons
   }
   E2F_TIMED("edge_tp", launch_edge_tp(ctx->dev[L], pos, feat, row_ptr, col_idx, alpha, n, C, p->heads, y, s));
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
+  return E2F_OK;
+}
+
+e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos,
+                                      const int32_t* graph_id, const float* feat, const float* grad_out, int32_t n,
+                                      const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges,
+                                      const float* alpha, float* grad_feat, float* grad_alpha, void* stream) {
+  if (!grad_feat && !grad_alpha) return fail(E2F_EINVAL, "neither grad_feat nor grad_alpha is requested");
+  if (grad_alpha && n > 0 && !feat) return fail(E2F_EINVAL, "feat is required for grad_alpha");
+  e2f_status rs = check_params(ctx, p);
+  if (rs != E2F_OK) return rs;
+  if (grad_alpha && p->channels > 256) return fail(E2F_EUNSUPPORTED, "grad_alpha needs channels <= 256");
+  rs = check_conv(ctx, p, pos, grad_out, n, row_ptr, col_idx, n_edges, const_cast<float*>(grad_out));
+  if (rs != E2F_OK) return rs;
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  const int L = p->lmax, C = p->channels, H = p->heads, nk = nk_of(L), L1 = L + 1;
+  const std::vector<double> w = path_weights(p);
+  rs = set_weights(ctx, L, w, s);
+  if (rs != E2F_OK) return rs;
+  if (n == 0) return E2F_OK;
+  const bool mixing = p->mix_w != nullptr;
+  const size_t wt_bytes = (size_t)L1 * C * C * (p->mix_dtype == E2F_BF16 ? 2 : 4);
+  const size_t tmp_b = transpose_tmp_bytes(n, n_edges);
+  const bool want_t = grad_feat != nullptr && n_edges > 0;
+  const size_t need = (mixing ? al256(sizeof(float) * (size_t)n * nk * C) + al256(wt_bytes) : 0) +
+                      (want_t ? 5 * al256(sizeof(int32_t) * (size_t)n_edges) + 2 * al256(sizeof(int64_t) * (n + 1)) +
+                                    al256(sizeof(float) * (size_t)n_edges * H) + al256(tmp_b)
+                              : 0) + 256;
+  rs = ensure(ctx, ctx->d, need, s);
+  if (rs != E2F_OK) return rs;
+  Carver cd{(char*)ctx->d.p};
+  // ---- gradient of the unmixed output: y-bar = W^T out-bar per degree
+  const float* gy = grad_out;
+  if (mixing) {
+    float* gyb = cd.take<float>((size_t)n * nk * C);
+    void* WT = cd.take<char>(wt_bytes);
+    E2F_TIMED("mix", launch_transpose_mix(p->mix_w, p->mix_dtype == E2F_BF16, L, C, WT, s));
+    E2F_TIMED("mix", launch_mix(L, grad_out, WT, p->mix_dtype == E2F_BF16, n, C, gyb, s));
+    gy = gyb;
+  }
+  // ---- attention weights: per edge, by the edge filter
+  if (grad_alpha && n_edges > 0)
+    E2F_TIMED("edge_vjp_alpha", launch_edge_vjp_alpha(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, n, C, H,
+                                                      grad_alpha, s));
+  // ---- features: the same layer on the transposed graph, input degree o,
+  // output degree a, weights w[a][f][o] kappa(a,f,o) (-1)^f
+  if (grad_feat) {
+    if (n_edges == 0) {
+      E2F_HIP(hipMemsetAsync(grad_feat, 0, sizeof(float) * (size_t)n * nk * C, s));
+      return E2F_OK;
+    }
+    const std::vector<double>* kap = nullptr;
+    rs = transpose_factors(ctx, L, kap);
+    if (rs != E2F_OK) return rs;
+    std::vector<double> wt((size_t)L1 * L1 * L1, 0.0);
+    for (int a = 0; a <= L; ++a)
+      for (int f = 0; f <= L; ++f)
+        for (int o = std::abs(a - f); o <= std::min(a + f, L); ++o) {
+          const size_t q = ((size_t)a * L1 + f) * L1 + o;
+          wt[((size_t)o * L1 + f) * L1 + a] = w[q] * (*kap)[q] * ((f & 1) ? -1.0 : 1.0);
+        }
+    int32_t* rows = cd.take<int32_t>((size_t)n_edges);
+    int32_t* iota = cd.take<int32_t>((size_t)n_edges);
+    int32_t* keys_out = cd.take<int32_t>((size_t)n_edges);
+    int32_t* perm = cd.take<int32_t>((size_t)n_edges);
+    int32_t* colT = cd.take<int32_t>((size_t)n_edges);
+    int64_t* cnt = cd.take<int64_t>((size_t)n + 1);
+    int64_t* rowT = cd.take<int64_t>((size_t)n + 1);
+    float* alphaT = cd.take<float>((size_t)n_edges * H);
+    void* tmp = cd.take<char>(tmp_b);
+    E2F_TIMED("transpose", launch_transpose_graph(row_ptr, col_idx, alpha, n, n_edges, H, rows, iota, keys_out, perm,
+                                                  cnt, rowT, colT, alpha ? alphaT : nullptr, tmp, tmp_b, s));
+    e2f_conv_params pt = *p;
+    pt.path_w = wt.data();
+    pt.mix_w = nullptr;
+    return e2f_wigner6j_conv_forward(ctx, &pt, pos, graph_id, gy, n, rowT, colT, n_edges, alpha ? alphaT : nullptr,
+                                     grad_feat, stream);
+  }
   return E2F_OK;
 }
 

@@ -840,6 +840,110 @@ __global__ void k_plan_pack(const int32_t* __restrict__ pidx, const int32_t* __r
   if (t < keys) out[4 + keys + t] = pstart[t];
 }
 
+// ------------------------------------------------------------ backward
+// Gradient with respect to the attention weights: per edge e = (i, j) and
+// head h, galpha = sum_{c of h} sum_k gy_i[k][c] (K_e h_j)[k][c] with the edge
+// filter K_e of the baseline built once per edge in LDS.  One thread per
+// channel; the per-head sums run over the channels in order (deterministic).
+template <int L>
+__global__ __launch_bounds__(256) void k_edge_vjp_alpha(DevTables t, const float* __restrict__ pos,
+                                                        const float* __restrict__ feat, const float* __restrict__ gy,
+                                                        const int64_t* __restrict__ row_ptr,
+                                                        const int32_t* __restrict__ col, int C, int H,
+                                                        float* __restrict__ galpha) {
+  constexpr int NK = (L + 1) * (L + 1);
+  constexpr int EB = 4;
+  extern __shared__ float sm[];
+  float* Kl = sm;                        // [EB][NK*NK]
+  float* Rl = Kl + EB * NK * NK;         // [EB][NK]
+  float* vb = Rl + EB * NK;              // [EB][blockDim.x]
+  const int i = blockIdx.x;
+  const int dh = C / H;
+  const int c = threadIdx.x;
+  const bool live = c < C;
+  const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+  const float xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
+  float g[NK];
+#pragma unroll
+  for (int k = 0; k < NK; ++k) g[k] = live ? gy[((size_t)i * NK + k) * C + c] : 0.0f;
+  for (int64_t eb = e0; eb < e1; eb += EB) {
+    const int nb = (e1 - eb) < EB ? (int)(e1 - eb) : EB;
+    __syncthreads();
+    for (int q = threadIdx.x; q < nb * NK; q += blockDim.x) {
+      const int b = q / NK, k = q % NK;
+      const int j = col[eb + b];
+      Rl[q] = sh_poly<float>(t, k, xi - pos[3 * j], yi - pos[3 * j + 1], zi - pos[3 * j + 2]);
+    }
+    __syncthreads();
+    for (int q = threadIdx.x; q < nb * NK * NK; q += blockDim.x) {
+      const int b = q / (NK * NK), s = q % (NK * NK);
+      float v = 0.0f;
+      for (int e = t.k_ptr[s]; e < t.k_ptr[s + 1]; ++e) v += t.k_coef[e] * Rl[b * NK + t.k_ridx[e]];
+      Kl[q] = v;
+    }
+    __syncthreads();
+    for (int b = 0; b < nb; ++b) {
+      float v = 0.0f;
+      if (live) {
+        const int j = col[eb + b];
+        const float* Kb = Kl + b * NK * NK;
+#pragma unroll
+        for (int q = 0; q < NK; ++q) {
+          float u = 0.0f;
+#pragma unroll
+          for (int k = 0; k < NK; ++k) u += g[k] * Kb[k * NK + q];
+          v += u * feat[((size_t)j * NK + q) * C + c];
+        }
+      }
+      vb[b * blockDim.x + threadIdx.x] = v;
+    }
+    __syncthreads();
+    for (int q = threadIdx.x; q < nb * H; q += blockDim.x) {
+      const int b = q / H, h = q % H;
+      float s = 0.0f;
+      for (int tt = 0; tt < dh; ++tt) s += vb[b * blockDim.x + h * dh + tt];
+      galpha[(eb + b) * H + h] = s;
+    }
+  }
+}
+
+// transposed graph: rows[e] = receiver of edge e; counts of every sender
+__global__ void k_edge_rows(const int64_t* __restrict__ row_ptr, int n, int32_t* __restrict__ rows) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) rows[e] = i;
+}
+
+__global__ void k_sender_counts(const int32_t* __restrict__ col, int64_t E, int n, int64_t* __restrict__ cnt,
+                                int32_t* __restrict__ iota) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e < E) {
+    atomicAdd((unsigned long long*)&cnt[col[e]], 1ull);
+    iota[e] = (int32_t)e;
+  }
+}
+
+__global__ void k_transpose_gather(const int32_t* __restrict__ perm, const int32_t* __restrict__ rows,
+                                   const float* __restrict__ alpha, int64_t E, int H, int32_t* __restrict__ colT,
+                                   float* __restrict__ alphaT) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= E) return;
+  const int64_t e = perm[t];
+  colT[t] = rows[e];
+  if (alpha)
+    for (int h = 0; h < H; ++h) alphaT[t * H + h] = alpha[e * H + h];
+}
+
+// W^T[o][c][c'] = W[o][c'][c] (elements of `bytes` bytes)
+template <typename E>
+__global__ void k_transpose_mix(const E* __restrict__ W, int L1, int C, E* __restrict__ WT) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= (int64_t)L1 * C * C) return;
+  const int64_t o = q / ((int64_t)C * C), r = q % ((int64_t)C * C);
+  const int a = (int)(r / C), b = (int)(r % C);
+  WT[(o * C + b) * C + a] = W[q];
+}
+
 // ------------------------------------------------------------ dense graphs
 // Every atom attends to every other (the dense graphs of the scaling study,
 // Sec. 4.1): the aggregation S_h = A_h T_h is a dense product with
@@ -1200,6 +1304,67 @@ hipError_t launch_iota(int n, int32_t* v, hipStream_t s) {
 hipError_t launch_plan_pack(const int32_t* pidx, const int32_t* flags, int64_t count, const int32_t* max_degree,
                             const int32_t* rstart, const int32_t* pstart, int keys, int32_t* out, hipStream_t s) {
   k_plan_pack<<<(keys + 256) / 256, 256, 0, s>>>(pidx, flags, count, max_degree, rstart, pstart, keys, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_vjp_alpha(const DevTables& t, const float* pos, const float* feat, const float* gy,
+                                 const int64_t* row_ptr, const int32_t* col_idx, int n, int C, int H, float* galpha,
+                                 hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  if (C > 256) return hipErrorInvalidValue;
+  const int threads = (C + 63) / 64 * 64;
+  const size_t lds = sizeof(float) * ((size_t)4 * t.nk * t.nk + (size_t)4 * t.nk + (size_t)4 * threads);
+  switch (t.L) {
+#define E2F_CASE(LL)                                                                                        \
+  case LL:                                                                                                  \
+    if (hipError_t e = allow_lds(k_edge_vjp_alpha<LL>, lds); e != hipSuccess) return e;                     \
+    k_edge_vjp_alpha<LL><<<n, threads, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx, C, H, galpha);         \
+    break;
+    E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
+#undef E2F_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+size_t transpose_tmp_bytes(int n, int64_t E) {
+  size_t a = 0, b = 0;
+  hipcub::DeviceRadixSort::SortPairs(nullptr, a, (const int32_t*)nullptr, (int32_t*)nullptr, (const int32_t*)nullptr,
+                                     (int32_t*)nullptr, (int)E);
+  hipcub::DeviceScan::ExclusiveSum(nullptr, b, (int64_t*)nullptr, (int64_t*)nullptr, n + 1);
+  return std::max(a, b);
+}
+
+hipError_t launch_transpose_graph(const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n,
+                                  int64_t E, int H, int32_t* rows, int32_t* iota, int32_t* keys_out, int32_t* perm,
+                                  int64_t* cnt, int64_t* rowT_ptr, int32_t* colT, float* alphaT, void* tmp,
+                                  size_t tmp_bytes, hipStream_t s) {
+  hipError_t e = hipMemsetAsync(cnt, 0, sizeof(int64_t) * (size_t)(n + 1), s);
+  if (e != hipSuccess) return e;
+  if (E > 0) {
+    k_edge_rows<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, n, rows);
+    k_sender_counts<<<(unsigned)((E + 255) / 256), 256, 0, s>>>(col_idx, E, n, cnt, iota);
+    int bits = 1;
+    while ((1LL << bits) < (int64_t)n) ++bits;
+    size_t b = tmp_bytes;
+    // stable: edges of one sender keep their (ascending receiver) order
+    if ((e = hipcub::DeviceRadixSort::SortPairs(tmp, b, col_idx, keys_out, iota, perm, (int)E, 0, bits, s)) !=
+        hipSuccess)
+      return e;
+  }
+  size_t b = tmp_bytes;
+  if ((e = hipcub::DeviceScan::ExclusiveSum(tmp, b, cnt, rowT_ptr, n + 1, s)) != hipSuccess) return e;
+  if (E > 0) k_transpose_gather<<<(unsigned)((E + 255) / 256), 256, 0, s>>>(perm, rows, alpha, E, H, colT, alphaT);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_mix(const void* W, bool bf16, int L, int C, void* WT, hipStream_t s) {
+  const int64_t total = (int64_t)(L + 1) * C * C;
+  const unsigned grid = (unsigned)((total + 255) / 256);
+  if (bf16)
+    k_transpose_mix<uint16_t><<<grid, 256, 0, s>>>((const uint16_t*)W, L + 1, C, (uint16_t*)WT);
+  else
+    k_transpose_mix<float><<<grid, 256, 0, s>>>((const float*)W, L + 1, C, (float*)WT);
   return hipGetLastError();
 }
 

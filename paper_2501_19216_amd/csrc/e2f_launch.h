@@ -100,6 +100,21 @@ hipError_t launch_attention(const float* pos, const float* q, const float* k, in
                             const float* rbf_w, int R, float rc, const int64_t* row_ptr, const int32_t* col_idx,
                             float* alpha, hipStream_t s);
 
+// ---- backward
+// galpha[e][h] = sum_{c of h} <gy_i[.][c], (K_e h_j)[.][c]> for the edges of rows 0..n-1 (C <= 256)
+hipError_t launch_edge_vjp_alpha(const DevTables& t, const float* pos, const float* feat, const float* gy,
+                                 const int64_t* row_ptr, const int32_t* col_idx, int n, int C, int H, float* galpha,
+                                 hipStream_t s);
+// transposed CSR (row = sender, ascending receivers) and alpha in its order;
+// scratch: rows, iota, keys_out, perm [E], cnt [n+1]
+size_t transpose_tmp_bytes(int n, int64_t E);
+hipError_t launch_transpose_graph(const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n,
+                                  int64_t E, int H, int32_t* rows, int32_t* iota, int32_t* keys_out, int32_t* perm,
+                                  int64_t* cnt, int64_t* rowT_ptr, int32_t* colT, float* alphaT, void* tmp,
+                                  size_t tmp_bytes, hipStream_t s);
+// WT[o][c][c'] = W[o][c'][c], float32 or bf16 elements
+hipError_t launch_transpose_mix(const void* W, bool bf16, int L, int C, void* WT, hipStream_t s);
+
 // ---- dense graphs: A[h][i][j] = alpha[i][j][h] (1 if alpha is NULL), 0 for i == j
 hipError_t launch_dense_alpha(const float* alpha, int n, int H, float* A, hipStream_t s);
 hipError_t launch_iota(int n, int32_t* v, hipStream_t s);
