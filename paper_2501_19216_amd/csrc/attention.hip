@@ -5,9 +5,10 @@
 //   alpha[(i,j)][h] = env(d) * softmax over the row of logit[.][h],
 //   env(d) = (cos(pi d / cutoff) + 1) / 2 below the cutoff, 0 from it on.
 // One wave per receiver row: lane l takes head l % Hp (Hp = H rounded up to a
-// power of two) and every (64/Hp)-th edge, so a wave's writes of alpha
+// power of two) and every (64/Hp)-th edge, so a wave's accesses of alpha
 // [E][H] are contiguous and the per-head max and sum are xor-shuffle
-// reductions over the lanes of one head (fixed order: deterministic).
+// reductions over the lanes of one head (fixed order: deterministic).  The
+// logits are computed once and kept in alpha between the passes.
 #include <hip/hip_runtime.h>
 
 #include "e2f_launch.h"
@@ -36,6 +37,12 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ pos
   const float sigma = rc / (float)(R - 1), inv = 1.0f / sigma;
   const float xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
   const float* qi = q + ((size_t)i * H + hc) * dk;
+  // q of this lane's head in registers, as float4 (d_k a multiple of 4, up to 64)
+  const bool vec = (dk & 3) == 0 && dk <= 64;
+  float4 q4[16];
+#pragma unroll
+  for (int t = 0; t < 16; ++t)
+    q4[t] = (vec && 4 * t < dk) ? ((const float4*)qi)[t] : make_float4(0.f, 0.f, 0.f, 0.f);
   const float kPi = 3.14159265358979f;
   auto logit = [&](int64_t e, float& env) {
     const int j = col[e];
@@ -43,7 +50,17 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ pos
     const float d = sqrtf(dx * dx + dy * dy + dz * dz);
     const float* kj = kf + ((size_t)j * H + hc) * dk;
     float l = 0.0f;
-    for (int t = 0; t < dk; ++t) l += qi[t] * kj[t];
+    if (vec) {
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        if (4 * t < dk) {
+          const float4 kv = ((const float4*)kj)[t];
+          l += q4[t].x * kv.x + q4[t].y * kv.y + q4[t].z * kv.z + q4[t].w * kv.w;
+        }
+      }
+    } else {
+      for (int t = 0; t < dk; ++t) l += qi[t] * kj[t];
+    }
 #pragma unroll
     for (int r = 0; r < kAttnMaxRbf; ++r) {
       if (r < R) {
@@ -54,25 +71,33 @@ __global__ __launch_bounds__(256) void k_attention(const float* __restrict__ pos
     env = d < rc ? 0.5f * (cosf(kPi * d / rc) + 1.0f) : 0.0f;
     return l;
   };
+  // pass 1: logits, kept in the output; pass 2: exponentials; pass 3: scale
   float mx = -INFINITY;
   for (int64_t e = e0 + el; e < e1; e += EPI) {
     float env;
-    mx = fmaxf(mx, logit(e, env));
+    const float l = logit(e, env);
+    if (hv) alpha[e * H + h] = l;
+    mx = fmaxf(mx, l);
   }
 #pragma unroll
   for (int o = 32; o >= HP; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
   float den = 0.0f;
   for (int64_t e = e0 + el; e < e1; e += EPI) {
-    float env;
-    den += expf(logit(e, env) - mx);
+    if (!hv) continue;
+    const float ex = expf(alpha[e * H + h] - mx);
+    alpha[e * H + h] = ex;
+    den += ex;
   }
 #pragma unroll
   for (int o = 32; o >= HP; o >>= 1) den += __shfl_xor(den, o);
   const float rden = 1.0f / den;
   for (int64_t e = e0 + el; e < e1; e += EPI) {
-    float env;
-    const float ex = expf(logit(e, env) - mx);
-    if (hv) alpha[e * H + h] = env * ex * rden;
+    if (!hv) continue;
+    const int j = col[e];
+    const float dx = xi - pos[3 * j], dy = yi - pos[3 * j + 1], dz = zi - pos[3 * j + 2];
+    const float d = sqrtf(dx * dx + dy * dy + dz * dz);
+    const float env = d < rc ? 0.5f * (cosf(kPi * d / rc) + 1.0f) : 0.0f;
+    alpha[e * H + h] = env * alpha[e * H + h] * rden;
   }
 }
 

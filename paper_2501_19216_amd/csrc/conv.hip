@@ -845,14 +845,14 @@ __global__ void k_plan_pack(const int32_t* __restrict__ pidx, const int32_t* __r
 // head h, galpha = sum_{c of h} sum_k gy_i[k][c] (K_e h_j)[k][c] with the edge
 // filter K_e of the baseline built once per edge in LDS.  One thread per
 // channel; the per-head sums run over the channels in order (deterministic).
-template <int L>
+template <int L, bool SHFL>
 __global__ __launch_bounds__(256) void k_edge_vjp_alpha(DevTables t, const float* __restrict__ pos,
                                                         const float* __restrict__ feat, const float* __restrict__ gy,
                                                         const int64_t* __restrict__ row_ptr,
                                                         const int32_t* __restrict__ col, int C, int H,
                                                         float* __restrict__ galpha) {
   constexpr int NK = (L + 1) * (L + 1);
-  constexpr int EB = 4;
+  constexpr int EB = 8;
   extern __shared__ float sm[];
   float* Kl = sm;                        // [EB][NK*NK]
   float* Rl = Kl + EB * NK * NK;         // [EB][NK]
@@ -895,14 +895,22 @@ __global__ __launch_bounds__(256) void k_edge_vjp_alpha(DevTables t, const float
           v += u * feat[((size_t)j * NK + q) * C + c];
         }
       }
-      vb[b * blockDim.x + threadIdx.x] = v;
+      if (SHFL) {
+        // the dh channels of a head are consecutive lanes of one wave
+        for (int o = dh >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o);
+        if (live && c % dh == 0) galpha[(eb + b) * H + c / dh] = v;
+      } else {
+        vb[b * blockDim.x + threadIdx.x] = v;
+      }
     }
-    __syncthreads();
-    for (int q = threadIdx.x; q < nb * H; q += blockDim.x) {
-      const int b = q / H, h = q % H;
-      float s = 0.0f;
-      for (int tt = 0; tt < dh; ++tt) s += vb[b * blockDim.x + h * dh + tt];
-      galpha[(eb + b) * H + h] = s;
+    if (!SHFL) {
+      __syncthreads();
+      for (int q = threadIdx.x; q < nb * H; q += blockDim.x) {
+        const int b = q / H, h = q % H;
+        float s = 0.0f;
+        for (int tt = 0; tt < dh; ++tt) s += vb[b * blockDim.x + h * dh + tt];
+        galpha[(eb + b) * H + h] = s;
+      }
     }
   }
 }
@@ -1313,12 +1321,19 @@ hipError_t launch_edge_vjp_alpha(const DevTables& t, const float* pos, const flo
   if (n == 0) return hipSuccess;
   if (C > 256) return hipErrorInvalidValue;
   const int threads = (C + 63) / 64 * 64;
-  const size_t lds = sizeof(float) * ((size_t)4 * t.nk * t.nk + (size_t)4 * t.nk + (size_t)4 * threads);
+  const int dh = C / H;
+  const bool shfl = (dh & (dh - 1)) == 0 && dh <= 64;
+  const size_t lds = sizeof(float) * ((size_t)8 * t.nk * t.nk + (size_t)8 * t.nk + (size_t)8 * threads);
   switch (t.L) {
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
-    if (hipError_t e = allow_lds(k_edge_vjp_alpha<LL>, lds); e != hipSuccess) return e;                     \
-    k_edge_vjp_alpha<LL><<<n, threads, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx, C, H, galpha);         \
+    if (shfl) {                                                                                             \
+      if (hipError_t e = allow_lds(k_edge_vjp_alpha<LL, true>, lds); e != hipSuccess) return e;             \
+      k_edge_vjp_alpha<LL, true><<<n, threads, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx, C, H, galpha); \
+    } else {                                                                                                \
+      if (hipError_t e = allow_lds(k_edge_vjp_alpha<LL, false>, lds); e != hipSuccess) return e;            \
+      k_edge_vjp_alpha<LL, false><<<n, threads, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx, C, H, galpha);\
+    }                                                                                                       \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
 #undef E2F_CASE
