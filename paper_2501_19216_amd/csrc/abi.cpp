@@ -496,10 +496,13 @@ e2f_status e2f_neighbor_list(e2f_ctx* ctx, const float* pos, const int32_t* grap
   }
   rs = ensure(ctx, ctx->a, nl_scratch_bytes(n, cg), s);
   if (rs != E2F_OK) return rs;
-  E2F_TIMED("nl_count", launch_nl_count(pos, graph_id, n, rc * rc, cg, ctx->a.p, row_ptr, s));
+  E2F_TIMED("nl_count", launch_nl_count(pos, graph_id, n, rc * rc, cg, ctx->a.p, row_ptr, ctx->stats + 9, s));
   E2F_HIP(hipMemcpyAsync(ctx->pinned, row_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  E2F_HIP(hipMemcpyAsync(ctx->pinned + 1, ctx->stats + 9, sizeof(int), hipMemcpyDeviceToHost, s));
   E2F_HIP(hipStreamSynchronize(s));
   const int64_t E = ctx->pinned[0];
+  int max_degree = 0;
+  std::memcpy(&max_degree, ctx->pinned + 1, sizeof(int));
   *n_edges = E;
   if (!col_idx || E > capacity) return fail(E2F_ECAPACITY, "the graph has %lld edges", (long long)E);
   if (E > std::numeric_limits<int32_t>::max()) return fail(E2F_EUNSUPPORTED, "more than 2^31-1 edges");
@@ -510,7 +513,8 @@ e2f_status e2f_neighbor_list(e2f_ctx* ctx, const float* pos, const int32_t* grap
   Carver cv{(char*)ctx->b.p};
   int32_t* unsorted = cv.take<int32_t>((size_t)E);
   void* sort_tmp = cv.take<char>(sort_b);
-  E2F_TIMED("nl_fill", launch_nl_fill(pos, graph_id, n, rc * rc, cg, ctx->a.p, row_ptr, unsorted, col_idx, E, sort_tmp, sort_b, s));
+  E2F_TIMED("nl_fill", launch_nl_fill(pos, graph_id, n, rc * rc, cg, ctx->a.p, row_ptr, unsorted, col_idx, E,
+                                      max_degree, sort_tmp, sort_b, s));
   return E2F_OK;
 }
 

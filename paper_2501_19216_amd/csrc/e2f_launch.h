@@ -21,12 +21,15 @@ struct CellGrid {
   int64_t ncell;
 };
 size_t nl_scratch_bytes(int n, const CellGrid& g);  // cell tables and counts
+// max_degree: device int, receives the largest row length
 hipError_t launch_nl_count(const float* pos, const int32_t* graph_id, int n, double r2, const CellGrid& g,
-                           void* scratch, int64_t* row_ptr, hipStream_t s);
+                           void* scratch, int64_t* row_ptr, int* max_degree, hipStream_t s);
 // After the count: sorts n+1 counts into row_ptr (exclusive scan).  Part of launch_nl_count.
+// rows up to 1024 long are sorted in LDS; longer graphs go through `unsorted`
+// and a segmented sort
 hipError_t launch_nl_fill(const float* pos, const int32_t* graph_id, int n, double r2, const CellGrid& g,
                           void* scratch, const int64_t* row_ptr, int32_t* unsorted, int32_t* col_idx, int64_t E,
-                          void* sort_tmp, size_t sort_tmp_bytes, hipStream_t s);
+                          int max_degree, void* sort_tmp, size_t sort_tmp_bytes, hipStream_t s);
 size_t nl_sort_tmp_bytes(int n, int64_t E);
 // k-nearest-neighbour graph: row sizes min(k, graph size - 1) into row_ptr
 // (graph ids in [0, ngraph)), then the rows (k <= kKnnMaxK).

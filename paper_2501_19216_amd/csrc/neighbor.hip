@@ -1,8 +1,9 @@
 // Radius graph on gfx950 (Alg. 1 step 2: D_ij = |r_i - r_j|, kept below the
 // cutoff).  Cell list with integer cell coordinates on the 2^-16 A grid:
 //   bbox (atomic min/max) -> cell counts -> exclusive scan -> cell members ->
-//   per-atom neighbour count over the 27 cells (exact integer predicate) ->
-//   exclusive scan into row_ptr -> fill -> segmented sort of every row.
+//   per-atom neighbour count over the 27 cells (exact integer predicate; one
+//   64-lane workgroup per atom) -> exclusive scan into row_ptr -> fill with
+//   every row sorted in LDS (rows above 1024: fill, then a segmented sort).
 // Only integer atomics are used, and the rows are sorted at the end, so the
 // CSR is bitwise deterministic.
 #include <hip/hip_runtime.h>
@@ -113,6 +114,113 @@ __global__ void k_neighbors(const float* __restrict__ pos, const int32_t* __rest
     }
   }
   if (!WRITE) counts[i] = cnt;
+}
+
+// One 64-lane workgroup per atom i: the members of the 27 cells around i are
+// enumerated as one list through a prefix over the cells (lane c < 27 holds
+// cell c), 64 candidates at a time.  Count: ballot totals, and the largest
+// degree.  Fill: the row is collected in LDS, sorted there (bitonic) and
+// written in ascending order; rows longer than kNlRowMax take the global
+// segmented sort instead (the host picks the path from the largest degree).
+constexpr int kNlRowMax = 1024;
+
+__device__ __forceinline__ int wave_prefix_incl(int v, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(v, o);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+template <bool WRITE>
+__global__ __launch_bounds__(64) void k_neighbors_wave(const float* __restrict__ pos, const int32_t* __restrict__ gid,
+                                                       int n, double r2, Grid g, const int* __restrict__ cell_of,
+                                                       const int* __restrict__ cell_start,
+                                                       const int* __restrict__ members, int64_t* __restrict__ counts,
+                                                       int* __restrict__ max_degree,
+                                                       const int64_t* __restrict__ row_ptr, int32_t* __restrict__ out) {
+  __shared__ int32_t row[kNlRowMax];
+  const int i = blockIdx.x, lane = threadIdx.x;
+  const int xi = grid_coord(pos[3 * i]), yi = grid_coord(pos[3 * i + 1]), zi = grid_coord(pos[3 * i + 2]);
+  const int gi = gid ? gid[i] : 0;
+  const int c = cell_of[i];
+  const int cx = c % g.d0, cy = (c / g.d0) % g.d1, cz = c / (g.d0 * g.d1);
+  // lane q < 27: neighbour cell q (dx, dy, dz in -1..1), its first member and count
+  int cs = 0, cn = 0;
+  if (lane < 27) {
+    const int x = cx + lane % 3 - 1, y = cy + (lane / 3) % 3 - 1, z = cz + lane / 9 - 1;
+    if (x >= 0 && x < g.d0 && y >= 0 && y < g.d1 && z >= 0 && z < g.d2) {
+      const int cc = (z * g.d1 + y) * g.d0 + x;
+      cs = cell_start[cc];
+      cn = cell_start[cc + 1] - cs;
+    }
+  }
+  const int incl = wave_prefix_incl(cn, lane);
+  const int total = __shfl(incl, 63);
+  int found = 0;
+  for (int t0 = 0; t0 < total; t0 += 64) {
+    // every lane searches (the shuffles need the whole wave); lanes past the
+    // list search for the last candidate and count nothing
+    const int t = t0 + lane;
+    const bool valid = t < total;
+    const int tc = valid ? t : total - 1;
+    // cell of candidate tc: the first q with incl[q] > tc, i.e. the number of
+    // q with incl[q] <= tc (incl is nondecreasing and incl[26..63] = total >
+    // tc).  Five fixed steps with no branch around the shuffles: every lane
+    // of the wave takes part in each one (a lane that had left a data-dependent
+    // loop would not supply its value).
+    int lo = 0;
+#pragma unroll
+    for (int step = 16; step >= 1; step >>= 1) {
+      const int v = __shfl(incl, lo + step - 1);
+      lo += v <= tc ? step : 0;
+    }
+    const int cnl = __shfl(cn, lo), off = tc - (__shfl(incl, lo) - cnl), base = __shfl(cs, lo);
+    const bool inr = off >= 0 && off < cnl;  // always true; keeps every read inside the cell
+    const int j = inr ? members[base + off] : i;
+    bool hit = false;
+    if (valid && j != i && (!gid || gid[j] == gi)) {
+      const int64_t ddx = (int64_t)grid_coord(pos[3 * j]) - xi;
+      const int64_t ddy = (int64_t)grid_coord(pos[3 * j + 1]) - yi;
+      const int64_t ddz = (int64_t)grid_coord(pos[3 * j + 2]) - zi;
+      const int64_t d2 = ddx * ddx + ddy * ddy + ddz * ddz;  // < 2^53 for cutoff <= 64 A
+      hit = (double)d2 < r2;
+    }
+    const uint64_t m = __ballot(hit);
+    if (WRITE && hit) {
+      const int rank = __popcll(m & ((1ull << lane) - 1));
+      row[found + rank] = j;
+    }
+    found += __popcll(m);
+  }
+  if (!WRITE) {
+    if (lane == 0) {
+      counts[i] = found;
+      atomicMax(max_degree, found);
+    }
+    return;
+  }
+  __syncthreads();
+  int p2 = 1;
+  while (p2 < found) p2 <<= 1;
+  for (int q = found + lane; q < p2; q += 64) row[q] = INT_MAX;
+  __syncthreads();
+  for (int size = 2; size <= p2; size <<= 1)
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int t = lane; t < p2 / 2; t += 64) {
+        const int lo = 2 * t - (t & (stride - 1)), hi = lo + stride;
+        const bool up = (lo & size) == 0;
+        const int a = row[lo], b = row[hi];
+        if ((a > b) == up) {
+          row[lo] = b;
+          row[hi] = a;
+        }
+      }
+      __syncthreads();
+    }
+  const int64_t r0 = row_ptr[i];
+  for (int q = lane; q < found; q += 64) out[r0 + q] = row[q];
 }
 
 __global__ void k_zero_last(int64_t* counts, int n) { counts[n] = 0; }
@@ -287,7 +395,7 @@ size_t nl_scratch_bytes(int n, const CellGrid& g) {
 }
 
 hipError_t launch_nl_count(const float* pos, const int32_t* graph_id, int n, double r2, const CellGrid& cg,
-                           void* scratch, int64_t* row_ptr, hipStream_t st) {
+                           void* scratch, int64_t* row_ptr, int* max_degree, hipStream_t st) {
   NlScratch s = carve(scratch, n, cg);
   Grid g = to_grid(cg);
   hipError_t e = hipMemsetAsync(s.cell_cnt, 0, sizeof(int) * (size_t)(cg.ncell + 1), st);
@@ -300,8 +408,9 @@ hipError_t launch_nl_count(const float* pos, const int32_t* graph_id, int n, dou
   e = hipMemsetAsync(s.cell_cnt, 0, sizeof(int) * (size_t)(cg.ncell + 1), st);
   if (e != hipSuccess) return e;
   k_cell_place<<<blocks, 256, 0, st>>>(n, s.cell_of, s.cell_start, s.cell_cnt, s.members);
-  k_neighbors<false><<<blocks, 256, 0, st>>>(pos, graph_id, n, r2, g, s.cell_of, s.cell_start, s.members, s.counts,
-                                            nullptr, nullptr);
+  if ((e = hipMemsetAsync(max_degree, 0, sizeof(int), st)) != hipSuccess) return e;
+  k_neighbors_wave<false><<<n, 64, 0, st>>>(pos, graph_id, n, r2, g, s.cell_of, s.cell_start, s.members, s.counts,
+                                            max_degree, nullptr, nullptr);
   k_zero_last<<<1, 1, 0, st>>>(s.counts, n);
   tb = s.scan_bytes;
   e = hipcub::DeviceScan::ExclusiveSum(s.scan_tmp, tb, s.counts, row_ptr, n + 1, st);
@@ -318,9 +427,14 @@ size_t nl_sort_tmp_bytes(int n, int64_t E) {
 
 hipError_t launch_nl_fill(const float* pos, const int32_t* graph_id, int n, double r2, const CellGrid& cg,
                           void* scratch, const int64_t* row_ptr, int32_t* unsorted, int32_t* col_idx, int64_t E,
-                          void* sort_tmp, size_t sort_tmp_bytes, hipStream_t st) {
+                          int max_degree, void* sort_tmp, size_t sort_tmp_bytes, hipStream_t st) {
   NlScratch s = carve(scratch, n, cg);
   Grid g = to_grid(cg);
+  if (max_degree <= kNlRowMax) {  // rows sorted in LDS
+    k_neighbors_wave<true><<<n, 64, 0, st>>>(pos, graph_id, n, r2, g, s.cell_of, s.cell_start, s.members, nullptr,
+                                             nullptr, row_ptr, col_idx);
+    return hipGetLastError();
+  }
   k_neighbors<true><<<(n + 255) / 256, 256, 0, st>>>(pos, graph_id, n, r2, g, s.cell_of, s.cell_start, s.members,
                                                     nullptr, row_ptr, unsorted);
   hipError_t e = hipGetLastError();
