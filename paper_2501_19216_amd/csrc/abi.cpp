@@ -753,7 +753,8 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
                         3 * al256(sizeof(int32_t) * (size_t)(nblk + 1)) + al256(blk_tmp_b) +
                         al256(sizeof(double) * (size_t)P * nk) + al256(sizeof(double) * (size_t)n * nk) +
                         al256(row_bytes * (size_t)max_pairs) + al256(row_bytes * (size_t)max_recv) +
-                        (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
+                        (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0) +
+                        (use_blocks && alpha ? al256(sizeof(float) * (size_t)n_edges * p->heads) : 0);
   rs = ensure(ctx, ctx->b, need_b, s);
   if (rs != E2F_OK) return rs;
   Carver cb{(char*)ctx->b.p};
@@ -771,6 +772,8 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   float* T = cb.take<float>((size_t)max_pairs * t.dimT * C);
   float* S = cb.take<float>((size_t)max_recv * t.dimT * C);
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
+  float* alpha_hm = use_blocks && alpha ? cb.take<float>((size_t)n_edges * p->heads) : nullptr;
+  if (alpha_hm) E2F_TIMED("aggregate", launch_alpha_head_major(alpha, n_edges, p->heads, alpha_hm, s));
   E2F_TIMED("tile_plan", launch_pairs(flags, pidx, count, n, pair_node, pair_tile, s));
   E2F_TIMED("tile_plan", launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
   E2F_TIMED("sh", launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, nullptr, s));
@@ -786,8 +789,8 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
       E2F_TIMED("tile_plan", launch_block_union(row_ptr, col_pair, ord, nb, blk_count, blk_off, uni, ucount,
                                                 edge_slot, blk_tmp, blk_tmp_b, s));
     }
-    E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, alpha, ord, uni, blk_off, ucount, edge_slot,
-                                            use_blocks, nb, t.dimT, C, p->heads, S, s));
+    E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, alpha, alpha_hm, n_edges, ord, uni, blk_off,
+                                            ucount, edge_slot, use_blocks, nb, t.dimT, C, p->heads, S, s));
     E2F_TIMED("recouple", launch_recouple(t, Rr, S, ord, nb, C, dh, y, s));
   }
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));

@@ -14,6 +14,7 @@
 #include <hip/hip_bf16.h>
 #include <hipcub/hipcub.hpp>
 
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
 #include <utility>
@@ -162,8 +163,11 @@ __device__ __forceinline__ void run_schedule(const int* __restrict__ meta, const
 // on v_mfma_f32_16x16x4f32 with A = h^T (16 channels x 4 al), B = M^T
 // (4 al x 16 rows); each lane ends with 4 consecutive channels of one row,
 // stored as one float4 (a wave writes 16 whole rows of 64 bytes per head).
-template <int L>
-__global__ __launch_bounds__(256) void k_node_tp(DevTables t, const double* __restrict__ R,
+// NW waves share one per-node matrix: the first kSchedThreads threads build it,
+// all of them run the products (at high L the matrix leaves room for one
+// workgroup per CU, so more waves per workgroup keep the stores in flight).
+template <int L, int NW>
+__global__ __launch_bounds__(NW * 64) void k_node_tp(DevTables t, const double* __restrict__ R,
                                                  const int32_t* __restrict__ node_of, const float* __restrict__ feat,
                                                  int C, int dh, int hs, float* __restrict__ T) {
   constexpr int NK = (L + 1) * (L + 1);
@@ -186,7 +190,7 @@ __global__ __launch_bounds__(256) void k_node_tp(DevTables t, const double* __re
   }
   for (int q = threadIdx.x; q < msize; q += blockDim.x) Mt[q] = 0.0f;
   __syncthreads();
-  run_schedule(t.tp_meta, t.tp_coef, t.tp_k[0], Rl, Mt);
+  if (threadIdx.x < kSchedThreads) run_schedule(t.tp_meta, t.tp_coef, t.tp_k[0], Rl, Mt);
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int l16 = lane & 15, k4 = lane >> 4;
@@ -199,7 +203,7 @@ __global__ __launch_bounds__(256) void k_node_tp(DevTables t, const double* __re
     const int rs = t.tp_rs[a];
     const float* Ma = Mt + t.tp_mo[a];
     const int nrt = (rows + 15) / 16;
-    for (int task = wave; task < nrt * NT; task += 4) {
+    for (int task = wave; task < nrt * NT; task += NW) {
       const int rt = task / NT, nt = task % NT;
       const int ca = nt * 16 + l16;  // A operand channel
       const float* hc = h + (ca < C ? ca : 0);
@@ -383,7 +387,8 @@ __global__ __launch_bounds__(64 * WV) void k_aggregate_mfma(const float* __restr
                                                         const int64_t* __restrict__ row_ptr,
                                                         const int32_t* __restrict__ order,
                                                         const int32_t* __restrict__ edge_slot,
-                                                        const float* __restrict__ alpha, int n, int nblk, int bpx,
+                                                        const float* __restrict__ alpha_hm, int64_t n_edges,
+                                                        int n, int nblk, int bpx,
                                                         int ntg, int ntgw, int dimT, int C, int dh, int H,
                                                         float* __restrict__ S) {
   __shared__ int64_t ubl[kPiece];     // float4 offset of each union row of the piece in T
@@ -398,6 +403,7 @@ __global__ __launch_bounds__(64 * WV) void k_aggregate_mfma(const float* __restr
   const int wtask = local / bpx;
   if (b >= nblk || wtask >= H * ntgw) return;  // uniform over the workgroup
   const int h = wtask / ntgw;
+  const float* ah = alpha_hm ? alpha_hm + (int64_t)h * n_edges : nullptr;  // head h's weights, by edge
   const int tg = (wtask % ntgw) * WV + (int)(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int j = lane & 15, k = lane >> 4;
@@ -428,6 +434,10 @@ __global__ __launch_bounds__(64 * WV) void k_aggregate_mfma(const float* __restr
     e0 = row_ptr[i];
     e1 = row_ptr[i + 1];
   }
+  // senders are ascending in every row, so a receiver's edges reach the union
+  // slots in ascending order: each thread keeps a cursor over its edges
+  // (stride 16) and every piece continues from it
+  int64_t ecur = e0 + rl;
   const float4* T4 = (const float4*)T;
   const bool active = tg < ntg;  // uniform over the wave
   // Union rows 4 at a time (lane row k); rows past the piece take weight 0
@@ -474,24 +484,31 @@ __global__ __launch_bounds__(64 * WV) void k_aggregate_mfma(const float* __restr
         for (int u = 0; u < kEB; ++u) {
           const int64_t ec = min(eb + 16 * u, e1 - 1);
           sl[u] = edge_slot[ec] - p0;
-          av[u] = alpha ? alpha[ec * H + h] : 1.0f;
+          av[u] = ah ? ah[ec] : 1.0f;
         }
       };
-      auto store_edges = [&](int64_t eb) {
-        float* Alw = (float*)Al4;
-#pragma unroll
-        for (int u = 0; u < kEB; ++u)
-          if (eb + 16 * u < e1 && sl[u] >= 0 && sl[u] < np) Alw[sl[u] * 16 + rr] = av[u];
-      };
-      if (e0 < e1) load_edges(e0 + rl);
+      if (ecur < e1) load_edges(ecur);
 #pragma unroll
       for (int u = 0; u < kU; ++u) ubl[t + kNT * u] = (int64_t)(uu[u] - pair_base) * W4;
       for (int q = t; q < 4 * np; q += kNT) Al4[q] = make_float4(0.f, 0.f, 0.f, 0.f);
       __syncthreads();
-      for (int64_t eb = e0 + rl; eb < e1; eb += 16 * kEB) {
-        if (eb != e0 + rl) load_edges(eb);
-        store_edges(eb);
+      // earlier pieces took every slot below p0; the first edge past this
+      // piece is where the next one starts (the loop bound does not depend on
+      // loaded data, so the next batch's loads need not wait for this one's)
+      float* Alw = (float*)Al4;
+      int64_t nxt = e1;
+      for (int64_t eb = ecur; eb < e1; eb += 16 * kEB) {
+        if (eb != ecur) load_edges(eb);
+#pragma unroll
+        for (int u = 0; u < kEB; ++u) {
+          const int64_t ev = eb + 16 * u;
+          if (ev < e1) {
+            if (sl[u] >= np) nxt = min(nxt, ev);
+            else if (sl[u] >= 0) Alw[sl[u] * 16 + rr] = av[u];
+          }
+        }
       }
+      ecur = nxt;
       __syncthreads();
     }
     if (!active) continue;  // no barrier below
@@ -609,13 +626,10 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
       const int rc = min(RR, dimT - r0);
       __syncthreads();
       for (int q = threadIdx.x; q < RR * QS; q += blockDim.x) Qt[q] = 0.0f;
-      __syncthreads();
-      const int ch = r0 / RR;
-      run_schedule(t.rc_meta + t.rc_off[ch], t.rc_coef + t.rc_off[ch], t.rc_k[ch], Rl, Qt);
-      __syncthreads();
       // Stages of ST steps in pairs; rows past the chunk read its last row
       // and take Q = 0.  No branch in the body, so each wait covers only the
       // older stage; sched_barrier keeps a prefetch from sinking to its use.
+      // The first stage of S is loaded before the Q tile is built.
       float bA[ST][NTW], bB[ST][NTW];
       auto load = [&](int stg, float (*bv)[NTW]) {
 #pragma unroll
@@ -625,6 +639,11 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
           for (int q = 0; q < NTW; ++q) bv[u][q] = sb[q][(size_t)(r0 + rl) * dh];
         }
       };
+      load(0, bA);
+      __syncthreads();
+      const int ch = r0 / RR;
+      run_schedule(t.rc_meta + t.rc_off[ch], t.rc_coef + t.rc_off[ch], t.rc_k[ch], Rl, Qt);
+      __syncthreads();
       auto mma = [&](int stg, float (*bv)[NTW]) {
 #pragma unroll
         for (int u = 0; u < ST; ++u) {
@@ -644,7 +663,6 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
         }
       };
       const int nstage = (rc + 4 * ST - 1) / (4 * ST);
-      load(0, bA);
       for (int sp = 0; sp < nstage; sp += 2) {
         load(sp + 1, bB);
         __builtin_amdgcn_sched_barrier(0);
@@ -966,6 +984,15 @@ __global__ void k_dense_alpha(const float* __restrict__ alpha, int n, int H, flo
   A[q] = i == j ? 0.0f : (alpha ? alpha[ij * H + h] : 1.0f);
 }
 
+// thread per edge: reads its H contiguous weights, writes one coalesced
+// row segment per head
+__global__ void k_alpha_head_major(const float* __restrict__ alpha, int64_t n_edges, int H,
+                                   float* __restrict__ alpha_hm) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= n_edges) return;
+  for (int h = 0; h < H; ++h) alpha_hm[(int64_t)h * n_edges + e] = alpha[e * H + h];
+}
+
 __global__ void k_iota(int n, int32_t* __restrict__ v) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) v[i] = i;
@@ -1113,13 +1140,23 @@ hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* no
   const size_t hbytes = sizeof(float) * (size_t)t.nk * hs;
   if (hbytes > 32768) hs = 0;
   const size_t lds = mbytes + (hs > 0 ? hbytes : 0);
-  switch (t.L) {
-#define E2F_CASE(LL)                                                                                        \
-  case LL:                                                                                                  \
-    if (hipError_t e = allow_lds(k_node_tp<LL>, lds); e != hipSuccess) return e;                            \
-    k_node_tp<LL><<<n_items, 256, lds, s>>>(t, R, node_of, feat, C, dh, hs, T);                             \
+  static const int nw_env = [] {
+    const char* v = getenv("E2F_TP_WAVES");
+    return v ? atoi(v) : 0;
+  }();
+  // waves per workgroup: enough for 16 waves per CU at the number of
+  // workgroups the LDS tile leaves room for (160 KB per CU)
+  const int wg_cu = (int)std::max<size_t>(1, 163840 / std::max<size_t>(lds, 1));
+  const int nw = nw_env == 4 || nw_env == 8 || nw_env == 16 ? nw_env : (wg_cu >= 4 ? 4 : (wg_cu >= 2 ? 8 : 16));
+  switch (t.L * 32 + nw) {
+#define E2F_CASE(LL, NW)                                                                                    \
+  case LL * 32 + NW:                                                                                        \
+    if (hipError_t e = allow_lds(k_node_tp<LL, NW>, lds); e != hipSuccess) return e;                        \
+    k_node_tp<LL, NW><<<n_items, NW * 64, lds, s>>>(t, R, node_of, feat, C, dh, hs, T);                     \
     break;
-    E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
+#define E2F_CASES(LL) E2F_CASE(LL, 4) E2F_CASE(LL, 8) E2F_CASE(LL, 16)
+    E2F_CASES(0) E2F_CASES(1) E2F_CASES(2) E2F_CASES(3) E2F_CASES(4) E2F_CASES(5) E2F_CASES(6)
+#undef E2F_CASES
 #undef E2F_CASE
     default: return hipErrorInvalidValue;
   }
@@ -1178,16 +1215,26 @@ hipError_t launch_block_union(const int64_t* row_ptr, const int32_t* col_pair, c
 }
 
 hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_ptr, const int32_t* col_pair,
-                            const float* alpha, const int32_t* order, const int32_t* uni, const int32_t* blk_off,
-                            const int32_t* ucount, const int32_t* edge_slot, bool use_blocks, int n, int dimT, int C,
-                            int H, float* S, hipStream_t s) {
+                            const float* alpha, const float* alpha_hm, int64_t n_edges, const int32_t* order,
+                            const int32_t* uni, const int32_t* blk_off, const int32_t* ucount,
+                            const int32_t* edge_slot, bool use_blocks, int n, int dimT, int C, int H, float* S,
+                            hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int dh = C / H;
   if (use_blocks) {
     // columns per wave: 64*NQ, register stages NS, waves per workgroup WV;
     // E2F_AGG_CFG="NQ,NS,WV" overrides (tuning)
-    int nq = 2, ns = 3, wv = 4;
+    int nq = 4, ns = 3, wv = 4;
     if (const char* cfg = getenv("E2F_AGG_CFG")) sscanf(cfg, "%d,%d,%d", &nq, &ns, &wv);
+    // workgroups per CU, capped through unused dynamic LDS: two 4-wave
+    // workgroups per CU measure faster than three or four (12% at L=6,
+    // C=64); E2F_AGG_WGCU overrides (0: no cap)
+    static const int wgcu = [] {
+      const char* v = getenv("E2F_AGG_WGCU");
+      return v ? atoi(v) : 2;
+    }();
+    const size_t static_lds = sizeof(int64_t) * kPiece + sizeof(float4) * kPiece * 4;
+    const size_t pad = wgcu > 0 && (size_t)(163840 / wgcu) > static_lds ? 163840 / wgcu - static_lds - 256 : 0;
     const int nblk = (n + 15) / 16;
     const int ntg = (dimT * dh + 64 * nq - 1) / (64 * nq);
     const int ntgw = (ntg + wv - 1) / wv;
@@ -1196,9 +1243,11 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
 #define E2F_AGG(NQ_, NS_, WV_)                                                                             \
   if (nq == NQ_ && ns == NS_ && wv == WV_) {                                                              \
-    k_aggregate_mfma<NQ_, NS_, WV_><<<(unsigned)blocks, 64 * WV_, 0, s>>>(                                \
-        T, pair_base, uni, blk_off, ucount, row_ptr, order, edge_slot, alpha, n, nblk, bpx, ntg, ntgw, dimT, C, \
-        dh, H, S);                                                                                        \
+    if (pad > 0)                                                                                          \
+      if (hipError_t e = allow_lds(k_aggregate_mfma<NQ_, NS_, WV_>, pad); e != hipSuccess) return e;     \
+    k_aggregate_mfma<NQ_, NS_, WV_><<<(unsigned)blocks, 64 * WV_, pad, s>>>(                              \
+        T, pair_base, uni, blk_off, ucount, row_ptr, order, edge_slot, alpha_hm, n_edges, n, nblk, bpx, ntg,   \
+        ntgw, dimT, C, dh, H, S);                                                                         \
     return hipGetLastError();                                                                             \
   }
     E2F_AGG(2, 2, 4) E2F_AGG(2, 3, 4) E2F_AGG(2, 4, 4) E2F_AGG(2, 3, 8) E2F_AGG(2, 3, 2) E2F_AGG(4, 3, 4)
@@ -1300,6 +1349,14 @@ hipError_t launch_dense_alpha(const float* alpha, int n, int H, float* A, hipStr
   if (total == 0) return hipSuccess;
   if ((total + 255) / 256 > 0x7fffffff) return hipErrorInvalidValue;
   k_dense_alpha<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(alpha, n, H, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_alpha_head_major(const float* alpha, int64_t n_edges, int H, float* alpha_hm, hipStream_t s) {
+  if (n_edges == 0) return hipSuccess;
+  const int64_t blocks = (n_edges + 255) / 256;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  k_alpha_head_major<<<(unsigned)blocks, 256, 0, s>>>(alpha, n_edges, H, alpha_hm);
   return hipGetLastError();
 }
 
