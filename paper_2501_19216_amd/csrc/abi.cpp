@@ -789,8 +789,8 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
       E2F_TIMED("tile_plan", launch_block_union(row_ptr, col_pair, ord, nb, blk_count, blk_off, uni, ucount,
                                                 edge_slot, blk_tmp, blk_tmp_b, s));
     }
-    E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, alpha, alpha_hm, n_edges, ord, uni, blk_off,
-                                            ucount, edge_slot, use_blocks, nb, t.dimT, C, p->heads, S, s));
+    E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, alpha, alpha_hm, n_edges, n, ord, uni,
+                                            blk_off, ucount, edge_slot, use_blocks, nb, t.dimT, C, p->heads, S, s));
     E2F_TIMED("recouple", launch_recouple(t, Rr, S, ord, nb, C, dh, y, s));
   }
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));

@@ -388,7 +388,7 @@ __global__ __launch_bounds__(64 * WV) void k_aggregate_mfma(const float* __restr
                                                         const int32_t* __restrict__ order,
                                                         const int32_t* __restrict__ edge_slot,
                                                         const float* __restrict__ alpha_hm, int64_t n_edges,
-                                                        int n, int nblk, int bpx,
+                                                        int n, int nblk, int bpx, int by_task,
                                                         int ntg, int ntgw, int dimT, int C, int dh, int H,
                                                         float* __restrict__ S) {
   __shared__ int64_t ubl[kPiece];     // float4 offset of each union row of the piece in T
@@ -399,8 +399,8 @@ __global__ __launch_bounds__(64 * WV) void k_aggregate_mfma(const float* __restr
   // flight on an XCD share T rows through its L2
   const int bid = blockIdx.x;
   const int xcd = bid % kXcds, local = bid / kXcds;
-  const int b = xcd * bpx + local % bpx;
-  const int wtask = local / bpx;
+  const int b = by_task ? local % nblk : xcd * bpx + local % bpx;
+  const int wtask = by_task ? (local / nblk) * kXcds + xcd : local / bpx;
   if (b >= nblk || wtask >= H * ntgw) return;  // uniform over the workgroup
   const int h = wtask / ntgw;
   const float* ah = alpha_hm ? alpha_hm + (int64_t)h * n_edges : nullptr;  // head h's weights, by edge
@@ -1215,23 +1215,33 @@ hipError_t launch_block_union(const int64_t* row_ptr, const int32_t* col_pair, c
 }
 
 hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_ptr, const int32_t* col_pair,
-                            const float* alpha, const float* alpha_hm, int64_t n_edges, const int32_t* order,
-                            const int32_t* uni, const int32_t* blk_off, const int32_t* ucount,
-                            const int32_t* edge_slot, bool use_blocks, int n, int dimT, int C, int H, float* S,
-                            hipStream_t s) {
+                            const float* alpha, const float* alpha_hm, int64_t n_edges, int n_total,
+                            const int32_t* order, const int32_t* uni, const int32_t* blk_off,
+                            const int32_t* ucount, const int32_t* edge_slot, bool use_blocks, int n, int dimT, int C,
+                            int H, float* S, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int dh = C / H;
   if (use_blocks) {
-    // columns per wave: 64*NQ, register stages NS, waves per workgroup WV;
-    // E2F_AGG_CFG="NQ,NS,WV" overrides (tuning)
-    int nq = 4, ns = 3, wv = 4;
+    // columns per wave: 64*NQ, register stages NS, waves per workgroup WV,
+    // and a cap on workgroups per CU (through unused dynamic LDS; 0: none).
+    // Measured: at a mean degree of ~80 (20k atoms, L=4) NQ=2 with four
+    // workgroups per CU is fastest; at ~200 (200k atoms, L=6) NQ=4 with two
+    // (the A-operand build of a workgroup grows with its block's edges).
+    // E2F_AGG_CFG="NQ,NS,WV" and E2F_AGG_WGCU override (tuning).
+    const bool dense_rows = n_edges >= (int64_t)128 * n_total;
+    int nq = dense_rows ? 4 : 2, ns = 3, wv = 4;
     if (const char* cfg = getenv("E2F_AGG_CFG")) sscanf(cfg, "%d,%d,%d", &nq, &ns, &wv);
-    // workgroups per CU, capped through unused dynamic LDS: two 4-wave
-    // workgroups per CU measure faster than three or four (12% at L=6,
-    // C=64); E2F_AGG_WGCU overrides (0: no cap)
-    static const int wgcu = [] {
+    static const int wgcu_env = [] {
       const char* v = getenv("E2F_AGG_WGCU");
-      return v ? atoi(v) : 2;
+      return v ? atoi(v) : -1;
+    }();
+    const int wgcu = wgcu_env >= 0 ? wgcu_env : (dense_rows ? 2 : 0);
+    // XCD x takes the column tasks x, x+8, ... over every block, so each T
+    // element is read by one XCD's L2 (blocks in space order within a task);
+    // E2F_AGG_MAP=0 gives each XCD a contiguous range of blocks instead
+    static const int by_task = [] {
+      const char* v = getenv("E2F_AGG_MAP");
+      return v ? atoi(v) : 1;
     }();
     const size_t static_lds = sizeof(int64_t) * kPiece + sizeof(float4) * kPiece * 4;
     const size_t pad = wgcu > 0 && (size_t)(163840 / wgcu) > static_lds ? 163840 / wgcu - static_lds - 256 : 0;
@@ -1239,14 +1249,16 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
     const int ntg = (dimT * dh + 64 * nq - 1) / (64 * nq);
     const int ntgw = (ntg + wv - 1) / wv;
     const int bpx = (nblk + kXcds - 1) / kXcds;
-    const int64_t blocks = (int64_t)kXcds * bpx * H * ntgw;
+    const int64_t blocks = by_task ? (int64_t)kXcds * ((H * ntgw + kXcds - 1) / kXcds) * nblk
+                                   : (int64_t)kXcds * bpx * H * ntgw;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
 #define E2F_AGG(NQ_, NS_, WV_)                                                                             \
   if (nq == NQ_ && ns == NS_ && wv == WV_) {                                                              \
     if (pad > 0)                                                                                          \
       if (hipError_t e = allow_lds(k_aggregate_mfma<NQ_, NS_, WV_>, pad); e != hipSuccess) return e;     \
     k_aggregate_mfma<NQ_, NS_, WV_><<<(unsigned)blocks, 64 * WV_, pad, s>>>(                              \
-        T, pair_base, uni, blk_off, ucount, row_ptr, order, edge_slot, alpha_hm, n_edges, n, nblk, bpx, ntg,   \
+        T, pair_base, uni, blk_off, ucount, row_ptr, order, edge_slot, alpha_hm, n_edges, n, nblk, bpx,        \
+        by_task, ntg,                                                                                     \
         ntgw, dimT, C, dh, H, S);                                                                         \
     return hipGetLastError();                                                                             \
   }

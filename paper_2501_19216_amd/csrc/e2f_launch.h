@@ -89,12 +89,13 @@ hipError_t launch_block_union(const int64_t* row_ptr, const int32_t* col_pair, c
 // pairs from pair_base on.  use_blocks: MFMA form over the block plan (built
 // for the same n receivers; the attention operand is assembled from the
 // head-major weights alpha_hm [H][n_edges] and edge_slot); else per-receiver
-// rows from L2 with alpha [n_edges][H].  Null weights mean all ones.
+// rows from L2 with alpha [n_edges][H].  Null weights mean all ones.  n_edges
+// and n_total are the whole graph's edges and atoms (mean degree).
 hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_ptr, const int32_t* col_pair,
-                            const float* alpha, const float* alpha_hm, int64_t n_edges, const int32_t* order,
-                            const int32_t* uni, const int32_t* blk_off, const int32_t* ucount,
-                            const int32_t* edge_slot, bool use_blocks, int n, int dimT, int C, int H, float* S,
-                            hipStream_t s);
+                            const float* alpha, const float* alpha_hm, int64_t n_edges, int n_total,
+                            const int32_t* order, const int32_t* uni, const int32_t* blk_off,
+                            const int32_t* ucount, const int32_t* edge_slot, bool use_blocks, int n, int dimT, int C,
+                            int H, float* S, hipStream_t s);
 // alpha_hm[h][e] = alpha[e][h]
 hipError_t launch_alpha_head_major(const float* alpha, int64_t n_edges, int H, float* alpha_hm, hipStream_t s);
 // y[order[r]] from S row r (head-major like T), r < n
