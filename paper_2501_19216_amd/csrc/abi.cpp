@@ -773,7 +773,7 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   float* S = cb.take<float>((size_t)max_recv * t.dimT * C);
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
   float* alpha_hm = use_blocks && alpha ? cb.take<float>((size_t)n_edges * p->heads) : nullptr;
-  if (alpha_hm) E2F_TIMED("aggregate", launch_alpha_head_major(alpha, n_edges, p->heads, alpha_hm, s));
+  if (alpha_hm) E2F_TIMED("alpha_hm", launch_alpha_head_major(alpha, n_edges, p->heads, alpha_hm, s));
   E2F_TIMED("tile_plan", launch_pairs(flags, pidx, count, n, pair_node, pair_tile, s));
   E2F_TIMED("tile_plan", launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
   E2F_TIMED("sh", launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, nullptr, s));
