@@ -66,6 +66,8 @@ def lib():
             L.e2fo_conv_edge.argtypes = [i, i, i, p, p, i, p, p, p, p, p, i, p]
             L.e2fo_conv_factorised.restype = i
             L.e2fo_conv_factorised.argtypes = [i, i, i, p, p, i, p, p, p, p, p, p]
+            L.e2fo_conv_global.restype = i
+            L.e2fo_conv_global.argtypes = [i, i, p, p, i, p, p, p]
             L.e2fo_mix.restype = None
             L.e2fo_mix.argtypes = [i, i, i, p, p, p]
             _lib = L
@@ -224,6 +226,21 @@ def conv_factorised(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, ori
                                     _ptr(_c(path_w, np.float64)), _ptr(org), _ptr(out))
     if rc:
         raise ValueError("e2fo_conv_factorised failed (%d)" % rc)
+    return out
+
+
+def conv_global(lmax, pos, feat, path_w, origin) -> np.ndarray:
+    """Uniform attention over the whole graph (alpha = 1 for every pair, self
+    included) in the global-moment form of App. G; y [N, (L+1)^2, C] float64."""
+    pos = _c(pos, np.float32)
+    feat = _c(feat, np.float32)
+    n, nk, C = feat.shape
+    out = np.zeros((n, nk, C))
+    org = np.ascontiguousarray(origin, dtype=np.float64)
+    rc = lib().e2fo_conv_global(lmax, C, _ptr(pos), _ptr(feat), n, _ptr(_c(path_w, np.float64)), _ptr(org),
+                                _ptr(out))
+    if rc:
+        raise ValueError("e2fo_conv_global failed (%d)" % rc)
     return out
 
 

@@ -626,6 +626,60 @@ static double binom_(int n, int k) {
     return r;
 }
 
+/* i-side recoupling of one node (blue box of Thm. 3.3; Wigner6jTP of Alg. 1):
+ * y^(o) = sum_{a,f} w_afo sum_{u<=f} (-1)^(f-u) binom(f,u) sum_d X(a,f-u,u,o;d)
+ *         [R^(u)(p_i) (x) S^(a,f-u,d)]^(o),
+ * with S indexed [a][b][d][delta][c] (d < 2L+1, delta < 4L+1) and Ru = R(p_i). */
+static void iside(int L, int C, const double *Ru0, const double *S, const double *path_w, double *y) {
+    int nk = (L + 1) * (L + 1), L1 = L + 1, DM = 4 * L + 1;
+    memset(y, 0, sizeof(double) * (size_t)nk * C);
+    for (int a = 0; a <= L; ++a)
+        for (int f = 0; f <= L; ++f)
+            for (int o = iabs_(a - f); o <= imin_(a + f, L); ++o) {
+                double w = path_w[(a * L1 + f) * L1 + o];
+                if (w == 0.0) continue;
+                for (int u = 0; u <= f; ++u) {
+                    int b = f - u;
+                    double coef = w * sgn_pow(f - u) * binom_(f, u);
+                    for (int d = iabs_(a - b); d <= a + b; ++d) {
+                        double x = e2fo_recoupling_x(a, b, u, o, d);
+                        if (x == 0.0) continue;
+                        const double *c3 = cg(u, d, o);
+                        const double *Ru = Ru0 + u * u;
+                        for (int ga = 0; ga < 2 * u + 1; ++ga)
+                            for (int de = 0; de < 2 * d + 1; ++de)
+                                for (int m = 0; m < 2 * o + 1; ++m) {
+                                    double k = coef * x * c3[(ga * (2 * d + 1) + de) * (2 * o + 1) + m] * Ru[ga];
+                                    if (k == 0.0) continue;
+                                    double *yrow = y + (size_t)(o * o + m) * C;
+                                    const double *srow = S + ((((size_t)a * L1 + b) * (2 * L + 1) + d) * DM + de) * C;
+                                    for (int c = 0; c < C; ++c) yrow[c] += k * srow[c];
+                                }
+                    }
+                }
+            }
+}
+
+/* j-side product of one node (red box of Thm. 3.3): T^(a,b,d) = [h^(a) (x) R^(b)(p)]^(d)
+ * added with weight s into T indexed like S above. */
+static void jside_add(int L, int C, const double *Rb0, const float *h, double s, double *T) {
+    int L1 = L + 1, DM = 4 * L + 1;
+    for (int a = 0; a <= L; ++a)
+        for (int b = 0; b <= L; ++b)
+            for (int d = iabs_(a - b); d <= a + b; ++d) {
+                const double *c3 = cg(a, b, d);
+                const double *Rb = Rb0 + b * b;
+                double *Tb = T + (((size_t)a * L1 + b) * (2 * L + 1) + d) * DM * C;
+                for (int al = 0; al < 2 * a + 1; ++al)
+                    for (int be = 0; be < 2 * b + 1; ++be)
+                        for (int de = 0; de < 2 * d + 1; ++de) {
+                            double k = s * c3[(al * (2 * b + 1) + be) * (2 * d + 1) + de] * Rb[be];
+                            if (k == 0.0) continue;
+                            for (int c = 0; c < C; ++c) Tb[(size_t)de * C + c] += k * (double)h[(size_t)(a * a + al) * C + c];
+                        }
+            }
+}
+
 int e2fo_conv_factorised(int L, int C, int H, const float *pos, const float *feat, int n, const int64_t *row_ptr,
                          const int32_t *col_idx, const float *alpha, const double *path_w, const double *origin,
                          double *out) {
@@ -638,27 +692,12 @@ int e2fo_conv_factorised(int L, int C, int H, const float *pos, const float *fea
     double *S = (double *)calloc((size_t)n * per_node, sizeof(double));
     double *Rp = (double *)malloc(sizeof(double) * (size_t)n * nk);
     if (!T || !S || !Rp) { free(T); free(S); free(Rp); return 2; }
-#define TIDX(node, a, b, d, de, c) ((((((size_t)(node) * L1 + (a)) * L1 + (b)) * (2 * L + 1) + (d)) * DM + (de)) * C + (c))
     for (int i = 0; i < n; ++i) {
         double p[3] = {(double)pos[3 * i] - origin[0], (double)pos[3 * i + 1] - origin[1], (double)pos[3 * i + 2] - origin[2]};
         e2fo_solid_harmonics(L, p, Rp + (size_t)i * nk);
     }
     /* j-side tensor products (red box of Thm. 3.3; T_k of Alg. 1) */
-    for (int j = 0; j < n; ++j)
-        for (int a = 0; a <= L; ++a)
-            for (int b = 0; b <= L; ++b)
-                for (int d = iabs_(a - b); d <= a + b; ++d) {
-                    const double *c3 = cg(a, b, d);
-                    const double *Rb = Rp + (size_t)j * nk + b * b;
-                    for (int al = 0; al < 2 * a + 1; ++al)
-                        for (int be = 0; be < 2 * b + 1; ++be)
-                            for (int de = 0; de < 2 * d + 1; ++de) {
-                                double k = c3[(al * (2 * b + 1) + be) * (2 * d + 1) + de] * Rb[be];
-                                if (k == 0.0) continue;
-                                for (int c = 0; c < C; ++c)
-                                    T[TIDX(j, a, b, d, de, c)] += k * (double)feat[((size_t)j * nk + a * a + al) * C + c];
-                            }
-                }
+    for (int j = 0; j < n; ++j) jside_add(L, C, Rp + (size_t)j * nk, feat + (size_t)j * nk * C, 1.0, T + (size_t)j * per_node);
     /* attention-weighted aggregation (einsum "ijh,jhds->ihds" of Alg. 1) */
     for (int i = 0; i < n; ++i)
         for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
@@ -669,34 +708,34 @@ int e2fo_conv_factorised(int L, int C, int H, const float *pos, const float *fea
             }
         }
     /* i-side recoupling (blue box of Thm. 3.3; Wigner6jTP of Alg. 1) */
-    memset(out, 0, sizeof(double) * (size_t)n * nk * C);
     for (int i = 0; i < n; ++i)
-        for (int a = 0; a <= L; ++a)
-            for (int f = 0; f <= L; ++f)
-                for (int o = iabs_(a - f); o <= imin_(a + f, L); ++o) {
-                    double w = path_w[(a * L1 + f) * L1 + o];
-                    if (w == 0.0) continue;
-                    for (int u = 0; u <= f; ++u) {
-                        int b = f - u;
-                        double coef = w * sgn_pow(f - u) * binom_(f, u);
-                        for (int d = iabs_(a - b); d <= a + b; ++d) {
-                            double x = e2fo_recoupling_x(a, b, u, o, d);
-                            if (x == 0.0) continue;
-                            const double *c3 = cg(u, d, o);
-                            const double *Ru = Rp + (size_t)i * nk + u * u;
-                            for (int ga = 0; ga < 2 * u + 1; ++ga)
-                                for (int de = 0; de < 2 * d + 1; ++de)
-                                    for (int m = 0; m < 2 * o + 1; ++m) {
-                                        double k = coef * x * c3[(ga * (2 * d + 1) + de) * (2 * o + 1) + m] * Ru[ga];
-                                        if (k == 0.0) continue;
-                                        double *yrow = out + ((size_t)i * nk + o * o + m) * C;
-                                        for (int c = 0; c < C; ++c) yrow[c] += k * S[TIDX(i, a, b, d, de, c)];
-                                    }
-                        }
-                    }
-                }
-#undef TIDX
+        iside(L, C, Rp + (size_t)i * nk, S + (size_t)i * per_node, path_w, out + (size_t)i * nk * C);
     free(T); free(S); free(Rp);
+    return 0;
+}
+
+/* ---------- uniform attention over the whole graph (App. G) ----------
+ * alpha_ij = 1 for every pair i, j of the n atoms, j = i included.  With
+ * p = r - origin, the moments M^(a,b,d) = sum_j [h_j^(a) (x) R^(b)(p_j)]^(d)
+ * are summed once (O(n)) and every node contracts them with its own R^(u)(p_i)
+ * exactly as in the factorised layer: y_i = iside(R(p_i), M).
+ * out: [n][(L+1)^2][C]. */
+int e2fo_conv_global(int L, int C, const float *pos, const float *feat, int n, const double *path_w,
+                     const double *origin, double *out) {
+    if (L < 0 || L > 6 || C < 1) return 1;
+    int nk = (L + 1) * (L + 1), L1 = L + 1, DM = 4 * L + 1;
+    warm_cg(2 * L, 2 * L);
+    size_t per_node = (size_t)L1 * L1 * (2 * L + 1) * DM * C;
+    double *M = (double *)calloc(per_node, sizeof(double));
+    double *Rp = (double *)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1) * nk);
+    if (!M || !Rp) { free(M); free(Rp); return 2; }
+    for (int i = 0; i < n; ++i) {
+        double p[3] = {(double)pos[3 * i] - origin[0], (double)pos[3 * i + 1] - origin[1], (double)pos[3 * i + 2] - origin[2]};
+        e2fo_solid_harmonics(L, p, Rp + (size_t)i * nk);
+    }
+    for (int j = 0; j < n; ++j) jside_add(L, C, Rp + (size_t)j * nk, feat + (size_t)j * nk * C, 1.0, M);
+    for (int i = 0; i < n; ++i) iside(L, C, Rp + (size_t)i * nk, M, path_w, out + (size_t)i * nk * C);
+    free(M); free(Rp);
     return 0;
 }
 

@@ -496,6 +496,26 @@ def test_factorised_equals_definition(L):
         assert np.max(np.abs(y1 - y2)) <= tol * np.max(np.abs(y1))
 
 
+@pytest.mark.parametrize("L", [0, 2, 3, 4])
+def test_global_moment_equals_definition(L):
+    # App. G: with alpha = 1 on every pair (self included) the moments
+    # M = sum_j h_j (x) R(p_j) are shared by all nodes; the O(n) form equals
+    # the layer's definition on the complete graph with self edges
+    n, C = (7, 3) if L < 4 else (5, 2)
+    pos, _, _, feat, _, w = small_graph(L, n, C, 1, seed=40 + L)
+    rp = np.arange(n + 1, dtype=np.int64) * n
+    ci = np.tile(np.arange(n, dtype=np.int32), n)
+    y1 = o.conv_edge(L, 1, pos, feat, rp, ci, np.ones((n * n, 1), np.float32), w)
+    for origin in ([0, 0, 0], [-2.5, 1.0, 6.0]):
+        y2 = o.conv_global(L, pos, feat, w, np.array(origin, dtype=np.float64))
+        maxp = np.max(np.linalg.norm(pos.astype(np.float64) - np.array(origin), axis=1))
+        tol = 1e-13 * max(1.0, maxp / 3.0) ** L
+        assert np.max(np.abs(y1 - y2)) <= tol * np.max(np.abs(y1))
+    if L == 0:
+        # closed form: every node receives w_000 * sum_j h_j
+        assert np.allclose(y2[:, 0, :], w[0] * feat[:, 0, :].astype(np.float64).sum(0)[None, :], rtol=1e-13)
+
+
 def test_layer_equivariance_and_translation():
     # Lemma (equivariance, App. E): rotating positions and features rotates
     # every output irrep by D^(o); a translation changes nothing.
