@@ -320,6 +320,12 @@ def main():
     att_only = lambda: e2f.e2f_attention_weights(ctx, pos, row_ptr, col, wl.cutoff, q_att, k_att, w_att, out=a_out)
     att_only()
     ms_att = timed(att_only, args.steps)
+    # uniform attention over all N^2 pairs (App. G): the global-moment form
+    glob_out = torch.empty_like(feat)
+    glob_only = lambda: e2f.e2f_wigner6j_conv_forward_global(ctx, pos, feat, L, H, wl.cutoff, mix_w=mix_w,
+                                                             out=glob_out)
+    glob_only()
+    ms_glob = timed(glob_only, args.steps)
     # the backward of the timed forward (fp32 mixing): both products, then each alone
     g_out = torch.randn(out.shape, device=dev, generator=g)
 
@@ -448,6 +454,7 @@ def main():
         "fwd_bf16_mix": bf16_res,
         "neighbor_list_ms": ms_nl,
         "backward": {"ms": ms_bwd, "grad_feat_ms": ms_bwd_feat, "grad_alpha_ms": ms_bwd_alpha},
+        "global_moment": {"ms": ms_glob, "pairs": n * n, "atoms_per_s": n / (ms_glob * 1e-3)},
         "attention": {"ms": ms_att, "dk": 16, "n_rbf": 8, "bytes_GBps": (E * (4 + 4 * H) + 12.0 * n) / (ms_att * 1e-3) / 1e9},
         "kernels": kernels,
         "roofline": roof,

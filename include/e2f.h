@@ -172,6 +172,19 @@ e2f_status e2f_wigner6j_conv_forward_dense(e2f_ctx* ctx, const e2f_conv_params* 
                                            const float* feat, int32_t n, const float* alpha, float* out,
                                            void* stream);
 
+/* Uniform attention over the whole graph (the global-moment special case of
+ * App. G): alpha = 1 for every pair i, j of the N atoms, j = i included, so
+ * the aggregation collapses to the moments M = sum_j [h_j (x) R^(b)(r_j - o)]^(d)
+ * of all atoms, summed once, and every atom contracts M with its own
+ * R^(u)(r_i - o) (Thm. 3.3): O(N).  o is the centre of the bounding box; the
+ * self term of j = i is R^(f)(0) = [f == 0].  heads only sets the layout of
+ * the intermediates (every head sees the same weights); tile_side is unused.
+ * out: [N][(L+1)^2][C].  M is summed in float64 in a fixed order
+ * (deterministic).  Workspace: about N (L+1)^2 doubles plus the T rows of one
+ * batch of atoms (at most 8 GiB).  (sync: one small device->host read) */
+e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
+                                            const float* feat, int32_t n, float* out, void* stream);
+
 /* Backward of e2f_wigner6j_conv_forward (same parameters and graph): the
  * vector-Jacobian products for the output gradient grad_out [N][(L+1)^2][C].
  * The layer is linear in the features and in the attention weights:

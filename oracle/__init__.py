@@ -67,7 +67,7 @@ def lib():
             L.e2fo_conv_factorised.restype = i
             L.e2fo_conv_factorised.argtypes = [i, i, i, p, p, i, p, p, p, p, p, p]
             L.e2fo_conv_global.restype = i
-            L.e2fo_conv_global.argtypes = [i, i, p, p, i, p, p, p]
+            L.e2fo_conv_global.argtypes = [i, i, p, p, i, p, p, p, i, p]
             L.e2fo_mix.restype = None
             L.e2fo_mix.argtypes = [i, i, i, p, p, p]
             _lib = L
@@ -229,16 +229,18 @@ def conv_factorised(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, ori
     return out
 
 
-def conv_global(lmax, pos, feat, path_w, origin) -> np.ndarray:
+def conv_global(lmax, pos, feat, path_w, origin, rows=None) -> np.ndarray:
     """Uniform attention over the whole graph (alpha = 1 for every pair, self
-    included) in the global-moment form of App. G; y [N, (L+1)^2, C] float64."""
+    included) in the global-moment form of App. G; y [N or len(rows), (L+1)^2, C]
+    float64."""
     pos = _c(pos, np.float32)
     feat = _c(feat, np.float32)
     n, nk, C = feat.shape
-    out = np.zeros((n, nk, C))
+    r = None if rows is None else _c(rows, np.int32)
+    out = np.zeros((n if r is None else len(r), nk, C))
     org = np.ascontiguousarray(origin, dtype=np.float64)
     rc = lib().e2fo_conv_global(lmax, C, _ptr(pos), _ptr(feat), n, _ptr(_c(path_w, np.float64)), _ptr(org),
-                                _ptr(out))
+                                None if r is None else _ptr(r), 0 if r is None else len(r), _ptr(out))
     if rc:
         raise ValueError("e2fo_conv_global failed (%d)" % rc)
     return out

@@ -719,9 +719,9 @@ int e2fo_conv_factorised(int L, int C, int H, const float *pos, const float *fea
  * p = r - origin, the moments M^(a,b,d) = sum_j [h_j^(a) (x) R^(b)(p_j)]^(d)
  * are summed once (O(n)) and every node contracts them with its own R^(u)(p_i)
  * exactly as in the factorised layer: y_i = iside(R(p_i), M).
- * out: [n][(L+1)^2][C]. */
+ * out: [n_rows][(L+1)^2][C] for the nodes rows[] (all n if rows is NULL). */
 int e2fo_conv_global(int L, int C, const float *pos, const float *feat, int n, const double *path_w,
-                     const double *origin, double *out) {
+                     const double *origin, const int32_t *rows, int n_rows, double *out) {
     if (L < 0 || L > 6 || C < 1) return 1;
     int nk = (L + 1) * (L + 1), L1 = L + 1, DM = 4 * L + 1;
     warm_cg(2 * L, 2 * L);
@@ -734,7 +734,13 @@ int e2fo_conv_global(int L, int C, const float *pos, const float *feat, int n, c
         e2fo_solid_harmonics(L, p, Rp + (size_t)i * nk);
     }
     for (int j = 0; j < n; ++j) jside_add(L, C, Rp + (size_t)j * nk, feat + (size_t)j * nk * C, 1.0, M);
-    for (int i = 0; i < n; ++i) iside(L, C, Rp + (size_t)i * nk, M, path_w, out + (size_t)i * nk * C);
+    /* out row r belongs to node rows[r] (every node in order if rows is NULL) */
+    int nr = rows ? n_rows : n;
+    for (int r = 0; r < nr; ++r) {
+        int i = rows ? rows[r] : r;
+        if (i < 0 || i >= n) { free(M); free(Rp); return 1; }
+        iside(L, C, Rp + (size_t)i * nk, M, path_w, out + (size_t)r * nk * C);
+    }
     free(M); free(Rp);
     return 0;
 }

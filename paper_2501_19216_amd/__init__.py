@@ -24,7 +24,8 @@ _STATUS = {0: "E2F_OK", 1: "E2F_EINVAL", 2: "E2F_ECAPACITY", 3: "E2F_ENOMEM", 4:
 # every function declared in include/e2f.h
 EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg", "e2f_knn_graph", "e2f_attention_weights",
             "e2f_recoupling_weight", "e2f_neighbor_list", "e2f_solid_harmonics", "e2f_node_tp",
-            "e2f_wigner6j_conv_forward", "e2f_wigner6j_conv_forward_dense", "e2f_wigner6j_conv_backward", "e2f_edge_tp_conv_forward", "e2f_profile", "e2f_profile_read", "e2f_last_plan"]
+            "e2f_wigner6j_conv_forward", "e2f_wigner6j_conv_forward_dense", "e2f_wigner6j_conv_forward_global",
+            "e2f_wigner6j_conv_backward", "e2f_edge_tp_conv_forward", "e2f_profile", "e2f_profile_read", "e2f_last_plan"]
 
 
 class E2FError(RuntimeError):
@@ -79,6 +80,8 @@ def _load():
         fn.restype = i
     L.e2f_wigner6j_conv_forward_dense.argtypes = [p, ctypes.POINTER(ConvParams), p, p, i32, p, p, p]
     L.e2f_wigner6j_conv_forward_dense.restype = i
+    L.e2f_wigner6j_conv_forward_global.argtypes = [p, ctypes.POINTER(ConvParams), p, p, i32, p, p]
+    L.e2f_wigner6j_conv_forward_global.restype = i
     L.e2f_wigner6j_conv_backward.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, p, i32, p, p, i64, p, p, p, p]
     L.e2f_wigner6j_conv_backward.restype = i
     return L
@@ -319,6 +322,23 @@ def e2f_wigner6j_conv_forward_dense(ctx, pos, feat, alpha, lmax, heads, cutoff, 
                                              _ptr(out), _stream(feat.device))
     del keep
     _check(st, "e2f_wigner6j_conv_forward_dense")
+    return out
+
+
+def e2f_wigner6j_conv_forward_global(ctx, pos, feat, lmax, heads, cutoff, path_w=None, mix_w=None, out=None):
+    """Uniform attention over the whole graph (alpha = 1 for every pair, self
+    included), in O(N) through the global moments; returns out [N,(L+1)^2,C]."""
+    _dev(pos, torch.float32, "pos")
+    _dev(feat, torch.float32, "feat")
+    n, nk, C = feat.shape
+    if out is None:
+        out = torch.empty_like(feat)
+    _dev(out, torch.float32, "out")
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, 0.0)
+    st = lib.e2f_wigner6j_conv_forward_global(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(feat), n, _ptr(out),
+                                              _stream(feat.device))
+    del keep
+    _check(st, "e2f_wigner6j_conv_forward_global")
     return out
 
 

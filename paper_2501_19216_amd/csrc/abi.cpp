@@ -791,7 +791,7 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
     }
     E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, alpha, alpha_hm, n_edges, n, ord, uni,
                                             blk_off, ucount, edge_slot, use_blocks, nb, t.dimT, C, p->heads, S, s));
-    E2F_TIMED("recouple", launch_recouple(t, Rr, S, ord, nb, C, dh, y, s));
+    E2F_TIMED("recouple", launch_recouple(t, Rr, S, false, ord, nb, C, dh, y, s));
   }
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
   ctx->last_batches = (int64_t)batches.size();
@@ -968,7 +968,61 @@ e2f_status e2f_wigner6j_conv_forward_dense(e2f_ctx* ctx, const e2f_conv_params* 
     if (bs != rocblas_status_success)
       return fail(E2F_EDEVICE, "rocblas_sgemm_strided_batched: %s", rocblas_status_to_string(bs));
   }
-  E2F_TIMED("recouple", launch_recouple(t, R, S, order, n, C, dh, y, s));
+  E2F_TIMED("recouple", launch_recouple(t, R, S, false, order, n, C, dh, y, s));
+  if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
+  return E2F_OK;
+}
+
+e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos,
+                                            const float* feat, int32_t n, float* out, void* stream) {
+  e2f_status rs = check_params(ctx, p);
+  if (rs != E2F_OK) return rs;
+  if (n < 0) return fail(E2F_EINVAL, "n < 0");
+  if (n > 0 && (!pos || !feat || !out)) return fail(E2F_EINVAL, "pos, feat and out are required");
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  const int L = p->lmax, C = p->channels, nk = nk_of(L), dh = C / p->heads;
+  rs = set_weights(ctx, L, path_weights(p), s);
+  if (rs != E2F_OK) return rs;
+  if (n == 0) return E2F_OK;
+  const DevTables& t = ctx->dev[L];
+  int st[kStatsInts];
+  rs = run_bbox(ctx, pos, nullptr, n, s, st);
+  if (rs != E2F_OK) return rs;
+  // one origin, the centre of the bounding box (every pair is coupled)
+  double origin[3];
+  for (int k = 0; k < 3; ++k) origin[k] = (((int64_t)st[k] + st[3 + k]) / 2) / kGrid;
+  const int64_t W = (int64_t)t.dimT * C;
+  const size_t rowb = sizeof(float) * (size_t)W;
+  // T is produced and summed in batches of at most 8 GB
+  const int nbmax = (int)std::max<int64_t>(1, std::min<int64_t>(n, (int64_t)(((size_t)8 << 30) / rowb)));
+  const int G = moment_groups(nbmax, W);
+  const bool mixing = p->mix_w != nullptr;
+  const size_t need = al256(sizeof(double) * 3) + al256(sizeof(double) * (size_t)n * nk) + al256(rowb * nbmax) +
+                      al256(sizeof(double) * (size_t)G * W) + al256(sizeof(double) * (size_t)W) + al256(rowb) +
+                      al256(sizeof(int32_t) * (size_t)n) + (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
+  rs = ensure(ctx, ctx->b, need, s);
+  if (rs != E2F_OK) return rs;
+  Carver cb{(char*)ctx->b.p};
+  double* org = cb.take<double>(3);
+  double* R = cb.take<double>((size_t)n * nk);
+  float* T = cb.take<float>((size_t)nbmax * W);
+  double* part = cb.take<double>((size_t)G * W);
+  double* M64 = cb.take<double>((size_t)W);
+  float* M32 = cb.take<float>((size_t)W);
+  int32_t* order = cb.take<int32_t>((size_t)n);
+  float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
+  ctx->origins_host.assign(origin, origin + 3);
+  E2F_HIP(hipMemcpyAsync(org, ctx->origins_host.data(), sizeof(double) * 3, hipMemcpyHostToDevice, s));
+  E2F_TIMED("sh", launch_sh(t, pos, nullptr, org, nullptr, nullptr, 1, n, R, nullptr, s));
+  for (int b0 = 0; b0 < n; b0 += nbmax) {
+    const int nb = std::min(nbmax, n - b0);
+    E2F_TIMED("node_tp", launch_node_tp(t, R + (size_t)b0 * nk, nullptr, feat + (size_t)b0 * nk * C, nb, C, dh, T, s));
+    E2F_TIMED("aggregate", launch_moment(T, nb, W, part, b0 == 0, b0 + nb >= n, M64, M32, s));
+  }
+  E2F_TIMED("tile_plan", launch_iota(n, order, s));
+  E2F_TIMED("recouple", launch_recouple(t, R, M32, true, order, n, C, dh, y, s));
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
   return E2F_OK;
 }

@@ -589,8 +589,9 @@ __global__ __launch_bounds__(64 * kAggRecv) void k_aggregate_rows(const float4* 
 
 template <int L, int NTW>
 __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __restrict__ R,
-                                                  const float* __restrict__ S, const int32_t* __restrict__ order,
-                                                  int C, int dh, float* __restrict__ y) {
+                                                  const float* __restrict__ S, int64_t s_stride,
+                                                  const int32_t* __restrict__ order, int C, int dh,
+                                                  float* __restrict__ y) {
   constexpr int NK = (L + 1) * (L + 1);
   constexpr int MT = (NK + 15) / 16;  // NTW: channel tiles per wave and pass
   constexpr int QS = rc_qstride(NK);
@@ -603,7 +604,7 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int j = lane & 15, k4 = lane >> 4;
   const int dimT = t.dimT;
-  const float* Si = S + (size_t)blockIdx.x * dimT * C;
+  const float* Si = S + (size_t)blockIdx.x * s_stride;  // s_stride 0: one S row shared by all
   const int NT = (C + 15) / 16;
   for (int ns = 0; ns < NT; ns += 4 * NTW) {
     // B operand: lane (j, k4) reads channel c(q) of row 4s + k4; channels
@@ -984,6 +985,30 @@ __global__ void k_dense_alpha(const float* __restrict__ alpha, int n, int H, flo
   A[q] = i == j ? 0.0f : (alpha ? alpha[ij * H + h] : 1.0f);
 }
 
+// Column sums of a batch of T rows in float64 (uniform attention over the
+// whole graph): workgroup (column block, row group g) sums rows
+// g, g + G, ... of its 256 columns; the finish adds the G partials in order to
+// the running float64 moment and, on the last batch, rounds it to float32.
+__global__ void k_moment_partial(const float* __restrict__ T, int rows, int64_t W, int G,
+                                 double* __restrict__ part) {
+  const int64_t col = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int g = blockIdx.y;
+  if (col >= W) return;
+  double acc = 0.0;
+  for (int r = g; r < rows; r += G) acc += (double)T[(size_t)r * W + col];
+  part[(size_t)g * W + col] = acc;
+}
+
+__global__ void k_moment_finish(const double* __restrict__ part, int64_t W, int G, bool first, bool last,
+                                double* __restrict__ M64, float* __restrict__ M32) {
+  const int64_t col = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (col >= W) return;
+  double acc = first ? 0.0 : M64[col];
+  for (int g = 0; g < G; ++g) acc += part[(size_t)g * W + col];
+  M64[col] = acc;
+  if (last) M32[col] = (float)acc;
+}
+
 // thread per edge: reads its H contiguous weights, writes one coalesced
 // row segment per head
 __global__ void k_alpha_head_major(const float* __restrict__ alpha, int64_t n_edges, int H,
@@ -1279,8 +1304,9 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
   return hipGetLastError();
 }
 
-hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, const int32_t* order, int n, int C,
-                           int dh, float* y, hipStream_t s) {
+hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, bool shared_s, const int32_t* order,
+                           int n, int C, int dh, float* y, hipStream_t s) {
+  const int64_t s_stride = shared_s ? 0 : (int64_t)t.dimT * C;
   if (n == 0) return hipSuccess;
   const int nt = (C + 15) / 16;  // channel tiles; 4 waves
   const int ntw = nt <= 4 ? 1 : (nt <= 8 ? 2 : 4);
@@ -1289,7 +1315,7 @@ hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, 
 #define E2F_RC(LL, W)                                                                                       \
   if (ntw == W) {                                                                                           \
     if (hipError_t e = allow_lds(k_recouple<LL, W>, lds); e != hipSuccess) return e;                        \
-    k_recouple<LL, W><<<n, 256, lds, s>>>(t, R, S, order, C, dh, y);                                        \
+    k_recouple<LL, W><<<n, 256, lds, s>>>(t, R, S, s_stride, order, C, dh, y);                              \
   }
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
@@ -1361,6 +1387,22 @@ hipError_t launch_dense_alpha(const float* alpha, int n, int H, float* A, hipStr
   if (total == 0) return hipSuccess;
   if ((total + 255) / 256 > 0x7fffffff) return hipErrorInvalidValue;
   k_dense_alpha<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(alpha, n, H, A);
+  return hipGetLastError();
+}
+
+int moment_groups(int rows, int64_t W) {
+  const int64_t colblocks = (W + 255) / 256;
+  int G = (int)std::max<int64_t>(1, std::min<int64_t>(rows, (4096 + colblocks - 1) / colblocks));
+  return std::min(G, 64);
+}
+
+hipError_t launch_moment(const float* T, int rows, int64_t W, double* part, bool first, bool last, double* M64,
+                         float* M32, hipStream_t s) {
+  const int G = moment_groups(rows, W);
+  const int64_t colblocks = (W + 255) / 256;
+  if (colblocks > 0x7fffffff) return hipErrorInvalidValue;
+  if (rows > 0) k_moment_partial<<<dim3((unsigned)colblocks, (unsigned)G), 256, 0, s>>>(T, rows, W, G, part);
+  k_moment_finish<<<(unsigned)colblocks, 256, 0, s>>>(part, W, rows > 0 ? G : 0, first, last, M64, M32);
   return hipGetLastError();
 }
 

@@ -98,9 +98,15 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
                             int H, float* S, hipStream_t s);
 // alpha_hm[h][e] = alpha[e][h]
 hipError_t launch_alpha_head_major(const float* alpha, int64_t n_edges, int H, float* alpha_hm, hipStream_t s);
-// y[order[r]] from S row r (head-major like T), r < n
-hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, const int32_t* order, int n, int C,
-                           int dh, float* y, hipStream_t s);
+// y[order[r]] from S row r (head-major like T), r < n; shared_s: every r
+// reads S row 0
+hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, bool shared_s, const int32_t* order,
+                           int n, int C, int dh, float* y, hipStream_t s);
+// Moment of T rows: part holds moment_groups(rows, W) * W doubles; M64 runs
+// over batches (first: start from 0), M32 = M64 rounded on the last batch.
+int moment_groups(int rows, int64_t W);
+hipError_t launch_moment(const float* T, int rows, int64_t W, double* part, bool first, bool last, double* M64,
+                         float* M32, hipStream_t s);
 
 // ---- attention weights [E][H] (H <= 64, 2 <= R <= kAttnMaxRbf radial functions)
 constexpr int kAttnMaxRbf = 32;

@@ -123,6 +123,13 @@ def test_other_argument_checks(e2f):
     assert dense(_params(e2f), n=-1) == e2f.E2F_EINVAL
     assert dense(_params(e2f), pos=None) == e2f.E2F_EINVAL
     assert dense(_params(e2f), n=40000) == e2f.E2F_EUNSUPPORTED  # N^2 H = 6.4e9
+    glob = lambda prm, n=10, pos=FAKE: lib.e2f_wigner6j_conv_forward_global(
+        ctx.handle, ctypes.byref(prm) if prm is not None else None, pos, FAKE, n, FAKE, None)
+    assert glob(_params(e2f)) == e2f.E2F_EDEVICE
+    assert glob(None) == e2f.E2F_EINVAL
+    assert glob(_params(e2f, heads=3)) == e2f.E2F_EINVAL
+    assert glob(_params(e2f), n=-1) == e2f.E2F_EINVAL
+    assert glob(_params(e2f), pos=None) == e2f.E2F_EINVAL
     att = lambda heads=4, dk=2, R=8, rc=5.0, q=FAKE, w=FAKE: lib.e2f_attention_weights(
         ctx.handle, FAKE, q, FAKE, 10, heads, dk, w, R, rc, FAKE, FAKE, 30, FAKE, None)
     assert att() == e2f.E2F_EDEVICE

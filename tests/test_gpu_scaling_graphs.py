@@ -1,7 +1,9 @@
 """The graphs of the scaling study (Sec. 4.1 / Fig. 2): the GPU
 k-nearest-neighbour graph against the oracle, bit-exact; the Wigner-6j layer
 on kNN graphs and on dense graphs (every atom attends to every other) against
-the oracle's definition of the layer.
+the oracle's definition of the layer; uniform attention over the whole graph
+(App. G, global moments) against the oracle's global-moment form and, on a
+small graph, the definition.
 
 Run with -m gpu."""
 import itertools
@@ -139,3 +141,62 @@ def test_dense_graph_single_atom(e2f, ctx):
     got = e2f.e2f_wigner6j_conv_forward_dense(ctx, gpu(np.zeros((1, 3), np.float32)), gpu(feat),
                                               gpu(np.ones((1, 1, 2), np.float32)), 2, 2, 5.0).cpu().numpy()
     assert np.all(got == 0)
+
+
+# ------------------------------------------------------------ global moments (App. G)
+def default_w(L, cutoff):
+    w = np.zeros((L + 1) ** 3)
+    for a, f, oo in itertools.product(range(L + 1), repeat=3):
+        if abs(a - f) <= oo <= a + f:
+            w[(a * (L + 1) + f) * (L + 1) + oo] = cutoff ** (-f)
+    return w
+
+
+@pytest.mark.parametrize("n,L,C,H,rows,mix", [(200, 2, 16, 4, None, False), (1500, 4, 64, 8, 64, True),
+                                               (400, 6, 16, 2, 32, False), (5000, 4, 128, 8, 24, False),
+                                               (333, 3, 12, 3, None, True)])
+def test_global_moment_layer(e2f, ctx, n, L, C, H, rows, mix):
+    rng = np.random.default_rng(7 * n + L)
+    side = (n / 0.1) ** (1.0 / 3.0)
+    pos = syn.quantize(rng.uniform(0, side, size=(n, 3)))
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    cutoff = 10.0
+    w = default_w(L, cutoff)
+    mix_w = (rng.standard_normal((L + 1, C, C)) / np.sqrt(C)).astype(np.float32) if mix else None
+    r = np.arange(n, dtype=np.int32) if rows is None else np.linspace(0, n - 1, rows).astype(np.int32)
+    y = o.conv_global(L, pos, feat, w, pos.astype(np.float64).mean(0), rows=r)
+    ref = y if mix_w is None else o.mix(L, y, mix_w)
+    print("global n %d L %d C %d: case" % (n, L, C), flush=True)
+    got = e2f.e2f_wigner6j_conv_forward_global(ctx, gpu(pos), gpu(feat), L, H, cutoff,
+                                               mix_w=gpu(mix_w)).cpu().numpy()
+    err = o.max_rel_err(got[r], ref, L)
+    print("global n %d L %d: err %.3e" % (n, L, err))
+    assert err <= TOL_F32
+    # default path weights are cutoff^-f on the triangle-valid paths
+    got_d = e2f.e2f_wigner6j_conv_forward_global(ctx, gpu(pos), gpu(feat), L, H, cutoff, path_w=None,
+                                                 mix_w=gpu(mix_w)).cpu().numpy()
+    assert np.array_equal(got_d, got)
+
+
+def test_global_moment_equals_definition(e2f, ctx):
+    # the definition on the complete graph with self edges and alpha = 1
+    n, L, C, H = 90, 3, 8, 2
+    rng = np.random.default_rng(5)
+    pos = syn.quantize(rng.uniform(0, 9.0, size=(n, 3)))
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    w = default_w(L, 5.0)
+    rp = np.arange(n + 1, dtype=np.int64) * n
+    ci = np.tile(np.arange(n, dtype=np.int32), n)
+    ref = o.layer(L, H, pos, feat, rp, ci, np.ones((n * n, H), np.float32), w)
+    got = e2f.e2f_wigner6j_conv_forward_global(ctx, gpu(pos), gpu(feat), L, H, 5.0).cpu().numpy()
+    err = o.max_rel_err(got, ref, L)
+    print("global vs definition: err %.3e" % err)
+    assert err <= TOL_F32
+    # one atom: only its self term, R^(f)(0) = [f == 0]
+    one = e2f.e2f_wigner6j_conv_forward_global(ctx, gpu(pos[:1]), gpu(feat[:1]), L, H, 5.0).cpu().numpy()
+    ref1 = o.layer(L, H, pos[:1], feat[:1], np.array([0, 1], np.int64), np.zeros(1, np.int32),
+                   np.ones((1, H), np.float32), w)
+    assert o.max_rel_err(one, ref1, L) <= TOL_F32
+    # deterministic: a second call gives the same bits
+    again = e2f.e2f_wigner6j_conv_forward_global(ctx, gpu(pos), gpu(feat), L, H, 5.0).cpu().numpy()
+    assert np.array_equal(again, got)

@@ -511,6 +511,8 @@ def test_global_moment_equals_definition(L):
         maxp = np.max(np.linalg.norm(pos.astype(np.float64) - np.array(origin), axis=1))
         tol = 1e-13 * max(1.0, maxp / 3.0) ** L
         assert np.max(np.abs(y1 - y2)) <= tol * np.max(np.abs(y1))
+    sub = np.array([n - 1, 0, 2], dtype=np.int32)
+    assert np.array_equal(o.conv_global(L, pos, feat, w, np.array(origin, dtype=np.float64), rows=sub), y2[sub])
     if L == 0:
         # closed form: every node receives w_000 * sum_j h_j
         assert np.allclose(y2[:, 0, :], w[0] * feat[:, 0, :].astype(np.float64).sum(0)[None, :], rtol=1e-13)
