@@ -63,7 +63,7 @@ def lib():
             L.e2fo_attention_weights.restype = None
             L.e2fo_attention_weights.argtypes = [p, p, p, i, i, i, p, i, ctypes.c_float, p, p, p]
             L.e2fo_conv_edge.restype = i
-            L.e2fo_conv_edge.argtypes = [i, i, i, p, p, i, p, p, p, p, p, i, p]
+            L.e2fo_conv_edge.argtypes = [i, i, i, p, p, i, p, p, p, p, p, i, i, p]
             L.e2fo_conv_factorised.restype = i
             L.e2fo_conv_factorised.argtypes = [i, i, i, p, p, i, p, p, p, p, p, p]
             L.e2fo_conv_global.restype = i
@@ -170,8 +170,9 @@ def attention_weights(pos, q, k, rbf_w, cutoff: float, row_ptr, col_idx) -> np.n
 
 
 # ---------------------------------------------------------------- the layer
-def conv_edge(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, rows=None) -> np.ndarray:
-    """The layer by its definition; returns y [n_rows, (L+1)^2, C] float64."""
+def conv_edge(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, rows=None, y_norm=False) -> np.ndarray:
+    """The layer by its definition; returns y [n_rows, (L+1)^2, C] float64.
+    y_norm: attention weights alpha / D^f per filter degree f (Alg. 1)."""
     pos = _c(pos, np.float32)
     feat = _c(feat, np.float32)
     row_ptr = _c(row_ptr, np.int64)
@@ -182,7 +183,7 @@ def conv_edge(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, rows=None
     rows = np.arange(n, dtype=np.int32) if rows is None else _c(rows, np.int32)
     out = np.zeros((rows.shape[0], nk, C))
     rc = lib().e2fo_conv_edge(lmax, C, heads, _ptr(pos), _ptr(feat), n, _ptr(row_ptr), _ptr(col_idx),
-                              _ptr(alpha), _ptr(path_w), _ptr(rows), rows.shape[0], _ptr(out))
+                              _ptr(alpha), _ptr(path_w), _ptr(rows), rows.shape[0], int(bool(y_norm)), _ptr(out))
     if rc:
         raise ValueError("e2fo_conv_edge rejected its arguments")
     return out
@@ -254,9 +255,9 @@ def mix(lmax, y, W) -> np.ndarray:
     return out
 
 
-def layer(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, mix_w=None, rows=None) -> np.ndarray:
+def layer(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, mix_w=None, rows=None, y_norm=False) -> np.ndarray:
     """Definition plus optional per-irrep mixing: the full forward output."""
-    y = conv_edge(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, rows)
+    y = conv_edge(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, rows, y_norm)
     return y if mix_w is None else mix(lmax, y, mix_w)
 
 

@@ -462,7 +462,7 @@ int64_t e2fo_neighbor_list_cells(const float *pos, const int32_t *graph_id, int 
  * out: [n_rows][(L+1)^2][C]. */
 int e2fo_conv_edge(int L, int C, int H, const float *pos, const float *feat, int n, const int64_t *row_ptr,
                    const int32_t *col_idx, const float *alpha, const double *path_w, const int32_t *rows, int n_rows,
-                   double *out) {
+                   int y_norm, double *out) {
     if (L < 0 || L > 6 || C < 1 || H < 1 || C % H) return 1;
     (void)n;
     int nk = (L + 1) * (L + 1), dh = C / H;
@@ -478,11 +478,18 @@ int e2fo_conv_edge(int L, int C, int H, const float *pos, const float *feat, int
             double v[3] = {(double)pos[3 * i] - pos[3 * j], (double)pos[3 * i + 1] - pos[3 * j + 1],
                            (double)pos[3 * i + 2] - pos[3 * j + 2]};
             e2fo_solid_harmonics(L, v, R);
+            /* y_norm: Alg. 1's per-degree weights alpha / D^f, D = |r_i - r_j|
+             * (filters Y^(f) of the unit vector); 0 for f > 0 at D = 0 */
+            double dpow[7] = {1, 1, 1, 1, 1, 1, 1};
+            if (y_norm) {
+                double D = sqrt(v[0] * v[0] + v[1] * v[1] + v[2] * v[2]);
+                for (int f = 1; f <= L; ++f) dpow[f] = D > 0.0 ? dpow[f - 1] / D : 0.0;
+            }
             const float *hj = feat + (size_t)j * nk * C;
             for (int a = 0; a <= L; ++a)
                 for (int f = 0; f <= L; ++f)
                     for (int o = iabs_(a - f); o <= imin_(a + f, L); ++o) {
-                        double w = path_w[(a * (L + 1) + f) * (L + 1) + o];
+                        double w = path_w[(a * (L + 1) + f) * (L + 1) + o] * dpow[f];
                         if (w == 0.0) continue;
                         const double *c3 = cg(a, f, o);
                         for (int ma = 0; ma < 2 * a + 1; ++ma)

@@ -518,6 +518,32 @@ def test_global_moment_equals_definition(L):
         assert np.allclose(y2[:, 0, :], w[0] * feat[:, 0, :].astype(np.float64).sum(0)[None, :], rtol=1e-13)
 
 
+def test_y_norm_closed_forms():
+    # Alg. 1's per-degree weights alpha / D^f: on a lattice whose edges all
+    # have length D the variant equals the plain layer with w_afo D^-f; scaling
+    # every position by 2 leaves it unchanged, while the plain layer's path f
+    # grows by 2^f
+    L, H, C = 3, 2, 4
+    g = np.array(list(itertools.product(range(4), repeat=3)), dtype=np.float32) * 1.5
+    rp, ci = o.neighbor_list(g, 1.6)  # the six nearest neighbours, all at 1.5
+    rng = np.random.default_rng(3)
+    feat = rng.standard_normal((len(g), (L + 1) ** 2, C)).astype(np.float32)
+    alpha = rng.uniform(0.2, 1.0, size=(len(ci), H)).astype(np.float32)
+    w = rng.uniform(0.5, 1.5, size=(L + 1) ** 3)
+    fpow = np.array([f for a in range(L + 1) for f in range(L + 1) for oo in range(L + 1)], dtype=float)
+    yn = o.conv_edge(L, H, g, feat, rp, ci, alpha, w, y_norm=True)
+    yp = o.conv_edge(L, H, g, feat, rp, ci, alpha, w * 1.5 ** -fpow)
+    assert np.max(np.abs(yn - yp)) <= 1e-13 * np.max(np.abs(yp))
+    pos, rp2, ci2, feat2, alpha2, w2 = small_graph(L, 9, C, H, seed=77)
+    a = o.conv_edge(L, H, pos, feat2, rp2, ci2, alpha2, w2, y_norm=True)
+    b = o.conv_edge(L, H, pos * 2, feat2, rp2, ci2, alpha2, w2, y_norm=True)
+    assert np.max(np.abs(a - b)) <= 1e-13 * np.max(np.abs(a))
+    c = o.conv_edge(L, H, pos * 2, feat2, rp2, ci2, alpha2, w2)
+    d = o.conv_edge(L, H, pos, feat2, rp2, ci2, alpha2, w2 * 2.0 ** fpow)
+    assert np.max(np.abs(c - d)) <= 1e-13 * np.max(np.abs(c))
+    assert np.max(np.abs(a - o.conv_edge(L, H, pos, feat2, rp2, ci2, alpha2, w2))) > 1e-3 * np.max(np.abs(a))
+
+
 def test_layer_equivariance_and_translation():
     # Lemma (equivariance, App. E): rotating positions and features rotates
     # every output irrep by D^(o); a translation changes nothing.
