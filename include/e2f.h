@@ -140,6 +140,13 @@ typedef struct {
   e2f_dtype mix_dtype;   /* E2F_F32, or E2F_BF16 (mixing inputs rounded to bf16, fp32 accumulate) */
   float tile_side;       /* side of the receiver tiles whose centres serve as local origins;
                             0 => cutoff * (8, 8, 8, 6, 4, 3, 2) for L = 0..6 */
+  int32_t y_norm;        /* 0: the layer above.  1: Alg. 1's per-degree attention weights
+                            alpha_ij / D_ij^f on the paths of filter degree f, D_ij = |r_i - r_j|
+                            (filters Y^(f) of the unit vector; the path f takes 0 at D = 0 for
+                            f > 0).  The factorised forward then aggregates once per f (L+1
+                            times the aggregation work and S memory); it needs every degree
+                            <= 512 (else E2F_EUNSUPPORTED).  Forward entry points only (the
+                            backward returns E2F_EUNSUPPORTED) */
 } e2f_conv_params;
 
 /* Wigner-6j convolution forward (Thm. 3.3, Alg. 1): the layer above computed

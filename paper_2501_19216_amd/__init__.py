@@ -37,7 +37,7 @@ class E2FError(RuntimeError):
 class ConvParams(ctypes.Structure):
     _fields_ = [("lmax", ctypes.c_int), ("channels", ctypes.c_int32), ("heads", ctypes.c_int32),
                 ("cutoff", ctypes.c_float), ("path_w", ctypes.c_void_p), ("mix_w", ctypes.c_void_p),
-                ("mix_dtype", ctypes.c_int), ("tile_side", ctypes.c_float)]
+                ("mix_dtype", ctypes.c_int), ("tile_side", ctypes.c_float), ("y_norm", ctypes.c_int32)]
 
 
 def _load():
@@ -248,7 +248,7 @@ def e2f_node_tp(ctx: Context, pos: torch.Tensor, feat: torch.Tensor, lmax: int, 
     return out
 
 
-def _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side):
+def _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm=False):
     import numpy as np
     keep = None
     pw = None
@@ -266,12 +266,12 @@ def _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side):
         if not mix_w.is_cuda or not mix_w.is_contiguous():
             raise ValueError("mix_w must be a contiguous device tensor")
     prm = ConvParams(lmax, channels, heads, cutoff, pw, None if mix_w is None else mix_w.data_ptr(), mix_dtype,
-                     float(tile_side))
+                     float(tile_side), int(bool(y_norm)))
     return prm, keep
 
 
 def _conv(fn_name, ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w, mix_w, graph_id,
-          tile_side, out):
+          tile_side, out, y_norm=False):
     _dev(pos, torch.float32, "pos")
     _dev(feat, torch.float32, "feat")
     _dev(row_ptr, torch.int64, "row_ptr")
@@ -282,7 +282,7 @@ def _conv(fn_name, ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff,
     if out is None:
         out = torch.empty_like(feat)
     _dev(out, torch.float32, "out")
-    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side)
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm)
     st = getattr(lib, fn_name)(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(graph_id), _ptr(feat), n,
                                _ptr(row_ptr), _ptr(col_idx), col_idx.numel(), _ptr(alpha), _ptr(out),
                                _stream(feat.device))
@@ -292,17 +292,18 @@ def _conv(fn_name, ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff,
 
 
 def e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None, mix_w=None,
-                              graph_id=None, tile_side=0.0, out=None):
-    """Wigner-6j convolution forward; returns out [N,(L+1)^2,C] float32."""
+                              graph_id=None, tile_side=0.0, out=None, y_norm=False):
+    """Wigner-6j convolution forward; returns out [N,(L+1)^2,C] float32.
+    y_norm: attention weights alpha / |r_i - r_j|^f per filter degree f."""
     return _conv("e2f_wigner6j_conv_forward", ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w,
-                 mix_w, graph_id, tile_side, out)
+                 mix_w, graph_id, tile_side, out, y_norm)
 
 
 def e2f_edge_tp_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None, mix_w=None,
-                             graph_id=None, tile_side=0.0, out=None):
+                             graph_id=None, tile_side=0.0, out=None, y_norm=False):
     """Per-edge SO(3) convolution baseline; same output as the 6j forward."""
     return _conv("e2f_edge_tp_conv_forward", ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w,
-                 mix_w, graph_id, tile_side, out)
+                 mix_w, graph_id, tile_side, out, y_norm)
 
 
 def e2f_wigner6j_conv_forward_dense(ctx, pos, feat, alpha, lmax, heads, cutoff, path_w=None, mix_w=None, out=None):

@@ -50,6 +50,9 @@ struct e2f_ctx {
   std::vector<void*> table_mem;            // structure arrays per L
   std::vector<void*> coef_mem;             // weighted coefficients per L
   std::vector<std::vector<double>> coef_w; // path weights of the uploaded coefficients
+  // per L and filter degree f: the recouple schedule restricted to b + u = f
+  std::vector<std::vector<const int*>> rcf_k, rcf_off, rcf_meta;
+  std::vector<std::vector<const double*>> rcf_coef;
   int* stats = nullptr;                    // device, kStatsInts ints
   int64_t* pinned = nullptr;               // host, 16 int64
   int32_t* pinned_plan = nullptr;          // host, plan sizes read back in one copy
@@ -196,6 +199,11 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
   push_array(blob, o, t.rc_sched.k);     // 20
   push_array(blob, o, t.rc_sched.off);   // 21
   push_array(blob, o, t.rc_sched.meta);  // 22
+  for (int f = 0; f <= L; ++f) {          // 23 + 3f .. 25 + 3f
+    push_array(blob, o, t.rcf_sched[f].k);
+    push_array(blob, o, t.rcf_sched[f].off);
+    push_array(blob, o, t.rcf_sched[f].meta);
+  }
   void* mem = nullptr;
   E2F_HIP(hipMalloc(&mem, blob.size()));
   ctx->table_mem[L] = mem;
@@ -229,6 +237,15 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
   d.rc_off = (const int*)(b + o[21]);
   d.rc_meta = (const int*)(b + o[22]);
   d.rc_coef = nullptr;
+  ctx->rcf_k[L].assign(L + 1, nullptr);
+  ctx->rcf_off[L].assign(L + 1, nullptr);
+  ctx->rcf_meta[L].assign(L + 1, nullptr);
+  ctx->rcf_coef[L].assign(L + 1, nullptr);
+  for (int f = 0; f <= L; ++f) {
+    ctx->rcf_k[L][f] = (const int*)(b + o[23 + 3 * f]);
+    ctx->rcf_off[L][f] = (const int*)(b + o[24 + 3 * f]);
+    ctx->rcf_meta[L][f] = (const int*)(b + o[25 + 3 * f]);
+  }
   d.q_coef = nullptr;
   d.k_coef = nullptr;
   d.max_qslots = t.max_qslots;
@@ -268,6 +285,12 @@ e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStr
   push_array(blob, o, q);
   push_array(blob, o, k);
   push_array(blob, o, rc);
+  for (int f = 0; f <= L; ++f) {  // o[3 + f]
+    const Schedule& sf = t.rcf_sched[f];
+    std::vector<double> c(sf.unit.size());
+    for (size_t e = 0; e < c.size(); ++e) c[e] = sf.path[e] < 0 ? 0.0 : sf.unit[e] * w[sf.path[e]];
+    push_array(blob, o, c);
+  }
   E2F_HIP(hipStreamSynchronize(s));  // earlier work may still read the old coefficients
   if (ctx->coef_mem[L]) E2F_HIP(hipFree(ctx->coef_mem[L]));
   ctx->coef_mem[L] = nullptr;
@@ -279,6 +302,7 @@ e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStr
   ctx->dev[L].q_coef = (const double*)((char*)mem + o[0]);
   ctx->dev[L].k_coef = (const float*)((char*)mem + o[1]);
   ctx->dev[L].rc_coef = (const double*)((char*)mem + o[2]);
+  for (int f = 0; f <= L; ++f) ctx->rcf_coef[L][f] = (const double*)((char*)mem + o[3 + f]);
   return E2F_OK;
 }
 
@@ -296,6 +320,7 @@ e2f_status check_params(e2f_ctx* ctx, const e2f_conv_params* p) {
                 p->channels, p->channels / p->heads);
   if (!finite_pos(p->cutoff) || p->cutoff > 64.0f) return fail(E2F_EINVAL, "cutoff must be finite, in (0, 64]");
   if (!std::isfinite(p->tile_side) || p->tile_side < 0.0f) return fail(E2F_EINVAL, "tile_side must be finite and >= 0");
+  if (p->y_norm != 0 && p->y_norm != 1) return fail(E2F_EINVAL, "y_norm must be 0 or 1");
   if (p->mix_dtype != E2F_F32 && p->mix_dtype != E2F_BF16) return fail(E2F_EINVAL, "unknown mix_dtype");
   if (p->path_w) {
     const int L1 = p->lmax + 1;
@@ -391,6 +416,10 @@ e2f_status e2f_create(int lmax_max, int device, e2f_ctx** out) {
   ctx->table_mem.assign(lmax_max + 1, nullptr);
   ctx->coef_mem.assign(lmax_max + 1, nullptr);
   ctx->coef_w.assign(lmax_max + 1, {});
+  ctx->rcf_k.assign(lmax_max + 1, {});
+  ctx->rcf_off.assign(lmax_max + 1, {});
+  ctx->rcf_meta.assign(lmax_max + 1, {});
+  ctx->rcf_coef.assign(lmax_max + 1, {});
   if (device >= 0) {
     int count = 0;
     if (hipGetDeviceCount(&count) != hipSuccess || device >= count) {
@@ -723,6 +752,11 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   ctx->last_tiles = keys;
   // the MFMA aggregation over receiver blocks of 16 needs 16 * degree <= 8192
   const bool use_blocks = max_degree <= kBlockMaxDegree;
+  // alpha / D^f: one aggregation and one S per filter degree f
+  const bool ynorm = p->y_norm != 0;
+  const int nS = ynorm ? L + 1 : 1;
+  if (ynorm && !use_blocks)
+    return fail(E2F_EUNSUPPORTED, "y_norm needs every degree <= %d (largest %d)", kBlockMaxDegree, max_degree);
   // ---- tile batches: T and S of a batch must fit the memory budget
   const size_t row_bytes = sizeof(float) * (size_t)t.dimT * C;
   size_t free_b = 0, total_b = 0;
@@ -737,7 +771,7 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   for (int t0 = 0; t0 < (int)keys;) {
     int t1 = t0 + 1;
     auto cost = [&](int a, int b) {
-      return (size_t)((int64_t)(pstart[b] - pstart[a]) + (rstart[b] - rstart[a])) * row_bytes;
+      return (size_t)((int64_t)(pstart[b] - pstart[a]) + (int64_t)nS * (rstart[b] - rstart[a])) * row_bytes;
     };
     while (t1 < (int)keys && cost(t0, t1 + 1) <= budget) ++t1;
     batches.push_back({t0, t1});
@@ -752,9 +786,10 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   const size_t need_b = 2 * al256(sizeof(int32_t) * (size_t)P) + 3 * al256(sizeof(int32_t) * (size_t)n_edges) +
                         3 * al256(sizeof(int32_t) * (size_t)(nblk + 1)) + al256(blk_tmp_b) +
                         al256(sizeof(double) * (size_t)P * nk) + al256(sizeof(double) * (size_t)n * nk) +
-                        al256(row_bytes * (size_t)max_pairs) + al256(row_bytes * (size_t)max_recv) +
+                        al256(row_bytes * (size_t)max_pairs) + al256(row_bytes * (size_t)max_recv * nS) +
                         (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0) +
-                        (use_blocks && alpha ? al256(sizeof(float) * (size_t)n_edges * p->heads) : 0);
+                        (use_blocks && (alpha || ynorm) ? al256(sizeof(float) * (size_t)n_edges * p->heads * nS) : 0) +
+                        (ynorm ? al256(sizeof(int32_t) * (size_t)n_edges) : 0);
   rs = ensure(ctx, ctx->b, need_b, s);
   if (rs != E2F_OK) return rs;
   Carver cb{(char*)ctx->b.p};
@@ -770,10 +805,15 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   double* Rp = cb.take<double>((size_t)P * nk);
   double* Rr = cb.take<double>((size_t)n * nk);
   float* T = cb.take<float>((size_t)max_pairs * t.dimT * C);
-  float* S = cb.take<float>((size_t)max_recv * t.dimT * C);
+  float* S = cb.take<float>((size_t)max_recv * t.dimT * C * nS);
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
-  float* alpha_hm = use_blocks && alpha ? cb.take<float>((size_t)n_edges * p->heads) : nullptr;
-  if (alpha_hm) E2F_TIMED("alpha_hm", launch_alpha_head_major(alpha, n_edges, p->heads, alpha_hm, s));
+  float* alpha_hm = use_blocks && (alpha || ynorm) ? cb.take<float>((size_t)n_edges * p->heads * nS) : nullptr;
+  if (ynorm) {
+    int32_t* erows = cb.take<int32_t>((size_t)n_edges);
+    E2F_TIMED("alpha_hm", launch_alpha_dnorm(pos, row_ptr, col_idx, alpha, n, n_edges, p->heads, L, erows, alpha_hm, s));
+  } else if (alpha_hm) {
+    E2F_TIMED("alpha_hm", launch_alpha_head_major(alpha, n_edges, p->heads, alpha_hm, s));
+  }
   E2F_TIMED("tile_plan", launch_pairs(flags, pidx, count, n, pair_node, pair_tile, s));
   E2F_TIMED("tile_plan", launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
   E2F_TIMED("sh", launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, nullptr, s));
@@ -789,9 +829,28 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
       E2F_TIMED("tile_plan", launch_block_union(row_ptr, col_pair, ord, nb, blk_count, blk_off, uni, ucount,
                                                 edge_slot, blk_tmp, blk_tmp_b, s));
     }
-    E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, alpha, alpha_hm, n_edges, n, ord, uni,
-                                            blk_off, ucount, edge_slot, use_blocks, nb, t.dimT, C, p->heads, S, s));
-    E2F_TIMED("recouple", launch_recouple(t, Rr, S, false, ord, nb, C, dh, y, s));
+    if (!ynorm) {
+      E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, alpha, alpha_hm, n_edges, n, ord, uni,
+                                              blk_off, ucount, edge_slot, use_blocks, nb, t.dimT, C, p->heads, S, s));
+      E2F_TIMED("recouple", launch_recouple(t, Rr, S, false, ord, nb, C, dh, y, s));
+    } else {
+      // S^(f) = sum_j alpha_ij D_ij^-f T_j, and the recouple terms of filter
+      // degree b + u = f read S^(f); the f = 0 pass stores y, the others add
+      const size_t sstride = (size_t)max_recv * t.dimT * C;
+      for (int f = 0; f <= L; ++f)
+        E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, nullptr,
+                                                alpha_hm + (size_t)f * p->heads * n_edges, n_edges, n, ord, uni,
+                                                blk_off, ucount, edge_slot, true, nb, t.dimT, C, p->heads,
+                                                S + f * sstride, s));
+      for (int f = 0; f <= L; ++f) {
+        DevTables tf = t;
+        tf.rc_k = ctx->rcf_k[L][f];
+        tf.rc_off = ctx->rcf_off[L][f];
+        tf.rc_meta = ctx->rcf_meta[L][f];
+        tf.rc_coef = ctx->rcf_coef[L][f];
+        E2F_TIMED("recouple", launch_recouple(tf, Rr, S + f * sstride, false, ord, nb, C, dh, y, s, f > 0));
+      }
+    }
   }
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
   ctx->last_batches = (int64_t)batches.size();
@@ -822,7 +881,8 @@ e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, cons
     if (rs != E2F_OK) return rs;
     y = (float*)ctx->c.p;
   }
-  E2F_TIMED("edge_tp", launch_edge_tp(ctx->dev[L], pos, feat, row_ptr, col_idx, alpha, n, C, p->heads, y, s));
+  E2F_TIMED("edge_tp", launch_edge_tp(ctx->dev[L], pos, feat, row_ptr, col_idx, alpha, n, C, p->heads, y, s,
+                                      p->y_norm != 0));
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
   return E2F_OK;
 }
@@ -835,6 +895,7 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
   if (grad_alpha && n > 0 && !feat) return fail(E2F_EINVAL, "feat is required for grad_alpha");
   e2f_status rs = check_params(ctx, p);
   if (rs != E2F_OK) return rs;
+  if (p->y_norm) return fail(E2F_EUNSUPPORTED, "y_norm: the backward covers the plain layer only");
   if (grad_alpha && p->channels > 256) return fail(E2F_EUNSUPPORTED, "grad_alpha needs channels <= 256");
   rs = check_conv(ctx, p, pos, grad_out, n, row_ptr, col_idx, n_edges, const_cast<float*>(grad_out));
   if (rs != E2F_OK) return rs;
@@ -914,6 +975,7 @@ e2f_status e2f_wigner6j_conv_forward_dense(e2f_ctx* ctx, const e2f_conv_params* 
   if (n < 0) return fail(E2F_EINVAL, "n < 0");
   if (n > 0 && (!pos || !feat || !out)) return fail(E2F_EINVAL, "pos, feat and out are required");
   if ((double)n * n * p->heads > 4.0e9) return fail(E2F_EUNSUPPORTED, "N^2 H = %.3g attention weights", (double)n * n * p->heads);
+  if (p->y_norm) return fail(E2F_EUNSUPPORTED, "y_norm: not available on this entry point");
   if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
   hipStream_t s = (hipStream_t)stream;
   DeviceGuard g(ctx->device);
@@ -979,6 +1041,7 @@ e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params*
   if (rs != E2F_OK) return rs;
   if (n < 0) return fail(E2F_EINVAL, "n < 0");
   if (n > 0 && (!pos || !feat || !out)) return fail(E2F_EINVAL, "pos, feat and out are required");
+  if (p->y_norm) return fail(E2F_EUNSUPPORTED, "y_norm: not available on this entry point");
   if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
   hipStream_t s = (hipStream_t)stream;
   DeviceGuard g(ctx->device);

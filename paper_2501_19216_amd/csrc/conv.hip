@@ -591,7 +591,7 @@ template <int L, int NTW>
 __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __restrict__ R,
                                                   const float* __restrict__ S, int64_t s_stride,
                                                   const int32_t* __restrict__ order, int C, int dh,
-                                                  float* __restrict__ y) {
+                                                  bool accumulate, float* __restrict__ y) {
   constexpr int NK = (L + 1) * (L + 1);
   constexpr int MT = (NK + 15) / 16;  // NTW: channel tiles per wave and pass
   constexpr int QS = rc_qstride(NK);
@@ -684,7 +684,10 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int row = mt * 16 + 4 * k4 + v;
-          if (row < NK) y[((size_t)i * NK + row) * C + c] = acc[q][mt][v];
+          if (row < NK) {
+            float* yp = y + ((size_t)i * NK + row) * C + c;
+            *yp = accumulate ? *yp + acc[q][mt][v] : acc[q][mt][v];
+          }
         }
     }
   }
@@ -1009,6 +1012,26 @@ __global__ void k_moment_finish(const double* __restrict__ part, int64_t W, int 
   if (last) M32[col] = (float)acc;
 }
 
+// Per-degree attention weights alpha / D^f (Alg. 1), D = |r_i - r_j| in
+// float64, head-major per f: alpha_f[(f*H + h)*E + e]; 0 for f > 0 at D = 0.
+__global__ void k_alpha_dnorm(const float* __restrict__ pos, const int32_t* __restrict__ rows,
+                              const int32_t* __restrict__ col, const float* __restrict__ alpha, int64_t n_edges,
+                              int H, int L, float* __restrict__ alpha_f) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= n_edges) return;
+  const int i = rows[e], j = col[e];
+  const double dx = (double)pos[3 * i] - pos[3 * j], dy = (double)pos[3 * i + 1] - pos[3 * j + 1],
+               dz = (double)pos[3 * i + 2] - pos[3 * j + 2];
+  const double D = sqrt(dx * dx + dy * dy + dz * dz);
+  const double inv = D > 0.0 ? 1.0 / D : 0.0;
+  double s = 1.0;
+  for (int f = 0; f <= L; ++f) {
+    for (int h = 0; h < H; ++h)
+      alpha_f[((int64_t)f * H + h) * n_edges + e] = (float)((alpha ? (double)alpha[e * H + h] : 1.0) * s);
+    s *= inv;
+  }
+}
+
 // thread per edge: reads its H contiguous weights, writes one coalesced
 // row segment per head
 __global__ void k_alpha_head_major(const float* __restrict__ alpha, int64_t n_edges, int H,
@@ -1031,7 +1054,7 @@ template <int L>
 __global__ __launch_bounds__(128) void k_edge_tp(DevTables t, const float* __restrict__ pos,
                                                  const float* __restrict__ feat, const int64_t* __restrict__ row_ptr,
                                                  const int32_t* __restrict__ col, const float* __restrict__ alpha,
-                                                 int C, int H, float* __restrict__ y) {
+                                                 int C, int H, bool y_norm, float* __restrict__ y) {
   constexpr int NK = (L + 1) * (L + 1);
   constexpr int EB = 4;
   extern __shared__ float sm[];
@@ -1053,7 +1076,13 @@ __global__ __launch_bounds__(128) void k_edge_tp(DevTables t, const float* __res
       for (int q = threadIdx.x; q < nb * NK; q += blockDim.x) {
         const int b = q / NK, k = q % NK;
         const int j = col[eb + b];
-        Rl[q] = sh_poly<float>(t, k, xi - pos[3 * j], yi - pos[3 * j + 1], zi - pos[3 * j + 2]);
+        float dx = xi - pos[3 * j], dy = yi - pos[3 * j + 1], dz = zi - pos[3 * j + 2];
+        if (y_norm) {  // R^(f)(r / D) = R^(f)(r) / D^f; the zero vector at D = 0
+          const float D = sqrtf(dx * dx + dy * dy + dz * dz);
+          const float sc = D > 0.0f ? 1.0f / D : 0.0f;
+          dx *= sc, dy *= sc, dz *= sc;
+        }
+        Rl[q] = sh_poly<float>(t, k, dx, dy, dz);
       }
       __syncthreads();
       for (int q = threadIdx.x; q < nb * NK * NK; q += blockDim.x) {
@@ -1305,7 +1334,7 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
 }
 
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, bool shared_s, const int32_t* order,
-                           int n, int C, int dh, float* y, hipStream_t s) {
+                           int n, int C, int dh, float* y, hipStream_t s, bool accumulate) {
   const int64_t s_stride = shared_s ? 0 : (int64_t)t.dimT * C;
   if (n == 0) return hipSuccess;
   const int nt = (C + 15) / 16;  // channel tiles; 4 waves
@@ -1315,7 +1344,7 @@ hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, 
 #define E2F_RC(LL, W)                                                                                       \
   if (ntw == W) {                                                                                           \
     if (hipError_t e = allow_lds(k_recouple<LL, W>, lds); e != hipSuccess) return e;                        \
-    k_recouple<LL, W><<<n, 256, lds, s>>>(t, R, S, s_stride, order, C, dh, y);                              \
+    k_recouple<LL, W><<<n, 256, lds, s>>>(t, R, S, s_stride, order, C, dh, accumulate, y);                  \
   }
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
@@ -1365,7 +1394,7 @@ hipError_t launch_mix(int L, const float* y, const void* W, bool w_bf16, int n, 
 }
 
 hipError_t launch_edge_tp(const DevTables& t, const float* pos, const float* feat, const int64_t* row_ptr,
-                          const int32_t* col_idx, const float* alpha, int n, int C, int H, float* y, hipStream_t s) {
+                          const int32_t* col_idx, const float* alpha, int n, int C, int H, float* y, hipStream_t s, bool y_norm) {
   if (n == 0) return hipSuccess;
   const int threads = C <= 64 ? 64 : 128;
   const size_t lds = sizeof(float) * ((size_t)4 * t.nk * t.nk + (size_t)4 * t.nk);
@@ -1373,7 +1402,7 @@ hipError_t launch_edge_tp(const DevTables& t, const float* pos, const float* fea
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
     if (hipError_t e = allow_lds(k_edge_tp<LL>, lds); e != hipSuccess) return e;                            \
-    k_edge_tp<LL><<<n, threads, lds, s>>>(t, pos, feat, row_ptr, col_idx, alpha, C, H, y);                  \
+    k_edge_tp<LL><<<n, threads, lds, s>>>(t, pos, feat, row_ptr, col_idx, alpha, C, H, y_norm, y);          \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
 #undef E2F_CASE
@@ -1403,6 +1432,16 @@ hipError_t launch_moment(const float* T, int rows, int64_t W, double* part, bool
   if (colblocks > 0x7fffffff) return hipErrorInvalidValue;
   if (rows > 0) k_moment_partial<<<dim3((unsigned)colblocks, (unsigned)G), 256, 0, s>>>(T, rows, W, G, part);
   k_moment_finish<<<(unsigned)colblocks, 256, 0, s>>>(part, W, rows > 0 ? G : 0, first, last, M64, M32);
+  return hipGetLastError();
+}
+
+hipError_t launch_alpha_dnorm(const float* pos, const int64_t* row_ptr, const int32_t* col, const float* alpha, int n,
+                              int64_t n_edges, int H, int L, int32_t* rows, float* alpha_f, hipStream_t s) {
+  if (n_edges == 0) return hipSuccess;
+  const int64_t blocks = (n_edges + 255) / 256;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  k_edge_rows<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, n, rows);
+  k_alpha_dnorm<<<(unsigned)blocks, 256, 0, s>>>(pos, rows, col, alpha, n_edges, H, L, alpha_f);
   return hipGetLastError();
 }
 

@@ -86,6 +86,9 @@ struct LayerTables {
   Schedule tp_sched;
   std::vector<int> tp_rs, tp_mo;    // [L+1], [L+2]
   Schedule rc_sched;                // recouple: chunks of rc_rows T rows, dest = row*rc_qstride + (o*o+m)
+  // recouple restricted to the terms of filter degree f = b + u, one schedule
+  // per f (attention weights alpha / D^f need one aggregation per f)
+  std::vector<Schedule> rcf_sched;  // [L+1]
   int max_qslots = 0;               // largest (2o+1)*ncol[o]
   int m_slots() const { return m_rowoff.back(); }
 };

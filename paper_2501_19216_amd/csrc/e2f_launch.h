@@ -96,12 +96,17 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
                             const int32_t* order, const int32_t* uni, const int32_t* blk_off,
                             const int32_t* ucount, const int32_t* edge_slot, bool use_blocks, int n, int dimT, int C,
                             int H, float* S, hipStream_t s);
+// alpha_f[(f*H + h)*E + e] = alpha[e][h] / |r_i - r_j|^f for f <= L (rows:
+// E ints of scratch, the receiver of every edge); alpha NULL means ones
+hipError_t launch_alpha_dnorm(const float* pos, const int64_t* row_ptr, const int32_t* col, const float* alpha, int n,
+                              int64_t n_edges, int H, int L, int32_t* rows, float* alpha_f, hipStream_t s);
 // alpha_hm[h][e] = alpha[e][h]
 hipError_t launch_alpha_head_major(const float* alpha, int64_t n_edges, int H, float* alpha_hm, hipStream_t s);
 // y[order[r]] from S row r (head-major like T), r < n; shared_s: every r
 // reads S row 0
+// accumulate: y += the product instead of y = (one writer per element)
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, bool shared_s, const int32_t* order,
-                           int n, int C, int dh, float* y, hipStream_t s);
+                           int n, int C, int dh, float* y, hipStream_t s, bool accumulate = false);
 // Moment of T rows: part holds moment_groups(rows, W) * W doubles; M64 runs
 // over batches (first: start from 0), M32 = M64 rounded on the last batch.
 int moment_groups(int rows, int64_t W);
@@ -136,6 +141,6 @@ hipError_t launch_iota(int n, int32_t* v, hipStream_t s);
 // ---- per-irrep channel mixing and the edge baseline
 hipError_t launch_mix(int L, const float* y, const void* W, bool w_bf16, int n, int C, float* out, hipStream_t s);
 hipError_t launch_edge_tp(const DevTables& t, const float* pos, const float* feat, const int64_t* row_ptr,
-                          const int32_t* col_idx, const float* alpha, int n, int C, int H, float* y, hipStream_t s);
+                          const int32_t* col_idx, const float* alpha, int n, int C, int H, float* y, hipStream_t s, bool y_norm = false);
 
 }  // namespace e2f

@@ -359,6 +359,32 @@ LayerTables build_layer_tables(int L) {
         }
     }
     t.rc_sched = make_schedule(rchunks);
+    // per filter degree f: the entries of the same slots whose u = f - b
+    std::vector<int> row_b(t.dimT, 0);
+    for (const Block& B : t.blocks)
+      for (int de = 0; de < 2 * B.d + 1; ++de) row_b[B.toff + de] = B.b;
+    auto degree_of = [](int ridx) {  // ridx = u*u + gamma, gamma < 2u+1
+      int u = 0;
+      while ((u + 1) * (u + 1) <= ridx) ++u;
+      return u;
+    };
+    t.rcf_sched.clear();
+    for (int f = 0; f <= L; ++f) {
+      std::vector<std::vector<Slot>> fchunks((t.dimT + RR - 1) / RR);
+      for (int o = 0; o <= L; ++o) {
+        const int ncol = t.q_ncol[o];
+        for (int m = 0; m < 2 * o + 1; ++m)
+          for (int col = 0; col < ncol; ++col) {
+            const int s = t.q_slotoff[o] + m * ncol + col;
+            const int row = t.q_cols[t.q_coloff[o] + col];
+            Slot sl{(row % RR) * QS + o * o + m, {}};
+            for (int e = t.q_ptr[s]; e < t.q_ptr[s + 1]; ++e)
+              if (row_b[row] + degree_of(t.q_ridx[e]) == f) sl.e.push_back({t.q_ridx[e], t.q_path[e], t.q_unit[e]});
+            if (!sl.e.empty()) fchunks[row / RR].push_back(std::move(sl));
+          }
+      }
+      t.rcf_sched.push_back(make_schedule(fchunks));
+    }
   }
 
   // ---- edge filter K[k][q] = sum_f w_afo sum_mf C^{o m}_{a al, f mf} R^(f)_mf(r_ij)

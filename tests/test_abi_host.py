@@ -84,6 +84,8 @@ def test_conv_argument_checks(e2f, fn):
     assert call(_params(e2f, cutoff=float("nan"))) == EINVAL
     assert call(_params(e2f, tile_side=-1.0)) == EINVAL
     assert call(_params(e2f, mix_dtype=7)) == EINVAL
+    assert call(_params(e2f, y_norm=2)) == EINVAL
+    assert call(_params(e2f, y_norm=1)) == EDEV
     assert call(_params(e2f), n=-1) == EINVAL
     assert call(_params(e2f), E=-1) == EINVAL
     assert call(_params(e2f), E=2 ** 31) == EUNS
@@ -130,6 +132,8 @@ def test_other_argument_checks(e2f):
     assert glob(_params(e2f, heads=3)) == e2f.E2F_EINVAL
     assert glob(_params(e2f), n=-1) == e2f.E2F_EINVAL
     assert glob(_params(e2f), pos=None) == e2f.E2F_EINVAL
+    assert glob(_params(e2f, y_norm=1)) == e2f.E2F_EUNSUPPORTED
+    assert dense(_params(e2f, y_norm=1)) == e2f.E2F_EUNSUPPORTED
     att = lambda heads=4, dk=2, R=8, rc=5.0, q=FAKE, w=FAKE: lib.e2f_attention_weights(
         ctx.handle, FAKE, q, FAKE, 10, heads, dk, w, R, rc, FAKE, FAKE, 30, FAKE, None)
     assert att() == e2f.E2F_EDEVICE
@@ -145,6 +149,7 @@ def test_other_argument_checks(e2f):
         ctx.handle, ctypes.byref(prm), FAKE, None, feat, FAKE, 10, FAKE, FAKE, 30, None, gf, ga, None)
     assert bwd(_params(e2f)) == e2f.E2F_EDEVICE
     assert bwd(_params(e2f), gf=None, ga=None) == e2f.E2F_EINVAL
+    assert bwd(_params(e2f, y_norm=1)) == e2f.E2F_EUNSUPPORTED
     assert bwd(_params(e2f), feat=None) == e2f.E2F_EINVAL  # grad_alpha needs the features
     assert bwd(_params(e2f, channels=512, heads=8)) == e2f.E2F_EUNSUPPORTED
     assert bwd(_params(e2f, channels=512, heads=8), ga=None) == e2f.E2F_EDEVICE
