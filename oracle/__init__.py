@@ -52,6 +52,10 @@ def lib():
             L.e2fo_recoupling_x.argtypes = [i] * 5
             L.e2fo_solid_harmonics.restype = None
             L.e2fo_solid_harmonics.argtypes = [i, p, p]
+            L.e2fo_solid_harmonics_grad.restype = None
+            L.e2fo_solid_harmonics_grad.argtypes = [i, p, p]
+            L.e2fo_conv_edge_grad_pos.restype = i
+            L.e2fo_conv_edge_grad_pos.argtypes = [i, i, i, p, p, p, i, p, p, p, p, p, i, p]
             L.e2fo_neighbor_list.restype = i64
             L.e2fo_neighbor_list.argtypes = [p, p, i, ctypes.c_float, p, p, i64]
             L.e2fo_neighbor_list_cells.restype = i64
@@ -123,6 +127,14 @@ def solid_harmonics(lmax: int, v) -> np.ndarray:
 
 
 # ---------------------------------------------------------------- graph
+def solid_harmonics_grad(lmax: int, v) -> np.ndarray:
+    """dR^(l)_m / dv_x for l <= lmax; v: [3] -> [3, (lmax+1)^2] (float64)."""
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    out = np.zeros((3, (lmax + 1) ** 2))
+    lib().e2fo_solid_harmonics_grad(lmax, _ptr(v), _ptr(out))
+    return out
+
+
 def neighbor_list(pos, cutoff: float, graph_id=None, method: str = "auto"):
     """Radius graph as CSR (row_ptr int64 [N+1], col_idx int32 [E])."""
     pos = _c(pos, np.float32)
@@ -213,6 +225,23 @@ def conv_edge_vjp(lmax, heads, pos, feat, gy, row_ptr, col_idx, alpha, path_w, w
     if rc:
         raise ValueError("e2fo_conv_edge_vjp rejected its arguments")
     return gf, ga
+
+
+def conv_edge_grad_pos(lmax, heads, pos, feat, gy, row_ptr, col_idx, alpha, path_w, atoms=None) -> np.ndarray:
+    """Gradient of sum(gy * layer) with respect to the positions (the graph
+    and alpha held fixed), by the definition: [n or len(atoms), 3] float64."""
+    at = _c(atoms, np.int32)
+    pos = _c(pos, np.float32)
+    feat = _c(feat, np.float32)
+    n, nk, C = feat.shape
+    out = np.zeros((n if at is None else len(at), 3))
+    rc = lib().e2fo_conv_edge_grad_pos(lmax, C, heads, _ptr(pos), _ptr(feat), _ptr(_c(gy, np.float64)), n,
+                                       _ptr(_c(row_ptr, np.int64)), _ptr(_c(col_idx, np.int32)),
+                                       _ptr(_c(alpha, np.float32)), _ptr(_c(path_w, np.float64)), _ptr(at),
+                                       0 if at is None else len(at), _ptr(out))
+    if rc:
+        raise ValueError("e2fo_conv_edge_grad_pos rejected its arguments")
+    return out
 
 
 def conv_factorised(lmax, heads, pos, feat, row_ptr, col_idx, alpha, path_w, origin) -> np.ndarray:

@@ -176,6 +176,29 @@ void e2fo_solid_harmonics(int lmax, const double *v, double *out) {
     for (int l = 2; l <= lmax; ++l) couple(l - 1, out + (l - 1) * (l - 1), 1, r1, l, out + l * l);
 }
 
+/* Gradient of the solid harmonics: out[x*nk + k] = dR_k / dv_x (x, y, z),
+ * by the product rule on the recursion R^(l) = [R^(l-1) (x) R^(1)]^(l), whose
+ * coupling is bilinear: dR^(l) = [dR^(l-1) (x) R^(1)] + [R^(l-1) (x) dR^(1)]. */
+void e2fo_solid_harmonics_grad(int lmax, const double *v, double *out) {
+    int nk = (lmax + 1) * (lmax + 1);
+    double R[49], t1[13], t2[13];
+    e2fo_solid_harmonics(lmax, v, R);
+    for (int x = 0; x < 3; ++x) {
+        double *d = out + (size_t)x * nk;
+        d[0] = 0.0;
+        if (lmax < 1) continue;
+        /* R^(1) = (v_y, v_z, v_x) */
+        double d1[3] = {x == 1 ? 1.0 : 0.0, x == 2 ? 1.0 : 0.0, x == 0 ? 1.0 : 0.0};
+        double r1[3] = {v[1], v[2], v[0]};
+        d[1] = d1[0]; d[2] = d1[1]; d[3] = d1[2];
+        for (int l = 2; l <= lmax; ++l) {
+            couple(l - 1, d + (l - 1) * (l - 1), 1, r1, l, t1);
+            couple(l - 1, R + (l - 1) * (l - 1), 1, d1, l, t2);
+            for (int k = 0; k < 2 * l + 1; ++k) d[l * l + k] = t1[k] + t2[k];
+        }
+    }
+}
+
 /* ---------- Wigner 6j: Racah's single-sum formula ---------- */
 static long double delta_tri(int a, int b, int c) {
     return sqrtl(fact(a + b - c) * fact(a - b + c) * fact(-a + b + c) / fact(a + b + c + 1));
@@ -618,6 +641,88 @@ int e2fo_conv_edge_vjp(int L, int C, int H, const float *pos, const float *feat,
         free(trecv);
     }
     return 0;
+}
+
+/* ---------- gradient with respect to the positions (forces) ----------
+ * For the output gradient gy, the edge e = (i, j) with r = r_i - r_j carries
+ *   g_e[x] = sum_{o,m,c} gy_i[o,m,c] alpha_{e,h(c)} sum_{a,f} w_afo
+ *            sum_{ma,mf} C^{o m}_{a ma, f mf} h_j^(a)[ma,c] dR^(f)_mf(r)/dr_x,
+ * which adds to atom i and subtracts from atom j (r depends on r_i - r_j
+ * only).  out[r][x] for the atoms atoms[r] (all n in order if atoms is NULL):
+ * the sum over the edges of which the atom is receiver, minus the sum over
+ * those of which it is sender, each in ascending edge order. */
+static void edge_force(int L, int C, int H, const float *pos, const float *feat, const double *gy, int i, int j,
+                       int64_t e, const float *alpha, const double *path_w, double g[3]) {
+    const int nk = (L + 1) * (L + 1), dh = C / H;
+    double v[3] = {(double)pos[3 * i] - pos[3 * j], (double)pos[3 * i + 1] - pos[3 * j + 1],
+                   (double)pos[3 * i + 2] - pos[3 * j + 2]};
+    double dR[3 * 49];
+    e2fo_solid_harmonics_grad(L, v, dR);
+    const float *hj = feat + (size_t)j * nk * C;
+    const double *gyi = gy + (size_t)i * nk * C;
+    g[0] = g[1] = g[2] = 0.0;
+    for (int a = 0; a <= L; ++a)
+        for (int f = 0; f <= L; ++f)
+            for (int o = iabs_(a - f); o <= imin_(a + f, L); ++o) {
+                const double w = path_w[(a * (L + 1) + f) * (L + 1) + o];
+                if (w == 0.0) continue;
+                const double *c3 = cg(a, f, o);
+                for (int ma = 0; ma < 2 * a + 1; ++ma)
+                    for (int mf = 0; mf < 2 * f + 1; ++mf)
+                        for (int m = 0; m < 2 * o + 1; ++m) {
+                            const double cgv = c3[(ma * (2 * f + 1) + mf) * (2 * o + 1) + m];
+                            if (cgv == 0.0) continue;
+                            const float *hrow = hj + (size_t)(a * a + ma) * C;
+                            const double *grow = gyi + (size_t)(o * o + m) * C;
+                            double s = 0.0;
+                            for (int c = 0; c < C; ++c) s += (double)alpha[e * H + c / dh] * hrow[c] * grow[c];
+                            for (int x = 0; x < 3; ++x) g[x] += w * cgv * dR[x * nk + f * f + mf] * s;
+                        }
+            }
+}
+
+int e2fo_conv_edge_grad_pos(int L, int C, int H, const float *pos, const float *feat, const double *gy, int n,
+                            const int64_t *row_ptr, const int32_t *col_idx, const float *alpha, const double *path_w,
+                            const int32_t *atoms, int n_atoms, double *out) {
+    if (L < 0 || L > 6 || C < 1 || H < 1 || C % H) return 1;
+    const int64_t E = row_ptr[n];
+    warm_cg(L, L);
+    /* the edges of every sender, by ascending e */
+    int64_t *tptr = (int64_t *)calloc((size_t)n + 1, sizeof(int64_t));
+    int64_t *tedge = (int64_t *)malloc(sizeof(int64_t) * (size_t)(E > 0 ? E : 1));
+    int32_t *trecv = (int32_t *)malloc(sizeof(int32_t) * (size_t)(E > 0 ? E : 1));
+    int64_t *fill = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    if (!tptr || !tedge || !trecv || !fill) { free(tptr); free(tedge); free(trecv); free(fill); return 2; }
+    for (int64_t e = 0; e < E; ++e) tptr[col_idx[e] + 1]++;
+    for (int j = 0; j < n; ++j) tptr[j + 1] += tptr[j];
+    for (int j = 0; j < n; ++j) fill[j] = tptr[j];
+    for (int i = 0; i < n; ++i)
+        for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+            const int64_t t = fill[col_idx[e]]++;
+            tedge[t] = e;
+            trecv[t] = i;
+        }
+    free(fill);
+    const int na = atoms ? n_atoms : n;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 2)
+    for (int r = 0; r < na; ++r) {
+        const int a = atoms ? atoms[r] : r;
+        double *o3 = out + (size_t)r * 3;
+        o3[0] = o3[1] = o3[2] = 0.0;
+        if (a < 0 || a >= n) { bad = 1; continue; }
+        double g[3];
+        for (int64_t e = row_ptr[a]; e < row_ptr[a + 1]; ++e) {
+            edge_force(L, C, H, pos, feat, gy, a, col_idx[e], e, alpha, path_w, g);
+            for (int x = 0; x < 3; ++x) o3[x] += g[x];
+        }
+        for (int64_t t = tptr[a]; t < tptr[a + 1]; ++t) {
+            edge_force(L, C, H, pos, feat, gy, trecv[t], a, tedge[t], alpha, path_w, g);
+            for (int x = 0; x < 3; ++x) o3[x] -= g[x];
+        }
+    }
+    free(tptr); free(tedge); free(trecv);
+    return bad;
 }
 
 /* ---------- the layer by node factorisation (Thm. 3.3, Alg. 1) ----------

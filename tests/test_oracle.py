@@ -544,6 +544,50 @@ def test_y_norm_closed_forms():
     assert np.max(np.abs(a - o.conv_edge(L, H, pos, feat2, rp2, ci2, alpha2, w2))) > 1e-3 * np.max(np.abs(a))
 
 
+def test_solid_harmonics_gradient():
+    # central differences in float64, and Euler's identity for the
+    # homogeneous polynomials R^(l): sum_x v_x dR^(l)/dv_x = l R^(l)
+    L = 6
+    rng = np.random.default_rng(12)
+    for _ in range(5):
+        v = rng.uniform(-2.0, 2.0, size=3)
+        d = o.solid_harmonics_grad(L, v)
+        for x in range(3):
+            e = np.zeros(3)
+            e[x] = 1e-5
+            fd = (o.solid_harmonics(L, v + e) - o.solid_harmonics(L, v - e)) / 2e-5
+            assert np.allclose(d[x], fd, rtol=1e-7, atol=1e-7 * np.abs(fd).max())
+        deg = np.array([l for l in range(L + 1) for _ in range(2 * l + 1)], dtype=float)
+        assert np.allclose(v @ d, deg * o.solid_harmonics(L, v), rtol=1e-12, atol=1e-12)
+
+
+def test_forces_definition():
+    # the position gradient of sum(gy * layer) with the graph and alpha fixed:
+    # finite differences of the layer (actual float32 steps), zero net force
+    # (the layer depends on differences of positions), rotation covariance
+    L, H, C = 3, 2, 4
+    pos, rp, ci, feat, alpha, w = small_graph(L, 10, C, H, seed=31)
+    gy = np.random.default_rng(4).standard_normal((10, (L + 1) ** 2, C))
+    g = o.conv_edge_grad_pos(L, H, pos, feat, gy, rp, ci, alpha, w)
+    assert np.allclose(g.sum(0), 0.0, atol=1e-11 * np.abs(g).max())
+    loss = lambda p: float((gy * o.conv_edge(L, H, p, feat, rp, ci, alpha, w)).sum())
+    for a, x in ((0, 0), (3, 1), (7, 2), (9, 0)):
+        up, dn = pos.copy(), pos.copy()
+        up[a, x] = np.float32(pos[a, x] + np.float32(1e-3))
+        dn[a, x] = np.float32(pos[a, x] - np.float32(1e-3))
+        fd = (loss(up) - loss(dn)) / (float(up[a, x]) - float(dn[a, x]))
+        assert abs(fd - g[a, x]) <= 1e-5 * np.abs(g).max(), (a, x, fd, g[a, x])
+    sub = np.array([9, 2, 5], dtype=np.int32)
+    assert np.array_equal(o.conv_edge_grad_pos(L, H, pos, feat, gy, rp, ci, alpha, w, atoms=sub), g[sub])
+    Q = o.random_rotation(8)
+    D = o.wigner_d(L, Q)
+    rot = lambda t: np.concatenate([np.einsum("mn,inc->imc", D[l], t[:, l * l:(l + 1) ** 2]) for l in range(L + 1)], 1)
+    center = pos.astype(np.float64).mean(0)
+    pos_r = ((pos.astype(np.float64) - center) @ Q.T + center).astype(np.float32)
+    g_r = o.conv_edge_grad_pos(L, H, pos_r, rot(feat).astype(np.float32), rot(gy), rp, ci, alpha, w)
+    assert np.allclose(g_r, g @ Q.T, atol=2e-5 * np.abs(g).max())
+
+
 def test_layer_equivariance_and_translation():
     # Lemma (equivariance, App. E): rotating positions and features rotates
     # every output irrep by D^(o); a translation changes nothing.
