@@ -329,12 +329,14 @@ def main():
     # the backward of the timed forward (fp32 mixing): both products, then each alone
     g_out = torch.randn(out.shape, device=dev, generator=g)
 
-    def bwd(wf, wa):
+    def bwd(wf, wa, wp=False):
         return lambda: e2f.e2f_wigner6j_conv_backward(ctx, pos, feat, g_out, row_ptr, col, alpha, L, H, wl.cutoff,
-                                                      mix_w=mix_w, graph_id=gid, want_feat=wf, want_alpha=wa)
+                                                      mix_w=mix_w, graph_id=gid, want_feat=wf, want_alpha=wa,
+                                                      want_pos=wp)
 
-    bwd(True, True)()
-    ms_bwd = timed(bwd(True, True), args.steps)
+    bwd(True, True, True)()
+    ms_bwd = timed(bwd(True, True, True), args.steps)
+    ms_bwd_pos = timed(bwd(False, False, True), args.steps)
     ms_bwd_feat = timed(bwd(True, False), args.steps)
     ms_bwd_alpha = timed(bwd(False, True), args.steps)
     pairs, tiles = e2f.e2f_last_plan(ctx)
@@ -453,7 +455,8 @@ def main():
         "speedup_vs_edge_tp": ms_edge / ms_fwd,
         "fwd_bf16_mix": bf16_res,
         "neighbor_list_ms": ms_nl,
-        "backward": {"ms": ms_bwd, "grad_feat_ms": ms_bwd_feat, "grad_alpha_ms": ms_bwd_alpha},
+        "backward": {"ms": ms_bwd, "grad_feat_ms": ms_bwd_feat, "grad_alpha_ms": ms_bwd_alpha,
+                     "grad_pos_ms": ms_bwd_pos},
         "global_moment": {"ms": ms_glob, "pairs": n * n, "atoms_per_s": n / (ms_glob * 1e-3)},
         "attention": {"ms": ms_att, "dk": 16, "n_rbf": 8, "bytes_GBps": (E * (4 + 4 * H) + 12.0 * n) / (ms_att * 1e-3) / 1e9},
         "kernels": kernels,

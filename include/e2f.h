@@ -202,12 +202,19 @@ e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params*
  *     tables); the mixing contributes W^(o) transposed;
  *   grad_alpha [E][H]: per edge and head, the dot product of the unmixed
  *     output gradient of the receiver with the edge's message (the per-edge
- *     filter of the baseline); needs feat and C <= 256.
- * Either output may be NULL (not both).  Positions are not differentiated. */
+ *     filter of the baseline); needs feat and C <= 256;
+ *   grad_pos [N][3]: the gradient with respect to the positions (the graph
+ *     and alpha held fixed; forces are its negative).  Per edge (i, j) the
+ *     message depends on r_i - r_j only, through R^(f); its derivative uses
+ *     the gradient of the solid harmonics, and the edge's vector adds to i and
+ *     subtracts from j (per atom in a fixed order: deterministic); needs feat
+ *     and C <= 256.
+ * Any of the outputs may be NULL (not all).  Not available with y_norm. */
 e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
                                       const int32_t* graph_id, const float* feat, const float* grad_out, int32_t n,
                                       const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges,
-                                      const float* alpha, float* grad_feat, float* grad_alpha, void* stream);
+                                      const float* alpha, float* grad_feat, float* grad_alpha, float* grad_pos,
+                                      void* stream);
 
 /* The conventional per-edge SO(3) convolution (Def. 3.1): the same layer
  * computed edge by edge with R^(f)(r_i - r_j) and the CG product per edge.

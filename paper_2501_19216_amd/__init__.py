@@ -82,7 +82,7 @@ def _load():
     L.e2f_wigner6j_conv_forward_dense.restype = i
     L.e2f_wigner6j_conv_forward_global.argtypes = [p, ctypes.POINTER(ConvParams), p, p, i32, p, p]
     L.e2f_wigner6j_conv_forward_global.restype = i
-    L.e2f_wigner6j_conv_backward.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, p, i32, p, p, i64, p, p, p, p]
+    L.e2f_wigner6j_conv_backward.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, p, i32, p, p, i64, p, p, p, p, p]
     L.e2f_wigner6j_conv_backward.restype = i
     return L
 
@@ -344,9 +344,10 @@ def e2f_wigner6j_conv_forward_global(ctx, pos, feat, lmax, heads, cutoff, path_w
 
 
 def e2f_wigner6j_conv_backward(ctx, pos, feat, grad_out, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None,
-                               mix_w=None, graph_id=None, tile_side=0.0, want_feat=True, want_alpha=True):
-    """Vector-Jacobian products of the forward: (grad_feat [N,(L+1)^2,C] or
-    None, grad_alpha [E,H] or None)."""
+                               mix_w=None, graph_id=None, tile_side=0.0, want_feat=True, want_alpha=True,
+                               want_pos=False):
+    """Vector-Jacobian products of the forward: (grad_feat [N,(L+1)^2,C],
+    grad_alpha [E,H], grad_pos [N,3]), each None unless requested."""
     for t, name in ((pos, "pos"), (feat, "feat"), (grad_out, "grad_out"), (alpha, "alpha")):
         _dev(t, torch.float32, name)
     _dev(row_ptr, torch.int64, "row_ptr")
@@ -356,13 +357,14 @@ def e2f_wigner6j_conv_backward(ctx, pos, feat, grad_out, row_ptr, col_idx, alpha
     E = col_idx.numel()
     gf = torch.empty_like(grad_out) if want_feat else None
     ga = torch.empty(E, heads, dtype=torch.float32, device=grad_out.device) if want_alpha else None
+    gp = torch.empty(n, 3, dtype=torch.float32, device=grad_out.device) if want_pos else None
     prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side)
     st = lib.e2f_wigner6j_conv_backward(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(graph_id), _ptr(feat),
                                         _ptr(grad_out), n, _ptr(row_ptr), _ptr(col_idx), E, _ptr(alpha), _ptr(gf),
-                                        _ptr(ga), _stream(grad_out.device))
+                                        _ptr(ga), _ptr(gp), _stream(grad_out.device))
     del keep
     _check(st, "e2f_wigner6j_conv_backward")
-    return gf, ga
+    return gf, ga, gp
 
 
 def e2f_profile(ctx: Context, enable: bool) -> None:

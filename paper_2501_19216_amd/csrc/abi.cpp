@@ -890,13 +890,15 @@ e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, cons
 e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos,
                                       const int32_t* graph_id, const float* feat, const float* grad_out, int32_t n,
                                       const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges,
-                                      const float* alpha, float* grad_feat, float* grad_alpha, void* stream) {
-  if (!grad_feat && !grad_alpha) return fail(E2F_EINVAL, "neither grad_feat nor grad_alpha is requested");
-  if (grad_alpha && n > 0 && !feat) return fail(E2F_EINVAL, "feat is required for grad_alpha");
+                                      const float* alpha, float* grad_feat, float* grad_alpha, float* grad_pos,
+                                      void* stream) {
+  if (!grad_feat && !grad_alpha && !grad_pos) return fail(E2F_EINVAL, "no gradient is requested");
+  if ((grad_alpha || grad_pos) && n > 0 && !feat) return fail(E2F_EINVAL, "feat is required for grad_alpha and grad_pos");
   e2f_status rs = check_params(ctx, p);
   if (rs != E2F_OK) return rs;
   if (p->y_norm) return fail(E2F_EUNSUPPORTED, "y_norm: the backward covers the plain layer only");
-  if (grad_alpha && p->channels > 256) return fail(E2F_EUNSUPPORTED, "grad_alpha needs channels <= 256");
+  if ((grad_alpha || grad_pos) && p->channels > 256)
+    return fail(E2F_EUNSUPPORTED, "grad_alpha and grad_pos need channels <= 256");
   rs = check_conv(ctx, p, pos, grad_out, n, row_ptr, col_idx, n_edges, const_cast<float*>(grad_out));
   if (rs != E2F_OK) return rs;
   hipStream_t s = (hipStream_t)stream;
@@ -909,11 +911,12 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
   const bool mixing = p->mix_w != nullptr;
   const size_t wt_bytes = (size_t)L1 * C * C * (p->mix_dtype == E2F_BF16 ? 2 : 4);
   const size_t tmp_b = transpose_tmp_bytes(n, n_edges);
-  const bool want_t = grad_feat != nullptr && n_edges > 0;
+  const bool want_t = (grad_feat != nullptr || grad_pos != nullptr) && n_edges > 0;
   const size_t need = (mixing ? al256(sizeof(float) * (size_t)n * nk * C) + al256(wt_bytes) : 0) +
                       (want_t ? 5 * al256(sizeof(int32_t) * (size_t)n_edges) + 2 * al256(sizeof(int64_t) * (n + 1)) +
                                     al256(sizeof(float) * (size_t)n_edges * H) + al256(tmp_b)
-                              : 0) + 256;
+                              : 0) +
+                      (grad_pos ? al256(sizeof(float) * (size_t)n_edges * 3) : 0) + 256;
   rs = ensure(ctx, ctx->d, need, s);
   if (rs != E2F_OK) return rs;
   Carver cd{(char*)ctx->d.p};
@@ -930,13 +933,38 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
   if (grad_alpha && n_edges > 0)
     E2F_TIMED("edge_vjp_alpha", launch_edge_vjp_alpha(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, n, C, H,
                                                       grad_alpha, s));
+  if (n_edges == 0) {
+    if (grad_pos) E2F_HIP(hipMemsetAsync(grad_pos, 0, sizeof(float) * (size_t)n * 3, s));
+    if (grad_feat) E2F_HIP(hipMemsetAsync(grad_feat, 0, sizeof(float) * (size_t)n * nk * C, s));
+    return E2F_OK;
+  }
+  // ---- the transposed graph (senders' rows), for the features and the positions
+  int32_t* perm = nullptr;
+  int32_t* colT = nullptr;
+  int64_t* rowT = nullptr;
+  float* alphaT = nullptr;
+  if (want_t) {
+    int32_t* rows = cd.take<int32_t>((size_t)n_edges);
+    int32_t* iota = cd.take<int32_t>((size_t)n_edges);
+    int32_t* keys_out = cd.take<int32_t>((size_t)n_edges);
+    perm = cd.take<int32_t>((size_t)n_edges);
+    colT = cd.take<int32_t>((size_t)n_edges);
+    int64_t* cnt = cd.take<int64_t>((size_t)n + 1);
+    rowT = cd.take<int64_t>((size_t)n + 1);
+    alphaT = cd.take<float>((size_t)n_edges * H);
+    void* tmp = cd.take<char>(tmp_b);
+    E2F_TIMED("transpose", launch_transpose_graph(row_ptr, col_idx, alpha, n, n_edges, H, rows, iota, keys_out, perm,
+                                                  cnt, rowT, colT, alpha ? alphaT : nullptr, tmp, tmp_b, s));
+  }
+  // ---- positions: per-edge force vectors, then per atom received minus sent
+  if (grad_pos) {
+    float* gedge = cd.take<float>((size_t)n_edges * 3);
+    E2F_TIMED("edge_force", launch_edge_force(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, alpha, n, C, H, gedge, s));
+    E2F_TIMED("edge_force", launch_force_gather(row_ptr, rowT, perm, gedge, n, grad_pos, s));
+  }
   // ---- features: the same layer on the transposed graph, input degree o,
   // output degree a, weights w[a][f][o] kappa(a,f,o) (-1)^f
   if (grad_feat) {
-    if (n_edges == 0) {
-      E2F_HIP(hipMemsetAsync(grad_feat, 0, sizeof(float) * (size_t)n * nk * C, s));
-      return E2F_OK;
-    }
     const std::vector<double>* kap = nullptr;
     rs = transpose_factors(ctx, L, kap);
     if (rs != E2F_OK) return rs;
@@ -947,17 +975,6 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
           const size_t q = ((size_t)a * L1 + f) * L1 + o;
           wt[((size_t)o * L1 + f) * L1 + a] = w[q] * (*kap)[q] * ((f & 1) ? -1.0 : 1.0);
         }
-    int32_t* rows = cd.take<int32_t>((size_t)n_edges);
-    int32_t* iota = cd.take<int32_t>((size_t)n_edges);
-    int32_t* keys_out = cd.take<int32_t>((size_t)n_edges);
-    int32_t* perm = cd.take<int32_t>((size_t)n_edges);
-    int32_t* colT = cd.take<int32_t>((size_t)n_edges);
-    int64_t* cnt = cd.take<int64_t>((size_t)n + 1);
-    int64_t* rowT = cd.take<int64_t>((size_t)n + 1);
-    float* alphaT = cd.take<float>((size_t)n_edges * H);
-    void* tmp = cd.take<char>(tmp_b);
-    E2F_TIMED("transpose", launch_transpose_graph(row_ptr, col_idx, alpha, n, n_edges, H, rows, iota, keys_out, perm,
-                                                  cnt, rowT, colT, alpha ? alphaT : nullptr, tmp, tmp_b, s));
     e2f_conv_params pt = *p;
     pt.path_w = wt.data();
     pt.mix_w = nullptr;

@@ -40,6 +40,27 @@ __device__ __forceinline__ F sh_poly(const DevTables& t, int k, F x, F y, F z) {
   return acc;
 }
 
+// Gradient of one solid harmonic from its monomials: d/dx of c x^a y^b z^e
+// is c a x^(a-1) y^b z^e (no term when a = 0).
+template <typename F>
+__device__ __forceinline__ void sh_poly_grad(const DevTables& t, int k, F x, F y, F z, F& gx, F& gy, F& gz) {
+  auto ipow = [](F b, int n) {
+    F r = 1;
+    for (int q = 0; q < n; ++q) r *= b;
+    return r;
+  };
+  gx = 0, gy = 0, gz = 0;
+  for (int e = t.sh_ptr[k]; e < t.sh_ptr[k + 1]; ++e) {
+    const int pw = t.sh_pow[e];
+    const int ex = pw & 15, ey = (pw >> 4) & 15, ez = (pw >> 8) & 15;
+    const F c = (F)t.sh_coef[e];
+    const F X = ipow(x, ex), Y = ipow(y, ey), Z = ipow(z, ez);
+    if (ex) gx += c * (F)ex * ipow(x, ex - 1) * Y * Z;
+    if (ey) gy += c * (F)ey * X * ipow(y, ey - 1) * Z;
+    if (ez) gz += c * (F)ez * X * Y * ipow(z, ez - 1);
+  }
+}
+
 __global__ void k_sh(DevTables t, const float* __restrict__ pos, const int32_t* __restrict__ node_of,
                      const double* __restrict__ origins_d, const float* __restrict__ origins_f,
                      const int32_t* __restrict__ origin_id, int origin_mod, int n, double* __restrict__ out_d,
@@ -937,6 +958,111 @@ __global__ __launch_bounds__(256) void k_edge_vjp_alpha(DevTables t, const float
   }
 }
 
+// Gradient with respect to the positions: per edge e = (i, j), r = r_i - r_j,
+//   g_e[x] = sum_c alpha_{e,h(c)} sum_{k,q} gy_i[k][c] (dK_e/dr_x)[k][q] h_j[q][c],
+// with dK_e/dr_x the edge filter of the baseline built from the gradient of
+// the solid harmonics (three filters per edge in LDS).  One thread per
+// channel; the sum over channels runs by wave shuffles, then over the waves
+// in order (deterministic).  The per-atom sums follow in k_force_gather.
+template <int L, int EB>
+__global__ __launch_bounds__(256) void k_edge_force(DevTables t, const float* __restrict__ pos,
+                                                    const float* __restrict__ feat, const float* __restrict__ gy,
+                                                    const int64_t* __restrict__ row_ptr,
+                                                    const int32_t* __restrict__ col, const float* __restrict__ alpha,
+                                                    int C, int H, float* __restrict__ gedge) {
+  constexpr int NK = (L + 1) * (L + 1);
+  extern __shared__ float sm[];
+  float* dK = sm;                      // [3][EB][NK*NK]
+  float* dR = dK + 3 * EB * NK * NK;   // [3][EB][NK]
+  float* red = dR + 3 * EB * NK;       // [EB*3][waves]
+  const int i = blockIdx.x;
+  const int dh = C / H;
+  const int c = threadIdx.x;
+  const bool live = c < C;
+  const int nw = blockDim.x >> 6, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+  const float xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
+  float g[NK];
+#pragma unroll
+  for (int k = 0; k < NK; ++k) g[k] = live ? gy[((size_t)i * NK + k) * C + c] : 0.0f;
+  for (int64_t eb = e0; eb < e1; eb += EB) {
+    const int nb = (e1 - eb) < EB ? (int)(e1 - eb) : EB;
+    __syncthreads();
+    for (int q = threadIdx.x; q < nb * NK; q += blockDim.x) {
+      const int b = q / NK, k = q % NK;
+      const int j = col[eb + b];
+      float gx, gyy, gz;
+      sh_poly_grad<float>(t, k, xi - pos[3 * j], yi - pos[3 * j + 1], zi - pos[3 * j + 2], gx, gyy, gz);
+      dR[(0 * EB + b) * NK + k] = gx;
+      dR[(1 * EB + b) * NK + k] = gyy;
+      dR[(2 * EB + b) * NK + k] = gz;
+    }
+    __syncthreads();
+    for (int q = threadIdx.x; q < 3 * nb * NK * NK; q += blockDim.x) {
+      const int xb = q / (NK * NK), s = q % (NK * NK);  // xb = x * nb + b
+      const int x = xb / nb, b = xb % nb;
+      const float* Rb = dR + (x * EB + b) * NK;
+      float v = 0.0f;
+      for (int e = t.k_ptr[s]; e < t.k_ptr[s + 1]; ++e) v += t.k_coef[e] * Rb[t.k_ridx[e]];
+      dK[(x * EB + b) * NK * NK + s] = v;
+    }
+    __syncthreads();
+    for (int b = 0; b < nb; ++b) {
+      float v0 = 0.0f, v1 = 0.0f, v2 = 0.0f;
+      if (live) {
+        const int j = col[eb + b];
+        const float* K0 = dK + (0 * EB + b) * NK * NK;
+        const float* K1 = dK + (1 * EB + b) * NK * NK;
+        const float* K2 = dK + (2 * EB + b) * NK * NK;
+        for (int q = 0; q < NK; ++q) {
+          float u0 = 0.0f, u1 = 0.0f, u2 = 0.0f;
+#pragma unroll
+          for (int k = 0; k < NK; ++k) {
+            u0 += g[k] * K0[k * NK + q];
+            u1 += g[k] * K1[k * NK + q];
+            u2 += g[k] * K2[k * NK + q];
+          }
+          const float hv = feat[((size_t)j * NK + q) * C + c];
+          v0 += u0 * hv, v1 += u1 * hv, v2 += u2 * hv;
+        }
+        const float a = alpha ? alpha[(eb + b) * H + c / dh] : 1.0f;
+        v0 *= a, v1 *= a, v2 *= a;
+      }
+      // every lane of every wave takes the same shuffle steps
+      for (int o = 32; o > 0; o >>= 1) {
+        v0 += __shfl_xor(v0, o);
+        v1 += __shfl_xor(v1, o);
+        v2 += __shfl_xor(v2, o);
+      }
+      if (lane == 0) {
+        red[(b * 3 + 0) * nw + wave] = v0;
+        red[(b * 3 + 1) * nw + wave] = v1;
+        red[(b * 3 + 2) * nw + wave] = v2;
+      }
+    }
+    __syncthreads();
+    for (int q = threadIdx.x; q < nb * 3; q += blockDim.x) {
+      float sum = 0.0f;
+      for (int w = 0; w < nw; ++w) sum += red[q * nw + w];
+      gedge[(eb + q / 3) * 3 + q % 3] = sum;
+    }
+  }
+}
+
+// Per atom a: the forces of the edges it receives minus those it sends,
+// each in ascending order (the sent edges through the transposed graph).
+__global__ void k_force_gather(const int64_t* __restrict__ row_ptr, const int64_t* __restrict__ rowT,
+                               const int32_t* __restrict__ perm, const float* __restrict__ gedge, int n,
+                               float* __restrict__ gpos) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= (int64_t)n * 3) return;
+  const int a = (int)(q / 3), x = (int)(q % 3);
+  float s = 0.0f;
+  for (int64_t e = row_ptr[a]; e < row_ptr[a + 1]; ++e) s += gedge[e * 3 + x];
+  for (int64_t t = rowT[a]; t < rowT[a + 1]; ++t) s -= gedge[(int64_t)perm[t] * 3 + x];
+  gpos[q] = s;
+}
+
 // transposed graph: rows[e] = receiver of edge e; counts of every sender
 __global__ void k_edge_rows(const int64_t* __restrict__ row_ptr, int n, int32_t* __restrict__ rows) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -1462,6 +1588,35 @@ hipError_t launch_iota(int n, int32_t* v, hipStream_t s) {
 hipError_t launch_plan_pack(const int32_t* pidx, const int32_t* flags, int64_t count, const int32_t* max_degree,
                             const int32_t* rstart, const int32_t* pstart, int keys, int32_t* out, hipStream_t s) {
   k_plan_pack<<<(keys + 256) / 256, 256, 0, s>>>(pidx, flags, count, max_degree, rstart, pstart, keys, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_force(const DevTables& t, const float* pos, const float* feat, const float* gy,
+                             const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n, int C, int H,
+                             float* gedge, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  if (C > 256) return hipErrorInvalidValue;
+  const int threads = (C + 63) / 64 * 64;
+  const int eb = t.L <= 4 ? 4 : 2;
+  const size_t lds =
+      sizeof(float) * ((size_t)3 * eb * t.nk * t.nk + (size_t)3 * eb * t.nk + (size_t)eb * 3 * (threads / 64));
+  switch (t.L) {
+#define E2F_CASE(LL, EB_)                                                                                   \
+  case LL:                                                                                                  \
+    if (hipError_t e = allow_lds(k_edge_force<LL, EB_>, lds); e != hipSuccess) return e;                    \
+    k_edge_force<LL, EB_><<<n, threads, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx, alpha, C, H, gedge);  \
+    break;
+    E2F_CASE(0, 4) E2F_CASE(1, 4) E2F_CASE(2, 4) E2F_CASE(3, 4) E2F_CASE(4, 4) E2F_CASE(5, 2) E2F_CASE(6, 2)
+#undef E2F_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_force_gather(const int64_t* row_ptr, const int64_t* rowT, const int32_t* perm, const float* gedge,
+                               int n, float* gpos, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  k_force_gather<<<(unsigned)(((int64_t)n * 3 + 255) / 256), 256, 0, s>>>(row_ptr, rowT, perm, gedge, n, gpos);
   return hipGetLastError();
 }
 

@@ -121,6 +121,13 @@ hipError_t launch_attention(const float* pos, const float* q, const float* k, in
 
 // ---- backward
 // galpha[e][h] = sum_{c of h} <gy_i[.][c], (K_e h_j)[.][c]> for the edges of rows 0..n-1 (C <= 256)
+// Position gradient: gedge [E][3] per edge (C <= 256), then per atom the
+// edges it receives minus those it sends (rowT, perm: the transposed graph).
+hipError_t launch_edge_force(const DevTables& t, const float* pos, const float* feat, const float* gy,
+                             const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n, int C, int H,
+                             float* gedge, hipStream_t s);
+hipError_t launch_force_gather(const int64_t* row_ptr, const int64_t* rowT, const int32_t* perm, const float* gedge,
+                               int n, float* gpos, hipStream_t s);
 hipError_t launch_edge_vjp_alpha(const DevTables& t, const float* pos, const float* feat, const float* gy,
                                  const int64_t* row_ptr, const int32_t* col_idx, int n, int C, int H, float* galpha,
                                  hipStream_t s);

@@ -145,14 +145,17 @@ def test_other_argument_checks(e2f):
     assert att(q=None) == e2f.E2F_EINVAL
     assert att(w=None) == e2f.E2F_EINVAL
     assert att(dk=0, R=0, q=None, w=None) == e2f.E2F_EDEVICE
-    bwd = lambda prm, gf=FAKE, ga=FAKE, feat=FAKE: lib.e2f_wigner6j_conv_backward(
-        ctx.handle, ctypes.byref(prm), FAKE, None, feat, FAKE, 10, FAKE, FAKE, 30, None, gf, ga, None)
+    bwd = lambda prm, gf=FAKE, ga=FAKE, gp=None, feat=FAKE: lib.e2f_wigner6j_conv_backward(
+        ctx.handle, ctypes.byref(prm), FAKE, None, feat, FAKE, 10, FAKE, FAKE, 30, None, gf, ga, gp, None)
     assert bwd(_params(e2f)) == e2f.E2F_EDEVICE
     assert bwd(_params(e2f), gf=None, ga=None) == e2f.E2F_EINVAL
     assert bwd(_params(e2f, y_norm=1)) == e2f.E2F_EUNSUPPORTED
     assert bwd(_params(e2f), feat=None) == e2f.E2F_EINVAL  # grad_alpha needs the features
     assert bwd(_params(e2f, channels=512, heads=8)) == e2f.E2F_EUNSUPPORTED
     assert bwd(_params(e2f, channels=512, heads=8), ga=None) == e2f.E2F_EDEVICE
+    assert bwd(_params(e2f), gf=None, ga=None, gp=FAKE) == e2f.E2F_EDEVICE
+    assert bwd(_params(e2f), gf=None, ga=None, gp=FAKE, feat=None) == e2f.E2F_EINVAL  # forces need the features
+    assert bwd(_params(e2f, channels=512, heads=8), ga=None, gp=FAKE) == e2f.E2F_EUNSUPPORTED
     h = ctypes.c_void_p()
     assert lib.e2f_create(7, -1, ctypes.byref(h)) == e2f.E2F_EINVAL
     assert lib.e2f_create(3, -2, ctypes.byref(h)) == e2f.E2F_EINVAL

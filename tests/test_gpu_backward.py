@@ -1,6 +1,6 @@
 """GPU backward of the Wigner-6j convolution (vector-Jacobian products with
-respect to the features and the attention weights) against the oracle's
-products by the definition of the layer.  Run with -m gpu."""
+respect to the features, the attention weights and the positions) against
+the oracle's products by the definition of the layer.  Run with -m gpu."""
 import itertools
 
 import numpy as np
@@ -59,12 +59,20 @@ def check(e2f, ctx, pos, rp, ci, L, C, H, cutoff, seed, mix=None, bf16=False, gi
         gy = o.mix(L, gy, np.transpose(m, (0, 2, 1)))
         mw = gpu(mix).to(torch.bfloat16) if bf16 else gpu(mix)
     gf_ref, ga_ref = o.conv_edge_vjp(L, H, pos, feat, gy, rp, ci, alpha, w)
-    gf, ga = e2f.e2f_wigner6j_conv_backward(ctx, gpu(pos), gpu(feat), gpu(gout), gpu(rp), gpu(ci), gpu(alpha), L, H,
-                                            cutoff, mix_w=mw, graph_id=gpu(gid))
+    atoms = np.linspace(0, n - 1, min(n, 48)).astype(np.int32)
+    gp_ref = o.conv_edge_grad_pos(L, H, pos, feat, gy, rp, ci, alpha, w, atoms=atoms)
+    print("n %d L %d C %d: case" % (n, L, C), flush=True)
+    gf, ga, gp = e2f.e2f_wigner6j_conv_backward(ctx, gpu(pos), gpu(feat), gpu(gout), gpu(rp), gpu(ci), gpu(alpha), L,
+                                                H, cutoff, mix_w=mw, graph_id=gpu(gid), want_pos=True)
     ef = o.max_rel_err(gf.cpu().numpy(), gf_ref, L)
     ea = head_err(ga.cpu().numpy(), ga_ref)
-    print("n %d L %d C %d mix %s bf16 %s: grad_feat %.3e grad_alpha %.3e" % (n, L, C, mix is not None, bf16, ef, ea))
-    assert ef <= tol and ea <= tol
+    gp = gp.cpu().numpy()
+    ep = float(np.abs(gp[atoms] - gp_ref).max() / np.abs(gp_ref).max())
+    print("n %d L %d C %d mix %s bf16 %s: grad_feat %.3e grad_alpha %.3e grad_pos %.3e"
+          % (n, L, C, mix is not None, bf16, ef, ea, ep))
+    assert ef <= tol and ea <= tol and ep <= tol
+    # the layer depends on differences of positions: the gradient sums to zero
+    assert np.abs(gp.astype(np.float64).sum(0)).max() <= 1e-4 * np.abs(gp).max() * np.sqrt(n)
     return feat, alpha, gout, w, gf_ref, ga_ref
 
 
@@ -99,10 +107,16 @@ def test_backward_graphs_and_single_outputs(e2f, ctx):
     rp, ci = o.neighbor_list(inp.pos, 5.0, inp.graph_id)
     feat, alpha, gout, w, gf_ref, ga_ref = check(e2f, ctx, inp.pos, rp, ci, 3, 32, 8, 5.0, 6, gid=inp.graph_id)
     args = (gpu(inp.pos), gpu(feat), gpu(gout), gpu(rp), gpu(ci), gpu(alpha), 3, 8, 5.0)
-    gf, ga = e2f.e2f_wigner6j_conv_backward(ctx, *args, graph_id=gpu(inp.graph_id), want_alpha=False)
+    gf, ga, _ = e2f.e2f_wigner6j_conv_backward(ctx, *args, graph_id=gpu(inp.graph_id), want_alpha=False)
     assert ga is None and o.max_rel_err(gf.cpu().numpy(), gf_ref, 3) <= TOL_F32
-    gf, ga = e2f.e2f_wigner6j_conv_backward(ctx, *args, graph_id=gpu(inp.graph_id), want_feat=False)
+    gf, ga, _ = e2f.e2f_wigner6j_conv_backward(ctx, *args, graph_id=gpu(inp.graph_id), want_feat=False)
     assert gf is None and head_err(ga.cpu().numpy(), ga_ref) <= TOL_F32
+    gf, ga, gp = e2f.e2f_wigner6j_conv_backward(ctx, *args, graph_id=gpu(inp.graph_id), want_feat=False,
+                                                want_alpha=False, want_pos=True)
+    at = np.arange(0, 1200, 37, dtype=np.int32)
+    gp_ref = o.conv_edge_grad_pos(3, 8, inp.pos, feat, gout.astype(np.float64), rp, ci, alpha, w, atoms=at)
+    assert gf is None and ga is None
+    assert np.abs(gp.cpu().numpy()[at] - gp_ref).max() <= TOL_F32 * np.abs(gp_ref).max()
 
 
 def test_backward_protein_sampled(e2f, ctx):
@@ -112,14 +126,18 @@ def test_backward_protein_sampled(e2f, ctx):
     wl = inp.workload
     rng = np.random.default_rng(2)
     gout = rng.standard_normal(inp.feat.shape).astype(np.float32)
-    gf, ga = e2f.e2f_wigner6j_conv_backward(ctx, gpu(inp.pos), gpu(inp.feat), gpu(gout), gpu(rp), gpu(ci),
-                                            gpu(alpha), wl.lmax, wl.heads, wl.cutoff)
-    gf, ga = gf.cpu().numpy(), ga.cpu().numpy()
+    gf, ga, gp = e2f.e2f_wigner6j_conv_backward(ctx, gpu(inp.pos), gpu(inp.feat), gpu(gout), gpu(rp), gpu(ci),
+                                                gpu(alpha), wl.lmax, wl.heads, wl.cutoff, want_pos=True)
+    gf, ga, gp = gf.cpu().numpy(), ga.cpu().numpy(), gp.cpu().numpy()
     r = sample_rows(inp.pos.shape[0], 24, seed=4)
     gf_ref, ga_ref = o.conv_edge_vjp(wl.lmax, wl.heads, inp.pos, inp.feat, gout.astype(np.float64), rp, ci, alpha,
                                      inp.path_w, alpha_rows=r, feat_rows=r)
     ef = o.max_rel_err(gf[r], gf_ref[r], wl.lmax)
     ee = np.concatenate([np.arange(rp[i], rp[i + 1]) for i in r])
     ea = head_err(ga[ee], ga_ref[ee])
-    print("protein: grad_feat %.3e grad_alpha %.3e" % (ef, ea))
-    assert ef <= TOL_F32 and ea <= TOL_F32
+    rq = r[:12]
+    gp_ref = o.conv_edge_grad_pos(wl.lmax, wl.heads, inp.pos, inp.feat, gout.astype(np.float64), rp, ci, alpha,
+                                  inp.path_w, atoms=rq)
+    ep = float(np.abs(gp[rq] - gp_ref).max() / np.abs(gp_ref).max())
+    print("protein: grad_feat %.3e grad_alpha %.3e grad_pos %.3e" % (ef, ea, ep))
+    assert ef <= TOL_F32 and ea <= TOL_F32 and ep <= TOL_F32
