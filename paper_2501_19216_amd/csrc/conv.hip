@@ -112,10 +112,15 @@ __global__ void k_pair_flags(const int64_t* __restrict__ row_ptr, const int32_t*
                              const int32_t* __restrict__ tile_of, int n, int32_t* __restrict__ flags,
                              int32_t* __restrict__ max_degree) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  atomicMax(max_degree, (int32_t)(row_ptr[i + 1] - row_ptr[i]));
-  const int64_t base = (int64_t)tile_of[i] * n;
-  for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) flags[base + col[e]] = 1;
+  int deg = 0;
+  if (i < n) {
+    deg = (int)(row_ptr[i + 1] - row_ptr[i]);
+    const int64_t base = (int64_t)tile_of[i] * n;
+    for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) flags[base + col[e]] = 1;
+  }
+  // largest degree: wave maximum, one atomic per wave
+  for (int o = 32; o > 0; o >>= 1) deg = max(deg, __shfl_xor(deg, o));
+  if ((threadIdx.x & 63) == 0) atomicMax(max_degree, deg);
 }
 
 __global__ void k_pairs(const int32_t* __restrict__ flags, const int32_t* __restrict__ pidx, int64_t count, int n,
@@ -138,9 +143,23 @@ __global__ void k_col_pair(const int64_t* __restrict__ row_ptr, const int32_t* _
 
 // Per tile key: number of receivers (for their range in the receiver order)
 // and first pair index (pidx at the key's first flag).
-__global__ void k_key_counts(const int32_t* __restrict__ tile_of, int n, int32_t* __restrict__ counts) {
+// With few keys the workgroup counts in LDS and adds its nonzero bins once.
+constexpr int kKeyBins = 4096;
+template <bool LDS_BINS>
+__global__ __launch_bounds__(256) void k_key_counts(const int32_t* __restrict__ tile_of, int n, int keys,
+                                                    int32_t* __restrict__ counts) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) atomicAdd(&counts[tile_of[i]], 1);
+  if (!LDS_BINS) {
+    if (i < n) atomicAdd(&counts[tile_of[i]], 1);
+    return;
+  }
+  __shared__ int32_t bins[kKeyBins];
+  for (int q = threadIdx.x; q < keys; q += blockDim.x) bins[q] = 0;
+  __syncthreads();
+  if (i < n) atomicAdd(&bins[tile_of[i]], 1);
+  __syncthreads();
+  for (int q = threadIdx.x; q < keys; q += blockDim.x)
+    if (bins[q]) atomicAdd(&counts[q], bins[q]);
 }
 
 __global__ void k_key_pstart(const int32_t* __restrict__ pidx, int keys, int n, int32_t* __restrict__ pstart) {
@@ -1347,7 +1366,10 @@ hipError_t launch_tile_ranges(const int32_t* tile_of, const int32_t* pidx, int n
                               int32_t* rstart, int32_t* pstart, void* tmp, size_t tmp_bytes, hipStream_t s) {
   hipError_t e = hipMemsetAsync(counts, 0, sizeof(int32_t) * (size_t)(keys + 1), s);
   if (e != hipSuccess) return e;
-  if (n > 0) k_key_counts<<<(n + 255) / 256, 256, 0, s>>>(tile_of, n, counts);
+  if (n > 0) {
+    if (keys <= kKeyBins) k_key_counts<true><<<(n + 255) / 256, 256, 0, s>>>(tile_of, n, keys, counts);
+    else k_key_counts<false><<<(n + 255) / 256, 256, 0, s>>>(tile_of, n, keys, counts);
+  }
   size_t b = tmp_bytes;
   if ((e = hipcub::DeviceScan::ExclusiveSum(tmp, b, counts, rstart, keys + 1, s)) != hipSuccess) return e;
   k_key_pstart<<<(keys + 255) / 256, 256, 0, s>>>(pidx, keys, n, pstart);

@@ -9,6 +9,8 @@
 #include <hip/hip_runtime.h>
 #include <hipcub/hipcub.hpp>
 
+#include <algorithm>
+
 #include "e2f_launch.h"
 
 namespace e2f {
@@ -195,10 +197,7 @@ __global__ __launch_bounds__(64) void k_neighbors_wave(const float* __restrict__
     found += __popcll(m);
   }
   if (!WRITE) {
-    if (lane == 0) {
-      counts[i] = found;
-      atomicMax(max_degree, found);
-    }
+    if (lane == 0) counts[i] = found;
     return;
   }
   __syncthreads();
@@ -224,6 +223,20 @@ __global__ __launch_bounds__(64) void k_neighbors_wave(const float* __restrict__
 }
 
 __global__ void k_zero_last(int64_t* counts, int n) { counts[n] = 0; }
+
+// Largest row length: a maximum per workgroup (wave shuffles, then the four
+// waves through LDS), one atomic per workgroup.
+__global__ __launch_bounds__(256) void k_degree_max(const int64_t* __restrict__ counts, int n,
+                                                    int* __restrict__ max_degree) {
+  __shared__ int wmax[4];
+  int m = 0;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    m = max(m, (int)counts[i]);
+  for (int o = 32; o > 0; o >>= 1) m = max(m, __shfl_xor(m, o));
+  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) atomicMax(max_degree, max(max(wmax[0], wmax[1]), max(wmax[2], wmax[3])));
+}
 
 // ---------------------------------------------------------------- kNN graph
 // k nearest neighbours (the sparse graphs of the scaling study, Sec. 4.1):
@@ -411,6 +424,7 @@ hipError_t launch_nl_count(const float* pos, const int32_t* graph_id, int n, dou
   if ((e = hipMemsetAsync(max_degree, 0, sizeof(int), st)) != hipSuccess) return e;
   k_neighbors_wave<false><<<n, 64, 0, st>>>(pos, graph_id, n, r2, g, s.cell_of, s.cell_start, s.members, s.counts,
                                             max_degree, nullptr, nullptr);
+  k_degree_max<<<std::min((n + 255) / 256, 256), 256, 0, st>>>(s.counts, n, max_degree);
   k_zero_last<<<1, 1, 0, st>>>(s.counts, n);
   tb = s.scan_bytes;
   e = hipcub::DeviceScan::ExclusiveSum(s.scan_tmp, tb, s.counts, row_ptr, n + 1, st);
