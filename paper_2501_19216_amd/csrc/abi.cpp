@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <cstring>
 #include <limits>
+#include <map>
 #include <string>
 #include <vector>
 
@@ -72,6 +73,13 @@ struct e2f_ctx {
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
   rocblas_handle blas = nullptr;  // created on the first dense-graph forward
+  // coupling schedules of the aggregation of uncoupled products, per (L, groups)
+  struct Couple {
+    int k = 0;
+    int* meta = nullptr;
+    float* coef = nullptr;
+  };
+  std::map<std::pair<int, int>, Couple> couple;
 };
 
 namespace {
@@ -171,6 +179,24 @@ void push_array(std::vector<char>& blob, std::vector<size_t>& offs, const std::v
   offs.push_back(off);
 }
 
+// The coupling schedule for (L, groups), uploaded on first use.
+e2f_status couple_of(e2f_ctx* ctx, int L, int groups, const e2f_ctx::Couple*& out) {
+  auto key = std::make_pair(L, groups);
+  auto it = ctx->couple.find(key);
+  if (it == ctx->couple.end()) {
+    const CoupleSchedule cs = couple_schedule(ctx->host[L], groups);
+    e2f_ctx::Couple c;
+    c.k = cs.k;
+    E2F_HIP(hipMalloc((void**)&c.meta, sizeof(int) * std::max<size_t>(cs.meta.size(), 1)));
+    E2F_HIP(hipMalloc((void**)&c.coef, sizeof(float) * std::max<size_t>(cs.coef.size(), 1)));
+    E2F_HIP(hipMemcpy(c.meta, cs.meta.data(), sizeof(int) * cs.meta.size(), hipMemcpyHostToDevice));
+    E2F_HIP(hipMemcpy(c.coef, cs.coef.data(), sizeof(float) * cs.coef.size(), hipMemcpyHostToDevice));
+    it = ctx->couple.emplace(key, c).first;
+  }
+  out = &it->second;
+  return E2F_OK;
+}
+
 e2f_status upload_tables(e2f_ctx* ctx, int L) {
   const LayerTables& t = ctx->host[L];
   std::vector<char> blob;
@@ -204,6 +230,10 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
     push_array(blob, o, t.rcf_sched[f].off);
     push_array(blob, o, t.rcf_sched[f].meta);
   }
+  const size_t oag = o.size();
+  push_array(blob, o, t.ag_ptr);          // oag
+  push_array(blob, o, t.ag_idx);          // oag + 1
+  push_array(blob, o, t.ag_coef);         // oag + 2
   void* mem = nullptr;
   E2F_HIP(hipMalloc(&mem, blob.size()));
   ctx->table_mem[L] = mem;
@@ -237,6 +267,9 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
   d.rc_off = (const int*)(b + o[21]);
   d.rc_meta = (const int*)(b + o[22]);
   d.rc_coef = nullptr;
+  d.ag_ptr = (const int*)(b + o[oag]);
+  d.ag_idx = (const int*)(b + o[oag + 1]);
+  d.ag_coef = (const float*)(b + o[oag + 2]);
   ctx->rcf_k[L].assign(L + 1, nullptr);
   ctx->rcf_off[L].assign(L + 1, nullptr);
   ctx->rcf_meta[L].assign(L + 1, nullptr);
@@ -459,6 +492,10 @@ void e2f_destroy(e2f_ctx* ctx) {
     for (Buf* b : {&ctx->a, &ctx->b, &ctx->c, &ctx->d})
       if (b->p) (void)hipFree(b->p);
     if (ctx->blas) (void)rocblas_destroy_handle(ctx->blas);
+    for (auto& kv : ctx->couple) {
+      if (kv.second.meta) (void)hipFree(kv.second.meta);
+      if (kv.second.coef) (void)hipFree(kv.second.coef);
+    }
     for (auto& r : ctx->recs) {
       ctx->pool.push_back(r.start);
       ctx->pool.push_back(r.stop);
@@ -757,6 +794,10 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   const int nS = ynorm ? L + 1 : 1;
   if (ynorm && !use_blocks)
     return fail(E2F_EUNSUPPORTED, "y_norm needs every degree <= %d (largest %d)", kBlockMaxDegree, max_degree);
+  // aggregation of the uncoupled node products (no T); E2F_AGG_T selects the
+  // T-row aggregation over receiver blocks instead (comparison, and y_norm)
+  static const bool force_t = getenv("E2F_AGG_T") != nullptr;
+  const bool outer = !ynorm && !force_t && outer_agg_supported(L, C, p->heads);
   // ---- tile batches: T and S of a batch must fit the memory budget
   const size_t row_bytes = sizeof(float) * (size_t)t.dimT * C;
   size_t free_b = 0, total_b = 0;
@@ -771,7 +812,8 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   for (int t0 = 0; t0 < (int)keys;) {
     int t1 = t0 + 1;
     auto cost = [&](int a, int b) {
-      return (size_t)((int64_t)(pstart[b] - pstart[a]) + (int64_t)nS * (rstart[b] - rstart[a])) * row_bytes;
+      return (size_t)((outer ? 0 : (int64_t)(pstart[b] - pstart[a])) + (int64_t)nS * (rstart[b] - rstart[a])) *
+             row_bytes;
     };
     while (t1 < (int)keys && cost(t0, t1 + 1) <= budget) ++t1;
     batches.push_back({t0, t1});
@@ -786,9 +828,10 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   const size_t need_b = 2 * al256(sizeof(int32_t) * (size_t)P) + 3 * al256(sizeof(int32_t) * (size_t)n_edges) +
                         3 * al256(sizeof(int32_t) * (size_t)(nblk + 1)) + al256(blk_tmp_b) +
                         al256(sizeof(double) * (size_t)P * nk) + al256(sizeof(double) * (size_t)n * nk) +
-                        al256(row_bytes * (size_t)max_pairs) + al256(row_bytes * (size_t)max_recv * nS) +
+                        (outer ? 0 : al256(row_bytes * (size_t)max_pairs)) + al256(row_bytes * (size_t)max_recv * nS) +
                         (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0) +
-                        (use_blocks && (alpha || ynorm) ? al256(sizeof(float) * (size_t)n_edges * p->heads * nS) : 0) +
+                        ((use_blocks || outer) && (alpha || ynorm) ? al256(sizeof(float) * (size_t)n_edges * p->heads * nS)
+                                                                   : 0) +
                         (ynorm ? al256(sizeof(int32_t) * (size_t)n_edges) : 0);
   rs = ensure(ctx, ctx->b, need_b, s);
   if (rs != E2F_OK) return rs;
@@ -804,10 +847,11 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   void* blk_tmp = cb.take<char>(blk_tmp_b);
   double* Rp = cb.take<double>((size_t)P * nk);
   double* Rr = cb.take<double>((size_t)n * nk);
-  float* T = cb.take<float>((size_t)max_pairs * t.dimT * C);
+  float* T = outer ? nullptr : cb.take<float>((size_t)max_pairs * t.dimT * C);
   float* S = cb.take<float>((size_t)max_recv * t.dimT * C * nS);
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
-  float* alpha_hm = use_blocks && (alpha || ynorm) ? cb.take<float>((size_t)n_edges * p->heads * nS) : nullptr;
+  float* alpha_hm =
+      (use_blocks || outer) && (alpha || ynorm) ? cb.take<float>((size_t)n_edges * p->heads * nS) : nullptr;
   if (ynorm) {
     int32_t* erows = cb.take<int32_t>((size_t)n_edges);
     E2F_TIMED("alpha_hm", launch_alpha_dnorm(pos, row_ptr, col_idx, alpha, n, n_edges, p->heads, L, erows, alpha_hm, s));
@@ -819,11 +863,20 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   E2F_TIMED("sh", launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, nullptr, s));
   E2F_TIMED("sh", launch_sh(t, pos, nullptr, origins, nullptr, tile_of, tp.ncell, n, Rr, nullptr, s));
   const int dh = C / p->heads;
+  const int cgroups = outer ? outer_agg_groups(L, C, p->heads) : 0;
+  const e2f_ctx::Couple* cpl = nullptr;
+  if (outer && (rs = couple_of(ctx, L, cgroups, cpl)) != E2F_OK) return rs;
   for (const Batch& bt : batches) {
     const int p0 = pstart[bt.t0], q0 = rstart[bt.t0];
     const int pb = pstart[bt.t1] - p0, nb = rstart[bt.t1] - q0;
     if (nb == 0) continue;
     const int32_t* ord = order + q0;
+    if (outer) {
+      E2F_TIMED("aggregate", launch_outer_agg(t, Rp, row_ptr, col_idx, col_pair, alpha_hm, n_edges, feat, ord,
+                                              cpl->meta, cpl->coef, cpl->k, cgroups, nb, C, p->heads, S, s));
+      E2F_TIMED("recouple", launch_recouple(t, Rr, S, false, ord, nb, C, dh, y, s));
+      continue;
+    }
     E2F_TIMED("node_tp", launch_node_tp(t, Rp + (size_t)p0 * nk, pair_node + p0, feat, pb, C, dh, T, s));
     if (use_blocks) {
       E2F_TIMED("tile_plan", launch_block_union(row_ptr, col_pair, ord, nb, blk_count, blk_off, uni, ucount,

@@ -620,6 +620,186 @@ __global__ __launch_bounds__(64 * kAggRecv) void k_aggregate_rows(const float4* 
   S[(size_t)r * W4 + q] = acc;  // S rows follow the receiver order
 }
 
+// ------------------------------------------------------------ aggregation of the node products
+// The j-side product is linear, so the aggregation can run on the uncoupled
+// products and the coupling follow per receiver:
+//   S_i^(a,b,d)[de][c] = sum_j alpha_ij [h_j^(a) (x) R^(b)(p_j)]^(d)_de[c]
+//                      = sum_{al,be} C^{d de}_{a al, b be} G_i[(b,be)][(a,al)][c],
+//   G_i[be][q][c]      = sum_j alpha_ij,h(c) R_be(p_j) h_j[q][c].
+// Per (receiver, head) G_i is one dense product on v_mfma_f32_16x16x4f32:
+// M = the (L+1)^2 components be of R (padded to 16), K = the receiver's
+// neighbours four at a time, N = the (L+1)^2 * dh columns (q, t) of head h,
+// with A = alpha * R staged in LDS per chunk of edges and B = the neighbours'
+// features read from L2.  There are no structural zeros (only the padding of
+// M), and the operands are the features h (not one T row per tile and
+// sender).  G then sits in LDS and the coupling to S uses the node product's
+// CG tables (row -> slots al -> entries (be, C)); S is written head-major, as
+// the recouple reads it.
+constexpr int kOuterEdges = 128;  // edges staged per chunk
+
+template <int L, int NTWM, int LB>
+__global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const double* __restrict__ Rp,
+                                                    const int64_t* __restrict__ row_ptr,
+                                                    const int32_t* __restrict__ col,
+                                                    const int32_t* __restrict__ col_pair,
+                                                    const float* __restrict__ alpha_hm, int64_t n_edges,
+                                                    const float* __restrict__ feat, const int32_t* __restrict__ order,
+                                                    const int* __restrict__ cmeta, const float* __restrict__ ccoef,
+                                                    int ck, int cgroups, int work_floats, int n, int nrx, int rpw,
+                                                    int C, int H, float* __restrict__ S) {
+  constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
+  constexpr int EC = kOuterEdges;
+  extern __shared__ float sm[];
+  float* Al = sm;                   // [EC][MP]: Al[nb*MP + be] = alpha * R_be of the chunk's edge nb
+  int* jl = (int*)(sm + EC * MP);   // [EC]: sender of the edge (clamped past the chunk)
+  float* G = sm;                    // [NK][GS], after the products (reuses the staging space)
+  // the coupling schedule, staged once in LDS after the work space when
+  // work_floats > 0 (else read from global memory)
+  const int* sm_meta = work_floats > 0 ? (const int*)(sm + work_floats) : cmeta;
+  const float* sm_coef = work_floats > 0 ? sm + work_floats + ck * cgroups : ccoef;
+  if (work_floats > 0) {
+    for (int q = threadIdx.x; q < ck * cgroups; q += blockDim.x) {
+      ((int*)(sm + work_floats))[q] = cmeta[q];
+      sm[work_floats + ck * cgroups + q] = ccoef[q];
+    }
+  }
+  const int dh = C / H, NC = NK * dh, NT = (NC + 15) / 16, GS = NC + 4;
+  // workgroup -> (rpw consecutive receivers, head h); the receivers of one
+  // XCD are contiguous in the spatial order and their heads consecutive
+  const int bid = blockIdx.x, xcd = bid % 8, local = bid / 8;
+  const int h = local % H, rfirst = xcd * nrx + (local / H) * rpw;
+  const int rlast = min(min(rfirst + rpw, (xcd + 1) * nrx), n);  // uniform over the workgroup
+  const int NW = blockDim.x >> 6, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int l16 = lane & 15, k4 = lane >> 4;
+  // the wave's column tiles nt = wave + NW w; lane column n = nt*16 + l16
+  int off[NTWM];
+  bool cok[NTWM], tok[NTWM];
+#pragma unroll
+  for (int w = 0; w < NTWM; ++w) {
+    const int nt = wave + NW * w, nn = nt * 16 + l16;
+    tok[w] = nt < NT;  // uniform over the wave
+    cok[w] = tok[w] && nn < NC;
+    const int q = cok[w] ? nn / dh : 0, tt = cok[w] ? nn % dh : 0;
+    off[w] = q * C + h * dh + tt;
+  }
+  for (int r = rfirst; r < rlast; ++r) {
+  const int i = order[r];
+  v4f acc[MT][NTWM];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int w = 0; w < NTWM; ++w) acc[mt][w] = (v4f){0.f, 0.f, 0.f, 0.f};
+  const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+  __syncthreads();  // the previous receiver's coupling has read G (and the schedule is staged)
+  for (int64_t c0 = e0; c0 < e1; c0 += EC) {
+    const int ne = (int)min((int64_t)EC, e1 - c0);
+    __syncthreads();
+    // staging: thread -> edge nb = tid % EC, components be = tid / EC + k P
+    // (P = threads per edge); every load is issued before the first store
+    {
+      const int nb = threadIdx.x % EC, p0 = threadIdx.x / EC, P = blockDim.x / EC;
+      if (p0 < P) {
+        const bool live = nb < ne;
+        const int64_t e = c0 + (live ? nb : 0);
+        const float a = !live ? 0.0f : (alpha_hm ? alpha_hm[(int64_t)h * n_edges + e] : 1.0f);
+        const double* Re = Rp + (size_t)col_pair[e] * NK;
+        // rounds of four components (be = p0 + P k), loads before stores
+        for (int be0 = p0; be0 < MP; be0 += 4 * P) {
+          float rv[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int be = be0 + u * P;
+            rv[u] = be < NK ? (float)Re[be] : 0.0f;
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int be = be0 + u * P;
+            if (be < MP) Al[nb * MP + be] = a * rv[u];
+          }
+        }
+        if (p0 == 0) jl[nb] = col[e];
+      }
+    }
+    __syncthreads();
+    const int ns = (ne + 3) / 4;
+    // two-stage pipeline: the features of step st+1 are loaded while the
+    // MFMAs of step st run
+    float bA[NTWM], bB[NTWM];
+    auto loadb = [&](int st, float* b) {
+      const int nb = min(4 * st + k4, EC - 1);  // rows past ne carry A = 0 and read a valid sender
+      const float* hj = feat + (size_t)jl[nb] * NK * C;
+#pragma unroll
+      for (int w = 0; w < NTWM; ++w) b[w] = hj[off[w]];
+    };
+    auto mma = [&](int st, const float* b) {
+      const int nb = min(4 * st + k4, EC - 1);
+      float a[MT];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) a[mt] = 4 * st + k4 < EC ? Al[nb * MP + mt * 16 + l16] : 0.0f;
+#pragma unroll
+      for (int w = 0; w < NTWM; ++w) {
+        if (!tok[w]) continue;
+        const float bv = cok[w] ? b[w] : 0.0f;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[mt][w] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv, acc[mt][w], 0, 0, 0);
+      }
+    };
+    float bC[NTWM];
+    loadb(0, bA);
+    loadb(1, bB);
+    for (int st = 0; st < ns; st += 3) {
+      loadb(st + 2, bC);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(st, bA);
+      __builtin_amdgcn_sched_barrier(0);
+      loadb(st + 3, bA);
+      __builtin_amdgcn_sched_barrier(0);
+      if (st + 1 < ns) mma(st + 1, bB);
+      __builtin_amdgcn_sched_barrier(0);
+      loadb(st + 4, bB);
+      __builtin_amdgcn_sched_barrier(0);
+      if (st + 2 < ns) mma(st + 2, bC);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  __syncthreads();  // the staging space becomes G
+  // acc[mt][w][v] = G[be = mt*16 + 4 k4 + v][n = nt*16 + l16]
+#pragma unroll
+  for (int w = 0; w < NTWM; ++w) {
+    if (!cok[w]) continue;
+    const int nn = (wave + NW * w) * 16 + l16;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int be = mt * 16 + 4 * k4 + v;
+        if (be < NK) G[be * GS + nn] = acc[mt][w][v];
+      }
+  }
+  __syncthreads();
+  // j-side coupling: S[row][tt] = sum over the row's entries of C * G[be][q dh + tt],
+  // from a thread-balanced schedule: group g = tid / dh walks its entries
+  // k*cgroups + g (coalesced loads shared by the group's dh channels)
+  // (four channels per thread: group g = tid / (dh/4), channels 4 tq .. 4 tq + 3)
+  float* Sr = S + (size_t)r * t.dimT * C + (size_t)h * t.dimT * dh;
+  const int dq = dh >> 2, g = threadIdx.x / dq, tq = threadIdx.x % dq;
+  if (g < cgroups) {
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+    for (int k = 0; k < ck; ++k) {
+      const int m = sm_meta[k * cgroups + g];
+      const float c = sm_coef[k * cgroups + g];
+      const float4 gv = *(const float4*)(G + ((m >> 6) & 63) * GS + (m & 63) * dh + 4 * tq);
+      v.x += c * gv.x, v.y += c * gv.y, v.z += c * gv.z, v.w += c * gv.w;
+      if (m < 0) {
+        *(float4*)(Sr + ((m >> 12) & 4095) * dh + 4 * tq) = v;
+        v = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  }
+  }  // receivers of the workgroup
+}
+
 // ------------------------------------------------------------ i-side recouple
 // y_i[k][c] = sum_r Q_i[k][r] S_i[r][c] over the T rows r, with the per-node
 // matrix Q_i[(o,m)][(a,b,d,de)] = sum_u K(a,b,d,u,o) sum_ga C^{o m}_{u ga, d de}
@@ -1478,6 +1658,85 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
   k_aggregate_rows<<<(unsigned)blocks, 64 * kAggRecv, 0, s>>>((const float4*)T, pair_base, row_ptr, col_pair, alpha,
                                                               order, n,
                                                               (int)W4, nchunk, ngroups, gpx, C, dh, H, (float4*)S);
+  return hipGetLastError();
+}
+
+namespace {
+struct OuterShape {
+  int nw = 0;
+  size_t lds = 0;   // work space (staging, then G)
+};
+// column tiles per wave: 4 (measured faster than 8 at L = 4: more waves,
+// fewer registers each); E2F_OUTER_NTW=8 selects 8 at L <= 4 (tuning)
+int outer_ntw(int L) {
+  static const int env = [] {
+    const char* v = getenv("E2F_OUTER_NTW");
+    return v ? atoi(v) : 0;
+  }();
+  return L > 4 ? 4 : (env == 4 || env == 8 ? env : 4);
+}
+
+OuterShape outer_shape(int L, int C, int H) {
+  const int nk = (L + 1) * (L + 1), mp = 16 * ((nk + 15) / 16), dh = C / H;
+  const int nc = nk * dh, nt = (nc + 15) / 16, ntwm = outer_ntw(L);
+  OuterShape o;
+  o.nw = (nt + ntwm - 1) / ntwm;
+  o.nw = std::max(o.nw, 2);  // the staging needs at least kOuterEdges threads
+  o.lds = std::max(sizeof(float) * (size_t)kOuterEdges * mp + sizeof(int) * kOuterEdges,
+                   sizeof(float) * (size_t)nk * (nc + 4));
+  return o;
+}
+}  // namespace
+
+int outer_agg_groups(int L, int C, int H) { return 64 * outer_shape(L, C, H).nw / (C / H / 4); }
+
+bool outer_agg_supported(int L, int C, int H) {
+  const OuterShape o = outer_shape(L, C, H);
+  return o.nw >= 1 && o.nw <= (outer_ntw(L) == 8 ? 8 : 16) && o.lds <= 160 * 1024;
+}
+
+hipError_t launch_outer_agg(const DevTables& t, const double* Rp, const int64_t* row_ptr, const int32_t* col,
+                            const int32_t* col_pair, const float* alpha_hm, int64_t n_edges, const float* feat,
+                            const int32_t* order, const int* cmeta, const float* ccoef, int ck, int cgroups, int n,
+                            int C, int H, float* S, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  if (!outer_agg_supported(t.L, C, H) || cgroups != outer_agg_groups(t.L, C, H)) return hipErrorInvalidValue;
+  const OuterShape o = outer_shape(t.L, C, H);
+  // receivers per workgroup, and the coupling schedule in LDS when it fits
+  // beside the work space with two workgroups per CU
+  static const int rpw_env = [] {
+    const char* v = getenv("E2F_OUTER_RPW");
+    return v ? atoi(v) : 0;
+  }();
+  const int rpw = rpw_env > 0 ? rpw_env : 4;
+  const size_t sched_b = sizeof(float) * 2 * (size_t)ck * cgroups;
+  const bool sched_lds = o.lds + sched_b <= 80 * 1024;
+  const int work_floats = sched_lds ? (int)(o.lds / sizeof(float)) : 0;
+  const size_t lds = o.lds + (sched_lds ? sched_b : 0);
+  const int nrx = (n + kXcds - 1) / kXcds;
+  const int64_t blocks = (int64_t)kXcds * ((nrx + rpw - 1) / rpw) * H;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  // launch bound 512 (up to 256 VGPRs) at L <= 4 with at most 8 waves; at
+  // L = 5, 6 the bound 1024 keeps two workgroups per CU (170 VGPRs under
+  // 512 allow one; 1024 spills a few and measures faster: 311 vs 404 ms for
+  // 200k atoms, L = 6)
+  const int lb = t.L <= 4 && o.nw <= 8 ? 512 : 1024;
+  switch (t.L * 64 + outer_ntw(t.L) * 4 + (lb == 512 ? 0 : 1)) {
+#define E2F_CASE(LL, NTWM, LB)                                                                              \
+  case LL * 64 + NTWM * 4 + (LB == 512 ? 0 : 1):                                                            \
+    if (hipError_t e = allow_lds(k_outer_agg<LL, NTWM, LB>, lds); e != hipSuccess) return e;                \
+    k_outer_agg<LL, NTWM, LB><<<(unsigned)blocks, 64 * o.nw, lds, s>>>(t, Rp, row_ptr, col, col_pair,       \
+                                                                      alpha_hm, n_edges, feat, order, cmeta, \
+                                                                      ccoef, ck, cgroups, work_floats, n,    \
+                                                                      nrx, rpw, C, H, S);                    \
+    break;
+#define E2F_CASES(LL) E2F_CASE(LL, 4, 512) E2F_CASE(LL, 4, 1024)
+    E2F_CASES(0) E2F_CASES(1) E2F_CASES(2) E2F_CASES(3) E2F_CASES(4) E2F_CASES(5) E2F_CASES(6)
+    E2F_CASE(0, 8, 512) E2F_CASE(1, 8, 512) E2F_CASE(2, 8, 512) E2F_CASE(3, 8, 512) E2F_CASE(4, 8, 512)
+#undef E2F_CASES
+#undef E2F_CASE
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -89,11 +89,27 @@ struct LayerTables {
   // recouple restricted to the terms of filter degree f = b + u, one schedule
   // per f (attention weights alpha / D^f need one aggregation per f)
   std::vector<Schedule> rcf_sched;  // [L+1]
+  // j-side coupling of aggregated uncoupled products: S[row] = sum over the
+  // row's entries of coef * G[be][q], entries ag_ptr[row] .. ag_ptr[row+1]
+  // with ag_idx = be << 6 | q (be, q < (L+1)^2)
+  std::vector<int> ag_ptr, ag_idx;
+  std::vector<float> ag_coef;
   int max_qslots = 0;               // largest (2o+1)*ncol[o]
   int m_slots() const { return m_rowoff.back(); }
 };
 
 LayerTables build_layer_tables(int L);
+
+// The coupling after aggregation as a thread-balanced schedule for `groups`
+// groups of threads (one thread per channel in a group): entry k of group g
+// at k*groups + g; meta = gidx (bits 0-11, be << 6 | q) | row << 12 | last
+// (bit 31); rows are spread over the groups by entry count.
+struct CoupleSchedule {
+  int groups = 0, k = 0;
+  std::vector<int> meta;
+  std::vector<float> coef;
+};
+CoupleSchedule couple_schedule(const LayerTables& t, int groups);
 int64_t node_tp_dim(int L);
 
 // ---------------------------------------------------------------- device side
@@ -108,6 +124,7 @@ struct DevTables {
   const int* k_ptr; const int* k_ridx; const float* k_coef;  // k_coef includes path weights
   const int* tp_k; const int* tp_off; const int* tp_meta; const double* tp_coef;
   const int* rc_k; const int* rc_off; const int* rc_meta; const double* rc_coef;  // rc_coef includes path weights
+  const int* ag_ptr; const int* ag_idx; const float* ag_coef;
   int max_qslots, m_slots;
   int tp_rs[kMaxL + 1], tp_mo[kMaxL + 2];
 };

@@ -104,6 +104,16 @@ hipError_t launch_alpha_dnorm(const float* pos, const int64_t* row_ptr, const in
 hipError_t launch_alpha_head_major(const float* alpha, int64_t n_edges, int H, float* alpha_hm, hipStream_t s);
 // y[order[r]] from S row r (head-major like T), r < n; shared_s: every r
 // reads S row 0
+// S rows r < n (receivers order[r]) by aggregating the uncoupled node products
+// alpha_ij R(p_j) (x) h_j and coupling per receiver (no T): Rp [pairs][nk]
+// (pair col_pair[e] of edge e), alpha_hm [H][n_edges] or NULL (ones)
+// with the coupling schedule of couple_schedule(tables, outer_agg_groups(L, C, H))
+bool outer_agg_supported(int L, int C, int H);
+int outer_agg_groups(int L, int C, int H);
+hipError_t launch_outer_agg(const DevTables& t, const double* Rp, const int64_t* row_ptr, const int32_t* col,
+                            const int32_t* col_pair, const float* alpha_hm, int64_t n_edges, const float* feat,
+                            const int32_t* order, const int* cmeta, const float* ccoef, int ck, int cgroups, int n,
+                            int C, int H, float* S, hipStream_t s);
 // accumulate: y += the product instead of y = (one writer per element)
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, bool shared_s, const int32_t* order,
                            int n, int C, int dh, float* y, hipStream_t s, bool accumulate = false);

@@ -280,6 +280,19 @@ LayerTables build_layer_tables(int L) {
     }
   }
 
+  // ---- the same CG entries by row, for the coupling after aggregation
+  t.ag_ptr.assign(1, 0);
+  for (int r = 0; r < t.dimT; ++r) {
+    const int s0 = t.m_rowoff[r], s1 = t.m_rowoff[r + 1];
+    const int a = (s1 - s0 - 1) / 2;
+    for (int sl = s0; sl < s1; ++sl)
+      for (int e = t.m_ptr[sl]; e < t.m_ptr[sl + 1]; ++e) {
+        t.ag_idx.push_back((t.m_ridx[e] << 6) | (a * a + sl - s0));
+        t.ag_coef.push_back((float)t.m_coef[e]);
+      }
+    t.ag_ptr.push_back((int)t.ag_idx.size());
+  }
+
   // ---- i-side matrices Q_o: y^(o)[m] = sum_cols Q_o[m][col] S[col]
   t.q_ncol.assign(L1, 0);
   t.q_coloff.assign(L1 + 1, 0);
@@ -407,6 +420,46 @@ LayerTables build_layer_tables(int L) {
           t.k_ptr.push_back((int)t.k_unit.size());
         }
   return t;
+}
+
+CoupleSchedule couple_schedule(const LayerTables& t, int groups) {
+  CoupleSchedule cs;
+  cs.groups = groups;
+  std::vector<int> order(t.dimT);
+  for (int r = 0; r < t.dimT; ++r) order[r] = r;
+  auto len = [&](int r) { return t.ag_ptr[r + 1] - t.ag_ptr[r]; };
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return len(x) > len(y); });
+  std::vector<std::vector<int>> per(groups);
+  std::vector<int> load(groups, 0);
+  for (int r : order) {
+    int best = 0;
+    for (int g = 1; g < groups; ++g)
+      if (load[g] < load[best]) best = g;
+    per[best].push_back(r);
+    load[best] += std::max(1, len(r));  // an empty row still stores its zero
+  }
+  int K = 0;
+  for (int g = 0; g < groups; ++g) K = std::max(K, load[g]);
+  cs.k = K;
+  cs.meta.assign((size_t)K * groups, 0);
+  cs.coef.assign((size_t)K * groups, 0.0f);
+  for (int g = 0; g < groups; ++g) {
+    int k = 0;
+    for (int r : per[g]) {
+      const int a0 = t.ag_ptr[r], a1 = t.ag_ptr[r + 1];
+      if (a0 == a1) {  // no entry: store 0
+        cs.meta[(size_t)k * groups + g] = (r << 12) | (int)0x80000000u;
+        ++k;
+        continue;
+      }
+      for (int e = a0; e < a1; ++e, ++k) {
+        const bool last = e + 1 == a1;
+        cs.meta[(size_t)k * groups + g] = t.ag_idx[e] | (r << 12) | (last ? (int)0x80000000u : 0);
+        cs.coef[(size_t)k * groups + g] = t.ag_coef[e];
+      }
+    }
+  }
+  return cs;
 }
 
 }  // namespace e2f
