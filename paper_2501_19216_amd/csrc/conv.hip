@@ -671,17 +671,22 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const double* __r
   const int rlast = min(min(rfirst + rpw, (xcd + 1) * nrx), n);  // uniform over the workgroup
   const int NW = blockDim.x >> 6, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int l16 = lane & 15, k4 = lane >> 4;
-  // the wave's column tiles nt = wave + NW w; lane column n = nt*16 + l16
-  int off[NTWM];
-  bool cok[NTWM], tok[NTWM];
+  // the wave's column blocks cb = wave + NW u (u < NTWM/4) of 64 columns:
+  // tile w of block u holds the columns cb*64 + 4 l16 + w, so lane l16 reads
+  // the four consecutive columns 4 l16 .. 4 l16 + 3 (one q, as 4 | dh) as
+  // one float4
+  constexpr int NB = NTWM / 4;
+  int off[NB];
+  bool cok[NB], tok[NB];
 #pragma unroll
-  for (int w = 0; w < NTWM; ++w) {
-    const int nt = wave + NW * w, nn = nt * 16 + l16;
-    tok[w] = nt < NT;  // uniform over the wave
-    cok[w] = tok[w] && nn < NC;
-    const int q = cok[w] ? nn / dh : 0, tt = cok[w] ? nn % dh : 0;
-    off[w] = q * C + h * dh + tt;
+  for (int u = 0; u < NB; ++u) {
+    const int cb = wave + NW * u, nn = cb * 64 + 4 * l16;
+    tok[u] = cb * 64 < NC;  // uniform over the wave
+    cok[u] = nn < NC;
+    const int q = cok[u] ? nn / dh : 0, tt = cok[u] ? nn % dh : 0;
+    off[u] = q * C + h * dh + tt;
   }
+  (void)NT;
   for (int r = rfirst; r < rlast; ++r) {
   const int i = order[r];
   v4f acc[MT][NTWM];
@@ -722,29 +727,34 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const double* __r
     }
     __syncthreads();
     const int ns = (ne + 3) / 4;
-    // two-stage pipeline: the features of step st+1 are loaded while the
-    // MFMAs of step st run
-    float bA[NTWM], bB[NTWM];
-    auto loadb = [&](int st, float* b) {
+    // three-stage pipeline: the features of steps st+1, st+2 are loaded
+    // while the MFMAs of step st run
+    float4 bA[NB], bB[NB];
+    auto loadb = [&](int st, float4* b) {
       const int nb = min(4 * st + k4, EC - 1);  // rows past ne carry A = 0 and read a valid sender
       const float* hj = feat + (size_t)jl[nb] * NK * C;
 #pragma unroll
-      for (int w = 0; w < NTWM; ++w) b[w] = hj[off[w]];
+      for (int u = 0; u < NB; ++u) b[u] = *(const float4*)(hj + off[u]);
     };
-    auto mma = [&](int st, const float* b) {
+    auto mma = [&](int st, const float4* b) {
       const int nb = min(4 * st + k4, EC - 1);
       float a[MT];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) a[mt] = 4 * st + k4 < EC ? Al[nb * MP + mt * 16 + l16] : 0.0f;
 #pragma unroll
-      for (int w = 0; w < NTWM; ++w) {
-        if (!tok[w]) continue;
-        const float bv = cok[w] ? b[w] : 0.0f;
+      for (int u = 0; u < NB; ++u) {
+        if (!tok[u]) continue;
+        const float4 bv = cok[u] ? b[u] : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[mt][w] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv, acc[mt][w], 0, 0, 0);
+        for (int mt = 0; mt < MT; ++mt) {
+          acc[mt][4 * u + 0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv.x, acc[mt][4 * u + 0], 0, 0, 0);
+          acc[mt][4 * u + 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv.y, acc[mt][4 * u + 1], 0, 0, 0);
+          acc[mt][4 * u + 2] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv.z, acc[mt][4 * u + 2], 0, 0, 0);
+          acc[mt][4 * u + 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv.w, acc[mt][4 * u + 3], 0, 0, 0);
+        }
       }
     };
-    float bC[NTWM];
+    float4 bC[NB];
     loadb(0, bA);
     loadb(1, bB);
     for (int st = 0; st < ns; st += 3) {
@@ -763,17 +773,20 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const double* __r
     }
   }
   __syncthreads();  // the staging space becomes G
-  // acc[mt][w][v] = G[be = mt*16 + 4 k4 + v][n = nt*16 + l16]
+  // acc[mt][4u + w][v] = G[be = mt*16 + 4 k4 + v][n = cb*64 + 4 l16 + w]:
+  // one float4 per (block, tile row, v)
 #pragma unroll
-  for (int w = 0; w < NTWM; ++w) {
-    if (!cok[w]) continue;
-    const int nn = (wave + NW * w) * 16 + l16;
+  for (int u = 0; u < NB; ++u) {
+    if (!cok[u]) continue;
+    const int nn = (wave + NW * u) * 64 + 4 * l16;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int be = mt * 16 + 4 * k4 + v;
-        if (be < NK) G[be * GS + nn] = acc[mt][w][v];
+        if (be < NK)
+          *(float4*)(G + be * GS + nn) =
+              make_float4(acc[mt][4 * u][v], acc[mt][4 * u + 1][v], acc[mt][4 * u + 2][v], acc[mt][4 * u + 3][v]);
       }
   }
   __syncthreads();
@@ -1678,7 +1691,7 @@ int outer_ntw(int L) {
 
 OuterShape outer_shape(int L, int C, int H) {
   const int nk = (L + 1) * (L + 1), mp = 16 * ((nk + 15) / 16), dh = C / H;
-  const int nc = nk * dh, nt = (nc + 15) / 16, ntwm = outer_ntw(L);
+  const int nc = nk * dh, nt = (nc + 63) / 64 * 4, ntwm = outer_ntw(L);  // tiles in whole 64-column blocks
   OuterShape o;
   o.nw = (nt + ntwm - 1) / ntwm;
   o.nw = std::max(o.nw, 2);  // the staging needs at least kOuterEdges threads
