@@ -650,8 +650,12 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const double* __r
   constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
   constexpr int EC = kOuterEdges;
   extern __shared__ float sm[];
-  float* Al = sm;                   // [EC][MP]: Al[nb*MP + be] = alpha * R_be of the chunk's edge nb
-  int* jl = (int*)(sm + EC * MP);   // [EC]: sender of the edge (clamped past the chunk)
+  // rows of AS = MP + 16 floats: the four rows an MFMA step reads (one per
+  // lane group k4) start 48 banks apart, so the operand reads are
+  // conflict-free
+  constexpr int AS = MP + 16;
+  float* Al = sm;                   // [EC][AS]: Al[nb*AS + be] = alpha * R_be of the chunk's edge nb
+  int* jl = (int*)(sm + EC * AS);   // [EC]: sender of the edge (clamped past the chunk)
   float* G = sm;                    // [NK][GS], after the products (reuses the staging space)
   // the coupling schedule, staged once in LDS after the work space when
   // work_floats > 0 (else read from global memory)
@@ -699,32 +703,26 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const double* __r
   for (int64_t c0 = e0; c0 < e1; c0 += EC) {
     const int ne = (int)min((int64_t)EC, e1 - c0);
     __syncthreads();
-    // staging: thread -> edge nb = tid % EC, components be = tid / EC + k P
-    // (P = threads per edge); every load is issued before the first store
-    {
-      const int nb = threadIdx.x % EC, p0 = threadIdx.x / EC, P = blockDim.x / EC;
-      if (p0 < P) {
-        const bool live = nb < ne;
-        const int64_t e = c0 + (live ? nb : 0);
-        const float a = !live ? 0.0f : (alpha_hm ? alpha_hm[(int64_t)h * n_edges + e] : 1.0f);
-        const double* Re = Rp + (size_t)col_pair[e] * NK;
-        // rounds of four components (be = p0 + P k), loads before stores
-        for (int be0 = p0; be0 < MP; be0 += 4 * P) {
-          float rv[4];
+    // staging: consecutive lanes take consecutive components be of one edge
+    // (contiguous R loads, conflict-free LDS stores); four values per thread
+    // in flight, loads before stores
+    for (int base = threadIdx.x; base < EC * MP; base += 4 * blockDim.x) {
+      float v[4];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int be = be0 + u * P;
-            rv[u] = be < NK ? (float)Re[be] : 0.0f;
-          }
+      for (int u = 0; u < 4; ++u) {
+        const int idx = base + u * blockDim.x, nb = idx / MP, be = idx % MP;
+        const bool ok = idx < EC * MP && nb < ne && be < NK;
+        const int64_t e = c0 + (ok ? nb : 0);
+        const float a = ok ? (alpha_hm ? alpha_hm[(int64_t)h * n_edges + e] : 1.0f) : 0.0f;
+        v[u] = ok ? a * (float)Rp[(size_t)col_pair[e] * NK + be] : 0.0f;
+      }
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int be = be0 + u * P;
-            if (be < MP) Al[nb * MP + be] = a * rv[u];
-          }
-        }
-        if (p0 == 0) jl[nb] = col[e];
+      for (int u = 0; u < 4; ++u) {
+        const int idx = base + u * blockDim.x;
+        if (idx < EC * MP) Al[(idx / MP) * AS + idx % MP] = v[u];
       }
     }
+    for (int q = threadIdx.x; q < EC; q += blockDim.x) jl[q] = col[c0 + (q < ne ? q : 0)];
     __syncthreads();
     const int ns = (ne + 3) / 4;
     // three-stage pipeline: the features of steps st+1, st+2 are loaded
@@ -740,7 +738,7 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const double* __r
       const int nb = min(4 * st + k4, EC - 1);
       float a[MT];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) a[mt] = 4 * st + k4 < EC ? Al[nb * MP + mt * 16 + l16] : 0.0f;
+      for (int mt = 0; mt < MT; ++mt) a[mt] = 4 * st + k4 < EC ? Al[nb * AS + mt * 16 + l16] : 0.0f;
 #pragma unroll
       for (int u = 0; u < NB; ++u) {
         if (!tok[u]) continue;
@@ -1695,7 +1693,7 @@ OuterShape outer_shape(int L, int C, int H) {
   OuterShape o;
   o.nw = (nt + ntwm - 1) / ntwm;
   o.nw = std::max(o.nw, 2);  // the staging needs at least kOuterEdges threads
-  o.lds = std::max(sizeof(float) * (size_t)kOuterEdges * mp + sizeof(int) * kOuterEdges,
+  o.lds = std::max(sizeof(float) * (size_t)kOuterEdges * (mp + 16) + sizeof(int) * kOuterEdges,
                    sizeof(float) * (size_t)nk * (nc + 4));
   return o;
 }
