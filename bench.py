@@ -52,6 +52,18 @@ def layer_counts(L):
     return dict(dimT=dimT, m_slots=m_slots, q_slots=q_slots, k_slots=(L + 1) ** 4)
 
 
+def coupling_entries(e2f, L):
+    """Nonzero CG entries (row, alpha, beta) of the j-side coupling [h^(a) (x) R^(b)]^(d)
+    over the blocks the layer uses (per channel)."""
+    n = 0
+    for a in range(L + 1):
+        for b in range(L + 1):
+            for d in range(abs(a - b), a + b + 1):
+                if any(tri(a, b + u, o) and tri(u, d, o) for u in range(L - b + 1) for o in range(L + 1)):
+                    n += int(np.count_nonzero(np.abs(e2f.e2f_real_cg(a, b, d)) > 1e-14))
+    return n
+
+
 def file_sha(path):
     with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()
@@ -347,9 +359,14 @@ def main():
     cnt = layer_counts(L)
     dimT = cnt["dimT"]
     # algorithmic bytes / flops per launch of each kernel of the forward
+    nk = (L + 1) ** 2
+    if "node_tp" in kernels:  # T rows per (tile, sender), aggregated over receiver blocks
+        agg = dict(bytes=4.0 * dimT * C * (pairs + n) + 4.0 * E * (1 + H) + 8.0 * (n + 1), flops=2.0 * E * dimT * C)
+    else:  # uncoupled products aggregated per receiver, then coupled: read h once, write S once
+        agg = dict(bytes=4.0 * n * nk * C + 4.0 * E * (1 + H) + 8.0 * pairs * nk + 8.0 * (n + 1) + 4.0 * n * dimT * C,
+                   flops=2.0 * E * nk * nk * C + 2.0 * n * coupling_entries(e2f, L) * C)
     alg = {
-        "aggregate": dict(bytes=4.0 * dimT * C * (pairs + n) + 4.0 * E * (1 + H) + 8.0 * (n + 1),
-                          flops=2.0 * E * dimT * C),
+        "aggregate": agg,
         "node_tp": dict(bytes=4.0 * C * (n * (L + 1) ** 2 + pairs * dimT), flops=2.0 * pairs * cnt["m_slots"] * C),
         "recouple": dict(bytes=4.0 * C * n * (dimT + (L + 1) ** 2), flops=2.0 * n * cnt["q_slots"] * C),
         "mix": dict(bytes=8.0 * n * (L + 1) ** 2 * C + 4.0 * (L + 1) * C * C, flops=2.0 * n * (L + 1) ** 2 * C * C),
