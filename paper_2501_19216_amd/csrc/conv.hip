@@ -638,7 +638,7 @@ __global__ __launch_bounds__(64 * kAggRecv) void k_aggregate_rows(const float4* 
 constexpr int kOuterEdges = 128;  // edges staged per chunk
 
 template <int L, int NTWM, int LB>
-__global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const double* __restrict__ Rp,
+__global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __restrict__ Rp,
                                                     const int64_t* __restrict__ row_ptr,
                                                     const int32_t* __restrict__ col,
                                                     const int32_t* __restrict__ col_pair,
@@ -703,28 +703,29 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const double* __r
   for (int64_t c0 = e0; c0 < e1; c0 += EC) {
     const int ne = (int)min((int64_t)EC, e1 - c0);
     __syncthreads();
-    // staging: consecutive lanes take consecutive components be of one edge
+    // staging of the rows the steps read (4 ns <= EC; rows past ne hold 0):
+    // consecutive lanes take consecutive components be of one edge
     // (contiguous R loads, conflict-free LDS stores); four values per thread
     // in flight, loads before stores
-    for (int base = threadIdx.x; base < EC * MP; base += 4 * blockDim.x) {
+    const int ns = (ne + 3) / 4, nsl = 4 * ns * MP;
+    for (int base = threadIdx.x; base < nsl; base += 4 * blockDim.x) {
       float v[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int idx = base + u * blockDim.x, nb = idx / MP, be = idx % MP;
-        const bool ok = idx < EC * MP && nb < ne && be < NK;
+        const bool ok = idx < nsl && nb < ne && be < NK;
         const int64_t e = c0 + (ok ? nb : 0);
         const float a = ok ? (alpha_hm ? alpha_hm[(int64_t)h * n_edges + e] : 1.0f) : 0.0f;
-        v[u] = ok ? a * (float)Rp[(size_t)col_pair[e] * NK + be] : 0.0f;
+        v[u] = ok ? a * Rp[(size_t)col_pair[e] * NK + be] : 0.0f;
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int idx = base + u * blockDim.x;
-        if (idx < EC * MP) Al[(idx / MP) * AS + idx % MP] = v[u];
+        if (idx < nsl) Al[(idx / MP) * AS + idx % MP] = v[u];
       }
     }
     for (int q = threadIdx.x; q < EC; q += blockDim.x) jl[q] = col[c0 + (q < ne ? q : 0)];
     __syncthreads();
-    const int ns = (ne + 3) / 4;
     // three-stage pipeline: the features of steps st+1, st+2 are loaded
     // while the MFMAs of step st run
     float4 bA[NB], bB[NB];
@@ -1706,7 +1707,7 @@ bool outer_agg_supported(int L, int C, int H) {
   return o.nw >= 1 && o.nw <= (outer_ntw(L) == 8 ? 8 : 16) && o.lds <= 160 * 1024;
 }
 
-hipError_t launch_outer_agg(const DevTables& t, const double* Rp, const int64_t* row_ptr, const int32_t* col,
+hipError_t launch_outer_agg(const DevTables& t, const float* Rp, const int64_t* row_ptr, const int32_t* col,
                             const int32_t* col_pair, const float* alpha_hm, int64_t n_edges, const float* feat,
                             const int32_t* order, const int* cmeta, const float* ccoef, int ck, int cgroups, int n,
                             int C, int H, float* S, hipStream_t s) {

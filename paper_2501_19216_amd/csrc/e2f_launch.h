@@ -105,12 +105,12 @@ hipError_t launch_alpha_head_major(const float* alpha, int64_t n_edges, int H, f
 // y[order[r]] from S row r (head-major like T), r < n; shared_s: every r
 // reads S row 0
 // S rows r < n (receivers order[r]) by aggregating the uncoupled node products
-// alpha_ij R(p_j) (x) h_j and coupling per receiver (no T): Rp [pairs][nk]
+// alpha_ij R(p_j) (x) h_j and coupling per receiver (no T): Rp [pairs][nk] float32
 // (pair col_pair[e] of edge e), alpha_hm [H][n_edges] or NULL (ones)
 // with the coupling schedule of couple_schedule(tables, outer_agg_groups(L, C, H))
 bool outer_agg_supported(int L, int C, int H);
 int outer_agg_groups(int L, int C, int H);
-hipError_t launch_outer_agg(const DevTables& t, const double* Rp, const int64_t* row_ptr, const int32_t* col,
+hipError_t launch_outer_agg(const DevTables& t, const float* Rp, const int64_t* row_ptr, const int32_t* col,
                             const int32_t* col_pair, const float* alpha_hm, int64_t n_edges, const float* feat,
                             const int32_t* order, const int* cmeta, const float* ccoef, int ck, int cgroups, int n,
                             int C, int H, float* S, hipStream_t s);
