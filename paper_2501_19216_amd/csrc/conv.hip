@@ -1720,7 +1720,7 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Rp, const int64_t* 
     const char* v = getenv("E2F_OUTER_RPW");
     return v ? atoi(v) : 0;
   }();
-  const int rpw = rpw_env > 0 ? rpw_env : 4;
+  const int rpw = rpw_env > 0 ? rpw_env : 8;
   const size_t sched_b = sizeof(float) * 2 * (size_t)ck * cgroups;
   const bool sched_lds = o.lds + sched_b <= 80 * 1024;
   const int work_floats = sched_lds ? (int)(o.lds / sizeof(float)) : 0;
