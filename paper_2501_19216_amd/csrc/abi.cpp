@@ -281,6 +281,8 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
   }
   d.q_coef = nullptr;
   d.k_coef = nullptr;
+  d.z_ptr = d.z_k = nullptr;
+  d.z_coef = nullptr;
   d.max_qslots = t.max_qslots;
   d.m_slots = t.m_slots();
   for (int a = 0; a <= L; ++a) d.tp_rs[a] = t.tp_rs[a];
@@ -324,6 +326,24 @@ e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStr
     for (size_t e = 0; e < c.size(); ++e) c[e] = sf.path[e] < 0 ? 0.0 : sf.unit[e] * w[sf.path[e]];
     push_array(blob, o, c);
   }
+  // the filter coefficients again, keyed by (be, q) with entries (k, coef) in
+  // ascending k: o[4 + L] .. o[6 + L]
+  const int nk = t.nk;
+  std::vector<int> zp((size_t)nk * nk + 1, 0), zk(t.k_unit.size());
+  std::vector<float> zc(t.k_unit.size());
+  for (int sidx = 0; sidx < nk * nk; ++sidx)
+    for (int e = t.k_ptr[sidx]; e < t.k_ptr[sidx + 1]; ++e) ++zp[(size_t)t.k_ridx[e] * nk + sidx % nk + 1];
+  for (size_t key = 0; key < (size_t)nk * nk; ++key) zp[key + 1] += zp[key];
+  std::vector<int> fill(zp.begin(), zp.end() - 1);
+  for (int sidx = 0; sidx < nk * nk; ++sidx)
+    for (int e = t.k_ptr[sidx]; e < t.k_ptr[sidx + 1]; ++e) {
+      const int at = fill[(size_t)t.k_ridx[e] * nk + sidx % nk]++;
+      zk[at] = sidx / nk;
+      zc[at] = (float)(t.k_unit[e] * w[t.k_path[e]]);
+    }
+  push_array(blob, o, zp);
+  push_array(blob, o, zk);
+  push_array(blob, o, zc);
   E2F_HIP(hipStreamSynchronize(s));  // earlier work may still read the old coefficients
   if (ctx->coef_mem[L]) E2F_HIP(hipFree(ctx->coef_mem[L]));
   ctx->coef_mem[L] = nullptr;
@@ -336,6 +356,9 @@ e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStr
   ctx->dev[L].k_coef = (const float*)((char*)mem + o[1]);
   ctx->dev[L].rc_coef = (const double*)((char*)mem + o[2]);
   for (int f = 0; f <= L; ++f) ctx->rcf_coef[L][f] = (const double*)((char*)mem + o[3 + f]);
+  ctx->dev[L].z_ptr = (const int*)((char*)mem + o[4 + L]);
+  ctx->dev[L].z_k = (const int*)((char*)mem + o[5 + L]);
+  ctx->dev[L].z_coef = (const float*)((char*)mem + o[6 + L]);
   return E2F_OK;
 }
 
@@ -984,8 +1007,10 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
     E2F_TIMED("mix", launch_mix(L, grad_out, WT, p->mix_dtype == E2F_BF16, n, C, gyb, s));
     gy = gyb;
   }
-  // ---- attention weights: per edge, by the edge filter
-  if (grad_alpha && n_edges > 0)
+  // ---- attention weights: per edge, by the edge filter (in the fused pass
+  // with the forces below where the head width allows)
+  const bool fused = edge_geom_supported(C, H);
+  if (grad_alpha && n_edges > 0 && !fused)
     E2F_TIMED("edge_vjp_alpha", launch_edge_vjp_alpha(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, n, C, H,
                                                       grad_alpha, s));
   if (n_edges == 0) {
@@ -1012,11 +1037,13 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
                                                   cnt, rowT, colT, alpha ? alphaT : nullptr, tmp, tmp_b, s));
   }
   // ---- positions: per-edge force vectors, then per atom received minus sent
-  if (grad_pos) {
-    float* gedge = cd.take<float>((size_t)n_edges * 3);
+  float* gedge = grad_pos ? cd.take<float>((size_t)n_edges * 3) : nullptr;
+  if (fused && (grad_alpha || gedge))
+    E2F_TIMED("edge_geom", launch_edge_geom(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, alpha, n, C, H, grad_alpha,
+                                            gedge, s));
+  else if (gedge)
     E2F_TIMED("edge_force", launch_edge_force(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, alpha, n, C, H, gedge, s));
-    E2F_TIMED("edge_force", launch_force_gather(row_ptr, rowT, perm, gedge, n, grad_pos, s));
-  }
+  if (gedge) E2F_TIMED("force_gather", launch_force_gather(row_ptr, rowT, perm, gedge, n, grad_pos, s));
   // ---- features: the same layer on the transposed graph, input degree o,
   // output degree a, weights w[a][f][o] kappa(a,f,o) (-1)^f
   if (grad_feat) {

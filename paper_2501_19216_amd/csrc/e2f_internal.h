@@ -125,6 +125,7 @@ struct DevTables {
   const int* tp_k; const int* tp_off; const int* tp_meta; const double* tp_coef;
   const int* rc_k; const int* rc_off; const int* rc_meta; const double* rc_coef;  // rc_coef includes path weights
   const int* ag_ptr; const int* ag_idx; const float* ag_coef;
+  const int* z_ptr; const int* z_k; const float* z_coef;        // filter coefficients keyed by (be, q); weighted
   int max_qslots, m_slots;
   int tp_rs[kMaxL + 1], tp_mo[kMaxL + 2];
 };

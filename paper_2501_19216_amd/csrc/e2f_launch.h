@@ -136,6 +136,12 @@ hipError_t launch_attention(const float* pos, const float* q, const float* k, in
 hipError_t launch_edge_force(const DevTables& t, const float* pos, const float* feat, const float* gy,
                              const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n, int C, int H,
                              float* gedge, hipStream_t s);
+// Both per-edge backward products in one pass (either output may be NULL):
+// galpha [E][H], gedge [E][3]; needs C/H a multiple of 16, at most 128.
+bool edge_geom_supported(int C, int H);
+hipError_t launch_edge_geom(const DevTables& t, const float* pos, const float* feat, const float* gy,
+                            const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n, int C, int H,
+                            float* galpha, float* gedge, hipStream_t s);
 hipError_t launch_force_gather(const int64_t* row_ptr, const int64_t* rowT, const int32_t* perm, const float* gedge,
                                int n, float* gpos, hipStream_t s);
 hipError_t launch_edge_vjp_alpha(const DevTables& t, const float* pos, const float* feat, const float* gy,

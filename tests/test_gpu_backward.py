@@ -61,7 +61,7 @@ def check(e2f, ctx, pos, rp, ci, L, C, H, cutoff, seed, mix=None, bf16=False, gi
     gf_ref, ga_ref = o.conv_edge_vjp(L, H, pos, feat, gy, rp, ci, alpha, w)
     atoms = np.linspace(0, n - 1, min(n, 48)).astype(np.int32)
     gp_ref = o.conv_edge_grad_pos(L, H, pos, feat, gy, rp, ci, alpha, w, atoms=atoms)
-    print("n %d L %d C %d: case" % (n, L, C), flush=True)
+    print("n %d L %d C %d H %d rc %g: case" % (n, L, C, H, cutoff), flush=True)
     gf, ga, gp = e2f.e2f_wigner6j_conv_backward(ctx, gpu(pos), gpu(feat), gpu(gout), gpu(rp), gpu(ci), gpu(alpha), L,
                                                 H, cutoff, mix_w=mw, graph_id=gpu(gid), want_pos=True)
     ef = o.max_rel_err(gf.cpu().numpy(), gf_ref, L)
@@ -76,13 +76,18 @@ def check(e2f, ctx, pos, rp, ci, L, C, H, cutoff, seed, mix=None, bf16=False, gi
     return feat, alpha, gout, w, gf_ref, ga_ref
 
 
-@pytest.mark.parametrize("L,C,H,mix", [(2, 16, 4, False), (3, 32, 4, True), (4, 64, 8, False), (6, 16, 4, False)])
-def test_backward_radius_graph(e2f, ctx, L, C, H, mix):
+# head widths 4 and 8 take the per-edge kernels, multiples of 16 the per-receiver
+# MFMA product (L=6 runs its filter rows in several passes; the 7 A cutoff
+# gives receivers of more than 128 edges, several edge chunks)
+@pytest.mark.parametrize("L,C,H,mix,rc", [(2, 16, 4, False, 5.0), (3, 32, 4, True, 5.0), (4, 64, 8, False, 5.0),
+                                          (6, 16, 4, False, 5.0), (4, 128, 8, False, 5.0), (2, 64, 2, True, 5.0),
+                                          (3, 64, 1, False, 5.0), (6, 32, 2, False, 5.0), (4, 32, 2, False, 7.0)])
+def test_backward_radius_graph(e2f, ctx, L, C, H, mix, rc):
     rng = np.random.default_rng(L)
     pos = syn.quantize(rng.uniform(0, 14, size=(400, 3)))
-    rp, ci = o.neighbor_list(pos, 5.0)
+    rp, ci = o.neighbor_list(pos, rc)
     m = (rng.standard_normal((L + 1, C, C)) / np.sqrt(C)).astype(np.float32) if mix else None
-    check(e2f, ctx, pos, rp, ci, L, C, H, 5.0, 10 + L, mix=m)
+    check(e2f, ctx, pos, rp, ci, L, C, H, rc, 10 + L, mix=m)
 
 
 def test_backward_bf16_mixing(e2f, ctx):
@@ -102,11 +107,12 @@ def test_backward_knn_graph_is_transposed(e2f, ctx):
     check(e2f, ctx, pos, rp, ci, 3, 32, 4, float(d.max()) * 1.001, 5)
 
 
-def test_backward_graphs_and_single_outputs(e2f, ctx):
+@pytest.mark.parametrize("H", [8, 2])
+def test_backward_graphs_and_single_outputs(e2f, ctx, H):
     inp = syn.make_inputs(syn.WORKLOADS["molecules256x30_L3"], n_atoms=40 * 30)
     rp, ci = o.neighbor_list(inp.pos, 5.0, inp.graph_id)
-    feat, alpha, gout, w, gf_ref, ga_ref = check(e2f, ctx, inp.pos, rp, ci, 3, 32, 8, 5.0, 6, gid=inp.graph_id)
-    args = (gpu(inp.pos), gpu(feat), gpu(gout), gpu(rp), gpu(ci), gpu(alpha), 3, 8, 5.0)
+    feat, alpha, gout, w, gf_ref, ga_ref = check(e2f, ctx, inp.pos, rp, ci, 3, 32, H, 5.0, 6, gid=inp.graph_id)
+    args = (gpu(inp.pos), gpu(feat), gpu(gout), gpu(rp), gpu(ci), gpu(alpha), 3, H, 5.0)
     gf, ga, _ = e2f.e2f_wigner6j_conv_backward(ctx, *args, graph_id=gpu(inp.graph_id), want_alpha=False)
     assert ga is None and o.max_rel_err(gf.cpu().numpy(), gf_ref, 3) <= TOL_F32
     gf, ga, _ = e2f.e2f_wigner6j_conv_backward(ctx, *args, graph_id=gpu(inp.graph_id), want_feat=False)
@@ -114,7 +120,7 @@ def test_backward_graphs_and_single_outputs(e2f, ctx):
     gf, ga, gp = e2f.e2f_wigner6j_conv_backward(ctx, *args, graph_id=gpu(inp.graph_id), want_feat=False,
                                                 want_alpha=False, want_pos=True)
     at = np.arange(0, 1200, 37, dtype=np.int32)
-    gp_ref = o.conv_edge_grad_pos(3, 8, inp.pos, feat, gout.astype(np.float64), rp, ci, alpha, w, atoms=at)
+    gp_ref = o.conv_edge_grad_pos(3, H, inp.pos, feat, gout.astype(np.float64), rp, ci, alpha, w, atoms=at)
     assert gf is None and ga is None
     assert np.abs(gp.cpu().numpy()[at] - gp_ref).max() <= TOL_F32 * np.abs(gp_ref).max()
 
