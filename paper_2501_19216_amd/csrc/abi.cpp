@@ -80,6 +80,14 @@ struct e2f_ctx {
     float* coef = nullptr;
   };
   std::map<std::pair<int, int>, Couple> couple;
+  // schedules of the backward's filter contraction, per (L, rows per pass)
+  struct Geom {
+    int qc = 0, tot = 0;  // filter rows per pass, schedule entries
+    int* meta = nullptr;
+    float* unit = nullptr;
+    int* oc = nullptr;  // [nchunk][2]: offset, steps
+  };
+  std::map<std::pair<int, int>, Geom> geom;  // per (L, head width)
 };
 
 namespace {
@@ -197,6 +205,37 @@ e2f_status couple_of(e2f_ctx* ctx, int L, int groups, const e2f_ctx::Couple*& ou
   return E2F_OK;
 }
 
+// The backward's filter-contraction schedule for (L, head width dh), uploaded
+// on first use: the most filter rows per pass whose LDS (gy slice, schedule
+// up to L = 4, Z) fits 40 KB, so that four workgroups share a CU; else one
+// row per pass.
+e2f_status geom_of(e2f_ctx* ctx, int L, int dh, const e2f_ctx::Geom*& out) {
+  auto key = std::make_pair(L, dh);
+  auto it = ctx->geom.find(key);
+  if (it == ctx->geom.end()) {
+    const LayerTables& t = ctx->host[L];
+    GeomSchedule gs;
+    for (int qc = t.nk; qc >= 1; --qc) {
+      gs = geom_schedule(t, qc);
+      if (edge_geom_lds(L, dh, qc, (int)gs.meta.size()) <= 40960) break;
+    }
+    std::vector<int> oc;
+    for (int c = 0; c < gs.nchunk; ++c) oc.push_back(gs.off[c]), oc.push_back(gs.ck[c]);
+    e2f_ctx::Geom g;
+    g.qc = gs.qc;
+    g.tot = (int)gs.meta.size();
+    E2F_HIP(hipMalloc((void**)&g.meta, sizeof(int) * std::max<size_t>(gs.meta.size(), 1)));
+    E2F_HIP(hipMalloc((void**)&g.unit, sizeof(float) * std::max<size_t>(gs.unit.size(), 1)));
+    E2F_HIP(hipMalloc((void**)&g.oc, sizeof(int) * std::max<size_t>(oc.size(), 1)));
+    E2F_HIP(hipMemcpy(g.meta, gs.meta.data(), sizeof(int) * gs.meta.size(), hipMemcpyHostToDevice));
+    E2F_HIP(hipMemcpy(g.unit, gs.unit.data(), sizeof(float) * gs.unit.size(), hipMemcpyHostToDevice));
+    E2F_HIP(hipMemcpy(g.oc, oc.data(), sizeof(int) * oc.size(), hipMemcpyHostToDevice));
+    it = ctx->geom.emplace(key, g).first;
+  }
+  out = &it->second;
+  return E2F_OK;
+}
+
 e2f_status upload_tables(e2f_ctx* ctx, int L) {
   const LayerTables& t = ctx->host[L];
   std::vector<char> blob;
@@ -281,8 +320,7 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
   }
   d.q_coef = nullptr;
   d.k_coef = nullptr;
-  d.z_ptr = d.z_k = nullptr;
-  d.z_coef = nullptr;
+  d.w_f = nullptr;
   d.max_qslots = t.max_qslots;
   d.m_slots = t.m_slots();
   for (int a = 0; a <= L; ++a) d.tp_rs[a] = t.tp_rs[a];
@@ -326,24 +364,8 @@ e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStr
     for (size_t e = 0; e < c.size(); ++e) c[e] = sf.path[e] < 0 ? 0.0 : sf.unit[e] * w[sf.path[e]];
     push_array(blob, o, c);
   }
-  // the filter coefficients again, keyed by (be, q) with entries (k, coef) in
-  // ascending k: o[4 + L] .. o[6 + L]
-  const int nk = t.nk;
-  std::vector<int> zp((size_t)nk * nk + 1, 0), zk(t.k_unit.size());
-  std::vector<float> zc(t.k_unit.size());
-  for (int sidx = 0; sidx < nk * nk; ++sidx)
-    for (int e = t.k_ptr[sidx]; e < t.k_ptr[sidx + 1]; ++e) ++zp[(size_t)t.k_ridx[e] * nk + sidx % nk + 1];
-  for (size_t key = 0; key < (size_t)nk * nk; ++key) zp[key + 1] += zp[key];
-  std::vector<int> fill(zp.begin(), zp.end() - 1);
-  for (int sidx = 0; sidx < nk * nk; ++sidx)
-    for (int e = t.k_ptr[sidx]; e < t.k_ptr[sidx + 1]; ++e) {
-      const int at = fill[(size_t)t.k_ridx[e] * nk + sidx % nk]++;
-      zk[at] = sidx / nk;
-      zc[at] = (float)(t.k_unit[e] * w[t.k_path[e]]);
-    }
-  push_array(blob, o, zp);
-  push_array(blob, o, zk);
-  push_array(blob, o, zc);
+  std::vector<float> wf(w.begin(), w.end());  // o[4 + L]
+  push_array(blob, o, wf);
   E2F_HIP(hipStreamSynchronize(s));  // earlier work may still read the old coefficients
   if (ctx->coef_mem[L]) E2F_HIP(hipFree(ctx->coef_mem[L]));
   ctx->coef_mem[L] = nullptr;
@@ -356,9 +378,7 @@ e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStr
   ctx->dev[L].k_coef = (const float*)((char*)mem + o[1]);
   ctx->dev[L].rc_coef = (const double*)((char*)mem + o[2]);
   for (int f = 0; f <= L; ++f) ctx->rcf_coef[L][f] = (const double*)((char*)mem + o[3 + f]);
-  ctx->dev[L].z_ptr = (const int*)((char*)mem + o[4 + L]);
-  ctx->dev[L].z_k = (const int*)((char*)mem + o[5 + L]);
-  ctx->dev[L].z_coef = (const float*)((char*)mem + o[6 + L]);
+  ctx->dev[L].w_f = (const float*)((char*)mem + o[4 + L]);
   return E2F_OK;
 }
 
@@ -518,6 +538,11 @@ void e2f_destroy(e2f_ctx* ctx) {
     for (auto& kv : ctx->couple) {
       if (kv.second.meta) (void)hipFree(kv.second.meta);
       if (kv.second.coef) (void)hipFree(kv.second.coef);
+    }
+    for (auto& kv : ctx->geom) {
+      if (kv.second.meta) (void)hipFree(kv.second.meta);
+      if (kv.second.unit) (void)hipFree(kv.second.unit);
+      if (kv.second.oc) (void)hipFree(kv.second.oc);
     }
     for (auto& r : ctx->recs) {
       ctx->pool.push_back(r.start);
@@ -1038,9 +1063,12 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
   }
   // ---- positions: per-edge force vectors, then per atom received minus sent
   float* gedge = grad_pos ? cd.take<float>((size_t)n_edges * 3) : nullptr;
-  if (fused && (grad_alpha || gedge))
-    E2F_TIMED("edge_geom", launch_edge_geom(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, alpha, n, C, H, grad_alpha,
-                                            gedge, s));
+  if (fused && (grad_alpha || gedge)) {
+    const e2f_ctx::Geom* gsch = nullptr;
+    if ((rs = geom_of(ctx, L, C / H, gsch)) != E2F_OK) return rs;
+    E2F_TIMED("edge_geom", launch_edge_geom(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, alpha, n, C, H, gsch->qc,
+                                            gsch->meta, gsch->unit, gsch->oc, gsch->tot, grad_alpha, gedge, s));
+  }
   else if (gedge)
     E2F_TIMED("edge_force", launch_edge_force(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, alpha, n, C, H, gedge, s));
   if (gedge) E2F_TIMED("force_gather", launch_force_gather(row_ptr, rowT, perm, gedge, n, grad_pos, s));

@@ -1274,160 +1274,198 @@ __global__ __launch_bounds__(256) void k_edge_force(DevTables t, const float* __
 // of 16), edges as columns (tiles of 16 edges; NTE tiles per wave, the
 // wave's tiles are wave + NW et) and (q, c) as the reduction: lane group k4
 // takes channels 16 s + 4 k4 .. + 3 of row q as one float4, and MFMA w of
-// four uses component w.  Z lives in LDS, qc rows q at a time, with row
-// stride qc dh + 4 floats (the 16 rows be of an operand read start in
-// distinct bank quadruples).  Edge chunks of NW NTE 16 edges; Z is rebuilt per
-// chunk and head.  Each output element has one writer.
+// four uses component w.  LDS holds, per workgroup, the schedule of the Z
+// sums (path weights folded in, staged once; read from global memory above
+// L = 4, where it outgrows LDS), the head's slice of gy_i and Z
+// for qc rows q at a time, with row stride qc dh + 4 floats (the 16 rows be
+// of an operand read start in distinct bank quadruples).  A workgroup takes
+// rpw consecutive receivers; edge chunks of NW NTE 16 edges, Z rebuilt per
+// chunk, head and row pass.  Each output element has one writer.
 template <int L, int NTE, bool WA, bool WP>
 __global__ __launch_bounds__(128) void k_edge_geom(DevTables t, const float* __restrict__ pos,
                                                    const float* __restrict__ feat, const float* __restrict__ gy,
                                                    const int64_t* __restrict__ row_ptr,
                                                    const int32_t* __restrict__ col, const float* __restrict__ alpha,
-                                                   int n, int C, int H, int qc, float* __restrict__ galpha,
-                                                   float* __restrict__ gedge) {
+                                                   int n, int rpw, int C, int H, int qc,
+                                                   const int* __restrict__ gmeta, const float* __restrict__ gunit,
+                                                   const int* __restrict__ goc, int gtot,
+                                                   float* __restrict__ galpha, float* __restrict__ gedge) {
   constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16;
+  constexpr bool STAGED = L <= 4;  // the schedule in LDS (it outgrows LDS above L = 4)
   extern __shared__ float4 sm4[];
-  float* Z = (float*)sm4;  // [NK be][ZS]: Z[be][qq][c] at be*ZS + qq*dh + c
   const int dh = C / H, dq = dh >> 2, S16 = dh >> 4, ZS = qc * dh + 4;
-  // workgroup -> receiver: the receivers of one XCD are contiguous
-  const int nxr = (n + 7) / 8, i = (blockIdx.x % 8) * nxr + blockIdx.x / 8;
-  if (i >= n) return;  // uniform over the workgroup
+  float* gyl = (float*)sm4;  // [NK][dh]: gy_i of the head
+  // STAGED: [gtot] schedule, [gtot] its coefficients times the path weights
+  int* smeta = (int*)(gyl + NK * dh);
+  float* sunit = gyl + NK * dh + gtot;
+  float* Z = gyl + NK * dh + (STAGED ? 2 * gtot : 0);  // [NK be][ZS]: Z[be][qq][c] at be*ZS + qq*dh + c
+  if (STAGED)
+    for (int x = threadIdx.x; x < gtot; x += blockDim.x) {
+      const int m = gmeta[x];
+      smeta[x] = m;
+      sunit[x] = gunit[x] * t.w_f[(m >> 18) & 511];
+    }
+  // workgroup -> rpw consecutive receivers; the receivers of one XCD are contiguous
+  const int nxr = (n + 7) / 8, xcd = blockIdx.x % 8;
+  const int rfirst = xcd * nxr + (blockIdx.x / 8) * rpw;
+  const int rlast = min(min(rfirst + rpw, (xcd + 1) * nxr), n);  // uniform over the workgroup
   const int NW = blockDim.x >> 6, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int l16 = lane & 15, k4 = lane >> 4;
-  const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
-  const float xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
-  const float* gyi = gy + (size_t)i * NK * C;
-  for (int64_t c0 = e0; c0 < e1; c0 += NW * NTE * 16) {
-    const int ne = (int)min((int64_t)NW * NTE * 16, e1 - c0);
-    const int ntiles = (ne + 15) / 16;
-    int jn[NTE];
-    bool ev[NTE];
-    float dx[NTE], dy[NTE], dz[NTE];
-    float Rv[NTE][MT][4];
-    v4f W[NTE][MT];
-#pragma unroll
-    for (int et = 0; et < NTE; ++et) {
-      const int nb = (wave + NW * et) * 16 + l16;
-      ev[et] = nb < ne;
-      jn[et] = col[c0 + (ev[et] ? nb : 0)];  // columns past ne read a valid sender, never stored
-      dx[et] = xi - pos[3 * jn[et]], dy[et] = yi - pos[3 * jn[et] + 1], dz[et] = zi - pos[3 * jn[et] + 2];
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        W[et][mt] = (v4f){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int be = mt * 16 + 4 * k4 + v;
-          Rv[et][mt][v] = (WA && be < NK) ? sh_poly<float>(t, be, dx[et], dy[et], dz[et]) : 0.0f;
-        }
-      }
-    }
-    for (int h = 0; h < H; ++h) {
-      v4f X[NTE][MT];
-#pragma unroll
-      for (int et = 0; et < NTE; ++et)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) X[et][mt] = (v4f){0.f, 0.f, 0.f, 0.f};
-      for (int q0 = 0; q0 < NK; q0 += qc) {
-        const int nq = min(qc, NK - q0);
-        __syncthreads();  // the previous steps have read Z
-        for (int it = threadIdx.x; it < NK * nq * dq; it += blockDim.x) {
-          const int be = it / (nq * dq), rem = it % (nq * dq), qq = rem / dq, c4 = rem % dq;
-          const int key = be * NK + q0 + qq;
-          float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-          for (int e = t.z_ptr[key]; e < t.z_ptr[key + 1]; ++e) {
-            const float cf = t.z_coef[e];
-            const float4 g = *(const float4*)(gyi + (size_t)t.z_k[e] * C + h * dh + 4 * c4);
-            v.x += cf * g.x, v.y += cf * g.y, v.z += cf * g.z, v.w += cf * g.w;
-          }
-          *(float4*)(Z + be * ZS + qq * dh + 4 * c4) = v;
-        }
-        __syncthreads();
-        // two-stage pipeline: the features of step st+1 load while the MFMAs of st run
-        const int nst = nq * S16;
-        auto loadb = [&](int st, float4* b) {
-          const int sc = min(st, nst - 1);
-          const int q = q0 + sc / S16, s = sc % S16;
-#pragma unroll
-          for (int et = 0; et < NTE; ++et)
-            b[et] = *(const float4*)(feat + ((size_t)jn[et] * NK + q) * C + h * dh + 16 * s + 4 * k4);
-        };
-        auto mma = [&](int st, const float4* b) {
-          const int qq = st / S16, s = st % S16;
-          float4 a[MT];
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            const int be = mt * 16 + l16;
-            a[mt] = be < NK ? *(const float4*)(Z + be * ZS + qq * dh + 16 * s + 4 * k4)
-                            : make_float4(0.f, 0.f, 0.f, 0.f);
-          }
-#pragma unroll
-          for (int et = 0; et < NTE; ++et) {
-            if (wave + NW * et >= ntiles) continue;  // uniform over the wave
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-              X[et][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt].x, b[et].x, X[et][mt], 0, 0, 0);
-              X[et][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt].y, b[et].y, X[et][mt], 0, 0, 0);
-              X[et][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt].z, b[et].z, X[et][mt], 0, 0, 0);
-              X[et][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt].w, b[et].w, X[et][mt], 0, 0, 0);
-            }
-          }
-        };
-        float4 bA[NTE], bB[NTE];
-        loadb(0, bA);
-        for (int st = 0; st < nst; st += 2) {
-          loadb(st + 1, bB);
-          __builtin_amdgcn_sched_barrier(0);
-          mma(st, bA);
-          __builtin_amdgcn_sched_barrier(0);
-          loadb(st + 2, bA);
-          __builtin_amdgcn_sched_barrier(0);
-          if (st + 1 < nst) mma(st + 1, bB);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      }
-      // lane (k4, l16) holds X_h[be = mt*16 + 4 k4 + v][edge column l16]
+  const int grp = threadIdx.x >> 2, sub = threadIdx.x & 3;  // kGeomGroups groups of four threads
+  for (int i = rfirst; i < rlast; ++i) {
+    const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+    const float xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
+    const float* gyi = gy + (size_t)i * NK * C;
+    for (int64_t c0 = e0; c0 < e1; c0 += NW * NTE * 16) {
+      const int ne = (int)min((int64_t)NW * NTE * 16, e1 - c0);
+      const int ntiles = (ne + 15) / 16;
+      int jn[NTE];
+      bool ev[NTE];
+      float dx[NTE], dy[NTE], dz[NTE];
+      float Rv[NTE][MT][4];
+      v4f W[NTE][MT];
 #pragma unroll
       for (int et = 0; et < NTE; ++et) {
-        if (wave + NW * et >= ntiles) continue;  // uniform over the wave
-        const int64_t e = c0 + (wave + NW * et) * 16 + l16;
-        if (WA) {
-          float p = 0.0f;
+        const int nb = (wave + NW * et) * 16 + l16;
+        ev[et] = nb < ne;
+        jn[et] = col[c0 + (ev[et] ? nb : 0)];  // columns past ne read a valid sender, never stored
+        dx[et] = xi - pos[3 * jn[et]], dy[et] = yi - pos[3 * jn[et] + 1], dz[et] = zi - pos[3 * jn[et] + 2];
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) p += Rv[et][mt][v] * X[et][mt][v];
-          p += __shfl_xor(p, 16);
-          p += __shfl_xor(p, 32);
-          if (k4 == 0 && ev[et]) galpha[e * H + h] = p;
-        }
-        if (WP) {
-          const float aw = (alpha && ev[et]) ? alpha[e * H + h] : 1.0f;
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) W[et][mt] += aw * X[et][mt];
-        }
-      }
-    }
-    if (WP) {
-#pragma unroll
-      for (int et = 0; et < NTE; ++et) {
-        if (wave + NW * et >= ntiles) continue;  // uniform over the wave
-        float fx = 0.f, fy = 0.f, fz = 0.f;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int mt = 0; mt < MT; ++mt) {
+          W[et][mt] = (v4f){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const int be = mt * 16 + 4 * k4 + v;
-            if (be < NK) {
-              float gx, gyy, gz;
-              sh_poly_grad<float>(t, be, dx[et], dy[et], dz[et], gx, gyy, gz);
-              fx += gx * W[et][mt][v], fy += gyy * W[et][mt][v], fz += gz * W[et][mt][v];
+            Rv[et][mt][v] = (WA && be < NK) ? sh_poly<float>(t, be, dx[et], dy[et], dz[et]) : 0.0f;
+          }
+        }
+      }
+      for (int h = 0; h < H; ++h) {
+        // every thread has passed a barrier since the last Z sums read gyl
+        for (int x = threadIdx.x; x < NK * dq; x += blockDim.x)
+          *(float4*)(gyl + 4 * x) = *(const float4*)(gyi + (size_t)(x / dq) * C + h * dh + 4 * (x % dq));
+        v4f X[NTE][MT];
+#pragma unroll
+        for (int et = 0; et < NTE; ++et)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) X[et][mt] = (v4f){0.f, 0.f, 0.f, 0.f};
+        for (int q0 = 0; q0 < NK; q0 += qc) {
+          const int nq = min(qc, NK - q0);
+          __syncthreads();  // gyl is staged; the previous steps have read Z
+          {
+            // Z rows of this pass: group grp walks its schedule entries, each
+            // of its four threads takes the channel quads sub, sub + 4, ..
+            const int ch = q0 / qc, off = goc[2 * ch], ck = goc[2 * ch + 1];
+            for (int cq = sub; cq < dq; cq += 4) {
+              float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+              for (int k = 0; k < ck; ++k) {
+                const int x = off + k * kGeomGroups + grp;
+                const int m = STAGED ? smeta[x] : gmeta[x];
+                const float cf = STAGED ? sunit[x] : gunit[x] * t.w_f[(m >> 18) & 511];
+                const float4 g = *(const float4*)(gyl + (m & 63) * dh + 4 * cq);
+                v.x += cf * g.x, v.y += cf * g.y, v.z += cf * g.z, v.w += cf * g.w;
+                if (m < 0) {
+                  *(float4*)(Z + ((m >> 6) & 63) * ZS + ((m >> 12) & 63) * dh + 4 * cq) = v;
+                  v = make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+              }
             }
           }
-        fx += __shfl_xor(fx, 16), fy += __shfl_xor(fy, 16), fz += __shfl_xor(fz, 16);
-        fx += __shfl_xor(fx, 32), fy += __shfl_xor(fy, 32), fz += __shfl_xor(fz, 32);
-        if (k4 == 0 && ev[et]) {
+          __syncthreads();
+          // three-stage pipeline: the features of steps st+1, st+2 load while
+          // the MFMAs of st run
+          const int nst = nq * S16;
+          auto loadb = [&](int st, float4* b) {
+            const int sc = min(st, nst - 1);
+            const int q = q0 + sc / S16, s = sc % S16;
+#pragma unroll
+            for (int et = 0; et < NTE; ++et)
+              b[et] = *(const float4*)(feat + ((size_t)jn[et] * NK + q) * C + h * dh + 16 * s + 4 * k4);
+          };
+          auto mma = [&](int st, const float4* b) {
+            const int qq = st / S16, s = st % S16;
+            float4 a[MT];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+              const int be = mt * 16 + l16;
+              a[mt] = be < NK ? *(const float4*)(Z + be * ZS + qq * dh + 16 * s + 4 * k4)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int et = 0; et < NTE; ++et) {
+              if (wave + NW * et >= ntiles) continue;  // uniform over the wave
+#pragma unroll
+              for (int mt = 0; mt < MT; ++mt) {
+                X[et][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt].x, b[et].x, X[et][mt], 0, 0, 0);
+                X[et][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt].y, b[et].y, X[et][mt], 0, 0, 0);
+                X[et][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt].z, b[et].z, X[et][mt], 0, 0, 0);
+                X[et][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt].w, b[et].w, X[et][mt], 0, 0, 0);
+              }
+            }
+          };
+          float4 bA[NTE], bB[NTE], bC[NTE];
+          loadb(0, bA);
+          loadb(1, bB);
+          for (int st = 0; st < nst; st += 3) {
+            loadb(st + 2, bC);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(st, bA);
+            __builtin_amdgcn_sched_barrier(0);
+            loadb(st + 3, bA);
+            __builtin_amdgcn_sched_barrier(0);
+            if (st + 1 < nst) mma(st + 1, bB);
+            __builtin_amdgcn_sched_barrier(0);
+            loadb(st + 4, bB);
+            __builtin_amdgcn_sched_barrier(0);
+            if (st + 2 < nst) mma(st + 2, bC);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+        // lane (k4, l16) holds X_h[be = mt*16 + 4 k4 + v][edge column l16]
+#pragma unroll
+        for (int et = 0; et < NTE; ++et) {
+          if (wave + NW * et >= ntiles) continue;  // uniform over the wave
           const int64_t e = c0 + (wave + NW * et) * 16 + l16;
-          gedge[e * 3] = fx, gedge[e * 3 + 1] = fy, gedge[e * 3 + 2] = fz;
+          if (WA) {
+            float p = 0.0f;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+              for (int v = 0; v < 4; ++v) p += Rv[et][mt][v] * X[et][mt][v];
+            p += __shfl_xor(p, 16);
+            p += __shfl_xor(p, 32);
+            if (k4 == 0 && ev[et]) galpha[e * H + h] = p;
+          }
+          if (WP) {
+            const float aw = (alpha && ev[et]) ? alpha[e * H + h] : 1.0f;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) W[et][mt] += aw * X[et][mt];
+          }
+        }
+      }
+      if (WP) {
+#pragma unroll
+        for (int et = 0; et < NTE; ++et) {
+          if (wave + NW * et >= ntiles) continue;  // uniform over the wave
+          float fx = 0.f, fy = 0.f, fz = 0.f;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const int be = mt * 16 + 4 * k4 + v;
+              if (be < NK) {
+                float gx, gyy, gz;
+                sh_poly_grad<float>(t, be, dx[et], dy[et], dz[et], gx, gyy, gz);
+                fx += gx * W[et][mt][v], fy += gyy * W[et][mt][v], fz += gz * W[et][mt][v];
+              }
+            }
+          fx += __shfl_xor(fx, 16), fy += __shfl_xor(fy, 16), fz += __shfl_xor(fz, 16);
+          fx += __shfl_xor(fx, 32), fy += __shfl_xor(fy, 32), fz += __shfl_xor(fz, 32);
+          if (k4 == 0 && ev[et]) {
+            const int64_t e = c0 + (wave + NW * et) * 16 + l16;
+            gedge[e * 3] = fx, gedge[e * 3 + 1] = fy, gedge[e * 3 + 2] = fz;
+          }
         }
       }
     }
@@ -2084,23 +2122,32 @@ bool edge_geom_supported(int C, int H) {
   return C % H == 0 && (C / H) % 16 == 0 && C / H <= 128;
 }
 
+size_t edge_geom_lds(int L, int dh, int qc, int gtot) {
+  const size_t nk = (size_t)(L + 1) * (L + 1);
+  return sizeof(float) * (nk * dh + (L <= 4 ? 2 * (size_t)gtot : 0) + nk * (qc * dh + 4));
+}
+
 hipError_t launch_edge_geom(const DevTables& t, const float* pos, const float* feat, const float* gy,
                             const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n, int C, int H,
-                            float* galpha, float* gedge, hipStream_t s) {
+                            int qc, const int* gmeta, const float* gunit, const int* goc, int gtot, float* galpha,
+                            float* gedge, hipStream_t s) {
   if (n == 0 || (!galpha && !gedge)) return hipSuccess;
-  if (!edge_geom_supported(C, H)) return hipErrorInvalidValue;
+  if (!edge_geom_supported(C, H) || qc < 1 || qc > t.nk) return hipErrorInvalidValue;
   const int dh = C / H;
-  // rows q of Z per pass: about 40 KB of LDS, so that four workgroups fit a CU
-  const int qc = std::max(1, std::min(t.nk, (10240 / t.nk - 4) / dh));
-  const size_t lds = sizeof(float) * (size_t)t.nk * (qc * dh + 4);
+  const size_t lds = edge_geom_lds(t.L, dh, qc, gtot);
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
   const int mode = (galpha ? 1 : 0) + (gedge ? 2 : 0);
-  const unsigned grid = 8u * (unsigned)((n + 7) / 8);
+  int rpw = 4;
+  if (const char* v = getenv("E2F_GEOM_RPW")) rpw = std::max(1, atoi(v));
+  const int nxr = (n + 7) / 8;
+  const unsigned grid = 8u * (unsigned)((nxr + rpw - 1) / rpw);
   switch (t.L * 4 + mode) {
 #define E2F_G(LL, WA_, WP_)                                                                                   \
   case LL * 4 + (WA_ ? 1 : 0) + (WP_ ? 2 : 0):                                                                \
     if (hipError_t e = allow_lds(k_edge_geom<LL, (LL <= 4 ? 4 : 2), WA_, WP_>, lds); e != hipSuccess) return e; \
     k_edge_geom<LL, (LL <= 4 ? 4 : 2), WA_, WP_><<<grid, 128, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx,    \
-                                                                         alpha, n, C, H, qc, galpha, gedge); \
+                                                                         alpha, n, rpw, C, H, qc, gmeta,     \
+                                                                         gunit, goc, gtot, galpha, gedge);   \
     break;
 #define E2F_GL(LL) E2F_G(LL, true, false) E2F_G(LL, false, true) E2F_G(LL, true, true)
     E2F_GL(0) E2F_GL(1) E2F_GL(2) E2F_GL(3) E2F_GL(4) E2F_GL(5) E2F_GL(6)

@@ -110,6 +110,23 @@ struct CoupleSchedule {
   std::vector<float> coef;
 };
 CoupleSchedule couple_schedule(const LayerTables& t, int groups);
+
+// Schedule of the per-receiver filter contraction of the backward,
+// Z[be][q][c] = sum_k w(path) unit * gy[k][c], for filter rows q taken qc at a
+// time (chunk ch covers q in [ch*qc, min(nk, (ch+1)*qc))).  Per chunk the
+// keys (be, q) are spread over kGeomGroups groups by entry count; group g
+// walks entries off[ch] + k*kGeomGroups + g for k < ck[ch]; meta = k (bits
+// 0-5) | be << 6 | (q - ch*qc) << 12 | path << 18 | last (bit 31); a key
+// without entries stores its zero from one entry of unit 0; padding entries
+// are all zero and follow the group's last store.
+constexpr int kGeomGroups = 32;
+struct GeomSchedule {
+  int qc = 0, nchunk = 0;
+  std::vector<int> off, ck;
+  std::vector<int> meta;
+  std::vector<float> unit;
+};
+GeomSchedule geom_schedule(const LayerTables& t, int qc);
 int64_t node_tp_dim(int L);
 
 // ---------------------------------------------------------------- device side
@@ -125,7 +142,7 @@ struct DevTables {
   const int* tp_k; const int* tp_off; const int* tp_meta; const double* tp_coef;
   const int* rc_k; const int* rc_off; const int* rc_meta; const double* rc_coef;  // rc_coef includes path weights
   const int* ag_ptr; const int* ag_idx; const float* ag_coef;
-  const int* z_ptr; const int* z_k; const float* z_coef;        // filter coefficients keyed by (be, q); weighted
+  const float* w_f;  // path weights w[(a*(L+1) + f)*(L+1) + o] as float
   int max_qslots, m_slots;
   int tp_rs[kMaxL + 1], tp_mo[kMaxL + 2];
 };

@@ -139,9 +139,13 @@ hipError_t launch_edge_force(const DevTables& t, const float* pos, const float* 
 // Both per-edge backward products in one pass (either output may be NULL):
 // galpha [E][H], gedge [E][3]; needs C/H a multiple of 16, at most 128.
 bool edge_geom_supported(int C, int H);
+// LDS bytes of the backward kernel for qc filter rows per pass and a
+// schedule of gtot entries (staged in LDS up to L = 4)
+size_t edge_geom_lds(int L, int dh, int qc, int gtot);
 hipError_t launch_edge_geom(const DevTables& t, const float* pos, const float* feat, const float* gy,
                             const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n, int C, int H,
-                            float* galpha, float* gedge, hipStream_t s);
+                            int qc, const int* gmeta, const float* gunit, const int* goc, int gtot, float* galpha,
+                            float* gedge, hipStream_t s);
 hipError_t launch_force_gather(const int64_t* row_ptr, const int64_t* rowT, const int32_t* perm, const float* gedge,
                                int n, float* gpos, hipStream_t s);
 hipError_t launch_edge_vjp_alpha(const DevTables& t, const float* pos, const float* feat, const float* gy,

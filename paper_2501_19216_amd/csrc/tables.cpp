@@ -462,4 +462,59 @@ CoupleSchedule couple_schedule(const LayerTables& t, int groups) {
   return cs;
 }
 
+GeomSchedule geom_schedule(const LayerTables& t, int qc) {
+  GeomSchedule gs;
+  const int nk = t.nk, G = kGeomGroups;
+  gs.qc = qc;
+  gs.nchunk = (nk + qc - 1) / qc;
+  // entries (k, unit, path) of each key (be, q), in ascending k
+  struct Ent { int k, path; double unit; };
+  std::vector<std::vector<Ent>> ent((size_t)nk * nk);
+  for (int sidx = 0; sidx < nk * nk; ++sidx)
+    for (int e = t.k_ptr[sidx]; e < t.k_ptr[sidx + 1]; ++e)
+      ent[(size_t)t.k_ridx[e] * nk + sidx % nk].push_back({sidx / nk, t.k_path[e], t.k_unit[e]});
+  for (int ch = 0; ch < gs.nchunk; ++ch) {
+    const int q0 = ch * qc, nq = std::min(qc, nk - q0);
+    std::vector<int> keys;
+    for (int be = 0; be < nk; ++be)
+      for (int qq = 0; qq < nq; ++qq) keys.push_back(be * nk + q0 + qq);
+    auto len = [&](int key) { return std::max<int>(1, (int)ent[key].size()); };
+    std::stable_sort(keys.begin(), keys.end(), [&](int x, int y) { return len(x) > len(y); });
+    std::vector<std::vector<int>> per(G);
+    std::vector<int> load(G, 0);
+    for (int key : keys) {
+      int best = 0;
+      for (int g = 1; g < G; ++g)
+        if (load[g] < load[best]) best = g;
+      per[best].push_back(key);
+      load[best] += len(key);
+    }
+    const int K = *std::max_element(load.begin(), load.end());
+    const size_t base = gs.meta.size();
+    gs.off.push_back((int)base);
+    gs.ck.push_back(K);
+    gs.meta.resize(base + (size_t)K * G, 0);
+    gs.unit.resize(base + (size_t)K * G, 0.0f);
+    for (int g = 0; g < G; ++g) {
+      int k = 0;
+      for (int key : per[g]) {
+        const int be = key / nk, qq = key % nk - q0;
+        const int kb = (be << 6) | (qq << 12);
+        if (ent[key].empty()) {
+          gs.meta[base + (size_t)k * G + g] = kb | (int)0x80000000u;
+          ++k;
+          continue;
+        }
+        for (size_t e = 0; e < ent[key].size(); ++e, ++k) {
+          const bool last = e + 1 == ent[key].size();
+          gs.meta[base + (size_t)k * G + g] =
+              ent[key][e].k | kb | (ent[key][e].path << 18) | (last ? (int)0x80000000u : 0);
+          gs.unit[base + (size_t)k * G + g] = (float)ent[key][e].unit;
+        }
+      }
+    }
+  }
+  return gs;
+}
+
 }  // namespace e2f
