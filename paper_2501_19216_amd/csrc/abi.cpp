@@ -1032,12 +1032,6 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
     E2F_TIMED("mix", launch_mix(L, grad_out, WT, p->mix_dtype == E2F_BF16, n, C, gyb, s));
     gy = gyb;
   }
-  // ---- attention weights: per edge, by the edge filter (in the fused pass
-  // with the forces below where the head width allows)
-  const bool fused = edge_geom_supported(C, H);
-  if (grad_alpha && n_edges > 0 && !fused)
-    E2F_TIMED("edge_vjp_alpha", launch_edge_vjp_alpha(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, n, C, H,
-                                                      grad_alpha, s));
   if (n_edges == 0) {
     if (grad_pos) E2F_HIP(hipMemsetAsync(grad_pos, 0, sizeof(float) * (size_t)n * 3, s));
     if (grad_feat) E2F_HIP(hipMemsetAsync(grad_feat, 0, sizeof(float) * (size_t)n * nk * C, s));
@@ -1061,16 +1055,15 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
     E2F_TIMED("transpose", launch_transpose_graph(row_ptr, col_idx, alpha, n, n_edges, H, rows, iota, keys_out, perm,
                                                   cnt, rowT, colT, alpha ? alphaT : nullptr, tmp, tmp_b, s));
   }
-  // ---- positions: per-edge force vectors, then per atom received minus sent
+  // ---- attention weights and positions: per edge, both from one product per
+  // (receiver, head); then per atom the forces received minus those sent
   float* gedge = grad_pos ? cd.take<float>((size_t)n_edges * 3) : nullptr;
-  if (fused && (grad_alpha || gedge)) {
+  if (grad_alpha || gedge) {
     const e2f_ctx::Geom* gsch = nullptr;
     if ((rs = geom_of(ctx, L, C / H, gsch)) != E2F_OK) return rs;
     E2F_TIMED("edge_geom", launch_edge_geom(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, alpha, n, C, H, gsch->qc,
                                             gsch->meta, gsch->unit, gsch->oc, gsch->tot, grad_alpha, gedge, s));
   }
-  else if (gedge)
-    E2F_TIMED("edge_force", launch_edge_force(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, alpha, n, C, H, gedge, s));
   if (gedge) E2F_TIMED("force_gather", launch_force_gather(row_ptr, rowT, perm, gedge, n, grad_pos, s));
   // ---- features: the same layer on the transposed graph, input degree o,
   // output degree a, weights w[a][f][o] kappa(a,f,o) (-1)^f

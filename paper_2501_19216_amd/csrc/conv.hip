@@ -1095,171 +1095,6 @@ __global__ void k_plan_pack(const int32_t* __restrict__ pidx, const int32_t* __r
 }
 
 // ------------------------------------------------------------ backward
-// Gradient with respect to the attention weights: per edge e = (i, j) and
-// head h, galpha = sum_{c of h} sum_k gy_i[k][c] (K_e h_j)[k][c] with the edge
-// filter K_e of the baseline built once per edge in LDS.  One thread per
-// channel; the per-head sums run over the channels in order (deterministic).
-template <int L, bool SHFL>
-__global__ __launch_bounds__(256) void k_edge_vjp_alpha(DevTables t, const float* __restrict__ pos,
-                                                        const float* __restrict__ feat, const float* __restrict__ gy,
-                                                        const int64_t* __restrict__ row_ptr,
-                                                        const int32_t* __restrict__ col, int C, int H,
-                                                        float* __restrict__ galpha) {
-  constexpr int NK = (L + 1) * (L + 1);
-  constexpr int EB = 8;
-  extern __shared__ float sm[];
-  float* Kl = sm;                        // [EB][NK*NK]
-  float* Rl = Kl + EB * NK * NK;         // [EB][NK]
-  float* vb = Rl + EB * NK;              // [EB][blockDim.x]
-  const int i = blockIdx.x;
-  const int dh = C / H;
-  const int c = threadIdx.x;
-  const bool live = c < C;
-  const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
-  const float xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
-  float g[NK];
-#pragma unroll
-  for (int k = 0; k < NK; ++k) g[k] = live ? gy[((size_t)i * NK + k) * C + c] : 0.0f;
-  for (int64_t eb = e0; eb < e1; eb += EB) {
-    const int nb = (e1 - eb) < EB ? (int)(e1 - eb) : EB;
-    __syncthreads();
-    for (int q = threadIdx.x; q < nb * NK; q += blockDim.x) {
-      const int b = q / NK, k = q % NK;
-      const int j = col[eb + b];
-      Rl[q] = sh_poly<float>(t, k, xi - pos[3 * j], yi - pos[3 * j + 1], zi - pos[3 * j + 2]);
-    }
-    __syncthreads();
-    for (int q = threadIdx.x; q < nb * NK * NK; q += blockDim.x) {
-      const int b = q / (NK * NK), s = q % (NK * NK);
-      float v = 0.0f;
-      for (int e = t.k_ptr[s]; e < t.k_ptr[s + 1]; ++e) v += t.k_coef[e] * Rl[b * NK + t.k_ridx[e]];
-      Kl[q] = v;
-    }
-    __syncthreads();
-    for (int b = 0; b < nb; ++b) {
-      float v = 0.0f;
-      if (live) {
-        const int j = col[eb + b];
-        const float* Kb = Kl + b * NK * NK;
-#pragma unroll
-        for (int q = 0; q < NK; ++q) {
-          float u = 0.0f;
-#pragma unroll
-          for (int k = 0; k < NK; ++k) u += g[k] * Kb[k * NK + q];
-          v += u * feat[((size_t)j * NK + q) * C + c];
-        }
-      }
-      if (SHFL) {
-        // the dh channels of a head are consecutive lanes of one wave
-        for (int o = dh >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o);
-        if (live && c % dh == 0) galpha[(eb + b) * H + c / dh] = v;
-      } else {
-        vb[b * blockDim.x + threadIdx.x] = v;
-      }
-    }
-    if (!SHFL) {
-      __syncthreads();
-      for (int q = threadIdx.x; q < nb * H; q += blockDim.x) {
-        const int b = q / H, h = q % H;
-        float s = 0.0f;
-        for (int tt = 0; tt < dh; ++tt) s += vb[b * blockDim.x + h * dh + tt];
-        galpha[(eb + b) * H + h] = s;
-      }
-    }
-  }
-}
-
-// Gradient with respect to the positions: per edge e = (i, j), r = r_i - r_j,
-//   g_e[x] = sum_c alpha_{e,h(c)} sum_{k,q} gy_i[k][c] (dK_e/dr_x)[k][q] h_j[q][c],
-// with dK_e/dr_x the edge filter of the baseline built from the gradient of
-// the solid harmonics (three filters per edge in LDS).  One thread per
-// channel; the sum over channels runs by wave shuffles, then over the waves
-// in order (deterministic).  The per-atom sums follow in k_force_gather.
-template <int L, int EB>
-__global__ __launch_bounds__(256) void k_edge_force(DevTables t, const float* __restrict__ pos,
-                                                    const float* __restrict__ feat, const float* __restrict__ gy,
-                                                    const int64_t* __restrict__ row_ptr,
-                                                    const int32_t* __restrict__ col, const float* __restrict__ alpha,
-                                                    int C, int H, float* __restrict__ gedge) {
-  constexpr int NK = (L + 1) * (L + 1);
-  extern __shared__ float sm[];
-  float* dK = sm;                      // [3][EB][NK*NK]
-  float* dR = dK + 3 * EB * NK * NK;   // [3][EB][NK]
-  float* red = dR + 3 * EB * NK;       // [EB*3][waves]
-  const int i = blockIdx.x;
-  const int dh = C / H;
-  const int c = threadIdx.x;
-  const bool live = c < C;
-  const int nw = blockDim.x >> 6, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
-  const float xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
-  float g[NK];
-#pragma unroll
-  for (int k = 0; k < NK; ++k) g[k] = live ? gy[((size_t)i * NK + k) * C + c] : 0.0f;
-  for (int64_t eb = e0; eb < e1; eb += EB) {
-    const int nb = (e1 - eb) < EB ? (int)(e1 - eb) : EB;
-    __syncthreads();
-    for (int q = threadIdx.x; q < nb * NK; q += blockDim.x) {
-      const int b = q / NK, k = q % NK;
-      const int j = col[eb + b];
-      float gx, gyy, gz;
-      sh_poly_grad<float>(t, k, xi - pos[3 * j], yi - pos[3 * j + 1], zi - pos[3 * j + 2], gx, gyy, gz);
-      dR[(0 * EB + b) * NK + k] = gx;
-      dR[(1 * EB + b) * NK + k] = gyy;
-      dR[(2 * EB + b) * NK + k] = gz;
-    }
-    __syncthreads();
-    for (int q = threadIdx.x; q < 3 * nb * NK * NK; q += blockDim.x) {
-      const int xb = q / (NK * NK), s = q % (NK * NK);  // xb = x * nb + b
-      const int x = xb / nb, b = xb % nb;
-      const float* Rb = dR + (x * EB + b) * NK;
-      float v = 0.0f;
-      for (int e = t.k_ptr[s]; e < t.k_ptr[s + 1]; ++e) v += t.k_coef[e] * Rb[t.k_ridx[e]];
-      dK[(x * EB + b) * NK * NK + s] = v;
-    }
-    __syncthreads();
-    for (int b = 0; b < nb; ++b) {
-      float v0 = 0.0f, v1 = 0.0f, v2 = 0.0f;
-      if (live) {
-        const int j = col[eb + b];
-        const float* K0 = dK + (0 * EB + b) * NK * NK;
-        const float* K1 = dK + (1 * EB + b) * NK * NK;
-        const float* K2 = dK + (2 * EB + b) * NK * NK;
-        for (int q = 0; q < NK; ++q) {
-          float u0 = 0.0f, u1 = 0.0f, u2 = 0.0f;
-#pragma unroll
-          for (int k = 0; k < NK; ++k) {
-            u0 += g[k] * K0[k * NK + q];
-            u1 += g[k] * K1[k * NK + q];
-            u2 += g[k] * K2[k * NK + q];
-          }
-          const float hv = feat[((size_t)j * NK + q) * C + c];
-          v0 += u0 * hv, v1 += u1 * hv, v2 += u2 * hv;
-        }
-        const float a = alpha ? alpha[(eb + b) * H + c / dh] : 1.0f;
-        v0 *= a, v1 *= a, v2 *= a;
-      }
-      // every lane of every wave takes the same shuffle steps
-      for (int o = 32; o > 0; o >>= 1) {
-        v0 += __shfl_xor(v0, o);
-        v1 += __shfl_xor(v1, o);
-        v2 += __shfl_xor(v2, o);
-      }
-      if (lane == 0) {
-        red[(b * 3 + 0) * nw + wave] = v0;
-        red[(b * 3 + 1) * nw + wave] = v1;
-        red[(b * 3 + 2) * nw + wave] = v2;
-      }
-    }
-    __syncthreads();
-    for (int q = threadIdx.x; q < nb * 3; q += blockDim.x) {
-      float sum = 0.0f;
-      for (int w = 0; w < nw; ++w) sum += red[q * nw + w];
-      gedge[(eb + q / 3) * 3 + q % 3] = sum;
-    }
-  }
-}
-
 // Both per-edge products of the backward from one matrix product per
 // (receiver, head).  The edge filter is linear in the solid harmonics,
 // K_e[k][q] = sum_be R_be(r_e) Kc[be][k][q] with Kc the path-weighted filter
@@ -1272,13 +1107,15 @@ __global__ __launch_bounds__(256) void k_edge_force(DevTables t, const float* __
 //   gedge[e][x]  = sum_be dR_be/dx(r_e) W[be][e],  W = sum_h alpha_eh X_h.
 // The contraction runs on v_mfma_f32_16x16x4f32 with be as rows (MT tiles
 // of 16), edges as columns (tiles of 16 edges; NTE tiles per wave, the
-// wave's tiles are wave + NW et) and (q, c) as the reduction: lane group k4
-// takes channels 16 s + 4 k4 .. + 3 of row q as one float4, and MFMA w of
-// four uses component w.  LDS holds, per workgroup, the schedule of the Z
+// wave's tiles are wave + NW et) and kappa = q dh + c as the reduction:
+// step st covers kappa in [16 st, 16 st + 16), lane group k4 takes kappa =
+// 16 st + 4 k4 .. + 3 (four channels of one row q, as 4 | dh) as one float4,
+// and MFMA w of four uses component w.  LDS holds, per workgroup, the schedule of the Z
 // sums (path weights folded in, staged once; read from global memory above
 // L = 4, where it outgrows LDS), the head's slice of gy_i and Z
-// for qc rows q at a time, with row stride qc dh + 4 floats (the 16 rows be
-// of an operand read start in distinct bank quadruples).  A workgroup takes
+// for qc rows q at a time (Z[be][kappa - q0 dh]), with a row stride of
+// qc dh + 4 or + 8 floats, an odd number of quadruples (the 16 rows be of an
+// operand read start in distinct bank quadruples).  A workgroup takes
 // rpw consecutive receivers; edge chunks of NW NTE 16 edges, Z rebuilt per
 // chunk, head and row pass.  Each output element has one writer.
 template <int L, int NTE, bool WA, bool WP>
@@ -1293,7 +1130,7 @@ __global__ __launch_bounds__(128) void k_edge_geom(DevTables t, const float* __r
   constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16;
   constexpr bool STAGED = L <= 4;  // the schedule in LDS (it outgrows LDS above L = 4)
   extern __shared__ float4 sm4[];
-  const int dh = C / H, dq = dh >> 2, S16 = dh >> 4, ZS = qc * dh + 4;
+  const int dh = C / H, dq = dh >> 2, ZS = qc * dh + (((qc * dh) >> 2) & 1 ? 8 : 4);
   float* gyl = (float*)sm4;  // [NK][dh]: gy_i of the head
   // STAGED: [gtot] schedule, [gtot] its coefficients times the path weights
   int* smeta = (int*)(gyl + NK * dh);
@@ -1375,22 +1212,22 @@ __global__ __launch_bounds__(128) void k_edge_geom(DevTables t, const float* __r
           __syncthreads();
           // three-stage pipeline: the features of steps st+1, st+2 load while
           // the MFMAs of st run
-          const int nst = nq * S16;
+          const int nkap = nq * dh, nst = (nkap + 15) / 16;
           auto loadb = [&](int st, float4* b) {
-            const int sc = min(st, nst - 1);
-            const int q = q0 + sc / S16, s = sc % S16;
+            const int kap = 16 * min(st, nst - 1) + 4 * k4;
+            const int kc = kap < nkap ? kap : 0;  // past the pass: a valid row, A = 0
+            const int q = q0 + kc / dh, c = kc % dh;
 #pragma unroll
             for (int et = 0; et < NTE; ++et)
-              b[et] = *(const float4*)(feat + ((size_t)jn[et] * NK + q) * C + h * dh + 16 * s + 4 * k4);
+              b[et] = *(const float4*)(feat + ((size_t)jn[et] * NK + q) * C + h * dh + c);
           };
           auto mma = [&](int st, const float4* b) {
-            const int qq = st / S16, s = st % S16;
+            const int kap = 16 * st + 4 * k4;
             float4 a[MT];
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
               const int be = mt * 16 + l16;
-              a[mt] = be < NK ? *(const float4*)(Z + be * ZS + qq * dh + 16 * s + 4 * k4)
-                              : make_float4(0.f, 0.f, 0.f, 0.f);
+              a[mt] = (be < NK && kap < nkap) ? *(const float4*)(Z + be * ZS + kap) : make_float4(0.f, 0.f, 0.f, 0.f);
             }
 #pragma unroll
             for (int et = 0; et < NTE; ++et) {
@@ -2096,35 +1933,14 @@ hipError_t launch_plan_pack(const int32_t* pidx, const int32_t* flags, int64_t c
   return hipGetLastError();
 }
 
-hipError_t launch_edge_force(const DevTables& t, const float* pos, const float* feat, const float* gy,
-                             const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n, int C, int H,
-                             float* gedge, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  if (C > 256) return hipErrorInvalidValue;
-  const int threads = (C + 63) / 64 * 64;
-  const int eb = t.L <= 4 ? 4 : 2;
-  const size_t lds =
-      sizeof(float) * ((size_t)3 * eb * t.nk * t.nk + (size_t)3 * eb * t.nk + (size_t)eb * 3 * (threads / 64));
-  switch (t.L) {
-#define E2F_CASE(LL, EB_)                                                                                   \
-  case LL:                                                                                                  \
-    if (hipError_t e = allow_lds(k_edge_force<LL, EB_>, lds); e != hipSuccess) return e;                    \
-    k_edge_force<LL, EB_><<<n, threads, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx, alpha, C, H, gedge);  \
-    break;
-    E2F_CASE(0, 4) E2F_CASE(1, 4) E2F_CASE(2, 4) E2F_CASE(3, 4) E2F_CASE(4, 4) E2F_CASE(5, 2) E2F_CASE(6, 2)
-#undef E2F_CASE
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-
 bool edge_geom_supported(int C, int H) {
-  return C % H == 0 && (C / H) % 16 == 0 && C / H <= 128;
+  return C % H == 0 && (C / H) % 4 == 0 && C <= 256;
 }
 
 size_t edge_geom_lds(int L, int dh, int qc, int gtot) {
   const size_t nk = (size_t)(L + 1) * (L + 1);
-  return sizeof(float) * (nk * dh + (L <= 4 ? 2 * (size_t)gtot : 0) + nk * (qc * dh + 4));
+  const size_t zs = (size_t)qc * dh + (((qc * dh) >> 2) & 1 ? 8 : 4);
+  return sizeof(float) * (nk * dh + (L <= 4 ? 2 * (size_t)gtot : 0) + nk * zs);
 }
 
 hipError_t launch_edge_geom(const DevTables& t, const float* pos, const float* feat, const float* gy,
@@ -2165,32 +1981,6 @@ hipError_t launch_force_gather(const int64_t* row_ptr, const int64_t* rowT, cons
   return hipGetLastError();
 }
 
-hipError_t launch_edge_vjp_alpha(const DevTables& t, const float* pos, const float* feat, const float* gy,
-                                 const int64_t* row_ptr, const int32_t* col_idx, int n, int C, int H, float* galpha,
-                                 hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  if (C > 256) return hipErrorInvalidValue;
-  const int threads = (C + 63) / 64 * 64;
-  const int dh = C / H;
-  const bool shfl = (dh & (dh - 1)) == 0 && dh <= 64;
-  const size_t lds = sizeof(float) * ((size_t)8 * t.nk * t.nk + (size_t)8 * t.nk + (size_t)8 * threads);
-  switch (t.L) {
-#define E2F_CASE(LL)                                                                                        \
-  case LL:                                                                                                  \
-    if (shfl) {                                                                                             \
-      if (hipError_t e = allow_lds(k_edge_vjp_alpha<LL, true>, lds); e != hipSuccess) return e;             \
-      k_edge_vjp_alpha<LL, true><<<n, threads, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx, C, H, galpha); \
-    } else {                                                                                                \
-      if (hipError_t e = allow_lds(k_edge_vjp_alpha<LL, false>, lds); e != hipSuccess) return e;            \
-      k_edge_vjp_alpha<LL, false><<<n, threads, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx, C, H, galpha);\
-    }                                                                                                       \
-    break;
-    E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
-#undef E2F_CASE
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
 
 size_t transpose_tmp_bytes(int n, int64_t E) {
   size_t a = 0, b = 0;

@@ -130,14 +130,11 @@ hipError_t launch_attention(const float* pos, const float* q, const float* k, in
                             float* alpha, hipStream_t s);
 
 // ---- backward
-// galpha[e][h] = sum_{c of h} <gy_i[.][c], (K_e h_j)[.][c]> for the edges of rows 0..n-1 (C <= 256)
-// Position gradient: gedge [E][3] per edge (C <= 256), then per atom the
-// edges it receives minus those it sends (rowT, perm: the transposed graph).
-hipError_t launch_edge_force(const DevTables& t, const float* pos, const float* feat, const float* gy,
-                             const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n, int C, int H,
-                             float* gedge, hipStream_t s);
 // Both per-edge backward products in one pass (either output may be NULL):
-// galpha [E][H], gedge [E][3]; needs C/H a multiple of 16, at most 128.
+// galpha[e][h] = sum_{c of h} <gy_i[.][c], (K_e h_j)[.][c]> [E][H] and the
+// position gradient per edge gedge [E][3]; needs 4 | C/H and C <= 256.
+// launch_force_gather then sums per atom the edges it receives minus those it
+// sends (rowT, perm: the transposed graph).
 bool edge_geom_supported(int C, int H);
 // LDS bytes of the backward kernel for qc filter rows per pass and a
 // schedule of gtot entries (staged in LDS up to L = 4)
@@ -148,9 +145,6 @@ hipError_t launch_edge_geom(const DevTables& t, const float* pos, const float* f
                             float* gedge, hipStream_t s);
 hipError_t launch_force_gather(const int64_t* row_ptr, const int64_t* rowT, const int32_t* perm, const float* gedge,
                                int n, float* gpos, hipStream_t s);
-hipError_t launch_edge_vjp_alpha(const DevTables& t, const float* pos, const float* feat, const float* gy,
-                                 const int64_t* row_ptr, const int32_t* col_idx, int n, int C, int H, float* galpha,
-                                 hipStream_t s);
 // transposed CSR (row = sender, ascending receivers) and alpha in its order;
 // scratch: rows, iota, keys_out, perm [E], cnt [n+1]
 size_t transpose_tmp_bytes(int n, int64_t E);
