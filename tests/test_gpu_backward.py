@@ -147,3 +147,40 @@ def test_backward_protein_sampled(e2f, ctx):
     ep = float(np.abs(gp[rq] - gp_ref).max() / np.abs(gp_ref).max())
     print("protein: grad_feat %.3e grad_alpha %.3e grad_pos %.3e" % (ef, ea, ep))
     assert ef <= TOL_F32 and ea <= TOL_F32 and ep <= TOL_F32
+
+
+@pytest.mark.parametrize("L,C,H", [(4, 32, 2), (3, 16, 4)])
+def test_backward_uniform_alpha_and_isolated_atoms(e2f, ctx, L, C, H):
+    # alpha = NULL (uniform weights); atoms without neighbours give empty rows
+    rng = np.random.default_rng(30 + L)
+    lone = 60.0 + 20.0 * np.arange(5)[:, None] * np.ones((1, 3))
+    pos = syn.quantize(np.concatenate([rng.uniform(0, 11, size=(200, 3)), lone]))
+    rp, ci = o.neighbor_list(pos, 5.0)
+    n = pos.shape[0]
+    assert (np.diff(rp)[200:] == 0).all()
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    gout = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    w = default_w(L, 5.0)
+    ones = np.ones((len(ci), H))
+    gf_ref, ga_ref = o.conv_edge_vjp(L, H, pos, feat, gout.astype(np.float64), rp, ci, ones, w)
+    atoms = np.r_[np.arange(0, 200, 9), np.arange(200, n)].astype(np.int32)
+    gp_ref = o.conv_edge_grad_pos(L, H, pos, feat, gout.astype(np.float64), rp, ci, ones, w, atoms=atoms)
+    print("uniform alpha, isolated atoms: L %d C %d H %d" % (L, C, H), flush=True)
+    gf, ga, gp = e2f.e2f_wigner6j_conv_backward(ctx, gpu(pos), gpu(feat), gpu(gout), gpu(rp), gpu(ci), None, L, H, 5.0,
+                                                want_pos=True)
+    gf, ga, gp = gf.cpu().numpy(), ga.cpu().numpy(), gp.cpu().numpy()
+    assert o.max_rel_err(gf, gf_ref, L) <= TOL_F32 and head_err(ga, ga_ref) <= TOL_F32
+    assert np.abs(gp[atoms] - gp_ref).max() <= TOL_F32 * np.abs(gp_ref).max()
+    assert (gp[200:] == 0).all() and (gf[200:] == 0).all()
+
+
+def test_backward_without_edges(e2f, ctx):
+    pos = syn.quantize(10.0 * np.arange(12)[:, None] * np.ones((1, 3)))
+    rp, ci = o.neighbor_list(pos, 5.0)
+    assert len(ci) == 0
+    rng = np.random.default_rng(1)
+    feat = rng.standard_normal((12, 16, 16)).astype(np.float32)
+    gout = rng.standard_normal((12, 16, 16)).astype(np.float32)
+    gf, ga, gp = e2f.e2f_wigner6j_conv_backward(ctx, gpu(pos), gpu(feat), gpu(gout), gpu(rp), gpu(ci),
+                                                gpu(np.zeros((0, 4), np.float32)), 3, 4, 5.0, want_pos=True)
+    assert ga.shape == (0, 4) and (gf.cpu().numpy() == 0).all() and (gp.cpu().numpy() == 0).all()
