@@ -363,7 +363,7 @@ def main():
     if "node_tp" in kernels:  # T rows per (tile, sender), aggregated over receiver blocks
         agg = dict(bytes=4.0 * dimT * C * (pairs + n) + 4.0 * E * (1 + H) + 8.0 * (n + 1), flops=2.0 * E * dimT * C)
     else:  # uncoupled products aggregated per receiver, then coupled: read h once, write S once
-        agg = dict(bytes=4.0 * n * nk * C + 4.0 * E * (1 + H) + 8.0 * pairs * nk + 8.0 * (n + 1) + 4.0 * n * dimT * C,
+        agg = dict(bytes=4.0 * n * nk * C + 4.0 * E * (1 + H) + 4.0 * pairs * nk + 8.0 * (n + 1) + 4.0 * n * dimT * C,
                    flops=2.0 * E * nk * nk * C + 2.0 * n * coupling_entries(e2f, L) * C)
     alg = {
         "aggregate": agg,
