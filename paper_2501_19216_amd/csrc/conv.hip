@@ -180,15 +180,26 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 // Schedule): coalesced, independent loads; each thread sums its slots.
 __device__ __forceinline__ void run_schedule(const int* __restrict__ meta, const double* __restrict__ coef, int K,
                                              const double* Rl, float* dst) {
+  // eight entries' loads issued before the first is used (the schedule sits
+  // in L2: each batch costs one load latency); entries past K are zeros
   double acc = 0.0;
   const int t = threadIdx.x;
-#pragma unroll 4
-  for (int k = 0; k < K; ++k) {
-    const int m = meta[k * kSchedThreads + t];
-    acc += coef[k * kSchedThreads + t] * Rl[(m >> 20) & 127];
-    if (m < 0) {
-      dst[m & 0xfffff] = (float)acc;
-      acc = 0.0;
+  for (int k0 = 0; k0 < K; k0 += 8) {
+    int m[8];
+    double c[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const bool ok = k0 + u < K;
+      m[u] = ok ? meta[(k0 + u) * kSchedThreads + t] : 0;
+      c[u] = ok ? coef[(k0 + u) * kSchedThreads + t] : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      acc += c[u] * Rl[(m[u] >> 20) & 127];
+      if (m[u] < 0) {
+        dst[m[u] & 0xfffff] = (float)acc;
+        acc = 0.0;
+      }
     }
   }
 }
