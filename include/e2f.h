@@ -201,14 +201,19 @@ e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params*
  *     ratio of the real CG tensors of (a,f,o) and (o,f,a) (computed from the
  *     tables); the mixing contributes W^(o) transposed;
  *   grad_alpha [E][H]: per edge and head, the dot product of the unmixed
- *     output gradient of the receiver with the edge's message (the per-edge
- *     filter of the baseline); needs feat and C <= 256;
+ *     output gradient of the receiver with the edge's message; needs feat
+ *     and C <= 256;
  *   grad_pos [N][3]: the gradient with respect to the positions (the graph
  *     and alpha held fixed; forces are its negative).  Per edge (i, j) the
  *     message depends on r_i - r_j only, through R^(f); its derivative uses
  *     the gradient of the solid harmonics, and the edge's vector adds to i and
  *     subtracts from j (per atom in a fixed order: deterministic); needs feat
  *     and C <= 256.
+ * Both per-edge products use that the edge filter is linear in R(r_i - r_j):
+ * the receiver's output gradient is contracted with the filter coefficients
+ * once per receiver, and one product with the senders' features per head
+ * gives the contraction against R (grad_alpha) and against its gradient
+ * weighted by alpha (grad_pos) for every edge of the receiver.
  * Any of the outputs may be NULL (not all).  Not available with y_norm. */
 e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
                                       const int32_t* graph_id, const float* feat, const float* grad_out, int32_t n,
