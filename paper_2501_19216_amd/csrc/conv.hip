@@ -692,11 +692,11 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
   // one float4
   constexpr int NB = NTWM / 4;
   int off[NB];
-  bool cok[NB], tok[NB];
+  bool cok[NB], tlive[NB];
 #pragma unroll
   for (int u = 0; u < NB; ++u) {
     const int cb = wave + NW * u, nn = cb * 64 + 4 * l16;
-    tok[u] = cb * 64 < NC;  // uniform over the wave
+    tlive[u] = __builtin_amdgcn_readfirstlane(cb * 64 < NC ? 1 : 0) != 0;  // uniform over the wave
     cok[u] = nn < NC;
     const int q = cok[u] ? nn / dh : 0, tt = cok[u] ? nn % dh : 0;
     off[u] = q * C + h * dh + tt;
@@ -739,46 +739,48 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
     __syncthreads();
     // three-stage pipeline: the features of steps st+1, st+2 are loaded
     // while the MFMAs of step st run
-    float4 bA[NB], bB[NB];
-    auto loadb = [&](int st, float4* b) {
-      const int nb = min(4 * st + k4, EC - 1);  // rows past ne carry A = 0 and read a valid sender
+    // Each stage holds both operands of a step: A (the lane's two rows of
+    // alpha R from LDS) and B (the features), so no wait precedes the MFMAs.
+    // Rows 4 st + k4 < 4 ns <= EC hold alpha R (zeros past ne); steps past ns
+    // read row EC - 1 and a valid sender and are never multiplied.  Columns
+    // past NC read column 0 (valid) and their results are never stored.
+    float aA[MT], aB[MT], aC[MT];
+    float4 bA[NB], bB[NB], bC[NB];
+    auto loadb = [&](int st, float* a, float4* b) {
+      const int nb = min(4 * st + k4, EC - 1);
       const float* hj = feat + (size_t)jl[nb] * NK * C;
 #pragma unroll
       for (int u = 0; u < NB; ++u) b[u] = *(const float4*)(hj + off[u]);
-    };
-    auto mma = [&](int st, const float4* b) {
-      const int nb = min(4 * st + k4, EC - 1);
-      float a[MT];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) a[mt] = 4 * st + k4 < EC ? Al[nb * AS + mt * 16 + l16] : 0.0f;
+      for (int mt = 0; mt < MT; ++mt) a[mt] = Al[nb * AS + mt * 16 + l16];
+    };
+    auto mma = [&](const float* a, const float4* b) {
 #pragma unroll
       for (int u = 0; u < NB; ++u) {
-        if (!tok[u]) continue;
-        const float4 bv = cok[u] ? b[u] : make_float4(0.f, 0.f, 0.f, 0.f);
+        if (!tlive[u]) continue;  // scalar: uniform over the wave
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-          acc[mt][4 * u + 0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv.x, acc[mt][4 * u + 0], 0, 0, 0);
-          acc[mt][4 * u + 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv.y, acc[mt][4 * u + 1], 0, 0, 0);
-          acc[mt][4 * u + 2] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv.z, acc[mt][4 * u + 2], 0, 0, 0);
-          acc[mt][4 * u + 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv.w, acc[mt][4 * u + 3], 0, 0, 0);
+          acc[mt][4 * u + 0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], b[u].x, acc[mt][4 * u + 0], 0, 0, 0);
+          acc[mt][4 * u + 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], b[u].y, acc[mt][4 * u + 1], 0, 0, 0);
+          acc[mt][4 * u + 2] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], b[u].z, acc[mt][4 * u + 2], 0, 0, 0);
+          acc[mt][4 * u + 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], b[u].w, acc[mt][4 * u + 3], 0, 0, 0);
         }
       }
     };
-    float4 bC[NB];
-    loadb(0, bA);
-    loadb(1, bB);
+    loadb(0, aA, bA);
+    loadb(1, aB, bB);
     for (int st = 0; st < ns; st += 3) {
-      loadb(st + 2, bC);
+      loadb(st + 2, aC, bC);
       __builtin_amdgcn_sched_barrier(0);
-      mma(st, bA);
+      mma(aA, bA);
       __builtin_amdgcn_sched_barrier(0);
-      loadb(st + 3, bA);
+      loadb(st + 3, aA, bA);
       __builtin_amdgcn_sched_barrier(0);
-      if (st + 1 < ns) mma(st + 1, bB);
+      if (st + 1 < ns) mma(aB, bB);
       __builtin_amdgcn_sched_barrier(0);
-      loadb(st + 4, bB);
+      loadb(st + 4, aB, bB);
       __builtin_amdgcn_sched_barrier(0);
-      if (st + 2 < ns) mma(st + 2, bC);
+      if (st + 2 < ns) mma(aC, bC);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
