@@ -1225,22 +1225,22 @@ __global__ __launch_bounds__(128) void k_edge_geom(DevTables t, const float* __r
           // three-stage pipeline: the features of steps st+1, st+2 load while
           // the MFMAs of st run
           const int nkap = nq * dh, nst = (nkap + 15) / 16;
-          auto loadb = [&](int st, float4* b) {
+          // each stage holds both operands of a step (A from LDS, B from the
+          // senders' features), so no wait precedes the MFMAs
+          auto loadb = [&](int st, float4* a, float4* b) {
             const int kap = 16 * min(st, nst - 1) + 4 * k4;
             const int kc = kap < nkap ? kap : 0;  // past the pass: a valid row, A = 0
             const int q = q0 + kc / dh, c = kc % dh;
 #pragma unroll
             for (int et = 0; et < NTE; ++et)
               b[et] = *(const float4*)(feat + ((size_t)jn[et] * NK + q) * C + h * dh + c);
-          };
-          auto mma = [&](int st, const float4* b) {
-            const int kap = 16 * st + 4 * k4;
-            float4 a[MT];
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
               const int be = mt * 16 + l16;
               a[mt] = (be < NK && kap < nkap) ? *(const float4*)(Z + be * ZS + kap) : make_float4(0.f, 0.f, 0.f, 0.f);
             }
+          };
+          auto mma = [&](const float4* a, const float4* b) {
 #pragma unroll
             for (int et = 0; et < NTE; ++et) {
               if (wave + NW * et >= ntiles) continue;  // uniform over the wave
@@ -1253,21 +1253,21 @@ __global__ __launch_bounds__(128) void k_edge_geom(DevTables t, const float* __r
               }
             }
           };
-          float4 bA[NTE], bB[NTE], bC[NTE];
-          loadb(0, bA);
-          loadb(1, bB);
+          float4 aA[MT], aB[MT], aC[MT], bA[NTE], bB[NTE], bC[NTE];
+          loadb(0, aA, bA);
+          loadb(1, aB, bB);
           for (int st = 0; st < nst; st += 3) {
-            loadb(st + 2, bC);
+            loadb(st + 2, aC, bC);
             __builtin_amdgcn_sched_barrier(0);
-            mma(st, bA);
+            mma(aA, bA);
             __builtin_amdgcn_sched_barrier(0);
-            loadb(st + 3, bA);
+            loadb(st + 3, aA, bA);
             __builtin_amdgcn_sched_barrier(0);
-            if (st + 1 < nst) mma(st + 1, bB);
+            if (st + 1 < nst) mma(aB, bB);
             __builtin_amdgcn_sched_barrier(0);
-            loadb(st + 4, bB);
+            loadb(st + 4, aB, bB);
             __builtin_amdgcn_sched_barrier(0);
-            if (st + 2 < nst) mma(st + 2, bC);
+            if (st + 2 < nst) mma(aC, bC);
             __builtin_amdgcn_sched_barrier(0);
           }
         }
