@@ -1131,7 +1131,7 @@ __global__ void k_plan_pack(const int32_t* __restrict__ pidx, const int32_t* __r
 // rpw consecutive receivers; edge chunks of NW NTE 16 edges, Z rebuilt per
 // chunk, head and row pass.  Each output element has one writer.
 template <int L, int NTE, bool WA, bool WP>
-__global__ __launch_bounds__(128) void k_edge_geom(DevTables t, const float* __restrict__ pos,
+__global__ __launch_bounds__(256) void k_edge_geom(DevTables t, const float* __restrict__ pos,
                                                    const float* __restrict__ feat, const float* __restrict__ gy,
                                                    const int64_t* __restrict__ row_ptr,
                                                    const int32_t* __restrict__ col, const float* __restrict__ alpha,
@@ -1205,7 +1205,7 @@ __global__ __launch_bounds__(128) void k_edge_geom(DevTables t, const float* __r
             // Z rows of this pass: group grp walks its schedule entries, each
             // of its four threads takes the channel quads sub, sub + 4, ..
             const int ch = q0 / qc, off = goc[2 * ch], ck = goc[2 * ch + 1];
-            for (int cq = sub; cq < dq; cq += 4) {
+            for (int cq = sub; cq < dq && grp < kGeomGroups; cq += 4) {
               float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll 4
               for (int k = 0; k < ck; ++k) {
@@ -1969,11 +1969,12 @@ hipError_t launch_edge_geom(const DevTables& t, const float* pos, const float* f
   if (const char* v = getenv("E2F_GEOM_RPW")) rpw = std::max(1, atoi(v));
   const int nxr = (n + 7) / 8;
   const unsigned grid = 8u * (unsigned)((nxr + rpw - 1) / rpw);
+  const int geom_threads = 256;  // four waves of two edge tiles (the schedule's 128 threads build Z)
   switch (t.L * 4 + mode) {
 #define E2F_G(LL, WA_, WP_)                                                                                   \
   case LL * 4 + (WA_ ? 1 : 0) + (WP_ ? 2 : 0):                                                                \
-    if (hipError_t e = allow_lds(k_edge_geom<LL, (LL <= 4 ? 4 : 2), WA_, WP_>, lds); e != hipSuccess) return e; \
-    k_edge_geom<LL, (LL <= 4 ? 4 : 2), WA_, WP_><<<grid, 128, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx,    \
+    if (hipError_t e = allow_lds(k_edge_geom<LL, 2, WA_, WP_>, lds); e != hipSuccess) return e;               \
+    k_edge_geom<LL, 2, WA_, WP_><<<grid, geom_threads, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx,           \
                                                                          alpha, n, rpw, C, H, qc, gmeta,     \
                                                                          gunit, goc, gtot, galpha, gedge);   \
     break;
