@@ -723,19 +723,26 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
     // in flight, loads before stores
     const int ns = (ne + 3) / 4, nsl = 4 * ns * MP;
     for (int base = threadIdx.x; base < nsl; base += 4 * blockDim.x) {
-      float v[4];
+      // branch-free: clamped indices, all loads of a round issued before the
+      // first use (alpha and the pair of the edge, then R of the pair)
+      float av[4], rv[4];
+      int pv[4], bv[4];
+      bool okv[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int idx = base + u * blockDim.x, nb = idx / MP, be = idx % MP;
-        const bool ok = idx < nsl && nb < ne && be < NK;
-        const int64_t e = c0 + (ok ? nb : 0);
-        const float a = ok ? (alpha_hm ? alpha_hm[(int64_t)h * n_edges + e] : 1.0f) : 0.0f;
-        v[u] = ok ? a * Rp[(size_t)col_pair[e] * NK + be] : 0.0f;
+        okv[u] = idx < nsl && nb < ne && be < NK;
+        const int64_t e = c0 + (nb < ne ? nb : 0);
+        bv[u] = be < NK ? be : 0;
+        av[u] = alpha_hm ? alpha_hm[(int64_t)h * n_edges + e] : 1.0f;
+        pv[u] = col_pair[e];
       }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) rv[u] = Rp[(size_t)pv[u] * NK + bv[u]];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int idx = base + u * blockDim.x;
-        if (idx < nsl) Al[(idx / MP) * AS + idx % MP] = v[u];
+        if (idx < nsl) Al[(idx / MP) * AS + idx % MP] = okv[u] ? av[u] * rv[u] : 0.0f;
       }
     }
     for (int q = threadIdx.x; q < EC; q += blockDim.x) jl[q] = col[c0 + (q < ne ? q : 0)];
