@@ -673,8 +673,6 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
   float* G = sm;                    // [NK][GS], after the products (reuses the staging space)
   // the coupling schedule, staged once in LDS after the work space when
   // work_floats > 0 (else read from global memory)
-  const int* sm_meta = work_floats > 0 ? (const int*)(sm + work_floats) : cmeta;
-  const float* sm_coef = work_floats > 0 ? sm + work_floats + ck * cgroups : ccoef;
   if (work_floats > 0) {
     for (int q = threadIdx.x; q < ck * cgroups; q += blockDim.x) {
       ((int*)(sm + work_floats))[q] = cmeta[q];
@@ -814,19 +812,39 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
   // (four channels per thread: group g = tid / (dh/4), channels 4 tq .. 4 tq + 3)
   float* Sr = S + (size_t)r * t.dimT * C + (size_t)h * t.dimT * dh;
   const int dq = dh >> 2, g = threadIdx.x / dq, tq = threadIdx.x % dq;
-  if (g < cgroups) {
+  // four entries at a time: their schedule reads, then their G reads, then
+  // the sums (past ck: entry 0 with coefficient 0, never the last of a row);
+  // one copy of the loop per memory holding the schedule, so that its reads
+  // are plain LDS or global loads
+  auto couple = [&](const int* __restrict__ meta, const float* __restrict__ coef) {
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 4
-    for (int k = 0; k < ck; ++k) {
-      const int m = sm_meta[k * cgroups + g];
-      const float c = sm_coef[k * cgroups + g];
-      const float4 gv = *(const float4*)(G + ((m >> 6) & 63) * GS + (m & 63) * dh + 4 * tq);
-      v.x += c * gv.x, v.y += c * gv.y, v.z += c * gv.z, v.w += c * gv.w;
-      if (m < 0) {
-        *(float4*)(Sr + ((m >> 12) & 4095) * dh + 4 * tq) = v;
-        v = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int k0 = 0; k0 < ck; k0 += 4) {
+      int m[4];
+      float c[4];
+      float4 gv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bool ok = k0 + u < ck;
+        m[u] = ok ? meta[(k0 + u) * cgroups + g] : 0;
+        c[u] = ok ? coef[(k0 + u) * cgroups + g] : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) gv[u] = *(const float4*)(G + ((m[u] >> 6) & 63) * GS + (m[u] & 63) * dh + 4 * tq);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        v.x += c[u] * gv[u].x, v.y += c[u] * gv[u].y, v.z += c[u] * gv[u].z, v.w += c[u] * gv[u].w;
+        if (m[u] < 0) {
+          *(float4*)(Sr + ((m[u] >> 12) & 4095) * dh + 4 * tq) = v;
+          v = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
       }
     }
+  };
+  if (g < cgroups) {
+    if (work_floats > 0)
+      couple((const int*)(sm + work_floats), sm + work_floats + ck * cgroups);
+    else
+      couple(cmeta, ccoef);
   }
   }  // receivers of the workgroup
 }
