@@ -1194,7 +1194,9 @@ __global__ __launch_bounds__(256) void k_edge_geom(DevTables t, const float* __r
       const int ne = (int)min((int64_t)NW * NTE * 16, e1 - c0);
       const int ntiles = (ne + 15) / 16;
       int jn[NTE];
-      bool ev[NTE];
+      bool ev[NTE], tlive[NTE];
+#pragma unroll
+      for (int et = 0; et < NTE; ++et) tlive[et] = __builtin_amdgcn_readfirstlane(wave + NW * et < ntiles ? 1 : 0) != 0;
       float dx[NTE], dy[NTE], dz[NTE];
       float Rv[NTE][MT][4];
       v4f W[NTE][MT];
@@ -1252,23 +1254,26 @@ __global__ __launch_bounds__(256) void k_edge_geom(DevTables t, const float* __r
           const int nkap = nq * dh, nst = (nkap + 15) / 16;
           // each stage holds both operands of a step (A from LDS, B from the
           // senders' features), so no wait precedes the MFMAs
+          // branch-free: clamped addresses, zeros selected after the loads
           auto loadb = [&](int st, float4* a, float4* b) {
             const int kap = 16 * min(st, nst - 1) + 4 * k4;
-            const int kc = kap < nkap ? kap : 0;  // past the pass: a valid row, A = 0
-            const int q = q0 + kc / dh, c = kc % dh;
+            const bool kok = kap < nkap;
+            const unsigned kc = kok ? kap : 0;  // past the pass: a valid row, A = 0
+            const unsigned q = q0 + kc / (unsigned)dh, c = kc % (unsigned)dh;
 #pragma unroll
             for (int et = 0; et < NTE; ++et)
               b[et] = *(const float4*)(feat + ((size_t)jn[et] * NK + q) * C + h * dh + c);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
               const int be = mt * 16 + l16;
-              a[mt] = (be < NK && kap < nkap) ? *(const float4*)(Z + be * ZS + kap) : make_float4(0.f, 0.f, 0.f, 0.f);
+              const float4 z = *(const float4*)(Z + (be < NK ? be : 0) * ZS + kc);
+              a[mt] = (be < NK && kok) ? z : make_float4(0.f, 0.f, 0.f, 0.f);
             }
           };
           auto mma = [&](const float4* a, const float4* b) {
 #pragma unroll
             for (int et = 0; et < NTE; ++et) {
-              if (wave + NW * et >= ntiles) continue;  // uniform over the wave
+              if (!tlive[et]) continue;  // scalar: uniform over the wave
 #pragma unroll
               for (int mt = 0; mt < MT; ++mt) {
                 X[et][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt].x, b[et].x, X[et][mt], 0, 0, 0);
