@@ -181,7 +181,8 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void run_schedule(const int* __restrict__ meta, const double* __restrict__ coef, int K,
                                              const double* Rl, float* dst) {
   // eight entries' loads issued before the first is used (the schedule sits
-  // in L2: each batch costs one load latency); entries past K are zeros
+  // in L2: each batch costs one load latency), then their eight R values
+  // read from LDS together; entries past K are zeros
   double acc = 0.0;
   const int t = threadIdx.x;
   for (int k0 = 0; k0 < K; k0 += 8) {
@@ -193,9 +194,12 @@ __device__ __forceinline__ void run_schedule(const int* __restrict__ meta, const
       m[u] = ok ? meta[(k0 + u) * kSchedThreads + t] : 0;
       c[u] = ok ? coef[(k0 + u) * kSchedThreads + t] : 0.0;
     }
+    double rv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) rv[u] = Rl[(m[u] >> 20) & 127];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      acc += c[u] * Rl[(m[u] >> 20) & 127];
+      acc += c[u] * rv[u];
       if (m[u] < 0) {
         dst[m[u] & 0xfffff] = (float)acc;
         acc = 0.0;
