@@ -724,6 +724,8 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
     // (contiguous R loads, conflict-free LDS stores); four values per thread
     // in flight, loads before stores
     const int ns = (ne + 3) / 4, nsl = 4 * ns * MP;
+    // the chunk's senders (blockDim >= EC), loaded with the staging's first round
+    const int jv = threadIdx.x < EC ? col[c0 + ((int)threadIdx.x < ne ? threadIdx.x : 0)] : 0;
     for (int base = threadIdx.x; base < nsl; base += 4 * blockDim.x) {
       // branch-free: clamped indices, all loads of a round issued before the
       // first use (alpha and the pair of the edge, then R of the pair)
@@ -747,7 +749,7 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
         if (idx < nsl) Al[(idx / MP) * AS + idx % MP] = okv[u] ? av[u] * rv[u] : 0.0f;
       }
     }
-    for (int q = threadIdx.x; q < EC; q += blockDim.x) jl[q] = col[c0 + (q < ne ? q : 0)];
+    if (threadIdx.x < EC) jl[threadIdx.x] = jv;
     __syncthreads();
     // three-stage pipeline: the features of steps st+1, st+2 are loaded
     // while the MFMAs of step st run
