@@ -86,6 +86,7 @@ def sweep_one(name, steps, warmup):
 
     wl = syn.WORKLOADS[name]
     inp = syn.make_inputs(wl)
+    print("[sweep] %s: %d atoms generated" % (name, inp.pos.shape[0]), file=sys.stderr, flush=True)
     dev = torch.device("cuda:0")
     ctx = e2f.e2f_create(wl.lmax, 0)
 
@@ -99,6 +100,8 @@ def sweep_one(name, steps, warmup):
         rp, ci = e2f.e2f_neighbor_list(ctx, pos, wl.cutoff, gid)
         al = syn.attention_weights(pos_h, spc, rp.cpu().numpy(), ci.cpu().numpy(), wl.heads, wl.cutoff, wl.species,
                                    wl.seed)
+        print("[sweep] %s: graph and attention weights of %d atoms ready" % (name, pos_h.shape[0]), file=sys.stderr,
+              flush=True)
         return pos, torch.from_numpy(feat_h).to(dev), gid, rp, ci, torch.from_numpy(al).to(dev)
 
     mix_w = torch.from_numpy(inp.mix_w).to(dev)

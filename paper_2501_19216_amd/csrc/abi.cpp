@@ -876,6 +876,7 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   const size_t need_b = 2 * al256(sizeof(int32_t) * (size_t)P) + 3 * al256(sizeof(int32_t) * (size_t)n_edges) +
                         3 * al256(sizeof(int32_t) * (size_t)(nblk + 1)) + al256(blk_tmp_b) +
                         al256((outer ? sizeof(float) : sizeof(double)) * (size_t)P * nk) +
+                        (outer ? al256(sizeof(float) * (size_t)n_edges * nk) : 0) +
                         al256(sizeof(double) * (size_t)n * nk) +
                         (outer ? 0 : al256(row_bytes * (size_t)max_pairs)) + al256(row_bytes * (size_t)max_recv * nS) +
                         (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0) +
@@ -896,6 +897,7 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   void* blk_tmp = cb.take<char>(blk_tmp_b);
   double* Rp = outer ? nullptr : cb.take<double>((size_t)P * nk);
   float* Rpf = outer ? cb.take<float>((size_t)P * nk) : nullptr;  // the outer-product aggregation reads fp32
+  float* Re = outer ? cb.take<float>((size_t)n_edges * nk) : nullptr;  // ... per edge
   double* Rr = cb.take<double>((size_t)n * nk);
   float* T = outer ? nullptr : cb.take<float>((size_t)max_pairs * t.dimT * C);
   float* S = cb.take<float>((size_t)max_recv * t.dimT * C * nS);
@@ -912,6 +914,7 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   E2F_TIMED("tile_plan", launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
   E2F_TIMED("sh", launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, Rpf, s));
   E2F_TIMED("sh", launch_sh(t, pos, nullptr, origins, nullptr, tile_of, tp.ncell, n, Rr, nullptr, s));
+  if (outer) E2F_TIMED("sh", launch_edge_R(col_pair, Rpf, n_edges, nk, Re, s));
   const int dh = C / p->heads;
   const int cgroups = outer ? outer_agg_groups(L, C, p->heads) : 0;
   const e2f_ctx::Couple* cpl = nullptr;
@@ -922,7 +925,7 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
     if (nb == 0) continue;
     const int32_t* ord = order + q0;
     if (outer) {
-      E2F_TIMED("aggregate", launch_outer_agg(t, Rpf, row_ptr, col_idx, col_pair, alpha_hm, n_edges, feat, ord,
+      E2F_TIMED("aggregate", launch_outer_agg(t, Re, row_ptr, col_idx, alpha_hm, n_edges, feat, ord,
                                               cpl->meta, cpl->coef, cpl->k, cgroups, nb, C, p->heads, S, s));
       E2F_TIMED("recouple", launch_recouple(t, Rr, S, false, ord, nb, C, dh, y, s));
       continue;

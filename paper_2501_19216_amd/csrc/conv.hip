@@ -656,10 +656,9 @@ constexpr int kOuterEdges = 128;  // edges staged per chunk
 constexpr int kOuterStages = 3;
 
 template <int L, int NTWM, int LB>
-__global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __restrict__ Rp,
+__global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __restrict__ Re,
                                                     const int64_t* __restrict__ row_ptr,
                                                     const int32_t* __restrict__ col,
-                                                    const int32_t* __restrict__ col_pair,
                                                     const float* __restrict__ alpha_hm, int64_t n_edges,
                                                     const float* __restrict__ feat, const int32_t* __restrict__ order,
                                                     const int* __restrict__ cmeta, const float* __restrict__ ccoef,
@@ -727,22 +726,18 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
     // the chunk's senders (blockDim >= EC), loaded with the staging's first round
     const int jv = threadIdx.x < EC ? col[c0 + ((int)threadIdx.x < ne ? threadIdx.x : 0)] : 0;
     for (int base = threadIdx.x; base < nsl; base += 4 * blockDim.x) {
-      // branch-free: clamped indices, all loads of a round issued before the
-      // first use (alpha and the pair of the edge, then R of the pair)
+      // branch-free: clamped indices, all loads of a round (alpha and R of
+      // the edge, both addressed by the edge) issued before the first use
       float av[4], rv[4];
-      int pv[4], bv[4];
       bool okv[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int idx = base + u * blockDim.x, nb = idx / MP, be = idx % MP;
         okv[u] = idx < nsl && nb < ne && be < NK;
         const int64_t e = c0 + (nb < ne ? nb : 0);
-        bv[u] = be < NK ? be : 0;
         av[u] = alpha_hm ? alpha_hm[(int64_t)h * n_edges + e] : 1.0f;
-        pv[u] = col_pair[e];
+        rv[u] = Re[(size_t)e * NK + (be < NK ? be : 0)];
       }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) rv[u] = Rp[(size_t)pv[u] * NK + bv[u]];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int idx = base + u * blockDim.x;
@@ -1619,6 +1614,26 @@ hipError_t launch_pairs(const int32_t* flags, const int32_t* pidx, int64_t count
   return hipGetLastError();
 }
 
+// Re[e][k] = Rp[col_pair[e]][k]: the harmonics of each edge's sender under
+// its receiver's tile origin, in edge order (the aggregation's staging then
+// reads one contiguous block per chunk, addressed by the edge alone)
+__global__ void k_edge_R(const int32_t* __restrict__ col_pair, const float* __restrict__ Rp, int64_t n_edges,
+                         int nk, float* __restrict__ Re) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= n_edges * nk) return;
+  const int64_t e = x / nk;
+  Re[x] = Rp[(size_t)col_pair[e] * nk + (int)(x - e * nk)];
+}
+
+hipError_t launch_edge_R(const int32_t* col_pair, const float* Rp, int64_t n_edges, int nk, float* Re,
+                         hipStream_t s) {
+  if (n_edges == 0) return hipSuccess;
+  const int64_t blocks = (n_edges * nk + 255) / 256;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  k_edge_R<<<(unsigned)blocks, 256, 0, s>>>(col_pair, Rp, n_edges, nk, Re);
+  return hipGetLastError();
+}
+
 hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of,
                            const int32_t* pidx, int n, int32_t* col_pair, hipStream_t s) {
   if (n > 0) k_col_pair<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, col_idx, tile_of, pidx, n, col_pair);
@@ -1811,8 +1826,8 @@ bool outer_agg_supported(int L, int C, int H) {
   return o.nw >= 1 && o.nw <= (outer_ntw(L) == 8 ? 8 : 16) && o.lds <= 160 * 1024;
 }
 
-hipError_t launch_outer_agg(const DevTables& t, const float* Rp, const int64_t* row_ptr, const int32_t* col,
-                            const int32_t* col_pair, const float* alpha_hm, int64_t n_edges, const float* feat,
+hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* row_ptr, const int32_t* col,
+                            const float* alpha_hm, int64_t n_edges, const float* feat,
                             const int32_t* order, const int* cmeta, const float* ccoef, int ck, int cgroups, int n,
                             int C, int H, float* S, hipStream_t s) {
   if (n == 0) return hipSuccess;
@@ -1841,7 +1856,7 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Rp, const int64_t* 
 #define E2F_CASE(LL, NTWM, LB)                                                                              \
   case LL * 64 + NTWM * 4 + (LB == 512 ? 0 : 1):                                                            \
     if (hipError_t e = allow_lds(k_outer_agg<LL, NTWM, LB>, lds); e != hipSuccess) return e;                \
-    k_outer_agg<LL, NTWM, LB><<<(unsigned)blocks, 64 * o.nw, lds, s>>>(t, Rp, row_ptr, col, col_pair,       \
+    k_outer_agg<LL, NTWM, LB><<<(unsigned)blocks, 64 * o.nw, lds, s>>>(t, Re, row_ptr, col,                 \
                                                                       alpha_hm, n_edges, feat, order, cmeta, \
                                                                       ccoef, ck, cgroups, work_floats, n,    \
                                                                       nrx, rpw, C, H, S);                    \

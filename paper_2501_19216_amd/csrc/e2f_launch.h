@@ -55,6 +55,9 @@ size_t scan_tmp_bytes(int64_t count);
 hipError_t launch_scan_i32(const int32_t* in, int32_t* out, int64_t count, void* tmp, size_t tmp_bytes, hipStream_t s);
 hipError_t launch_pairs(const int32_t* flags, const int32_t* pidx, int64_t count, int n, int32_t* pair_node,
                         int32_t* pair_tile, hipStream_t s);
+// Re [E][nk] float32: Rp [pairs][nk] of each edge's pair, in edge order
+hipError_t launch_edge_R(const int32_t* col_pair, const float* Rp, int64_t n_edges, int nk, float* Re,
+                         hipStream_t s);
 hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of,
                            const int32_t* pidx, int n, int32_t* col_pair, hipStream_t s);
 
@@ -105,13 +108,13 @@ hipError_t launch_alpha_head_major(const float* alpha, int64_t n_edges, int H, f
 // y[order[r]] from S row r (head-major like T), r < n; shared_s: every r
 // reads S row 0
 // S rows r < n (receivers order[r]) by aggregating the uncoupled node products
-// alpha_ij R(p_j) (x) h_j and coupling per receiver (no T): Rp [pairs][nk] float32
-// (pair col_pair[e] of edge e), alpha_hm [H][n_edges] or NULL (ones)
+// alpha_ij R(p_j) (x) h_j and coupling per receiver (no T): Re [E][nk] float32
+// (launch_edge_R), alpha_hm [H][n_edges] or NULL (ones)
 // with the coupling schedule of couple_schedule(tables, outer_agg_groups(L, C, H))
 bool outer_agg_supported(int L, int C, int H);
 int outer_agg_groups(int L, int C, int H);
-hipError_t launch_outer_agg(const DevTables& t, const float* Rp, const int64_t* row_ptr, const int32_t* col,
-                            const int32_t* col_pair, const float* alpha_hm, int64_t n_edges, const float* feat,
+hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* row_ptr, const int32_t* col,
+                            const float* alpha_hm, int64_t n_edges, const float* feat,
                             const int32_t* order, const int* cmeta, const float* ccoef, int ck, int cgroups, int n,
                             int C, int H, float* S, hipStream_t s);
 // accumulate: y += the product instead of y = (one writer per element)
