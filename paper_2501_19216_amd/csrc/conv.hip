@@ -44,9 +44,12 @@ __device__ __forceinline__ F sh_poly(const DevTables& t, int k, F x, F y, F z) {
 // is c a x^(a-1) y^b z^e (no term when a = 0).
 template <typename F>
 __device__ __forceinline__ void sh_poly_grad(const DevTables& t, int k, F x, F y, F z, F& gx, F& gy, F& gz) {
-  auto ipow = [](F b, int n) {
+  // per monomial one power loop per coordinate: b^(n-1) (1 for n = 0, where
+  // the derivative's factor n is 0), then b^n = b^(n-1) b selected without a
+  // branch
+  auto pm1 = [](F b, int n) {
     F r = 1;
-    for (int q = 0; q < n; ++q) r *= b;
+    for (int q = 1; q < n; ++q) r *= b;
     return r;
   };
   gx = 0, gy = 0, gz = 0;
@@ -54,10 +57,11 @@ __device__ __forceinline__ void sh_poly_grad(const DevTables& t, int k, F x, F y
     const int pw = t.sh_pow[e];
     const int ex = pw & 15, ey = (pw >> 4) & 15, ez = (pw >> 8) & 15;
     const F c = (F)t.sh_coef[e];
-    const F X = ipow(x, ex), Y = ipow(y, ey), Z = ipow(z, ez);
-    if (ex) gx += c * (F)ex * ipow(x, ex - 1) * Y * Z;
-    if (ey) gy += c * (F)ey * X * ipow(y, ey - 1) * Z;
-    if (ez) gz += c * (F)ez * X * Y * ipow(z, ez - 1);
+    const F xm = pm1(x, ex), ym = pm1(y, ey), zm = pm1(z, ez);
+    const F X = ex > 0 ? xm * x : (F)1, Y = ey > 0 ? ym * y : (F)1, Z = ez > 0 ? zm * z : (F)1;
+    gx += c * (F)ex * xm * Y * Z;
+    gy += c * (F)ey * X * ym * Z;
+    gz += c * (F)ez * X * Y * zm;
   }
 }
 
