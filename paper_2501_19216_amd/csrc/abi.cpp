@@ -1018,11 +1018,18 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
   const size_t wt_bytes = (size_t)L1 * C * C * (p->mix_dtype == E2F_BF16 ? 2 : 4);
   const size_t tmp_b = transpose_tmp_bytes(n, n_edges);
   const bool want_t = (grad_feat != nullptr || grad_pos != nullptr) && n_edges > 0;
+  // the forces read the harmonic gradients of every edge from a table when it
+  // stays under 4 GiB (else the per-edge kernel evaluates them itself)
+  const size_t gt_bytes_full = sizeof(float) * 3 * (size_t)n_edges * (16 * ((nk + 15) / 16));
+  const char* gt_env = getenv("E2F_GEOM_GT");  // "0": always evaluate in the per-edge kernel (read per call)
+  const size_t gt_bytes = grad_pos && n_edges > 0 && gt_bytes_full <= ((size_t)4 << 30) && !(gt_env && atoi(gt_env) == 0)
+                              ? gt_bytes_full
+                              : 0;
   const size_t need = (mixing ? al256(sizeof(float) * (size_t)n * nk * C) + al256(wt_bytes) : 0) +
                       (want_t ? 5 * al256(sizeof(int32_t) * (size_t)n_edges) + 2 * al256(sizeof(int64_t) * (n + 1)) +
                                     al256(sizeof(float) * (size_t)n_edges * H) + al256(tmp_b)
                               : 0) +
-                      (grad_pos ? al256(sizeof(float) * (size_t)n_edges * 3) : 0) + 256;
+                      (grad_pos ? al256(sizeof(float) * (size_t)n_edges * 3) : 0) + al256(gt_bytes) + 256;
   rs = ensure(ctx, ctx->d, need, s);
   if (rs != E2F_OK) return rs;
   Carver cd{(char*)ctx->d.p};
@@ -1045,8 +1052,9 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
   int32_t* colT = nullptr;
   int64_t* rowT = nullptr;
   float* alphaT = nullptr;
+  int32_t* rows = nullptr;  // the receiver of every edge
   if (want_t) {
-    int32_t* rows = cd.take<int32_t>((size_t)n_edges);
+    rows = cd.take<int32_t>((size_t)n_edges);
     int32_t* iota = cd.take<int32_t>((size_t)n_edges);
     int32_t* keys_out = cd.take<int32_t>((size_t)n_edges);
     perm = cd.take<int32_t>((size_t)n_edges);
@@ -1061,11 +1069,14 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
   // ---- attention weights and positions: per edge, both from one product per
   // (receiver, head); then per atom the forces received minus those sent
   float* gedge = grad_pos ? cd.take<float>((size_t)n_edges * 3) : nullptr;
+  float* Gt = gt_bytes ? cd.take<float>(gt_bytes / sizeof(float)) : nullptr;
+  if (Gt) E2F_TIMED("edge_geom", launch_edge_shgrad(ctx->dev[L], pos, rows, col_idx, n_edges, Gt, s));
   if (grad_alpha || gedge) {
     const e2f_ctx::Geom* gsch = nullptr;
     if ((rs = geom_of(ctx, L, C / H, gsch)) != E2F_OK) return rs;
     E2F_TIMED("edge_geom", launch_edge_geom(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, alpha, n, C, H, gsch->qc,
-                                            gsch->meta, gsch->unit, gsch->oc, gsch->tot, grad_alpha, gedge, s));
+                                            gsch->meta, gsch->unit, gsch->oc, gsch->tot, Gt, n_edges, grad_alpha,
+                                            gedge, s));
   }
   if (gedge) E2F_TIMED("force_gather", launch_force_gather(row_ptr, rowT, perm, gedge, n, grad_pos, s));
   // ---- features: the same layer on the transposed graph, input degree o,

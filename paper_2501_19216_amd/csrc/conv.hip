@@ -1160,16 +1160,17 @@ __global__ void k_plan_pack(const int32_t* __restrict__ pidx, const int32_t* __r
 // operand read start in distinct bank quadruples).  A workgroup takes
 // rpw consecutive receivers; edge chunks of NW NTE 16 edges, Z rebuilt per
 // chunk, head and row pass.  Each output element has one writer.
-template <int L, int NTE, bool WA, bool WP>
-__global__ __launch_bounds__(256) void k_edge_geom(DevTables t, const float* __restrict__ pos,
+template <int L, int NTE, bool WA, bool WP, bool GT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_edge_geom(DevTables t, const float* __restrict__ pos,
                                                    const float* __restrict__ feat, const float* __restrict__ gy,
                                                    const int64_t* __restrict__ row_ptr,
                                                    const int32_t* __restrict__ col, const float* __restrict__ alpha,
                                                    int n, int rpw, int C, int H, int qc,
                                                    const int* __restrict__ gmeta, const float* __restrict__ gunit,
                                                    const int* __restrict__ goc, int gtot,
+                                                   const float* __restrict__ Gt, int64_t n_edges,
                                                    float* __restrict__ galpha, float* __restrict__ gedge) {
-  constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16;
+  constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
   constexpr bool STAGED = L <= 4;  // the schedule in LDS (it outgrows LDS above L = 4)
   extern __shared__ float4 sm4[];
   const int dh = C / H, dq = dh >> 2, ZS = qc * dh + (((qc * dh) >> 2) & 1 ? 8 : 4);
@@ -1333,17 +1334,32 @@ __global__ __launch_bounds__(256) void k_edge_geom(DevTables t, const float* __r
         for (int et = 0; et < NTE; ++et) {
           if (wave + NW * et >= ntiles) continue;  // uniform over the wave
           float fx = 0.f, fy = 0.f, fz = 0.f;
+          if (GT) {
+            // the gradients from the per-edge table [3][E][MP] (zeros past NK)
+            const int64_t ec = c0 + (ev[et] ? (wave + NW * et) * 16 + l16 : 0);
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-              const int be = mt * 16 + 4 * k4 + v;
-              if (be < NK) {
-                float gx, gyy, gz;
-                sh_poly_grad<float>(t, be, dx[et], dy[et], dz[et], gx, gyy, gz);
-                fx += gx * W[et][mt][v], fy += gyy * W[et][mt][v], fz += gz * W[et][mt][v];
-              }
+            for (int mt = 0; mt < MT; ++mt) {
+              const float* gp = Gt + (size_t)ec * MP + mt * 16 + 4 * k4;
+              const float4 gx = *(const float4*)gp, gyy = *(const float4*)(gp + (size_t)n_edges * MP),
+                           gz = *(const float4*)(gp + 2 * (size_t)n_edges * MP);
+              const v4f w = W[et][mt];
+              fx += gx.x * w[0] + gx.y * w[1] + gx.z * w[2] + gx.w * w[3];
+              fy += gyy.x * w[0] + gyy.y * w[1] + gyy.z * w[2] + gyy.w * w[3];
+              fz += gz.x * w[0] + gz.y * w[1] + gz.z * w[2] + gz.w * w[3];
             }
+          } else {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+              for (int v = 0; v < 4; ++v) {
+                const int be = mt * 16 + 4 * k4 + v;
+                if (be < NK) {
+                  float gx, gyy, gz;
+                  sh_poly_grad<float>(t, be, dx[et], dy[et], dz[et], gx, gyy, gz);
+                  fx += gx * W[et][mt][v], fy += gyy * W[et][mt][v], fz += gz * W[et][mt][v];
+                }
+              }
+          }
           fx += __shfl_xor(fx, 16), fy += __shfl_xor(fy, 16), fz += __shfl_xor(fz, 16);
           fx += __shfl_xor(fx, 32), fy += __shfl_xor(fy, 32), fz += __shfl_xor(fz, 32);
           if (k4 == 0 && ev[et]) {
@@ -2021,8 +2037,8 @@ size_t edge_geom_lds(int L, int dh, int qc, int gtot) {
 
 hipError_t launch_edge_geom(const DevTables& t, const float* pos, const float* feat, const float* gy,
                             const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n, int C, int H,
-                            int qc, const int* gmeta, const float* gunit, const int* goc, int gtot, float* galpha,
-                            float* gedge, hipStream_t s) {
+                            int qc, const int* gmeta, const float* gunit, const int* goc, int gtot, const float* Gt,
+                            int64_t n_edges, float* galpha, float* gedge, hipStream_t s) {
   if (n == 0 || (!galpha && !gedge)) return hipSuccess;
   if (!edge_geom_supported(C, H) || qc < 1 || qc > t.nk) return hipErrorInvalidValue;
   const int dh = C / H;
@@ -2034,20 +2050,53 @@ hipError_t launch_edge_geom(const DevTables& t, const float* pos, const float* f
   const int nxr = (n + 7) / 8;
   const unsigned grid = 8u * (unsigned)((nxr + rpw - 1) / rpw);
   const int geom_threads = 256;  // four waves of two edge tiles (the schedule's 128 threads build Z)
-  switch (t.L * 4 + mode) {
-#define E2F_G(LL, WA_, WP_)                                                                                   \
-  case LL * 4 + (WA_ ? 1 : 0) + (WP_ ? 2 : 0):                                                                \
-    if (hipError_t e = allow_lds(k_edge_geom<LL, 2, WA_, WP_>, lds); e != hipSuccess) return e;               \
-    k_edge_geom<LL, 2, WA_, WP_><<<grid, geom_threads, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx,           \
+  switch (t.L * 8 + mode + (Gt && gedge ? 4 : 0)) {
+#define E2F_G(LL, WA_, WP_, GT_)                                                                              \
+  case LL * 8 + (WA_ ? 1 : 0) + (WP_ ? 2 : 0) + (GT_ ? 4 : 0):                                                \
+    if (hipError_t e = allow_lds(k_edge_geom<LL, 2, WA_, WP_, GT_>, lds); e != hipSuccess) return e;          \
+    k_edge_geom<LL, 2, WA_, WP_, GT_><<<grid, geom_threads, lds, s>>>(t, pos, feat, gy, row_ptr, col_idx,      \
                                                                          alpha, n, rpw, C, H, qc, gmeta,     \
-                                                                         gunit, goc, gtot, galpha, gedge);   \
+                                                                         gunit, goc, gtot, Gt, n_edges,      \
+                                                                         galpha, gedge);                     \
     break;
-#define E2F_GL(LL) E2F_G(LL, true, false) E2F_G(LL, false, true) E2F_G(LL, true, true)
+#define E2F_GL(LL)                                                                                            \
+  E2F_G(LL, true, false, false) E2F_G(LL, false, true, false) E2F_G(LL, true, true, false)                    \
+  E2F_G(LL, false, true, true) E2F_G(LL, true, true, true)
     E2F_GL(0) E2F_GL(1) E2F_GL(2) E2F_GL(3) E2F_GL(4) E2F_GL(5) E2F_GL(6)
 #undef E2F_GL
 #undef E2F_G
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+// Gradients of the solid harmonics of every edge, r_e = r_i - r_j:
+// Gt[c][e][be] = dR_be/dr_c (c = x, y, z), rows padded to MP = 16 ceil(nk/16)
+// with zeros.  One thread per (edge, component be).
+__global__ void k_edge_shgrad(DevTables t, const float* __restrict__ pos, const int32_t* __restrict__ rows,
+                              const int32_t* __restrict__ col, int64_t n_edges, int mp, float* __restrict__ Gt) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= n_edges * mp) return;
+  const int64_t e = x / mp;
+  const int be = (int)(x - e * mp);
+  float gx = 0.f, gyy = 0.f, gz = 0.f;
+  if (be < t.nk) {
+    const int i = rows[e], j = col[e];
+    sh_poly_grad<float>(t, be, pos[3 * i] - pos[3 * j], pos[3 * i + 1] - pos[3 * j + 1], pos[3 * i + 2] - pos[3 * j + 2],
+                        gx, gyy, gz);
+  }
+  Gt[x] = gx;
+  Gt[(size_t)n_edges * mp + x] = gyy;
+  Gt[2 * (size_t)n_edges * mp + x] = gz;
+}
+
+hipError_t launch_edge_shgrad(const DevTables& t, const float* pos, const int32_t* rows, const int32_t* col,
+                              int64_t n_edges, float* Gt, hipStream_t s) {
+  if (n_edges == 0) return hipSuccess;
+  const int mp = 16 * ((t.nk + 15) / 16);
+  const int64_t blocks = (n_edges * mp + 255) / 256;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  k_edge_shgrad<<<(unsigned)blocks, 256, 0, s>>>(t, pos, rows, col, n_edges, mp, Gt);
   return hipGetLastError();
 }
 

@@ -184,3 +184,14 @@ def test_backward_without_edges(e2f, ctx):
     gf, ga, gp = e2f.e2f_wigner6j_conv_backward(ctx, gpu(pos), gpu(feat), gpu(gout), gpu(rp), gpu(ci),
                                                 gpu(np.zeros((0, 4), np.float32)), 3, 4, 5.0, want_pos=True)
     assert ga.shape == (0, 4) and (gf.cpu().numpy() == 0).all() and (gp.cpu().numpy() == 0).all()
+
+
+def test_backward_forces_without_gradient_table(e2f, ctx, monkeypatch):
+    # the per-edge kernel evaluates the harmonic gradients itself when the
+    # per-edge table would exceed its memory cap; force that path here
+    monkeypatch.setenv("E2F_GEOM_GT", "0")
+    rng = np.random.default_rng(41)
+    pos = syn.quantize(rng.uniform(0, 14, size=(400, 3)))
+    rp, ci = o.neighbor_list(pos, 5.0)
+    check(e2f, ctx, pos, rp, ci, 4, 32, 2, 5.0, 42)
+    check(e2f, ctx, pos, rp, ci, 6, 16, 4, 5.0, 43)
