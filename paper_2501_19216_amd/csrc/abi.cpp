@@ -837,15 +837,19 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   ctx->last_tiles = keys;
   // the MFMA aggregation over receiver blocks of 16 needs 16 * degree <= 8192
   const bool use_blocks = max_degree <= kBlockMaxDegree;
-  // alpha / D^f: one aggregation and one S per filter degree f
+  // alpha / D^f: one aggregation per filter degree f
   const bool ynorm = p->y_norm != 0;
-  const int nS = ynorm ? L + 1 : 1;
-  if (ynorm && !use_blocks)
-    return fail(E2F_EUNSUPPORTED, "y_norm needs every degree <= %d (largest %d)", kBlockMaxDegree, max_degree);
   // aggregation of the uncoupled node products (no T); E2F_AGG_T selects the
-  // T-row aggregation over receiver blocks instead (comparison, and y_norm)
+  // T-row aggregation over receiver blocks instead (comparison)
   static const bool force_t = getenv("E2F_AGG_T") != nullptr;
-  const bool outer = !ynorm && !force_t && outer_agg_supported(L, C, p->heads);
+  const bool outer = !force_t && outer_agg_supported(L, C, p->heads);
+  // S buffers: with the T rows, one per filter degree under y_norm (all the
+  // aggregations run before the recouples); the reordered aggregation reuses
+  // one (aggregation and recouple of each degree in turn)
+  const int nS = ynorm && !outer ? L + 1 : 1;
+  const int nA = ynorm ? L + 1 : 1;  // head-major attention weights per filter degree
+  if (ynorm && !outer && !use_blocks)
+    return fail(E2F_EUNSUPPORTED, "y_norm needs every degree <= %d (largest %d)", kBlockMaxDegree, max_degree);
   // ---- tile batches: T and S of a batch must fit the memory budget
   const size_t row_bytes = sizeof(float) * (size_t)t.dimT * C;
   size_t free_b = 0, total_b = 0;
@@ -880,7 +884,7 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
                         al256(sizeof(double) * (size_t)n * nk) +
                         (outer ? 0 : al256(row_bytes * (size_t)max_pairs)) + al256(row_bytes * (size_t)max_recv * nS) +
                         (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0) +
-                        ((use_blocks || outer) && (alpha || ynorm) ? al256(sizeof(float) * (size_t)n_edges * p->heads * nS)
+                        ((use_blocks || outer) && (alpha || ynorm) ? al256(sizeof(float) * (size_t)n_edges * p->heads * nA)
                                                                    : 0) +
                         (ynorm ? al256(sizeof(int32_t) * (size_t)n_edges) : 0);
   rs = ensure(ctx, ctx->b, need_b, s);
@@ -903,7 +907,7 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   float* S = cb.take<float>((size_t)max_recv * t.dimT * C * nS);
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
   float* alpha_hm =
-      (use_blocks || outer) && (alpha || ynorm) ? cb.take<float>((size_t)n_edges * p->heads * nS) : nullptr;
+      (use_blocks || outer) && (alpha || ynorm) ? cb.take<float>((size_t)n_edges * p->heads * nA) : nullptr;
   if (ynorm) {
     int32_t* erows = cb.take<int32_t>((size_t)n_edges);
     E2F_TIMED("alpha_hm", launch_alpha_dnorm(pos, row_ptr, col_idx, alpha, n, n_edges, p->heads, L, erows, alpha_hm, s));
@@ -924,10 +928,27 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
     const int pb = pstart[bt.t1] - p0, nb = rstart[bt.t1] - q0;
     if (nb == 0) continue;
     const int32_t* ord = order + q0;
-    if (outer) {
+    if (outer && !ynorm) {
       E2F_TIMED("aggregate", launch_outer_agg(t, Re, row_ptr, col_idx, alpha_hm, n_edges, feat, ord,
                                               cpl->meta, cpl->coef, cpl->k, cgroups, nb, C, p->heads, S, s));
       E2F_TIMED("recouple", launch_recouple(t, Rr, S, false, ord, nb, C, dh, y, s));
+      continue;
+    }
+    if (outer) {
+      // S^(f) = sum_j alpha_ij D_ij^-f [h_j (x) R(p_j)] coupled, then the
+      // recouple terms of filter degree b + u = f; the f = 0 pass stores y,
+      // the others add
+      for (int f = 0; f <= L; ++f) {
+        E2F_TIMED("aggregate", launch_outer_agg(t, Re, row_ptr, col_idx, alpha_hm + (size_t)f * p->heads * n_edges,
+                                                n_edges, feat, ord, cpl->meta, cpl->coef, cpl->k, cgroups, nb, C,
+                                                p->heads, S, s));
+        DevTables tf = t;
+        tf.rc_k = ctx->rcf_k[L][f];
+        tf.rc_off = ctx->rcf_off[L][f];
+        tf.rc_meta = ctx->rcf_meta[L][f];
+        tf.rc_coef = ctx->rcf_coef[L][f];
+        E2F_TIMED("recouple", launch_recouple(tf, Rr, S, false, ord, nb, C, dh, y, s, f > 0));
+      }
       continue;
     }
     E2F_TIMED("node_tp", launch_node_tp(t, Rp + (size_t)p0 * nk, pair_node + p0, feat, pb, C, dh, T, s));
