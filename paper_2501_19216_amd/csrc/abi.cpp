@@ -1041,7 +1041,7 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
   const bool want_t = (grad_feat != nullptr || grad_pos != nullptr) && n_edges > 0;
   // the forces read the harmonic gradients of every edge from a table when it
   // stays under 4 GiB (else the per-edge kernel evaluates them itself)
-  const size_t gt_bytes_full = sizeof(float) * 3 * (size_t)n_edges * (16 * ((nk + 15) / 16));
+  const size_t gt_bytes_full = sizeof(float) * 3 * (size_t)n_edges * nk;
   const char* gt_env = getenv("E2F_GEOM_GT");  // "0": always evaluate in the per-edge kernel (read per call)
   const size_t gt_bytes = grad_pos && n_edges > 0 && gt_bytes_full <= ((size_t)4 << 30) && !(gt_env && atoi(gt_env) == 0)
                               ? gt_bytes_full

@@ -1170,7 +1170,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
                                                    const int* __restrict__ goc, int gtot,
                                                    const float* __restrict__ Gt, int64_t n_edges,
                                                    float* __restrict__ galpha, float* __restrict__ gedge) {
-  constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
+  constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16;
   constexpr bool STAGED = L <= 4;  // the schedule in LDS (it outgrows LDS above L = 4)
   extern __shared__ float4 sm4[];
   const int dh = C / H, dq = dh >> 2, ZS = qc * dh + (((qc * dh) >> 2) & 1 ? 8 : 4);
@@ -1335,18 +1335,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
           if (wave + NW * et >= ntiles) continue;  // uniform over the wave
           float fx = 0.f, fy = 0.f, fz = 0.f;
           if (GT) {
-            // the gradients from the per-edge table [3][E][MP] (zeros past NK)
+            // the gradients from the per-edge table [3][NK][E] (consecutive
+            // lanes l16 read consecutive edges)
             const int64_t ec = c0 + (ev[et] ? (wave + NW * et) * 16 + l16 : 0);
+            const size_t plane = (size_t)NK * n_edges;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-              const float* gp = Gt + (size_t)ec * MP + mt * 16 + 4 * k4;
-              const float4 gx = *(const float4*)gp, gyy = *(const float4*)(gp + (size_t)n_edges * MP),
-                           gz = *(const float4*)(gp + 2 * (size_t)n_edges * MP);
-              const v4f w = W[et][mt];
-              fx += gx.x * w[0] + gx.y * w[1] + gx.z * w[2] + gx.w * w[3];
-              fy += gyy.x * w[0] + gyy.y * w[1] + gyy.z * w[2] + gyy.w * w[3];
-              fz += gz.x * w[0] + gz.y * w[1] + gz.z * w[2] + gz.w * w[3];
-            }
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+              for (int v = 0; v < 4; ++v) {
+                const int be = mt * 16 + 4 * k4 + v;
+                if (be < NK) {
+                  const float* gp = Gt + (size_t)be * n_edges + ec;
+                  const float w = W[et][mt][v];
+                  fx += gp[0] * w, fy += gp[plane] * w, fz += gp[2 * plane] * w;
+                }
+              }
           } else {
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
@@ -2071,32 +2074,30 @@ hipError_t launch_edge_geom(const DevTables& t, const float* pos, const float* f
 }
 
 // Gradients of the solid harmonics of every edge, r_e = r_i - r_j:
-// Gt[c][e][be] = dR_be/dr_c (c = x, y, z), rows padded to MP = 16 ceil(nk/16)
-// with zeros.  One thread per (edge, component be).
+// Gt[c][be][e] = dR_be/dr_c (c = x, y, z) for be < nk.  Component-major:
+// blockIdx.y = be, so a wave evaluates one polynomial (no divergence, its
+// table reads uniform) and stores consecutive edges.
 __global__ void k_edge_shgrad(DevTables t, const float* __restrict__ pos, const int32_t* __restrict__ rows,
-                              const int32_t* __restrict__ col, int64_t n_edges, int mp, float* __restrict__ Gt) {
-  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (x >= n_edges * mp) return;
-  const int64_t e = x / mp;
-  const int be = (int)(x - e * mp);
-  float gx = 0.f, gyy = 0.f, gz = 0.f;
-  if (be < t.nk) {
-    const int i = rows[e], j = col[e];
-    sh_poly_grad<float>(t, be, pos[3 * i] - pos[3 * j], pos[3 * i + 1] - pos[3 * j + 1], pos[3 * i + 2] - pos[3 * j + 2],
-                        gx, gyy, gz);
-  }
+                              const int32_t* __restrict__ col, int64_t n_edges, float* __restrict__ Gt) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int be = blockIdx.y;
+  if (e >= n_edges) return;
+  const int i = rows[e], j = col[e];
+  float gx, gyy, gz;
+  sh_poly_grad<float>(t, be, pos[3 * i] - pos[3 * j], pos[3 * i + 1] - pos[3 * j + 1], pos[3 * i + 2] - pos[3 * j + 2],
+                      gx, gyy, gz);
+  const size_t plane = (size_t)t.nk * n_edges, x = (size_t)be * n_edges + e;
   Gt[x] = gx;
-  Gt[(size_t)n_edges * mp + x] = gyy;
-  Gt[2 * (size_t)n_edges * mp + x] = gz;
+  Gt[plane + x] = gyy;
+  Gt[2 * plane + x] = gz;
 }
 
 hipError_t launch_edge_shgrad(const DevTables& t, const float* pos, const int32_t* rows, const int32_t* col,
                               int64_t n_edges, float* Gt, hipStream_t s) {
   if (n_edges == 0) return hipSuccess;
-  const int mp = 16 * ((t.nk + 15) / 16);
-  const int64_t blocks = (n_edges * mp + 255) / 256;
+  const int64_t blocks = (n_edges + 255) / 256;
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  k_edge_shgrad<<<(unsigned)blocks, 256, 0, s>>>(t, pos, rows, col, n_edges, mp, Gt);
+  k_edge_shgrad<<<dim3((unsigned)blocks, (unsigned)t.nk), 256, 0, s>>>(t, pos, rows, col, n_edges, Gt);
   return hipGetLastError();
 }
 

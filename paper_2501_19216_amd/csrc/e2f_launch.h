@@ -146,8 +146,8 @@ hipError_t launch_edge_geom(const DevTables& t, const float* pos, const float* f
                             const int64_t* row_ptr, const int32_t* col_idx, const float* alpha, int n, int C, int H,
                             int qc, const int* gmeta, const float* gunit, const int* goc, int gtot, const float* Gt,
                             int64_t n_edges, float* galpha, float* gedge, hipStream_t s);
-// Gt [3][E][16 ceil(nk/16)]: the harmonic gradients of every edge (rows: the
-// receiver of each edge), read by launch_edge_geom when not NULL
+// Gt [3][nk][E]: the harmonic gradients of every edge (rows: the receiver of
+// each edge), read by launch_edge_geom when not NULL
 hipError_t launch_edge_shgrad(const DevTables& t, const float* pos, const int32_t* rows, const int32_t* col,
                               int64_t n_edges, float* Gt, hipStream_t s);
 hipError_t launch_force_gather(const int64_t* row_ptr, const int64_t* rowT, const int32_t* perm, const float* gedge,
