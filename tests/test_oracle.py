@@ -7,6 +7,7 @@ them.
 """
 import itertools
 import math
+import os
 
 import numpy as np
 import pytest
@@ -20,13 +21,28 @@ def tri(a, b, c):
     return abs(a - b) <= c <= a + b
 
 
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def golden_lines(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return [ln.split() for ln in f if ln.strip() and not ln.lstrip().startswith("#")]
+
+
 # ---------------------------------------------------------------- 3j / CG
+def test_wigner_symbols_tabulated():
+    # tests/golden/wigner_symbols_tabulated.txt: exact tabulated 3j and 6j values
+    rows = golden_lines("wigner_symbols_tabulated.txt")
+    assert len(rows) >= 9
+    for r in rows:
+        j = [int(v) for v in r[1:7]]
+        sign, num, den = int(r[7]), int(r[8]), int(r[9])
+        want = sign * math.sqrt(num / den)
+        got = o.wigner3j(*j) if r[0] == "3j" else o.wigner6j(*j)
+        assert got == pytest.approx(want, abs=1e-15), r
+
+
 def test_3j_textbook_values():
-    # standard tabulated values (e.g. Edmonds, Table 2)
-    assert o.wigner3j(1, 1, 0, 0, 0, 0) == pytest.approx(-1 / math.sqrt(3), abs=1e-15)
-    assert o.wigner3j(1, 1, 2, 0, 0, 0) == pytest.approx(math.sqrt(2 / 15), abs=1e-15)
-    assert o.wigner3j(2, 2, 2, 0, 0, 0) == pytest.approx(-math.sqrt(2 / 35), abs=1e-15)
-    assert o.wigner3j(1, 1, 1, 1, -1, 0) == pytest.approx(1 / math.sqrt(6), abs=1e-15)
     assert o.cg_complex(1, 0, 1, 0, 0, 0) == pytest.approx(-1 / math.sqrt(3), abs=1e-15)
     assert o.cg_complex(1, 1, 1, 0, 2, 1) == pytest.approx(1 / math.sqrt(2), abs=1e-15)
     # selection rules (App. C.1)
@@ -126,16 +142,33 @@ def test_solid_harmonics_closed_form():
 
 
 def test_solid_harmonics_paper_shapes():
-    # Def. 2.1: R^(1)(v) proportional to (y, z, x); R^(2) proportional to
-    # (xy, yz, 3z^2 - r^2, xz, x^2 - y^2), m = -2..2
+    # Def. 2.1: R^(1)(v) proportional to (y, z, x); the degree-2 example the
+    # paper prints (tests/golden/real_sh_degree2_cartesian.txt): each R^(2)_m
+    # is a fixed positive multiple of its Cartesian form
     v = np.array([0.37, -1.21, 0.83])
     x, y, z = v
-    r2 = v @ v
     R = o.solid_harmonics(2, v)
     assert np.allclose(R[1:4], [y, z, x], atol=1e-15)
-    shapes = np.array([x * y, y * z, 3 * z * z - r2, x * z, x * x - y * y])
+    forms = {}
+    for r in golden_lines("real_sh_degree2_cartesian.txt"):
+        terms = []
+        for tok in r[1:]:
+            c, e = tok.split(":")
+            terms.append((float(c), [int(k) for k in e.split(",")]))
+        forms[int(r[0])] = terms
+    assert sorted(forms) == [-2, -1, 0, 1, 2]
+
+    def form(m, p):
+        return sum(c * p[0] ** e[0] * p[1] ** e[1] * p[2] ** e[2] for c, e in forms[m])
+
+    rng = np.random.default_rng(7)
+    pts = rng.standard_normal((6, 3))
+    for m in range(-2, 3):
+        ratios = [o.solid_harmonics(2, p)[4 + m + 2] / form(m, p) for p in pts]
+        assert min(ratios) > 0 and max(ratios) - min(ratios) <= 1e-12 * max(ratios), (m, ratios)
+    # the constants of the stretched-power convention (C_l scaled by sqrt(l!/(2l-1)!!))
     scale = np.array([math.sqrt(2), math.sqrt(2), 1 / math.sqrt(6), math.sqrt(2), 1 / math.sqrt(2)])
-    assert np.allclose(R[4:9], scale * shapes, atol=1e-14)
+    assert np.allclose(R[4:9], scale * np.array([form(m, v) for m in range(-2, 3)]), atol=1e-14)
     # value on the z axis: R^(l)_0(z) = sqrt(l!/(2l-1)!!)
     Rz = o.solid_harmonics(6, np.array([0.0, 0.0, 1.0]))
     for l in range(7):
