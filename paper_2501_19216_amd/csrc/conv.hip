@@ -920,22 +920,25 @@ __global__ __launch_bounds__(256) void k_recouple(DevTables t, const double* __r
       run_schedule(t.rc_meta + t.rc_off[ch], t.rc_coef + t.rc_off[ch], t.rc_k[ch], Rl, Qt);
       __syncthreads();
       auto mma = [&](int stg, float (*bv)[NTW]) {
+        // the stage's A values read from LDS together, then its MFMAs
+        float a[ST][MT];
 #pragma unroll
         for (int u = 0; u < ST; ++u) {
           const int rl = (stg * ST + u) * 4 + k4;
           const int rq = min(rl, RR - 1);
-          float a[MT];
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
             const float qv = Qt[rq * QS + mt * 16 + j];
-            a[mt] = rl < rc ? qv : 0.0f;
+            a[u][mt] = rl < rc ? qv : 0.0f;
           }
+        }
+#pragma unroll
+        for (int u = 0; u < ST; ++u)
 #pragma unroll
           for (int q = 0; q < NTW; ++q)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
-              acc[q][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bv[u][q], acc[q][mt], 0, 0, 0);
-        }
+              acc[q][mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][mt], bv[u][q], acc[q][mt], 0, 0, 0);
       };
       const int nstage = (rc + 4 * ST - 1) / (4 * ST);
       for (int sp = 0; sp < nstage; sp += 2) {
