@@ -841,7 +841,8 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
   const bool ynorm = p->y_norm != 0;
   // aggregation of the uncoupled node products (no T); E2F_AGG_T selects the
   // T-row aggregation over receiver blocks instead (comparison)
-  static const bool force_t = getenv("E2F_AGG_T") != nullptr;
+  const char* agg_t = getenv("E2F_AGG_T");  // read per call
+  const bool force_t = agg_t && atoi(agg_t) != 0;
   const bool outer = !force_t && outer_agg_supported(L, C, p->heads);
   // S buffers: with the T rows, one per filter degree under y_norm (all the
   // aggregations run before the recouples); the reordered aggregation reuses

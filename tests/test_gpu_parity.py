@@ -220,6 +220,28 @@ def test_determinism_and_translation(e2f, ctx):
     assert o.max_rel_err(a3, a1, wl.lmax) <= TOL_F32 and o.max_rel_err(b3, b1, wl.lmax) <= TOL_F32
 
 
+@pytest.mark.parametrize("L,C,H,cut,n,box", [(2, 32, 4, 5.0, 300, 12.0), (4, 64, 4, 5.0, 300, 12.0),
+                                              (2, 16, 2, 30.0, 700, 10.0)])
+def test_conv_stored_t_rows(e2f, ctx, monkeypatch, L, C, H, cut, n, box):
+    # the aggregation of stored T rows (E2F_AGG_T): over 16-receiver blocks,
+    # and row by row when a receiver has more than 512 neighbours (the last
+    # case is a complete graph of 700 atoms)
+    monkeypatch.setenv("E2F_AGG_T", "1")
+    rng = np.random.default_rng(100 + L + n)
+    pos = syn.quantize(rng.uniform(0, box, size=(n, 3)))
+    rp, ci = o.neighbor_list(pos, cut)
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    alpha = rng.uniform(0.05, 1.0, size=(len(ci), H)).astype(np.float32)
+    w = rng.uniform(0.2, 1.0, size=(L + 1) ** 3)
+    ref = o.conv_edge(L, H, pos, feat, rp, ci, alpha, w)
+    print("stored T rows: L %d C %d n %d max degree %d" % (L, C, n, int(np.diff(rp).max())), flush=True)
+    got = e2f.e2f_wigner6j_conv_forward(ctx, gpu(pos), gpu(feat), gpu(rp), gpu(ci), gpu(alpha), L, H, cut,
+                                        path_w=w).cpu().numpy()
+    err = o.max_rel_err(got, ref, L)
+    print("stored T rows: err %.3e" % err)
+    assert err <= TOL_F32
+
+
 def test_conv_tile_batches(e2f, ctx, monkeypatch):
     # small tiles and a tiny memory budget force many tiles and several batches
     inp, rp, ci, alpha = case("water2000_L4")
