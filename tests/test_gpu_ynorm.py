@@ -1,7 +1,8 @@
 """Alg. 1's per-degree attention weights alpha / D^f (Y-based filters, the
 y_norm flag): both forms of the layer on the GPU against the oracle's
 definition of the variant.  The factorised forward aggregates once per
-filter degree f and recouples the terms of degree b + u = f from S^(f).
+filter degree f and recouples the terms of degree b + u = f from S^(f)
+(through the reordered aggregation, or the stored T rows with E2F_AGG_T).
 
 Run with -m gpu."""
 import numpy as np
@@ -62,6 +63,22 @@ def test_y_norm_workloads(e2f, ctx, name, rows, mix):
     # the variant differs from the plain layer (the flag reaches both kernels)
     plain = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, mw, rows=r[:8])
     assert o.max_rel_err(ref[:8], plain, wl.lmax) > 1e-2
+
+
+@pytest.mark.parametrize("name,rows", [("molecules256x30_L3", 256), ("water2000_L4", 64)])
+def test_y_norm_stored_t_rows(e2f, ctx, monkeypatch, name, rows):
+    # the same variant through the aggregation of stored T rows (E2F_AGG_T):
+    # one S buffer per filter degree, every aggregation before the recouples
+    monkeypatch.setenv("E2F_AGG_T", "1")
+    inp, rp, ci, alpha = case(name)
+    wl = inp.workload
+    r = sample_rows(inp.pos.shape[0], rows, seed=13)
+    ref = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, inp.mix_w, rows=r, y_norm=True)
+    print("%s y_norm stored T: case" % name, flush=True)
+    y6, _ = both(e2f, ctx, inp, rp, ci, alpha, wl, inp.mix_w)
+    e6 = o.max_rel_err(y6[r], ref, wl.lmax)
+    print("%s y_norm stored T: 6j %.3e" % (name, e6))
+    assert e6 <= TOL_F32
 
 
 def jittered_lattice(k, spacing, jitter, seed):
