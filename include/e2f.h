@@ -186,9 +186,11 @@ e2f_status e2f_wigner6j_conv_forward_dense(e2f_ctx* ctx, const e2f_conv_params* 
  * R^(u)(r_i - o) (Thm. 3.3): O(N).  o is the centre of the bounding box; the
  * self term of j = i is R^(f)(0) = [f == 0].  heads only sets the layout of
  * the intermediates (every head sees the same weights); tile_side is unused.
- * out: [N][(L+1)^2][C].  M is summed in float64 in a fixed order
- * (deterministic).  Workspace: about N (L+1)^2 doubles plus the T rows of one
- * batch of atoms (at most 8 GiB).  (sync: one small device->host read) */
+ * out: [N][(L+1)^2][C].  The moments are taken of the uncoupled products,
+ * G = sum_j R(r_j - o) (x) h_j, summed in float64 in a fixed order
+ * (deterministic), and coupled once.  Workspace: N (L+1)^2 doubles plus
+ * float64 partial sums of G (about 2048 (L+1)^2 * 256 doubles, some 10-25 MB).
+ * (sync: one small device->host read) */
 e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
                                             const float* feat, int32_t n, float* out, void* stream);
 

@@ -1212,34 +1212,29 @@ e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params*
   // one origin, the centre of the bounding box (every pair is coupled)
   double origin[3];
   for (int k = 0; k < 3; ++k) origin[k] = (((int64_t)st[k] + st[3 + k]) / 2) / kGrid;
-  const int64_t W = (int64_t)t.dimT * C;
-  const size_t rowb = sizeof(float) * (size_t)W;
-  // T is produced and summed in batches of at most 8 GB
-  const int nbmax = (int)std::max<int64_t>(1, std::min<int64_t>(n, (int64_t)(((size_t)8 << 30) / rowb)));
-  const int G = moment_groups(nbmax, W);
+  // the moment of the uncoupled products G[be][(q, c)] = sum_j R_be(p_j) h_j[q][c]
+  // (fp64, fixed order), coupled once into the shared S row
+  const int64_t W = (int64_t)t.dimT * C, WG = (int64_t)nk * nk * C;
+  const int G = global_groups(n, nk, C);
   const bool mixing = p->mix_w != nullptr;
-  const size_t need = al256(sizeof(double) * 3) + al256(sizeof(double) * (size_t)n * nk) + al256(rowb * nbmax) +
-                      al256(sizeof(double) * (size_t)G * W) + al256(sizeof(double) * (size_t)W) + al256(rowb) +
-                      al256(sizeof(int32_t) * (size_t)n) + (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
+  const size_t need = al256(sizeof(double) * 3) + al256(sizeof(double) * (size_t)n * nk) +
+                      al256(sizeof(double) * (size_t)G * WG) + al256(sizeof(double) * (size_t)WG) +
+                      al256(sizeof(float) * (size_t)W) + al256(sizeof(int32_t) * (size_t)n) +
+                      (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
   rs = ensure(ctx, ctx->b, need, s);
   if (rs != E2F_OK) return rs;
   Carver cb{(char*)ctx->b.p};
   double* org = cb.take<double>(3);
   double* R = cb.take<double>((size_t)n * nk);
-  float* T = cb.take<float>((size_t)nbmax * W);
-  double* part = cb.take<double>((size_t)G * W);
-  double* M64 = cb.take<double>((size_t)W);
+  double* part = cb.take<double>((size_t)G * WG);
+  double* G64 = cb.take<double>((size_t)WG);
   float* M32 = cb.take<float>((size_t)W);
   int32_t* order = cb.take<int32_t>((size_t)n);
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
   ctx->origins_host.assign(origin, origin + 3);
   E2F_HIP(hipMemcpyAsync(org, ctx->origins_host.data(), sizeof(double) * 3, hipMemcpyHostToDevice, s));
   E2F_TIMED("sh", launch_sh(t, pos, nullptr, org, nullptr, nullptr, 1, n, R, nullptr, s));
-  for (int b0 = 0; b0 < n; b0 += nbmax) {
-    const int nb = std::min(nbmax, n - b0);
-    E2F_TIMED("node_tp", launch_node_tp(t, R + (size_t)b0 * nk, nullptr, feat + (size_t)b0 * nk * C, nb, C, dh, T, s));
-    E2F_TIMED("aggregate", launch_moment(T, nb, W, part, b0 == 0, b0 + nb >= n, M64, M32, s));
-  }
+  E2F_TIMED("aggregate", launch_global_moment(t, R, feat, n, C, dh, part, G64, M32, s));
   E2F_TIMED("tile_plan", launch_iota(n, order, s));
   E2F_TIMED("recouple", launch_recouple(t, R, M32, true, order, n, C, dh, y, s));
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));

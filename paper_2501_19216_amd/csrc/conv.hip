@@ -1443,35 +1443,52 @@ __global__ void k_dense_alpha(const float* __restrict__ alpha, int n, int H, flo
   A[q] = i == j ? 0.0f : (alpha ? alpha[ij * H + h] : 1.0f);
 }
 
-// Column sums of a batch of T rows in float64 (uniform attention over the
-// whole graph): workgroup (column block, row group g) sums rows
-// g, g + G, ... of its 256 columns; the finish adds the G partials in order to
-// the running float64 moment and, on the last batch, rounds it to float32.
-// four columns per thread (W % 4 == 0), float4 loads; each column is summed
-// over the rows r = g, g + G, .. in order (deterministic)
-__global__ void k_moment_partial(const float* __restrict__ T, int rows, int64_t W, int G,
-                                 double* __restrict__ part) {
-  const int64_t c4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// Global moments of the uncoupled products (App. G with every pair weighted
+// alike): G[be][col] = sum_j R_be(p_j) h_j[col], col = q*C + c over the
+// (L+1)^2 C columns of the features.  One thread per column, the (L+1)^2
+// sums in fp64 registers over the atoms j = g, g + G, .. (in order) of group
+// g = blockIdx.y; R of each atom is read by the whole workgroup (uniform).
+template <int NK>
+__global__ __launch_bounds__(256) void k_global_G_partial(const double* __restrict__ R, const float* __restrict__ feat,
+                                                          int n, int cols, int G, double* __restrict__ part) {
+  const int col = blockIdx.x * blockDim.x + threadIdx.x;
   const int g = blockIdx.y;
-  if (4 * c4 >= W) return;
-  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
-#pragma unroll 4
-  for (int r = g; r < rows; r += G) {
-    const float4 v = *(const float4*)(T + (size_t)r * W + 4 * c4);
-    a0 += (double)v.x, a1 += (double)v.y, a2 += (double)v.z, a3 += (double)v.w;
+  const int cc = col < cols ? col : 0;  // columns past the end compute column 0, never stored
+  double acc[NK];
+#pragma unroll
+  for (int b = 0; b < NK; ++b) acc[b] = 0.0;
+  for (int j = g; j < n; j += G) {
+    const double hv = (double)feat[(size_t)j * cols + cc];
+    const double* Rj = R + (size_t)j * NK;
+#pragma unroll
+    for (int b = 0; b < NK; ++b) acc[b] += Rj[b] * hv;
   }
-  double* p = part + (size_t)g * W + 4 * c4;
-  p[0] = a0, p[1] = a1, p[2] = a2, p[3] = a3;
+  if (col < cols)
+#pragma unroll
+    for (int b = 0; b < NK; ++b) part[((size_t)g * NK + b) * cols + col] = acc[b];
 }
 
-__global__ void k_moment_finish(const double* __restrict__ part, int64_t W, int G, bool first, bool last,
-                                double* __restrict__ M64, float* __restrict__ M32) {
-  const int64_t col = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (col >= W) return;
-  double acc = first ? 0.0 : M64[col];
-  for (int g = 0; g < G; ++g) acc += part[(size_t)g * W + col];
-  M64[col] = acc;
-  if (last) M32[col] = (float)acc;
+// G64 = sum over the groups in order; then the j-side coupling of the one
+// global row: M[h][row][t] = sum over the row's entries of coef G64[be][q*C + c]
+// (c = h*dh + t, the head-major layout of an S row).
+__global__ void k_global_G_finish(const double* __restrict__ part, int64_t W, int G, double* __restrict__ G64) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= W) return;
+  double acc = 0.0;
+  for (int g = 0; g < G; ++g) acc += part[(size_t)g * W + x];
+  G64[x] = acc;
+}
+
+__global__ void k_global_couple(DevTables t, const double* __restrict__ G64, int C, int dh, float* __restrict__ M32) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= (int64_t)t.dimT * C) return;
+  const int row = (int)(x / C), c = (int)(x % C);
+  double acc = 0.0;
+  for (int e = t.ag_ptr[row]; e < t.ag_ptr[row + 1]; ++e) {
+    const int gi = t.ag_idx[e];
+    acc += (double)t.ag_coef[e] * G64[(size_t)(gi >> 6) * t.nk * C + (size_t)(gi & 63) * C + c];
+  }
+  M32[((size_t)(c / dh) * t.dimT + row) * dh + c % dh] = (float)acc;
 }
 
 // Per-degree attention weights alpha / D^f (Alg. 1), D = |r_i - r_j| in
@@ -1983,21 +2000,27 @@ hipError_t launch_dense_alpha(const float* alpha, int n, int H, float* A, hipStr
   return hipGetLastError();
 }
 
-int moment_groups(int rows, int64_t W) {
-  const int64_t colblocks = (W / 4 + 255) / 256;
-  int G = (int)std::max<int64_t>(1, std::min<int64_t>(rows, (4096 + colblocks - 1) / colblocks));
-  return std::min(G, 64);
+int global_groups(int n, int nk, int C) {
+  const int colblocks = (nk * C + 255) / 256;
+  return std::max(1, std::min(n, (2048 + colblocks - 1) / colblocks));
 }
 
-hipError_t launch_moment(const float* T, int rows, int64_t W, double* part, bool first, bool last, double* M64,
-                         float* M32, hipStream_t s) {
-  if (W % 4) return hipErrorInvalidValue;
-  const int G = moment_groups(rows, W);
-  const int64_t colblocks = (W + 255) / 256;
-  const int64_t colblocks4 = (W / 4 + 255) / 256;
-  if (colblocks > 0x7fffffff) return hipErrorInvalidValue;
-  if (rows > 0) k_moment_partial<<<dim3((unsigned)colblocks4, (unsigned)G), 256, 0, s>>>(T, rows, W, G, part);
-  k_moment_finish<<<(unsigned)colblocks, 256, 0, s>>>(part, W, rows > 0 ? G : 0, first, last, M64, M32);
+hipError_t launch_global_moment(const DevTables& t, const double* R, const float* feat, int n, int C, int dh,
+                                double* part, double* G64, float* M32, hipStream_t s) {
+  const int nk = t.nk, cols = nk * C, G = global_groups(n, nk, C);
+  const int64_t W = (int64_t)nk * cols;
+  const dim3 grid((unsigned)((cols + 255) / 256), (unsigned)G);
+  switch (t.L) {
+#define E2F_CASE(LL)                                                                                        \
+  case LL:                                                                                                  \
+    k_global_G_partial<(LL + 1) * (LL + 1)><<<grid, 256, 0, s>>>(R, feat, n, cols, G, part);                \
+    break;
+    E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
+#undef E2F_CASE
+    default: return hipErrorInvalidValue;
+  }
+  k_global_G_finish<<<(unsigned)((W + 255) / 256), 256, 0, s>>>(part, W, G, G64);
+  k_global_couple<<<(unsigned)(((int64_t)t.dimT * C + 255) / 256), 256, 0, s>>>(t, G64, C, dh, M32);
   return hipGetLastError();
 }
 

@@ -120,11 +120,12 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* 
 // accumulate: y += the product instead of y = (one writer per element)
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, bool shared_s, const int32_t* order,
                            int n, int C, int dh, float* y, hipStream_t s, bool accumulate = false);
-// Moment of T rows: part holds moment_groups(rows, W) * W doubles; M64 runs
-// over batches (first: start from 0), M32 = M64 rounded on the last batch.
-int moment_groups(int rows, int64_t W);
-hipError_t launch_moment(const float* T, int rows, int64_t W, double* part, bool first, bool last, double* M64,
-                         float* M32, hipStream_t s);
+// The global moment of every atom's uncoupled products, coupled into one S
+// row M32 [H][dimT][dh]: part holds global_groups(n, nk, C) * nk * nk * C
+// doubles, G64 nk * nk * C doubles; R [n][nk] float64 (one origin)
+int global_groups(int n, int nk, int C);
+hipError_t launch_global_moment(const DevTables& t, const double* R, const float* feat, int n, int C, int dh,
+                                double* part, double* G64, float* M32, hipStream_t s);
 
 // ---- attention weights [E][H] (H <= 64, 2 <= R <= kAttnMaxRbf radial functions)
 constexpr int kAttnMaxRbf = 32;
