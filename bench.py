@@ -226,6 +226,18 @@ def fig2_point(panel, k, L, n, steps, warmup, C=128, H=8):
             "edge_tp_ms": mse, "speedup_vs_edge_tp": mse / ms6, "atoms_per_s": n / ms6 * 1e3}
 
 
+def _cpu_model():
+    """The host CPU's model name (first 'model name' line of /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -450,7 +462,8 @@ def main():
         ref = oracle.layer(L, H, inp.pos, inp.feat, orp, oci, alpha_h, inp.path_w, inp.mix_w, rows=rows)
         dt = time.perf_counter() - t0
         cpu = dict(value=k / dt, unit="atoms/s", cores=cores, kind="oracle",
-                   sample="%d of %d receiver rows (evenly spaced), fp64 layer definition + mixing, %.1f s" % (k, n, dt))
+                   sample="%d of %d receiver rows (evenly spaced), fp64 layer definition + mixing, %.1f s" % (k, n, dt),
+                   cpu_model=_cpu_model())
         parity = dict(rows=k, max_rel_err=oracle.max_rel_err(out_step[rows], ref, L), graph_bit_exact=graph_equal)
 
     res = {
