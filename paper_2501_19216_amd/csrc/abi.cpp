@@ -75,9 +75,11 @@ struct e2f_ctx {
   rocblas_handle blas = nullptr;  // created on the first dense-graph forward
   // coupling schedules of the aggregation of uncoupled products, per (L, groups)
   struct Couple {
-    int k = 0;
+    int k = 0, ntab = 0;
     int* meta = nullptr;
     float* coef = nullptr;
+    int* pmeta = nullptr;  // packed entries and their coefficient table (ntab > 0)
+    float* tab = nullptr;
   };
   std::map<std::pair<int, int>, Couple> couple;
   // schedules of the backward's filter contraction, per (L, rows per pass)
@@ -199,6 +201,13 @@ e2f_status couple_of(e2f_ctx* ctx, int L, int groups, const e2f_ctx::Couple*& ou
     E2F_HIP(hipMalloc((void**)&c.coef, sizeof(float) * std::max<size_t>(cs.coef.size(), 1)));
     E2F_HIP(hipMemcpy(c.meta, cs.meta.data(), sizeof(int) * cs.meta.size(), hipMemcpyHostToDevice));
     E2F_HIP(hipMemcpy(c.coef, cs.coef.data(), sizeof(float) * cs.coef.size(), hipMemcpyHostToDevice));
+    if (!cs.tab.empty()) {
+      c.ntab = (int)cs.tab.size();
+      E2F_HIP(hipMalloc((void**)&c.pmeta, sizeof(int) * std::max<size_t>(cs.pmeta.size(), 1)));
+      E2F_HIP(hipMalloc((void**)&c.tab, sizeof(float) * cs.tab.size()));
+      E2F_HIP(hipMemcpy(c.pmeta, cs.pmeta.data(), sizeof(int) * cs.pmeta.size(), hipMemcpyHostToDevice));
+      E2F_HIP(hipMemcpy(c.tab, cs.tab.data(), sizeof(float) * cs.tab.size(), hipMemcpyHostToDevice));
+    }
     it = ctx->couple.emplace(key, c).first;
   }
   out = &it->second;
@@ -538,6 +547,8 @@ void e2f_destroy(e2f_ctx* ctx) {
     for (auto& kv : ctx->couple) {
       if (kv.second.meta) (void)hipFree(kv.second.meta);
       if (kv.second.coef) (void)hipFree(kv.second.coef);
+      if (kv.second.pmeta) (void)hipFree(kv.second.pmeta);
+      if (kv.second.tab) (void)hipFree(kv.second.tab);
     }
     for (auto& kv : ctx->geom) {
       if (kv.second.meta) (void)hipFree(kv.second.meta);
@@ -931,7 +942,8 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
     const int32_t* ord = order + q0;
     if (outer && !ynorm) {
       E2F_TIMED("aggregate", launch_outer_agg(t, Re, row_ptr, col_idx, alpha_hm, n_edges, feat, ord,
-                                              cpl->meta, cpl->coef, cpl->k, cgroups, nb, C, p->heads, S, s));
+                                              cpl->meta, cpl->coef, cpl->pmeta, cpl->tab, cpl->ntab, cpl->k,
+                                              cgroups, nb, C, p->heads, S, s));
       E2F_TIMED("recouple", launch_recouple(t, Rr, S, false, ord, nb, C, dh, y, s));
       continue;
     }
@@ -941,8 +953,8 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
       // the others add
       for (int f = 0; f <= L; ++f) {
         E2F_TIMED("aggregate", launch_outer_agg(t, Re, row_ptr, col_idx, alpha_hm + (size_t)f * p->heads * n_edges,
-                                                n_edges, feat, ord, cpl->meta, cpl->coef, cpl->k, cgroups, nb, C,
-                                                p->heads, S, s));
+                                                n_edges, feat, ord, cpl->meta, cpl->coef, cpl->pmeta, cpl->tab,
+                                                cpl->ntab, cpl->k, cgroups, nb, C, p->heads, S, s));
         DevTables tf = t;
         tf.rc_k = ctx->rcf_k[L][f];
         tf.rc_off = ctx->rcf_off[L][f];

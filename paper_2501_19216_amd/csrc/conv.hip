@@ -17,6 +17,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstdlib>
+#include <type_traits>
 #include <utility>
 
 #include "e2f_launch.h"
@@ -666,8 +667,9 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
                                                     const float* __restrict__ alpha_hm, int64_t n_edges,
                                                     const float* __restrict__ feat, const int32_t* __restrict__ order,
                                                     const int* __restrict__ cmeta, const float* __restrict__ ccoef,
-                                                    int ck, int cgroups, int work_floats, int n, int nrx, int rpw,
-                                                    int C, int H, float* __restrict__ S) {
+                                                    const int* __restrict__ pmeta, const float* __restrict__ ptab,
+                                                    int ntab, int ck, int cgroups, int work_floats, int n, int nrx,
+                                                    int rpw, int C, int H, float* __restrict__ S) {
   constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
   constexpr int EC = kOuterEdges;
   extern __shared__ float sm[];
@@ -679,8 +681,12 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
   int* jl = (int*)(sm + EC * AS);   // [EC]: sender of the edge (clamped past the chunk)
   float* G = sm;                    // [NK][GS], after the products (reuses the staging space)
   // the coupling schedule, staged once in LDS after the work space when
-  // work_floats > 0 (else read from global memory)
-  if (work_floats > 0) {
+  // work_floats > 0 (else read from global memory): packed entries and their
+  // coefficient table when ntab > 0, else entries and coefficients
+  if (work_floats > 0 && ntab > 0) {
+    for (int q = threadIdx.x; q < ck * cgroups; q += blockDim.x) ((int*)(sm + work_floats))[q] = pmeta[q];
+    for (int q = threadIdx.x; q < ntab; q += blockDim.x) sm[work_floats + ck * cgroups + q] = ptab[q];
+  } else if (work_floats > 0) {
     for (int q = threadIdx.x; q < ck * cgroups; q += blockDim.x) {
       ((int*)(sm + work_floats))[q] = cmeta[q];
       sm[work_floats + ck * cgroups + q] = ccoef[q];
@@ -821,7 +827,10 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
   // the sums (past ck: entry 0 with coefficient 0, never the last of a row);
   // one copy of the loop per memory holding the schedule, so that its reads
   // are plain LDS or global loads
-  auto couple = [&](const int* __restrict__ meta, const float* __restrict__ coef) {
+  // Packed entries (PK) hold a 9-bit row and the index of their coefficient
+  // in coef; otherwise coef runs beside meta and the row has 12 bits.
+  auto couple = [&](const int* __restrict__ meta, const float* __restrict__ coef, auto packed) {
+    constexpr bool PK = decltype(packed)::value;
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int k0 = 0; k0 < ck; k0 += 4) {
       int m[4];
@@ -831,7 +840,14 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
       for (int u = 0; u < 4; ++u) {
         const bool ok = k0 + u < ck;
         m[u] = ok ? meta[(k0 + u) * cgroups + g] : 0;
-        c[u] = ok ? coef[(k0 + u) * cgroups + g] : 0.0f;
+        if (!PK) c[u] = ok ? coef[(k0 + u) * cgroups + g] : 0.0f;
+      }
+      if (PK) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float cv = coef[(m[u] >> 21) & 1023];
+          c[u] = k0 + u < ck ? cv : 0.0f;
+        }
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) gv[u] = *(const float4*)(G + ((m[u] >> 6) & 63) * GS + (m[u] & 63) * dh + 4 * tq);
@@ -839,17 +855,19 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
       for (int u = 0; u < 4; ++u) {
         v.x += c[u] * gv[u].x, v.y += c[u] * gv[u].y, v.z += c[u] * gv[u].z, v.w += c[u] * gv[u].w;
         if (m[u] < 0) {
-          *(float4*)(Sr + ((m[u] >> 12) & 4095) * dh + 4 * tq) = v;
+          *(float4*)(Sr + ((m[u] >> 12) & (PK ? 511 : 4095)) * dh + 4 * tq) = v;
           v = make_float4(0.f, 0.f, 0.f, 0.f);
         }
       }
     }
   };
   if (g < cgroups) {
-    if (work_floats > 0)
-      couple((const int*)(sm + work_floats), sm + work_floats + ck * cgroups);
+    if (work_floats > 0 && ntab > 0)
+      couple((const int*)(sm + work_floats), sm + work_floats + ck * cgroups, std::true_type{});
+    else if (work_floats > 0)
+      couple((const int*)(sm + work_floats), sm + work_floats + ck * cgroups, std::false_type{});
     else
-      couple(cmeta, ccoef);
+      couple(cmeta, ccoef, std::false_type{});
   }
   }  // receivers of the workgroup
 }
@@ -1871,8 +1889,9 @@ bool outer_agg_supported(int L, int C, int H) {
 
 hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* row_ptr, const int32_t* col,
                             const float* alpha_hm, int64_t n_edges, const float* feat,
-                            const int32_t* order, const int* cmeta, const float* ccoef, int ck, int cgroups, int n,
-                            int C, int H, float* S, hipStream_t s) {
+                            const int32_t* order, const int* cmeta, const float* ccoef, const int* pmeta,
+                            const float* ptab, int ntab, int ck, int cgroups, int n, int C, int H, float* S,
+                            hipStream_t s) {
   if (n == 0) return hipSuccess;
   if (!outer_agg_supported(t.L, C, H) || cgroups != outer_agg_groups(t.L, C, H)) return hipErrorInvalidValue;
   const OuterShape o = outer_shape(t.L, C, H);
@@ -1883,8 +1902,17 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* 
     return v ? atoi(v) : 0;
   }();
   const int rpw = rpw_env > 0 ? rpw_env : 8;
-  const size_t sched_b = sizeof(float) * 2 * (size_t)ck * cgroups;
+  // the packed schedule (L <= 4) leaves room for three workgroups per CU at
+  // L = 4, C = 128, H = 8; E2F_OUTER_PACKED=0 stages the unpacked one (tuning)
+  static const bool packed_env = [] {
+    const char* v = getenv("E2F_OUTER_PACKED");
+    return !v || atoi(v) != 0;
+  }();
+  const bool packed = packed_env && ntab > 0 && pmeta && ptab;
+  const size_t sched_b = packed ? sizeof(float) * ((size_t)ck * cgroups + ntab)
+                                : sizeof(float) * 2 * (size_t)ck * cgroups;
   const bool sched_lds = o.lds + sched_b <= 80 * 1024;
+  const int ntab_k = packed && sched_lds ? ntab : 0;
   const int work_floats = sched_lds ? (int)(o.lds / sizeof(float)) : 0;
   const size_t lds = o.lds + (sched_lds ? sched_b : 0);
   const int nrx = (n + kXcds - 1) / kXcds;
@@ -1901,8 +1929,9 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* 
     if (hipError_t e = allow_lds(k_outer_agg<LL, NTWM, LB>, lds); e != hipSuccess) return e;                \
     k_outer_agg<LL, NTWM, LB><<<(unsigned)blocks, 64 * o.nw, lds, s>>>(t, Re, row_ptr, col,                 \
                                                                       alpha_hm, n_edges, feat, order, cmeta, \
-                                                                      ccoef, ck, cgroups, work_floats, n,    \
-                                                                      nrx, rpw, C, H, S);                    \
+                                                                      ccoef, pmeta, ptab, ntab_k, ck,        \
+                                                                      cgroups, work_floats, n, nrx, rpw, C,  \
+                                                                      H, S);                                 \
     break;
 #define E2F_CASES(LL) E2F_CASE(LL, 4, 512) E2F_CASE(LL, 4, 1024)
     E2F_CASES(0) E2F_CASES(1) E2F_CASES(2) E2F_CASES(3) E2F_CASES(4) E2F_CASES(5) E2F_CASES(6)

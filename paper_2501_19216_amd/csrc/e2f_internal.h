@@ -108,6 +108,12 @@ struct CoupleSchedule {
   int groups = 0, k = 0;
   std::vector<int> meta;
   std::vector<float> coef;
+  // the same entries packed for LDS when dimT <= 512 and the coefficients take
+  // at most 1024 distinct values (L <= 4): pmeta = gidx | row << 12 (9 bits) |
+  // coefficient index << 21 (10 bits) | last (bit 31), tab = the coefficients
+  // (empty otherwise)
+  std::vector<int> pmeta;
+  std::vector<float> tab;
 };
 CoupleSchedule couple_schedule(const LayerTables& t, int groups);
 

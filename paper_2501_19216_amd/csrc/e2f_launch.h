@@ -111,12 +111,14 @@ hipError_t launch_alpha_head_major(const float* alpha, int64_t n_edges, int H, f
 // alpha_ij R(p_j) (x) h_j and coupling per receiver (no T): Re [E][nk] float32
 // (launch_edge_R), alpha_hm [H][n_edges] or NULL (ones)
 // with the coupling schedule of couple_schedule(tables, outer_agg_groups(L, C, H))
+// (its packed form pmeta/ptab, ntab > 0, is staged in LDS when it exists)
 bool outer_agg_supported(int L, int C, int H);
 int outer_agg_groups(int L, int C, int H);
 hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* row_ptr, const int32_t* col,
                             const float* alpha_hm, int64_t n_edges, const float* feat,
-                            const int32_t* order, const int* cmeta, const float* ccoef, int ck, int cgroups, int n,
-                            int C, int H, float* S, hipStream_t s);
+                            const int32_t* order, const int* cmeta, const float* ccoef, const int* pmeta,
+                            const float* ptab, int ntab, int ck, int cgroups, int n, int C, int H, float* S,
+                            hipStream_t s);
 // accumulate: y += the product instead of y = (one writer per element)
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, bool shared_s, const int32_t* order,
                            int n, int C, int dh, float* y, hipStream_t s, bool accumulate = false);

@@ -459,6 +459,21 @@ CoupleSchedule couple_schedule(const LayerTables& t, int groups) {
       }
     }
   }
+  if (t.dimT <= 512) {
+    std::map<float, int> idx;  // exact values (padding entries carry 0.0f)
+    cs.pmeta.resize(cs.meta.size());
+    for (size_t q = 0; q < cs.meta.size(); ++q) {
+      auto it = idx.emplace(cs.coef[q], (int)idx.size()).first;
+      const int m = cs.meta[q];
+      cs.pmeta[q] = (m & 0xfff) | (((m >> 12) & 511) << 12) | (it->second << 21) | (m & (int)0x80000000u);
+    }
+    if (idx.size() > 1024) {
+      cs.pmeta.clear();
+    } else {
+      cs.tab.resize(idx.size());
+      for (const auto& kv : idx) cs.tab[kv.second] = kv.first;
+    }
+  }
   return cs;
 }
 
