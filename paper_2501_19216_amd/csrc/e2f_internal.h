@@ -28,9 +28,10 @@ double wigner6j(int j1, int j2, int j3, int j4, int j5, int j6);
 // the caller's path weights change.
 // Thread count of the schedules that build per-node matrices in LDS.
 constexpr int kSchedThreads = 256;
-// Rows of T per chunk of the recouple's per-node matrix (fewer at high L so
-// that the LDS tile leaves room for two workgroups per CU).
-constexpr int rc_rows(int nk) { return nk > 25 ? 128 : 256; }
+// Rows of T per chunk of the recouple's per-node matrix: 192 at L <= 4 (a
+// 37 KB tile, four workgroups per CU: 1.18 vs 1.20 ms with 256 rows and three),
+// 128 above (two workgroups per CU).
+constexpr int rc_rows(int nk) { return nk > 25 ? 128 : 192; }
 // Row stride (floats) of the recouple's per-node matrix tile in LDS: the
 // 16*ceil(nk/16) used columns padded to 16 mod 32, so the MFMA operand reads
 // of 4 rows x 16 columns fall in distinct banks.
