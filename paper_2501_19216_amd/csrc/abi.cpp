@@ -927,10 +927,10 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
     E2F_TIMED("alpha_hm", launch_alpha_head_major(alpha, n_edges, p->heads, alpha_hm, s));
   }
   E2F_TIMED("tile_plan", launch_pairs(flags, pidx, count, n, pair_node, pair_tile, s));
-  E2F_TIMED("tile_plan", launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
+  if (!outer) E2F_TIMED("tile_plan", launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
   E2F_TIMED("sh", launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, Rpf, s));
   E2F_TIMED("sh", launch_sh(t, pos, nullptr, origins, nullptr, tile_of, tp.ncell, n, Rr, nullptr, s));
-  if (outer) E2F_TIMED("sh", launch_edge_R(col_pair, Rpf, n_edges, nk, Re, s));
+  if (outer) E2F_TIMED("sh", launch_edge_R(row_ptr, col_idx, tile_of, pidx, n, Rpf, nk, Re, s));
   const int dh = C / p->heads;
   const int cgroups = outer ? outer_agg_groups(L, C, p->heads) : 0;
   const e2f_ctx::Couple* cpl = nullptr;

@@ -1675,23 +1675,24 @@ hipError_t launch_pairs(const int32_t* flags, const int32_t* pidx, int64_t count
   return hipGetLastError();
 }
 
-// Re[e][k] = Rp[col_pair[e]][k]: the harmonics of each edge's sender under
+// Re[e][k] = Rp[pair of e][k]: the harmonics of each edge's sender under
 // its receiver's tile origin, in edge order (the aggregation's staging then
-// reads one contiguous block per chunk, addressed by the edge alone)
-__global__ void k_edge_R(const int32_t* __restrict__ col_pair, const float* __restrict__ Rp, int64_t n_edges,
-                         int nk, float* __restrict__ Re) {
-  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (x >= n_edges * nk) return;
-  const int64_t e = x / nk;
-  Re[x] = Rp[(size_t)col_pair[e] * nk + (int)(x - e * nk)];
+// reads one contiguous block per chunk, addressed by the edge alone).  One
+// workgroup per receiver i: the pair of its edge to j is pidx[tile_of[i] * n + j].
+__global__ void k_edge_R(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ col,
+                         const int32_t* __restrict__ tile_of, const int32_t* __restrict__ pidx, int n,
+                         const float* __restrict__ Rp, int nk, float* __restrict__ Re) {
+  const int i = blockIdx.x;
+  const int64_t base = (int64_t)tile_of[i] * n, e0 = row_ptr[i], cnt = (row_ptr[i + 1] - e0) * nk;
+  for (int64_t q = threadIdx.x; q < cnt; q += blockDim.x) {
+    const int64_t e = e0 + q / nk;
+    Re[e0 * nk + q] = Rp[(size_t)pidx[base + col[e]] * nk + (int)(q % nk)];
+  }
 }
 
-hipError_t launch_edge_R(const int32_t* col_pair, const float* Rp, int64_t n_edges, int nk, float* Re,
-                         hipStream_t s) {
-  if (n_edges == 0) return hipSuccess;
-  const int64_t blocks = (n_edges * nk + 255) / 256;
-  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  k_edge_R<<<(unsigned)blocks, 256, 0, s>>>(col_pair, Rp, n_edges, nk, Re);
+hipError_t launch_edge_R(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of,
+                         const int32_t* pidx, int n, const float* Rp, int nk, float* Re, hipStream_t s) {
+  if (n > 0) k_edge_R<<<(unsigned)n, 256, 0, s>>>(row_ptr, col_idx, tile_of, pidx, n, Rp, nk, Re);
   return hipGetLastError();
 }
 

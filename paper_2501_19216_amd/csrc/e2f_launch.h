@@ -55,9 +55,9 @@ size_t scan_tmp_bytes(int64_t count);
 hipError_t launch_scan_i32(const int32_t* in, int32_t* out, int64_t count, void* tmp, size_t tmp_bytes, hipStream_t s);
 hipError_t launch_pairs(const int32_t* flags, const int32_t* pidx, int64_t count, int n, int32_t* pair_node,
                         int32_t* pair_tile, hipStream_t s);
-// Re [E][nk] float32: Rp [pairs][nk] of each edge's pair, in edge order
-hipError_t launch_edge_R(const int32_t* col_pair, const float* Rp, int64_t n_edges, int nk, float* Re,
-                         hipStream_t s);
+// Re [E][nk] float32: Rp [pairs][nk] of each edge's pair (pidx[tile_of[i] * n + j]), in edge order
+hipError_t launch_edge_R(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of,
+                         const int32_t* pidx, int n, const float* Rp, int nk, float* Re, hipStream_t s);
 hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of,
                            const int32_t* pidx, int n, int32_t* col_pair, hipStream_t s);
 
