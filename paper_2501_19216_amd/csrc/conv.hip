@@ -113,19 +113,25 @@ __global__ void k_tile_keys(const float* __restrict__ pos, const int32_t* __rest
   tile_of[i] = (gid ? gid[i] : 0) * g.ncell + cell;
 }
 
-__global__ void k_pair_flags(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ col,
-                             const int32_t* __restrict__ tile_of, int n, int32_t* __restrict__ flags,
-                             int32_t* __restrict__ max_degree) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  int deg = 0;
-  if (i < n) {
-    deg = (int)(row_ptr[i + 1] - row_ptr[i]);
-    const int64_t base = (int64_t)tile_of[i] * n;
-    for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) flags[base + col[e]] = 1;
+// 64 receivers per workgroup of four waves: wave 0 takes the largest degree
+// of the 64 (one atomic per workgroup); wave w walks the edges of receivers
+// w, w + 4, ... with its lanes.
+__global__ __launch_bounds__(256) void k_pair_flags(const int64_t* __restrict__ row_ptr,
+                                                    const int32_t* __restrict__ col,
+                                                    const int32_t* __restrict__ tile_of, int n,
+                                                    int32_t* __restrict__ flags, int32_t* __restrict__ max_degree) {
+  const int i0 = blockIdx.x * 64, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (wave == 0) {
+    const int i = i0 + lane;
+    int deg = i < n ? (int)(row_ptr[i + 1] - row_ptr[i]) : 0;
+    for (int o = 32; o > 0; o >>= 1) deg = max(deg, __shfl_xor(deg, o));
+    if (lane == 0) atomicMax(max_degree, deg);
   }
-  // largest degree: wave maximum, one atomic per wave
-  for (int o = 32; o > 0; o >>= 1) deg = max(deg, __shfl_xor(deg, o));
-  if ((threadIdx.x & 63) == 0) atomicMax(max_degree, deg);
+  for (int r = wave; r < 64 && i0 + r < n; r += 4) {
+    const int i = i0 + r;
+    const int64_t base = (int64_t)tile_of[i] * n, e1 = row_ptr[i + 1];
+    for (int64_t e = row_ptr[i] + lane; e < e1; e += 64) flags[base + col[e]] = 1;
+  }
 }
 
 __global__ void k_pairs(const int32_t* __restrict__ flags, const int32_t* __restrict__ pidx, int64_t count, int n,
@@ -1652,7 +1658,7 @@ hipError_t launch_pair_flags(const int64_t* row_ptr, const int32_t* col_idx, con
                              int32_t* flags, int32_t* max_degree, hipStream_t s) {
   hipError_t e = hipMemsetAsync(max_degree, 0, sizeof(int32_t), s);
   if (e != hipSuccess) return e;
-  if (n > 0) k_pair_flags<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, col_idx, tile_of, n, flags, max_degree);
+  if (n > 0) k_pair_flags<<<(n + 63) / 64, 256, 0, s>>>(row_ptr, col_idx, tile_of, n, flags, max_degree);
   return hipGetLastError();
 }
 
