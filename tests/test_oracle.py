@@ -696,3 +696,55 @@ def test_row_subset_and_mixing():
     for l in range(L + 1):
         s = slice(l * l, (l + 1) ** 2)
         assert np.allclose(out[:, s, :], np.einsum("pc,nmc->nmp", W[l].astype(np.float64), y[:, s, :]), atol=1e-13)
+
+
+def test_mixing_closed_forms():
+    # App. F: the self-mix is one C x C matrix per output degree o, applied to
+    # the channels of every m of that degree, W stored [o][c_out][c_in].
+    L, C, n = 3, 5, 4
+    rng = np.random.default_rng(77)
+    y = rng.standard_normal((n, (L + 1) ** 2, C))
+    # W^(o) = (o + 1) I: each degree's rows are scaled by their own factor,
+    # which fixes the assignment of the blocks of W to the degrees
+    W = np.zeros((L + 1, C, C), np.float32)
+    for l in range(L + 1):
+        W[l] = (l + 1) * np.eye(C, dtype=np.float32)
+    out = o.mix(L, y, W)
+    for l in range(L + 1):
+        s = slice(l * l, (l + 1) ** 2)
+        assert np.array_equal(out[:, s, :], (l + 1) * y[:, s, :])
+    # a single entry W^(o)[1][0] = 1: output channel 1 of degree o receives
+    # input channel 0 and nothing else is written, which fixes the orientation
+    # (row = output channel, column = input channel)
+    for l in range(L + 1):
+        W = np.zeros((L + 1, C, C), np.float32)
+        W[l, 1, 0] = 1.0
+        out = o.mix(L, y, W)
+        s = slice(l * l, (l + 1) ** 2)
+        want = np.zeros_like(y)
+        want[:, s, 1] = y[:, s, 0]
+        assert np.array_equal(out, want)
+    # a cyclic channel shift on degree 2 only: out[c'] = y[(c' + 1) % C]
+    W = np.zeros((L + 1, C, C), np.float32)
+    for cp in range(C):
+        W[2, cp, (cp + 1) % C] = 1.0
+    out = o.mix(L, y, W)
+    assert np.array_equal(out[:, 4:9, :], np.roll(y[:, 4:9, :], -1, axis=2))
+    assert np.all(out[:, :4, :] == 0) and np.all(out[:, 9:, :] == 0)
+
+
+def test_global_moment_equals_definition_larger():
+    # App. G at a size where a dropped or misindexed moment term cannot hide:
+    # 40 atoms, every pair and the self term, against the definition
+    L, C, n = 3, 3, 40
+    rng = np.random.default_rng(91)
+    pos = (rng.uniform(-4.0, 4.0, size=(n, 3)) * 65536.0).round() / 65536.0
+    pos = pos.astype(np.float32)
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    w = rng.uniform(0.5, 1.5, size=(L + 1) ** 3)
+    rp = np.arange(n + 1, dtype=np.int64) * n
+    ci = np.tile(np.arange(n, dtype=np.int32), n)
+    y1 = o.conv_edge(L, 1, pos, feat, rp, ci, np.ones((n * n, 1), np.float32), w)
+    origin = np.array([0.3, -0.2, 0.1])
+    y2 = o.conv_global(L, pos, feat, w, origin)
+    assert np.max(np.abs(y1 - y2)) <= 1e-11 * np.max(np.abs(y1))
