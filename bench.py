@@ -3,17 +3,20 @@
 
 One step = the whole hot path over one synthetic input already resident in
 HBM: the radius graph (CSR) followed by the Wigner-6j convolution forward
-(tile plan, solid harmonics, j-side node products, CSR attention-weighted
-aggregation, i-side 6j recoupling, per-irrep fp32 channel mixing).
+(device-side tile plan, solid harmonics, aggregation of the neighbours'
+uncoupled products with their CG coupling, i-side 6j recoupling, per-irrep
+fp32 channel mixing), on the 20,000-atom protein-scale workload (L = 4,
+C = 128, 8 heads).
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu] [--no-configs]
 
 Prints ONE JSON line.  Besides the step throughput it reports the forward
 alone (atoms/s, edges/s), the per-edge tensor-product baseline on the same
 inputs and GPU, the per-kernel times (HIP events on the launch stream,
-recorded during the timed steps), the roofline of the dominant kernel, the
-fp64 oracle timed on the host cores on a bounded row sample, and the parity
-of the timed output on those rows.
+recorded during the timed steps), the roofline of the dominant kernel and of
+the whole forward, every workload's forward, baseline, speedup and sampled
+parity (`configs`), the fp64 oracle timed on the host cores on a bounded row
+sample, and the parity of the timed output on those rows.
 """
 from __future__ import annotations
 
@@ -77,78 +80,137 @@ def central_crop(pos, side):
     return np.nonzero(keep)[0]
 
 
-def sweep_one(name, steps, warmup):
-    """6j forward and edge-TP baseline on one workload (the 200k-atom system's
-    baseline runs on its central 58.48 A crop, with the 6j path timed there too)."""
+def alg_counts(e2f, L, C, H, n, E):
+    """Algorithmic work of the forward's kernels (per launch over the whole
+    graph), counted from the real-basis tables: the aggregation as the
+    factorised layer's a3 (dimT multiply-adds per edge and channel) plus the
+    j-side coupling of every receiver (a2); the recouple (a4); the mixing
+    (a5); and the compulsory bytes each kernel moves."""
+    cnt = layer_counts(L)
+    dimT, nk = cnt["dimT"], (L + 1) ** 2
+    cpl = coupling_entries(e2f, L)
+    mp = 16 * ((nk + 15) // 16)  # components of R per MFMA tile column, padded to 16
+    agg = dict(flops=2.0 * E * dimT * C + 2.0 * n * cpl * C,
+               bytes=4.0 * n * nk * C + 4.0 * E * nk + 4.0 * E * H + 4.0 * E + 8.0 * (n + 1) + 4.0 * n * dimT * C,
+               issued_flops=2.0 * E * mp * nk * C + 2.0 * n * cpl * C)
+    rec = dict(flops=2.0 * n * cnt["q_slots"] * C, bytes=4.0 * n * dimT * C + 4.0 * n * nk * C + 8.0 * n * nk)
+    mix = dict(flops=2.0 * n * nk * C * C, bytes=8.0 * n * nk * C + 4.0 * (L + 1) * C * C)
+    # the whole forward, fused: inputs and output once (h, positions, CSR,
+    # attention weights, mixing weights, out), all the arithmetic above
+    fwd = dict(flops=agg["flops"] + rec["flops"] + mix["flops"],
+               bytes=4.0 * n * nk * C * 2 + 12.0 * n + 4.0 * E + 8.0 * (n + 1) + 4.0 * E * H + 4.0 * (L + 1) * C * C)
+    return dict(aggregate=agg, recouple=rec, mix=mix, forward=fwd, dimT=dimT, coupling_entries=cpl,
+                recouple_entries=cnt["q_slots"])
+
+
+def roof_of(bytes_, flops, t_ms, peak_tf):
+    """Roofline position of one launch: the binding resource is the one
+    whose lower-bound time is larger."""
+    t_b, t_f = bytes_ / (HBM_PEAK_GBS * 1e9), flops / (peak_tf * 1e12)
+    if t_b >= t_f:
+        a = bytes_ / (t_ms * 1e-3) / 1e9
+        return dict(bound="hbm", achieved=a, peak=HBM_PEAK_GBS, unit="GB/s", frac=a / HBM_PEAK_GBS)
+    a = flops / (t_ms * 1e-3) / 1e12
+    return dict(bound="mfma", achieved=a, peak=peak_tf, unit="TFLOP/s", frac=a / peak_tf)
+
+
+def forward_floor(counts, t_ms):
+    """T_roof / T_meas of the whole forward against the fused floor."""
+    f = counts["forward"]
+    t_roof = max(f["bytes"] / (HBM_PEAK_GBS * 1e9), f["flops"] / (FP32_MFMA_PEAK_TFS * 1e12)) * 1e3
+    return dict(t_roof_ms=t_roof, t_meas_ms=t_ms, frac=t_roof / t_ms, flops=f["flops"], bytes=f["bytes"])
+
+
+def time_gpu(fn, steps, warmup):
+    """Mean wall time per call of `steps` calls after `warmup`, bracketed by
+    device synchronisation."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+def sweep_one(name, steps, warmup, crop=False, parity_rows=None, quiet=False):
+    """One workload: the 6j forward and the edge-TP baseline (fp32 mixing),
+    their speedup, and parity of both on sampled rows against the oracle.
+    crop: the central 58.48 A sub-cube of the workload (the 200,000-atom
+    system's baseline runs there).  Attention weights come from the seeded
+    generator on the device for every edge; the sampled rows' weights are
+    replaced by the host generator's, which the oracle reads, so both sides
+    see the same inputs on those rows."""
     import torch
     import e2f_synth as syn
+    import oracle
     import paper_2501_19216_amd as e2f
 
     wl = syn.WORKLOADS[name]
+    if parity_rows is None:
+        parity_rows = 256 if wl.lmax < 6 else 128
     inp = syn.make_inputs(wl)
-    print("[sweep] %s: %d atoms generated" % (name, inp.pos.shape[0]), file=sys.stderr, flush=True)
     dev = torch.device("cuda:0")
+    pos_h, feat_h, gid_h, spc = inp.pos, inp.feat, inp.graph_id, inp.species
+    if crop:
+        keep = central_crop(inp.pos, syn._cube_side(20000))
+        pos_h, feat_h, spc = np.ascontiguousarray(pos_h[keep]), np.ascontiguousarray(feat_h[keep]), spc[keep]
+        gid_h = None if gid_h is None else gid_h[keep]
+    if not quiet:
+        print("[configs] %s%s: %d atoms generated" % (name, " crop" if crop else "", pos_h.shape[0]),
+              file=sys.stderr, flush=True)
     ctx = e2f.e2f_create(wl.lmax, 0)
-
-    def setup(idx):
-        pos_h = inp.pos if idx is None else np.ascontiguousarray(inp.pos[idx])
-        feat_h = inp.feat if idx is None else np.ascontiguousarray(inp.feat[idx])
-        gid_h = inp.graph_id if (inp.graph_id is None or idx is None) else inp.graph_id[idx]
-        spc = inp.species if idx is None else inp.species[idx]
-        pos = torch.from_numpy(pos_h).to(dev)
-        gid = None if gid_h is None else torch.from_numpy(np.ascontiguousarray(gid_h)).to(dev)
-        rp, ci = e2f.e2f_neighbor_list(ctx, pos, wl.cutoff, gid)
-        al = syn.attention_weights(pos_h, spc, rp.cpu().numpy(), ci.cpu().numpy(), wl.heads, wl.cutoff, wl.species,
-                                   wl.seed)
-        print("[sweep] %s: graph and attention weights of %d atoms ready" % (name, pos_h.shape[0]), file=sys.stderr,
-              flush=True)
-        return pos, torch.from_numpy(feat_h).to(dev), gid, rp, ci, torch.from_numpy(al).to(dev)
-
+    pos = torch.from_numpy(pos_h).to(dev)
+    feat = torch.from_numpy(feat_h).to(dev)
+    gid = None if gid_h is None else torch.from_numpy(np.ascontiguousarray(gid_h)).to(dev)
+    rp, ci = e2f.e2f_neighbor_list(ctx, pos, wl.cutoff, gid)
+    rph, cih = rp.cpu().numpy(), ci.cpu().numpy()
+    n, E = pos_h.shape[0], len(cih)
+    al = syn.attention_weights_device(pos_h, spc, rph, cih, wl.heads, wl.cutoff, wl.species, wl.seed, dev)
+    rows = np.arange(n, dtype=np.int32) if n <= parity_rows else \
+        np.sort(np.random.default_rng(11).choice(n, parity_rows, replace=False)).astype(np.int32)
+    # the sampled rows' weights from the host generator (each row's weights
+    # depend on that row alone): a CSR of those rows, receiver k at node k,
+    # sender j at node len(rows) + j
+    sub_rp = np.concatenate([[0], np.cumsum(rph[rows + 1] - rph[rows])]).astype(np.int64)
+    sub_e = np.concatenate([np.arange(rph[r], rph[r + 1]) for r in rows]).astype(np.int64)
+    al_h = np.zeros((E, wl.heads), dtype=np.float32)
+    if len(sub_e):
+        rp_rows = np.concatenate([sub_rp, np.full(n, sub_rp[-1])]).astype(np.int64)
+        al_rows = syn.attention_weights(np.concatenate([pos_h[rows], pos_h]), np.concatenate([spc[rows], spc]),
+                                        rp_rows, (cih[sub_e] + len(rows)).astype(np.int32), wl.heads, wl.cutoff,
+                                        wl.species, wl.seed)
+        al_h[sub_e] = al_rows
+        al[torch.from_numpy(sub_e).to(dev)] = torch.from_numpy(al_rows).to(dev)
     mix_w = torch.from_numpy(inp.mix_w).to(dev)
-
-    def time_fn(fn, k):
-        for _ in range(warmup):
-            fn()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(k):
-            fn()
-        torch.cuda.synchronize()
-        return (time.perf_counter() - t0) * 1e3 / k
-
-    res = {"workload": name, "lmax": wl.lmax, "channels": wl.channels, "heads": wl.heads, "cutoff": wl.cutoff}
-    pos, feat, gid, rp, ci, al = setup(None)
-    out = torch.empty_like(feat)
-    n, E = feat.shape[0], ci.numel()
+    out6 = torch.empty_like(feat)
+    oute = torch.empty_like(feat)
+    e2f.e2f_wigner6j_prepare(ctx, wl.lmax, wl.channels, wl.heads, wl.cutoff, mix_w=mix_w)
     k6 = max(2, steps // 4) if n > 50000 else steps
     f6 = lambda: e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, rp, ci, al, wl.lmax, wl.heads, wl.cutoff,
-                                               mix_w=mix_w, graph_id=gid, out=out)
-    for _ in range(warmup):  # warm-up outside the profiled window (first call allocates)
-        f6()
+                                               mix_w=mix_w, graph_id=gid, out=out6)
+    ms6 = time_gpu(f6, k6, warmup)
+    res = {"workload": name + ("_crop" if crop else ""), "atoms": n, "edges": E, "lmax": wl.lmax,
+           "channels": wl.channels, "heads": wl.heads, "cutoff": wl.cutoff, "fwd_ms": ms6,
+           "atoms_per_s": n / ms6 * 1e3, "edges_per_s": E / ms6 * 1e3}
+    run_edge = n <= 50000
+    if run_edge:
+        fe = lambda: e2f.e2f_edge_tp_conv_forward(ctx, pos, feat, rp, ci, al, wl.lmax, wl.heads, wl.cutoff,
+                                                  mix_w=mix_w, out=oute)
+        mse = time_gpu(fe, max(2, steps // 2) if wl.lmax >= 6 else steps, warmup)
+        res.update(edge_tp_ms=mse, speedup_vs_edge_tp=mse / ms6)
     torch.cuda.synchronize()
-    e2f.e2f_profile(ctx, True)
-    ms6 = time_fn(f6, k6)
-    prof = e2f.e2f_profile_read(ctx)
-    e2f.e2f_profile(ctx, False)
-    pairs, tiles = e2f.e2f_last_plan(ctx)
-    res.update(atoms=n, edges=E, pairs=pairs, tiles=tiles, fwd_ms=ms6, atoms_per_s=n / ms6 * 1e3,
-               edges_per_s=E / ms6 * 1e3,
-               kernels_ms={k: v[1] / (warmup + k6) for k, v in prof.items()})
-    if n > 50000:
-        idx = central_crop(inp.pos, syn._cube_side(20000))
-        del out
-        pos, feat, gid, rp, ci, al = setup(idx)
-        out = torch.empty_like(feat)
-        res["crop"] = {"atoms": feat.shape[0], "edges": ci.numel()}
-        res["crop"]["fwd_ms"] = time_fn(lambda: e2f.e2f_wigner6j_conv_forward(
-            ctx, pos, feat, rp, ci, al, wl.lmax, wl.heads, wl.cutoff, mix_w=mix_w, graph_id=gid, out=out), steps)
-        base = res["crop"]
-    else:
-        base = res
-    oute = torch.empty_like(feat)
-    base["edge_tp_ms"] = time_fn(lambda: e2f.e2f_edge_tp_conv_forward(
-        ctx, pos, feat, rp, ci, al, wl.lmax, wl.heads, wl.cutoff, mix_w=mix_w, out=oute), steps)
-    base["speedup_vs_edge_tp"] = base["edge_tp_ms"] / base["fwd_ms"]
+    t0 = time.perf_counter()
+    ref = oracle.layer(wl.lmax, wl.heads, pos_h, feat_h, rph, cih, al_h, inp.path_w, inp.mix_w, rows=rows)
+    res["parity"] = {"rows": int(len(rows)), "oracle_s": time.perf_counter() - t0,
+                     "max_rel_err": oracle.max_rel_err(out6.cpu().numpy()[rows], ref, wl.lmax)}
+    if run_edge:
+        res["parity"]["edge_tp_max_rel_err"] = oracle.max_rel_err(oute.cpu().numpy()[rows], ref, wl.lmax)
+    if n <= 50000:
+        orp, oci = oracle.neighbor_list(pos_h, wl.cutoff, gid_h)
+        res["parity"]["graph_bit_exact"] = bool(np.array_equal(orp, rph) and np.array_equal(oci, cih))
     ctx.close()
     return res
 
@@ -212,17 +274,15 @@ def fig2_point(panel, k, L, n, steps, warmup, C=128, H=8):
 
     if k > 0:
         ms6 = timed(lambda: e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, rp, ci, alpha, L, H, reach, out=out))
-        pairs, tiles = e2f.e2f_last_plan(ctx)
     else:
         dense = torch.zeros(n, n, H, device=dev)
         dense[torch.from_numpy(np.repeat(np.arange(n), n - 1)).to(dev), ci.long()] = alpha
         ms6 = timed(lambda: e2f.e2f_wigner6j_conv_forward_dense(ctx, pos, feat, dense, L, H, reach, out=out))
-        pairs, tiles = n, 1
         del dense
     mse = timed(lambda: e2f.e2f_edge_tp_conv_forward(ctx, pos, feat, rp, ci, alpha, L, H, reach, out=out))
     ctx.close()
     return {"panel": panel, "graph": "knn" if k > 0 else "dense", "k": k, "lmax": L, "atoms": n, "edges": int(len(cih)), "channels": C,
-            "heads": H, "reach": reach, "tiles": tiles, "pairs": pairs, "knn_ms": ms_knn, "fwd_ms": ms6,
+            "heads": H, "reach": reach, "knn_ms": ms_knn, "fwd_ms": ms6,
             "edge_tp_ms": mse, "speedup_vs_edge_tp": mse / ms6, "atoms_per_s": n / ms6 * 1e3}
 
 
@@ -238,6 +298,13 @@ def _cpu_model():
     return None
 
 
+# Every workload of the benchmark, reported in the `configs` field: the five
+# synthetic systems, and the central crop of the 200,000-atom one (where its
+# per-edge baseline runs).
+CONFIGS = [("cluster32_L2", False), ("molecules256x30_L3", False), ("water2000_L4", False),
+           ("protein20k_L4", False), ("stress200k_L6", False), ("stress200k_L6", True)]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -245,8 +312,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="protein20k_L4")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-configs", action="store_true", help="skip the per-workload table")
     ap.add_argument("--cpu-rows", type=int, default=6144)
-    ap.add_argument("--copy-calib", action="store_true", help="also run a 1 GiB device copy (counter calibration)")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="also run a 1 GiB device copy and a 1 GiB device sum (counter calibration)")
     ap.add_argument("--sweep", action="store_true",
                     help="instead: one JSON line per workload (6j forward and edge-TP baseline times and speedup)")
     ap.add_argument("--sweep-workloads", default="", help="comma-separated subset of the sweep (default: all)")
@@ -272,9 +341,11 @@ def main():
         return
 
     if args.sweep:
-        names = [w for w in args.sweep_workloads.split(",") if w] or list(syn.WORKLOADS)
-        for name in names:
-            print(json.dumps(sweep_one(name, args.steps, args.warmup)), flush=True)
+        names = [w for w in args.sweep_workloads.split(",") if w]
+        for name, crop in CONFIGS:
+            if names and name not in names:
+                continue
+            print(json.dumps(sweep_one(name, args.steps, args.warmup, crop)), flush=True)
         return
 
     wl = syn.WORKLOADS[args.workload]
@@ -297,15 +368,19 @@ def main():
     rp_buf = torch.empty(n + 1, dtype=torch.int64, device=dev)
     col_buf = torch.empty(E, dtype=torch.int32, device=dev)
     out = torch.empty_like(feat)
+    # the caller-owned workspace of the one-pass forward, allocated once
+    ws_bytes = e2f.e2f_wigner6j_workspace_size(ctx, n, E, L, C, H, wl.cutoff, mix_w=mix_w)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    e2f.e2f_wigner6j_prepare(ctx, L, C, H, wl.cutoff, mix_w=mix_w)
 
     def step():
         rp, ci = e2f.e2f_neighbor_list(ctx, pos, wl.cutoff, gid, rp_buf, col_buf)
         e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, rp, ci, alpha, L, H, wl.cutoff, mix_w=mix_w, graph_id=gid,
-                                      out=out)
+                                      out=out, workspace=ws)
 
     def fwd_only():
         e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col, alpha, L, H, wl.cutoff, mix_w=mix_w,
-                                      graph_id=gid, out=out)
+                                      graph_id=gid, out=out, workspace=ws)
 
     out_e = torch.empty_like(feat)
 
@@ -366,50 +441,30 @@ def main():
     ms_bwd_pos = timed(bwd(False, False, True), args.steps)
     ms_bwd_feat = timed(bwd(True, False), args.steps)
     ms_bwd_alpha = timed(bwd(False, True), args.steps)
-    pairs, tiles = e2f.e2f_last_plan(ctx)
     print("[bench] fwd %.3f ms, edge-TP %.3f ms, graph %.3f ms" % (ms_fwd, ms_edge, ms_nl), file=sys.stderr,
           flush=True)
 
     kernels = {k: dict(launches=v[0] // args.steps, ms=v[1] / args.steps) for k, v in prof.items()}
-    cnt = layer_counts(L)
-    dimT = cnt["dimT"]
-    # algorithmic bytes / flops per launch of each kernel of the forward
-    nk = (L + 1) ** 2
-    if "node_tp" in kernels:  # T rows per (tile, sender), aggregated over receiver blocks
-        agg = dict(bytes=4.0 * dimT * C * (pairs + n) + 4.0 * E * (1 + H) + 8.0 * (n + 1), flops=2.0 * E * dimT * C)
-    else:  # uncoupled products aggregated per receiver, then coupled: read h once, write S once
-        agg = dict(bytes=4.0 * n * nk * C + 4.0 * E * (1 + H) + 4.0 * pairs * nk + 8.0 * (n + 1) + 4.0 * n * dimT * C,
-                   flops=2.0 * E * nk * nk * C + 2.0 * n * coupling_entries(e2f, L) * C)
-    alg = {
-        "aggregate": agg,
-        "node_tp": dict(bytes=4.0 * C * (n * (L + 1) ** 2 + pairs * dimT), flops=2.0 * pairs * cnt["m_slots"] * C),
-        "recouple": dict(bytes=4.0 * C * n * (dimT + (L + 1) ** 2), flops=2.0 * n * cnt["q_slots"] * C),
-        "mix": dict(bytes=8.0 * n * (L + 1) ** 2 * C + 4.0 * (L + 1) * C * C, flops=2.0 * n * (L + 1) ** 2 * C * C),
-    }
-    peaks = {k: FP32_MFMA_PEAK_TFS for k in alg}  # all four run on fp32 MFMA
-
-    def roof_of(bytes_, flops, t_ms, peak_tf):
-        """Roofline position of one launch: the binding resource is the one
-        whose lower-bound time is larger."""
-        t_b, t_f = bytes_ / (HBM_PEAK_GBS * 1e9), flops / (peak_tf * 1e12)
-        if t_b >= t_f:
-            a = bytes_ / (t_ms * 1e-3) / 1e9
-            return dict(bound="hbm", achieved=a, peak=HBM_PEAK_GBS, unit="GB/s", frac=a / HBM_PEAK_GBS)
-        a = flops / (t_ms * 1e-3) / 1e12
-        return dict(bound="mfma", achieved=a, peak=peak_tf, unit="TFLOP/s", frac=a / peak_tf)
-
+    counts = alg_counts(e2f, L, C, H, n, E)
+    peaks = {"aggregate": FP32_MFMA_PEAK_TFS, "recouple": FP32_MFMA_PEAK_TFS, "mix": FP32_MFMA_PEAK_TFS}
     for k, v in kernels.items():
-        if k in alg:
+        if k in peaks:
             tk = v["ms"] / max(1, v["launches"])
-            v["alg_GBps"] = alg[k]["bytes"] / (tk * 1e-3) / 1e9
-            v["alg_TFLOPs"] = alg[k]["flops"] / (tk * 1e-3) / 1e12
-            r = roof_of(alg[k]["bytes"], alg[k]["flops"], tk, peaks[k])
+            v["alg_GBps"] = counts[k]["bytes"] / (tk * 1e-3) / 1e9
+            v["alg_TFLOPs"] = counts[k]["flops"] / (tk * 1e-3) / 1e12
+            r = roof_of(counts[k]["bytes"], counts[k]["flops"], tk, peaks[k])
             v["bound"], v["frac"] = r["bound"], r["frac"]
-    dom = max((k for k in kernels if k in alg), key=lambda k: kernels[k]["ms"])
+    dom = max((k for k in kernels if k in peaks), key=lambda k: kernels[k]["ms"])
     t_dom = kernels[dom]["ms"] / max(1, kernels[dom]["launches"])
-    roof = roof_of(alg[dom]["bytes"], alg[dom]["flops"], t_dom, peaks[dom])
+    roof = roof_of(counts[dom]["bytes"], counts[dom]["flops"], t_dom, peaks[dom])
     roof["traffic"] = None
     roof["kernel"] = dom
+    roof["launch_ms"] = t_dom
+    roof["alg_flops"] = counts[dom]["flops"]
+    roof["alg_bytes"] = counts[dom]["bytes"]
+    if "issued_flops" in counts[dom]:
+        roof["issued_flops"] = counts[dom]["issued_flops"]
+        roof["issued_TFLOPs"] = counts[dom]["issued_flops"] / (t_dom * 1e-3) / 1e12
     tr_path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (dom, wl.name))
     if os.path.exists(tr_path):
         tr = json.load(open(tr_path))
@@ -419,13 +474,14 @@ def main():
             # measured HBM rate: counter bytes over the same launch time
             roof["traffic_GBps"] = tr["bytes_per_launch"] / (t_dom * 1e-3) / 1e9
             roof["traffic_frac"] = roof["traffic_GBps"] / HBM_PEAK_GBS
+    floor = forward_floor(counts, ms_fwd)
 
     # ---- the bf16 channel-mixing variant of the same forward
     mix_bf16 = mix_w.to(torch.bfloat16)
 
     def fwd_bf16():
         e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col, alpha, L, H, wl.cutoff, mix_w=mix_bf16,
-                                      graph_id=gid, out=out)
+                                      graph_id=gid, out=out, workspace=ws)
 
     for _ in range(2):
         fwd_bf16()
@@ -437,15 +493,17 @@ def main():
     bf16_res = {"ms": ms_fwd_bf16, "atoms_per_s": n / (ms_fwd_bf16 * 1e-3), "mix_ms": mix16_ms}
     if mix16_ms:
         mb = 8.0 * n * (L + 1) ** 2 * C + 2.0 * (L + 1) * C * C
-        r = roof_of(mb, alg["mix"]["flops"], mix16_ms, BF16_MFMA_PEAK_TFS)
+        r = roof_of(mb, counts["mix"]["flops"], mix16_ms, BF16_MFMA_PEAK_TFS)
         bf16_res.update(mix_alg_GBps=mb / (mix16_ms * 1e-3) / 1e9,
-                        mix_alg_TFLOPs=alg["mix"]["flops"] / (mix16_ms * 1e-3) / 1e12,
+                        mix_alg_TFLOPs=counts["mix"]["flops"] / (mix16_ms * 1e-3) / 1e12,
                         mix_bound=r["bound"], mix_frac=r["frac"])
 
     if args.copy_calib:
         x = torch.empty(1 << 28, dtype=torch.float32, device=dev)
         y = torch.empty_like(x)
         y.copy_(x)
+        torch.cuda.synchronize()
+        x.sum()
         torch.cuda.synchronize()
 
     # ---- oracle on the host cores, bounded row sample; parity of the timed output
@@ -465,6 +523,25 @@ def main():
                    sample="%d of %d receiver rows (evenly spaced), fp64 layer definition + mixing, %.1f s" % (k, n, dt),
                    cpu_model=_cpu_model())
         parity = dict(rows=k, max_rel_err=oracle.max_rel_err(out_step[rows], ref, L), graph_bit_exact=graph_equal)
+    ctx.close()
+    del ws
+
+    # ---- every workload: forward, baseline, speedup, sampled parity
+    configs = None
+    if not args.no_configs:
+        configs = []
+        for name, crop in CONFIGS:
+            if name == wl.name and not crop:
+                configs.append({"workload": name, "atoms": n, "edges": E, "lmax": L, "channels": C, "heads": H,
+                                "cutoff": wl.cutoff, "fwd_ms": ms_fwd, "atoms_per_s": n / ms_fwd * 1e3,
+                                "edges_per_s": E / ms_fwd * 1e3, "edge_tp_ms": ms_edge,
+                                "speedup_vs_edge_tp": ms_edge / ms_fwd, "parity": parity})
+                continue
+            r = sweep_one(name, max(3, args.steps // 4), 2, crop)
+            print("[bench] %s: fwd %.3f ms%s, parity %.2e" % (
+                r["workload"], r["fwd_ms"], (", edge-TP %.3f ms" % r["edge_tp_ms"]) if "edge_tp_ms" in r else "",
+                r["parity"]["max_rel_err"]), file=sys.stderr, flush=True)
+            configs.append(r)
 
     res = {
         "metric": METRIC,
@@ -480,22 +557,26 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "atoms": n, "edges": E, "lmax": L, "channels": C, "heads": H,
-                   "cutoff": wl.cutoff, "mix": "fp32", "pairs": pairs, "tiles": tiles,
-                   "step": "radius graph + Wigner-6j conv forward"},
+                   "cutoff": wl.cutoff, "mix": "fp32", "step": "radius graph + Wigner-6j conv forward"},
         "edges_per_s": E / (ms_step * 1e-3),
-        "fwd": {"ms": ms_fwd, "atoms_per_s": n / (ms_fwd * 1e-3), "edges_per_s": E / (ms_fwd * 1e-3)},
+        "fwd": {"ms": ms_fwd, "atoms_per_s": n / (ms_fwd * 1e-3), "edges_per_s": E / (ms_fwd * 1e-3),
+                "roofline": floor},
         "edge_tp": {"ms": ms_edge, "atoms_per_s": n / (ms_edge * 1e-3), "edges_per_s": E / (ms_edge * 1e-3)},
         "speedup_vs_edge_tp": ms_edge / ms_fwd,
         "fwd_bf16_mix": bf16_res,
         "neighbor_list_ms": ms_nl,
+        "workspace_bytes": ws_bytes,
         "backward": {"ms": ms_bwd, "grad_feat_ms": ms_bwd_feat, "grad_alpha_ms": ms_bwd_alpha,
                      "grad_pos_ms": ms_bwd_pos},
         "global_moment": {"ms": ms_glob, "pairs": n * n, "atoms_per_s": n / (ms_glob * 1e-3)},
         "attention": {"ms": ms_att, "dk": 16, "n_rbf": 8, "bytes_GBps": (E * (4 + 4 * H) + 12.0 * n) / (ms_att * 1e-3) / 1e9},
+        "counts": {"dimT": counts["dimT"], "coupling_entries": counts["coupling_entries"],
+                   "recouple_entries": counts["recouple_entries"]},
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": cpu,
         "parity": parity,
+        "configs": configs,
     }
     print(json.dumps(res))
 

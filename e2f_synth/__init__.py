@@ -157,6 +157,54 @@ def make_inputs(wl: Workload, n_atoms: int | None = None) -> Inputs:
     return Inputs(pos, graph_id, species, feat, mix_w, default_path_weights(wl.lmax, wl.cutoff), wl)
 
 
+def _attention_tables(heads: int, cutoff: float, n_species: int, seed: int):
+    """The seeded species embedding, radial mixing weights and radial centres
+    of the synthetic attention weights (shared by both generators below)."""
+    rng = np.random.default_rng(0xA1FA0000 + seed)
+    emb = rng.standard_normal((n_species, heads))
+    rho = rng.standard_normal((heads, 8)) / math.sqrt(8.0)
+    mu = np.arange(8) * cutoff / 7.0
+    return emb, rho, mu, cutoff / 7.0
+
+
+def attention_weights_device(pos, species, row_ptr, col_idx, heads: int, cutoff: float, n_species: int, seed: int,
+                             device):
+    """The same synthetic attention weights as attention_weights, computed
+    with torch in float64 on `device` (for inputs too large for the host
+    generator) and rounded to float32: [E, H].  Row sums are taken in another
+    order than on the host, so values may differ from attention_weights in
+    the last bit."""
+    import torch
+    emb, rho, mu, sigma = _attention_tables(heads, cutoff, n_species, seed)
+    rp = torch.as_tensor(np.asarray(row_ptr, dtype=np.int64), device=device)
+    ci = torch.as_tensor(np.asarray(col_idx, dtype=np.int64), device=device)
+    n = rp.numel() - 1
+    E = int(rp[-1].item())
+    if E == 0:
+        return torch.empty(0, heads, dtype=torch.float32, device=device)
+    recv = torch.repeat_interleave(torch.arange(n, device=device), rp[1:] - rp[:-1])
+    p64 = torch.as_tensor(np.asarray(pos, dtype=np.float64), device=device)
+    sp = torch.as_tensor(np.asarray(species, dtype=np.int64), device=device)
+    emb_t = torch.as_tensor(emb, device=device)
+    rho_t = torch.as_tensor(rho, device=device)
+    mu_t = torch.as_tensor(mu, device=device)
+    logits = torch.empty(E, heads, dtype=torch.float64, device=device)
+    env = torch.empty(E, dtype=torch.float64, device=device)
+    chunk = 1 << 22
+    for s in range(0, E, chunk):
+        i, j = recv[s:s + chunk], ci[s:s + chunk]
+        d = torch.linalg.norm(p64[i] - p64[j], dim=1)
+        rbf = torch.exp(-(((d[:, None] - mu_t[None, :]) / sigma) ** 2))
+        logits[s:s + chunk] = emb_t[sp[i]] * emb_t[sp[j]] + rbf @ rho_t.T
+        env[s:s + chunk] = 0.5 * (torch.cos(math.pi * d / cutoff) + 1.0)
+    idx = recv[:, None].expand(-1, heads)
+    rmax = torch.zeros(n, heads, dtype=torch.float64, device=device).scatter_reduce_(0, idx, logits, "amax",
+                                                                                      include_self=False)
+    ex = torch.exp(logits - rmax[recv])
+    den = torch.zeros(n, heads, dtype=torch.float64, device=device).index_add_(0, recv, ex)
+    return (env[:, None] * ex / den[recv]).to(torch.float32)
+
+
 def attention_weights(pos: np.ndarray, species: np.ndarray, row_ptr: np.ndarray, col_idx: np.ndarray,
                       heads: int, cutoff: float, n_species: int, seed: int) -> np.ndarray:
     """Synthetic per-edge, per-head attention weights [E, H] float32.
@@ -166,11 +214,7 @@ def attention_weights(pos: np.ndarray, species: np.ndarray, row_ptr: np.ndarray,
     Depends only on distances and species, so it is rotation and translation
     invariant.  Computed in float64, rounded to float32.
     """
-    rng = np.random.default_rng(0xA1FA0000 + seed)
-    emb = rng.standard_normal((n_species, heads))
-    rho = rng.standard_normal((heads, 8)) / math.sqrt(8.0)
-    mu = np.arange(8) * cutoff / 7.0
-    sigma = cutoff / 7.0
+    emb, rho, mu, sigma = _attention_tables(heads, cutoff, n_species, seed)
     row_ptr = np.asarray(row_ptr, dtype=np.int64)
     col_idx = np.asarray(col_idx, dtype=np.int64)
     n = row_ptr.shape[0] - 1

@@ -24,11 +24,18 @@
  *
  * Memory: every pointer argument is HIP device memory owned by the caller
  * unless it is marked "host".  The library never frees caller memory.  A
- * context owns its coefficient tables and an internal workspace that grows
- * on demand (hipMalloc) and is released by e2f_destroy.
+ * context owns its coefficient tables: the structure tables of every degree
+ * (uploaded by e2f_create) and one set of path-weighted coefficients per
+ * path-weight vector it has seen (uploaded on first use, at most 16 per
+ * degree).  The Wigner-6j forward works in a workspace the caller provides
+ * (e2f_wigner6j_workspace_size); the other layer entry points (edge-TP
+ * baseline with mixing, dense and global forms, backward, node TP) keep an
+ * internal workspace that grows on demand (hipMalloc) and is released by
+ * e2f_destroy.
  *
  * Streams: `stream` is a hipStream_t passed as void* (NULL = null stream).
- * Work is enqueued on it; calls marked (sync) also wait for it.
+ * Work is enqueued on it; calls marked (sync) also wait for it.  Calls not
+ * marked (sync) neither wait for the device nor read anything back from it.
  *
  * Errors: functions return e2f_status and never throw.  Arguments are
  * checked on the host before any device work; on E2F_EINVAL no output is
@@ -133,38 +140,81 @@ e2f_status e2f_node_tp(e2f_ctx* ctx, const float* pos, const float* origins, con
 typedef struct {
   int lmax;              /* L, 0..6 */
   int32_t channels;      /* C, a multiple of 4, <= 1024 */
-  int32_t heads;         /* H, C % H == 0 and (C/H) % 4 == 0 */
+  int32_t heads;         /* H, C % H == 0 and (C/H) % 4 == 0 (a head wider than the aggregation's
+                            tile is split into channel groups that share its weights) */
   float cutoff;          /* r_c of the graph, used for default weights and tiles */
   const double* path_w;  /* host [(L+1)^3] w[a][f][o]; NULL => cutoff^-f on triangle-valid paths */
   const void* mix_w;     /* device [(L+1)][C][C] W[o][c_out][c_in] of mix_dtype; NULL => no mixing */
   e2f_dtype mix_dtype;   /* E2F_F32, or E2F_BF16 (mixing inputs rounded to bf16, fp32 accumulate) */
   float tile_side;       /* side of the receiver tiles whose centres serve as local origins;
-                            0 => cutoff * (8, 8, 8, 6, 4, 3, 2) for L = 0..6 */
+                            0 => cutoff * (8, 8, 8, 6, 4, 3, 2) for L = 0..6 (fp32 precision of
+                            the binomial expansion; the cost does not depend on it) */
   int32_t y_norm;        /* 0: the layer above.  1: Alg. 1's per-degree attention weights
                             alpha_ij / D_ij^f on the paths of filter degree f, D_ij = |r_i - r_j|
                             (filters Y^(f) of the unit vector; the path f takes 0 at D = 0 for
                             f > 0).  The factorised forward then aggregates once per f (L+1
-                            times the aggregation work and S memory); it needs every degree
-                            <= 512 (else E2F_EUNSUPPORTED).  Forward entry points only (the
-                            backward returns E2F_EUNSUPPORTED) */
+                            times the aggregation work).  The weights 1/D^f no longer damp the
+                            rounding of the binomial expansion (about eps ((|p_i| + |p_j|) /
+                            D_ij)^f per edge), so the tile side is capped at 2.31 times the
+                            shortest nonzero edge (found on the device), keeping that ratio
+                            below 5.  Forward entry points only (the backward returns
+                            E2F_EUNSUPPORTED) */
 } e2f_conv_params;
 
+/* Workspace of e2f_wigner6j_conv_forward for n atoms and n_edges edges:
+ * *bytes (host) = the size with which every receiver's S fits at once (one
+ * aggregation pass), about E (L+1)^2 4 + N dimT C 4 bytes plus the plan
+ * (N (L+1)^2 8 + 40 N bytes and the sort's scratch), E H 4 for the attention
+ * weights ((L+1) times that with y_norm) and N (L+1)^2 C 4 with mixing. */
+e2f_status e2f_wigner6j_workspace_size(e2f_ctx* ctx, const e2f_conv_params* params, int32_t n, int64_t n_edges,
+                                       size_t* bytes);
+/* The smallest workspace the forward accepts: the plan and per-edge arrays
+ * plus S for 256 receivers; any size between this and
+ * e2f_wigner6j_workspace_size works (receivers are then aggregated and
+ * recoupled in slices that fit, in the same order and with the same result). */
+e2f_status e2f_wigner6j_workspace_min(e2f_ctx* ctx, const e2f_conv_params* params, int32_t n, int64_t n_edges,
+                                      size_t* bytes);
+/* Uploads what the forward needs for these parameters (the coefficient set
+ * of the path weights, the aggregation's coupling schedule) so that later
+ * forwards with them do no host-to-device copy.  The forward does the same
+ * on first use.  (sync) */
+e2f_status e2f_wigner6j_prepare(e2f_ctx* ctx, const e2f_conv_params* params);
+
 /* Wigner-6j convolution forward (Thm. 3.3, Alg. 1): the layer above computed
- * by node factorisation.  Per receiver tile t (a cube of side tile_side per
- * graph) with centre o_t:  T_j = [h_j (x) R^(b)(r_j - o_t)]^(d) for the
- * senders of t's receivers,  S_i = sum_j alpha_ij T_j,
- * y_i = sum K(a,b,d,u,o) [R^(u)(r_i - o_t) (x) S_i^(a,b,d)]^(o), then mixing.
- * graph_id: [N] or NULL (must match the graph's).  alpha: [E][H] or NULL
- * (all ones).  out: [N][(L+1)^2][C].  Isolated atoms get zero rows.
- * Tiles are processed in batches whose T and S fit a memory budget (60% of
- * the free device memory, at most 96 GiB; the environment variable
- * E2F_TILE_BUDGET_MB overrides it), so the workspace stays bounded for large
- * systems.  Deterministic: no floating-point atomics.  (sync: small
- * device->host reads of the plan sizes) */
+ * by node factorisation.  Each receiver i takes as local origin o the centre
+ * of its tile (a cube of side tile_side of its graph's bounding box).  With
+ * p = r - o, the forward aggregates the uncoupled products of the neighbours,
+ *   G_i = sum_j alpha_ij R(p_j) (x) h_j   (the j-side node product before
+ *   its CG coupling, Alg. 1 clebsch_gorden_tp; linear in h_j (x) R(p_j)),
+ * couples them into S_i^(a,b,d) = [h (x) R^(b)]^(d) summed over j (the
+ * einsum "ijh,jhds->ihds"), and recouples at the receiver,
+ *   y_i = sum K(a,b,d,u,o) [R^(u)(p_i) (x) S_i^(a,b,d)]^(o)   (Wigner6jTP),
+ * then mixes.  graph_id: [N] or NULL (must match the graph's).  alpha:
+ * [E][H] or NULL (all ones).  out: [N][(L+1)^2][C].  Isolated atoms get zero
+ * rows.
+ * workspace: device memory of workspace_bytes >= e2f_wigner6j_workspace_min
+ * (else E2F_ECAPACITY), 256-byte aligned; its contents on entry do not
+ * matter and are overwritten.  Not needed (may be NULL) when n_edges = 0.
+ * Asynchronous: no host wait, no device allocation or host-to-device copy
+ * once the path weights are resident (e2f_wigner6j_prepare), so the call can
+ * be captured in a HIP graph.  The plan (bounding box, tiles, receiver order)
+ * is derived on the device: positions must be finite with |x| < 16384 A (an
+ * atom outside that range is placed in the nearest tile and its outputs are
+ * not meaningful; nothing is reported).  The CSR is trusted for values but
+ * read with clamped indices (a malformed graph gives wrong outputs, never an
+ * access outside the buffers); e2f_validate_graph checks one.
+ * Deterministic: no floating-point atomics. */
 e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
                                      const int32_t* graph_id, const float* feat, int32_t n, const int64_t* row_ptr,
                                      const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,
-                                     void* stream);
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Checks a CSR graph of n atoms: *bad (host) = 0 if row_ptr[0] = 0, row_ptr
+ * never decreases, row_ptr[n] = n_edges and every col_idx is in [0, n); else
+ * the OR of 1 (row_ptr[0]), 2 (a decreasing row_ptr), 4 (row_ptr[n]), 8 (a
+ * sender out of range).  Launches no layer kernel.  (sync) */
+e2f_status e2f_validate_graph(e2f_ctx* ctx, int32_t n, const int64_t* row_ptr, const int32_t* col_idx,
+                              int64_t n_edges, int32_t* bad /* host */, void* stream);
 
 /* The layer on a dense graph (every atom attends to every other atom; the
  * dense graphs of the scaling study, Sec. 4.1, and Alg. 1 with its attention
@@ -231,10 +281,9 @@ e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* params,
                                     const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,
                                     void* stream);
 
-/* Size of the tile plan of the last e2f_wigner6j_conv_forward on this
- * context: *pairs = number of (tile, sender) rows of T it computed, *tiles =
- * number of graph x cell tile keys.  Host outputs. */
-e2f_status e2f_last_plan(const e2f_ctx* ctx, int64_t* pairs /* host */, int64_t* tiles /* host */);
+/* Number of receiver slices the last e2f_wigner6j_conv_forward on this
+ * context ran (1 when the workspace held every receiver's S).  Host output. */
+e2f_status e2f_last_slices(const e2f_ctx* ctx, int64_t* slices /* host */);
 
 /* Kernel timing.  e2f_profile(ctx, 1) waits for the device, clears the
  * records and starts bracketing every launch group of this context with HIP

@@ -22,10 +22,12 @@ E2F_F32, E2F_BF16 = 0, 1
 _STATUS = {0: "E2F_OK", 1: "E2F_EINVAL", 2: "E2F_ECAPACITY", 3: "E2F_ENOMEM", 4: "E2F_EDEVICE", 5: "E2F_EUNSUPPORTED"}
 
 # every function declared in include/e2f.h
-EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg", "e2f_knn_graph", "e2f_attention_weights",
-            "e2f_recoupling_weight", "e2f_neighbor_list", "e2f_solid_harmonics", "e2f_node_tp",
-            "e2f_wigner6j_conv_forward", "e2f_wigner6j_conv_forward_dense", "e2f_wigner6j_conv_forward_global",
-            "e2f_wigner6j_conv_backward", "e2f_edge_tp_conv_forward", "e2f_profile", "e2f_profile_read", "e2f_last_plan"]
+EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg", "e2f_knn_graph",
+            "e2f_attention_weights", "e2f_recoupling_weight", "e2f_neighbor_list", "e2f_solid_harmonics",
+            "e2f_node_tp", "e2f_wigner6j_workspace_size", "e2f_wigner6j_workspace_min", "e2f_wigner6j_prepare",
+            "e2f_wigner6j_conv_forward", "e2f_validate_graph", "e2f_wigner6j_conv_forward_dense",
+            "e2f_wigner6j_conv_forward_global", "e2f_wigner6j_conv_backward", "e2f_edge_tp_conv_forward",
+            "e2f_profile", "e2f_profile_read", "e2f_last_slices"]
 
 
 class E2FError(RuntimeError):
@@ -68,16 +70,25 @@ def _load():
     L.e2f_solid_harmonics.restype = i
     L.e2f_node_tp.argtypes = [p, p, p, p, p, i32, i32, i, p, p]
     L.e2f_node_tp.restype = i
-    L.e2f_last_plan.argtypes = [p, ctypes.POINTER(i64), ctypes.POINTER(i64)]
-    L.e2f_last_plan.restype = i
+    L.e2f_last_slices.argtypes = [p, ctypes.POINTER(i64)]
+    L.e2f_last_slices.restype = i
+    for name in ("e2f_wigner6j_workspace_size", "e2f_wigner6j_workspace_min"):
+        fn = getattr(L, name)
+        fn.argtypes = [p, ctypes.POINTER(ConvParams), i32, i64, ctypes.POINTER(ctypes.c_size_t)]
+        fn.restype = i
+    L.e2f_wigner6j_prepare.argtypes = [p, ctypes.POINTER(ConvParams)]
+    L.e2f_wigner6j_prepare.restype = i
+    L.e2f_validate_graph.argtypes = [p, i32, p, p, i64, ctypes.POINTER(i32), p]
+    L.e2f_validate_graph.restype = i
     L.e2f_profile.argtypes = [p, i]
     L.e2f_profile.restype = i
     L.e2f_profile_read.argtypes = [p, ctypes.c_char_p, ctypes.c_size_t]
     L.e2f_profile_read.restype = i
-    for name in ("e2f_wigner6j_conv_forward", "e2f_edge_tp_conv_forward"):
-        fn = getattr(L, name)
-        fn.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, i32, p, p, i64, p, p, p]
-        fn.restype = i
+    L.e2f_wigner6j_conv_forward.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, i32, p, p, i64, p, p, p,
+                                            ctypes.c_size_t, p]
+    L.e2f_wigner6j_conv_forward.restype = i
+    L.e2f_edge_tp_conv_forward.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, i32, p, p, i64, p, p, p]
+    L.e2f_edge_tp_conv_forward.restype = i
     L.e2f_wigner6j_conv_forward_dense.argtypes = [p, ctypes.POINTER(ConvParams), p, p, i32, p, p, p]
     L.e2f_wigner6j_conv_forward_dense.restype = i
     L.e2f_wigner6j_conv_forward_global.argtypes = [p, ctypes.POINTER(ConvParams), p, p, i32, p, p]
@@ -115,7 +126,8 @@ def _dev(t, dtype, name):
 
 
 class Context:
-    """Owns an e2f_ctx (coefficient tables and workspace) on one device."""
+    """Owns an e2f_ctx (coefficient tables) on one device, and the device
+    workspace tensor the binding passes to the Wigner-6j forward."""
 
     def __init__(self, lmax_max: int = 6, device: int | None = 0):
         h = ctypes.c_void_p()
@@ -124,9 +136,18 @@ class Context:
         self.handle = h
         self.device = dev
         self.lmax_max = lmax_max
+        self.workspace = None
+
+    def workspace_for(self, nbytes: int, device) -> torch.Tensor:
+        """A device buffer of at least nbytes, kept for later calls."""
+        if self.workspace is None or self.workspace.numel() < nbytes:
+            self.workspace = None
+            self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        return self.workspace
 
     def close(self):
         if self.handle:
+            self.workspace = None
             lib.e2f_destroy(self.handle)
             self.handle = None
 
@@ -270,40 +291,87 @@ def _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm=Fals
     return prm, keep
 
 
-def _conv(fn_name, ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w, mix_w, graph_id,
-          tile_side, out, y_norm=False):
+def _conv_args(pos, feat, row_ptr, col_idx, alpha, graph_id, out):
     _dev(pos, torch.float32, "pos")
     _dev(feat, torch.float32, "feat")
     _dev(row_ptr, torch.int64, "row_ptr")
     _dev(col_idx, torch.int32, "col_idx")
     _dev(alpha, torch.float32, "alpha")
     _dev(graph_id, torch.int32, "graph_id")
-    n, nk, C = feat.shape
     if out is None:
         out = torch.empty_like(feat)
     _dev(out, torch.float32, "out")
-    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm)
-    st = getattr(lib, fn_name)(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(graph_id), _ptr(feat), n,
-                               _ptr(row_ptr), _ptr(col_idx), col_idx.numel(), _ptr(alpha), _ptr(out),
-                               _stream(feat.device))
-    del keep
-    _check(st, fn_name)
     return out
 
 
+def e2f_wigner6j_workspace_size(ctx, n, n_edges, lmax, channels, heads, cutoff, path_w=None, mix_w=None,
+                                tile_side=0.0, y_norm=False, minimum=False) -> int:
+    """Workspace bytes of the forward (the one-pass size, or with minimum=True
+    the smallest size it accepts)."""
+    prm, keep = _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm)
+    b = ctypes.c_size_t(0)
+    fn = lib.e2f_wigner6j_workspace_min if minimum else lib.e2f_wigner6j_workspace_size
+    _check(fn(ctx.handle, ctypes.byref(prm), n, n_edges, ctypes.byref(b)),
+           "e2f_wigner6j_workspace_min" if minimum else "e2f_wigner6j_workspace_size")
+    del keep
+    return b.value
+
+
+def e2f_wigner6j_prepare(ctx, lmax, channels, heads, cutoff, path_w=None, mix_w=None, tile_side=0.0,
+                         y_norm=False) -> None:
+    """Upload the coefficient set and coupling schedule these parameters use."""
+    prm, keep = _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm)
+    _check(lib.e2f_wigner6j_prepare(ctx.handle, ctypes.byref(prm)), "e2f_wigner6j_prepare")
+    del keep
+
+
 def e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None, mix_w=None,
-                              graph_id=None, tile_side=0.0, out=None, y_norm=False):
+                              graph_id=None, tile_side=0.0, out=None, y_norm=False, workspace=None):
     """Wigner-6j convolution forward; returns out [N,(L+1)^2,C] float32.
-    y_norm: attention weights alpha / |r_i - r_j|^f per filter degree f."""
-    return _conv("e2f_wigner6j_conv_forward", ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w,
-                 mix_w, graph_id, tile_side, out, y_norm)
+    y_norm: attention weights alpha / |r_i - r_j|^f per filter degree f.
+    workspace: a uint8 device tensor (any size from the minimum up); None
+    uses the context's own, grown to the one-pass size."""
+    out = _conv_args(pos, feat, row_ptr, col_idx, alpha, graph_id, out)
+    n, nk, C = feat.shape
+    E = col_idx.numel()
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm)
+    if workspace is None:
+        b = ctypes.c_size_t(0)
+        _check(lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm), n, E, ctypes.byref(b)),
+               "e2f_wigner6j_workspace_size")
+        workspace = ctx.workspace_for(b.value, feat.device)
+    elif not workspace.is_cuda or workspace.dtype != torch.uint8 or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 device tensor")
+    st = lib.e2f_wigner6j_conv_forward(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(graph_id), _ptr(feat), n,
+                                       _ptr(row_ptr), _ptr(col_idx), E, _ptr(alpha), _ptr(out), _ptr(workspace),
+                                       workspace.numel(), _stream(feat.device))
+    del keep
+    _check(st, "e2f_wigner6j_conv_forward")
+    return out
 
 
 def e2f_edge_tp_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None, mix_w=None,
                              graph_id=None, tile_side=0.0, out=None, y_norm=False):
     """Per-edge SO(3) convolution baseline; same output as the 6j forward."""
-    return _conv("e2f_edge_tp_conv_forward", ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w,
-                 mix_w, graph_id, tile_side, out, y_norm)
+    out = _conv_args(pos, feat, row_ptr, col_idx, alpha, graph_id, out)
+    n, nk, C = feat.shape
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm)
+    st = lib.e2f_edge_tp_conv_forward(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(graph_id), _ptr(feat), n,
+                                      _ptr(row_ptr), _ptr(col_idx), col_idx.numel(), _ptr(alpha), _ptr(out),
+                                      _stream(feat.device))
+    del keep
+    _check(st, "e2f_edge_tp_conv_forward")
+    return out
+
+
+def e2f_validate_graph(ctx, n, row_ptr, col_idx) -> int:
+    """0 if the device CSR is well formed, else the error bits of e2f.h."""
+    _dev(row_ptr, torch.int64, "row_ptr")
+    _dev(col_idx, torch.int32, "col_idx")
+    bad = ctypes.c_int32(0)
+    _check(lib.e2f_validate_graph(ctx.handle, n, _ptr(row_ptr), _ptr(col_idx), col_idx.numel(), ctypes.byref(bad),
+                                  _stream(row_ptr.device)), "e2f_validate_graph")
+    return bad.value
 
 
 def e2f_wigner6j_conv_forward_dense(ctx, pos, feat, alpha, lmax, heads, cutoff, path_w=None, mix_w=None, out=None):
@@ -383,8 +451,8 @@ def e2f_profile_read(ctx: Context) -> dict:
     return out
 
 
-def e2f_last_plan(ctx: Context) -> tuple:
-    """(pairs, tiles) of the last factorised forward on this context."""
-    P, T = ctypes.c_int64(0), ctypes.c_int64(0)
-    _check(lib.e2f_last_plan(ctx.handle, ctypes.byref(P), ctypes.byref(T)), "e2f_last_plan")
-    return P.value, T.value
+def e2f_last_slices(ctx: Context) -> int:
+    """Receiver slices of the last factorised forward on this context."""
+    v = ctypes.c_int64(0)
+    _check(lib.e2f_last_slices(ctx.handle, ctypes.byref(v)), "e2f_last_slices")
+    return v.value

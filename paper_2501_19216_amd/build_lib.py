@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libe2f.so")
-SOURCES = ["neighbor.hip", "conv.hip", "attention.hip", "abi.cpp", "tables.cpp"]
+SOURCES = ["neighbor.hip", "plan.hip", "conv.hip", "attention.hip", "abi.cpp", "tables.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall", "-Wno-unused-result",

@@ -49,11 +49,20 @@ struct e2f_ctx {
   std::vector<LayerTables> host;
   std::vector<DevTables> dev;
   std::vector<void*> table_mem;            // structure arrays per L
-  std::vector<void*> coef_mem;             // weighted coefficients per L
-  std::vector<std::vector<double>> coef_w; // path weights of the uploaded coefficients
+  // path-weighted coefficients, one set per path-weight vector (per L, most
+  // recently added last; at most kMaxCoefSets per L)
+  struct CoefSet {
+    std::vector<double> w;
+    void* mem = nullptr;
+    const double* q_coef = nullptr;
+    const float* k_coef = nullptr;
+    const double* rc_coef = nullptr;
+    std::vector<const double*> rcf_coef;  // per filter degree f
+    const float* w_f = nullptr;
+  };
+  std::vector<std::vector<CoefSet>> coefs;
   // per L and filter degree f: the recouple schedule restricted to b + u = f
   std::vector<std::vector<const int*>> rcf_k, rcf_off, rcf_meta;
-  std::vector<std::vector<const double*>> rcf_coef;
   int* stats = nullptr;                    // device, kStatsInts ints
   int64_t* pinned = nullptr;               // host, 16 int64
   int32_t* pinned_plan = nullptr;          // host, plan sizes read back in one copy
@@ -62,8 +71,7 @@ struct e2f_ctx {
   Buf a, b, c;
   Buf d;                                   // backward staging (transposed graph, input gradient)
   std::vector<std::vector<double>> kappa;  // per L: [a][f][o] real CG transpose factors (0 = not computed)
-  int64_t last_pairs = 0, last_tiles = 0;  // plan size of the last factorised forward
-  int64_t last_batches = 0;
+  int64_t last_slices = 0;                 // receiver slices of the last factorised forward
   // kernel timing (e2f_profile): events recorded on the launch stream
   bool prof = false;
   struct Rec {
@@ -321,7 +329,6 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
   ctx->rcf_k[L].assign(L + 1, nullptr);
   ctx->rcf_off[L].assign(L + 1, nullptr);
   ctx->rcf_meta[L].assign(L + 1, nullptr);
-  ctx->rcf_coef[L].assign(L + 1, nullptr);
   for (int f = 0; f <= L; ++f) {
     ctx->rcf_k[L][f] = (const int*)(b + o[23 + 3 * f]);
     ctx->rcf_off[L][f] = (const int*)(b + o[24 + 3 * f]);
@@ -352,9 +359,21 @@ std::vector<double> path_weights(const e2f_conv_params* p) {
   return w;
 }
 
-// Refresh the path-weighted coefficient arrays of degree L when the weights change.
-e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStream_t s) {
-  if (ctx->coef_mem[L] && ctx->coef_w[L] == w) return E2F_OK;
+constexpr size_t kMaxCoefSets = 16;
+
+// The coefficient set of degree L for the path weights w: found among the
+// resident sets, else built and uploaded (a synchronous upload, on first use
+// only; allow_upload = false makes a missing set an error instead).
+e2f_status coef_of(e2f_ctx* ctx, int L, const std::vector<double>& w, bool allow_upload,
+                   const e2f_ctx::CoefSet*& out) {
+  std::vector<e2f_ctx::CoefSet>& sets = ctx->coefs[L];
+  for (const e2f_ctx::CoefSet& c : sets)
+    if (c.w == w) {
+      out = &c;
+      return E2F_OK;
+    }
+  if (!allow_upload)
+    return fail(E2F_EINVAL, "these path weights are not resident on the context; call e2f_wigner6j_prepare first");
   const LayerTables& t = ctx->host[L];
   std::vector<double> q(t.q_unit.size());
   for (size_t e = 0; e < q.size(); ++e) q[e] = t.q_unit[e] * w[t.q_path[e]];
@@ -375,20 +394,48 @@ e2f_status set_weights(e2f_ctx* ctx, int L, const std::vector<double>& w, hipStr
   }
   std::vector<float> wf(w.begin(), w.end());  // o[4 + L]
   push_array(blob, o, wf);
-  E2F_HIP(hipStreamSynchronize(s));  // earlier work may still read the old coefficients
-  if (ctx->coef_mem[L]) E2F_HIP(hipFree(ctx->coef_mem[L]));
-  ctx->coef_mem[L] = nullptr;
+  if (sets.size() >= kMaxCoefSets) {  // the oldest set may still be read by queued work
+    E2F_HIP(hipDeviceSynchronize());
+    E2F_HIP(hipFree(sets.front().mem));
+    sets.erase(sets.begin());
+  }
   void* mem = nullptr;
   E2F_HIP(hipMalloc(&mem, blob.size()));
-  E2F_HIP(hipMemcpy(mem, blob.data(), blob.size(), hipMemcpyHostToDevice));
-  ctx->coef_mem[L] = mem;
-  ctx->coef_w[L] = w;
-  ctx->dev[L].q_coef = (const double*)((char*)mem + o[0]);
-  ctx->dev[L].k_coef = (const float*)((char*)mem + o[1]);
-  ctx->dev[L].rc_coef = (const double*)((char*)mem + o[2]);
-  for (int f = 0; f <= L; ++f) ctx->rcf_coef[L][f] = (const double*)((char*)mem + o[3 + f]);
-  ctx->dev[L].w_f = (const float*)((char*)mem + o[4 + L]);
+  if (hipMemcpy(mem, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipFree(mem);
+    return fail(E2F_EDEVICE, "coefficient upload failed");
+  }
+  e2f_ctx::CoefSet c;
+  c.w = w;
+  c.mem = mem;
+  c.q_coef = (const double*)((char*)mem + o[0]);
+  c.k_coef = (const float*)((char*)mem + o[1]);
+  c.rc_coef = (const double*)((char*)mem + o[2]);
+  for (int f = 0; f <= L; ++f) c.rcf_coef.push_back((const double*)((char*)mem + o[3 + f]));
+  c.w_f = (const float*)((char*)mem + o[4 + L]);
+  sets.push_back(std::move(c));
+  out = &sets.back();
   return E2F_OK;
+}
+
+// The device tables of degree L with the coefficients of one weight set.
+DevTables with_coef(const e2f_ctx* ctx, int L, const e2f_ctx::CoefSet& c) {
+  DevTables t = ctx->dev[L];
+  t.q_coef = c.q_coef;
+  t.k_coef = c.k_coef;
+  t.rc_coef = c.rc_coef;
+  t.w_f = c.w_f;
+  return t;
+}
+
+// The same restricted to the recouple terms of filter degree f.
+DevTables with_coef_f(const e2f_ctx* ctx, int L, const e2f_ctx::CoefSet& c, int f) {
+  DevTables t = with_coef(ctx, L, c);
+  t.rc_k = ctx->rcf_k[L][f];
+  t.rc_off = ctx->rcf_off[L][f];
+  t.rc_meta = ctx->rcf_meta[L][f];
+  t.rc_coef = c.rcf_coef[f];
+  return t;
 }
 
 bool finite_pos(float x) { return std::isfinite(x) && x > 0.0f; }
@@ -484,6 +531,163 @@ e2f_status transpose_factors(e2f_ctx* ctx, int L, const std::vector<double>*& ou
   return E2F_OK;
 }
 
+
+// ---------------------------------------------------------------- forward
+// Smallest slice of receivers a workspace must hold S for.
+constexpr int64_t kMinSlice = 256;
+
+// Byte layout of the forward's workspace: the plan and per-edge arrays (a
+// fixed part), then S for a slice of receivers.
+struct FwdLayout {
+  size_t stats = 0, dmin = 0, grid = 0, tile_of = 0, keys = 0, keys_out = 0, vals = 0, order = 0, sort_tmp = 0;
+  size_t sort_b = 0, Re = 0, Rr = 0, alpha_hm = 0, erows = 0, y = 0, S = 0;
+  size_t fixed = 0;  // bytes before S
+  size_t s_row = 0;  // S bytes per receiver
+  size_t total(int64_t slice) const { return fixed + s_row * (size_t)std::max<int64_t>(slice, 0); }
+};
+
+FwdLayout fwd_layout(const e2f_conv_params* p, int n, int64_t E, bool have_alpha) {
+  const int L = p->lmax, nk = nk_of(L), C = p->channels, H = p->heads;
+  const bool ynorm = p->y_norm != 0;
+  FwdLayout f;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += al256(bytes);
+    return at;
+  };
+  f.stats = take(sizeof(int) * 16);
+  f.dmin = take(sizeof(unsigned));
+  f.grid = take(sizeof(TileGridDev));
+  f.tile_of = take(sizeof(int32_t) * (size_t)n);
+  f.keys = take(sizeof(uint64_t) * (size_t)n);
+  f.keys_out = take(sizeof(uint64_t) * (size_t)n);
+  f.vals = take(sizeof(int32_t) * (size_t)n);
+  f.order = take(sizeof(int32_t) * (size_t)n);
+  f.sort_b = plan_sort_tmp_bytes(std::max(n, 1));
+  f.sort_tmp = take(f.sort_b);
+  f.Re = take(sizeof(float) * (size_t)E * nk);
+  f.Rr = take(sizeof(double) * (size_t)n * nk);
+  const size_t na = ynorm ? (size_t)(L + 1) : (have_alpha ? 1 : 0);
+  f.alpha_hm = take(sizeof(float) * (size_t)E * H * na);
+  f.erows = take(ynorm ? sizeof(int32_t) * (size_t)E : 0);
+  f.y = take(p->mix_w ? sizeof(float) * (size_t)n * nk * C : 0);
+  f.S = off;
+  f.fixed = off;
+  f.s_row = al256(sizeof(float) * (size_t)node_tp_dim(L) * C);
+  return f;
+}
+
+// The split of each head into hdiv channel groups (hdiv | C/H, width a
+// multiple of 4) with which the aggregation's per-receiver tile fits; 0 if none.
+int head_split(int L, int C, int H) {
+  const int dh = C / H;
+  for (int hd = 1; hd <= dh / 4; ++hd)
+    if (dh % hd == 0 && (dh / hd) % 4 == 0 && outer_agg_supported(L, C, H * hd)) return hd;
+  return 0;
+}
+
+// Tile side of the local origins (precision of the binomial expansion, which
+// loses about eps (|p| / cutoff)^L in fp32): cutoff * (8, 8, 8, 6, 4, 3, 2).
+constexpr double kTileCutoffs[kMaxL + 1] = {8.0, 8.0, 8.0, 6.0, 4.0, 3.0, 2.0};
+// With alpha / D^f the edge weights no longer damp that loss: tiles then have
+// a side of at most this many shortest-edge lengths, so that the largest
+// ratio (|p_i| + |p_j|) / |r_ij| stays below about 1 + 2.31 sqrt(3) = 5.
+constexpr double kYnormTileScale = 2.31;
+
+e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos, const int32_t* graph_id,
+                        const float* feat, int32_t n, const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges,
+                        const float* alpha, float* out, void* workspace, size_t workspace_bytes, void* stream,
+                        bool allow_upload) {
+  e2f_status rs = check_conv(ctx, p, pos, feat, n, row_ptr, col_idx, n_edges, out);
+  if (rs != E2F_OK) return rs;
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  const int L = p->lmax, C = p->channels, H = p->heads, nk = nk_of(L);
+  const e2f_ctx::CoefSet* cs = nullptr;
+  if ((rs = coef_of(ctx, L, path_weights(p), allow_upload, cs)) != E2F_OK) return rs;
+  const int hdiv = head_split(L, C, H);
+  if (hdiv < 1) return fail(E2F_EUNSUPPORTED, "no head split of width %d fits the aggregation", C / H);
+  const int Hv = H * hdiv, dv = C / Hv;
+  const int cgroups = outer_agg_groups(L, C, Hv);
+  const e2f_ctx::Couple* cpl = nullptr;
+  if (!allow_upload && ctx->couple.find(std::make_pair(L, cgroups)) == ctx->couple.end())
+    return fail(E2F_EINVAL, "the coupling schedule is not resident on the context; call e2f_wigner6j_prepare first");
+  if ((rs = couple_of(ctx, L, cgroups, cpl)) != E2F_OK) return rs;
+  if (n == 0) return E2F_OK;
+  const bool ynorm = p->y_norm != 0;
+  const FwdLayout f = fwd_layout(p, n, n_edges, alpha != nullptr);
+  if (n_edges > 0) {
+    if (!workspace) return fail(E2F_EINVAL, "workspace is NULL");
+    if ((uintptr_t)workspace % 256) return fail(E2F_EINVAL, "workspace must be 256-byte aligned");
+    const size_t need = f.total(std::min<int64_t>(n, kMinSlice));
+    if (workspace_bytes < need)
+      return fail(E2F_ECAPACITY, "workspace of %zu bytes is below the minimum %zu", workspace_bytes, need);
+  }
+  const DevTables t = with_coef(ctx, L, *cs);
+  if (n_edges == 0) {  // every receiver is isolated (a fill kernel, no memset: capture-safe)
+    E2F_HIP(launch_fill(out, (int64_t)n * nk * C, 0.0f, s));
+    ctx->last_slices = 0;
+    return E2F_OK;
+  }
+  char* ws = (char*)workspace;
+  int* stats = (int*)(ws + f.stats);
+  unsigned* dmin = (unsigned*)(ws + f.dmin);
+  TileGridDev* grid = (TileGridDev*)(ws + f.grid);
+  int32_t* tile_of = (int32_t*)(ws + f.tile_of);
+  int32_t* order = (int32_t*)(ws + f.order);
+  float* Re = (float*)(ws + f.Re);
+  double* Rr = (double*)(ws + f.Rr);
+  float* alpha_hm = (alpha || ynorm) ? (float*)(ws + f.alpha_hm) : nullptr;
+  float* y = p->mix_w ? (float*)(ws + f.y) : out;
+  float* S = (float*)(ws + f.S);
+  // ---- plan: bounding box, attention weights head-major (per filter degree
+  // under alpha / D^f, with the shortest edge), tile grid, receiver order,
+  // solid harmonics of the edges and receivers
+  E2F_TIMED("bbox", launch_plan_bbox(pos, graph_id, n, stats, ynorm ? dmin : nullptr, s));
+  if (ynorm) {
+    int32_t* erows = (int32_t*)(ws + f.erows);
+    E2F_TIMED("alpha_hm", launch_plan_edge_rows(row_ptr, n, n_edges, erows, s));
+    E2F_TIMED("alpha_hm", launch_plan_dmin(pos, erows, col_idx, n, n_edges, dmin, s));
+    E2F_TIMED("alpha_hm", launch_alpha_dnorm(pos, nullptr, col_idx, alpha, n, n_edges, H, L, erows, alpha_hm, s));
+  } else if (alpha) {
+    E2F_TIMED("alpha_hm", launch_alpha_head_major(alpha, n_edges, H, alpha_hm, s));
+  }
+  const double side = (p->tile_side > 0.0f ? (double)p->tile_side : kTileCutoffs[L] * (double)p->cutoff) * kGrid;
+  E2F_TIMED("tile_plan", launch_plan_grid(stats, ynorm ? dmin : nullptr, side, kYnormTileScale, graph_id != nullptr,
+                                          grid, s));
+  E2F_TIMED("tile_plan", launch_plan_order(pos, graph_id, n, grid, tile_of, (uint64_t*)(ws + f.keys),
+                                           (uint64_t*)(ws + f.keys_out), (int32_t*)(ws + f.vals), order,
+                                           ws + f.sort_tmp, f.sort_b, s));
+  E2F_TIMED("sh", launch_plan_sh(t, pos, row_ptr, col_idx, n, n_edges, tile_of, grid, Rr, Re, s));
+  // ---- aggregation and recouple per slice of receivers (S of one slice
+  // at a time in the workspace)
+  const int64_t slice = std::min<int64_t>(n, (int64_t)((workspace_bytes - f.fixed) / f.s_row));
+  int64_t slices = 0;
+  for (int64_t q0 = 0; q0 < n; q0 += slice, ++slices) {
+    const int nb = (int)std::min<int64_t>(slice, n - q0);
+    const int32_t* ord = order + q0;
+    if (!ynorm) {
+      E2F_TIMED("aggregate", launch_outer_agg(t, Re, row_ptr, col_idx, alpha_hm, n_edges, feat, ord, cpl->meta,
+                                              cpl->coef, cpl->pmeta, cpl->tab, cpl->ntab, cpl->k, cgroups, nb, C, Hv,
+                                              hdiv, n, S, s));
+      E2F_TIMED("recouple", launch_recouple(t, Rr, S, false, ord, nb, C, dv, y, s));
+      continue;
+    }
+    // S^(f) = sum_j alpha_ij D_ij^-f [h_j (x) R(p_j)] coupled, then the
+    // recouple terms of filter degree b + u = f; the f = 0 pass stores y,
+    // the others add
+    for (int fd = 0; fd <= L; ++fd) {
+      E2F_TIMED("aggregate", launch_outer_agg(t, Re, row_ptr, col_idx, alpha_hm + (size_t)fd * H * n_edges, n_edges,
+                                              feat, ord, cpl->meta, cpl->coef, cpl->pmeta, cpl->tab, cpl->ntab,
+                                              cpl->k, cgroups, nb, C, Hv, hdiv, n, S, s));
+      E2F_TIMED("recouple", launch_recouple(with_coef_f(ctx, L, *cs, fd), Rr, S, false, ord, nb, C, dv, y, s, fd > 0));
+    }
+  }
+  if (p->mix_w) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
+  ctx->last_slices = slices;
+  return E2F_OK;
+}
 }  // namespace
 
 extern "C" {
@@ -499,12 +703,10 @@ e2f_status e2f_create(int lmax_max, int device, e2f_ctx** out) {
   for (int L = 0; L <= lmax_max; ++L) ctx->host.push_back(build_layer_tables(L));
   ctx->dev.assign(lmax_max + 1, DevTables{});
   ctx->table_mem.assign(lmax_max + 1, nullptr);
-  ctx->coef_mem.assign(lmax_max + 1, nullptr);
-  ctx->coef_w.assign(lmax_max + 1, {});
+  ctx->coefs.assign(lmax_max + 1, {});
   ctx->rcf_k.assign(lmax_max + 1, {});
   ctx->rcf_off.assign(lmax_max + 1, {});
   ctx->rcf_meta.assign(lmax_max + 1, {});
-  ctx->rcf_coef.assign(lmax_max + 1, {});
   if (device >= 0) {
     int count = 0;
     if (hipGetDeviceCount(&count) != hipSuccess || device >= count) {
@@ -539,8 +741,9 @@ void e2f_destroy(e2f_ctx* ctx) {
     (void)hipDeviceSynchronize();
     for (void* p : ctx->table_mem)
       if (p) (void)hipFree(p);
-    for (void* p : ctx->coef_mem)
-      if (p) (void)hipFree(p);
+    for (auto& sets : ctx->coefs)
+      for (auto& c : sets)
+        if (c.mem) (void)hipFree(c.mem);
     for (Buf* b : {&ctx->a, &ctx->b, &ctx->c, &ctx->d})
       if (b->p) (void)hipFree(b->p);
     if (ctx->blas) (void)rocblas_destroy_handle(ctx->blas);
@@ -740,260 +943,59 @@ e2f_status e2f_node_tp(e2f_ctx* ctx, const float* pos, const float* origins, con
   return E2F_OK;
 }
 
+e2f_status e2f_wigner6j_workspace_size(e2f_ctx* ctx, const e2f_conv_params* p, int32_t n, int64_t n_edges,
+                                       size_t* bytes) {
+  if (!bytes) return fail(E2F_EINVAL, "bytes is NULL");
+  if (e2f_status rs = check_params(ctx, p); rs != E2F_OK) return rs;
+  if (n < 0 || n_edges < 0) return fail(E2F_EINVAL, "n or n_edges < 0");
+  *bytes = fwd_layout(p, n, n_edges, true).total(n);
+  return E2F_OK;
+}
+
+e2f_status e2f_wigner6j_workspace_min(e2f_ctx* ctx, const e2f_conv_params* p, int32_t n, int64_t n_edges,
+                                      size_t* bytes) {
+  if (!bytes) return fail(E2F_EINVAL, "bytes is NULL");
+  if (e2f_status rs = check_params(ctx, p); rs != E2F_OK) return rs;
+  if (n < 0 || n_edges < 0) return fail(E2F_EINVAL, "n or n_edges < 0");
+  *bytes = fwd_layout(p, n, n_edges, true).total(std::min<int64_t>(n, kMinSlice));
+  return E2F_OK;
+}
+
+e2f_status e2f_wigner6j_prepare(e2f_ctx* ctx, const e2f_conv_params* p) {
+  if (e2f_status rs = check_params(ctx, p); rs != E2F_OK) return rs;
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  DeviceGuard g(ctx->device);
+  const e2f_ctx::CoefSet* cs = nullptr;
+  if (e2f_status rs = coef_of(ctx, p->lmax, path_weights(p), true, cs); rs != E2F_OK) return rs;
+  const int hdiv = head_split(p->lmax, p->channels, p->heads);
+  if (hdiv < 1) return fail(E2F_EUNSUPPORTED, "no head split of width %d fits the aggregation", p->channels / p->heads);
+  const e2f_ctx::Couple* cpl = nullptr;
+  return couple_of(ctx, p->lmax, outer_agg_groups(p->lmax, p->channels, p->heads * hdiv), cpl);
+}
+
 e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos,
                                      const int32_t* graph_id, const float* feat, int32_t n, const int64_t* row_ptr,
                                      const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,
-                                     void* stream) {
-  e2f_status rs = check_conv(ctx, p, pos, feat, n, row_ptr, col_idx, n_edges, out);
-  if (rs != E2F_OK) return rs;
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  return forward_impl(ctx, p, pos, graph_id, feat, n, row_ptr, col_idx, n_edges, alpha, out, workspace,
+                      workspace_bytes, stream, true);
+}
+
+e2f_status e2f_validate_graph(e2f_ctx* ctx, int32_t n, const int64_t* row_ptr, const int32_t* col_idx,
+                              int64_t n_edges, int32_t* bad, void* stream) {
+  if (!ctx || !bad) return fail(E2F_EINVAL, "ctx and bad are required");
+  if (n < 0 || n_edges < 0) return fail(E2F_EINVAL, "n or n_edges < 0");
+  if (!row_ptr) return fail(E2F_EINVAL, "row_ptr is required");
+  if (n_edges > 0 && !col_idx) return fail(E2F_EINVAL, "col_idx is NULL with n_edges > 0");
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
   hipStream_t s = (hipStream_t)stream;
   DeviceGuard g(ctx->device);
-  const int L = p->lmax, C = p->channels, nk = nk_of(L);
-  rs = set_weights(ctx, L, path_weights(p), s);
-  if (rs != E2F_OK) return rs;
-  if (n == 0) return E2F_OK;
-  if (n_edges == 0) {
-    E2F_HIP(hipMemsetAsync(out, 0, sizeof(float) * (size_t)n * nk * C, s));
-    return E2F_OK;
-  }
-  const DevTables& t = ctx->dev[L];
-  int st[kStatsInts];
-  rs = run_bbox(ctx, pos, graph_id, n, s, st);
-  if (rs != E2F_OK) return rs;
-  // ---- tile grid (local origins; precision of the binomial expansion)
-  TilePlan tp;
-  // fp32 T and S lose about eps * (|p| / cutoff)^L in the binomial expansion, so
-  // the default tile (whose centre is the local origin) shrinks with L
-  static const double kTileCutoffs[kMaxL + 1] = {8.0, 8.0, 8.0, 6.0, 4.0, 3.0, 2.0};
-  const double side = (p->tile_side > 0.0f ? (double)p->tile_side : kTileCutoffs[L] * (double)p->cutoff) * kGrid;
-  tp.ncell = 1;
-  for (int k = 0; k < 3; ++k) {
-    tp.lo[k] = st[k];
-    tp.span[k] = (int64_t)st[3 + k] - st[k] + 1;
-    int64_t d = (int64_t)std::ceil((double)tp.span[k] / side);
-    d = std::max<int64_t>(1, std::min<int64_t>(d, 64));
-    tp.dim[k] = (int)d;
-    tp.ncell *= tp.dim[k];
-  }
-  tp.n_graphs = graph_id ? (int64_t)st[6] + 1 : 1;
-  const int64_t keys = tp.n_graphs * tp.ncell;
-  const int64_t count = keys * (int64_t)n;
-  if (count > std::numeric_limits<int32_t>::max() - 1)
-    return fail(E2F_EUNSUPPORTED, "tile plan of %lld graph-tiles x %d atoms exceeds 2^31", (long long)keys, n);
-  ctx->origins_host.assign((size_t)3 * tp.ncell, 0.0);
-  for (int cz = 0; cz < tp.dim[2]; ++cz)
-    for (int cy = 0; cy < tp.dim[1]; ++cy)
-      for (int cx = 0; cx < tp.dim[0]; ++cx) {
-        const int c[3] = {cx, cy, cz};
-        const int cell = (cz * tp.dim[1] + cy) * tp.dim[0] + cx;
-        for (int k = 0; k < 3; ++k) {
-          const int64_t og = tp.lo[k] + ((2 * (int64_t)c[k] + 1) * tp.span[k]) / (2 * (int64_t)tp.dim[k]);
-          ctx->origins_host[3 * cell + k] = (double)og / kGrid;
-        }
-      }
-  const size_t scan_b = std::max(scan_tmp_bytes(count), blocks_tmp_bytes((int)keys + 1));
-  const size_t sort_b = recv_sort_tmp_bytes(n);
-  size_t need_a = al256(sizeof(int32_t) * (size_t)n) + 2 * al256(sizeof(int32_t) * (size_t)count) + al256(scan_b) +
-                  al256(sizeof(double) * ctx->origins_host.size()) + 2 * al256(sizeof(uint64_t) * (size_t)n) +
-                  2 * al256(sizeof(int32_t) * (size_t)n) + al256(sort_b) + 3 * al256(sizeof(int32_t) * (keys + 1)) +
-                  al256(sizeof(int32_t) * (3 + 2 * ((size_t)keys + 1)));
-  rs = ensure(ctx, ctx->a, need_a, s);
-  if (rs != E2F_OK) return rs;
-  Carver ca{(char*)ctx->a.p};
-  int32_t* tile_of = ca.take<int32_t>(n);
-  int32_t* flags = ca.take<int32_t>((size_t)count);
-  int32_t* pidx = ca.take<int32_t>((size_t)count);
-  void* scan_tmp = ca.take<char>(scan_b);
-  double* origins = ca.take<double>(ctx->origins_host.size());
-  uint64_t* rkeys = ca.take<uint64_t>(n);
-  uint64_t* rkeys_out = ca.take<uint64_t>(n);
-  int32_t* rvals = ca.take<int32_t>(n);
-  int32_t* order = ca.take<int32_t>(n);
-  void* sort_tmp = ca.take<char>(sort_b);
-  int32_t* key_count = ca.take<int32_t>(keys + 1);
-  int32_t* rstart_d = ca.take<int32_t>(keys + 1);
-  int32_t* pstart_d = ca.take<int32_t>(keys + 1);
-  int32_t* plan_d = ca.take<int32_t>(3 + 2 * ((size_t)keys + 1));
-  E2F_HIP(hipMemcpyAsync(origins, ctx->origins_host.data(), sizeof(double) * ctx->origins_host.size(),
-                         hipMemcpyHostToDevice, s));
-  E2F_TIMED("tile_plan", launch_tile_keys(pos, graph_id, n, tp.lo, tp.dim, tp.span, tp.ncell, tile_of, s));
-  E2F_HIP(hipMemsetAsync(flags, 0, sizeof(int32_t) * (size_t)count, s));
-  E2F_TIMED("tile_plan", launch_pair_flags(row_ptr, col_idx, tile_of, n, flags, ctx->stats + 8, s));
-  // receivers in (tile, spatial) order: fine cells of 4 A give the L2 reuse of the aggregation
-  E2F_TIMED("tile_plan", launch_sort_receivers(pos, tile_of, n, tp.lo, (int64_t)(4.0 * kGrid), rkeys, rkeys_out,
-                                               rvals, order, sort_tmp, sort_b, s));
-  E2F_TIMED("tile_plan", launch_scan_i32(flags, pidx, count, scan_tmp, scan_b, s));
-  E2F_TIMED("tile_plan", launch_tile_ranges(tile_of, pidx, n, (int)keys, key_count, rstart_d, pstart_d, scan_tmp,
-                                            scan_b, s));
-  // one read-back of the plan sizes: last pair index and flag, largest degree,
-  // receiver and pair starts of every tile
-  const size_t plan_n = 3 + 2 * ((size_t)keys + 1);
-  if (ctx->pinned_plan_n < plan_n) {
-    if (ctx->pinned_plan) (void)hipHostFree(ctx->pinned_plan);
-    ctx->pinned_plan = nullptr;
-    ctx->pinned_plan_n = 0;
-    if (hipHostMalloc((void**)&ctx->pinned_plan, sizeof(int32_t) * plan_n, hipHostMallocDefault) != hipSuccess)
-      return fail(E2F_ENOMEM, "pinned allocation failed");
-    ctx->pinned_plan_n = plan_n;
-  }
-  E2F_TIMED("tile_plan", launch_plan_pack(pidx, flags, count, ctx->stats + 8, rstart_d, pstart_d, (int)keys, plan_d, s));
-  E2F_HIP(hipMemcpyAsync(ctx->pinned_plan, plan_d, sizeof(int32_t) * plan_n, hipMemcpyDeviceToHost, s));
+  E2F_HIP(launch_validate_graph(row_ptr, col_idx, n, n_edges, ctx->stats + 16, s));
+  E2F_HIP(hipMemcpyAsync(ctx->pinned, ctx->stats + 16, sizeof(int), hipMemcpyDeviceToHost, s));
   E2F_HIP(hipStreamSynchronize(s));
-  const int32_t* pp = ctx->pinned_plan;
-  const int32_t last_idx = pp[0], last_flag = pp[1], max_degree = pp[2];
-  std::vector<int32_t> rstart(pp + 3, pp + 3 + keys + 1), pstart(pp + 4 + keys, pp + 4 + 2 * keys + 1);
-  const int64_t P = (int64_t)last_idx + last_flag;
-  pstart[keys] = (int32_t)P;
-  ctx->last_pairs = P;
-  ctx->last_tiles = keys;
-  // the MFMA aggregation over receiver blocks of 16 needs 16 * degree <= 8192
-  const bool use_blocks = max_degree <= kBlockMaxDegree;
-  // alpha / D^f: one aggregation per filter degree f
-  const bool ynorm = p->y_norm != 0;
-  // aggregation of the uncoupled node products (no T); E2F_AGG_T selects the
-  // T-row aggregation over receiver blocks instead (comparison)
-  const char* agg_t = getenv("E2F_AGG_T");  // read per call
-  const bool force_t = agg_t && atoi(agg_t) != 0;
-  const bool outer = !force_t && outer_agg_supported(L, C, p->heads);
-  // S buffers: with the T rows, one per filter degree under y_norm (all the
-  // aggregations run before the recouples); the reordered aggregation reuses
-  // one (aggregation and recouple of each degree in turn)
-  const int nS = ynorm && !outer ? L + 1 : 1;
-  const int nA = ynorm ? L + 1 : 1;  // head-major attention weights per filter degree
-  if (ynorm && !outer && !use_blocks)
-    return fail(E2F_EUNSUPPORTED, "y_norm needs every degree <= %d (largest %d)", kBlockMaxDegree, max_degree);
-  // ---- tile batches: T and S of a batch must fit the memory budget
-  const size_t row_bytes = sizeof(float) * (size_t)t.dimT * C;
-  size_t free_b = 0, total_b = 0;
-  E2F_HIP(hipMemGetInfo(&free_b, &total_b));
-  size_t budget = std::min<size_t>((size_t)96 << 30, (free_b + ctx->b.n + ctx->c.n) / 10 * 6);
-  if (const char* cap = getenv("E2F_TILE_BUDGET_MB")) budget = (size_t)atoll(cap) << 20;
-  struct Batch {
-    int t0, t1;
-  };
-  std::vector<Batch> batches;
-  int64_t max_pairs = 0, max_recv = 0;
-  for (int t0 = 0; t0 < (int)keys;) {
-    int t1 = t0 + 1;
-    auto cost = [&](int a, int b) {
-      return (size_t)((outer ? 0 : (int64_t)(pstart[b] - pstart[a])) + (int64_t)nS * (rstart[b] - rstart[a])) *
-             row_bytes;
-    };
-    while (t1 < (int)keys && cost(t0, t1 + 1) <= budget) ++t1;
-    batches.push_back({t0, t1});
-    max_pairs = std::max<int64_t>(max_pairs, pstart[t1] - pstart[t0]);
-    max_recv = std::max<int64_t>(max_recv, rstart[t1] - rstart[t0]);
-    t0 = t1;
-  }
-  const int nblk = (int)((max_recv + 15) / 16);
-  const size_t blk_tmp_b = blocks_tmp_bytes(nblk);
-  // ---- phase 2 buffers
-  const bool mixing = p->mix_w != nullptr;
-  const size_t need_b = 2 * al256(sizeof(int32_t) * (size_t)P) + 3 * al256(sizeof(int32_t) * (size_t)n_edges) +
-                        3 * al256(sizeof(int32_t) * (size_t)(nblk + 1)) + al256(blk_tmp_b) +
-                        al256((outer ? sizeof(float) : sizeof(double)) * (size_t)P * nk) +
-                        (outer ? al256(sizeof(float) * (size_t)n_edges * nk) : 0) +
-                        al256(sizeof(double) * (size_t)n * nk) +
-                        (outer ? 0 : al256(row_bytes * (size_t)max_pairs)) + al256(row_bytes * (size_t)max_recv * nS) +
-                        (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0) +
-                        ((use_blocks || outer) && (alpha || ynorm) ? al256(sizeof(float) * (size_t)n_edges * p->heads * nA)
-                                                                   : 0) +
-                        (ynorm ? al256(sizeof(int32_t) * (size_t)n_edges) : 0);
-  rs = ensure(ctx, ctx->b, need_b, s);
-  if (rs != E2F_OK) return rs;
-  Carver cb{(char*)ctx->b.p};
-  int32_t* pair_node = cb.take<int32_t>((size_t)P);
-  int32_t* pair_tile = cb.take<int32_t>((size_t)P);
-  int32_t* col_pair = cb.take<int32_t>((size_t)n_edges);
-  int32_t* uni = cb.take<int32_t>((size_t)n_edges);
-  int32_t* edge_slot = cb.take<int32_t>((size_t)n_edges);
-  int32_t* blk_count = cb.take<int32_t>((size_t)nblk + 1);
-  int32_t* blk_off = cb.take<int32_t>((size_t)nblk + 1);
-  int32_t* ucount = cb.take<int32_t>((size_t)nblk + 1);
-  void* blk_tmp = cb.take<char>(blk_tmp_b);
-  double* Rp = outer ? nullptr : cb.take<double>((size_t)P * nk);
-  float* Rpf = outer ? cb.take<float>((size_t)P * nk) : nullptr;  // the outer-product aggregation reads fp32
-  float* Re = outer ? cb.take<float>((size_t)n_edges * nk) : nullptr;  // ... per edge
-  double* Rr = cb.take<double>((size_t)n * nk);
-  float* T = outer ? nullptr : cb.take<float>((size_t)max_pairs * t.dimT * C);
-  float* S = cb.take<float>((size_t)max_recv * t.dimT * C * nS);
-  float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
-  float* alpha_hm =
-      (use_blocks || outer) && (alpha || ynorm) ? cb.take<float>((size_t)n_edges * p->heads * nA) : nullptr;
-  if (ynorm) {
-    int32_t* erows = cb.take<int32_t>((size_t)n_edges);
-    E2F_TIMED("alpha_hm", launch_alpha_dnorm(pos, row_ptr, col_idx, alpha, n, n_edges, p->heads, L, erows, alpha_hm, s));
-  } else if (alpha_hm) {
-    E2F_TIMED("alpha_hm", launch_alpha_head_major(alpha, n_edges, p->heads, alpha_hm, s));
-  }
-  E2F_TIMED("tile_plan", launch_pairs(flags, pidx, count, n, pair_node, pair_tile, s));
-  if (!outer) E2F_TIMED("tile_plan", launch_col_pair(row_ptr, col_idx, tile_of, pidx, n, col_pair, s));
-  E2F_TIMED("sh", launch_sh(t, pos, pair_node, origins, nullptr, pair_tile, tp.ncell, (int)P, Rp, Rpf, s));
-  E2F_TIMED("sh", launch_sh(t, pos, nullptr, origins, nullptr, tile_of, tp.ncell, n, Rr, nullptr, s));
-  if (outer) E2F_TIMED("sh", launch_edge_R(row_ptr, col_idx, tile_of, pidx, n, Rpf, nk, Re, s));
-  const int dh = C / p->heads;
-  const int cgroups = outer ? outer_agg_groups(L, C, p->heads) : 0;
-  const e2f_ctx::Couple* cpl = nullptr;
-  if (outer && (rs = couple_of(ctx, L, cgroups, cpl)) != E2F_OK) return rs;
-  for (const Batch& bt : batches) {
-    const int p0 = pstart[bt.t0], q0 = rstart[bt.t0];
-    const int pb = pstart[bt.t1] - p0, nb = rstart[bt.t1] - q0;
-    if (nb == 0) continue;
-    const int32_t* ord = order + q0;
-    if (outer && !ynorm) {
-      E2F_TIMED("aggregate", launch_outer_agg(t, Re, row_ptr, col_idx, alpha_hm, n_edges, feat, ord,
-                                              cpl->meta, cpl->coef, cpl->pmeta, cpl->tab, cpl->ntab, cpl->k,
-                                              cgroups, nb, C, p->heads, S, s));
-      E2F_TIMED("recouple", launch_recouple(t, Rr, S, false, ord, nb, C, dh, y, s));
-      continue;
-    }
-    if (outer) {
-      // S^(f) = sum_j alpha_ij D_ij^-f [h_j (x) R(p_j)] coupled, then the
-      // recouple terms of filter degree b + u = f; the f = 0 pass stores y,
-      // the others add
-      for (int f = 0; f <= L; ++f) {
-        E2F_TIMED("aggregate", launch_outer_agg(t, Re, row_ptr, col_idx, alpha_hm + (size_t)f * p->heads * n_edges,
-                                                n_edges, feat, ord, cpl->meta, cpl->coef, cpl->pmeta, cpl->tab,
-                                                cpl->ntab, cpl->k, cgroups, nb, C, p->heads, S, s));
-        DevTables tf = t;
-        tf.rc_k = ctx->rcf_k[L][f];
-        tf.rc_off = ctx->rcf_off[L][f];
-        tf.rc_meta = ctx->rcf_meta[L][f];
-        tf.rc_coef = ctx->rcf_coef[L][f];
-        E2F_TIMED("recouple", launch_recouple(tf, Rr, S, false, ord, nb, C, dh, y, s, f > 0));
-      }
-      continue;
-    }
-    E2F_TIMED("node_tp", launch_node_tp(t, Rp + (size_t)p0 * nk, pair_node + p0, feat, pb, C, dh, T, s));
-    if (use_blocks) {
-      E2F_TIMED("tile_plan", launch_block_union(row_ptr, col_pair, ord, nb, blk_count, blk_off, uni, ucount,
-                                                edge_slot, blk_tmp, blk_tmp_b, s));
-    }
-    if (!ynorm) {
-      E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, alpha, alpha_hm, n_edges, n, ord, uni,
-                                              blk_off, ucount, edge_slot, use_blocks, nb, t.dimT, C, p->heads, S, s));
-      E2F_TIMED("recouple", launch_recouple(t, Rr, S, false, ord, nb, C, dh, y, s));
-    } else {
-      // S^(f) = sum_j alpha_ij D_ij^-f T_j, and the recouple terms of filter
-      // degree b + u = f read S^(f); the f = 0 pass stores y, the others add
-      const size_t sstride = (size_t)max_recv * t.dimT * C;
-      for (int f = 0; f <= L; ++f)
-        E2F_TIMED("aggregate", launch_aggregate(T, p0, row_ptr, col_pair, nullptr,
-                                                alpha_hm + (size_t)f * p->heads * n_edges, n_edges, n, ord, uni,
-                                                blk_off, ucount, edge_slot, true, nb, t.dimT, C, p->heads,
-                                                S + f * sstride, s));
-      for (int f = 0; f <= L; ++f) {
-        DevTables tf = t;
-        tf.rc_k = ctx->rcf_k[L][f];
-        tf.rc_off = ctx->rcf_off[L][f];
-        tf.rc_meta = ctx->rcf_meta[L][f];
-        tf.rc_coef = ctx->rcf_coef[L][f];
-        E2F_TIMED("recouple", launch_recouple(tf, Rr, S + f * sstride, false, ord, nb, C, dh, y, s, f > 0));
-      }
-    }
-  }
-  if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
-  ctx->last_batches = (int64_t)batches.size();
+  int v = 0;
+  std::memcpy(&v, ctx->pinned, sizeof(int));
+  *bad = v;
   return E2F_OK;
 }
 
@@ -1007,11 +1009,11 @@ e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, cons
   hipStream_t s = (hipStream_t)stream;
   DeviceGuard g(ctx->device);
   const int L = p->lmax, C = p->channels, nk = nk_of(L);
-  rs = set_weights(ctx, L, path_weights(p), s);
-  if (rs != E2F_OK) return rs;
+  const e2f_ctx::CoefSet* cs = nullptr;
+  if ((rs = coef_of(ctx, L, path_weights(p), true, cs)) != E2F_OK) return rs;
   if (n == 0) return E2F_OK;
   if (n_edges == 0) {
-    E2F_HIP(hipMemsetAsync(out, 0, sizeof(float) * (size_t)n * nk * C, s));
+    E2F_HIP(launch_fill(out, (int64_t)n * nk * C, 0.0f, s));
     return E2F_OK;
   }
   const bool mixing = p->mix_w != nullptr;
@@ -1021,8 +1023,8 @@ e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, cons
     if (rs != E2F_OK) return rs;
     y = (float*)ctx->c.p;
   }
-  E2F_TIMED("edge_tp", launch_edge_tp(ctx->dev[L], pos, feat, row_ptr, col_idx, alpha, n, C, p->heads, y, s,
-                                      p->y_norm != 0));
+  E2F_TIMED("edge_tp", launch_edge_tp(with_coef(ctx, L, *cs), pos, feat, row_ptr, col_idx, alpha, n, n_edges, C,
+                                      p->heads, y, s, p->y_norm != 0));
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
   return E2F_OK;
 }
@@ -1045,8 +1047,9 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
   DeviceGuard g(ctx->device);
   const int L = p->lmax, C = p->channels, H = p->heads, nk = nk_of(L), L1 = L + 1;
   const std::vector<double> w = path_weights(p);
-  rs = set_weights(ctx, L, w, s);
-  if (rs != E2F_OK) return rs;
+  const e2f_ctx::CoefSet* cs = nullptr;
+  if ((rs = coef_of(ctx, L, w, true, cs)) != E2F_OK) return rs;
+  const DevTables tw = with_coef(ctx, L, *cs);
   if (n == 0) return E2F_OK;
   const bool mixing = p->mix_w != nullptr;
   const size_t wt_bytes = (size_t)L1 * C * C * (p->mix_dtype == E2F_BF16 ? 2 : 4);
@@ -1104,11 +1107,11 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
   // (receiver, head); then per atom the forces received minus those sent
   float* gedge = grad_pos ? cd.take<float>((size_t)n_edges * 3) : nullptr;
   float* Gt = gt_bytes ? cd.take<float>(gt_bytes / sizeof(float)) : nullptr;
-  if (Gt) E2F_TIMED("edge_geom", launch_edge_shgrad(ctx->dev[L], pos, rows, col_idx, n_edges, Gt, s));
+  if (Gt) E2F_TIMED("edge_geom", launch_edge_shgrad(tw, pos, rows, col_idx, n_edges, Gt, s));
   if (grad_alpha || gedge) {
     const e2f_ctx::Geom* gsch = nullptr;
     if ((rs = geom_of(ctx, L, C / H, gsch)) != E2F_OK) return rs;
-    E2F_TIMED("edge_geom", launch_edge_geom(ctx->dev[L], pos, feat, gy, row_ptr, col_idx, alpha, n, C, H, gsch->qc,
+    E2F_TIMED("edge_geom", launch_edge_geom(tw, pos, feat, gy, row_ptr, col_idx, alpha, n, C, H, gsch->qc,
                                             gsch->meta, gsch->unit, gsch->oc, gsch->tot, Gt, n_edges, grad_alpha,
                                             gedge, s));
   }
@@ -1129,8 +1132,12 @@ e2f_status e2f_wigner6j_conv_backward(e2f_ctx* ctx, const e2f_conv_params* p, co
     e2f_conv_params pt = *p;
     pt.path_w = wt.data();
     pt.mix_w = nullptr;
-    return e2f_wigner6j_conv_forward(ctx, &pt, pos, graph_id, gy, n, rowT, colT, n_edges, alpha ? alphaT : nullptr,
-                                     grad_feat, stream);
+    // the forward on the transposed graph, in a workspace of the context's
+    // own (the backward's buffers, which it reads, stay where they are)
+    const size_t fb = fwd_layout(&pt, n, n_edges, alpha != nullptr).total(n);
+    if ((rs = ensure(ctx, ctx->c, fb, s)) != E2F_OK) return rs;
+    return forward_impl(ctx, &pt, pos, graph_id, gy, n, rowT, colT, n_edges, alpha ? alphaT : nullptr, grad_feat,
+                        ctx->c.p, ctx->c.n, stream, true);
   }
   return E2F_OK;
 }
@@ -1148,10 +1155,10 @@ e2f_status e2f_wigner6j_conv_forward_dense(e2f_ctx* ctx, const e2f_conv_params* 
   hipStream_t s = (hipStream_t)stream;
   DeviceGuard g(ctx->device);
   const int L = p->lmax, C = p->channels, H = p->heads, nk = nk_of(L), dh = C / H;
-  rs = set_weights(ctx, L, path_weights(p), s);
-  if (rs != E2F_OK) return rs;
+  const e2f_ctx::CoefSet* cs = nullptr;
+  if ((rs = coef_of(ctx, L, path_weights(p), true, cs)) != E2F_OK) return rs;
   if (n == 0) return E2F_OK;
-  const DevTables& t = ctx->dev[L];
+  const DevTables t = with_coef(ctx, L, *cs);
   int st[kStatsInts];
   rs = run_bbox(ctx, pos, nullptr, n, s, st);
   if (rs != E2F_OK) return rs;
@@ -1214,10 +1221,10 @@ e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params*
   hipStream_t s = (hipStream_t)stream;
   DeviceGuard g(ctx->device);
   const int L = p->lmax, C = p->channels, nk = nk_of(L), dh = C / p->heads;
-  rs = set_weights(ctx, L, path_weights(p), s);
-  if (rs != E2F_OK) return rs;
+  const e2f_ctx::CoefSet* cs = nullptr;
+  if ((rs = coef_of(ctx, L, path_weights(p), true, cs)) != E2F_OK) return rs;
   if (n == 0) return E2F_OK;
-  const DevTables& t = ctx->dev[L];
+  const DevTables t = with_coef(ctx, L, *cs);
   int st[kStatsInts];
   rs = run_bbox(ctx, pos, nullptr, n, s, st);
   if (rs != E2F_OK) return rs;
@@ -1253,10 +1260,9 @@ e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params*
   return E2F_OK;
 }
 
-e2f_status e2f_last_plan(const e2f_ctx* ctx, int64_t* pairs, int64_t* tiles) {
-  if (!ctx || !pairs || !tiles) return fail(E2F_EINVAL, "ctx, pairs and tiles are required");
-  *pairs = ctx->last_pairs;
-  *tiles = ctx->last_tiles;
+e2f_status e2f_last_slices(const e2f_ctx* ctx, int64_t* slices) {
+  if (!ctx || !slices) return fail(E2F_EINVAL, "ctx and slices are required");
+  *slices = ctx->last_slices;
   return E2F_OK;
 }
 

@@ -675,7 +675,8 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
                                                     const int* __restrict__ cmeta, const float* __restrict__ ccoef,
                                                     const int* __restrict__ pmeta, const float* __restrict__ ptab,
                                                     int ntab, int ck, int cgroups, int work_floats, int n, int nrx,
-                                                    int rpw, int C, int H, float* __restrict__ S) {
+                                                    int rpw, int C, int H, int hdiv, int n_nodes,
+                                                    float* __restrict__ S) {
   constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
   constexpr int EC = kOuterEdges;
   extern __shared__ float sm[];
@@ -729,7 +730,11 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int w = 0; w < NTWM; ++w) acc[mt][w] = (v4f){0.f, 0.f, 0.f, 0.f};
-  const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+  // row bounds clamped to [0, E] (a malformed graph cannot move a read
+  // outside the caller's buffers)
+  const int64_t rb0 = row_ptr[i], rb1 = row_ptr[i + 1];
+  const int64_t e0 = rb0 < 0 ? 0 : (rb0 > n_edges ? n_edges : rb0);
+  const int64_t e1 = rb1 < e0 ? e0 : (rb1 > n_edges ? n_edges : rb1);
   __syncthreads();  // the previous receiver's coupling has read G (and the schedule is staged)
   for (int64_t c0 = e0; c0 < e1; c0 += EC) {
     const int ne = (int)min((int64_t)EC, e1 - c0);
@@ -740,7 +745,8 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
     // in flight, loads before stores
     const int ns = (ne + 3) / 4, nsl = 4 * ns * MP;
     // the chunk's senders (blockDim >= EC), loaded with the staging's first round
-    const int jv = threadIdx.x < EC ? col[c0 + ((int)threadIdx.x < ne ? threadIdx.x : 0)] : 0;
+    int jv = threadIdx.x < EC ? col[c0 + ((int)threadIdx.x < ne ? threadIdx.x : 0)] : 0;
+    jv = (unsigned)jv < (unsigned)n_nodes ? jv : 0;
     for (int base = threadIdx.x; base < nsl; base += 4 * blockDim.x) {
       // branch-free: clamped indices, all loads of a round (alpha and R of
       // the edge, both addressed by the edge) issued before the first use
@@ -751,7 +757,7 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
         const int idx = base + u * blockDim.x, nb = idx / MP, be = idx % MP;
         okv[u] = idx < nsl && nb < ne && be < NK;
         const int64_t e = c0 + (nb < ne ? nb : 0);
-        av[u] = alpha_hm ? alpha_hm[(int64_t)h * n_edges + e] : 1.0f;
+        av[u] = alpha_hm ? alpha_hm[(int64_t)(h / hdiv) * n_edges + e] : 1.0f;
         rv[u] = Re[(size_t)e * NK + (be < NK ? be : 0)];
       }
 #pragma unroll
@@ -1518,11 +1524,12 @@ __global__ void k_global_couple(DevTables t, const double* __restrict__ G64, int
 // Per-degree attention weights alpha / D^f (Alg. 1), D = |r_i - r_j| in
 // float64, head-major per f: alpha_f[(f*H + h)*E + e]; 0 for f > 0 at D = 0.
 __global__ void k_alpha_dnorm(const float* __restrict__ pos, const int32_t* __restrict__ rows,
-                              const int32_t* __restrict__ col, const float* __restrict__ alpha, int64_t n_edges,
-                              int H, int L, float* __restrict__ alpha_f) {
+                              const int32_t* __restrict__ col, const float* __restrict__ alpha, int n,
+                              int64_t n_edges, int H, int L, float* __restrict__ alpha_f) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= n_edges) return;
-  const int i = rows[e], j = col[e];
+  const int i0 = rows[e], j0 = col[e];
+  const int i = (unsigned)i0 < (unsigned)n ? i0 : 0, j = (unsigned)j0 < (unsigned)n ? j0 : 0;
   const double dx = (double)pos[3 * i] - pos[3 * j], dy = (double)pos[3 * i + 1] - pos[3 * j + 1],
                dz = (double)pos[3 * i + 2] - pos[3 * j + 2];
   const double D = sqrt(dx * dx + dy * dy + dz * dz);
@@ -1557,7 +1564,8 @@ template <int L>
 __global__ __launch_bounds__(128) void k_edge_tp(DevTables t, const float* __restrict__ pos,
                                                  const float* __restrict__ feat, const int64_t* __restrict__ row_ptr,
                                                  const int32_t* __restrict__ col, const float* __restrict__ alpha,
-                                                 int C, int H, bool y_norm, float* __restrict__ y) {
+                                                 int C, int H, bool y_norm, int n_nodes, int64_t n_edges,
+                                                 float* __restrict__ y) {
   constexpr int NK = (L + 1) * (L + 1);
   constexpr int EB = 4;
   extern __shared__ float sm[];
@@ -1565,7 +1573,15 @@ __global__ __launch_bounds__(128) void k_edge_tp(DevTables t, const float* __res
   float* Rl = sm + EB * NK * NK;  // [EB][NK]
   const int i = blockIdx.x;
   const int dh = C / H;
-  const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+  // row bounds clamped to [0, E], senders to [0, n): a malformed graph
+  // cannot move a read outside the caller's buffers
+  const int64_t rb0 = row_ptr[i], rb1 = row_ptr[i + 1];
+  const int64_t e0 = rb0 < 0 ? 0 : (rb0 > n_edges ? n_edges : rb0);
+  const int64_t e1 = rb1 < e0 ? e0 : (rb1 > n_edges ? n_edges : rb1);
+  auto sender = [&](int64_t e) {
+    const int j = col[e];
+    return (unsigned)j < (unsigned)n_nodes ? j : 0;
+  };
   const float xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
   for (int c0 = 0; c0 < C; c0 += blockDim.x) {
     const int c = c0 + threadIdx.x;
@@ -1578,7 +1594,7 @@ __global__ __launch_bounds__(128) void k_edge_tp(DevTables t, const float* __res
       __syncthreads();
       for (int q = threadIdx.x; q < nb * NK; q += blockDim.x) {
         const int b = q / NK, k = q % NK;
-        const int j = col[eb + b];
+        const int j = sender(eb + b);
         float dx = xi - pos[3 * j], dy = yi - pos[3 * j + 1], dz = zi - pos[3 * j + 2];
         if (y_norm) {  // R^(f)(r / D) = R^(f)(r) / D^f; the zero vector at D = 0
           const float D = sqrtf(dx * dx + dy * dy + dz * dz);
@@ -1597,7 +1613,7 @@ __global__ __launch_bounds__(128) void k_edge_tp(DevTables t, const float* __res
       __syncthreads();
       if (live) {
         for (int b = 0; b < nb; ++b) {
-          const int j = col[eb + b];
+          const int j = sender(eb + b);
           const float a = alpha ? alpha[(eb + b) * H + c / dh] : 1.0f;
           float h[NK];
 #pragma unroll
@@ -1897,8 +1913,8 @@ bool outer_agg_supported(int L, int C, int H) {
 hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* row_ptr, const int32_t* col,
                             const float* alpha_hm, int64_t n_edges, const float* feat,
                             const int32_t* order, const int* cmeta, const float* ccoef, const int* pmeta,
-                            const float* ptab, int ntab, int ck, int cgroups, int n, int C, int H, float* S,
-                            hipStream_t s) {
+                            const float* ptab, int ntab, int ck, int cgroups, int n, int C, int H, int hdiv,
+                            int n_nodes, float* S, hipStream_t s) {
   if (n == 0) return hipSuccess;
   if (!outer_agg_supported(t.L, C, H) || cgroups != outer_agg_groups(t.L, C, H)) return hipErrorInvalidValue;
   const OuterShape o = outer_shape(t.L, C, H);
@@ -1938,7 +1954,7 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* 
                                                                       alpha_hm, n_edges, feat, order, cmeta, \
                                                                       ccoef, pmeta, ptab, ntab_k, ck,        \
                                                                       cgroups, work_floats, n, nrx, rpw, C,  \
-                                                                      H, S);                                 \
+                                                                      H, hdiv, n_nodes, S);                  \
     break;
 #define E2F_CASES(LL) E2F_CASE(LL, 4, 512) E2F_CASE(LL, 4, 1024)
     E2F_CASES(0) E2F_CASES(1) E2F_CASES(2) E2F_CASES(3) E2F_CASES(4) E2F_CASES(5) E2F_CASES(6)
@@ -2011,7 +2027,8 @@ hipError_t launch_mix(int L, const float* y, const void* W, bool w_bf16, int n, 
 }
 
 hipError_t launch_edge_tp(const DevTables& t, const float* pos, const float* feat, const int64_t* row_ptr,
-                          const int32_t* col_idx, const float* alpha, int n, int C, int H, float* y, hipStream_t s, bool y_norm) {
+                          const int32_t* col_idx, const float* alpha, int n, int64_t n_edges, int C, int H, float* y,
+                          hipStream_t s, bool y_norm) {
   if (n == 0) return hipSuccess;
   const int threads = C <= 64 ? 64 : 128;
   const size_t lds = sizeof(float) * ((size_t)4 * t.nk * t.nk + (size_t)4 * t.nk);
@@ -2019,7 +2036,7 @@ hipError_t launch_edge_tp(const DevTables& t, const float* pos, const float* fea
 #define E2F_CASE(LL)                                                                                        \
   case LL:                                                                                                  \
     if (hipError_t e = allow_lds(k_edge_tp<LL>, lds); e != hipSuccess) return e;                            \
-    k_edge_tp<LL><<<n, threads, lds, s>>>(t, pos, feat, row_ptr, col_idx, alpha, C, H, y_norm, y);          \
+    k_edge_tp<LL><<<n, threads, lds, s>>>(t, pos, feat, row_ptr, col_idx, alpha, C, H, y_norm, n, n_edges, y); \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4) E2F_CASE(5) E2F_CASE(6)
 #undef E2F_CASE
@@ -2065,8 +2082,8 @@ hipError_t launch_alpha_dnorm(const float* pos, const int64_t* row_ptr, const in
   if (n_edges == 0) return hipSuccess;
   const int64_t blocks = (n_edges + 255) / 256;
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  k_edge_rows<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, n, rows);
-  k_alpha_dnorm<<<(unsigned)blocks, 256, 0, s>>>(pos, rows, col, alpha, n_edges, H, L, alpha_f);
+  if (row_ptr) k_edge_rows<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, n, rows);
+  k_alpha_dnorm<<<(unsigned)blocks, 256, 0, s>>>(pos, rows, col, alpha, n, n_edges, H, L, alpha_f);
   return hipGetLastError();
 }
 

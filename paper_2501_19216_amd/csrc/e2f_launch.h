@@ -13,6 +13,43 @@ namespace e2f {
 constexpr int kStatsInts = 8;
 hipError_t launch_bbox(const float* pos, const int32_t* graph_id, int n, int* stats, hipStream_t s);
 
+// ---- device-side plan of the factorised forward (plan.hip)
+// Tile grid on the 2^-16 A lattice: cell (cx, cy, cz) of a graph covers
+// lo + [c span / dim, (c+1) span / dim) per axis; its centre is the local
+// origin of the receivers in it.
+struct TileGridDev {
+  int lo[3];
+  int dim[3];
+  int64_t span[3];
+  int ncell;
+  int pad;
+};
+// stats as for launch_bbox (initialised here); dmin (or NULL) receives the
+// shortest nonzero edge length as fp32 bits after launch_plan_dmin
+hipError_t launch_plan_bbox(const float* pos, const int32_t* graph_id, int n, int* stats, unsigned* dmin,
+                            hipStream_t s);
+hipError_t launch_plan_dmin(const float* pos, const int32_t* rows, const int32_t* col, int n, int64_t n_edges,
+                            unsigned* dmin, hipStream_t s);
+// side in grid units; with dmin, side = min(side, dmin_scale * shortest edge)
+hipError_t launch_plan_grid(const int* stats, const unsigned* dmin, double side, double dmin_scale, bool graphs,
+                            TileGridDev* grid, hipStream_t s);
+size_t plan_sort_tmp_bytes(int n);
+// tile_of [n]; order [n] = receivers sorted by (graph, Morton index of 4 A cells)
+hipError_t launch_plan_order(const float* pos, const int32_t* graph_id, int n, const TileGridDev* grid,
+                             int32_t* tile_of, uint64_t* keys, uint64_t* keys_out, int32_t* vals, int32_t* order,
+                             void* tmp, size_t tmp_bytes, hipStream_t s);
+// Rr [n][nk] float64 (receivers) and Re [E][nk] float32 (senders, CSR order),
+// both about the receiver's tile centre
+hipError_t launch_plan_sh(const DevTables& t, const float* pos, const int64_t* row_ptr, const int32_t* col, int n,
+                          int64_t n_edges, const int32_t* tile_of, const TileGridDev* grid, double* Rr, float* Re,
+                          hipStream_t s);
+hipError_t launch_plan_edge_rows(const int64_t* row_ptr, int n, int64_t n_edges, int32_t* rows, hipStream_t s);
+hipError_t launch_fill(float* p, int64_t count, float v, hipStream_t s);
+// *bad (device int) = 0, or the bits of k_validate_*: 1 row_ptr[0] != 0,
+// 2 a decreasing row_ptr, 4 row_ptr[n] != n_edges, 8 a sender outside [0, n)
+hipError_t launch_validate_graph(const int64_t* row_ptr, const int32_t* col, int n, int64_t n_edges, int* bad,
+                                 hipStream_t s);
+
 // ---- radius graph
 struct CellGrid {
   int lo[3];
@@ -100,7 +137,8 @@ hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_pt
                             const int32_t* ucount, const int32_t* edge_slot, bool use_blocks, int n, int dimT, int C,
                             int H, float* S, hipStream_t s);
 // alpha_f[(f*H + h)*E + e] = alpha[e][h] / |r_i - r_j|^f for f <= L (rows:
-// E ints of scratch, the receiver of every edge); alpha NULL means ones
+// E ints, the receiver of every edge, filled here unless row_ptr is NULL,
+// then read as given); alpha NULL means ones
 hipError_t launch_alpha_dnorm(const float* pos, const int64_t* row_ptr, const int32_t* col, const float* alpha, int n,
                               int64_t n_edges, int H, int L, int32_t* rows, float* alpha_f, hipStream_t s);
 // alpha_hm[h][e] = alpha[e][h]
@@ -108,6 +146,8 @@ hipError_t launch_alpha_head_major(const float* alpha, int64_t n_edges, int H, f
 // y[order[r]] from S row r (head-major like T), r < n; shared_s: every r
 // reads S row 0
 // S rows r < n (receivers order[r]) by aggregating the uncoupled node products
+// (H heads of C/H channels, each of the caller's heads split into hdiv: the
+// attention weight of head h is alpha_hm[h / hdiv]; n_nodes bounds the senders)
 // alpha_ij R(p_j) (x) h_j and coupling per receiver (no T): Re [E][nk] float32
 // (launch_edge_R), alpha_hm [H][n_edges] or NULL (ones)
 // with the coupling schedule of couple_schedule(tables, outer_agg_groups(L, C, H))
@@ -117,8 +157,8 @@ int outer_agg_groups(int L, int C, int H);
 hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* row_ptr, const int32_t* col,
                             const float* alpha_hm, int64_t n_edges, const float* feat,
                             const int32_t* order, const int* cmeta, const float* ccoef, const int* pmeta,
-                            const float* ptab, int ntab, int ck, int cgroups, int n, int C, int H, float* S,
-                            hipStream_t s);
+                            const float* ptab, int ntab, int ck, int cgroups, int n, int C, int H, int hdiv,
+                            int n_nodes, float* S, hipStream_t s);
 // accumulate: y += the product instead of y = (one writer per element)
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, bool shared_s, const int32_t* order,
                            int n, int C, int dh, float* y, hipStream_t s, bool accumulate = false);
@@ -172,6 +212,7 @@ hipError_t launch_iota(int n, int32_t* v, hipStream_t s);
 // ---- per-irrep channel mixing and the edge baseline
 hipError_t launch_mix(int L, const float* y, const void* W, bool w_bf16, int n, int C, float* out, hipStream_t s);
 hipError_t launch_edge_tp(const DevTables& t, const float* pos, const float* feat, const int64_t* row_ptr,
-                          const int32_t* col_idx, const float* alpha, int n, int C, int H, float* y, hipStream_t s, bool y_norm = false);
+                          const int32_t* col_idx, const float* alpha, int n, int64_t n_edges, int C, int H, float* y,
+                          hipStream_t s, bool y_norm = false);
 
 }  // namespace e2f

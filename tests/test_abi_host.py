@@ -70,7 +70,10 @@ def test_conv_argument_checks(e2f, fn):
     f = getattr(e2f.lib, fn)
 
     def call(prm, n=8, E=20, pos=FAKE, feat=FAKE, rp=FAKE, ci=FAKE, out=FAKE, handle=ctx.handle):
-        return f(handle, ctypes.byref(prm) if prm is not None else None, pos, None, feat, n, rp, ci, E, None, out, None)
+        args = [handle, ctypes.byref(prm) if prm is not None else None, pos, None, feat, n, rp, ci, E, None, out]
+        if fn == "e2f_wigner6j_conv_forward":
+            args += [FAKE, 1 << 20]  # workspace
+        return f(*args, None)
 
     EINVAL, EUNS, EDEV = e2f.E2F_EINVAL, e2f.E2F_EUNSUPPORTED, e2f.E2F_EDEVICE
     assert call(_params(e2f)) == EDEV  # valid, but the context has no device
@@ -159,4 +162,36 @@ def test_other_argument_checks(e2f):
     h = ctypes.c_void_p()
     assert lib.e2f_create(7, -1, ctypes.byref(h)) == e2f.E2F_EINVAL
     assert lib.e2f_create(3, -2, ctypes.byref(h)) == e2f.E2F_EINVAL
+    ctx.close()
+
+
+def test_workspace_size_query(e2f):
+    # the size query needs no device: the one-pass size holds S for every
+    # receiver, the minimum for 256 (the plan and per-edge arrays are shared)
+    ctx = e2f.e2f_create(6, None)
+    lib = e2f.lib
+    b, m = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    for L, C, H, n, E in ((2, 16, 4, 32, 738), (4, 128, 8, 20000, 1597678), (6, 64, 8, 200000, 39828996)):
+        prm = _params(e2f, lmax=L, channels=C, heads=H)
+        assert lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm), n, E, ctypes.byref(b)) == e2f.E2F_OK
+        assert lib.e2f_wigner6j_workspace_min(ctx.handle, ctypes.byref(prm), n, E, ctypes.byref(m)) == e2f.E2F_OK
+        dimT, nk = e2f.e2f_node_tp_dim(L), (L + 1) ** 2
+        s_row = -(-4 * dimT * C // 256) * 256
+        assert b.value - m.value == max(0, n - 256) * s_row
+        # at least the per-edge harmonics, the receivers' harmonics, the head-major weights and S
+        assert b.value >= 4 * E * nk + 8 * n * nk + 4 * E * H + n * s_row
+        prm_mix = _params(e2f, lmax=L, channels=C, heads=H, mix_w=FAKE)
+        assert lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm_mix), n, E, ctypes.byref(m)) == e2f.E2F_OK
+        assert m.value - b.value >= 4 * n * nk * C  # the unmixed output
+    prm = _params(e2f, heads=3)
+    assert lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm), 10, 10, ctypes.byref(b)) == e2f.E2F_EINVAL
+    prm = _params(e2f)
+    assert lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm), -1, 10, ctypes.byref(b)) == e2f.E2F_EINVAL
+    assert lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm), 10, 10, None) == e2f.E2F_EINVAL
+    assert lib.e2f_wigner6j_prepare(ctx.handle, ctypes.byref(prm)) == e2f.E2F_EDEVICE
+    bad = ctypes.c_int32(0)
+    assert lib.e2f_validate_graph(ctx.handle, 10, FAKE, FAKE, 30, ctypes.byref(bad), None) == e2f.E2F_EDEVICE
+    assert lib.e2f_validate_graph(ctx.handle, 10, None, FAKE, 30, ctypes.byref(bad), None) == e2f.E2F_EINVAL
+    assert lib.e2f_validate_graph(ctx.handle, 10, FAKE, None, 30, ctypes.byref(bad), None) == e2f.E2F_EINVAL
+    assert lib.e2f_validate_graph(ctx.handle, 10, FAKE, FAKE, 30, None, None) == e2f.E2F_EINVAL
     ctx.close()

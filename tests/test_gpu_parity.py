@@ -220,41 +220,60 @@ def test_determinism_and_translation(e2f, ctx):
     assert o.max_rel_err(a3, a1, wl.lmax) <= TOL_F32 and o.max_rel_err(b3, b1, wl.lmax) <= TOL_F32
 
 
-@pytest.mark.parametrize("L,C,H,cut,n,box", [(2, 32, 4, 5.0, 300, 12.0), (4, 64, 4, 5.0, 300, 12.0),
-                                              (2, 16, 2, 30.0, 700, 10.0)])
-def test_conv_stored_t_rows(e2f, ctx, monkeypatch, L, C, H, cut, n, box):
-    # the aggregation of stored T rows (E2F_AGG_T): over 16-receiver blocks,
-    # and row by row when a receiver has more than 512 neighbours (the last
-    # case is a complete graph of 700 atoms)
-    monkeypatch.setenv("E2F_AGG_T", "1")
+@pytest.mark.parametrize("L,C,H,cut,n,box", [(2, 32, 4, 5.0, 300, 12.0), (4, 128, 1, 5.0, 300, 12.0),
+                                              (6, 64, 2, 5.0, 200, 10.0), (2, 16, 2, 30.0, 700, 10.0)])
+def test_conv_wide_heads_and_long_rows(e2f, ctx, L, C, H, cut, n, box):
+    # heads wider than the aggregation's tile (128 channels in one head at
+    # L = 4, 32 per head at L = 6) are split into channel groups sharing the
+    # head's weights; the last case is a complete graph of 700 atoms (rows of
+    # 699 edges, several staging chunks per receiver)
     rng = np.random.default_rng(100 + L + n)
     pos = syn.quantize(rng.uniform(0, box, size=(n, 3)))
     rp, ci = o.neighbor_list(pos, cut)
     feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
     alpha = rng.uniform(0.05, 1.0, size=(len(ci), H)).astype(np.float32)
-    w = rng.uniform(0.2, 1.0, size=(L + 1) ** 3)
-    ref = o.conv_edge(L, H, pos, feat, rp, ci, alpha, w)
-    print("stored T rows: L %d C %d n %d max degree %d" % (L, C, n, int(np.diff(rp).max())), flush=True)
+    w = rng.uniform(0.2, 1.0, size=(L + 1) ** 3) * cut ** -np.arange(L + 1)[None, :, None].repeat(L + 1, 0).repeat(
+        L + 1, 2).reshape(-1)
+    r = sample_rows(n, 64, seed=L)
+    ref = o.conv_edge(L, H, pos, feat, rp, ci, alpha, w, rows=r)
+    print("wide heads / long rows: L %d C %d H %d n %d max degree %d" % (L, C, H, n, int(np.diff(rp).max())),
+          flush=True)
     got = e2f.e2f_wigner6j_conv_forward(ctx, gpu(pos), gpu(feat), gpu(rp), gpu(ci), gpu(alpha), L, H, cut,
                                         path_w=w).cpu().numpy()
-    err = o.max_rel_err(got, ref, L)
-    print("stored T rows: err %.3e" % err)
+    err = o.max_rel_err(got[r], ref, L)
+    print("wide heads / long rows: err %.3e" % err)
     assert err <= TOL_F32
 
 
-def test_conv_tile_batches(e2f, ctx, monkeypatch):
-    # small tiles and a tiny memory budget force many tiles and several batches
+def test_conv_workspace_slices(e2f, ctx):
+    # the smallest workspace the forward accepts: receivers are aggregated and
+    # recoupled in slices of 256, in the same order as in one pass, so the
+    # output is bitwise that of the one-pass workspace
     inp, rp, ci, alpha = case("water2000_L4")
     wl = inp.workload
-    r = sample_rows(inp.pos.shape[0], 64, seed=3)
+    n, E = inp.pos.shape[0], len(ci)
+    r = sample_rows(n, 64, seed=3)
     ref = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, inp.mix_w, rows=r)
-    monkeypatch.setenv("E2F_TILE_BUDGET_MB", "150")
-    y6, _ = run_both(e2f, ctx, inp, rp, ci, alpha, wl.lmax, wl.heads, wl.cutoff, mix=inp.mix_w, tile_side=10.0)
-    pairs, tiles = e2f.e2f_last_plan(ctx)
-    assert tiles == 27 and pairs > inp.pos.shape[0]
-    err = o.max_rel_err(y6[r], ref, wl.lmax)
-    print("water2000 in batches of 10 A tiles: err %.3e" % err)
+    args = (gpu(inp.pos), gpu(inp.feat), gpu(rp), gpu(ci), gpu(alpha), wl.lmax, wl.heads, wl.cutoff)
+    full = e2f.e2f_wigner6j_conv_forward(ctx, *args, mix_w=gpu(inp.mix_w)).cpu().numpy()
+    assert e2f.e2f_last_slices(ctx) == 1
+    wmin = e2f.e2f_wigner6j_workspace_size(ctx, n, E, wl.lmax, wl.channels, wl.heads, wl.cutoff,
+                                           mix_w=gpu(inp.mix_w), minimum=True)
+    wfull = e2f.e2f_wigner6j_workspace_size(ctx, n, E, wl.lmax, wl.channels, wl.heads, wl.cutoff,
+                                            mix_w=gpu(inp.mix_w))
+    assert wmin < wfull
+    ws = torch.empty(wmin, dtype=torch.uint8, device=DEV)
+    sliced = e2f.e2f_wigner6j_conv_forward(ctx, *args, mix_w=gpu(inp.mix_w), workspace=ws).cpu().numpy()
+    assert e2f.e2f_last_slices(ctx) == (n + 255) // 256
+    assert np.array_equal(sliced, full)
+    err = o.max_rel_err(sliced[r], ref, wl.lmax)
+    print("water2000 in slices of 256 receivers: err %.3e" % err)
     assert err <= TOL_F32
+    # one byte less than the minimum is refused before any device work
+    with pytest.raises(e2f.E2FError) as ei:
+        e2f.e2f_wigner6j_conv_forward(ctx, *args, mix_w=gpu(inp.mix_w),
+                                      workspace=torch.empty(wmin - 1, dtype=torch.uint8, device=DEV))
+    assert ei.value.status == e2f.E2F_ECAPACITY
 
 
 def test_conv_stress_200k_sampled(e2f, ctx):
@@ -268,8 +287,30 @@ def test_conv_stress_200k_sampled(e2f, ctx):
     out = e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, g_rp, g_ci, gpu(alpha), wl.lmax, wl.heads, wl.cutoff,
                                         mix_w=gpu(inp.mix_w))
     torch.cuda.synchronize()
-    r = sample_rows(inp.pos.shape[0], 24, seed=5)
+    r = sample_rows(inp.pos.shape[0], 256, seed=5)
     ref = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, inp.mix_w, rows=r)
     err = o.max_rel_err(out.cpu().numpy()[r], ref, wl.lmax)
     print("stress200k: %d edges, err %.3e" % (len(ci), err))
     assert err <= TOL_F32
+
+
+def test_stress_crop_both_paths(e2f, ctx):
+    # the central 58.48 A crop of the 200,000-atom system (about 20k atoms,
+    # 3.6 M edges, L = 6, C = 64): the factorised path and the per-edge
+    # baseline against the definition on sampled rows
+    inp, rp, ci, alpha = case("stress200k_L6")
+    wl = inp.workload
+    lo, hi = inp.pos.min(0), inp.pos.max(0)
+    keep = np.nonzero(np.all(np.abs(inp.pos - (lo + hi) / 2) < syn._cube_side(20000) / 2, axis=1))[0]
+    pos, feat = np.ascontiguousarray(inp.pos[keep]), np.ascontiguousarray(inp.feat[keep])
+    crp, cci = o.neighbor_list(pos, wl.cutoff)
+    calpha = syn.attention_weights(pos, inp.species[keep], crp, cci, wl.heads, wl.cutoff, wl.species, wl.seed)
+    n = pos.shape[0]
+    print("stress crop: %d atoms, %d edges" % (n, len(cci)), flush=True)
+    y6, ye = run_both(e2f, ctx, type(inp)(pos, None, inp.species[keep], feat, inp.mix_w, inp.path_w, wl), crp, cci,
+                      calpha, wl.lmax, wl.heads, wl.cutoff, mix=inp.mix_w)
+    r = sample_rows(n, 256, seed=9)
+    ref = o.layer(wl.lmax, wl.heads, pos, feat, crp, cci, calpha, inp.path_w, inp.mix_w, rows=r)
+    e6, ee = o.max_rel_err(y6[r], ref, wl.lmax), o.max_rel_err(ye[r], ref, wl.lmax)
+    print("stress crop: 6j err %.3e, edge-TP err %.3e" % (e6, ee))
+    assert e6 <= TOL_F32 and ee <= TOL_F32

@@ -1,8 +1,7 @@
 """Alg. 1's per-degree attention weights alpha / D^f (Y-based filters, the
 y_norm flag): both forms of the layer on the GPU against the oracle's
 definition of the variant.  The factorised forward aggregates once per
-filter degree f and recouples the terms of degree b + u = f from S^(f)
-(through the reordered aggregation, or the stored T rows with E2F_AGG_T).
+filter degree f and recouples the terms of degree b + u = f from S^(f).
 
 Run with -m gpu."""
 import numpy as np
@@ -65,60 +64,45 @@ def test_y_norm_workloads(e2f, ctx, name, rows, mix):
     assert o.max_rel_err(ref[:8], plain, wl.lmax) > 1e-2
 
 
-@pytest.mark.parametrize("name,rows", [("molecules256x30_L3", 256), ("water2000_L4", 64)])
-def test_y_norm_stored_t_rows(e2f, ctx, monkeypatch, name, rows):
-    # the same variant through the aggregation of stored T rows (E2F_AGG_T):
-    # one S buffer per filter degree, every aggregation before the recouples
-    monkeypatch.setenv("E2F_AGG_T", "1")
-    inp, rp, ci, alpha = case(name)
-    wl = inp.workload
-    r = sample_rows(inp.pos.shape[0], rows, seed=13)
-    ref = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, inp.mix_w, rows=r, y_norm=True)
-    print("%s y_norm stored T: case" % name, flush=True)
-    y6, _ = both(e2f, ctx, inp, rp, ci, alpha, wl, inp.mix_w)
-    e6 = o.max_rel_err(y6[r], ref, wl.lmax)
-    print("%s y_norm stored T: 6j %.3e" % (name, e6))
-    assert e6 <= TOL_F32
-
-
-def jittered_lattice(k, spacing, jitter, seed):
-    # atoms no closer than spacing - 2 jitter (weights 1/D^f of short edges
-    # amplify the rounding of the binomial expansion, see the variant's notes)
-    import itertools
-    rng = np.random.default_rng(seed)
-    g = np.array(list(itertools.product(range(k), repeat=3)), dtype=np.float64) * spacing
-    return syn.quantize(g + rng.uniform(-jitter, jitter, size=g.shape))
-
-
-def test_y_norm_high_degree_and_batches(e2f, ctx, monkeypatch):
-    # L = 6 on a jittered lattice (nearest atoms >= 0.9 A apart), and water2000
-    # split into several tile batches
+def test_y_norm_short_contacts_and_slices(e2f, ctx):
+    # L = 6 on uniform random positions (no minimum distance: the closest
+    # pairs are about 0.1 A apart), where the weights 1/D^f of the short edges
+    # amplify the rounding of the binomial expansion unless the local origins
+    # are close enough (the tile side follows the shortest edge); then
+    # water2000 through the smallest workspace (slices of 256 receivers)
     rng = np.random.default_rng(61)
     L, C, H, cutoff = 6, 8, 2, 5.0
-    pos = jittered_lattice(7, 1.6, 0.35, 61)
+    pos = syn.quantize(rng.uniform(0.0, 10.0, size=(343, 3)))
     n = pos.shape[0]
     rp, ci = o.neighbor_list(pos, cutoff)
+    d = np.linalg.norm(pos[np.repeat(np.arange(n), np.diff(rp))].astype(np.float64) - pos[ci], axis=1)
     feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
     alpha = rng.uniform(0.1, 1.0, size=(len(ci), H)).astype(np.float32)
     w = rng.uniform(0.5, 1.5, size=(L + 1) ** 3)
     r = sample_rows(n, 40, seed=2)
+    near = np.unique(np.repeat(np.arange(n), np.diff(rp))[d < 0.5])
+    r = np.unique(np.concatenate([r, near])).astype(np.int32)  # every receiver of a contact below 0.5 A
     ref = o.layer(L, H, pos, feat, rp, ci, alpha, w, rows=r, y_norm=True)
-    print("L6 y_norm: case", flush=True)
+    print("L6 y_norm short contacts: shortest edge %.3f A, %d rows" % (d.min(), len(r)), flush=True)
     got = e2f.e2f_wigner6j_conv_forward(ctx, gpu(pos), gpu(feat), gpu(rp), gpu(ci), gpu(alpha), L, H, cutoff,
                                         path_w=w, y_norm=True).cpu().numpy()
     err = o.max_rel_err(got[r], ref, L)
-    print("L6 y_norm: err %.3e" % err)
+    print("L6 y_norm short contacts: err %.3e" % err)
     assert err <= TOL_F32
     inp, rp, ci, alpha = case("water2000_L4")
     wl = inp.workload
-    r = sample_rows(inp.pos.shape[0], 48, seed=4)
+    n, E = inp.pos.shape[0], len(ci)
+    r = sample_rows(n, 48, seed=4)
     ref = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, rows=r, y_norm=True)
-    monkeypatch.setenv("E2F_TILE_BUDGET_MB", "300")
-    print("water2000 y_norm batches: case", flush=True)
-    y6, _ = both(e2f, ctx, inp, rp, ci, alpha, wl, None, tile_side=10.0)
-    assert e2f.e2f_last_plan(ctx)[1] == 27
-    err = o.max_rel_err(y6[r], ref, wl.lmax)
-    print("water2000 y_norm in batches: err %.3e" % err)
+    wmin = e2f.e2f_wigner6j_workspace_size(ctx, n, E, wl.lmax, wl.channels, wl.heads, wl.cutoff, y_norm=True,
+                                           minimum=True)
+    print("water2000 y_norm slices: case", flush=True)
+    got = e2f.e2f_wigner6j_conv_forward(ctx, gpu(inp.pos), gpu(inp.feat), gpu(rp), gpu(ci), gpu(alpha), wl.lmax,
+                                        wl.heads, wl.cutoff, y_norm=True,
+                                        workspace=torch.empty(wmin, dtype=torch.uint8, device=DEV)).cpu().numpy()
+    assert e2f.e2f_last_slices(ctx) == (n + 255) // 256
+    err = o.max_rel_err(got[r], ref, wl.lmax)
+    print("water2000 y_norm in slices: err %.3e" % err)
     assert err <= TOL_F32
 
 
