@@ -209,6 +209,25 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* params
                                      const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,
                                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* e2f_wigner6j_conv_forward for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same computation and result, in a scratch area of
+ * 128 MiB that the library holds in every GPU it runs on (a static device
+ * array, resolved per device by e2f_create) instead of a caller workspace.
+ * It calls no hipMalloc, hipFree, host-to-device copy or allocating library
+ * routine: the path weights' coefficient set and the coupling schedule must
+ * already be resident (e2f_wigner6j_prepare, or an earlier forward with the
+ * same parameters), else E2F_EINVAL.  Inputs whose smallest workspace
+ * (e2f_wigner6j_workspace_min) exceeds 128 MiB return E2F_ECAPACITY.  All
+ * calls on one GPU share its scratch area: calls that overlap on one GPU
+ * (two streams, two threads, two contexts) race and must be serialised by
+ * the caller.  Nothing in it needs to start at zero; it keeps the last
+ * call's contents. */
+e2f_status e2f_wigner6j_conv_forward_noalloc(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
+                                             const int32_t* graph_id, const float* feat, int32_t n,
+                                             const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges,
+                                             const float* alpha, float* out, void* stream);
+
 /* Checks a CSR graph of n atoms: *bad (host) = 0 if row_ptr[0] = 0, row_ptr
  * never decreases, row_ptr[n] = n_edges and every col_idx is in [0, n); else
  * the OR of 1 (row_ptr[0]), 2 (a decreasing row_ptr), 4 (row_ptr[n]), 8 (a

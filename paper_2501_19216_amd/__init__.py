@@ -25,7 +25,7 @@ _STATUS = {0: "E2F_OK", 1: "E2F_EINVAL", 2: "E2F_ECAPACITY", 3: "E2F_ENOMEM", 4:
 EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg", "e2f_knn_graph",
             "e2f_attention_weights", "e2f_recoupling_weight", "e2f_neighbor_list", "e2f_solid_harmonics",
             "e2f_node_tp", "e2f_wigner6j_workspace_size", "e2f_wigner6j_workspace_min", "e2f_wigner6j_prepare",
-            "e2f_wigner6j_conv_forward", "e2f_validate_graph", "e2f_wigner6j_conv_forward_dense",
+            "e2f_wigner6j_conv_forward", "e2f_wigner6j_conv_forward_noalloc", "e2f_validate_graph", "e2f_wigner6j_conv_forward_dense",
             "e2f_wigner6j_conv_forward_global", "e2f_wigner6j_conv_backward", "e2f_edge_tp_conv_forward",
             "e2f_profile", "e2f_profile_read", "e2f_last_slices"]
 
@@ -87,6 +87,9 @@ def _load():
     L.e2f_wigner6j_conv_forward.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, i32, p, p, i64, p, p, p,
                                             ctypes.c_size_t, p]
     L.e2f_wigner6j_conv_forward.restype = i
+    L.e2f_wigner6j_conv_forward_noalloc.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, i32, p, p, i64, p, p,
+                                                    p]
+    L.e2f_wigner6j_conv_forward_noalloc.restype = i
     L.e2f_edge_tp_conv_forward.argtypes = [p, ctypes.POINTER(ConvParams), p, p, p, i32, p, p, i64, p, p, p]
     L.e2f_edge_tp_conv_forward.restype = i
     L.e2f_wigner6j_conv_forward_dense.argtypes = [p, ctypes.POINTER(ConvParams), p, p, i32, p, p, p]
@@ -347,6 +350,22 @@ def e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, hea
                                        workspace.numel(), _stream(feat.device))
     del keep
     _check(st, "e2f_wigner6j_conv_forward")
+    return out
+
+
+def e2f_wigner6j_conv_forward_noalloc(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None,
+                                      mix_w=None, graph_id=None, tile_side=0.0, out=None, y_norm=False):
+    """The forward in the library's per-GPU scratch memory (no allocation;
+    the parameters must have been prepared).  out must be given by callers
+    that cannot allocate: with out=None the binding allocates it."""
+    out = _conv_args(pos, feat, row_ptr, col_idx, alpha, graph_id, out)
+    n, nk, C = feat.shape
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm)
+    st = lib.e2f_wigner6j_conv_forward_noalloc(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(graph_id), _ptr(feat),
+                                               n, _ptr(row_ptr), _ptr(col_idx), col_idx.numel(), _ptr(alpha),
+                                               _ptr(out), _stream(feat.device))
+    del keep
+    _check(st, "e2f_wigner6j_conv_forward_noalloc")
     return out
 
 

@@ -22,6 +22,13 @@
 
 using namespace e2f;
 
+// Scratch memory of e2f_wigner6j_conv_forward_noalloc (for callers that
+// cannot allocate): a file-scope device array, one copy per GPU, held until
+// the process ends.  Host code never uses its name as an address: e2f_create
+// resolves this device's copy with hipGetSymbolAddress and keeps the pointer.
+constexpr size_t kScratchBytes = (size_t)128 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 namespace {
 
 thread_local std::string g_err;
@@ -64,6 +71,7 @@ struct e2f_ctx {
   // per L and filter degree f: the recouple schedule restricted to b + u = f
   std::vector<std::vector<const int*>> rcf_k, rcf_off, rcf_meta;
   int* stats = nullptr;                    // device, kStatsInts ints
+  void* scratch = nullptr;                 // this device's copy of the file-scope scratch array
   int64_t* pinned = nullptr;               // host, 16 int64
   int32_t* pinned_plan = nullptr;          // host, plan sizes read back in one copy
   size_t pinned_plan_n = 0;
@@ -725,6 +733,13 @@ e2f_status e2f_create(int lmax_max, int device, e2f_ctx** out) {
       st = fail(E2F_ENOMEM, "stats allocation failed");
     if (st == E2F_OK && hipHostMalloc((void**)&ctx->pinned, sizeof(int64_t) * 16, hipHostMallocDefault) != hipSuccess)
       st = fail(E2F_ENOMEM, "pinned allocation failed");
+    if (st == E2F_OK) {  // this device's copy of the scratch array (the device is current here)
+      const hipError_t e = hipGetSymbolAddress(&ctx->scratch, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !ctx->scratch) {
+        ctx->scratch = nullptr;
+        st = fail(E2F_EDEVICE, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+      }
+    }
     if (st != E2F_OK) {
       e2f_destroy(ctx);
       return st;
@@ -979,6 +994,21 @@ e2f_status e2f_wigner6j_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, con
                                      void* workspace, size_t workspace_bytes, void* stream) {
   return forward_impl(ctx, p, pos, graph_id, feat, n, row_ptr, col_idx, n_edges, alpha, out, workspace,
                       workspace_bytes, stream, true);
+}
+
+e2f_status e2f_wigner6j_conv_forward_noalloc(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos,
+                                             const int32_t* graph_id, const float* feat, int32_t n,
+                                             const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges,
+                                             const float* alpha, float* out, void* stream) {
+  if (e2f_status rs = check_conv(ctx, p, pos, feat, n, row_ptr, col_idx, n_edges, out); rs != E2F_OK) return rs;
+  if (!ctx->scratch) return fail(E2F_EDEVICE, "the context has no scratch memory");
+  const size_t need = fwd_layout(p, n, n_edges, alpha != nullptr).total(std::min<int64_t>(n, kMinSlice));
+  if (n_edges > 0 && need > kScratchBytes)
+    return fail(E2F_ECAPACITY, "the forward needs at least %zu bytes of workspace; the scratch memory holds %zu",
+                need, kScratchBytes);
+  // no upload: the coefficient set and coupling schedule must be resident
+  return forward_impl(ctx, p, pos, graph_id, feat, n, row_ptr, col_idx, n_edges, alpha, out, ctx->scratch,
+                      kScratchBytes, stream, false);
 }
 
 e2f_status e2f_validate_graph(e2f_ctx* ctx, int32_t n, const int64_t* row_ptr, const int32_t* col_idx,
