@@ -461,7 +461,9 @@ e2f_status check_params(e2f_ctx* ctx, const e2f_conv_params* p) {
   if (!finite_pos(p->cutoff) || p->cutoff > 64.0f) return fail(E2F_EINVAL, "cutoff must be finite, in (0, 64]");
   if (!std::isfinite(p->tile_side) || p->tile_side < 0.0f) return fail(E2F_EINVAL, "tile_side must be finite and >= 0");
   if (p->y_norm != 0 && p->y_norm != 1) return fail(E2F_EINVAL, "y_norm must be 0 or 1");
-  if (p->mix_dtype != E2F_F32 && p->mix_dtype != E2F_BF16) return fail(E2F_EINVAL, "unknown mix_dtype");
+  int md = 0;  // read as an int: a C caller may store any value in the enum field
+  std::memcpy(&md, &p->mix_dtype, sizeof(md));
+  if (md != E2F_F32 && md != E2F_BF16) return fail(E2F_EINVAL, "unknown mix_dtype");
   if (p->path_w) {
     const int L1 = p->lmax + 1;
     for (int q = 0; q < L1 * L1 * L1; ++q)
