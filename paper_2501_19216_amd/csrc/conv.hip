@@ -91,93 +91,6 @@ __global__ void k_sh(DevTables t, const float* __restrict__ pos, const int32_t* 
   else out_f[gid] = (float)v;
 }
 
-// ------------------------------------------------------------ tile plan
-struct TileGrid {
-  int lo[3];
-  int dim[3];
-  int64_t span[3];
-  int ncell;
-};
-
-__global__ void k_tile_keys(const float* __restrict__ pos, const int32_t* __restrict__ gid, int n, TileGrid g,
-                            int32_t* __restrict__ tile_of) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  int c[3];
-  for (int k = 0; k < 3; ++k) {
-    const int64_t X = __float2int_rn(pos[3 * i + k] * 65536.0f);
-    const int64_t q = (X - g.lo[k]) * g.dim[k] / g.span[k];
-    c[k] = (int)(q < g.dim[k] - 1 ? q : g.dim[k] - 1);
-  }
-  const int cell = (c[2] * g.dim[1] + c[1]) * g.dim[0] + c[0];
-  tile_of[i] = (gid ? gid[i] : 0) * g.ncell + cell;
-}
-
-// 64 receivers per workgroup of four waves: wave 0 takes the largest degree
-// of the 64 (one atomic per workgroup); wave w walks the edges of receivers
-// w, w + 4, ... with its lanes.
-__global__ __launch_bounds__(256) void k_pair_flags(const int64_t* __restrict__ row_ptr,
-                                                    const int32_t* __restrict__ col,
-                                                    const int32_t* __restrict__ tile_of, int n,
-                                                    int32_t* __restrict__ flags, int32_t* __restrict__ max_degree) {
-  const int i0 = blockIdx.x * 64, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  if (wave == 0) {
-    const int i = i0 + lane;
-    int deg = i < n ? (int)(row_ptr[i + 1] - row_ptr[i]) : 0;
-    for (int o = 32; o > 0; o >>= 1) deg = max(deg, __shfl_xor(deg, o));
-    if (lane == 0) atomicMax(max_degree, deg);
-  }
-  for (int r = wave; r < 64 && i0 + r < n; r += 4) {
-    const int i = i0 + r;
-    const int64_t base = (int64_t)tile_of[i] * n, e1 = row_ptr[i + 1];
-    for (int64_t e = row_ptr[i] + lane; e < e1; e += 64) flags[base + col[e]] = 1;
-  }
-}
-
-__global__ void k_pairs(const int32_t* __restrict__ flags, const int32_t* __restrict__ pidx, int64_t count, int n,
-                        int32_t* __restrict__ pair_node, int32_t* __restrict__ pair_tile) {
-  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= count || !flags[q]) return;
-  const int p = pidx[q];
-  pair_node[p] = (int)(q % n);
-  pair_tile[p] = (int)(q / n);
-}
-
-__global__ void k_col_pair(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ col,
-                           const int32_t* __restrict__ tile_of, const int32_t* __restrict__ pidx, int n,
-                           int32_t* __restrict__ col_pair) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const int64_t base = (int64_t)tile_of[i] * n;
-  for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) col_pair[e] = pidx[base + col[e]];
-}
-
-// Per tile key: number of receivers (for their range in the receiver order)
-// and first pair index (pidx at the key's first flag).
-// With few keys the workgroup counts in LDS and adds its nonzero bins once.
-constexpr int kKeyBins = 4096;
-template <bool LDS_BINS>
-__global__ __launch_bounds__(256) void k_key_counts(const int32_t* __restrict__ tile_of, int n, int keys,
-                                                    int32_t* __restrict__ counts) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (!LDS_BINS) {
-    if (i < n) atomicAdd(&counts[tile_of[i]], 1);
-    return;
-  }
-  __shared__ int32_t bins[kKeyBins];
-  for (int q = threadIdx.x; q < keys; q += blockDim.x) bins[q] = 0;
-  __syncthreads();
-  if (i < n) atomicAdd(&bins[tile_of[i]], 1);
-  __syncthreads();
-  for (int q = threadIdx.x; q < keys; q += blockDim.x)
-    if (bins[q]) atomicAdd(&counts[q], bins[q]);
-}
-
-__global__ void k_key_pstart(const int32_t* __restrict__ pidx, int keys, int n, int32_t* __restrict__ pstart) {
-  const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t < keys) pstart[t] = pidx[(int64_t)t * n];
-}
-
 // ------------------------------------------------------------ j-side node TP
 // T[item][r][c] = sum_al M[r][al] h_node^(a)[al][c] for the rows r of degree a,
 // with the per-node matrix M[r][al] = sum_be C^{d de}_{a al, b be} R^(b)_be(p)
@@ -288,34 +201,6 @@ __global__ __launch_bounds__(NW * 64) void k_node_tp(DevTables t, const double* 
             make_float4(acc[0], acc[1], acc[2], acc[3]);
     }
   }
-}
-
-// ------------------------------------------------------------ receiver order
-// Receivers sorted by (tile, Morton index of a fine spatial cell): groups of
-// consecutive receivers then share most of their senders, so their T rows
-// are reused from L2.
-__device__ __forceinline__ uint32_t spread3(uint32_t v) {
-  v &= 0x3ff;
-  v = (v | (v << 16)) & 0x030000ff;
-  v = (v | (v << 8)) & 0x0300f00f;
-  v = (v | (v << 4)) & 0x030c30c3;
-  v = (v | (v << 2)) & 0x09249249;
-  return v;
-}
-
-__global__ void k_recv_keys(const float* __restrict__ pos, const int32_t* __restrict__ tile_of, int n, int lo0,
-                            int lo1, int lo2, int64_t fine, uint64_t* __restrict__ keys, int32_t* __restrict__ vals) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const int lo[3] = {lo0, lo1, lo2};
-  uint32_t m = 0;
-  for (int k = 0; k < 3; ++k) {
-    int64_t c = ((int64_t)__float2int_rn(pos[3 * i + k] * 65536.0f) - lo[k]) / fine;
-    c = c < 0 ? 0 : (c > 1023 ? 1023 : c);
-    m |= spread3((uint32_t)c) << k;
-  }
-  keys[i] = ((uint64_t)(uint32_t)tile_of[i] << 32) | m;
-  vals[i] = i;
 }
 
 // ------------------------------------------------------------ receiver blocks
@@ -1153,22 +1038,6 @@ __global__ __launch_bounds__(64 * kMixWaves) void k_mix_mfma(const float* __rest
   }
 }
 
-// The plan sizes the host needs, gathered for one device->host copy:
-// out = {pidx[count-1], flags[count-1], largest degree, rstart[0..keys],
-// pstart[0..keys]} (pstart[keys] is left for the host).
-__global__ void k_plan_pack(const int32_t* __restrict__ pidx, const int32_t* __restrict__ flags, int64_t count,
-                            const int32_t* __restrict__ max_degree, const int32_t* __restrict__ rstart,
-                            const int32_t* __restrict__ pstart, int keys, int32_t* __restrict__ out) {
-  const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t == 0) {
-    out[0] = pidx[count - 1];
-    out[1] = flags[count - 1];
-    out[2] = *max_degree;
-  }
-  if (t <= keys) out[3 + t] = rstart[t];
-  if (t < keys) out[4 + keys + t] = pstart[t];
-}
-
 // ------------------------------------------------------------ backward
 // Both per-edge products of the backward from one matrix product per
 // (receiver, head).  The edge filter is linear in the solid harmonics,
@@ -1657,73 +1526,6 @@ hipError_t launch_sh(const DevTables& t, const float* pos, const int32_t* node_o
   return hipGetLastError();
 }
 
-hipError_t launch_tile_keys(const float* pos, const int32_t* graph_id, int n, const int* lo, const int* dim,
-                            const int64_t* span, int ncell, int32_t* tile_of, hipStream_t s) {
-  TileGrid g;
-  for (int k = 0; k < 3; ++k) {
-    g.lo[k] = lo[k];
-    g.dim[k] = dim[k];
-    g.span[k] = span[k];
-  }
-  g.ncell = ncell;
-  if (n > 0) k_tile_keys<<<(n + 255) / 256, 256, 0, s>>>(pos, graph_id, n, g, tile_of);
-  return hipGetLastError();
-}
-
-hipError_t launch_pair_flags(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of, int n,
-                             int32_t* flags, int32_t* max_degree, hipStream_t s) {
-  hipError_t e = hipMemsetAsync(max_degree, 0, sizeof(int32_t), s);
-  if (e != hipSuccess) return e;
-  if (n > 0) k_pair_flags<<<(n + 63) / 64, 256, 0, s>>>(row_ptr, col_idx, tile_of, n, flags, max_degree);
-  return hipGetLastError();
-}
-
-size_t scan_tmp_bytes(int64_t count) {
-  size_t b = 0;
-  hipcub::DeviceScan::ExclusiveSum(nullptr, b, (const int32_t*)nullptr, (int32_t*)nullptr, (int)count);
-  return b;
-}
-
-hipError_t launch_scan_i32(const int32_t* in, int32_t* out, int64_t count, void* tmp, size_t tmp_bytes,
-                           hipStream_t s) {
-  size_t b = tmp_bytes;
-  return hipcub::DeviceScan::ExclusiveSum(tmp, b, in, out, (int)count, s);
-}
-
-hipError_t launch_pairs(const int32_t* flags, const int32_t* pidx, int64_t count, int n, int32_t* pair_node,
-                        int32_t* pair_tile, hipStream_t s) {
-  if (count > 0)
-    k_pairs<<<(unsigned)((count + 255) / 256), 256, 0, s>>>(flags, pidx, count, n, pair_node, pair_tile);
-  return hipGetLastError();
-}
-
-// Re[e][k] = Rp[pair of e][k]: the harmonics of each edge's sender under
-// its receiver's tile origin, in edge order (the aggregation's staging then
-// reads one contiguous block per chunk, addressed by the edge alone).  One
-// workgroup per receiver i: the pair of its edge to j is pidx[tile_of[i] * n + j].
-__global__ void k_edge_R(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ col,
-                         const int32_t* __restrict__ tile_of, const int32_t* __restrict__ pidx, int n,
-                         const float* __restrict__ Rp, int nk, float* __restrict__ Re) {
-  const int i = blockIdx.x;
-  const int64_t base = (int64_t)tile_of[i] * n, e0 = row_ptr[i], cnt = (row_ptr[i + 1] - e0) * nk;
-  for (int64_t q = threadIdx.x; q < cnt; q += blockDim.x) {
-    const int64_t e = e0 + q / nk;
-    Re[e0 * nk + q] = Rp[(size_t)pidx[base + col[e]] * nk + (int)(q % nk)];
-  }
-}
-
-hipError_t launch_edge_R(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of,
-                         const int32_t* pidx, int n, const float* Rp, int nk, float* Re, hipStream_t s) {
-  if (n > 0) k_edge_R<<<(unsigned)n, 256, 0, s>>>(row_ptr, col_idx, tile_of, pidx, n, Rp, nk, Re);
-  return hipGetLastError();
-}
-
-hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of,
-                           const int32_t* pidx, int n, int32_t* col_pair, hipStream_t s) {
-  if (n > 0) k_col_pair<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, col_idx, tile_of, pidx, n, col_pair);
-  return hipGetLastError();
-}
-
 hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* node_of, const float* feat,
                           int n_items, int C, int dh, float* T, hipStream_t s) {
   if (n_items == 0) return hipSuccess;
@@ -1755,36 +1557,6 @@ hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* no
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
-}
-
-hipError_t launch_tile_ranges(const int32_t* tile_of, const int32_t* pidx, int n, int keys, int32_t* counts,
-                              int32_t* rstart, int32_t* pstart, void* tmp, size_t tmp_bytes, hipStream_t s) {
-  hipError_t e = hipMemsetAsync(counts, 0, sizeof(int32_t) * (size_t)(keys + 1), s);
-  if (e != hipSuccess) return e;
-  if (n > 0) {
-    if (keys <= kKeyBins) k_key_counts<true><<<(n + 255) / 256, 256, 0, s>>>(tile_of, n, keys, counts);
-    else k_key_counts<false><<<(n + 255) / 256, 256, 0, s>>>(tile_of, n, keys, counts);
-  }
-  size_t b = tmp_bytes;
-  if ((e = hipcub::DeviceScan::ExclusiveSum(tmp, b, counts, rstart, keys + 1, s)) != hipSuccess) return e;
-  k_key_pstart<<<(keys + 255) / 256, 256, 0, s>>>(pidx, keys, n, pstart);
-  return hipGetLastError();
-}
-
-size_t recv_sort_tmp_bytes(int n) {
-  size_t b = 0;
-  hipcub::DeviceRadixSort::SortPairs(nullptr, b, (const uint64_t*)nullptr, (uint64_t*)nullptr,
-                                     (const int32_t*)nullptr, (int32_t*)nullptr, n);
-  return b;
-}
-
-hipError_t launch_sort_receivers(const float* pos, const int32_t* tile_of, int n, const int* lo, int64_t fine,
-                                 uint64_t* keys, uint64_t* keys_out, int32_t* vals, int32_t* order, void* tmp,
-                                 size_t tmp_bytes, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  k_recv_keys<<<(n + 255) / 256, 256, 0, s>>>(pos, tile_of, n, lo[0], lo[1], lo[2], fine, keys, vals);
-  size_t b = tmp_bytes;
-  return hipcub::DeviceRadixSort::SortPairs(tmp, b, keys, keys_out, vals, order, n, 0, 64, s);
 }
 
 size_t blocks_tmp_bytes(int nblk) {
@@ -2098,12 +1870,6 @@ hipError_t launch_alpha_head_major(const float* alpha, int64_t n_edges, int H, f
 hipError_t launch_iota(int n, int32_t* v, hipStream_t s) {
   if (n == 0) return hipSuccess;
   k_iota<<<(n + 255) / 256, 256, 0, s>>>(n, v);
-  return hipGetLastError();
-}
-
-hipError_t launch_plan_pack(const int32_t* pidx, const int32_t* flags, int64_t count, const int32_t* max_degree,
-                            const int32_t* rstart, const int32_t* pstart, int keys, int32_t* out, hipStream_t s) {
-  k_plan_pack<<<(keys + 256) / 256, 256, 0, s>>>(pidx, flags, count, max_degree, rstart, pstart, keys, out);
   return hipGetLastError();
 }
 

@@ -1,4 +1,5 @@
-// Kernel launchers of libe2f (implemented in neighbor.hip and conv.hip).
+// Kernel launchers of libe2f (implemented in neighbor.hip, plan.hip, conv.hip
+// and attention.hip).
 // All sizes are checked by the callers in abi.cpp before these run.
 #pragma once
 
@@ -83,38 +84,10 @@ hipError_t launch_sh(const DevTables& t, const float* pos, const int32_t* node_o
                      const float* origins_f, const int32_t* origin_id, int origin_mod, int n, double* out_d,
                      float* out_f, hipStream_t s);
 
-// ---- tile plan of the factorised forward
-hipError_t launch_tile_keys(const float* pos, const int32_t* graph_id, int n, const int* lo, const int* dim,
-                            const int64_t* span, int ncell, int32_t* tile_of, hipStream_t s);
-hipError_t launch_pair_flags(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of, int n,
-                             int32_t* flags, int32_t* max_degree, hipStream_t s);
-size_t scan_tmp_bytes(int64_t count);
-hipError_t launch_scan_i32(const int32_t* in, int32_t* out, int64_t count, void* tmp, size_t tmp_bytes, hipStream_t s);
-hipError_t launch_pairs(const int32_t* flags, const int32_t* pidx, int64_t count, int n, int32_t* pair_node,
-                        int32_t* pair_tile, hipStream_t s);
-// Re [E][nk] float32: Rp [pairs][nk] of each edge's pair (pidx[tile_of[i] * n + j]), in edge order
-hipError_t launch_edge_R(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of,
-                         const int32_t* pidx, int n, const float* Rp, int nk, float* Re, hipStream_t s);
-hipError_t launch_col_pair(const int64_t* row_ptr, const int32_t* col_idx, const int32_t* tile_of,
-                           const int32_t* pidx, int n, int32_t* col_pair, hipStream_t s);
-
 // ---- factorised layer
 // T stored head-major: T[item][c / dh][row][c % dh] (dh = C: plain [row][c])
 hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* node_of, const float* feat,
                           int n_items, int C, int dh, float* T, hipStream_t s);
-// receivers per tile key (counts [keys+1]), their first position in the
-// receiver order (rstart [keys+1]) and the first pair of each key (pstart [keys])
-hipError_t launch_tile_ranges(const int32_t* tile_of, const int32_t* pidx, int n, int keys, int32_t* counts,
-                              int32_t* rstart, int32_t* pstart, void* tmp, size_t tmp_bytes, hipStream_t s);
-// plan sizes for one read-back: {pidx[count-1], flags[count-1], *max_degree,
-// rstart[0..keys], pstart[0..keys)}, 3 + 2(keys+1) ints
-hipError_t launch_plan_pack(const int32_t* pidx, const int32_t* flags, int64_t count, const int32_t* max_degree,
-                            const int32_t* rstart, const int32_t* pstart, int keys, int32_t* out, hipStream_t s);
-size_t recv_sort_tmp_bytes(int n);
-// order = receivers sorted by (tile, Morton index of fine cells of side `fine` grid units)
-hipError_t launch_sort_receivers(const float* pos, const int32_t* tile_of, int n, const int* lo, int64_t fine,
-                                 uint64_t* keys, uint64_t* keys_out, int32_t* vals, int32_t* order, void* tmp,
-                                 size_t tmp_bytes, hipStream_t s);
 // Receiver blocks of 16 consecutive entries of `order`: block edge counts
 // (blk_count [nblk+1]) and offsets (blk_off [nblk+1]), the sorted union of the
 // T rows each block reads (uni [E], block b at blk_off[b]), union sizes
@@ -143,13 +116,11 @@ hipError_t launch_alpha_dnorm(const float* pos, const int64_t* row_ptr, const in
                               int64_t n_edges, int H, int L, int32_t* rows, float* alpha_f, hipStream_t s);
 // alpha_hm[h][e] = alpha[e][h]
 hipError_t launch_alpha_head_major(const float* alpha, int64_t n_edges, int H, float* alpha_hm, hipStream_t s);
-// y[order[r]] from S row r (head-major like T), r < n; shared_s: every r
-// reads S row 0
 // S rows r < n (receivers order[r]) by aggregating the uncoupled node products
-// (H heads of C/H channels, each of the caller's heads split into hdiv: the
-// attention weight of head h is alpha_hm[h / hdiv]; n_nodes bounds the senders)
 // alpha_ij R(p_j) (x) h_j and coupling per receiver (no T): Re [E][nk] float32
-// (launch_edge_R), alpha_hm [H][n_edges] or NULL (ones)
+// (launch_plan_sh), alpha_hm [H][n_edges] or NULL (ones); H heads of C/H
+// channels, each of the caller's heads split into hdiv (the attention weight
+// of head h is alpha_hm[h / hdiv]); n_nodes bounds the senders
 // with the coupling schedule of couple_schedule(tables, outer_agg_groups(L, C, H))
 // (its packed form pmeta/ptab, ntab > 0, is staged in LDS when it exists)
 bool outer_agg_supported(int L, int C, int H);
@@ -159,7 +130,9 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* 
                             const int32_t* order, const int* cmeta, const float* ccoef, const int* pmeta,
                             const float* ptab, int ntab, int ck, int cgroups, int n, int C, int H, int hdiv,
                             int n_nodes, float* S, hipStream_t s);
-// accumulate: y += the product instead of y = (one writer per element)
+// y[order[r]] from S row r (head-major like T), r < n; shared_s: every r
+// reads S row 0; accumulate: y += the product instead of y = (one writer per
+// element)
 hipError_t launch_recouple(const DevTables& t, const double* R, const float* S, bool shared_s, const int32_t* order,
                            int n, int C, int dh, float* y, hipStream_t s, bool accumulate = false);
 // The global moment of every atom's uncoupled products, coupled into one S
