@@ -240,10 +240,12 @@ e2f_status e2f_validate_graph(e2f_ctx* ctx, int32_t n, const int64_t* row_ptr, c
  * tensor alpha in R^{N x N x H}): the sum runs over all j != i.
  * alpha [N][N][H] float32 (receiver i, sender j, head); alpha[i][i][*] is
  * ignored; NULL => 1 for every pair.  One origin, the centre of the bounding
- * box.  The aggregation S_h = A_h T_h is a dense product per head (rocBLAS
- * strided-batched SGEMM, fp32).  tile_side and cutoff serve only the default
- * path weights (cutoff^-f).  N^2 H must stay below 4e9.  Workspace: about
- * N(2 dimT C + N H) floats.  (sync: one small device->host read) */
+ * box (found on the device).  T_j is stored for every atom and the
+ * aggregation S_h = A_h T_h is a dense product per head on the matrix cores
+ * (fp32, a hand-written tiled kernel).  tile_side and cutoff serve only the
+ * default path weights (cutoff^-f).  N^2 H must stay below 4e9.  Internal
+ * workspace: about N (2 dimT C + N H) floats.  Positions must be finite with
+ * |x| < 16384 A (not reported). */
 e2f_status e2f_wigner6j_conv_forward_dense(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
                                            const float* feat, int32_t n, const float* alpha, float* out,
                                            void* stream);
@@ -257,9 +259,10 @@ e2f_status e2f_wigner6j_conv_forward_dense(e2f_ctx* ctx, const e2f_conv_params* 
  * the intermediates (every head sees the same weights); tile_side is unused.
  * out: [N][(L+1)^2][C].  The moments are taken of the uncoupled products,
  * G = sum_j R(r_j - o) (x) h_j, summed in float64 in a fixed order
- * (deterministic), and coupled once.  Workspace: N (L+1)^2 doubles plus
- * float64 partial sums of G (about 2048 (L+1)^2 * 256 doubles, some 10-25 MB).
- * (sync: one small device->host read) */
+ * (deterministic), and coupled once.  Internal workspace: N (L+1)^2 doubles
+ * plus float64 partial sums of G (about 2048 (L+1)^2 * 256 doubles, some
+ * 10-25 MB).  The centre is found on the device: positions must be finite
+ * with |x| < 16384 A (not reported). */
 e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params* params, const float* pos,
                                             const float* feat, int32_t n, float* out, void* stream);
 

@@ -16,7 +16,6 @@
 
 #include "../../include/e2f.h"
 
-#include <rocblas/rocblas.h>
 #include "e2f_internal.h"
 #include "e2f_launch.h"
 
@@ -75,7 +74,6 @@ struct e2f_ctx {
   int64_t* pinned = nullptr;               // host, 16 int64
   int32_t* pinned_plan = nullptr;          // host, plan sizes read back in one copy
   size_t pinned_plan_n = 0;
-  std::vector<double> origins_host;
   Buf a, b, c;
   Buf d;                                   // backward staging (transposed graph, input gradient)
   std::vector<std::vector<double>> kappa;  // per L: [a][f][o] real CG transpose factors (0 = not computed)
@@ -88,7 +86,6 @@ struct e2f_ctx {
   };
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
-  rocblas_handle blas = nullptr;  // created on the first dense-graph forward
   // coupling schedules of the aggregation of uncoupled products, per (L, groups)
   struct Couple {
     int k = 0, ntab = 0;
@@ -763,7 +760,6 @@ void e2f_destroy(e2f_ctx* ctx) {
         if (c.mem) (void)hipFree(c.mem);
     for (Buf* b : {&ctx->a, &ctx->b, &ctx->c, &ctx->d})
       if (b->p) (void)hipFree(b->p);
-    if (ctx->blas) (void)rocblas_destroy_handle(ctx->blas);
     for (auto& kv : ctx->couple) {
       if (kv.second.meta) (void)hipFree(kv.second.meta);
       if (kv.second.coef) (void)hipFree(kv.second.coef);
@@ -1191,52 +1187,31 @@ e2f_status e2f_wigner6j_conv_forward_dense(e2f_ctx* ctx, const e2f_conv_params* 
   if ((rs = coef_of(ctx, L, path_weights(p), true, cs)) != E2F_OK) return rs;
   if (n == 0) return E2F_OK;
   const DevTables t = with_coef(ctx, L, *cs);
-  int st[kStatsInts];
-  rs = run_bbox(ctx, pos, nullptr, n, s, st);
-  if (rs != E2F_OK) return rs;
-  // one origin, the centre of the bounding box (the products couple every pair)
-  double origin[3];
-  for (int k = 0; k < 3; ++k) origin[k] = (((int64_t)st[k] + st[3 + k]) / 2) / kGrid;
   const size_t rowb = sizeof(float) * (size_t)t.dimT * C;
   const bool mixing = p->mix_w != nullptr;
-  const size_t need = al256(sizeof(double) * 3) + al256(sizeof(double) * (size_t)n * nk) +
-                      2 * al256(rowb * (size_t)n) + al256(sizeof(float) * (size_t)n * n * H) +
+  const size_t need = al256(sizeof(int) * 16) + al256(sizeof(double) * 3) + al256(sizeof(double) * (size_t)n * nk) +
+                      2 * al256(rowb * (size_t)n) + al256(sizeof(float) * (size_t)n * dense_lda(n) * H) +
                       al256(sizeof(int32_t) * (size_t)n) + (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
   rs = ensure(ctx, ctx->b, need, s);
   if (rs != E2F_OK) return rs;
   Carver cb{(char*)ctx->b.p};
+  int* stats = cb.take<int>(16);
   double* org = cb.take<double>(3);
   double* R = cb.take<double>((size_t)n * nk);
   float* T = cb.take<float>((size_t)n * t.dimT * C);
   float* S = cb.take<float>((size_t)n * t.dimT * C);
-  float* A = cb.take<float>((size_t)n * n * H);
+  float* A = cb.take<float>((size_t)n * dense_lda(n) * H);
   int32_t* order = cb.take<int32_t>((size_t)n);
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
-  ctx->origins_host.assign(origin, origin + 3);
-  E2F_HIP(hipMemcpyAsync(org, ctx->origins_host.data(), sizeof(double) * 3, hipMemcpyHostToDevice, s));
+  // one origin, the centre of the bounding box (the products couple every
+  // pair), found on the device
+  E2F_TIMED("bbox", launch_plan_bbox(pos, nullptr, n, stats, nullptr, s));
+  E2F_TIMED("bbox", launch_plan_centre(stats, org, s));
   E2F_TIMED("sh", launch_sh(t, pos, nullptr, org, nullptr, nullptr, 1, n, R, nullptr, s));
   E2F_TIMED("node_tp", launch_node_tp(t, R, nullptr, feat, n, C, dh, T, s));
   E2F_TIMED("tile_plan", launch_dense_alpha(alpha, n, H, A, s));
   E2F_TIMED("tile_plan", launch_iota(n, order, s));
-  if (!ctx->blas) {
-    if (rocblas_create_handle(&ctx->blas) != rocblas_status_success) {
-      ctx->blas = nullptr;
-      return fail(E2F_EDEVICE, "rocblas_create_handle failed");
-    }
-  }
-  if (rocblas_set_stream(ctx->blas, s) != rocblas_status_success) return fail(E2F_EDEVICE, "rocblas_set_stream failed");
-  // per head: S_h^T (W x N) = T_h^T (W x N) . A_h^T (N x N) in column-major terms,
-  // T_h^T and S_h^T with leading dimension dimT*C, A_h^T = A_h stored row-major
-  const rocblas_int W = t.dimT * dh, ld = t.dimT * C;
-  const float one = 1.0f, zero = 0.0f;
-  {
-    Timed tm_(ctx, "aggregate", s);
-    const rocblas_status bs = rocblas_sgemm_strided_batched(ctx->blas, rocblas_operation_none, rocblas_operation_none,
-                                                            W, n, n, &one, T, ld, W, A, n, (rocblas_stride)n * n,
-                                                            &zero, S, ld, W, H);
-    if (bs != rocblas_status_success)
-      return fail(E2F_EDEVICE, "rocblas_sgemm_strided_batched: %s", rocblas_status_to_string(bs));
-  }
+  E2F_TIMED("aggregate", launch_dense_aggregate(A, n, T, t.dimT, C, H, S, s));
   E2F_TIMED("recouple", launch_recouple(t, R, S, false, order, n, C, dh, y, s));
   if (mixing) E2F_TIMED("mix", launch_mix(L, y, p->mix_w, p->mix_dtype == E2F_BF16, n, C, out, s));
   return E2F_OK;
@@ -1257,24 +1232,19 @@ e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params*
   if ((rs = coef_of(ctx, L, path_weights(p), true, cs)) != E2F_OK) return rs;
   if (n == 0) return E2F_OK;
   const DevTables t = with_coef(ctx, L, *cs);
-  int st[kStatsInts];
-  rs = run_bbox(ctx, pos, nullptr, n, s, st);
-  if (rs != E2F_OK) return rs;
-  // one origin, the centre of the bounding box (every pair is coupled)
-  double origin[3];
-  for (int k = 0; k < 3; ++k) origin[k] = (((int64_t)st[k] + st[3 + k]) / 2) / kGrid;
   // the moment of the uncoupled products G[be][(q, c)] = sum_j R_be(p_j) h_j[q][c]
   // (fp64, fixed order), coupled once into the shared S row
   const int64_t W = (int64_t)t.dimT * C, WG = (int64_t)nk * nk * C;
   const int G = global_groups(n, nk, C);
   const bool mixing = p->mix_w != nullptr;
-  const size_t need = al256(sizeof(double) * 3) + al256(sizeof(double) * (size_t)n * nk) +
+  const size_t need = al256(sizeof(int) * 16) + al256(sizeof(double) * 3) + al256(sizeof(double) * (size_t)n * nk) +
                       al256(sizeof(double) * (size_t)G * WG) + al256(sizeof(double) * (size_t)WG) +
                       al256(sizeof(float) * (size_t)W) + al256(sizeof(int32_t) * (size_t)n) +
                       (mixing ? al256(sizeof(float) * (size_t)n * nk * C) : 0);
   rs = ensure(ctx, ctx->b, need, s);
   if (rs != E2F_OK) return rs;
   Carver cb{(char*)ctx->b.p};
+  int* stats = cb.take<int>(16);
   double* org = cb.take<double>(3);
   double* R = cb.take<double>((size_t)n * nk);
   double* part = cb.take<double>((size_t)G * WG);
@@ -1282,8 +1252,9 @@ e2f_status e2f_wigner6j_conv_forward_global(e2f_ctx* ctx, const e2f_conv_params*
   float* M32 = cb.take<float>((size_t)W);
   int32_t* order = cb.take<int32_t>((size_t)n);
   float* y = mixing ? cb.take<float>((size_t)n * nk * C) : out;
-  ctx->origins_host.assign(origin, origin + 3);
-  E2F_HIP(hipMemcpyAsync(org, ctx->origins_host.data(), sizeof(double) * 3, hipMemcpyHostToDevice, s));
+  // one origin, the centre of the bounding box (every pair is coupled), found on the device
+  E2F_TIMED("bbox", launch_plan_bbox(pos, nullptr, n, stats, nullptr, s));
+  E2F_TIMED("bbox", launch_plan_centre(stats, org, s));
   E2F_TIMED("sh", launch_sh(t, pos, nullptr, org, nullptr, nullptr, 1, n, R, nullptr, s));
   E2F_TIMED("aggregate", launch_global_moment(t, R, feat, n, C, dh, part, G64, M32, s));
   E2F_TIMED("tile_plan", launch_iota(n, order, s));

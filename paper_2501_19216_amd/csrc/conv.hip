@@ -1332,15 +1332,6 @@ __global__ void k_transpose_mix(const E* __restrict__ W, int L1, int C, E* __res
 // Every atom attends to every other (the dense graphs of the scaling study,
 // Sec. 4.1): the aggregation S_h = A_h T_h is a dense product with
 // A_h[i][j] = alpha[i][j][h] for j != i and 0 on the diagonal.
-__global__ void k_dense_alpha(const float* __restrict__ alpha, int n, int H, float* __restrict__ A) {
-  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (h, i, j)
-  const int64_t nn = (int64_t)n * n;
-  if (q >= nn * H) return;
-  const int h = (int)(q / nn);
-  const int64_t ij = q - (int64_t)h * nn;
-  const int i = (int)(ij / n), j = (int)(ij - (int64_t)i * n);
-  A[q] = i == j ? 0.0f : (alpha ? alpha[ij * H + h] : 1.0f);
-}
 
 // Global moments of the uncoupled products (App. G with every pair weighted
 // alike): G[be][col] = sum_j R_be(p_j) h_j[col], col = q*C + c over the
@@ -1817,13 +1808,6 @@ hipError_t launch_edge_tp(const DevTables& t, const float* pos, const float* fea
   return hipGetLastError();
 }
 
-hipError_t launch_dense_alpha(const float* alpha, int n, int H, float* A, hipStream_t s) {
-  const int64_t total = (int64_t)n * n * H;
-  if (total == 0) return hipSuccess;
-  if ((total + 255) / 256 > 0x7fffffff) return hipErrorInvalidValue;
-  k_dense_alpha<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(alpha, n, H, A);
-  return hipGetLastError();
-}
 
 int global_groups(int n, int nk, int C) {
   const int colblocks = (nk * C + 255) / 256;

@@ -31,6 +31,8 @@ hipError_t launch_plan_bbox(const float* pos, const int32_t* graph_id, int n, in
                             hipStream_t s);
 hipError_t launch_plan_dmin(const float* pos, const int32_t* rows, const int32_t* col, int n, int64_t n_edges,
                             unsigned* dmin, hipStream_t s);
+// origin [3] float64 = the centre of the bounding box in stats
+hipError_t launch_plan_centre(const int* stats, double* origin, hipStream_t s);
 // side in grid units; with dmin, side = min(side, dmin_scale * shortest edge)
 hipError_t launch_plan_grid(const int* stats, const unsigned* dmin, double side, double dmin_scale, bool graphs,
                             TileGridDev* grid, hipStream_t s);
@@ -178,8 +180,13 @@ hipError_t launch_transpose_graph(const int64_t* row_ptr, const int32_t* col_idx
 // WT[o][c][c'] = W[o][c'][c], float32 or bf16 elements
 hipError_t launch_transpose_mix(const void* W, bool bf16, int L, int C, void* WT, hipStream_t s);
 
-// ---- dense graphs: A[h][i][j] = alpha[i][j][h] (1 if alpha is NULL), 0 for i == j
+// ---- dense graphs (dense.hip): A[h][i][j] = alpha[i][j][h] (1 if alpha is
+// NULL), 0 for i == j, rows of dense_lda(n) floats (zero padding)
+int dense_lda(int n);
 hipError_t launch_dense_alpha(const float* alpha, int n, int H, float* A, hipStream_t s);
+// S_h = A_h T_h per head on MFMA: T and S head-major [n][H][dimT][C/H]
+hipError_t launch_dense_aggregate(const float* A, int n, const float* T, int dimT, int C, int H, float* S,
+                                  hipStream_t s);
 hipError_t launch_iota(int n, int32_t* v, hipStream_t s);
 
 // ---- per-irrep channel mixing and the edge baseline

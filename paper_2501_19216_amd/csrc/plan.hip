@@ -241,6 +241,16 @@ __global__ void k_fill(float* __restrict__ p, int64_t count, float v) {
     p[q] = v;
 }
 
+// The centre of the bounding box (grid units halved exactly, as on the host
+// before), in Angstrom; the box of no finite position is the origin.
+__global__ void k_plan_centre(const int* __restrict__ st, double* __restrict__ org) {
+  if (threadIdx.x < 3) {
+    const int k = threadIdx.x;
+    const bool empty = st[k] > st[3 + k];
+    org[k] = empty ? 0.0 : (double)((((int64_t)st[k] + st[3 + k]) / 2)) / kGrid;
+  }
+}
+
 // Graph check: bit 1 row_ptr[0] != 0, bit 2 a row end below its start,
 // bit 4 row_ptr[n] != E, bit 8 a sender outside [0, n).
 __global__ void k_validate_rows(const int64_t* __restrict__ row_ptr, int n, int64_t n_edges, int* __restrict__ bad) {
@@ -265,6 +275,11 @@ hipError_t launch_plan_bbox(const float* pos, const int32_t* graph_id, int n, in
                             hipStream_t s) {
   k_plan_init<<<1, 64, 0, s>>>(stats, dmin);
   if (n > 0) k_plan_bbox<<<(n + 255) / 256, 256, 0, s>>>(pos, graph_id, n, stats);
+  return hipGetLastError();
+}
+
+hipError_t launch_plan_centre(const int* stats, double* origin, hipStream_t s) {
+  k_plan_centre<<<1, 64, 0, s>>>(stats, origin);
   return hipGetLastError();
 }
 
