@@ -577,7 +577,7 @@ FwdLayout fwd_layout(const e2f_conv_params* p, int n, int64_t E, bool have_alpha
   f.Rr = take(sizeof(double) * (size_t)n * nk);
   const size_t na = ynorm ? (size_t)(L + 1) : (have_alpha ? 1 : 0);
   f.alpha_hm = take(sizeof(float) * (size_t)E * H * na);
-  f.erows = take(ynorm ? sizeof(int32_t) * (size_t)E : 0);
+  f.erows = take(sizeof(int32_t) * (size_t)E);
   f.y = take(p->mix_w ? sizeof(float) * (size_t)n * nk * C : 0);
   f.S = off;
   f.fixed = off;
@@ -651,10 +651,10 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
   // ---- plan: bounding box, attention weights head-major (per filter degree
   // under alpha / D^f, with the shortest edge), tile grid, receiver order,
   // solid harmonics of the edges and receivers
+  int32_t* erows = (int32_t*)(ws + f.erows);
   E2F_TIMED("bbox", launch_plan_bbox(pos, graph_id, n, stats, ynorm ? dmin : nullptr, s));
+  E2F_TIMED("tile_plan", launch_plan_edge_rows(row_ptr, n, n_edges, erows, s));
   if (ynorm) {
-    int32_t* erows = (int32_t*)(ws + f.erows);
-    E2F_TIMED("alpha_hm", launch_plan_edge_rows(row_ptr, n, n_edges, erows, s));
     E2F_TIMED("alpha_hm", launch_plan_dmin(pos, erows, col_idx, n, n_edges, dmin, s));
     E2F_TIMED("alpha_hm", launch_alpha_dnorm(pos, nullptr, col_idx, alpha, n, n_edges, H, L, erows, alpha_hm, s));
   } else if (alpha) {
@@ -666,7 +666,7 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
   E2F_TIMED("tile_plan", launch_plan_order(pos, graph_id, n, grid, tile_of, (uint64_t*)(ws + f.keys),
                                            (uint64_t*)(ws + f.keys_out), (int32_t*)(ws + f.vals), order,
                                            ws + f.sort_tmp, f.sort_b, s));
-  E2F_TIMED("sh", launch_plan_sh(t, pos, row_ptr, col_idx, n, n_edges, tile_of, grid, Rr, Re, s));
+  E2F_TIMED("sh", launch_plan_sh(t, pos, erows, col_idx, n, n_edges, tile_of, grid, Rr, Re, s));
   // ---- aggregation and recouple per slice of receivers (S of one slice
   // at a time in the workspace)
   const int64_t slice = std::min<int64_t>(n, (int64_t)((workspace_bytes - f.fixed) / f.s_row));

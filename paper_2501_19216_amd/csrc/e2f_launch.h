@@ -42,8 +42,9 @@ hipError_t launch_plan_order(const float* pos, const int32_t* graph_id, int n, c
                              int32_t* tile_of, uint64_t* keys, uint64_t* keys_out, int32_t* vals, int32_t* order,
                              void* tmp, size_t tmp_bytes, hipStream_t s);
 // Rr [n][nk] float64 (receivers) and Re [E][nk] float32 (senders, CSR order),
-// both about the receiver's tile centre
-hipError_t launch_plan_sh(const DevTables& t, const float* pos, const int64_t* row_ptr, const int32_t* col, int n,
+// both about the receiver's tile centre; rows [E]: the receiver of every
+// edge (launch_plan_edge_rows)
+hipError_t launch_plan_sh(const DevTables& t, const float* pos, const int32_t* rows, const int32_t* col, int n,
                           int64_t n_edges, const int32_t* tile_of, const TileGridDev* grid, double* Rr, float* Re,
                           hipStream_t s);
 hipError_t launch_plan_edge_rows(const int64_t* row_ptr, int n, int64_t n_edges, int32_t* rows, hipStream_t s);

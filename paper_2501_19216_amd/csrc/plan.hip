@@ -195,45 +195,42 @@ __global__ __launch_bounds__(256) void k_plan_node_sh(DevTables t, const float* 
 }
 
 // Solid harmonics of every edge's sender about its receiver's tile centre,
-// fp32 [E][nk] in CSR order.  One wave per receiver, a lane per edge; the
-// values pass through LDS so that the wave stores whole rows contiguously.
+// fp32 [E][nk] in CSR order.  A thread per edge (rows: the receiver of every
+// edge), 256 consecutive edges per workgroup; the values pass through LDS so
+// that the workgroup stores its 256 rows as one contiguous block.
 template <int L>
-__global__ __launch_bounds__(64) void k_plan_edge_sh(DevTables t, const float* __restrict__ pos,
-                                                     const int64_t* __restrict__ row_ptr,
-                                                     const int32_t* __restrict__ col, int n, int64_t n_edges,
-                                                     const int32_t* __restrict__ tile_of,
-                                                     const TileGridDev* __restrict__ gp, float* __restrict__ Re) {
+__global__ __launch_bounds__(256) void k_plan_edge_sh(DevTables t, const float* __restrict__ pos,
+                                                      const int32_t* __restrict__ rows,
+                                                      const int32_t* __restrict__ col, int n, int64_t n_edges,
+                                                      const int32_t* __restrict__ tile_of,
+                                                      const TileGridDev* __restrict__ gp, float* __restrict__ Re) {
   constexpr int NK = (L + 1) * (L + 1), NKP = NK | 1;  // odd row stride: conflict-free LDS stores
-  __shared__ float buf[64 * NKP];
-  const int i = blockIdx.x, lane = threadIdx.x;
-  const TileGridDev g = *gp;
-  double ox, oy, oz;
-  tile_centre(g, tile_of[i] % g.ncell, ox, oy, oz);
-  int64_t e0, e1;
-  row_bounds(row_ptr, i, n_edges, e0, e1);
-  for (int64_t c0 = e0; c0 < e1; c0 += 64) {
-    const int cnt = (int)min((int64_t)64, e1 - c0);
-    if (lane < cnt) {
-      const int j = clamp_node(col[c0 + lane], n);
-      float* b = buf + lane * NKP;
-      sh_all<L>(t, (double)pos[3 * j] - ox, (double)pos[3 * j + 1] - oy, (double)pos[3 * j + 2] - oz,
-                [&](int k, double v) { b[k] = (float)v; });
-    }
-    __syncthreads();  // one wave per workgroup: orders the LDS stores before the reads
-    float* dst = Re + (size_t)c0 * NK;
-    for (int q = lane; q < cnt * NK; q += 64) dst[q] = buf[(q / NK) * NKP + q % NK];
-    __syncthreads();
+  __shared__ float buf[256 * NKP];
+  const int64_t e0 = (int64_t)blockIdx.x * 256, e = e0 + threadIdx.x;
+  const int cnt = (int)min((int64_t)256, n_edges - e0);
+  if (e < n_edges) {
+    const TileGridDev g = *gp;
+    const int i = clamp_node(rows[e], n), j = clamp_node(col[e], n);
+    double ox, oy, oz;
+    tile_centre(g, tile_of[i] % g.ncell, ox, oy, oz);
+    float* b = buf + threadIdx.x * NKP;
+    sh_all<L>(t, (double)pos[3 * j] - ox, (double)pos[3 * j + 1] - oy, (double)pos[3 * j + 2] - oz,
+              [&](int k, double v) { b[k] = (float)v; });
   }
+  __syncthreads();
+  float* dst = Re + e0 * NK;
+  for (int q = threadIdx.x; q < cnt * NK; q += 256) dst[q] = buf[(q / NK) * NKP + q % NK];
 }
 
 // The receiver of every edge (rows [E]), clamped like every CSR read.
-__global__ void k_plan_edge_rows(const int64_t* __restrict__ row_ptr, int n, int64_t n_edges,
-                                 int32_t* __restrict__ rows) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+// A wave per receiver, its lanes over the receiver's edges.
+__global__ __launch_bounds__(256) void k_plan_edge_rows(const int64_t* __restrict__ row_ptr, int n, int64_t n_edges,
+                                                        int32_t* __restrict__ rows) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (i >= n) return;
   int64_t e0, e1;
   row_bounds(row_ptr, i, n_edges, e0, e1);
-  for (int64_t e = e0; e < e1; ++e) rows[e] = i;
+  for (int64_t e = e0 + lane; e < e1; e += 64) rows[e] = i;
 }
 
 __global__ void k_fill(float* __restrict__ p, int64_t count, float v) {
@@ -313,15 +310,18 @@ hipError_t launch_plan_order(const float* pos, const int32_t* graph_id, int n, c
   return hipcub::DeviceRadixSort::SortPairs(tmp, b, keys, keys_out, vals, order, n, 0, graph_id ? 64 : 30, s);
 }
 
-hipError_t launch_plan_sh(const DevTables& t, const float* pos, const int64_t* row_ptr, const int32_t* col, int n,
+hipError_t launch_plan_sh(const DevTables& t, const float* pos, const int32_t* rows, const int32_t* col, int n,
                           int64_t n_edges, const int32_t* tile_of, const TileGridDev* grid, double* Rr, float* Re,
                           hipStream_t s) {
   if (n == 0) return hipSuccess;
+  const int64_t eblocks = (n_edges + 255) / 256;
+  if (eblocks > 0x7fffffff) return hipErrorInvalidValue;
   switch (t.L) {
 #define E2F_SH(LL)                                                                                          \
   case LL:                                                                                                  \
     k_plan_node_sh<LL><<<(n + 255) / 256, 256, 0, s>>>(t, pos, n, tile_of, grid, Rr);                       \
-    if (n_edges > 0) k_plan_edge_sh<LL><<<n, 64, 0, s>>>(t, pos, row_ptr, col, n, n_edges, tile_of, grid, Re); \
+    if (eblocks > 0)                                                                                        \
+      k_plan_edge_sh<LL><<<(unsigned)eblocks, 256, 0, s>>>(t, pos, rows, col, n, n_edges, tile_of, grid, Re); \
     break;
     E2F_SH(0) E2F_SH(1) E2F_SH(2) E2F_SH(3) E2F_SH(4) E2F_SH(5) E2F_SH(6)
 #undef E2F_SH
@@ -331,7 +331,7 @@ hipError_t launch_plan_sh(const DevTables& t, const float* pos, const int64_t* r
 }
 
 hipError_t launch_plan_edge_rows(const int64_t* row_ptr, int n, int64_t n_edges, int32_t* rows, hipStream_t s) {
-  if (n > 0) k_plan_edge_rows<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, n, n_edges, rows);
+  if (n > 0) k_plan_edge_rows<<<(n + 3) / 4, 256, 0, s>>>(row_ptr, n, n_edges, rows);
   return hipGetLastError();
 }
 
