@@ -80,24 +80,34 @@ def central_crop(pos, side):
     return np.nonzero(keep)[0]
 
 
-def alg_counts(e2f, L, C, H, n, E):
+def alg_counts(e2f, L, C, H, n, E, fused=False):
     """Algorithmic work of the forward's kernels (per launch over the whole
     graph), counted from the real-basis tables: the aggregation as the
     factorised layer's a3 (dimT multiply-adds per edge and channel) plus the
     j-side coupling of every receiver (a2); the recouple (a4); the mixing
-    (a5); and the compulsory bytes each kernel moves."""
+    (a5); and the compulsory bytes each kernel moves.  fused: the aggregation
+    applies the recouple itself (a2 + a3 + a4 in one kernel, y written
+    instead of S, and the per-receiver matrix F_i read)."""
     cnt = layer_counts(L)
     dimT, nk = cnt["dimT"], (L + 1) ** 2
     cpl = coupling_entries(e2f, L)
-    mp = 16 * ((nk + 15) // 16)  # components of R per MFMA tile column, padded to 16
-    agg = dict(flops=2.0 * E * dimT * C + 2.0 * n * cpl * C,
-               bytes=4.0 * n * nk * C + 4.0 * E * nk + 4.0 * E * H + 4.0 * E + 8.0 * (n + 1) + 4.0 * n * dimT * C,
-               issued_flops=2.0 * E * mp * nk * C + 2.0 * n * cpl * C)
+    mt = (nk + 15) // 16
+    mp = 16 * mt  # components of R per MFMA tile column, padded to 16
+    inputs = 4.0 * n * nk * C + 4.0 * E * nk + 4.0 * E * H + 4.0 * E + 8.0 * (n + 1)
+    if fused:
+        # issued: the products, then per receiver and head of 16 channels one
+        # 16x16x4 MFMA per (component q, row tile, K tile, K step)
+        agg = dict(flops=2.0 * E * dimT * C + 2.0 * n * (cpl + cnt["q_slots"]) * C,
+                   bytes=inputs + 4.0 * n * nk * nk * nk + 4.0 * n * nk * C,
+                   issued_flops=2.0 * E * mp * nk * C + 2.0 * n * (C // 16) * nk * mt * mt * 4 * 1024)
+    else:
+        agg = dict(flops=2.0 * E * dimT * C + 2.0 * n * cpl * C, bytes=inputs + 4.0 * n * dimT * C,
+                   issued_flops=2.0 * E * mp * nk * C + 2.0 * n * cpl * C)
     rec = dict(flops=2.0 * n * cnt["q_slots"] * C, bytes=4.0 * n * dimT * C + 4.0 * n * nk * C + 8.0 * n * nk)
     mix = dict(flops=2.0 * n * nk * C * C, bytes=8.0 * n * nk * C + 4.0 * (L + 1) * C * C)
     # the whole forward, fused: inputs and output once (h, positions, CSR,
     # attention weights, mixing weights, out), all the arithmetic above
-    fwd = dict(flops=agg["flops"] + rec["flops"] + mix["flops"],
+    fwd = dict(flops=2.0 * E * dimT * C + 2.0 * n * (cpl + cnt["q_slots"]) * C + mix["flops"],
                bytes=4.0 * n * nk * C * 2 + 12.0 * n + 4.0 * E + 8.0 * (n + 1) + 4.0 * E * H + 4.0 * (L + 1) * C * C)
     return dict(aggregate=agg, recouple=rec, mix=mix, forward=fwd, dimT=dimT, coupling_entries=cpl,
                 recouple_entries=cnt["q_slots"])
@@ -411,6 +421,16 @@ def main():
     for _ in range(2):
         fwd_only(), edge_only()
     ms_fwd = timed(fwd_only, args.steps)
+    # the two-kernel form of the same layer (S written, then recoupled; the
+    # context's own workspace, sized on the first call)
+    out_s = torch.empty_like(feat)
+
+    def fwd_split():
+        e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col, alpha, L, H, wl.cutoff, mix_w=mix_w,
+                                      graph_id=gid, out=out_s, split_recouple=True)
+
+    fwd_split()
+    ms_fwd_split = timed(fwd_split, args.steps)
     ms_edge = timed(edge_only, args.steps)
     ms_nl = timed(nl_only, args.steps)
     # the attention weights of the same graph (q.k over 16 dims per head + 8 radial functions)
@@ -445,7 +465,8 @@ def main():
           flush=True)
 
     kernels = {k: dict(launches=v[0] // args.steps, ms=v[1] / args.steps) for k, v in prof.items()}
-    counts = alg_counts(e2f, L, C, H, n, E)
+    fused = "fuse_build" in prof  # the aggregation applied the recouple itself
+    counts = alg_counts(e2f, L, C, H, n, E, fused)
     peaks = {"aggregate": FP32_MFMA_PEAK_TFS, "recouple": FP32_MFMA_PEAK_TFS, "mix": FP32_MFMA_PEAK_TFS}
     for k, v in kernels.items():
         if k in peaks:
@@ -560,7 +581,7 @@ def main():
                    "cutoff": wl.cutoff, "mix": "fp32", "step": "radius graph + Wigner-6j conv forward"},
         "edges_per_s": E / (ms_step * 1e-3),
         "fwd": {"ms": ms_fwd, "atoms_per_s": n / (ms_fwd * 1e-3), "edges_per_s": E / (ms_fwd * 1e-3),
-                "roofline": floor},
+                "roofline": floor, "recouple_in_aggregation": fused, "two_kernel_ms": ms_fwd_split},
         "edge_tp": {"ms": ms_edge, "atoms_per_s": n / (ms_edge * 1e-3), "edges_per_s": E / (ms_edge * 1e-3)},
         "speedup_vs_edge_tp": ms_edge / ms_fwd,
         "fwd_bf16_mix": bf16_res,

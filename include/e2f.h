@@ -159,6 +159,12 @@ typedef struct {
                             shortest nonzero edge (found on the device), keeping that ratio
                             below 5.  Forward entry points only (the backward returns
                             E2F_EUNSUPPORTED) */
+  int32_t split_recouple; /* 0: up to L = 4, with heads whose width is a multiple of 16 and
+                            y_norm 0, the aggregation applies the i-side recouple itself (the
+                            j-side coupling and the recouple of Thm. 3.3 composed into one
+                            (L+1)^2 x (L+1)^4 matrix per receiver), so S is never stored;
+                            elsewhere S is written and recoupled by a second kernel.
+                            1: always the second form (the same result up to rounding order) */
 } e2f_conv_params;
 
 /* Workspace of e2f_wigner6j_conv_forward for n atoms and n_edges edges:

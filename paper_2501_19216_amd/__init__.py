@@ -39,7 +39,8 @@ class E2FError(RuntimeError):
 class ConvParams(ctypes.Structure):
     _fields_ = [("lmax", ctypes.c_int), ("channels", ctypes.c_int32), ("heads", ctypes.c_int32),
                 ("cutoff", ctypes.c_float), ("path_w", ctypes.c_void_p), ("mix_w", ctypes.c_void_p),
-                ("mix_dtype", ctypes.c_int), ("tile_side", ctypes.c_float), ("y_norm", ctypes.c_int32)]
+                ("mix_dtype", ctypes.c_int), ("tile_side", ctypes.c_float), ("y_norm", ctypes.c_int32),
+                ("split_recouple", ctypes.c_int32)]
 
 
 def _load():
@@ -272,7 +273,7 @@ def e2f_node_tp(ctx: Context, pos: torch.Tensor, feat: torch.Tensor, lmax: int, 
     return out
 
 
-def _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm=False):
+def _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm=False, split_recouple=False):
     import numpy as np
     keep = None
     pw = None
@@ -290,7 +291,7 @@ def _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm=Fals
         if not mix_w.is_cuda or not mix_w.is_contiguous():
             raise ValueError("mix_w must be a contiguous device tensor")
     prm = ConvParams(lmax, channels, heads, cutoff, pw, None if mix_w is None else mix_w.data_ptr(), mix_dtype,
-                     float(tile_side), int(bool(y_norm)))
+                     float(tile_side), int(bool(y_norm)), int(bool(split_recouple)))
     return prm, keep
 
 
@@ -308,10 +309,10 @@ def _conv_args(pos, feat, row_ptr, col_idx, alpha, graph_id, out):
 
 
 def e2f_wigner6j_workspace_size(ctx, n, n_edges, lmax, channels, heads, cutoff, path_w=None, mix_w=None,
-                                tile_side=0.0, y_norm=False, minimum=False) -> int:
+                                tile_side=0.0, y_norm=False, minimum=False, split_recouple=False) -> int:
     """Workspace bytes of the forward (the one-pass size, or with minimum=True
     the smallest size it accepts)."""
-    prm, keep = _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm)
+    prm, keep = _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm, split_recouple)
     b = ctypes.c_size_t(0)
     fn = lib.e2f_wigner6j_workspace_min if minimum else lib.e2f_wigner6j_workspace_size
     _check(fn(ctx.handle, ctypes.byref(prm), n, n_edges, ctypes.byref(b)),
@@ -321,23 +322,26 @@ def e2f_wigner6j_workspace_size(ctx, n, n_edges, lmax, channels, heads, cutoff, 
 
 
 def e2f_wigner6j_prepare(ctx, lmax, channels, heads, cutoff, path_w=None, mix_w=None, tile_side=0.0,
-                         y_norm=False) -> None:
+                         y_norm=False, split_recouple=False) -> None:
     """Upload the coefficient set and coupling schedule these parameters use."""
-    prm, keep = _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm)
+    prm, keep = _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm, split_recouple)
     _check(lib.e2f_wigner6j_prepare(ctx.handle, ctypes.byref(prm)), "e2f_wigner6j_prepare")
     del keep
 
 
 def e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None, mix_w=None,
-                              graph_id=None, tile_side=0.0, out=None, y_norm=False, workspace=None):
+                              graph_id=None, tile_side=0.0, out=None, y_norm=False, workspace=None,
+                              split_recouple=False):
     """Wigner-6j convolution forward; returns out [N,(L+1)^2,C] float32.
     y_norm: attention weights alpha / |r_i - r_j|^f per filter degree f.
     workspace: a uint8 device tensor (any size from the minimum up); None
-    uses the context's own, grown to the one-pass size."""
+    uses the context's own, grown to the one-pass size.
+    split_recouple: write S and recouple it in a second kernel even where the
+    aggregation could apply the recouple itself."""
     out = _conv_args(pos, feat, row_ptr, col_idx, alpha, graph_id, out)
     n, nk, C = feat.shape
     E = col_idx.numel()
-    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm)
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm, split_recouple)
     if workspace is None:
         b = ctypes.c_size_t(0)
         _check(lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm), n, E, ctypes.byref(b)),
@@ -354,13 +358,14 @@ def e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, hea
 
 
 def e2f_wigner6j_conv_forward_noalloc(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None,
-                                      mix_w=None, graph_id=None, tile_side=0.0, out=None, y_norm=False):
+                                      mix_w=None, graph_id=None, tile_side=0.0, out=None, y_norm=False,
+                                      split_recouple=False):
     """The forward in the library's per-GPU scratch memory (no allocation;
     the parameters must have been prepared).  out must be given by callers
     that cannot allocate: with out=None the binding allocates it."""
     out = _conv_args(pos, feat, row_ptr, col_idx, alpha, graph_id, out)
     n, nk, C = feat.shape
-    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm)
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm, split_recouple)
     st = lib.e2f_wigner6j_conv_forward_noalloc(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(graph_id), _ptr(feat),
                                                n, _ptr(row_ptr), _ptr(col_idx), col_idx.numel(), _ptr(alpha),
                                                _ptr(out), _stream(feat.device))

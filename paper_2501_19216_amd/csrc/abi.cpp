@@ -65,6 +65,10 @@ struct e2f_ctx {
     const double* rc_coef = nullptr;
     std::vector<const double*> rcf_coef;  // per filter degree f
     const float* w_f = nullptr;
+    // fused recouple tensor (L <= kFuseMaxL): CSR over the positions of F
+    const int* f_ptr = nullptr;
+    const int* f_idx = nullptr;
+    const double* f_coef = nullptr;
   };
   std::vector<std::vector<CoefSet>> coefs;
   // per L and filter degree f: the recouple schedule restricted to b + u = f
@@ -399,6 +403,10 @@ e2f_status coef_of(e2f_ctx* ctx, int L, const std::vector<double>& w, bool allow
   }
   std::vector<float> wf(w.begin(), w.end());  // o[4 + L]
   push_array(blob, o, wf);
+  const FuseTable ft = fuse_table(t, w);  // o[5 + L] .. o[7 + L] (empty above kFuseMaxL)
+  push_array(blob, o, ft.ptr);
+  push_array(blob, o, ft.idx);
+  push_array(blob, o, ft.coef);
   if (sets.size() >= kMaxCoefSets) {  // the oldest set may still be read by queued work
     E2F_HIP(hipDeviceSynchronize());
     E2F_HIP(hipFree(sets.front().mem));
@@ -418,6 +426,11 @@ e2f_status coef_of(e2f_ctx* ctx, int L, const std::vector<double>& w, bool allow
   c.rc_coef = (const double*)((char*)mem + o[2]);
   for (int f = 0; f <= L; ++f) c.rcf_coef.push_back((const double*)((char*)mem + o[3 + f]));
   c.w_f = (const float*)((char*)mem + o[4 + L]);
+  if (!ft.coef.empty()) {
+    c.f_ptr = (const int*)((char*)mem + o[5 + L]);
+    c.f_idx = (const int*)((char*)mem + o[6 + L]);
+    c.f_coef = (const double*)((char*)mem + o[7 + L]);
+  }
   sets.push_back(std::move(c));
   out = &sets.back();
   return E2F_OK;
@@ -458,6 +471,7 @@ e2f_status check_params(e2f_ctx* ctx, const e2f_conv_params* p) {
   if (!finite_pos(p->cutoff) || p->cutoff > 64.0f) return fail(E2F_EINVAL, "cutoff must be finite, in (0, 64]");
   if (!std::isfinite(p->tile_side) || p->tile_side < 0.0f) return fail(E2F_EINVAL, "tile_side must be finite and >= 0");
   if (p->y_norm != 0 && p->y_norm != 1) return fail(E2F_EINVAL, "y_norm must be 0 or 1");
+  if (p->split_recouple != 0 && p->split_recouple != 1) return fail(E2F_EINVAL, "split_recouple must be 0 or 1");
   int md = 0;  // read as an int: a C caller may store any value in the enum field
   std::memcpy(&md, &p->mix_dtype, sizeof(md));
   if (md != E2F_F32 && md != E2F_BF16) return fail(E2F_EINVAL, "unknown mix_dtype");
@@ -547,11 +561,20 @@ constexpr int64_t kMinSlice = 256;
 // fixed part), then S for a slice of receivers.
 struct FwdLayout {
   size_t stats = 0, dmin = 0, grid = 0, tile_of = 0, keys = 0, keys_out = 0, vals = 0, order = 0, sort_tmp = 0;
-  size_t sort_b = 0, Re = 0, Rr = 0, alpha_hm = 0, erows = 0, y = 0, S = 0;
+  size_t sort_b = 0, Re = 0, Rr = 0, alpha_hm = 0, erows = 0, y = 0, featq = 0, S = 0;
   size_t fixed = 0;  // bytes before S
   size_t s_row = 0;  // S bytes per receiver
   size_t total(int64_t slice) const { return fixed + s_row * (size_t)std::max<int64_t>(slice, 0); }
 };
+
+// The split of each head into channel groups of 16 with which the
+// aggregation applies the recouple itself (L <= 4, head width a multiple of
+// 16, one attention weight per edge and head); 0 where the forward writes S.
+int fused_split(const e2f_conv_params* p) {
+  const int dh = p->channels / p->heads;
+  if (p->y_norm != 0 || p->split_recouple != 0 || dh % 16 != 0) return 0;
+  return outer_fused_supported(p->lmax, p->channels, p->channels / 16) ? dh / 16 : 0;
+}
 
 FwdLayout fwd_layout(const e2f_conv_params* p, int n, int64_t E, bool have_alpha) {
   const int L = p->lmax, nk = nk_of(L), C = p->channels, H = p->heads;
@@ -579,9 +602,12 @@ FwdLayout fwd_layout(const e2f_conv_params* p, int n, int64_t E, bool have_alpha
   f.alpha_hm = take(sizeof(float) * (size_t)E * H * na);
   f.erows = take(sizeof(int32_t) * (size_t)E);
   f.y = take(p->mix_w ? sizeof(float) * (size_t)n * nk * C : 0);
+  // the fused aggregation's copy of the features (groups of four components)
+  f.featq = take(fused_split(p) > 0 ? sizeof(float) * (size_t)n * C * 4 * fuse_groups(L) : 0);
   f.S = off;
   f.fixed = off;
-  f.s_row = al256(sizeof(float) * (size_t)node_tp_dim(L) * C);
+  // per receiver of a slice: F_i (fused) or S_i
+  f.s_row = fused_split(p) > 0 ? sizeof(float) * (size_t)fuse_stride(nk) : al256(sizeof(float) * (size_t)node_tp_dim(L) * C);
   return f;
 }
 
@@ -613,14 +639,19 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
   const int L = p->lmax, C = p->channels, H = p->heads, nk = nk_of(L);
   const e2f_ctx::CoefSet* cs = nullptr;
   if ((rs = coef_of(ctx, L, path_weights(p), allow_upload, cs)) != E2F_OK) return rs;
-  const int hdiv = head_split(L, C, H);
+  const int fsplit = fused_split(p);
+  const int hdiv = fsplit > 0 ? fsplit : head_split(L, C, H);
   if (hdiv < 1) return fail(E2F_EUNSUPPORTED, "no head split of width %d fits the aggregation", C / H);
   const int Hv = H * hdiv, dv = C / Hv;
   const int cgroups = outer_agg_groups(L, C, Hv);
   const e2f_ctx::Couple* cpl = nullptr;
-  if (!allow_upload && ctx->couple.find(std::make_pair(L, cgroups)) == ctx->couple.end())
-    return fail(E2F_EINVAL, "the coupling schedule is not resident on the context; call e2f_wigner6j_prepare first");
-  if ((rs = couple_of(ctx, L, cgroups, cpl)) != E2F_OK) return rs;
+  if (fsplit == 0) {
+    if (!allow_upload && ctx->couple.find(std::make_pair(L, cgroups)) == ctx->couple.end())
+      return fail(E2F_EINVAL, "the coupling schedule is not resident on the context; call e2f_wigner6j_prepare first");
+    if ((rs = couple_of(ctx, L, cgroups, cpl)) != E2F_OK) return rs;
+  } else if (!cs->f_ptr) {
+    return fail(E2F_EDEVICE, "the fused recouple table of L = %d is missing", L);
+  }
   if (n == 0) return E2F_OK;
   const bool ynorm = p->y_norm != 0;
   const FwdLayout f = fwd_layout(p, n, n_edges, alpha != nullptr);
@@ -671,9 +702,17 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
   // at a time in the workspace)
   const int64_t slice = std::min<int64_t>(n, (int64_t)((workspace_bytes - f.fixed) / f.s_row));
   int64_t slices = 0;
+  float* featq = (float*)(ws + f.featq);
+  if (fsplit > 0) E2F_TIMED("feat_qmajor", launch_feat_qmajor(L, feat, n, C, featq, s));
   for (int64_t q0 = 0; q0 < n; q0 += slice, ++slices) {
     const int nb = (int)std::min<int64_t>(slice, n - q0);
     const int32_t* ord = order + q0;
+    if (fsplit > 0) {  // F of the slice, then the aggregation with the recouple applied
+      E2F_TIMED("fuse_build", launch_fuse_build(L, cs->f_ptr, cs->f_idx, cs->f_coef, Rr, ord, nb, S, s));
+      E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, alpha_hm, n_edges, featq, ord, S, nb, C,
+                                                Hv, hdiv, n, y, s));
+      continue;
+    }
     if (!ynorm) {
       E2F_TIMED("aggregate", launch_outer_agg(t, Re, row_ptr, col_idx, alpha_hm, n_edges, feat, ord, cpl->meta,
                                               cpl->coef, cpl->pmeta, cpl->tab, cpl->ntab, cpl->k, cgroups, nb, C, Hv,
@@ -980,6 +1019,7 @@ e2f_status e2f_wigner6j_prepare(e2f_ctx* ctx, const e2f_conv_params* p) {
   DeviceGuard g(ctx->device);
   const e2f_ctx::CoefSet* cs = nullptr;
   if (e2f_status rs = coef_of(ctx, p->lmax, path_weights(p), true, cs); rs != E2F_OK) return rs;
+  if (fused_split(p) > 0) return E2F_OK;  // the fused table is part of the coefficient set
   const int hdiv = head_split(p->lmax, p->channels, p->heads);
   if (hdiv < 1) return fail(E2F_EUNSUPPORTED, "no head split of width %d fits the aggregation", p->channels / p->heads);
   const e2f_ctx::Couple* cpl = nullptr;

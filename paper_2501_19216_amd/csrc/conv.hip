@@ -551,6 +551,42 @@ constexpr int kOuterEdges = 128;  // edges staged per chunk
 // faster than 4 and 5: 6.47, 6.52, 6.62 ms at 20k atoms, L = 4)
 constexpr int kOuterStages = 3;
 
+// Staging of one chunk of ne <= EC edges from edge c0 for the products:
+// Al[nb * AS + be] = alpha_e R_be(p_j) of the chunk's edge nb for the 4
+// ceil(ne / 4) rows the steps read (zeros past ne and for be >= NK), jl[nb]
+// = its sender for nb < EC (edge c0 past ne, and 0 for an index outside
+// [0, n_nodes): no read leaves the caller's buffers).  alpha_h is the head's
+// row of the head-major weights (NULL: all ones).  Consecutive threads take
+// consecutive components of one edge (contiguous R loads, conflict-free LDS
+// stores); four values per thread in flight, loads before stores.  Needs
+// blockDim.x >= EC; the caller synchronises before and after.
+template <int NK, int MP, int AS, int EC>
+__device__ __forceinline__ void stage_chunk(const float* __restrict__ Re, const float* __restrict__ alpha_h,
+                                            const int32_t* __restrict__ col, int64_t c0, int ne, int n_nodes,
+                                            float* __restrict__ Al, int* __restrict__ jl) {
+  const int nsl = 4 * ((ne + 3) / 4) * MP;
+  int jv = threadIdx.x < EC ? col[c0 + ((int)threadIdx.x < ne ? threadIdx.x : 0)] : 0;
+  jv = (unsigned)jv < (unsigned)n_nodes ? jv : 0;
+  for (int base = threadIdx.x; base < nsl; base += 4 * blockDim.x) {
+    float av[4], rv[4];
+    bool okv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = base + u * blockDim.x, nb = idx / MP, be = idx % MP;
+      okv[u] = idx < nsl && nb < ne && be < NK;
+      const int64_t e = c0 + (nb < ne ? nb : 0);
+      av[u] = alpha_h ? alpha_h[e] : 1.0f;
+      rv[u] = Re[(size_t)e * NK + (be < NK ? be : 0)];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = base + u * blockDim.x;
+      if (idx < nsl) Al[(idx / MP) * AS + idx % MP] = okv[u] ? av[u] * rv[u] : 0.0f;
+    }
+  }
+  if (threadIdx.x < EC) jl[threadIdx.x] = jv;
+}
+
 // The j-side coupling of one receiver's G (in LDS, rows of GS floats) into
 // its S rows of one head (Sr, rows of dh floats), from a thread-balanced
 // schedule: group g walks its entries k*cgroups + g, four channels per
@@ -667,35 +703,10 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
   for (int64_t c0 = e0; c0 < e1; c0 += EC) {
     const int ne = (int)min((int64_t)EC, e1 - c0);
     __syncthreads();
-    // staging of the rows the steps read (4 ns <= EC; rows past ne hold 0):
-    // consecutive lanes take consecutive components be of one edge
-    // (contiguous R loads, conflict-free LDS stores); four values per thread
-    // in flight, loads before stores
-    const int ns = (ne + 3) / 4, nsl = 4 * ns * MP;
-    // the chunk's senders (blockDim >= EC), loaded with the staging's first round
-    int jv = threadIdx.x < EC ? col[c0 + ((int)threadIdx.x < ne ? threadIdx.x : 0)] : 0;
-    jv = (unsigned)jv < (unsigned)n_nodes ? jv : 0;
-    for (int base = threadIdx.x; base < nsl; base += 4 * blockDim.x) {
-      // branch-free: clamped indices, all loads of a round (alpha and R of
-      // the edge, both addressed by the edge) issued before the first use
-      float av[4], rv[4];
-      bool okv[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int idx = base + u * blockDim.x, nb = idx / MP, be = idx % MP;
-        okv[u] = idx < nsl && nb < ne && be < NK;
-        const int64_t e = c0 + (nb < ne ? nb : 0);
-        av[u] = alpha_hm ? alpha_hm[(int64_t)(h / hdiv) * n_edges + e] : 1.0f;
-        rv[u] = Re[(size_t)e * NK + (be < NK ? be : 0)];
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int idx = base + u * blockDim.x;
-        if (idx < nsl) Al[(idx / MP) * AS + idx % MP] = okv[u] ? av[u] * rv[u] : 0.0f;
-      }
-    }
-    if (threadIdx.x < EC) jl[threadIdx.x] = jv;
+    stage_chunk<NK, MP, AS, EC>(Re, alpha_hm ? alpha_hm + (int64_t)(h / hdiv) * n_edges : nullptr, col, c0, ne,
+                                n_nodes, Al, jl);
     __syncthreads();
+    const int ns = (ne + 3) / 4;
     // three-stage pipeline: the features of steps st+1, st+2 are loaded
     // while the MFMAs of step st run
     // Each stage holds both operands of a step: A (the lane's two rows of
@@ -771,6 +782,210 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
       couple_rows<false>(cmeta, ccoef, ck, cgroups, g, tq, G, GS, dh, Sr);
   }
   }  // receivers of the workgroup
+}
+
+// ------------------------------------------------------------ fused recouple
+// Up to L = 4 with heads of 16 channels the recouple is applied where G is
+// made: per receiver the matrix F_i = Q_i CG (the j-side coupling composed
+// with the i-side recouple, built once per receiver by k_fuse_build) takes
+// the aggregated uncoupled products straight to the output,
+//     y_i[k][h*16 + t] = sum_{be, q} F_i[k][be, q] G_i^h[be][q][t],
+// so neither the coupled S_i nor a second kernel's read of it exists.
+
+// F_i = sum_x R_x(p_i) K_x in float64, rounded once to float: a workgroup
+// builds kFuseRecv receivers' rows (the receivers order[r0 ..] of the slice,
+// row r0 + b), each thread a set of positions; position p sums its entries
+// fidx/fcoef[fptr[p] .. fptr[p+1]).
+constexpr int kFuseRecv = 16;
+__global__ __launch_bounds__(256) void k_fuse_build(const int* __restrict__ fptr, const int* __restrict__ fidx,
+                                                    const double* __restrict__ fcoef, int np, int nk,
+                                                    const double* __restrict__ R, const int32_t* __restrict__ order,
+                                                    int nb, float* __restrict__ F) {
+  __shared__ double Rl[kFuseRecv][(kFuseMaxL + 1) * (kFuseMaxL + 1)];
+  const int r0 = blockIdx.x * kFuseRecv;
+  const int nr = min(kFuseRecv, nb - r0);
+  for (int q = threadIdx.x; q < kFuseRecv * nk; q += blockDim.x) {
+    const int b = q / nk, x = q % nk;
+    Rl[b][x] = b < nr ? R[(size_t)order[r0 + b] * nk + x] : 0.0;
+  }
+  __syncthreads();
+  for (int p = threadIdx.x; p < np; p += blockDim.x) {
+    double acc[kFuseRecv];
+#pragma unroll
+    for (int b = 0; b < kFuseRecv; ++b) acc[b] = 0.0;
+    const int e1 = fptr[p + 1];
+    for (int e = fptr[p]; e < e1; ++e) {
+      const double c = fcoef[e];
+      const int x = fidx[e];
+#pragma unroll
+      for (int b = 0; b < kFuseRecv; ++b) acc[b] += c * Rl[b][x];
+    }
+#pragma unroll
+    for (int b = 0; b < kFuseRecv; ++b)
+      if (b < nr) F[(size_t)(r0 + b) * np + p] = (float)acc[b];
+  }
+}
+
+// The features in the order of the fused aggregation's B operand: per node
+// and head of 16 channels, groups of four components q = 4 g + i (zero past
+// (L+1)^2), each group [t][i] (t the channel in the head), so that lane t of
+// a wave reads the four components of its wave's group as one float4 and a
+// group of 16 lanes reads 256 contiguous bytes.
+__global__ void k_feat_qmajor(const float* __restrict__ feat, int n, int nk, int C, int ng,
+                              float4* __restrict__ out) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (node, head, group, t)
+  const int H = C / 16;
+  if (q >= (int64_t)n * H * ng * 16) return;
+  const int t = (int)(q % 16);
+  const int64_t r = q / 16;
+  const int g = (int)(r % ng), h = (int)(r / ng % H);
+  const int64_t j = r / ((int64_t)ng * H);
+  const float* src = feat + (size_t)j * nk * C + h * 16 + t;
+  float v[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = 4 * g + i < nk ? src[(size_t)(4 * g + i) * C] : 0.0f;
+  out[q] = make_float4(v[0], v[1], v[2], v[3]);
+}
+
+// The aggregation with the recouple applied in registers.  Work split as in
+// k_outer_agg (a workgroup: rpw consecutive receivers of one head h of 16
+// channels), but tile w of wave v holds the 16 channels t = l16 of one
+// component q = 4 v + w, so that after the products the accumulator element
+// s of a lane (l16, k4), G[16 mt + 4 k4 + s][q][l16], is exactly the B
+// operand of K step s of F_i G when the K index of that step is ordered as
+// be = 16 mt + 4 k4 + s; F_i is stored in the matching order.  Each wave sums
+// its components' share of y (rows 16 rt + 4 k4 + v, channel l16); the
+// shares meet in LDS and one pass stores the head's 16 channels of y_i.
+template <int L, int LB>
+__global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re, const int64_t* __restrict__ row_ptr,
+                                                    const int32_t* __restrict__ col,
+                                                    const float* __restrict__ alpha_hm, int64_t n_edges,
+                                                    const float4* __restrict__ featq,
+                                                    const int32_t* __restrict__ order, const float* __restrict__ F,
+                                                    int n, int nrx, int rpw, int C, int H, int hdiv, int n_nodes,
+                                                    float* __restrict__ y) {
+  constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
+  constexpr int EC = kOuterEdges, AS = MP + 16;
+  constexpr int QB = fuse_qblock(NK), FS = fuse_stride(NK);
+  extern __shared__ float sm[];
+  float* Al = sm;                  // [EC][AS] alpha R of the chunk's edges
+  int* jl = (int*)(sm + EC * AS);  // [EC] senders
+  float* yp = sm;                  // [NW][MP][16] the waves' shares of y (after the products)
+  const int bid = blockIdx.x, xcd = bid % 8, local = bid / 8;
+  const int h = local % H, rfirst = xcd * nrx + (local / H) * rpw;
+  const int rlast = min(min(rfirst + rpw, (xcd + 1) * nrx), n);  // uniform over the workgroup
+  const int NW = blockDim.x >> 6, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int l16 = lane & 15, k4 = lane >> 4;
+  constexpr int NG = (NK + 3) / 4;  // groups of four components (one per wave)
+  bool live[4];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) live[w] = __builtin_amdgcn_readfirstlane(4 * wave + w < NK ? 1 : 0) != 0;
+  // the lane's float4 of a sender: its wave's group (a wave past the groups
+  // reads the last one and multiplies nothing), channel t = l16
+  const int64_t fstride = (int64_t)H * NG * 16;  // float4 per node
+  const int foff = (h * NG + min(wave, NG - 1)) * 16 + l16;
+  const float* ah = alpha_hm ? alpha_hm + (int64_t)(h / hdiv) * n_edges : nullptr;
+  for (int r = rfirst; r < rlast; ++r) {
+    const int i = order[r];
+    v4f acc[MT][4];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) acc[mt][w] = (v4f){0.f, 0.f, 0.f, 0.f};
+    const int64_t rb0 = row_ptr[i], rb1 = row_ptr[i + 1];
+    const int64_t e0 = rb0 < 0 ? 0 : (rb0 > n_edges ? n_edges : rb0);
+    const int64_t e1 = rb1 < e0 ? e0 : (rb1 > n_edges ? n_edges : rb1);
+    for (int64_t c0 = e0; c0 < e1; c0 += EC) {
+      const int ne = (int)min((int64_t)EC, e1 - c0);
+      __syncthreads();  // the previous chunk's (or receiver's) reads of the staging space are done
+      stage_chunk<NK, MP, AS, EC>(Re, ah, col, c0, ne, n_nodes, Al, jl);
+      __syncthreads();
+      const int ns = (ne + 3) / 4;
+      // pipeline of the products as in k_outer_agg: the operands of steps
+      // st+1, st+2 are loaded while the MFMAs of step st run; steps past ns
+      // read row EC - 1 and a valid sender and are never multiplied
+      float aq[kOuterStages][MT];
+      float4 bq[kOuterStages];
+      auto loadb = [&](int st, float* a, float4& b) {
+        const int nb = min(4 * st + k4, EC - 1);
+        b = featq[jl[nb] * fstride + foff];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) a[mt] = Al[nb * AS + mt * 16 + l16];
+      };
+      auto mma = [&](const float* a, const float4& b) {
+        const float bw[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          if (!live[w]) continue;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+            acc[mt][w] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bw[w], acc[mt][w], 0, 0, 0);
+        }
+      };
+#pragma unroll
+      for (int u = 0; u + 1 < kOuterStages; ++u) loadb(u, aq[u], bq[u]);
+      for (int st = 0; st < ns; st += kOuterStages) {
+#pragma unroll
+        for (int u = 0; u < kOuterStages; ++u) {
+          const int w = (u + kOuterStages - 1) % kOuterStages;
+          loadb(st + u + kOuterStages - 1, aq[w], bq[w]);
+          __builtin_amdgcn_sched_barrier(0);
+          if (u == 0 || st + u < ns) mma(aq[u], bq[u]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+    // this wave's share of y_i: A = F_i (rows k, K = be in the step order
+    // above, zero past NK), B = the accumulators.  The F loads are
+    // unconditional (lanes past a sub-block's rows or K values, and dead
+    // tiles, read a valid element and take zero), so the wait counts stay
+    // exact; the next component's values load while this one's MFMAs run.
+    const float* Fr = F + (size_t)r * FS;
+    v4f ya[MT];
+#pragma unroll
+    for (int rt = 0; rt < MT; ++rt) ya[rt] = (v4f){0.f, 0.f, 0.f, 0.f};
+    float4 fv[2][MT][MT];
+    auto loadf = [&](int w, float4 (*f)[MT]) {
+      const int q = min(4 * wave + w, NK - 1);
+#pragma unroll
+      for (int rt = 0; rt < MT; ++rt)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const bool ok = l16 < fuse_rows(NK, rt) && k4 < fuse_kc(NK, mt);
+          const float4 v = *(const float4*)(Fr + q * QB + fuse_blk(NK, rt, mt) +
+                                            (ok ? (k4 * fuse_rows(NK, rt) + l16) * 4 : 0));
+          f[rt][mt] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    };
+    loadf(0, fv[0]);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (w + 1 < 4) loadf(w + 1, fv[(w + 1) & 1]);
+      if (!live[w]) continue;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int rt = 0; rt < MT; ++rt) {
+          const float4 f = fv[w & 1][rt][mt];
+          ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.x, acc[mt][w][0], ya[rt], 0, 0, 0);
+          ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.y, acc[mt][w][1], ya[rt], 0, 0, 0);
+          ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.z, acc[mt][w][2], ya[rt], 0, 0, 0);
+          ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.w, acc[mt][w][3], ya[rt], 0, 0, 0);
+        }
+    }
+    __syncthreads();  // the products' reads of the staging space are done
+#pragma unroll
+    for (int rt = 0; rt < MT; ++rt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) yp[(wave * MP + 16 * rt + 4 * k4 + v) * 16 + l16] = ya[rt][v];
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < NK * 16; idx += blockDim.x) {
+      const int row = idx >> 4, t = idx & 15;
+      float sum = 0.0f;
+      for (int wv = 0; wv < NW; ++wv) sum += yp[(wv * MP + row) * 16 + t];
+      y[((size_t)i * NK + row) * C + h * 16 + t] = sum;
+    }
+  }
 }
 
 // ------------------------------------------------------------ i-side recouple
@@ -1727,6 +1942,62 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* 
     E2F_CASES(0) E2F_CASES(1) E2F_CASES(2) E2F_CASES(3) E2F_CASES(4) E2F_CASES(5) E2F_CASES(6)
     E2F_CASE(0, 8, 512) E2F_CASE(1, 8, 512) E2F_CASE(2, 8, 512) E2F_CASE(3, 8, 512) E2F_CASE(4, 8, 512)
 #undef E2F_CASES
+#undef E2F_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+bool outer_fused_supported(int L, int C, int H) { return L >= 0 && L <= kFuseMaxL && H >= 1 && C == 16 * H; }
+
+hipError_t launch_fuse_build(int L, const int* fptr, const int* fidx, const double* fcoef, const double* R,
+                             const int32_t* order, int n, float* F, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  if (L < 0 || L > kFuseMaxL) return hipErrorInvalidValue;
+  const int nk = (L + 1) * (L + 1);
+  k_fuse_build<<<(n + kFuseRecv - 1) / kFuseRecv, 256, 0, s>>>(fptr, fidx, fcoef, fuse_stride(nk), nk, R, order, n,
+                                                                 F);
+  return hipGetLastError();
+}
+
+int fuse_groups(int L) { return ((L + 1) * (L + 1) + 3) / 4; }
+
+hipError_t launch_feat_qmajor(int L, const float* feat, int n, int C, float* featq, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  if (C % 16) return hipErrorInvalidValue;
+  const int64_t total = (int64_t)n * (C / 16) * fuse_groups(L) * 16;
+  if ((total + 255) / 256 > 0x7fffffff) return hipErrorInvalidValue;
+  k_feat_qmajor<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(feat, n, (L + 1) * (L + 1), C, fuse_groups(L),
+                                                                 (float4*)featq);
+  return hipGetLastError();
+}
+
+hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, const int32_t* col,
+                              const float* alpha_hm, int64_t n_edges, const float* featq, const int32_t* order,
+                              const float* F, int n, int C, int H, int hdiv, int n_nodes, float* y, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  if (!outer_fused_supported(L, C, H)) return hipErrorInvalidValue;
+  const int nk = (L + 1) * (L + 1), mp = 16 * ((nk + 15) / 16);
+  const int nw = std::max((nk + 3) / 4, 2);  // four components per wave; the staging needs kOuterEdges threads
+  const size_t lds = std::max(sizeof(float) * (size_t)kOuterEdges * (mp + 16) + sizeof(int) * kOuterEdges,
+                              sizeof(float) * (size_t)nw * mp * 16);
+  static const int rpw_env = [] {
+    const char* v = getenv("E2F_OUTER_RPW");
+    return v ? atoi(v) : 0;
+  }();
+  const int rpw = rpw_env > 0 ? rpw_env : 8;
+  const int nrx = (n + kXcds - 1) / kXcds;
+  const int64_t blocks = (int64_t)kXcds * ((nrx + rpw - 1) / rpw) * H;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  switch (L) {
+#define E2F_CASE(LL)                                                                                          \
+  case LL:                                                                                                    \
+    if (hipError_t e = allow_lds(k_outer_fused<LL, 512>, lds); e != hipSuccess) return e;                     \
+    k_outer_fused<LL, 512><<<(unsigned)blocks, 64 * nw, lds, s>>>(Re, row_ptr, col, alpha_hm, n_edges,         \
+                                                                  (const float4*)featq,                      \
+                                                                  order, F, n, nrx, rpw, C, H, hdiv, n_nodes, y); \
+    break;
+    E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4)
 #undef E2F_CASE
     default: return hipErrorInvalidValue;
   }

@@ -136,6 +136,51 @@ struct GeomSchedule {
 GeomSchedule geom_schedule(const LayerTables& t, int qc);
 int64_t node_tp_dim(int L);
 
+// ---------------------------------------------------------------- fused recouple
+// Up to L = 4 the j-side coupling and the i-side recouple compose into one
+// per-receiver matrix F_i = Q_i CG of (L+1)^2 rows k = (o, m) and (L+1)^4
+// columns (be, q), be the component of R(p_j) and q that of h_j:
+//     y_i[k][c] = sum_{be, q} F_i[k][be, q] G_i[be][q][c],
+//     G_i[be][q][c] = sum_j alpha_ij R_be(p_j) h_j[q][c].
+// F_i = sum_x R_x(p_i) K_x with fixed tensors K_x (x a component of R(p_i)),
+// K_x[k][be, q] = sum over T rows r of Q_i's coefficient of R_x in entry
+// (k, r) times CG[r][be, q].  F_i is stored per receiver in the order in which
+// the aggregation's waves read it as the A operand of v_mfma_f32_16x16x4f32:
+// per q a block of (row tile rt, K tile mt) sub-blocks, each [k4 < kc][l16 <
+// rows][s < 4] holding F[16 rt + l16][16 mt + 4 k4 + s][q] (zero where the
+// column index reaches (L+1)^2).
+constexpr int kFuseMaxL = 4;
+constexpr int fuse_rows(int nk, int rt) { return nk - 16 * rt < 16 ? nk - 16 * rt : 16; }
+constexpr int fuse_kc(int nk, int mt) { return (fuse_rows(nk, mt) + 3) / 4; }
+constexpr int fuse_tiles(int nk) { return (nk + 15) / 16; }
+// offset (floats) of sub-block (rt, mt) inside a q block, rt-major
+constexpr int fuse_blk(int nk, int rt, int mt) {
+  int off = 0;
+  for (int a = 0; a < fuse_tiles(nk); ++a)
+    for (int b = 0; b < fuse_tiles(nk); ++b) {
+      if (a == rt && b == mt) return off;
+      off += 4 * fuse_kc(nk, b) * fuse_rows(nk, a);
+    }
+  return off;
+}
+constexpr int fuse_qblock(int nk) { return fuse_blk(nk, fuse_tiles(nk), 0); }
+// floats of one receiver's F, rounded up to 64 (256-byte rows)
+constexpr int fuse_stride(int nk) { return (nk * fuse_qblock(nk) + 63) / 64 * 64; }
+// position of F[k][be][q] in a receiver's row
+constexpr int fuse_pos(int nk, int k, int be, int q) {
+  return q * fuse_qblock(nk) + fuse_blk(nk, k / 16, be / 16) + ((be % 16) / 4 * fuse_rows(nk, k / 16) + k % 16) * 4 +
+         be % 4;
+}
+// K_x by position of F (CSR over the positions 0 .. fuse_stride - 1): the
+// entries of position p are idx[e] (the component x) and coef[e] (float64,
+// path weights w[a][f][o] included) for e in ptr[p] .. ptr[p+1] - 1.
+struct FuseTable {
+  std::vector<int> ptr;
+  std::vector<int> idx;
+  std::vector<double> coef;
+};
+FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w);
+
 // ---------------------------------------------------------------- device side
 // Device copies of one LayerTables (pointers into one allocation).
 struct DevTables {

@@ -133,6 +133,20 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* 
                             const int32_t* order, const int* cmeta, const float* ccoef, const int* pmeta,
                             const float* ptab, int ntab, int ck, int cgroups, int n, int C, int H, int hdiv,
                             int n_nodes, float* S, hipStream_t s);
+// Fused aggregation and recouple (L <= kFuseMaxL, H virtual heads of 16
+// channels, C = 16 H): F rows r < n (receivers order[r]) of fuse_stride(nk)
+// floats from the fused table (fptr/fidx/fcoef, fuse_table) and R [N][nk]
+// float64; then y[order[r]] directly from the aggregated products and F row r
+// (other arguments as for launch_outer_agg)
+bool outer_fused_supported(int L, int C, int H);
+hipError_t launch_fuse_build(int L, const int* fptr, const int* fidx, const double* fcoef, const double* R,
+                             const int32_t* order, int n, float* F, hipStream_t s);
+// featq: the features re-laid by launch_feat_qmajor, n_nodes * C * 4 * fuse_groups(L) floats
+int fuse_groups(int L);
+hipError_t launch_feat_qmajor(int L, const float* feat, int n, int C, float* featq, hipStream_t s);
+hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, const int32_t* col,
+                              const float* alpha_hm, int64_t n_edges, const float* featq, const int32_t* order,
+                              const float* F, int n, int C, int H, int hdiv, int n_nodes, float* y, hipStream_t s);
 // y[order[r]] from S row r (head-major like T), r < n; shared_s: every r
 // reads S row 0; accumulate: y += the product instead of y = (one writer per
 // element)

@@ -532,4 +532,48 @@ GeomSchedule geom_schedule(const LayerTables& t, int qc) {
   return gs;
 }
 
+FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w) {
+  const int nk = t.nk;
+  FuseTable ft;
+  if (t.L > kFuseMaxL) return ft;
+  // dense K[pos][x], accumulated over the T rows r that link a recouple entry
+  // (k, r) with a coupling entry (r, be, q)
+  const int np = fuse_stride(nk);
+  std::vector<double> K((size_t)np * nk, 0.0), mag((size_t)np * nk, 0.0);
+  for (int o = 0; o <= t.L; ++o) {
+    const int ncol = t.q_ncol[o];
+    for (int m = 0; m < 2 * o + 1; ++m)
+      for (int col = 0; col < ncol; ++col) {
+        const int s = t.q_slotoff[o] + m * ncol + col;
+        const int r = t.q_cols[t.q_coloff[o] + col];
+        const int k = o * o + m;
+        const int s0 = t.m_rowoff[r], s1 = t.m_rowoff[r + 1];
+        const int a = (s1 - s0 - 1) / 2;
+        for (int e = t.q_ptr[s]; e < t.q_ptr[s + 1]; ++e) {
+          const double cq = t.q_unit[e] * w[t.q_path[e]];
+          const int x = t.q_ridx[e];
+          for (int sl = s0; sl < s1; ++sl)
+            for (int e2 = t.m_ptr[sl]; e2 < t.m_ptr[sl + 1]; ++e2) {
+              const size_t at = (size_t)fuse_pos(nk, k, t.m_ridx[e2], a * a + sl - s0) * nk + x;
+              K[at] += cq * t.m_coef[e2];
+              mag[at] += std::fabs(cq * t.m_coef[e2]);
+            }
+        }
+      }
+  }
+  // sums that cancel to rounding level are zeros of the exact tensor
+  ft.ptr.assign(1, 0);
+  for (int p = 0; p < np; ++p) {
+    for (int x = 0; x < nk; ++x) {
+      const double v = K[(size_t)p * nk + x];
+      if (v != 0.0 && std::fabs(v) > 1e-13 * mag[(size_t)p * nk + x]) {
+        ft.idx.push_back(x);
+        ft.coef.push_back(v);
+      }
+    }
+    ft.ptr.push_back((int)ft.idx.size());
+  }
+  return ft;
+}
+
 }  // namespace e2f

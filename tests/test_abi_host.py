@@ -89,6 +89,8 @@ def test_conv_argument_checks(e2f, fn):
     assert call(_params(e2f, mix_dtype=7)) == EINVAL
     assert call(_params(e2f, y_norm=2)) == EINVAL
     assert call(_params(e2f, y_norm=1)) == EDEV
+    assert call(_params(e2f, split_recouple=2)) == EINVAL
+    assert call(_params(e2f, split_recouple=1)) == EDEV
     assert call(_params(e2f), n=-1) == EINVAL
     assert call(_params(e2f), E=-1) == EINVAL
     assert call(_params(e2f), E=2 ** 31) == EUNS
@@ -165,22 +167,37 @@ def test_other_argument_checks(e2f):
     ctx.close()
 
 
+def _fused_row_bytes(L):
+    # one receiver's composed coupling-and-recouple matrix F_i: per component q
+    # of h, (row tile, K tile) blocks of 4 ceil(K rows / 4) x (rows) floats,
+    # the row rounded up to 64 floats
+    nk = (L + 1) ** 2
+    tiles = [min(16, nk - 16 * t) for t in range(-(-nk // 16))]
+    qblock = sum(4 * -(-kr // 4) * rows for rows in tiles for kr in tiles)
+    return 4 * (-(-nk * qblock // 64) * 64)
+
+
 def test_workspace_size_query(e2f):
-    # the size query needs no device: the one-pass size holds S for every
-    # receiver, the minimum for 256 (the plan and per-edge arrays are shared)
+    # the size query needs no device: the one-pass size holds S (or, where the
+    # aggregation recouples itself, F_i) for every receiver, the minimum for
+    # 256 (the plan and per-edge arrays are shared)
     ctx = e2f.e2f_create(6, None)
     lib = e2f.lib
     b, m = ctypes.c_size_t(0), ctypes.c_size_t(0)
-    for L, C, H, n, E in ((2, 16, 4, 32, 738), (4, 128, 8, 20000, 1597678), (6, 64, 8, 200000, 39828996)):
-        prm = _params(e2f, lmax=L, channels=C, heads=H)
+    assert _fused_row_bytes(4) == 4 * 17536 and _fused_row_bytes(3) == 4 * 4096
+    for L, C, H, n, E, split in ((2, 16, 4, 32, 738, 0), (4, 128, 8, 20000, 1597678, 0),
+                                 (4, 128, 8, 20000, 1597678, 1), (3, 64, 4, 7680, 49348, 0),
+                                 (3, 64, 8, 7680, 49348, 0), (6, 64, 8, 200000, 39828996, 0)):
+        prm = _params(e2f, lmax=L, channels=C, heads=H, split_recouple=split)
         assert lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm), n, E, ctypes.byref(b)) == e2f.E2F_OK
         assert lib.e2f_wigner6j_workspace_min(ctx.handle, ctypes.byref(prm), n, E, ctypes.byref(m)) == e2f.E2F_OK
         dimT, nk = e2f.e2f_node_tp_dim(L), (L + 1) ** 2
-        s_row = -(-4 * dimT * C // 256) * 256
+        fused = L <= 4 and (C // H) % 16 == 0 and not split
+        s_row = _fused_row_bytes(L) if fused else -(-4 * dimT * C // 256) * 256
         assert b.value - m.value == max(0, n - 256) * s_row
         # at least the per-edge harmonics, the receivers' harmonics, the head-major weights and S
         assert b.value >= 4 * E * nk + 8 * n * nk + 4 * E * H + n * s_row
-        prm_mix = _params(e2f, lmax=L, channels=C, heads=H, mix_w=FAKE)
+        prm_mix = _params(e2f, lmax=L, channels=C, heads=H, mix_w=FAKE, split_recouple=split)
         assert lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm_mix), n, E, ctypes.byref(m)) == e2f.E2F_OK
         assert m.value - b.value >= 4 * n * nk * C  # the unmixed output
     prm = _params(e2f, heads=3)
