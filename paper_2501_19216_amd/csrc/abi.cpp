@@ -570,10 +570,10 @@ struct FwdLayout {
 // The split of each head into channel groups of 16 with which the
 // aggregation applies the recouple itself (L <= 4, head width a multiple of
 // 16, one attention weight per edge and head); 0 where the forward writes S.
-int fused_split(const e2f_conv_params* p) {
+int fused_split(const e2f_conv_params* p, int64_t n) {
   const int dh = p->channels / p->heads;
   if (p->y_norm != 0 || p->split_recouple != 0 || dh % 16 != 0) return 0;
-  return outer_fused_supported(p->lmax, p->channels, p->channels / 16) ? dh / 16 : 0;
+  return outer_fused_supported(p->lmax, p->channels, p->channels / 16, n) ? dh / 16 : 0;
 }
 
 FwdLayout fwd_layout(const e2f_conv_params* p, int n, int64_t E, bool have_alpha) {
@@ -603,11 +603,11 @@ FwdLayout fwd_layout(const e2f_conv_params* p, int n, int64_t E, bool have_alpha
   f.erows = take(sizeof(int32_t) * (size_t)E);
   f.y = take(p->mix_w ? sizeof(float) * (size_t)n * nk * C : 0);
   // the fused aggregation's copy of the features (groups of four components)
-  f.featq = take(fused_split(p) > 0 ? sizeof(float) * (size_t)n * C * 4 * fuse_groups(L) : 0);
+  f.featq = take(fused_split(p, n) > 0 ? sizeof(float) * (size_t)n * C * 4 * fuse_groups(L) : 0);
   f.S = off;
   f.fixed = off;
   // per receiver of a slice: F_i (fused) or S_i
-  f.s_row = fused_split(p) > 0 ? sizeof(float) * (size_t)fuse_stride(nk) : al256(sizeof(float) * (size_t)node_tp_dim(L) * C);
+  f.s_row = fused_split(p, n) > 0 ? sizeof(float) * (size_t)fuse_stride(nk) : al256(sizeof(float) * (size_t)node_tp_dim(L) * C);
   return f;
 }
 
@@ -639,7 +639,7 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
   const int L = p->lmax, C = p->channels, H = p->heads, nk = nk_of(L);
   const e2f_ctx::CoefSet* cs = nullptr;
   if ((rs = coef_of(ctx, L, path_weights(p), allow_upload, cs)) != E2F_OK) return rs;
-  const int fsplit = fused_split(p);
+  const int fsplit = fused_split(p, n);
   const int hdiv = fsplit > 0 ? fsplit : head_split(L, C, H);
   if (hdiv < 1) return fail(E2F_EUNSUPPORTED, "no head split of width %d fits the aggregation", C / H);
   const int Hv = H * hdiv, dv = C / Hv;
@@ -1019,9 +1019,14 @@ e2f_status e2f_wigner6j_prepare(e2f_ctx* ctx, const e2f_conv_params* p) {
   DeviceGuard g(ctx->device);
   const e2f_ctx::CoefSet* cs = nullptr;
   if (e2f_status rs = coef_of(ctx, p->lmax, path_weights(p), true, cs); rs != E2F_OK) return rs;
-  if (fused_split(p) > 0) return E2F_OK;  // the fused table is part of the coefficient set
+  // the coupling schedule of the two-kernel form as well (the forward takes
+  // it for atom counts whose re-laid features exceed 32-bit offsets); the
+  // fused table is part of the coefficient set
   const int hdiv = head_split(p->lmax, p->channels, p->heads);
-  if (hdiv < 1) return fail(E2F_EUNSUPPORTED, "no head split of width %d fits the aggregation", p->channels / p->heads);
+  if (hdiv < 1) {
+    if (fused_split(p, 1) > 0) return E2F_OK;
+    return fail(E2F_EUNSUPPORTED, "no head split of width %d fits the aggregation", p->channels / p->heads);
+  }
   const e2f_ctx::Couple* cpl = nullptr;
   return couple_of(ctx, p->lmax, outer_agg_groups(p->lmax, p->channels, p->heads * hdiv), cpl);
 }

@@ -555,7 +555,8 @@ constexpr int kOuterStages = 3;
 // Al[nb * AS + be] = alpha_e R_be(p_j) of the chunk's edge nb for the 4
 // ceil(ne / 4) rows the steps read (zeros past ne and for be >= NK), jl[nb]
 // = its sender for nb < EC (edge c0 past ne, and 0 for an index outside
-// [0, n_nodes): no read leaves the caller's buffers).  alpha_h is the head's
+// [0, n_nodes): no read leaves the caller's buffers), times jmul (a row
+// stride; the product is stored as unsigned 32 bits).  alpha_h is the head's
 // row of the head-major weights (NULL: all ones).  Consecutive threads take
 // consecutive components of one edge (contiguous R loads, conflict-free LDS
 // stores); four values per thread in flight, loads before stores.  Needs
@@ -563,7 +564,7 @@ constexpr int kOuterStages = 3;
 template <int NK, int MP, int AS, int EC>
 __device__ __forceinline__ void stage_chunk(const float* __restrict__ Re, const float* __restrict__ alpha_h,
                                             const int32_t* __restrict__ col, int64_t c0, int ne, int n_nodes,
-                                            float* __restrict__ Al, int* __restrict__ jl) {
+                                            float* __restrict__ Al, int* __restrict__ jl, unsigned jmul = 1) {
   const int nsl = 4 * ((ne + 3) / 4) * MP;
   int jv = threadIdx.x < EC ? col[c0 + ((int)threadIdx.x < ne ? threadIdx.x : 0)] : 0;
   jv = (unsigned)jv < (unsigned)n_nodes ? jv : 0;
@@ -584,7 +585,7 @@ __device__ __forceinline__ void stage_chunk(const float* __restrict__ Re, const 
       if (idx < nsl) Al[(idx / MP) * AS + idx % MP] = okv[u] ? av[u] * rv[u] : 0.0f;
     }
   }
-  if (threadIdx.x < EC) jl[threadIdx.x] = jv;
+  if (threadIdx.x < EC) jl[threadIdx.x] = (int)((unsigned)jv * jmul);
 }
 
 // The j-side coupling of one receiver's G (in LDS, rows of GS floats) into
@@ -867,24 +868,30 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
   constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
   constexpr int EC = kOuterEdges, AS = MP + 16;
   constexpr int QB = fuse_qblock(NK), FS = fuse_stride(NK);
+  constexpr int NG = (NK + 3) / 4;  // groups of four components (one per wave)
   extern __shared__ float sm[];
-  float* Al = sm;                  // [EC][AS] alpha R of the chunk's edges
-  int* jl = (int*)(sm + EC * AS);  // [EC] senders
-  float* yp = sm;                  // [NW][MP][16] the waves' shares of y (after the products)
+  // staging: rows EC .. EC+PR-1 are padding (zero weights, sender offset 0):
+  // the last iteration of the step loop starts at a step st <= ns - 1 and
+  // loads up to step st + 2 (kOuterStages - 1) ahead, i.e. rows up to
+  // 4 (ns + 3) + 3 <= EC + 15
+  constexpr int PR = 4 * (2 * kOuterStages - 2);
+  static_assert(PR >= 16, "padding rows must cover the prefetch past a full chunk");
+  float* Al = sm;                         // [EC + PR][AS] alpha R of the chunk's edges
+  int* jo = (int*)(sm + (EC + PR) * AS);  // [EC + PR] the senders' offsets in featq (float4)
+  float* yp = sm;                        // [NW][MP][16] the waves' shares of y (after the products)
   const int bid = blockIdx.x, xcd = bid % 8, local = bid / 8;
   const int h = local % H, rfirst = xcd * nrx + (local / H) * rpw;
   const int rlast = min(min(rfirst + rpw, (xcd + 1) * nrx), n);  // uniform over the workgroup
   const int NW = blockDim.x >> 6, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int l16 = lane & 15, k4 = lane >> 4;
-  constexpr int NG = (NK + 3) / 4;  // groups of four components (one per wave)
-  bool live[4];
-#pragma unroll
-  for (int w = 0; w < 4; ++w) live[w] = __builtin_amdgcn_readfirstlane(4 * wave + w < NK ? 1 : 0) != 0;
-  // the lane's float4 of a sender: its wave's group (a wave past the groups
-  // reads the last one and multiplies nothing), channel t = l16
-  const int64_t fstride = (int64_t)H * NG * 16;  // float4 per node
-  const int foff = (h * NG + min(wave, NG - 1)) * 16 + l16;
+  // the wave's live tiles (components 4 wave .. 4 wave + nl - 1; uniform) and
+  // the lane's float4 of a sender: its wave's group, channel t = l16
+  const int nl = __builtin_amdgcn_readfirstlane(min(max(NK - 4 * wave, 0), 4));
+  const unsigned fstride = (unsigned)(H * NG * 16);
+  const unsigned foff = (unsigned)((h * NG + min(wave, NG - 1)) * 16 + l16);
   const float* ah = alpha_hm ? alpha_hm + (int64_t)(h / hdiv) * n_edges : nullptr;
+  for (int q = threadIdx.x; q < PR * AS; q += blockDim.x) Al[EC * AS + q] = 0.0f;
+  if (threadIdx.x < PR) jo[EC + threadIdx.x] = 0;
   for (int r = rfirst; r < rlast; ++r) {
     const int i = order[r];
     v4f acc[MT][4];
@@ -898,81 +905,97 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
     for (int64_t c0 = e0; c0 < e1; c0 += EC) {
       const int ne = (int)min((int64_t)EC, e1 - c0);
       __syncthreads();  // the previous chunk's (or receiver's) reads of the staging space are done
-      stage_chunk<NK, MP, AS, EC>(Re, ah, col, c0, ne, n_nodes, Al, jl);
+      stage_chunk<NK, MP, AS, EC>(Re, ah, col, c0, ne, n_nodes, Al, jo, fstride);
       __syncthreads();
       const int ns = (ne + 3) / 4;
       // pipeline of the products as in k_outer_agg: the operands of steps
       // st+1, st+2 are loaded while the MFMAs of step st run; steps past ns
-      // read row EC - 1 and a valid sender and are never multiplied
-      float aq[kOuterStages][MT];
-      float4 bq[kOuterStages];
-      auto loadb = [&](int st, float* a, float4& b) {
-        const int nb = min(4 * st + k4, EC - 1);
-        b = featq[jl[nb] * fstride + foff];
+      // read rows of zeros or stale weights with valid senders and are never
+      // multiplied.  NL (the wave's live tiles) is a constant of each copy of
+      // the loop, so a step is one float4 load, two LDS reads and 2 NL MFMAs.
+      auto products = [&](auto nlc) {
+        constexpr int NL = decltype(nlc)::value;
+        float aq[kOuterStages][MT];
+        float4 bq[kOuterStages];
+        auto loadb = [&](int st, float* a, float4& b) {
+          const int nb = min(4 * st + k4, EC + PR - 1);  // < EC + 16 without the clamp (see PR)
+          b = featq[(unsigned)jo[nb] + foff];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) a[mt] = Al[nb * AS + mt * 16 + l16];
-      };
-      auto mma = [&](const float* a, const float4& b) {
-        const float bw[4] = {b.x, b.y, b.z, b.w};
+          for (int mt = 0; mt < MT; ++mt) a[mt] = Al[nb * AS + mt * 16 + l16];
+        };
+        auto mma = [&](const float* a, const float4& b) {
+          const float bw[4] = {b.x, b.y, b.z, b.w};
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          if (!live[w]) continue;
+          for (int w = 0; w < NL; ++w)
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-            acc[mt][w] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bw[w], acc[mt][w], 0, 0, 0);
+            for (int mt = 0; mt < MT; ++mt)
+              acc[mt][w] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bw[w], acc[mt][w], 0, 0, 0);
+        };
+#pragma unroll
+        for (int u = 0; u + 1 < kOuterStages; ++u) loadb(u, aq[u], bq[u]);
+        for (int st = 0; st < ns; st += kOuterStages) {
+#pragma unroll
+          for (int u = 0; u < kOuterStages; ++u) {
+            const int w = (u + kOuterStages - 1) % kOuterStages;
+            loadb(st + u + kOuterStages - 1, aq[w], bq[w]);
+            __builtin_amdgcn_sched_barrier(0);
+            if (u == 0 || st + u < ns) mma(aq[u], bq[u]);
+            __builtin_amdgcn_sched_barrier(0);
+          }
         }
       };
-#pragma unroll
-      for (int u = 0; u + 1 < kOuterStages; ++u) loadb(u, aq[u], bq[u]);
-      for (int st = 0; st < ns; st += kOuterStages) {
-#pragma unroll
-        for (int u = 0; u < kOuterStages; ++u) {
-          const int w = (u + kOuterStages - 1) % kOuterStages;
-          loadb(st + u + kOuterStages - 1, aq[w], bq[w]);
-          __builtin_amdgcn_sched_barrier(0);
-          if (u == 0 || st + u < ns) mma(aq[u], bq[u]);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      }
+      if (nl == 4) products(std::integral_constant<int, 4>{});
+      else if (nl == 3) products(std::integral_constant<int, 3>{});
+      else if (nl == 2) products(std::integral_constant<int, 2>{});
+      else if (nl == 1) products(std::integral_constant<int, 1>{});
     }
     // this wave's share of y_i: A = F_i (rows k, K = be in the step order
     // above, zero past NK), B = the accumulators.  The F loads are
-    // unconditional (lanes past a sub-block's rows or K values, and dead
-    // tiles, read a valid element and take zero), so the wait counts stay
-    // exact; the next component's values load while this one's MFMAs run.
+    // unconditional (lanes past a sub-block's rows or K values read a valid
+    // element and take zero), so the wait counts stay exact; the next
+    // component's values load while this one's MFMAs run.
     const float* Fr = F + (size_t)r * FS;
     v4f ya[MT];
 #pragma unroll
     for (int rt = 0; rt < MT; ++rt) ya[rt] = (v4f){0.f, 0.f, 0.f, 0.f};
-    float4 fv[2][MT][MT];
-    auto loadf = [&](int w, float4 (*f)[MT]) {
-      const int q = min(4 * wave + w, NK - 1);
+    auto recouple = [&](auto nlc) {
+      constexpr int NL = decltype(nlc)::value;
+      float4 fv[2][MT][MT];
+      auto loadf = [&](int w, float4 (*f)[MT]) {
+        const int q = 4 * wave + w;  // < NK for w < NL
 #pragma unroll
-      for (int rt = 0; rt < MT; ++rt)
+        for (int rt = 0; rt < MT; ++rt)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const bool ok = l16 < fuse_rows(NK, rt) && k4 < fuse_kc(NK, mt);
-          const float4 v = *(const float4*)(Fr + q * QB + fuse_blk(NK, rt, mt) +
-                                            (ok ? (k4 * fuse_rows(NK, rt) + l16) * 4 : 0));
-          f[rt][mt] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+          for (int mt = 0; mt < MT; ++mt) {
+            // (a 0/1 factor rather than a select: a value every lane uses
+            // keeps the compiler from predicating the load)
+            const bool ok = l16 < fuse_rows(NK, rt) && k4 < fuse_kc(NK, mt);
+            const float z = ok ? 1.0f : 0.0f;
+            const float4 v = *(const float4*)(Fr + q * QB + fuse_blk(NK, rt, mt) +
+                                              (ok ? (k4 * fuse_rows(NK, rt) + l16) * 4 : 0));
+            f[rt][mt] = make_float4(v.x * z, v.y * z, v.z * z, v.w * z);
+          }
+      };
+      loadf(0, fv[0]);
+#pragma unroll
+      for (int w = 0; w < NL; ++w) {
+        if (w + 1 < NL) loadf(w + 1, fv[(w + 1) & 1]);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int rt = 0; rt < MT; ++rt) {
+            const float4 f = fv[w & 1][rt][mt];
+            ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.x, acc[mt][w][0], ya[rt], 0, 0, 0);
+            ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.y, acc[mt][w][1], ya[rt], 0, 0, 0);
+            ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.z, acc[mt][w][2], ya[rt], 0, 0, 0);
+            ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.w, acc[mt][w][3], ya[rt], 0, 0, 0);
+          }
+      }
     };
-    loadf(0, fv[0]);
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      if (w + 1 < 4) loadf(w + 1, fv[(w + 1) & 1]);
-      if (!live[w]) continue;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int rt = 0; rt < MT; ++rt) {
-          const float4 f = fv[w & 1][rt][mt];
-          ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.x, acc[mt][w][0], ya[rt], 0, 0, 0);
-          ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.y, acc[mt][w][1], ya[rt], 0, 0, 0);
-          ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.z, acc[mt][w][2], ya[rt], 0, 0, 0);
-          ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.w, acc[mt][w][3], ya[rt], 0, 0, 0);
-        }
-    }
+    if (nl == 4) recouple(std::integral_constant<int, 4>{});
+    else if (nl == 3) recouple(std::integral_constant<int, 3>{});
+    else if (nl == 2) recouple(std::integral_constant<int, 2>{});
+    else if (nl == 1) recouple(std::integral_constant<int, 1>{});
     __syncthreads();  // the products' reads of the staging space are done
 #pragma unroll
     for (int rt = 0; rt < MT; ++rt)
@@ -1948,7 +1971,12 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* 
   return hipGetLastError();
 }
 
-bool outer_fused_supported(int L, int C, int H) { return L >= 0 && L <= kFuseMaxL && H >= 1 && C == 16 * H; }
+int fuse_groups(int L) { return ((L + 1) * (L + 1) + 3) / 4; }
+
+bool outer_fused_supported(int L, int C, int H, int64_t n_nodes) {
+  return L >= 0 && L <= kFuseMaxL && H >= 1 && C == 16 * H &&
+         (uint64_t)n_nodes * H * fuse_groups(L) * 16 <= 0xffffffffull;
+}
 
 hipError_t launch_fuse_build(int L, const int* fptr, const int* fidx, const double* fcoef, const double* R,
                              const int32_t* order, int n, float* F, hipStream_t s) {
@@ -1959,8 +1987,6 @@ hipError_t launch_fuse_build(int L, const int* fptr, const int* fidx, const doub
                                                                  F);
   return hipGetLastError();
 }
-
-int fuse_groups(int L) { return ((L + 1) * (L + 1) + 3) / 4; }
 
 hipError_t launch_feat_qmajor(int L, const float* feat, int n, int C, float* featq, hipStream_t s) {
   if (n == 0) return hipSuccess;
@@ -1976,10 +2002,11 @@ hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, co
                               const float* alpha_hm, int64_t n_edges, const float* featq, const int32_t* order,
                               const float* F, int n, int C, int H, int hdiv, int n_nodes, float* y, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  if (!outer_fused_supported(L, C, H)) return hipErrorInvalidValue;
+  if (!outer_fused_supported(L, C, H, n_nodes)) return hipErrorInvalidValue;
   const int nk = (L + 1) * (L + 1), mp = 16 * ((nk + 15) / 16);
   const int nw = std::max((nk + 3) / 4, 2);  // four components per wave; the staging needs kOuterEdges threads
-  const size_t lds = std::max(sizeof(float) * (size_t)kOuterEdges * (mp + 16) + sizeof(int) * kOuterEdges,
+  const int pr = 4 * (2 * kOuterStages - 2);  // padding rows of the staging (k_outer_fused)
+  const size_t lds = std::max(sizeof(float) * (size_t)(kOuterEdges + pr) * (mp + 16) + sizeof(int) * (kOuterEdges + pr),
                               sizeof(float) * (size_t)nw * mp * 16);
   static const int rpw_env = [] {
     const char* v = getenv("E2F_OUTER_RPW");

@@ -138,7 +138,9 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* 
 // floats from the fused table (fptr/fidx/fcoef, fuse_table) and R [N][nk]
 // float64; then y[order[r]] directly from the aggregated products and F row r
 // (other arguments as for launch_outer_agg)
-bool outer_fused_supported(int L, int C, int H);
+// (L <= kFuseMaxL, C = 16 H, and the re-laid features of n_nodes atoms
+// addressable with 32-bit float4 offsets)
+bool outer_fused_supported(int L, int C, int H, int64_t n_nodes);
 hipError_t launch_fuse_build(int L, const int* fptr, const int* fidx, const double* fcoef, const double* R,
                              const int32_t* order, int n, float* F, hipStream_t s);
 // featq: the features re-laid by launch_feat_qmajor, n_nodes * C * 4 * fuse_groups(L) floats
