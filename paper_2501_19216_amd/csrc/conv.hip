@@ -857,6 +857,19 @@ __global__ void k_feat_qmajor(const float* __restrict__ feat, int n, int nk, int
 // be = 16 mt + 4 k4 + s; F_i is stored in the matching order.  Each wave sums
 // its components' share of y (rows 16 rt + 4 k4 + v, channel l16); the
 // shares meet in LDS and one pass stores the head's 16 channels of y_i.
+//
+// The workgroup walks its receivers' chunks of up to kOuterEdges edges (an
+// isolated receiver is one empty chunk).  Waves 0 .. NG-1 multiply (wave v:
+// the components 4v .. 4v+3); the last wave stages: while the others multiply
+// chunk k from one LDS buffer it loads chunk k+1 (alpha, R of the edges, the
+// senders) and writes alpha R and the senders' offsets into the other, so
+// the products never wait for a chunk's loads.  One barrier per chunk (two
+// more after a receiver's last chunk, for the shares of y, which reuse the
+// finished buffer).
+// register pipeline of the fused products: kFuseStages - 1 steps ahead
+constexpr int kFuseStages = 3;
+constexpr int kFuseRows = kOuterEdges + 4 * (2 * kFuseStages - 2);  // staging rows with the prefetch padding
+
 template <int L, int LB>
 __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re, const int64_t* __restrict__ row_ptr,
                                                     const int32_t* __restrict__ col,
@@ -868,57 +881,143 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
   constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
   constexpr int EC = kOuterEdges, AS = MP + 16;
   constexpr int QB = fuse_qblock(NK), FS = fuse_stride(NK);
-  constexpr int NG = (NK + 3) / 4;  // groups of four components (one per wave)
-  extern __shared__ float sm[];
-  // staging: rows EC .. EC+PR-1 are padding (zero weights, sender offset 0):
+  constexpr int NG = (NK + 3) / 4;  // groups of four components: one product wave each
+  // rows EC .. SR-1 of a buffer are padding (zero weights, sender offset 0):
   // the last iteration of the step loop starts at a step st <= ns - 1 and
-  // loads up to step st + 2 (kOuterStages - 1) ahead, i.e. rows up to
-  // 4 (ns + 3) + 3 <= EC + 15
-  constexpr int PR = 4 * (2 * kOuterStages - 2);
-  static_assert(PR >= 16, "padding rows must cover the prefetch past a full chunk");
-  float* Al = sm;                         // [EC + PR][AS] alpha R of the chunk's edges
-  int* jo = (int*)(sm + (EC + PR) * AS);  // [EC + PR] the senders' offsets in featq (float4)
-  float* yp = sm;                        // [NW][MP][16] the waves' shares of y (after the products)
+  // loads up to step st + 2 (kFuseStages - 1) ahead, i.e. rows up to
+  // 4 (ns - 1 + 2 (kFuseStages - 1)) + 3 <= EC + 8 kFuseStages - 9
+  constexpr int SR = kFuseRows, SB = SR * AS;
+  static_assert(SR - EC >= 8 * kFuseStages - 8, "padding rows must cover the prefetch past a full chunk");
+  static_assert(NG * MP * 16 <= SB, "the shares of y must fit one staging buffer");
+  constexpr int RPI = 64 / MP;            // rows the staging wave covers per pass (lane: be = lane % MP)
+  constexpr int ITER = EC / RPI;          // passes over a full chunk
+  extern __shared__ float sm[];
+  float* Alb = sm;                        // [2][SR][AS] alpha R of the chunk's edges (zero past its rows)
+  int* job = (int*)(sm + 2 * SB);         // [2][SR] the senders' offsets in featq (float4)
+  float* sa = sm + 2 * SB + 2 * SR;       // [EC] the staging wave's copy of the chunk's weights
   const int bid = blockIdx.x, xcd = bid % 8, local = bid / 8;
   const int h = local % H, rfirst = xcd * nrx + (local / H) * rpw;
   const int rlast = min(min(rfirst + rpw, (xcd + 1) * nrx), n);  // uniform over the workgroup
-  const int NW = blockDim.x >> 6, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (rfirst >= rlast) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int l16 = lane & 15, k4 = lane >> 4;
-  // the wave's live tiles (components 4 wave .. 4 wave + nl - 1; uniform) and
+  const bool stager = wave == NG;  // uniform over the wave
+  // a product wave's live tiles (components 4 wave .. 4 wave + nl - 1) and
   // the lane's float4 of a sender: its wave's group, channel t = l16
-  const int nl = __builtin_amdgcn_readfirstlane(min(max(NK - 4 * wave, 0), 4));
+  const int nl = stager ? 0 : __builtin_amdgcn_readfirstlane(min(NK - 4 * wave, 4));
   const unsigned fstride = (unsigned)(H * NG * 16);
   const unsigned foff = (unsigned)((h * NG + min(wave, NG - 1)) * 16 + l16);
   const float* ah = alpha_hm ? alpha_hm + (int64_t)(h / hdiv) * n_edges : nullptr;
-  for (int q = threadIdx.x; q < PR * AS; q += blockDim.x) Al[EC * AS + q] = 0.0f;
-  if (threadIdx.x < PR) jo[EC + threadIdx.x] = 0;
-  for (int r = rfirst; r < rlast; ++r) {
+  for (int q = threadIdx.x; q < 2 * (SR - EC) * AS; q += blockDim.x) {
+    const int b = q / ((SR - EC) * AS);
+    Alb[b * SB + EC * AS + q % ((SR - EC) * AS)] = 0.0f;
+  }
+  for (int q = threadIdx.x; q < 2 * (SR - EC); q += blockDim.x) job[(q / (SR - EC)) * SR + EC + q % (SR - EC)] = 0;
+  // edge range of receiver row r (clamped to [0, E]: a malformed graph
+  // cannot move a read outside the caller's buffers)
+  auto bounds = [&](int r, int64_t& e0, int64_t& e1) {
     const int i = order[r];
-    v4f acc[MT][4];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int w = 0; w < 4; ++w) acc[mt][w] = (v4f){0.f, 0.f, 0.f, 0.f};
     const int64_t rb0 = row_ptr[i], rb1 = row_ptr[i + 1];
-    const int64_t e0 = rb0 < 0 ? 0 : (rb0 > n_edges ? n_edges : rb0);
-    const int64_t e1 = rb1 < e0 ? e0 : (rb1 > n_edges ? n_edges : rb1);
-    for (int64_t c0 = e0; c0 < e1; c0 += EC) {
-      const int ne = (int)min((int64_t)EC, e1 - c0);
-      __syncthreads();  // the previous chunk's (or receiver's) reads of the staging space are done
-      stage_chunk<NK, MP, AS, EC>(Re, ah, col, c0, ne, n_nodes, Al, jo, fstride);
-      __syncthreads();
+    e0 = rb0 < 0 ? 0 : (rb0 > n_edges ? n_edges : rb0);
+    e1 = rb1 < e0 ? e0 : (rb1 > n_edges ? n_edges : rb1);
+  };
+  // the staging wave: chunk [c0, c0 + ne) into buffer b.  Every sender
+  // offset below EC is written (0 past ne); the weight rows read by the
+  // chunk's steps (4 ceil(ne / 4)) are written whole, zero past ne and in
+  // the columns NK .. MP-1.  Lane: component be = lane % MP of rows
+  // rs + RPI it; the R values load in batches of BT rows per lane, the next
+  // batch in flight while the current one is stored (clamped addresses, so
+  // the loads are unconditional; an empty chunk loads none).
+  auto stage = [&](int64_t c0, int ne, int b) {
+    float* Al = Alb + b * SB;
+    int* jo = job + b * SR;
+    float av[EC / 64];
+    int jv[EC / 64];
+#pragma unroll
+    for (int u = 0; u < EC / 64; ++u) {
+      const int nb = lane + 64 * u;
+      av[u] = nb < ne ? (ah ? ah[c0 + nb] : 1.0f) : 0.0f;
+      const int j = nb < ne ? col[c0 + nb] : 0;
+      jv[u] = (unsigned)j < (unsigned)n_nodes ? j : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < EC / 64; ++u) {
+      sa[lane + 64 * u] = av[u];
+      jo[lane + 64 * u] = (int)((unsigned)jv[u] * fstride);
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (ne == 0) return;
+    const int nrow = 4 * ((ne + 3) / 4);
+    const int be = lane % MP, rs = lane / MP;
+    const bool bok = be < NK;
+    // the lane's rows rs + RPI (BT bt + k): one base per batch, immediate
+    // offsets within it; rows past ne are not loaded
+    const float* src = Re + (size_t)(c0 + rs) * NK + (bok ? be : 0);
+    constexpr int BT = 16, NBT = ITER / BT;
+    static_assert(ITER % BT == 0, "batches must cover a chunk");
+    float cur[BT], nxt[BT];
+    auto load = [&](int bt, float* d) {
+      const float* sb = src + (size_t)bt * BT * RPI * NK;
+#pragma unroll
+      for (int k = 0; k < BT; ++k) d[k] = (bt * BT + k) * RPI + rs < ne ? sb[k * RPI * NK] : 0.0f;
+    };
+    load(0, cur);
+#pragma unroll 1
+    for (int bt = 0; bt < NBT && bt * BT * RPI < nrow; ++bt) {
+      const bool more_rows = bt + 1 < NBT && (bt + 1) * BT * RPI < nrow;
+      if (more_rows) load(bt + 1, nxt);
+#pragma unroll
+      for (int k = 0; k < BT; ++k) {
+        const int nb = (bt * BT + k) * RPI + rs;
+        if (nb < nrow) Al[nb * AS + be] = bok ? cur[k] * sa[nb] : 0.0f;
+      }
+      if (more_rows) {
+#pragma unroll
+        for (int k = 0; k < BT; ++k) cur[k] = nxt[k];
+      }
+    }
+  };
+  int r = rfirst;
+  int64_t e0, e1;
+  bounds(r, e0, e1);
+  int64_t c0 = e0;
+  if (stager) stage(c0, (int)min((int64_t)EC, e1 - c0), 0);
+  __syncthreads();
+  v4f acc[MT][4];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) acc[mt][w] = (v4f){0.f, 0.f, 0.f, 0.f};
+  for (int kb = 0;; kb ^= 1) {
+    const int ne = (int)min((int64_t)EC, e1 - c0);  // 0 for an isolated receiver
+    const bool last = c0 + EC >= e1;                 // the receiver's last chunk (uniform)
+    int rn = r;
+    int64_t c0n = c0 + EC, e0n = e0, e1n = e1;
+    if (last) {
+      rn = r + 1;
+      if (rn < rlast) {
+        bounds(rn, e0n, e1n);
+        c0n = e0n;
+      }
+    }
+    const bool more = rn < rlast;
+    if (stager) {
+      if (more) stage(c0n, (int)min((int64_t)EC, e1n - c0n), kb ^ 1);
+    } else {
+      const float* Al = Alb + kb * SB;
+      const int* jo = job + kb * SR;
       const int ns = (ne + 3) / 4;
-      // pipeline of the products as in k_outer_agg: the operands of steps
-      // st+1, st+2 are loaded while the MFMAs of step st run; steps past ns
-      // read rows of zeros or stale weights with valid senders and are never
-      // multiplied.  NL (the wave's live tiles) is a constant of each copy of
-      // the loop, so a step is one float4 load, two LDS reads and 2 NL MFMAs.
+      // pipeline of the products: the operands of steps st+1, st+2 are
+      // loaded while the MFMAs of step st run; steps past ns read rows of
+      // zeros or stale weights with valid senders and are never multiplied.
+      // NL (the wave's live tiles) is a constant of each copy of the loop,
+      // so a step is one float4 load, two LDS reads and 2 NL MFMAs.
       auto products = [&](auto nlc) {
         constexpr int NL = decltype(nlc)::value;
-        float aq[kOuterStages][MT];
-        float4 bq[kOuterStages];
+        float aq[kFuseStages][MT];
+        float4 bq[kFuseStages];
         auto loadb = [&](int st, float* a, float4& b) {
-          const int nb = min(4 * st + k4, EC + PR - 1);  // < EC + 16 without the clamp (see PR)
+          const int nb = min(4 * st + k4, SR - 1);  // < SR without the clamp (see SR)
           b = featq[(unsigned)jo[nb] + foff];
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) a[mt] = Al[nb * AS + mt * 16 + l16];
@@ -932,12 +1031,12 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
               acc[mt][w] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bw[w], acc[mt][w], 0, 0, 0);
         };
 #pragma unroll
-        for (int u = 0; u + 1 < kOuterStages; ++u) loadb(u, aq[u], bq[u]);
-        for (int st = 0; st < ns; st += kOuterStages) {
+        for (int u = 0; u + 1 < kFuseStages; ++u) loadb(u, aq[u], bq[u]);
+        for (int st = 0; st < ns; st += kFuseStages) {
 #pragma unroll
-          for (int u = 0; u < kOuterStages; ++u) {
-            const int w = (u + kOuterStages - 1) % kOuterStages;
-            loadb(st + u + kOuterStages - 1, aq[w], bq[w]);
+          for (int u = 0; u < kFuseStages; ++u) {
+            const int w = (u + kFuseStages - 1) % kFuseStages;
+            loadb(st + u + kFuseStages - 1, aq[w], bq[w]);
             __builtin_amdgcn_sched_barrier(0);
             if (u == 0 || st + u < ns) mma(aq[u], bq[u]);
             __builtin_amdgcn_sched_barrier(0);
@@ -949,65 +1048,81 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
       else if (nl == 2) products(std::integral_constant<int, 2>{});
       else if (nl == 1) products(std::integral_constant<int, 1>{});
     }
-    // this wave's share of y_i: A = F_i (rows k, K = be in the step order
-    // above, zero past NK), B = the accumulators.  The F loads are
-    // unconditional (lanes past a sub-block's rows or K values read a valid
-    // element and take zero), so the wait counts stay exact; the next
-    // component's values load while this one's MFMAs run.
-    const float* Fr = F + (size_t)r * FS;
-    v4f ya[MT];
+    if (last) {
+      // this wave's share of y_i: A = F_i (rows k, K = be in the step order
+      // above, zero past NK), B = the accumulators.  The F loads are
+      // unconditional (lanes past a sub-block's rows or K values read a
+      // valid element and take zero), so the wait counts stay exact; the
+      // next component's values load while this one's MFMAs run.
+      const float* Fr = F + (size_t)r * FS;
+      v4f ya[MT];
 #pragma unroll
-    for (int rt = 0; rt < MT; ++rt) ya[rt] = (v4f){0.f, 0.f, 0.f, 0.f};
-    auto recouple = [&](auto nlc) {
-      constexpr int NL = decltype(nlc)::value;
-      float4 fv[2][MT][MT];
-      auto loadf = [&](int w, float4 (*f)[MT]) {
-        const int q = 4 * wave + w;  // < NK for w < NL
+      for (int rt = 0; rt < MT; ++rt) ya[rt] = (v4f){0.f, 0.f, 0.f, 0.f};
+      auto recouple = [&](auto nlc) {
+        constexpr int NL = decltype(nlc)::value;
+        float4 fv[2][MT][MT];
+        auto loadf = [&](int w, float4 (*f)[MT]) {
+          const int q = 4 * wave + w;  // < NK for w < NL
+#pragma unroll
+          for (int rt = 0; rt < MT; ++rt)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+              // (a 0/1 factor rather than a select: a value every lane uses
+              // keeps the compiler from predicating the load)
+              const bool ok = l16 < fuse_rows(NK, rt) && k4 < fuse_kc(NK, mt);
+              const float z = ok ? 1.0f : 0.0f;
+              const float4 v = *(const float4*)(Fr + q * QB + fuse_blk(NK, rt, mt) +
+                                                (ok ? (k4 * fuse_rows(NK, rt) + l16) * 4 : 0));
+              f[rt][mt] = make_float4(v.x * z, v.y * z, v.z * z, v.w * z);
+            }
+        };
+        loadf(0, fv[0]);
+#pragma unroll
+        for (int w = 0; w < NL; ++w) {
+          if (w + 1 < NL) loadf(w + 1, fv[(w + 1) & 1]);
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int rt = 0; rt < MT; ++rt) {
+              const float4 f = fv[w & 1][rt][mt];
+              ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.x, acc[mt][w][0], ya[rt], 0, 0, 0);
+              ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.y, acc[mt][w][1], ya[rt], 0, 0, 0);
+              ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.z, acc[mt][w][2], ya[rt], 0, 0, 0);
+              ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.w, acc[mt][w][3], ya[rt], 0, 0, 0);
+            }
+        }
+      };
+      if (nl == 4) recouple(std::integral_constant<int, 4>{});
+      else if (nl == 3) recouple(std::integral_constant<int, 3>{});
+      else if (nl == 2) recouple(std::integral_constant<int, 2>{});
+      else if (nl == 1) recouple(std::integral_constant<int, 1>{});
+      __syncthreads();  // every product wave is done with buffer kb: it takes the shares of y
+      float* yp = Alb + kb * SB;  // [NG][MP][16]
+      if (!stager) {
 #pragma unroll
         for (int rt = 0; rt < MT; ++rt)
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            // (a 0/1 factor rather than a select: a value every lane uses
-            // keeps the compiler from predicating the load)
-            const bool ok = l16 < fuse_rows(NK, rt) && k4 < fuse_kc(NK, mt);
-            const float z = ok ? 1.0f : 0.0f;
-            const float4 v = *(const float4*)(Fr + q * QB + fuse_blk(NK, rt, mt) +
-                                              (ok ? (k4 * fuse_rows(NK, rt) + l16) * 4 : 0));
-            f[rt][mt] = make_float4(v.x * z, v.y * z, v.z * z, v.w * z);
-          }
-      };
-      loadf(0, fv[0]);
-#pragma unroll
-      for (int w = 0; w < NL; ++w) {
-        if (w + 1 < NL) loadf(w + 1, fv[(w + 1) & 1]);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int rt = 0; rt < MT; ++rt) {
-            const float4 f = fv[w & 1][rt][mt];
-            ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.x, acc[mt][w][0], ya[rt], 0, 0, 0);
-            ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.y, acc[mt][w][1], ya[rt], 0, 0, 0);
-            ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.z, acc[mt][w][2], ya[rt], 0, 0, 0);
-            ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.w, acc[mt][w][3], ya[rt], 0, 0, 0);
-          }
+          for (int v = 0; v < 4; ++v) yp[(wave * MP + 16 * rt + 4 * k4 + v) * 16 + l16] = ya[rt][v];
       }
-    };
-    if (nl == 4) recouple(std::integral_constant<int, 4>{});
-    else if (nl == 3) recouple(std::integral_constant<int, 3>{});
-    else if (nl == 2) recouple(std::integral_constant<int, 2>{});
-    else if (nl == 1) recouple(std::integral_constant<int, 1>{});
-    __syncthreads();  // the products' reads of the staging space are done
+      __syncthreads();
+      const int i = order[r];
+      for (int idx = threadIdx.x; idx < NK * 16; idx += blockDim.x) {
+        const int row = idx >> 4, t = idx & 15;
+        float sum = 0.0f;
+        for (int wv = 0; wv < NG; ++wv) sum += yp[(wv * MP + row) * 16 + t];
+        y[((size_t)i * NK + row) * C + h * 16 + t] = sum;
+      }
 #pragma unroll
-    for (int rt = 0; rt < MT; ++rt)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) yp[(wave * MP + 16 * rt + 4 * k4 + v) * 16 + l16] = ya[rt][v];
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < NK * 16; idx += blockDim.x) {
-      const int row = idx >> 4, t = idx & 15;
-      float sum = 0.0f;
-      for (int wv = 0; wv < NW; ++wv) sum += yp[(wv * MP + row) * 16 + t];
-      y[((size_t)i * NK + row) * C + h * 16 + t] = sum;
+        for (int w = 0; w < 4; ++w) acc[mt][w] = (v4f){0.f, 0.f, 0.f, 0.f};
     }
+    if (!more) break;
+    __syncthreads();  // buffer kb ^ 1 is staged; buffer kb (and the shares of y) is free
+    r = rn;
+    c0 = c0n;
+    e0 = e0n;
+    e1 = e1n;
   }
 }
 
@@ -2004,10 +2119,8 @@ hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, co
   if (n == 0) return hipSuccess;
   if (!outer_fused_supported(L, C, H, n_nodes)) return hipErrorInvalidValue;
   const int nk = (L + 1) * (L + 1), mp = 16 * ((nk + 15) / 16);
-  const int nw = std::max((nk + 3) / 4, 2);  // four components per wave; the staging needs kOuterEdges threads
-  const int pr = 4 * (2 * kOuterStages - 2);  // padding rows of the staging (k_outer_fused)
-  const size_t lds = std::max(sizeof(float) * (size_t)(kOuterEdges + pr) * (mp + 16) + sizeof(int) * (kOuterEdges + pr),
-                              sizeof(float) * (size_t)nw * mp * 16);
+  const int nw = (nk + 3) / 4 + 1;  // a product wave per group of four components, and the staging wave
+  const size_t lds = sizeof(float) * (2 * (size_t)kFuseRows * (mp + 16) + 2 * (size_t)kFuseRows + kOuterEdges);
   static const int rpw_env = [] {
     const char* v = getenv("E2F_OUTER_RPW");
     return v ? atoi(v) : 0;
