@@ -113,6 +113,16 @@ def alg_counts(e2f, L, C, H, n, E, fused=False):
                 recouple_entries=cnt["q_slots"])
 
 
+def morton_order(pos, cell=4.0):
+    """Atom indices sorted by the Morton key of their 4 A cells."""
+    q = np.floor((pos - pos.min(0)) / cell).astype(np.int64)
+    key = np.zeros(len(pos), dtype=np.int64)
+    for b in range(10):
+        for a in range(3):
+            key |= ((q[:, a] >> b) & 1) << (3 * b + a)
+    return np.argsort(key, kind="stable").astype(np.int32)
+
+
 def roof_of(bytes_, flops, t_ms, peak_tf):
     """Roofline position of one launch: the binding resource is the one
     whose lower-bound time is larger."""
@@ -464,6 +474,37 @@ def main():
     print("[bench] fwd %.3f ms, edge-TP %.3f ms, graph %.3f ms" % (ms_fwd, ms_edge, ms_nl), file=sys.stderr,
           flush=True)
 
+    # ---- the aggregation alone on stored node tensors T [n][H][dimT][C/H]
+    # (random; the unfused form of the aggregation, for its HBM rate): kernel
+    # time from HIP events, the call (with its checked plan and one read-back)
+    # by the wall clock
+    dimT = layer_counts(L)["dimT"]
+    T_a3 = torch.randn(n, H, dimT, C // H, device=dev, generator=g)
+    S_a3 = torch.empty_like(T_a3)
+    order_a3 = torch.from_numpy(morton_order(inp.pos)).to(dev)  # blocks of close receivers
+    a3_call = lambda: e2f.e2f_aggregate(ctx, T_a3, row_ptr, col, alpha, out=S_a3, order=order_a3)
+    a3_call()
+    e2f.e2f_profile(ctx, True)
+    ms_a3_call = timed(a3_call, max(3, args.steps // 2))
+    prof_a3 = e2f.e2f_profile_read(ctx)
+    e2f.e2f_profile(ctx, False)
+    t_a3 = prof_a3["a3_aggregate"][1] / prof_a3["a3_aggregate"][0]
+    a3_bytes = 2.0 * 4 * n * dimT * C + E * (4.0 + 4.0 * H) + 8.0 * (n + 1)  # T once, S once, CSR, weights
+    a3_flops = 2.0 * E * dimT * C
+    a3 = {"kernel_ms": t_a3, "call_ms": ms_a3_call, "alg_bytes": a3_bytes, "alg_flops": a3_flops,
+          "alg_GBps": a3_bytes / (t_a3 * 1e-3) / 1e9, "alg_frac_hbm": a3_bytes / (t_a3 * 1e-3) / 1e9 / HBM_PEAK_GBS,
+          "alg_TFLOPs": a3_flops / (t_a3 * 1e-3) / 1e12, "traffic": None}
+    a3_path = os.path.join(ROOT, "profiles", "traffic_a3_%s.json" % wl.name)
+    if os.path.exists(a3_path):
+        tr = json.load(open(a3_path))
+        if tr.get("conv_sha256") == file_sha(os.path.join(ROOT, "paper_2501_19216_amd", "csrc", "conv.hip")):
+            a3["traffic"] = tr["bytes_per_launch"]
+            a3["traffic_GBps"] = tr["bytes_per_launch"] / (t_a3 * 1e-3) / 1e9
+            a3["traffic_frac_hbm"] = a3["traffic_GBps"] / HBM_PEAK_GBS
+    del T_a3, S_a3, order_a3
+    print("[bench] aggregation alone %.3f ms (%.0f GB/s of compulsory bytes)" % (t_a3, a3["alg_GBps"]),
+          file=sys.stderr, flush=True)
+
     kernels = {k: dict(launches=v[0] // args.steps, ms=v[1] / args.steps) for k, v in prof.items()}
     fused = "fuse_build" in prof  # the aggregation applied the recouple itself
     counts = alg_counts(e2f, L, C, H, n, E, fused)
@@ -591,6 +632,7 @@ def main():
                      "grad_pos_ms": ms_bwd_pos},
         "global_moment": {"ms": ms_glob, "pairs": n * n, "atoms_per_s": n / (ms_glob * 1e-3)},
         "attention": {"ms": ms_att, "dk": 16, "n_rbf": 8, "bytes_GBps": (E * (4 + 4 * H) + 12.0 * n) / (ms_att * 1e-3) / 1e9},
+        "aggregate_alone": a3,
         "counts": {"dimT": counts["dimT"], "coupling_entries": counts["coupling_entries"],
                    "recouple_entries": counts["recouple_entries"]},
         "kernels": kernels,

@@ -137,6 +137,34 @@ e2f_status e2f_solid_harmonics(e2f_ctx* ctx, const float* pos, const float* orig
 e2f_status e2f_node_tp(e2f_ctx* ctx, const float* pos, const float* origins, const int32_t* origin_id,
                        const float* feat, int32_t n, int32_t channels, int lmax, float* out, void* stream);
 
+/* Attention-weighted aggregation of stored node tensors, on its own (the
+ * aggregation of Alg. 1, its einsum "ijh,jhds->ihds" restricted to the
+ * graph's edges, with T_j already made): for every receiver i, head h, row
+ * k < rows and channel t < C/heads of the head,
+ *     S[i][h][k][t] = sum over the edges e = (i, j) of row i of alpha[e][h] T[j][h][k][t].
+ * T, S: device [n][heads][rows][C/heads] float32 (head-major: a head's
+ * rows * C/heads values contiguous; S is written whole, isolated receivers
+ * get zeros).  row_ptr [n+1], col_idx [n_edges]: CSR whose rows list their
+ * senders strictly ascending (as e2f_neighbor_list writes them).  alpha:
+ * [n_edges][heads] in CSR order, or NULL (ones).  C/heads a multiple of 4;
+ * n_edges < 2^31.  Blocks of 16 receivers, consecutive in `order` (device
+ * [n], a permutation of 0..n-1; NULL = index order), aggregate the union of
+ * their senders on the matrix cores (A = the block's weights, B = the
+ * union's rows of T), so each row of T read from L2 serves every receiver of
+ * the block that has it as a neighbour: an order that keeps close atoms
+ * together (a cell or Morton order of the positions) makes the unions small.
+ * If some block has more than 8192 edges every receiver is summed on its own
+ * instead.  The graph is checked first (the bits of e2f_validate_graph, 16
+ * for a row not strictly ascending, 32 for an order that is not a
+ * permutation: E2F_EINVAL, nothing written).  workspace:
+ * e2f_aggregate_workspace_size bytes, 256-byte aligned (E2F_ECAPACITY
+ * below).  Deterministic for a given order.  (sync: one read-back of the
+ * check and the largest block) */
+e2f_status e2f_aggregate_workspace_size(e2f_ctx* ctx, int32_t n, int64_t n_edges, int32_t heads, size_t* bytes);
+e2f_status e2f_aggregate(e2f_ctx* ctx, const float* T, int32_t n, int32_t rows, int32_t channels, int32_t heads,
+                         const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges, const float* alpha,
+                         const int32_t* order, float* S, void* workspace, size_t workspace_bytes, void* stream);
+
 typedef struct {
   int lmax;              /* L, 0..6 */
   int32_t channels;      /* C, a multiple of 4, <= 1024 */

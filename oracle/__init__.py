@@ -74,6 +74,8 @@ def lib():
             L.e2fo_conv_global.argtypes = [i, i, p, p, i, p, p, p, i, p]
             L.e2fo_mix.restype = None
             L.e2fo_mix.argtypes = [i, i, i, p, p, p]
+            L.e2fo_aggregate.restype = i
+            L.e2fo_aggregate.argtypes = [i, i, i64, p, p, p, p, p, i, p]
             _lib = L
     return _lib
 
@@ -281,6 +283,27 @@ def mix(lmax, y, W) -> np.ndarray:
     W = _c(W, np.float32)
     out = np.zeros_like(y)
     lib().e2fo_mix(lmax, y.shape[2], y.shape[0], _ptr(y), _ptr(W), _ptr(out))
+    return out
+
+
+def aggregate(T, row_ptr, col_idx, alpha=None, rows=None) -> np.ndarray:
+    """S[i][h] = sum over row i's edges e = (i, j) of alpha[e][h] T[j][h]
+    (Alg. 1's einsum "ijh,jhds->ihds" over the graph's edges), float64, for
+    T [n, H, ...] float32 and alpha [E, H] or None (ones); rows: receivers
+    (default all)."""
+    T = _c(T, np.float32)
+    n, H = T.shape[0], T.shape[1]
+    W = int(np.prod(T.shape[2:]))
+    row_ptr = _c(row_ptr, np.int64)
+    col_idx = _c(col_idx, np.int32)
+    a = None if alpha is None else _c(alpha, np.float32)
+    r = None if rows is None else _c(rows, np.int32)
+    nr = n if r is None else r.shape[0]
+    out = np.zeros((nr,) + T.shape[1:])
+    rc = lib().e2fo_aggregate(n, H, W, _ptr(T), _ptr(row_ptr), _ptr(col_idx), None if a is None else _ptr(a),
+                              None if r is None else _ptr(r), nr, _ptr(out))
+    if rc:
+        raise ValueError("aggregate: an index is out of range")
     return out
 
 

@@ -29,6 +29,8 @@
  *   - the layer by the node factorisation of Thm. 3.3 / Alg. 1 (for the
  *     equality check of the two forms only);
  *   - the per-irrep linear channel mix of App. F;
+ *   - the attention-weighted aggregation of stored node tensors, Alg. 1's
+ *     einsum "ijh,jhds->ihds" summed over the graph's edges;
  *   - the vector-Jacobian products of the layer with respect to the features
  *     and the attention weights, by the definition (the layer is linear in
  *     both).
@@ -873,4 +875,33 @@ void e2fo_mix(int L, int C, int n_rows, const double *y, const float *W, double 
                     orow[cp] = s;
                 }
             }
+}
+
+/* ---------- aggregation of stored node tensors (Alg. 1's einsum "ijh,jhds->ihds") ----------
+ * For the receivers rows[r] (all n if rows is NULL):
+ *     out[r][h][k] = sum over the edges e = (i, j) of row i of alpha[e][h] T[j][h][k],
+ * T [n][H][W] (W = the values per head), alpha [E][H] or NULL (ones).
+ * Returns 1 for a receiver or sender index outside [0, n), else 0. */
+int e2fo_aggregate(int n, int H, int64_t W, const float *T, const int64_t *row_ptr, const int32_t *col_idx,
+                   const float *alpha, const int32_t *rows, int n_rows, double *out) {
+    int nr = rows ? n_rows : n;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 4) reduction(|:err)
+    for (int r = 0; r < nr; ++r) {
+        int i = rows ? rows[r] : r;
+        if (i < 0 || i >= n) { err = 1; continue; }
+        double *o = out + (size_t)r * H * W;
+        for (int64_t q = 0; q < (int64_t)H * W; ++q) o[q] = 0.0;
+        for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+            int j = col_idx[e];
+            if (j < 0 || j >= n) { err = 1; break; }
+            for (int h = 0; h < H; ++h) {
+                double a = alpha ? (double)alpha[e * H + h] : 1.0;
+                const float *t = T + ((size_t)j * H + h) * W;
+                double *oh = o + (size_t)h * W;
+                for (int64_t q = 0; q < W; ++q) oh[q] += a * (double)t[q];
+            }
+        }
+    }
+    return err;
 }

@@ -24,7 +24,7 @@ _STATUS = {0: "E2F_OK", 1: "E2F_EINVAL", 2: "E2F_ECAPACITY", 3: "E2F_ENOMEM", 4:
 # every function declared in include/e2f.h
 EXPORTED = ["e2f_create", "e2f_destroy", "e2f_last_error", "e2f_node_tp_dim", "e2f_real_cg", "e2f_knn_graph",
             "e2f_attention_weights", "e2f_recoupling_weight", "e2f_neighbor_list", "e2f_solid_harmonics",
-            "e2f_node_tp", "e2f_wigner6j_workspace_size", "e2f_wigner6j_workspace_min", "e2f_wigner6j_prepare",
+            "e2f_node_tp", "e2f_aggregate_workspace_size", "e2f_aggregate", "e2f_wigner6j_workspace_size", "e2f_wigner6j_workspace_min", "e2f_wigner6j_prepare",
             "e2f_wigner6j_conv_forward", "e2f_wigner6j_conv_forward_noalloc", "e2f_validate_graph", "e2f_wigner6j_conv_forward_dense",
             "e2f_wigner6j_conv_forward_global", "e2f_wigner6j_conv_backward", "e2f_edge_tp_conv_forward",
             "e2f_profile", "e2f_profile_read", "e2f_last_slices"]
@@ -71,6 +71,10 @@ def _load():
     L.e2f_solid_harmonics.restype = i
     L.e2f_node_tp.argtypes = [p, p, p, p, p, i32, i32, i, p, p]
     L.e2f_node_tp.restype = i
+    L.e2f_aggregate_workspace_size.argtypes = [p, i32, i64, i32, ctypes.POINTER(ctypes.c_size_t)]
+    L.e2f_aggregate_workspace_size.restype = i
+    L.e2f_aggregate.argtypes = [p, p, i32, i32, i32, i32, p, p, i64, p, p, p, p, ctypes.c_size_t, p]
+    L.e2f_aggregate.restype = i
     L.e2f_last_slices.argtypes = [p, ctypes.POINTER(i64)]
     L.e2f_last_slices.restype = i
     for name in ("e2f_wigner6j_workspace_size", "e2f_wigner6j_workspace_min"):
@@ -270,6 +274,38 @@ def e2f_node_tp(ctx: Context, pos: torch.Tensor, feat: torch.Tensor, lmax: int, 
     out = torch.empty(n, e2f_node_tp_dim(lmax), C, dtype=torch.float32, device=feat.device)
     _check(lib.e2f_node_tp(ctx.handle, _ptr(pos), _ptr(origins), _ptr(origin_id), _ptr(feat), n, C, lmax, _ptr(out),
                            _stream(feat.device)), "e2f_node_tp")
+    return out
+
+
+def e2f_aggregate(ctx: Context, T: torch.Tensor, row_ptr: torch.Tensor, col_idx: torch.Tensor,
+                  alpha: torch.Tensor | None, out: torch.Tensor | None = None,
+                  workspace: torch.Tensor | None = None, order: torch.Tensor | None = None) -> torch.Tensor:
+    """The aggregation alone: S[i][h] = sum over row i's edges e = (i, j) of
+    alpha[e][h] T[j][h] for T [n, heads, rows, C/heads] float32 (head-major);
+    alpha [E, heads] or None (ones); order: int32 [n], the permutation whose
+    consecutive receivers form the blocks (None: index order).  Returns S of
+    T's shape.  (sync)"""
+    _dev(T, torch.float32, "T")
+    _dev(row_ptr, torch.int64, "row_ptr")
+    _dev(col_idx, torch.int32, "col_idx")
+    _dev(alpha, torch.float32, "alpha")
+    _dev(order, torch.int32, "order")
+    if T.dim() != 4:
+        raise ValueError("T must be [n, heads, rows, C/heads]")
+    n, H, K, dh = T.shape
+    E = col_idx.numel()
+    if out is None:
+        out = torch.empty_like(T)
+    _dev(out, torch.float32, "out")
+    if workspace is None:
+        b = ctypes.c_size_t(0)
+        _check(lib.e2f_aggregate_workspace_size(ctx.handle, n, E, H, ctypes.byref(b)), "e2f_aggregate_workspace_size")
+        workspace = ctx.workspace_for(b.value, T.device)
+    elif not workspace.is_cuda or workspace.dtype != torch.uint8 or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 device tensor")
+    _check(lib.e2f_aggregate(ctx.handle, _ptr(T), n, K, H * dh, H, _ptr(row_ptr), _ptr(col_idx), E, _ptr(alpha),
+                             _ptr(order), _ptr(out), _ptr(workspace), workspace.numel(), _stream(T.device)),
+           "e2f_aggregate")
     return out
 
 

@@ -1072,6 +1072,105 @@ e2f_status e2f_validate_graph(e2f_ctx* ctx, int32_t n, const int64_t* row_ptr, c
   return E2F_OK;
 }
 
+// ---------------------------------------------------------------- standalone aggregation
+namespace {
+struct A3Layout {
+  size_t order = 0, blk_count = 0, blk_off = 0, ucount = 0, uni = 0, edge_slot = 0, alpha_hm = 0, tmp = 0;
+  size_t tmp_b = 0, total = 0;
+};
+A3Layout a3_layout(int n, int64_t E, int H) {
+  const int nblk = (n + 15) / 16;
+  A3Layout f;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += al256(bytes);
+    return at;
+  };
+  f.order = take(sizeof(int32_t) * (size_t)n);
+  f.blk_count = take(sizeof(int32_t) * (size_t)(nblk + 1));
+  f.blk_off = take(sizeof(int32_t) * (size_t)(nblk + 1));
+  f.ucount = take(sizeof(int32_t) * (size_t)(nblk + 1));
+  f.uni = take(sizeof(int32_t) * (size_t)E);
+  f.edge_slot = take(sizeof(int32_t) * (size_t)E);
+  f.alpha_hm = take(sizeof(float) * (size_t)E * H);
+  f.tmp_b = blocks_tmp_bytes(std::max(nblk, 1));
+  f.tmp = take(f.tmp_b);
+  f.total = off;
+  return f;
+}
+
+e2f_status check_a3(int32_t n, int32_t rows, int32_t channels, int32_t heads, int64_t n_edges) {
+  if (n < 0 || n_edges < 0) return fail(E2F_EINVAL, "n or n_edges < 0");
+  if (rows < 1 || channels < 1 || heads < 1) return fail(E2F_EINVAL, "rows, channels and heads must be positive");
+  if (channels % heads || (channels / heads) % 4)
+    return fail(E2F_EINVAL, "channels %d must split into heads of a multiple of 4 channels", channels);
+  if (n_edges >= ((int64_t)1 << 31)) return fail(E2F_EUNSUPPORTED, "n_edges must be below 2^31");
+  if ((double)n * rows * channels > 4.0e18) return fail(E2F_EINVAL, "index space overflows int64");
+  return E2F_OK;
+}
+}  // namespace
+
+e2f_status e2f_aggregate_workspace_size(e2f_ctx* ctx, int32_t n, int64_t n_edges, int32_t heads, size_t* bytes) {
+  if (!ctx || !bytes) return fail(E2F_EINVAL, "ctx and bytes are required");
+  if (e2f_status rs = check_a3(n, 1, 4 * std::max(heads, 1), heads, n_edges); rs != E2F_OK) return rs;
+  *bytes = a3_layout(n, n_edges, heads).total;
+  return E2F_OK;
+}
+
+e2f_status e2f_aggregate(e2f_ctx* ctx, const float* T, int32_t n, int32_t rows, int32_t channels, int32_t heads,
+                         const int64_t* row_ptr, const int32_t* col_idx, int64_t n_edges, const float* alpha,
+                         const int32_t* order_in, float* S, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!ctx) return fail(E2F_EINVAL, "ctx is NULL");
+  if (e2f_status rs = check_a3(n, rows, channels, heads, n_edges); rs != E2F_OK) return rs;
+  if (!T || !S || !row_ptr) return fail(E2F_EINVAL, "T, S and row_ptr are required");
+  if (n_edges > 0 && !col_idx) return fail(E2F_EINVAL, "col_idx is NULL with n_edges > 0");
+  if (ctx->device < 0) return fail(E2F_EDEVICE, "context has no device");
+  hipStream_t s = (hipStream_t)stream;
+  DeviceGuard g(ctx->device);
+  if (n == 0) return E2F_OK;
+  if (n_edges == 0) {  // every receiver is isolated
+    E2F_HIP(launch_fill(S, (int64_t)n * rows * channels, 0.0f, s));
+    return E2F_OK;
+  }
+  const A3Layout f = a3_layout(n, n_edges, heads);
+  if (!workspace) return fail(E2F_EINVAL, "workspace is NULL");
+  if ((uintptr_t)workspace % 256) return fail(E2F_EINVAL, "workspace must be 256-byte aligned");
+  if (workspace_bytes < f.total)
+    return fail(E2F_ECAPACITY, "workspace of %zu bytes is below the required %zu", workspace_bytes, f.total);
+  char* ws = (char*)workspace;
+  int32_t* order = (int32_t*)(ws + f.order);
+  int* bad = ctx->stats + 24;
+  int* maxc = ctx->stats + 25;
+  // the graph checks and the largest block, read back once
+  E2F_TIMED("a3_plan", launch_validate_graph(row_ptr, col_idx, n, n_edges, bad, s));
+  E2F_TIMED("a3_plan", launch_a3_checks(row_ptr, col_idx, n, n_edges, bad, maxc, s));
+  if (order_in) E2F_TIMED("a3_plan", launch_a3_order_check(order_in, n, order, bad, s));  // order's space as scratch
+  E2F_HIP(hipMemcpyAsync(ctx->pinned, bad, 2 * sizeof(int), hipMemcpyDeviceToHost, s));
+  E2F_HIP(hipStreamSynchronize(s));
+  int st[2];
+  std::memcpy(st, ctx->pinned, sizeof(st));
+  if (st[0]) return fail(E2F_EINVAL, "malformed graph (bits %d: 1 row_ptr[0], 2 decreasing row_ptr, 4 row_ptr[n], "
+                         "8 sender out of range, 16 senders of a row not strictly ascending, 32 order not a "
+                         "permutation)", st[0]);
+  const bool blocks = st[1] <= a3_union_max();
+  float* alpha_hm = alpha ? (float*)(ws + f.alpha_hm) : nullptr;
+  if (order_in) E2F_HIP(hipMemcpyAsync(order, order_in, sizeof(int32_t) * (size_t)n, hipMemcpyDeviceToDevice, s));
+  else E2F_TIMED("a3_plan", launch_iota(n, order, s));
+  if (alpha && blocks) E2F_TIMED("a3_plan", launch_alpha_head_major(alpha, n_edges, heads, alpha_hm, s));
+  int32_t* blk_count = (int32_t*)(ws + f.blk_count);
+  int32_t* blk_off = (int32_t*)(ws + f.blk_off);
+  int32_t* ucount = (int32_t*)(ws + f.ucount);
+  int32_t* uni = (int32_t*)(ws + f.uni);
+  int32_t* edge_slot = (int32_t*)(ws + f.edge_slot);
+  if (blocks)
+    E2F_TIMED("a3_plan", launch_block_union(row_ptr, col_idx, order, n, blk_count, blk_off, uni, ucount, edge_slot,
+                                            ws + f.tmp, f.tmp_b, s));
+  E2F_TIMED("a3_aggregate", launch_aggregate(T, 0, row_ptr, col_idx, alpha, alpha_hm, n_edges, n, order, uni, blk_off,
+                                             ucount, edge_slot, blocks, n, rows, channels, heads, S, s));
+  return E2F_OK;
+}
+
 e2f_status e2f_edge_tp_conv_forward(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos,
                                     const int32_t* graph_id, const float* feat, int32_t n, const int64_t* row_ptr,
                                     const int32_t* col_idx, int64_t n_edges, const float* alpha, float* out,

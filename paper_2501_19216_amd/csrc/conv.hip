@@ -487,7 +487,7 @@ __global__ __launch_bounds__(64 * WV) void k_aggregate_mfma(const float* __restr
   for (int v = 0; v < 4; ++v) {
     const int r = b * 16 + 4 * k + v;
     if (r >= n) continue;
-    float4* srow = (float4*)S + (int64_t)r * W4;  // S rows follow the receiver order
+    float4* srow = (float4*)S + (int64_t)order[r] * W4;  // S rows by receiver
 #pragma unroll
     for (int q = 0; q < NQ; ++q)
       if (cvalid[q]) srow[c4[q]] = make_float4(acc[4 * q][v], acc[4 * q + 1][v], acc[4 * q + 2][v], acc[4 * q + 3][v]);
@@ -528,7 +528,7 @@ __global__ __launch_bounds__(64 * kAggRecv) void k_aggregate_rows(const float4* 
     acc.z += a * v.z;
     acc.w += a * v.w;
   }
-  S[(size_t)r * W4 + q] = acc;  // S rows follow the receiver order
+  S[(size_t)i * W4 + q] = acc;  // S rows by receiver
 }
 
 // ------------------------------------------------------------ aggregation of the node products
@@ -1907,6 +1907,55 @@ hipError_t launch_node_tp(const DevTables& t, const double* R, const int32_t* no
   return hipGetLastError();
 }
 
+namespace {
+// Checks of the standalone aggregation's plan, one thread per receiver (in
+// index order): bit 16 of *bad when a row's senders are not strictly
+// ascending; *maxc = the largest edge count of a block of G consecutive
+// receivers.  Row bounds are clamped to [0, n_edges].
+__global__ void k_a3_checks(const int64_t* __restrict__ row_ptr, const int32_t* __restrict__ col, int n,
+                            int64_t n_edges, int G, int* __restrict__ bad, int* __restrict__ maxc) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  auto clampe = [&](int64_t v) { return v < 0 ? (int64_t)0 : (v > n_edges ? n_edges : v); };
+  const int64_t e0 = clampe(row_ptr[i]), e1 = max(e0, clampe(row_ptr[i + 1]));
+  bool asc = true;
+  for (int64_t e = e0 + 1; e < e1; ++e) asc = asc && col[e] > col[e - 1];
+  if (!asc) atomicOr(bad, 16);
+  if (i % G == 0) {
+    const int last = min(n, i + G);
+    const int64_t b0 = clampe(row_ptr[i]), b1 = max(b0, clampe(row_ptr[last]));
+    atomicMax(maxc, (int)min(b1 - b0, (int64_t)0x7fffffff));
+  }
+}
+// order: bit 32 of *bad unless every entry is in [0, n) and taken once
+// (cnt: n ints, zero on entry)
+__global__ void k_a3_order(const int32_t* __restrict__ order, int n, int* __restrict__ cnt, int* __restrict__ bad) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= n) return;
+  const int i = order[r];
+  if ((unsigned)i >= (unsigned)n) atomicOr(bad, 32);
+  else if (atomicAdd(cnt + i, 1) != 0) atomicOr(bad, 32);
+}
+}  // namespace
+
+hipError_t launch_a3_order_check(const int32_t* order, int n, int* cnt, int* bad, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipError_t e = launch_fill((float*)cnt, n, 0.0f, s);
+  if (e != hipSuccess) return e;
+  k_a3_order<<<(n + 255) / 256, 256, 0, s>>>(order, n, cnt, bad);
+  return hipGetLastError();
+}
+
+hipError_t launch_a3_checks(const int64_t* row_ptr, const int32_t* col, int n, int64_t n_edges, int* bad,
+                            int* maxc, hipStream_t s) {
+  hipError_t e = launch_fill((float*)maxc, 1, 0.0f, s);
+  if (e != hipSuccess || n == 0) return e;
+  k_a3_checks<<<(n + 255) / 256, 256, 0, s>>>(row_ptr, col, n, n_edges, 16, bad, maxc);
+  return hipGetLastError();
+}
+
+int a3_union_max() { return kUnionMax; }
+
 size_t blocks_tmp_bytes(int nblk) {
   size_t b = 0;
   hipcub::DeviceScan::ExclusiveSum(nullptr, b, (const int32_t*)nullptr, (int32_t*)nullptr, nblk + 1);
@@ -1919,9 +1968,10 @@ hipError_t launch_block_union(const int64_t* row_ptr, const int32_t* col_pair, c
   if (n == 0) return hipSuccess;
   const int G = 16;
   const int nblk = (n + G - 1) / G;
-  hipError_t e = hipMemsetAsync(blk_count + nblk, 0, sizeof(int32_t), s);
+  // the scan's extra element, cleared by a fill kernel (0.0f has the bits of int 0)
+  hipError_t e = launch_fill((float*)(blk_count + nblk), 1, 0.0f, s);
   if (e != hipSuccess) return e;
-  if ((e = hipMemsetAsync(ucount + nblk, 0, sizeof(int32_t), s)) != hipSuccess) return e;
+  if ((e = launch_fill((float*)(ucount + nblk), 1, 0.0f, s)) != hipSuccess) return e;
   k_block_edges<<<(nblk + 255) / 256, 256, 0, s>>>(row_ptr, order, n, G, nblk, blk_count);
   size_t b = tmp_bytes;
   if ((e = hipcub::DeviceScan::ExclusiveSum(tmp, b, blk_count, blk_off, nblk + 1, s)) != hipSuccess) return e;

@@ -107,6 +107,15 @@ hipError_t launch_block_union(const int64_t* row_ptr, const int32_t* col_pair, c
 // head-major weights alpha_hm [H][n_edges] and edge_slot); else per-receiver
 // rows from L2 with alpha [n_edges][H].  Null weights mean all ones.  n_edges
 // and n_total are the whole graph's edges and atoms (mean degree).
+// Standalone aggregation plan checks (receivers in index order): bit 16 of
+// *bad for a row whose senders are not strictly ascending; *maxc = the
+// largest edge count of a block of 16 consecutive receivers (the block path
+// of launch_aggregate takes blocks of at most a3_union_max() edges)
+hipError_t launch_a3_checks(const int64_t* row_ptr, const int32_t* col, int n, int64_t n_edges, int* bad,
+                            int* maxc, hipStream_t s);
+int a3_union_max();
+// bit 32 of *bad unless order is a permutation of 0..n-1 (cnt: n ints of scratch)
+hipError_t launch_a3_order_check(const int32_t* order, int n, int* cnt, int* bad, hipStream_t s);
 hipError_t launch_aggregate(const float* T, int pair_base, const int64_t* row_ptr, const int32_t* col_pair,
                             const float* alpha, const float* alpha_hm, int64_t n_edges, int n_total,
                             const int32_t* order, const int32_t* uni, const int32_t* blk_off,

@@ -748,3 +748,36 @@ def test_global_moment_equals_definition_larger():
     origin = np.array([0.3, -0.2, 0.1])
     y2 = o.conv_global(L, pos, feat, w, origin)
     assert np.max(np.abs(y1 - y2)) <= 1e-11 * np.max(np.abs(y1))
+
+
+def test_aggregate_equals_dense_einsum_and_hand_example():
+    # Alg. 1's aggregation written as the paper's dense einsum "ijh,jhds->ihds"
+    # (alpha scattered into an N x N x H tensor, zero off the graph) against
+    # the oracle's edge loop; plus a three-atom example summed by hand
+    rng = np.random.default_rng(21)
+    n, H, K, dh = 23, 3, 5, 4
+    pos = rng.uniform(0, 6, size=(n, 3)).astype(np.float32)
+    rp, ci = o.neighbor_list(pos, 3.0)
+    T = rng.standard_normal((n, H, K, dh)).astype(np.float32)
+    alpha = rng.uniform(0, 1, size=(len(ci), H)).astype(np.float32)
+    A = np.zeros((n, n, H))
+    for i in range(n):
+        for e in range(rp[i], rp[i + 1]):
+            A[i, ci[e]] = alpha[e]
+    dense = np.einsum("ijh,jhkd->ihkd", A, T.astype(np.float64))
+    got = o.aggregate(T, rp, ci, alpha)
+    assert np.max(np.abs(got - dense)) <= 1e-12 * np.max(np.abs(dense))
+    rows = np.array([n - 1, 0, 7], dtype=np.int32)
+    assert np.array_equal(o.aggregate(T, rp, ci, alpha, rows=rows), got[rows])
+    ones = o.aggregate(T, rp, ci, None)
+    assert np.allclose(ones, np.einsum("ijh,jhkd->ihkd", (A != 0).astype(np.float64), T.astype(np.float64)),
+                       rtol=0, atol=1e-12)
+    # 0 <- {1, 2}, 1 <- {0}, 2 isolated; one head of two values
+    T3 = np.array([[[1.0, 2.0]], [[3.0, 5.0]], [[7.0, 11.0]]], dtype=np.float32)[:, :, None, :]
+    rp3 = np.array([0, 2, 3, 3], dtype=np.int64)
+    ci3 = np.array([1, 2, 0], dtype=np.int32)
+    a3 = np.array([[0.5], [2.0], [4.0]], dtype=np.float32)
+    S3 = o.aggregate(T3, rp3, ci3, a3)
+    assert np.array_equal(S3[0, 0, 0], [0.5 * 3 + 2 * 7, 0.5 * 5 + 2 * 11])
+    assert np.array_equal(S3[1, 0, 0], [4.0 * 1, 4.0 * 2])
+    assert np.array_equal(S3[2], np.zeros((1, 1, 2)))
