@@ -596,10 +596,10 @@ FwdLayout fwd_layout(const e2f_conv_params* p, int n, int64_t E, bool have_alpha
   f.order = take(sizeof(int32_t) * (size_t)n);
   f.sort_b = plan_sort_tmp_bytes(std::max(n, 1));
   f.sort_tmp = take(f.sort_b);
-  f.Re = take(sizeof(float) * (size_t)E * nk);
+  f.Re = take(sizeof(float) * (size_t)(E + kEdgePad) * nk);
   f.Rr = take(sizeof(double) * (size_t)n * nk);
   const size_t na = ynorm ? (size_t)(L + 1) : (have_alpha ? 1 : 0);
-  f.alpha_hm = take(sizeof(float) * (size_t)E * H * na);
+  f.alpha_hm = take(sizeof(float) * ((size_t)E * H * na + kEdgePad));
   f.erows = take(sizeof(int32_t) * (size_t)E);
   f.y = take(p->mix_w ? sizeof(float) * (size_t)n * nk * C : 0);
   // the fused aggregation's copy of the features (groups of four components)

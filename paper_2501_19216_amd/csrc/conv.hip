@@ -931,14 +931,29 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
   auto stage = [&](int64_t c0, int ne, int b) {
     float* Al = Alb + b * SB;
     int* jo = job + b * SR;
+    if (ne == 0) {  // an isolated receiver: zero weights, sender offsets 0
+#pragma unroll
+      for (int u = 0; u < EC / 64; ++u) {
+        sa[lane + 64 * u] = 0.0f;
+        jo[lane + 64 * u] = 0;
+      }
+      return;
+    }
+    // unconditional loads (the compiler can then keep every batch in flight):
+    // the weights and harmonics of edges c0 .. c0 + EC - 1 lie inside their
+    // arrays, which carry kEdgePad rows of padding past the last edge (a
+    // missing weight array reads the harmonics instead); the caller's senders
+    // are read at a clamped index.  Rows past ne are masked by selects.
+    const float* ap = ah ? ah : Re;
     float av[EC / 64];
     int jv[EC / 64];
 #pragma unroll
     for (int u = 0; u < EC / 64; ++u) {
       const int nb = lane + 64 * u;
-      av[u] = nb < ne ? (ah ? ah[c0 + nb] : 1.0f) : 0.0f;
-      const int j = nb < ne ? col[c0 + nb] : 0;
-      jv[u] = (unsigned)j < (unsigned)n_nodes ? j : 0;
+      const float a = ap[c0 + nb];
+      const int j = col[c0 + min(nb, ne - 1)];
+      av[u] = nb < ne ? (ah ? a : 1.0f) : 0.0f;
+      jv[u] = nb < ne && (unsigned)j < (unsigned)n_nodes ? j : 0;
     }
 #pragma unroll
     for (int u = 0; u < EC / 64; ++u) {
@@ -946,20 +961,20 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
       jo[lane + 64 * u] = (int)((unsigned)jv[u] * fstride);
     }
     __builtin_amdgcn_wave_barrier();
-    if (ne == 0) return;
     const int nrow = 4 * ((ne + 3) / 4);
     const int be = lane % MP, rs = lane / MP;
     const bool bok = be < NK;
     // the lane's rows rs + RPI (BT bt + k): one base per batch, immediate
-    // offsets within it; rows past ne are not loaded
+    // offsets within it
     const float* src = Re + (size_t)(c0 + rs) * NK + (bok ? be : 0);
     constexpr int BT = 16, NBT = ITER / BT;
     static_assert(ITER % BT == 0, "batches must cover a chunk");
+    static_assert(kEdgePad >= EC, "the per-edge arrays must be padded by a chunk");
     float cur[BT], nxt[BT];
     auto load = [&](int bt, float* d) {
       const float* sb = src + (size_t)bt * BT * RPI * NK;
 #pragma unroll
-      for (int k = 0; k < BT; ++k) d[k] = (bt * BT + k) * RPI + rs < ne ? sb[k * RPI * NK] : 0.0f;
+      for (int k = 0; k < BT; ++k) d[k] = sb[k * RPI * NK];
     };
     load(0, cur);
 #pragma unroll 1
@@ -969,7 +984,8 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
 #pragma unroll
       for (int k = 0; k < BT; ++k) {
         const int nb = (bt * BT + k) * RPI + rs;
-        if (nb < nrow) Al[nb * AS + be] = bok ? cur[k] * sa[nb] : 0.0f;
+        const float w = cur[k] * sa[nb];
+        if (nb < nrow) Al[nb * AS + be] = bok && nb < ne ? w : 0.0f;
       }
       if (more_rows) {
 #pragma unroll

@@ -12,6 +12,10 @@ namespace e2f {
 // stats[0..2] = min grid coordinate, stats[3..5] = max, stats[6] = max
 // graph id, stats[7] = error bits (1: bad position, 2: negative graph id).
 constexpr int kStatsInts = 8;
+// rows of padding after the forward's per-edge arrays (harmonics of the
+// edges, head-major attention weights): the fused aggregation's staging
+// loads whole chunks of edges without a bound check
+constexpr int kEdgePad = 128;
 hipError_t launch_bbox(const float* pos, const int32_t* graph_id, int n, int* stats, hipStream_t s);
 
 // ---- device-side plan of the factorised forward (plan.hip)
