@@ -292,8 +292,14 @@ def fig2_point(panel, k, L, n, steps, warmup, C=128, H=8):
         torch.cuda.synchronize()
         return (time.perf_counter() - t0) * 1e3 / steps
 
+    ms_split = ms_fused = None
     if k > 0:
         ms6 = timed(lambda: e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, rp, ci, alpha, L, H, reach, out=out))
+        ms_split = timed(lambda: e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, rp, ci, alpha, L, H, reach, out=out,
+                                                               form="split"))
+        if L <= 4:
+            ms_fused = timed(lambda: e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, rp, ci, alpha, L, H, reach,
+                                                                   out=out, form="fused"))
     else:
         dense = torch.zeros(n, n, H, device=dev)
         dense[torch.from_numpy(np.repeat(np.arange(n), n - 1)).to(dev), ci.long()] = alpha
@@ -302,7 +308,7 @@ def fig2_point(panel, k, L, n, steps, warmup, C=128, H=8):
     mse = timed(lambda: e2f.e2f_edge_tp_conv_forward(ctx, pos, feat, rp, ci, alpha, L, H, reach, out=out))
     ctx.close()
     return {"panel": panel, "graph": "knn" if k > 0 else "dense", "k": k, "lmax": L, "atoms": n, "edges": int(len(cih)), "channels": C,
-            "heads": H, "reach": reach, "knn_ms": ms_knn, "fwd_ms": ms6,
+            "heads": H, "reach": reach, "knn_ms": ms_knn, "fwd_ms": ms6, "split_ms": ms_split, "fused_ms": ms_fused,
             "edge_tp_ms": mse, "speedup_vs_edge_tp": mse / ms6, "atoms_per_s": n / ms6 * 1e3}
 
 
@@ -437,7 +443,7 @@ def main():
 
     def fwd_split():
         e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col, alpha, L, H, wl.cutoff, mix_w=mix_w,
-                                      graph_id=gid, out=out_s, split_recouple=True)
+                                      graph_id=gid, out=out_s, form="split")
 
     fwd_split()
     ms_fwd_split = timed(fwd_split, args.steps)

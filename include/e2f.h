@@ -63,6 +63,7 @@ typedef enum {
 } e2f_status;
 
 typedef enum { E2F_F32 = 0, E2F_BF16 = 1 } e2f_dtype;
+typedef enum { E2F_FORM_AUTO = 0, E2F_FORM_SPLIT = 1, E2F_FORM_FUSED = 2 } e2f_form;
 
 typedef struct e2f_ctx e2f_ctx;
 
@@ -187,12 +188,17 @@ typedef struct {
                             shortest nonzero edge (found on the device), keeping that ratio
                             below 5.  Forward entry points only (the backward returns
                             E2F_EUNSUPPORTED) */
-  int32_t split_recouple; /* 0: up to L = 4, with heads whose width is a multiple of 16 and
-                            y_norm 0, the aggregation applies the i-side recouple itself (the
+  int32_t form;          /* which form of the aggregation and recouple the forward runs (e2f_form):
+                            E2F_FORM_FUSED: up to L = 4, with heads whose width is a multiple of 16
+                            and y_norm 0, the aggregation applies the i-side recouple itself (the
                             j-side coupling and the recouple of Thm. 3.3 composed into one
                             (L+1)^2 x (L+1)^4 matrix per receiver), so S is never stored;
-                            elsewhere S is written and recoupled by a second kernel.
-                            1: always the second form (the same result up to rounding order) */
+                            elsewhere the split form.  E2F_FORM_SPLIT: S is written and recoupled
+                            by a second kernel.  E2F_FORM_AUTO (0): fused at L = 4 where the split
+                            form's S (n dimT C floats) would exceed 256 MiB (beyond the on-die
+                            cache its round trip through HBM outweighs the fused form's extra
+                            matrix-core work per receiver), else split.  All forms give the same
+                            result up to rounding order */
 } e2f_conv_params;
 
 /* Workspace of e2f_wigner6j_conv_forward for n atoms and n_edges edges:

@@ -19,6 +19,8 @@ LIB_PATH = os.path.join(_HERE, "libe2f.so")
 
 E2F_OK, E2F_EINVAL, E2F_ECAPACITY, E2F_ENOMEM, E2F_EDEVICE, E2F_EUNSUPPORTED = range(6)
 E2F_F32, E2F_BF16 = 0, 1
+E2F_FORM_AUTO, E2F_FORM_SPLIT, E2F_FORM_FUSED = 0, 1, 2
+_FORMS = {"auto": E2F_FORM_AUTO, "split": E2F_FORM_SPLIT, "fused": E2F_FORM_FUSED}
 _STATUS = {0: "E2F_OK", 1: "E2F_EINVAL", 2: "E2F_ECAPACITY", 3: "E2F_ENOMEM", 4: "E2F_EDEVICE", 5: "E2F_EUNSUPPORTED"}
 
 # every function declared in include/e2f.h
@@ -40,7 +42,7 @@ class ConvParams(ctypes.Structure):
     _fields_ = [("lmax", ctypes.c_int), ("channels", ctypes.c_int32), ("heads", ctypes.c_int32),
                 ("cutoff", ctypes.c_float), ("path_w", ctypes.c_void_p), ("mix_w", ctypes.c_void_p),
                 ("mix_dtype", ctypes.c_int), ("tile_side", ctypes.c_float), ("y_norm", ctypes.c_int32),
-                ("split_recouple", ctypes.c_int32)]
+                ("form", ctypes.c_int32)]
 
 
 def _load():
@@ -309,7 +311,7 @@ def e2f_aggregate(ctx: Context, T: torch.Tensor, row_ptr: torch.Tensor, col_idx:
     return out
 
 
-def _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm=False, split_recouple=False):
+def _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm=False, form="auto"):
     import numpy as np
     keep = None
     pw = None
@@ -327,7 +329,7 @@ def _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm=Fals
         if not mix_w.is_cuda or not mix_w.is_contiguous():
             raise ValueError("mix_w must be a contiguous device tensor")
     prm = ConvParams(lmax, channels, heads, cutoff, pw, None if mix_w is None else mix_w.data_ptr(), mix_dtype,
-                     float(tile_side), int(bool(y_norm)), int(bool(split_recouple)))
+                     float(tile_side), int(bool(y_norm)), _FORMS[form] if isinstance(form, str) else int(form))
     return prm, keep
 
 
@@ -345,10 +347,10 @@ def _conv_args(pos, feat, row_ptr, col_idx, alpha, graph_id, out):
 
 
 def e2f_wigner6j_workspace_size(ctx, n, n_edges, lmax, channels, heads, cutoff, path_w=None, mix_w=None,
-                                tile_side=0.0, y_norm=False, minimum=False, split_recouple=False) -> int:
+                                tile_side=0.0, y_norm=False, minimum=False, form="auto") -> int:
     """Workspace bytes of the forward (the one-pass size, or with minimum=True
     the smallest size it accepts)."""
-    prm, keep = _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm, split_recouple)
+    prm, keep = _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm, form)
     b = ctypes.c_size_t(0)
     fn = lib.e2f_wigner6j_workspace_min if minimum else lib.e2f_wigner6j_workspace_size
     _check(fn(ctx.handle, ctypes.byref(prm), n, n_edges, ctypes.byref(b)),
@@ -358,26 +360,26 @@ def e2f_wigner6j_workspace_size(ctx, n, n_edges, lmax, channels, heads, cutoff, 
 
 
 def e2f_wigner6j_prepare(ctx, lmax, channels, heads, cutoff, path_w=None, mix_w=None, tile_side=0.0,
-                         y_norm=False, split_recouple=False) -> None:
+                         y_norm=False, form="auto") -> None:
     """Upload the coefficient set and coupling schedule these parameters use."""
-    prm, keep = _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm, split_recouple)
+    prm, keep = _params(lmax, channels, heads, cutoff, path_w, mix_w, tile_side, y_norm, form)
     _check(lib.e2f_wigner6j_prepare(ctx.handle, ctypes.byref(prm)), "e2f_wigner6j_prepare")
     del keep
 
 
 def e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None, mix_w=None,
                               graph_id=None, tile_side=0.0, out=None, y_norm=False, workspace=None,
-                              split_recouple=False):
+                              form="auto"):
     """Wigner-6j convolution forward; returns out [N,(L+1)^2,C] float32.
     y_norm: attention weights alpha / |r_i - r_j|^f per filter degree f.
     workspace: a uint8 device tensor (any size from the minimum up); None
     uses the context's own, grown to the one-pass size.
-    split_recouple: write S and recouple it in a second kernel even where the
-    aggregation could apply the recouple itself."""
+    form: "auto", "split" (S written, then recoupled by a second kernel) or
+    "fused" (the aggregation applies the recouple itself where it can)."""
     out = _conv_args(pos, feat, row_ptr, col_idx, alpha, graph_id, out)
     n, nk, C = feat.shape
     E = col_idx.numel()
-    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm, split_recouple)
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm, form)
     if workspace is None:
         b = ctypes.c_size_t(0)
         _check(lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm), n, E, ctypes.byref(b)),
@@ -395,13 +397,13 @@ def e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, hea
 
 def e2f_wigner6j_conv_forward_noalloc(ctx, pos, feat, row_ptr, col_idx, alpha, lmax, heads, cutoff, path_w=None,
                                       mix_w=None, graph_id=None, tile_side=0.0, out=None, y_norm=False,
-                                      split_recouple=False):
+                                      form="auto"):
     """The forward in the library's per-GPU scratch memory (no allocation;
     the parameters must have been prepared).  out must be given by callers
     that cannot allocate: with out=None the binding allocates it."""
     out = _conv_args(pos, feat, row_ptr, col_idx, alpha, graph_id, out)
     n, nk, C = feat.shape
-    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm, split_recouple)
+    prm, keep = _params(lmax, C, heads, cutoff, path_w, mix_w, tile_side, y_norm, form)
     st = lib.e2f_wigner6j_conv_forward_noalloc(ctx.handle, ctypes.byref(prm), _ptr(pos), _ptr(graph_id), _ptr(feat),
                                                n, _ptr(row_ptr), _ptr(col_idx), col_idx.numel(), _ptr(alpha),
                                                _ptr(out), _stream(feat.device))

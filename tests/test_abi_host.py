@@ -89,8 +89,10 @@ def test_conv_argument_checks(e2f, fn):
     assert call(_params(e2f, mix_dtype=7)) == EINVAL
     assert call(_params(e2f, y_norm=2)) == EINVAL
     assert call(_params(e2f, y_norm=1)) == EDEV
-    assert call(_params(e2f, split_recouple=2)) == EINVAL
-    assert call(_params(e2f, split_recouple=1)) == EDEV
+    assert call(_params(e2f, form=3)) == EINVAL
+    assert call(_params(e2f, form=-1)) == EINVAL
+    assert call(_params(e2f, form=1)) == EDEV
+    assert call(_params(e2f, form=2)) == EDEV
     assert call(_params(e2f), n=-1) == EINVAL
     assert call(_params(e2f), E=-1) == EINVAL
     assert call(_params(e2f), E=2 ** 31) == EUNS
@@ -185,19 +187,23 @@ def test_workspace_size_query(e2f):
     lib = e2f.lib
     b, m = ctypes.c_size_t(0), ctypes.c_size_t(0)
     assert _fused_row_bytes(4) == 4 * 17536 and _fused_row_bytes(3) == 4 * 4096
-    for L, C, H, n, E, split in ((2, 16, 4, 32, 738, 0), (4, 128, 8, 20000, 1597678, 0),
-                                 (4, 128, 8, 20000, 1597678, 1), (3, 64, 4, 7680, 49348, 0),
-                                 (3, 64, 8, 7680, 49348, 0), (6, 64, 8, 200000, 39828996, 0)):
-        prm = _params(e2f, lmax=L, channels=C, heads=H, split_recouple=split)
+    # form: 0 automatic (fused at L = 4 once S exceeds 256 MiB), 1 split, 2 fused where supported
+    for L, C, H, n, E, form in ((2, 16, 4, 32, 738, 0), (4, 128, 8, 20000, 1597678, 0),
+                                (4, 128, 8, 20000, 1597678, 1), (4, 128, 8, 1000, 32000, 0),
+                                (4, 128, 8, 1000, 32000, 2), (3, 64, 4, 7680, 49348, 0),
+                                (3, 64, 4, 7680, 49348, 2), (3, 64, 8, 7680, 49348, 2),
+                                (6, 64, 8, 200000, 39828996, 0)):
+        prm = _params(e2f, lmax=L, channels=C, heads=H, form=form)
         assert lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm), n, E, ctypes.byref(b)) == e2f.E2F_OK
         assert lib.e2f_wigner6j_workspace_min(ctx.handle, ctypes.byref(prm), n, E, ctypes.byref(m)) == e2f.E2F_OK
         dimT, nk = e2f.e2f_node_tp_dim(L), (L + 1) ** 2
-        fused = L <= 4 and (C // H) % 16 == 0 and not split
+        s_big = 4 * n * e2f.e2f_node_tp_dim(L) * C > 256 * 2 ** 20
+        fused = L <= 4 and (C // H) % 16 == 0 and (form == 2 or (form == 0 and L == 4 and s_big))
         s_row = _fused_row_bytes(L) if fused else -(-4 * dimT * C // 256) * 256
         assert b.value - m.value == max(0, n - 256) * s_row
         # at least the per-edge harmonics, the receivers' harmonics, the head-major weights and S
         assert b.value >= 4 * E * nk + 8 * n * nk + 4 * E * H + n * s_row
-        prm_mix = _params(e2f, lmax=L, channels=C, heads=H, mix_w=FAKE, split_recouple=split)
+        prm_mix = _params(e2f, lmax=L, channels=C, heads=H, mix_w=FAKE, form=form)
         assert lib.e2f_wigner6j_workspace_size(ctx.handle, ctypes.byref(prm_mix), n, E, ctypes.byref(m)) == e2f.E2F_OK
         assert m.value - b.value >= 4 * n * nk * C  # the unmixed output
     prm = _params(e2f, heads=3)

@@ -1,7 +1,8 @@
 """GPU parity of the forward whose aggregation applies the i-side recouple
 itself (L <= 4, heads of a multiple of 16 channels): against the fp64 oracle's
 definition of the layer and against the two-kernel form (S written, then
-recoupled), which is selected with split_recouple.
+recoupled), selected with the form argument ("fused", "split"; the default
+"auto" picks the fused form at L = 4 once S would exceed 256 MiB).
 
 Calls go through the C ABI.  Bar: float32 max relative error <= 1e-4 per
 output irrep block.
@@ -62,8 +63,8 @@ def test_fused_forward(e2f, ctx, L, C, H, n, box, cut, with_alpha):
     print("fused L %d C %d H %d n %d edges %d max degree %d" % (L, C, H, n, len(ci), int(np.diff(rp).max())),
           flush=True)
     args = (gpu(pos), gpu(feat), gpu(rp), gpu(ci), gpu(alpha) if with_alpha else None, L, H, cut)
-    fused = e2f.e2f_wigner6j_conv_forward(ctx, *args, path_w=w).cpu().numpy()
-    split = e2f.e2f_wigner6j_conv_forward(ctx, *args, path_w=w, split_recouple=True).cpu().numpy()
+    fused = e2f.e2f_wigner6j_conv_forward(ctx, *args, path_w=w, form="fused").cpu().numpy()
+    split = e2f.e2f_wigner6j_conv_forward(ctx, *args, path_w=w, form="split").cpu().numpy()
     ef, es = o.max_rel_err(fused[r], ref, L), o.max_rel_err(split[r], ref, L)
     print("  fused err %.3e  two-kernel err %.3e" % (ef, es))
     assert ef <= TOL_F32 and es <= TOL_F32
@@ -82,15 +83,16 @@ def test_fused_protein_rows_and_workspace_sizes(e2f, ctx):
     r = sample_rows(n, 256, seed=11)
     ref = o.conv_edge(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, rows=r)
     args = (gpu(inp.pos), gpu(inp.feat), gpu(rp), gpu(ci), gpu(alpha), wl.lmax, wl.heads, wl.cutoff)
-    fused = e2f.e2f_wigner6j_conv_forward(ctx, *args).cpu().numpy()
+    fused = e2f.e2f_wigner6j_conv_forward(ctx, *args).cpu().numpy()  # the automatic choice: fused (S 4.65 GB)
     assert e2f.e2f_last_slices(ctx) == 1
-    split = e2f.e2f_wigner6j_conv_forward(ctx, *args, split_recouple=True).cpu().numpy()
+    assert np.array_equal(fused, e2f.e2f_wigner6j_conv_forward(ctx, *args, form="fused").cpu().numpy())
+    split = e2f.e2f_wigner6j_conv_forward(ctx, *args, form="split").cpu().numpy()
     ef, es = o.max_rel_err(fused[r], ref, wl.lmax), o.max_rel_err(split[r], ref, wl.lmax)
     print("protein20k: fused err %.3e  two-kernel err %.3e on %d rows" % (ef, es, len(r)))
     assert ef <= TOL_F32 and es <= TOL_F32
     wmin = e2f.e2f_wigner6j_workspace_size(ctx, n, E, wl.lmax, wl.channels, wl.heads, wl.cutoff, minimum=True)
     wsplit = e2f.e2f_wigner6j_workspace_size(ctx, n, E, wl.lmax, wl.channels, wl.heads, wl.cutoff,
-                                             split_recouple=True)
+                                             form="split")
     wfull = e2f.e2f_wigner6j_workspace_size(ctx, n, E, wl.lmax, wl.channels, wl.heads, wl.cutoff)
     assert wmin < wfull < wsplit  # F_i (70 KB a receiver) instead of S_i (232 KB)
     ws = torch.empty(wmin, dtype=torch.uint8, device=DEV)
