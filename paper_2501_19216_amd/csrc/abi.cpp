@@ -610,8 +610,9 @@ FwdLayout fwd_layout(const e2f_conv_params* p, int n, int64_t E, bool have_alpha
   f.alpha_hm = take(sizeof(float) * ((size_t)E * H * na + kEdgePad));
   f.erows = take(sizeof(int32_t) * (size_t)E);
   f.y = take(p->mix_w ? sizeof(float) * (size_t)n * nk * C : 0);
-  // the fused aggregation's copy of the features (groups of four components)
-  f.featq = take(fused_split(p, n) > 0 ? sizeof(float) * (size_t)n * C * 4 * fuse_groups(L) : 0);
+  // the fused aggregation's copy of the features (groups of four components,
+  // each value split into three bfloat16 parts: 6 bytes)
+  f.featq = take(fused_split(p, n) > 0 ? sizeof(float) * (size_t)n * C * 6 * fuse_groups(L) : 0);
   f.S = off;
   f.fixed = off;
   // per receiver of a slice: F_i (fused) or S_i

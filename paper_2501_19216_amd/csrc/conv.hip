@@ -99,6 +99,8 @@ __global__ void k_sh(DevTables t, const float* __restrict__ pos, const int32_t* 
 // K operand h^(a), 2a+1 values padded to a multiple of 4) by 16 channels.
 // T is stored head-major, T[item][c / dh][r][c % dh] (dh = C: plain [r][c]).
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 // Build one chunk of a per-node matrix into LDS from its schedule (see
 // Schedule): coalesced, independent loads; each thread sums its slots.
@@ -827,13 +829,33 @@ __global__ __launch_bounds__(256) void k_fuse_build(const int* __restrict__ fptr
   }
 }
 
-// The features in the order of the fused aggregation's B operand: per node
-// and head of 16 channels, groups of four components q = 4 g + i (zero past
-// (L+1)^2), each group [t][i] (t the channel in the head), so that lane t of
-// a wave reads the four components of its wave's group as one float4 and a
-// group of 16 lanes reads 256 contiguous bytes.
-__global__ void k_feat_qmajor(const float* __restrict__ feat, int n, int nk, int C, int ng,
-                              float4* __restrict__ out) {
+
+// x = hi + mid + lo exactly, each part a bfloat16 rounded to nearest even
+// (8 + 8 + 8 significant bits hold a float's 24), returned as bit patterns.
+// The products of the split operands that reach 2^-24 relative (hi hi,
+// hi mid, mid hi, hi lo, mid mid, lo hi) are exact in float and summed in
+// float by the matrix cores, so six bf16 products stand in for one float
+// product within float rounding.
+__device__ __forceinline__ void split_bf16x3(float x, unsigned& hi, unsigned& mid, unsigned& lo) {
+  const __bf16 h = (__bf16)x;
+  const float r = x - (float)h;
+  const __bf16 m = (__bf16)r;
+  const __bf16 l = (__bf16)(r - (float)m);
+  hi = __builtin_bit_cast(unsigned short, h);
+  mid = __builtin_bit_cast(unsigned short, m);
+  lo = __builtin_bit_cast(unsigned short, l);
+}
+
+// The features in the order of the fused aggregation's B operand, each value
+// split into three bfloat16 parts: per node and head of 16 channels, groups
+// of four components q = 4 g + i (zero past (L+1)^2), each group [t][i] (t
+// the channel in the head): a uint4 of the four components' hi | mid << 16
+// and, in the second array (same index), a uint2 of their lo parts
+// (components 0, 1 in the first word, low half first).  Lane t of a wave
+// reads its group's four components with one 16-byte and one 8-byte load; a
+// group of 16 lanes reads 256 + 128 contiguous bytes.
+__global__ void k_feat_qmajor3(const float* __restrict__ feat, int n, int nk, int C, int ng,
+                               uint4* __restrict__ hm, uint2* __restrict__ lo) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (node, head, group, t)
   const int H = C / 16;
   if (q >= (int64_t)n * H * ng * 16) return;
@@ -842,10 +864,16 @@ __global__ void k_feat_qmajor(const float* __restrict__ feat, int n, int nk, int
   const int g = (int)(r % ng), h = (int)(r / ng % H);
   const int64_t j = r / ((int64_t)ng * H);
   const float* src = feat + (size_t)j * nk * C + h * 16 + t;
-  float v[4];
+  unsigned a[4], b[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) v[i] = 4 * g + i < nk ? src[(size_t)(4 * g + i) * C] : 0.0f;
-  out[q] = make_float4(v[0], v[1], v[2], v[3]);
+  for (int i = 0; i < 4; ++i) {
+    unsigned x, y, z;
+    split_bf16x3(4 * g + i < nk ? src[(size_t)(4 * g + i) * C] : 0.0f, x, y, z);
+    a[i] = x | y << 16;
+    b[i] = z;
+  }
+  hm[q] = make_uint4(a[0], a[1], a[2], a[3]);
+  lo[q] = make_uint2(b[0] | b[1] << 16, b[2] | b[3] << 16);
 }
 
 // The aggregation with the recouple applied in registers.  Work split as in
@@ -874,12 +902,18 @@ template <int L, int LB>
 __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re, const int64_t* __restrict__ row_ptr,
                                                     const int32_t* __restrict__ col,
                                                     const float* __restrict__ alpha_hm, int64_t n_edges,
-                                                    const float4* __restrict__ featq,
+                                                    const uint4* __restrict__ fhm, const uint2* __restrict__ flo,
                                                     const int32_t* __restrict__ order, const float* __restrict__ F,
                                                     int n, int nrx, int rpw, int C, int H, int hdiv, int n_nodes,
                                                     float* __restrict__ y) {
   constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
-  constexpr int EC = kOuterEdges, AS = MP + 16;
+  constexpr int EC = kOuterEdges;
+  // staging row stride in words: two words per component (a 64-bit read per
+  // lane), odd rows rotated by 16 components where 2 MP is a multiple of 64,
+  // so rows 4 st + k4 of one step alternate between the two halves of the
+  // banks
+  constexpr int AS = 2 * MP;
+  constexpr int ROT = (2 * MP) % 64 == 0 ? 16 : 0;
   constexpr int QB = fuse_qblock(NK), FS = fuse_stride(NK);
   constexpr int NG = (NK + 3) / 4;  // groups of four components: one product wave each
   // rows EC .. SR-1 of a buffer are padding (zero weights, sender offset 0):
@@ -892,8 +926,8 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
   constexpr int RPI = 64 / MP;            // rows the staging wave covers per pass (lane: be = lane % MP)
   constexpr int ITER = EC / RPI;          // passes over a full chunk
   extern __shared__ float sm[];
-  float* Alb = sm;                        // [2][SR][AS] alpha R of the chunk's edges (zero past its rows)
-  int* job = (int*)(sm + 2 * SB);         // [2][SR] the senders' offsets in featq (float4)
+  float* Alb = sm;                        // [2][SR][AS] alpha R of the chunk's edges, split (zero past its rows)
+  int* job = (int*)(sm + 2 * SB);         // [2][SR] the senders' offsets in the re-laid features
   float* sa = sm + 2 * SB + 2 * SR;       // [EC] the staging wave's copy of the chunk's weights
   const int bid = blockIdx.x, xcd = bid % 8, local = bid / 8;
   const int h = local % H, rfirst = xcd * nrx + (local / H) * rpw;
@@ -985,7 +1019,13 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
       for (int k = 0; k < BT; ++k) {
         const int nb = (bt * BT + k) * RPI + rs;
         const float w = cur[k] * sa[nb];
-        if (nb < nrow) Al[nb * AS + be] = bok && nb < ne ? w : 0.0f;
+        const float v = bok && nb < ne ? w : 0.0f;
+        if (nb < nrow) {
+          // A of the split products: words hi | mid << 16 and hi | lo << 16
+          unsigned hi, mid, lo;
+          split_bf16x3(v, hi, mid, lo);
+          ((uint2*)(Al + nb * AS))[(be + (nb & 1) * ROT) % MP] = make_uint2(hi | mid << 16, hi | lo << 16);
+        }
       }
       if (more_rows) {
 #pragma unroll
@@ -1026,35 +1066,50 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
       // pipeline of the products: the operands of steps st+1, st+2 are
       // loaded while the MFMAs of step st run; steps past ns read rows of
       // zeros or stale weights with valid senders and are never multiplied.
-      // NL (the wave's live tiles) is a constant of each copy of the loop,
-      // so a step is one float4 load, two LDS reads and 2 NL MFMAs.
+      // NL (the wave's live tiles) is a constant of each copy of the loop.
+      // The products are split: K of one v_mfma_f32_16x16x32_bf16 is 4
+      // edges (k4) x 8 slots, six of them the cross products of the parts,
+      //   A = {hi|mid, hi|lo, hi|mid, 0}, B = {hi|mid, mid|hi, lo|hi, 0}
+      // (A from the staging words, B from the lane's uint4 / uint2 of the
+      // sender), so a step is two loads, MT 64-bit LDS reads, two ALU
+      // operations per tile and NL MT MFMAs of half the fp32 cost.
       auto products = [&](auto nlc) {
         constexpr int NL = decltype(nlc)::value;
-        float aq[kFuseStages][MT];
-        float4 bq[kFuseStages];
-        auto loadb = [&](int st, float* a, float4& b) {
+        uint2 aq[kFuseStages][MT];
+        uint4 bh[kFuseStages];
+        uint2 bl[kFuseStages];
+        auto loadb = [&](int st, uint2* a, uint4& h4, uint2& l2) {
           const int nb = min(4 * st + k4, SR - 1);  // < SR without the clamp (see SR)
-          b = featq[(unsigned)jo[nb] + foff];
+          const unsigned o = (unsigned)jo[nb] + foff;
+          h4 = fhm[o];
+          l2 = flo[o];
+          const uint2* row = (const uint2*)(Al + nb * AS);
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) a[mt] = Al[nb * AS + mt * 16 + l16];
+          for (int mt = 0; mt < MT; ++mt) a[mt] = row[(mt * 16 + l16 + (nb & 1) * ROT) % MP];
         };
-        auto mma = [&](const float* a, const float4& b) {
-          const float bw[4] = {b.x, b.y, b.z, b.w};
+        auto mma = [&](const uint2* a, const uint4& h4, const uint2& l2) {
+          const unsigned hw[4] = {h4.x, h4.y, h4.z, h4.w};
+          const unsigned lw[4] = {l2.x & 0xffffu, l2.x >> 16, l2.y & 0xffffu, l2.y >> 16};
 #pragma unroll
-          for (int w = 0; w < NL; ++w)
+          for (int w = 0; w < NL; ++w) {
+            const v8bf bv =
+                __builtin_bit_cast(v8bf, (v4u){hw[w], (hw[w] >> 16) | (hw[w] << 16), lw[w] | (hw[w] << 16), 0u});
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-              acc[mt][w] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mt], bw[w], acc[mt][w], 0, 0, 0);
+            for (int mt = 0; mt < MT; ++mt) {
+              const v8bf av = __builtin_bit_cast(v8bf, (v4u){a[mt].x, a[mt].y, a[mt].x, 0u});
+              acc[mt][w] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc[mt][w], 0, 0, 0);
+            }
+          }
         };
 #pragma unroll
-        for (int u = 0; u + 1 < kFuseStages; ++u) loadb(u, aq[u], bq[u]);
+        for (int u = 0; u + 1 < kFuseStages; ++u) loadb(u, aq[u], bh[u], bl[u]);
         for (int st = 0; st < ns; st += kFuseStages) {
 #pragma unroll
           for (int u = 0; u < kFuseStages; ++u) {
             const int w = (u + kFuseStages - 1) % kFuseStages;
-            loadb(st + u + kFuseStages - 1, aq[w], bq[w]);
+            loadb(st + u + kFuseStages - 1, aq[w], bh[w], bl[w]);
             __builtin_amdgcn_sched_barrier(0);
-            if (u == 0 || st + u < ns) mma(aq[u], bq[u]);
+            if (u == 0 || st + u < ns) mma(aq[u], bh[u], bl[u]);
             __builtin_amdgcn_sched_barrier(0);
           }
         }
@@ -1092,10 +1147,14 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
               f[rt][mt] = make_float4(v.x * z, v.y * z, v.z * z, v.w * z);
             }
         };
+        // (scheduling barriers keep the next component's loads ahead of
+        // this one's MFMAs; without them the loads sink to their first use
+        // and every F block waits out a full L2 round trip)
         loadf(0, fv[0]);
 #pragma unroll
         for (int w = 0; w < NL; ++w) {
           if (w + 1 < NL) loadf(w + 1, fv[(w + 1) & 1]);
+          __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -1106,6 +1165,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
               ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.z, acc[mt][w][2], ya[rt], 0, 0, 0);
               ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.w, acc[mt][w][3], ya[rt], 0, 0, 0);
             }
+          __builtin_amdgcn_sched_barrier(0);
         }
       };
       if (nl == 4) recouple(std::integral_constant<int, 4>{});
@@ -2174,8 +2234,8 @@ hipError_t launch_feat_qmajor(int L, const float* feat, int n, int C, float* fea
   if (C % 16) return hipErrorInvalidValue;
   const int64_t total = (int64_t)n * (C / 16) * fuse_groups(L) * 16;
   if ((total + 255) / 256 > 0x7fffffff) return hipErrorInvalidValue;
-  k_feat_qmajor<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(feat, n, (L + 1) * (L + 1), C, fuse_groups(L),
-                                                                 (float4*)featq);
+  k_feat_qmajor3<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(feat, n, (L + 1) * (L + 1), C, fuse_groups(L),
+                                                                  (uint4*)featq, (uint2*)featq + 2 * total);
   return hipGetLastError();
 }
 
@@ -2186,7 +2246,10 @@ hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, co
   if (!outer_fused_supported(L, C, H, n_nodes)) return hipErrorInvalidValue;
   const int nk = (L + 1) * (L + 1), mp = 16 * ((nk + 15) / 16);
   const int nw = (nk + 3) / 4 + 1;  // a product wave per group of four components, and the staging wave
-  const size_t lds = sizeof(float) * (2 * (size_t)kFuseRows * (mp + 16) + 2 * (size_t)kFuseRows + kOuterEdges);
+  const size_t lds = sizeof(float) * (2 * (size_t)kFuseRows * 2 * mp + 2 * (size_t)kFuseRows + kOuterEdges);
+  const size_t nq = (size_t)n_nodes * H * fuse_groups(L) * 16;  // entries of the re-laid features
+  const uint4* fhm = (const uint4*)featq;
+  const uint2* flo = (const uint2*)(fhm + nq);
   static const int rpw_env = [] {
     const char* v = getenv("E2F_OUTER_RPW");
     return v ? atoi(v) : 0;
@@ -2199,8 +2262,7 @@ hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, co
 #define E2F_CASE(LL)                                                                                          \
   case LL:                                                                                                    \
     if (hipError_t e = allow_lds(k_outer_fused<LL, 512>, lds); e != hipSuccess) return e;                     \
-    k_outer_fused<LL, 512><<<(unsigned)blocks, 64 * nw, lds, s>>>(Re, row_ptr, col, alpha_hm, n_edges,         \
-                                                                  (const float4*)featq,                      \
+    k_outer_fused<LL, 512><<<(unsigned)blocks, 64 * nw, lds, s>>>(Re, row_ptr, col, alpha_hm, n_edges, fhm, flo, \
                                                                   order, F, n, nrx, rpw, C, H, hdiv, n_nodes, y); \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4)

@@ -152,11 +152,14 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* 
 // float64; then y[order[r]] directly from the aggregated products and F row r
 // (other arguments as for launch_outer_agg)
 // (L <= kFuseMaxL, C = 16 H, and the re-laid features of n_nodes atoms
-// addressable with 32-bit float4 offsets)
+// addressable with 32-bit entry offsets)
 bool outer_fused_supported(int L, int C, int H, int64_t n_nodes);
 hipError_t launch_fuse_build(int L, const int* fptr, const int* fidx, const double* fcoef, const double* R,
                              const int32_t* order, int n, float* F, hipStream_t s);
-// featq: the features re-laid by launch_feat_qmajor, n_nodes * C * 4 * fuse_groups(L) floats
+// featq: the features re-laid and split into bfloat16 parts by
+// launch_feat_qmajor, n_nodes * C * 6 * fuse_groups(L) floats of space (a
+// 16-byte and an 8-byte array of n_nodes * C / 16 * fuse_groups(L) * 16
+// entries each)
 int fuse_groups(int L);
 hipError_t launch_feat_qmajor(int L, const float* feat, int n, int C, float* featq, hipStream_t s);
 hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, const int32_t* col,
