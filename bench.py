@@ -95,11 +95,15 @@ def alg_counts(e2f, L, C, H, n, E, fused=False):
     mp = 16 * mt  # components of R per MFMA tile column, padded to 16
     inputs = 4.0 * n * nk * C + 4.0 * E * nk + 4.0 * E * H + 4.0 * E + 8.0 * (n + 1)
     if fused:
-        # issued: the products, then per receiver and head of 16 channels one
-        # 16x16x4 MFMA per (component q, row tile, K tile, K step)
+        # issued: the products as split bf16 (one v_mfma_f32_16x16x32_bf16 of
+        # 16384 flops per 4 edges, 16 rows and 16 columns: 8 bf16 products, six
+        # of them used, per fp32 multiply-add), then per receiver and head of
+        # 16 channels one fp32 16x16x4 MFMA per (component q, row tile, K tile,
+        # K step)
         agg = dict(flops=2.0 * E * dimT * C + 2.0 * n * (cpl + cnt["q_slots"]) * C,
                    bytes=inputs + 4.0 * n * nk * nk * nk + 4.0 * n * nk * C,
-                   issued_flops=2.0 * E * mp * nk * C + 2.0 * n * (C // 16) * nk * mt * mt * 4 * 1024)
+                   issued_flops=2.0 * n * (C // 16) * nk * mt * mt * 4 * 1024,
+                   issued_bf16_flops=16.0 * E * mp * nk * C)
     else:
         agg = dict(flops=2.0 * E * dimT * C + 2.0 * n * cpl * C, bytes=inputs + 4.0 * n * dimT * C,
                    issued_flops=2.0 * E * mp * nk * C + 2.0 * n * cpl * C)
@@ -170,7 +174,7 @@ def sweep_one(name, steps, warmup, crop=False, parity_rows=None, quiet=False):
 
     wl = syn.WORKLOADS[name]
     if parity_rows is None:
-        parity_rows = 256 if wl.lmax < 6 else 128
+        parity_rows = 256
     inp = syn.make_inputs(wl)
     dev = torch.device("cuda:0")
     pos_h, feat_h, gid_h, spc = inp.pos, inp.feat, inp.graph_id, inp.species
@@ -533,6 +537,13 @@ def main():
     if "issued_flops" in counts[dom]:
         roof["issued_flops"] = counts[dom]["issued_flops"]
         roof["issued_TFLOPs"] = counts[dom]["issued_flops"] / (t_dom * 1e-3) / 1e12
+    if "issued_bf16_flops" in counts[dom]:
+        # the fp32 products issued on the bf16 matrix cores (split operands);
+        # issued_flops then counts the fp32 MFMAs alone
+        roof["issued_bf16_flops"] = counts[dom]["issued_bf16_flops"]
+        roof["issued_bf16_TFLOPs"] = counts[dom]["issued_bf16_flops"] / (t_dom * 1e-3) / 1e12
+        roof["mfma_time_at_peak_ms"] = (counts[dom]["issued_flops"] / (FP32_MFMA_PEAK_TFS * 1e12)
+                                        + counts[dom]["issued_bf16_flops"] / (BF16_MFMA_PEAK_TFS * 1e12)) * 1e3
     tr_path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (dom, wl.name))
     if os.path.exists(tr_path):
         tr = json.load(open(tr_path))

@@ -122,10 +122,10 @@ def test_y_norm_unit_lattice_equals_plain(e2f, ctx):
 
 
 def test_y_norm_stress_200k_sampled(e2f, ctx):
-    # the 200,000-atom L = 6 system, factorised path, sampled receiver rows
+    # the 200,000-atom L = 6 system, factorised path, 256 sampled receiver rows
     inp, rp, ci, alpha = case("stress200k_L6")
     wl = inp.workload
-    r = sample_rows(inp.pos.shape[0], 12, seed=5)
+    r = sample_rows(inp.pos.shape[0], 256, seed=5)
     ref = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, rows=r, y_norm=True)
     print("stress200k y_norm: case", flush=True)
     got = e2f.e2f_wigner6j_conv_forward(ctx, gpu(inp.pos), gpu(inp.feat), gpu(rp), gpu(ci), gpu(alpha), wl.lmax,
