@@ -198,7 +198,11 @@ typedef struct {
                             form's S (n dimT C floats) would exceed 256 MiB (beyond the on-die
                             cache its round trip through HBM outweighs the fused form's extra
                             matrix-core work per receiver), else split.  All forms give the same
-                            result up to rounding order */
+                            result up to rounding order: the fused form multiplies on the bf16
+                            matrix cores with each float operand split into three bf16 parts
+                            (x = hi + mid + lo exactly) and the six cross products that reach
+                            2^-24 of the product accumulated in float, i.e. float products to
+                            within float rounding */
 } e2f_conv_params;
 
 /* Workspace of e2f_wigner6j_conv_forward for n atoms and n_edges edges:
