@@ -846,10 +846,27 @@ __device__ __forceinline__ void split_bf16x3(float x, unsigned& hi, unsigned& mi
   lo = __builtin_bit_cast(unsigned short, l);
 }
 
+// The fused aggregation's groups of components, one product wave each: NG =
+// ceil(NK / 4) groups of at most four, as even as possible (NK = 25: 4, 4, 4,
+// 4, 3, 3, 3), so that two product waves sharing a SIMD hold at most 7 of the
+// 25 component tiles; group g holds the components fuse_g0(NK, g) ..
+// fuse_g0(NK, g) + fuse_gn(NK, g) - 1.
+__host__ __device__ constexpr int fuse_gn(int nk, int g) {
+  return nk / ((nk + 3) / 4) + (g < nk % ((nk + 3) / 4) ? 1 : 0);
+}
+__host__ __device__ constexpr int fuse_g0(int nk, int g) {
+  return g * (nk / ((nk + 3) / 4)) + (g < nk % ((nk + 3) / 4) ? g : nk % ((nk + 3) / 4));
+}
+static_assert(fuse_g0(25, 6) + fuse_gn(25, 6) == 25 && fuse_gn(25, 3) == 4 && fuse_gn(25, 4) == 3,
+              "groups of 25 components: 4, 4, 4, 4, 3, 3, 3");
+static_assert(fuse_g0(16, 3) == 12 && fuse_gn(16, 3) == 4 && fuse_g0(9, 2) == 6 && fuse_gn(1, 0) == 1,
+              "groups of 16, 9 and 1 components");
+
 // The features in the order of the fused aggregation's B operand, each value
-// split into three bfloat16 parts: per node and head of 16 channels, groups
-// of four components q = 4 g + i (zero past (L+1)^2), each group [t][i] (t
-// the channel in the head): a uint4 of the four components' hi | mid << 16
+// split into three bfloat16 parts: per node and head of 16 channels, the
+// groups of components above (slot i of group g: component fuse_g0(NK, g) +
+// i, zero from fuse_gn(NK, g) on), each group [t][i] (t the channel in the
+// head): a uint4 of the four components' hi | mid << 16
 // and, in the second array (same index), a uint2 of their lo parts
 // (components 0, 1 in the first word, low half first).  Lane t of a wave
 // reads its group's four components with one 16-byte and one 8-byte load; a
@@ -868,7 +885,7 @@ __global__ void k_feat_qmajor3(const float* __restrict__ feat, int n, int nk, in
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     unsigned x, y, z;
-    split_bf16x3(4 * g + i < nk ? src[(size_t)(4 * g + i) * C] : 0.0f, x, y, z);
+    split_bf16x3(i < fuse_gn(nk, g) ? src[(size_t)(fuse_g0(nk, g) + i) * C] : 0.0f, x, y, z);
     a[i] = x | y << 16;
     b[i] = z;
   }
@@ -879,7 +896,7 @@ __global__ void k_feat_qmajor3(const float* __restrict__ feat, int n, int nk, in
 // The aggregation with the recouple applied in registers.  Work split as in
 // k_outer_agg (a workgroup: rpw consecutive receivers of one head h of 16
 // channels), but tile w of wave v holds the 16 channels t = l16 of one
-// component q = 4 v + w, so that after the products the accumulator element
+// component q = fuse_g0(NK, v) + w, so that after the products the accumulator element
 // s of a lane (l16, k4), G[16 mt + 4 k4 + s][q][l16], is exactly the B
 // operand of K step s of F_i G when the K index of that step is ordered as
 // be = 16 mt + 4 k4 + s; F_i is stored in the matching order.  Each wave sums
@@ -888,7 +905,7 @@ __global__ void k_feat_qmajor3(const float* __restrict__ feat, int n, int nk, in
 //
 // The workgroup walks its receivers' chunks of up to kOuterEdges edges (an
 // isolated receiver is one empty chunk).  Waves 0 .. NG-1 multiply (wave v:
-// the components 4v .. 4v+3); the last wave stages: while the others multiply
+// the fuse_gn(NK, v) components of group v); the last wave stages: while the others multiply
 // chunk k from one LDS buffer it loads chunk k+1 (alpha, R of the edges, the
 // senders) and writes alpha R and the senders' offsets into the other, so
 // the products never wait for a chunk's loads.  One barrier per chunk (two
@@ -915,7 +932,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
   constexpr int AS = 2 * MP;
   constexpr int ROT = (2 * MP) % 64 == 0 ? 16 : 0;
   constexpr int QB = fuse_qblock(NK), FS = fuse_stride(NK);
-  constexpr int NG = (NK + 3) / 4;  // groups of four components: one product wave each
+  constexpr int NG = (NK + 3) / 4;  // groups of at most four components (fuse_gn): one product wave each
   // rows EC .. SR-1 of a buffer are padding (zero weights, sender offset 0):
   // the last iteration of the step loop starts at a step st <= ns - 1 and
   // loads up to step st + 2 (kFuseStages - 1) ahead, i.e. rows up to
@@ -936,9 +953,10 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int l16 = lane & 15, k4 = lane >> 4;
   const bool stager = wave == NG;  // uniform over the wave
-  // a product wave's live tiles (components 4 wave .. 4 wave + nl - 1) and
-  // the lane's float4 of a sender: its wave's group, channel t = l16
-  const int nl = stager ? 0 : __builtin_amdgcn_readfirstlane(min(NK - 4 * wave, 4));
+  // a product wave's live tiles (the components q0 .. q0 + nl - 1 of its
+  // group) and the lane's entry of a sender: its wave's group, channel t = l16
+  const int nl = stager ? 0 : __builtin_amdgcn_readfirstlane(fuse_gn(NK, wave));
+  const int q0 = stager ? 0 : fuse_g0(NK, wave);
   const unsigned fstride = (unsigned)(H * NG * 16);
   const unsigned foff = (unsigned)((h * NG + min(wave, NG - 1)) * 16 + l16);
   const float* ah = alpha_hm ? alpha_hm + (int64_t)(h / hdiv) * n_edges : nullptr;
@@ -996,11 +1014,17 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
     }
     __builtin_amdgcn_wave_barrier();
     const int nrow = 4 * ((ne + 3) / 4);
-    const int be = lane % MP, rs = lane / MP;
-    const bool bok = be < NK;
+    // the lane's position p = lane % MP of the row holds component be (the
+    // K order of F: within tile p / 16, component j at 4 (j / ks) + j % ks),
+    // or nothing (zeros) where no component takes it
+    const int p = lane % MP, rs = lane / MP;
+    const int pt = p / 16, pk4 = (p % 16) / 4, ps = p % 4, ks = fuse_ks(NK, pt);
+    const int pj = pk4 * ks + ps;
+    const bool bok = pt * 16 < NK && ps < ks && pj < fuse_rows(NK, pt);
+    const int be = bok ? 16 * pt + pj : 0;
     // the lane's rows rs + RPI (BT bt + k): one base per batch, immediate
     // offsets within it
-    const float* src = Re + (size_t)(c0 + rs) * NK + (bok ? be : 0);
+    const float* src = Re + (size_t)(c0 + rs) * NK + be;
     constexpr int BT = 16, NBT = ITER / BT;
     static_assert(ITER % BT == 0, "batches must cover a chunk");
     static_assert(kEdgePad >= EC, "the per-edge arrays must be padded by a chunk");
@@ -1024,7 +1048,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
           // A of the split products: words hi | mid << 16 and hi | lo << 16
           unsigned hi, mid, lo;
           split_bf16x3(v, hi, mid, lo);
-          ((uint2*)(Al + nb * AS))[(be + (nb & 1) * ROT) % MP] = make_uint2(hi | mid << 16, hi | lo << 16);
+          ((uint2*)(Al + nb * AS))[(p + (nb & 1) * ROT) % MP] = make_uint2(hi | mid << 16, hi | lo << 16);
         }
       }
       if (more_rows) {
@@ -1133,7 +1157,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
         constexpr int NL = decltype(nlc)::value;
         float4 fv[2][MT][MT];
         auto loadf = [&](int w, float4 (*f)[MT]) {
-          const int q = 4 * wave + w;  // < NK for w < NL
+          const int q = q0 + w;  // < NK for w < NL
 #pragma unroll
           for (int rt = 0; rt < MT; ++rt)
 #pragma unroll
@@ -1159,11 +1183,16 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int rt = 0; rt < MT; ++rt) {
+              // K steps s >= fuse_ks(NK, mt) hold no component (zero F and
+              // G): skipped (mt is a constant of the unrolled loop)
               const float4 f = fv[w & 1][rt][mt];
               ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.x, acc[mt][w][0], ya[rt], 0, 0, 0);
-              ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.y, acc[mt][w][1], ya[rt], 0, 0, 0);
-              ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.z, acc[mt][w][2], ya[rt], 0, 0, 0);
-              ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.w, acc[mt][w][3], ya[rt], 0, 0, 0);
+              if (fuse_ks(NK, mt) > 1)
+                ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.y, acc[mt][w][1], ya[rt], 0, 0, 0);
+              if (fuse_ks(NK, mt) > 2)
+                ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.z, acc[mt][w][2], ya[rt], 0, 0, 0);
+              if (fuse_ks(NK, mt) > 3)
+                ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.w, acc[mt][w][3], ya[rt], 0, 0, 0);
             }
           __builtin_amdgcn_sched_barrier(0);
         }

@@ -147,12 +147,24 @@ int64_t node_tp_dim(int L);
 // (k, r) times CG[r][be, q].  F_i is stored per receiver in the order in which
 // the aggregation's waves read it as the A operand of v_mfma_f32_16x16x4f32:
 // per q a block of (row tile rt, K tile mt) sub-blocks, each [k4 < kc][l16 <
-// rows][s < 4] holding F[16 rt + l16][16 mt + 4 k4 + s][q] (zero where the
-// column index reaches (L+1)^2).
+// rows][s < 4] holding F[16 rt + l16][be][q] at K position 4 k4 + s =
+// fuse_kpos(be) of be's tile (zero at positions no component takes).  A tile
+// of r components uses kc = ceil(r / 4) groups k4 and ks = ceil(r / kc)
+// steps s each (component j of the tile at k4 = j / ks, s = j % ks), so where
+// r <= 12 the steps s >= ks hold only zeros and F_i G_i skips them (at
+// L = 4 the second tile's 9 components take s < 3).
 constexpr int kFuseMaxL = 4;
 constexpr int fuse_rows(int nk, int rt) { return nk - 16 * rt < 16 ? nk - 16 * rt : 16; }
 constexpr int fuse_kc(int nk, int mt) { return (fuse_rows(nk, mt) + 3) / 4; }
 constexpr int fuse_tiles(int nk) { return (nk + 15) / 16; }
+constexpr int fuse_ks(int nk, int mt) { return (fuse_rows(nk, mt) + fuse_kc(nk, mt) - 1) / fuse_kc(nk, mt); }
+// K position (0 .. 15) of component be inside its tile be / 16
+constexpr int fuse_kpos(int nk, int be) {
+  return 4 * ((be % 16) / fuse_ks(nk, be / 16)) + (be % 16) % fuse_ks(nk, be / 16);
+}
+static_assert(fuse_ks(25, 1) == 3 && fuse_kpos(25, 24) == 10 && fuse_kpos(25, 19) == 4 && fuse_kpos(25, 7) == 7 &&
+                  fuse_ks(16, 0) == 4 && fuse_ks(1, 0) == 1 && fuse_ks(9, 0) == 3,
+              "K positions of the fused layout");
 // offset (floats) of sub-block (rt, mt) inside a q block, rt-major
 constexpr int fuse_blk(int nk, int rt, int mt) {
   int off = 0;
@@ -168,8 +180,8 @@ constexpr int fuse_qblock(int nk) { return fuse_blk(nk, fuse_tiles(nk), 0); }
 constexpr int fuse_stride(int nk) { return (nk * fuse_qblock(nk) + 63) / 64 * 64; }
 // position of F[k][be][q] in a receiver's row
 constexpr int fuse_pos(int nk, int k, int be, int q) {
-  return q * fuse_qblock(nk) + fuse_blk(nk, k / 16, be / 16) + ((be % 16) / 4 * fuse_rows(nk, k / 16) + k % 16) * 4 +
-         be % 4;
+  return q * fuse_qblock(nk) + fuse_blk(nk, k / 16, be / 16) +
+         (fuse_kpos(nk, be) / 4 * fuse_rows(nk, k / 16) + k % 16) * 4 + fuse_kpos(nk, be) % 4;
 }
 // K_x by position of F (CSR over the positions 0 .. fuse_stride - 1): the
 // entries of position p are idx[e] (the component x) and coef[e] (float64,
