@@ -99,10 +99,14 @@ def alg_counts(e2f, L, C, H, n, E, fused=False):
         # 16384 flops per 4 edges, 16 rows and 16 columns: 8 bf16 products, six
         # of them used, per fp32 multiply-add), then per receiver and head of
         # 16 channels one fp32 16x16x4 MFMA per (component q, row tile, K tile,
-        # K step)
+        # K step), a K tile of r components taking ceil(r / ceil(r / 4)) steps
+        ksteps = 0
+        for t in range(mt):
+            r = min(16, nk - 16 * t)
+            ksteps += -(-r // -(-r // 4))
         agg = dict(flops=2.0 * E * dimT * C + 2.0 * n * (cpl + cnt["q_slots"]) * C,
                    bytes=inputs + 4.0 * n * nk * nk * nk + 4.0 * n * nk * C,
-                   issued_flops=2.0 * n * (C // 16) * nk * mt * mt * 4 * 1024,
+                   issued_flops=2.0 * n * (C // 16) * nk * mt * ksteps * 1024,
                    issued_bf16_flops=16.0 * E * mp * nk * C)
     else:
         agg = dict(flops=2.0 * E * dimT * C + 2.0 * n * cpl * C, bytes=inputs + 4.0 * n * dimT * C,
