@@ -99,3 +99,23 @@ def test_fused_protein_rows_and_workspace_sizes(e2f, ctx):
     sliced = e2f.e2f_wigner6j_conv_forward(ctx, *args, workspace=ws).cpu().numpy()
     assert e2f.e2f_last_slices(ctx) == (n + 255) // 256
     assert np.array_equal(sliced, fused)
+
+
+@pytest.mark.parametrize("scale_exp", [-40, 40])
+def test_fused_power_of_two_scaling_is_exact(e2f, ctx, scale_exp):
+    # the forward is linear in h, and a power of two commutes with every step
+    # of the fused form (the three-part bf16 split of the features, the exact
+    # bf16 products, float sums, F_i G_i): scaling h by 2^k scales y bit for
+    # bit, far from the float range's ends (values here stay within 2^-70 ..
+    # 2^60)
+    L, C, H, n = 4, 32, 2, 120
+    rng = np.random.default_rng(77)
+    pos = syn.quantize(rng.uniform(0, 10.0, size=(n, 3)))
+    rp, ci = o.neighbor_list(pos, 5.0)
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    alpha = rng.uniform(0.05, 1.0, size=(len(ci), H)).astype(np.float32)
+    args = (gpu(rp), gpu(ci), gpu(alpha), L, H, 5.0)
+    y1 = e2f.e2f_wigner6j_conv_forward(ctx, gpu(pos), gpu(feat), *args, form="fused").cpu().numpy()
+    fs = np.ldexp(feat, scale_exp).astype(np.float32)
+    y2 = e2f.e2f_wigner6j_conv_forward(ctx, gpu(pos), gpu(fs), *args, form="fused").cpu().numpy()
+    assert np.array_equal(np.ldexp(y1, scale_exp).astype(np.float32), y2)
