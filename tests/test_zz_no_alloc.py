@@ -46,6 +46,21 @@ def test_forward_without_allocation():
             print("no-alloc forward: %s err vs workspace entry %.3e" % (name, err), flush=True)
             assert err <= TOL_F32
             runs.append(name)
+        # the fused form (split-bf16 products, F_i per receiver, re-laid
+        # features) in the scratch memory, after the two-kernel calls above
+        inp, rp, ci, alpha = case("water2000_L4")
+        wl = inp.workload
+        args = (gpu(inp.pos), gpu(inp.feat), gpu(rp), gpu(ci), gpu(alpha), wl.lmax, wl.heads, wl.cutoff)
+        print("no-alloc forward: water2000_L4 fused, %d atoms, %d edges" % (inp.pos.shape[0], len(ci)), flush=True)
+        e2f.e2f_wigner6j_prepare(ctx, wl.lmax, wl.channels, wl.heads, wl.cutoff, form="fused")
+        out = torch.full_like(gpu(inp.feat), float("nan"))
+        e2f.e2f_wigner6j_conv_forward_noalloc(ctx, *args, out=out, form="fused")
+        want = e2f.e2f_wigner6j_conv_forward(ctx, *args, form="fused").cpu().numpy()
+        got = out.cpu().numpy()
+        assert np.isfinite(got).all()
+        err = o.max_rel_err(got, want.astype(np.float64), wl.lmax)
+        print("no-alloc forward: water2000_L4 fused err vs workspace entry %.3e" % err, flush=True)
+        assert err <= TOL_F32
         # an input whose smallest workspace exceeds the scratch memory
         inp, rp, ci, alpha = case("protein20k_L4")
         wl = inp.workload
