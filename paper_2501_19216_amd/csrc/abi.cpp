@@ -692,7 +692,11 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
   // under alpha / D^f, with the shortest edge), tile grid, receiver order,
   // solid harmonics of the edges and receivers
   int32_t* erows = (int32_t*)(ws + f.erows);
-  E2F_TIMED("bbox", launch_plan_bbox(pos, graph_id, n, stats, ynorm ? dmin : nullptr, s));
+  // (a graph of at most kPlanSmallMax atoms takes the whole plan in one
+  // workgroup: box, grid, tiles and the sorted order in one launch)
+  const bool small_plan = n <= kPlanSmallMax;
+  if (!small_plan) E2F_TIMED("bbox", launch_plan_bbox(pos, graph_id, n, stats, ynorm ? dmin : nullptr, s));
+  else if (ynorm) E2F_TIMED("bbox", launch_plan_init(stats, dmin, s));
   E2F_TIMED("tile_plan", launch_plan_edge_rows(row_ptr, n, n_edges, erows, s));
   if (ynorm) {
     E2F_TIMED("alpha_hm", launch_plan_dmin(pos, erows, col_idx, n, n_edges, dmin, s));
@@ -701,11 +705,15 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
     E2F_TIMED("alpha_hm", launch_alpha_head_major(alpha, n_edges, H, alpha_hm, s));
   }
   const double side = (p->tile_side > 0.0f ? (double)p->tile_side : kTileCutoffs[L] * (double)p->cutoff) * kGrid;
-  E2F_TIMED("tile_plan", launch_plan_grid(stats, ynorm ? dmin : nullptr, side, kYnormTileScale, graph_id != nullptr,
-                                          grid, s));
-  E2F_TIMED("tile_plan", launch_plan_order(pos, graph_id, n, grid, tile_of, (uint64_t*)(ws + f.keys),
-                                           (uint64_t*)(ws + f.keys_out), (int32_t*)(ws + f.vals), order,
-                                           ws + f.sort_tmp, f.sort_b, s));
+  if (small_plan) {
+    E2F_TIMED("tile_plan", launch_plan_small(pos, graph_id, n, ynorm ? dmin : nullptr, side, kYnormTileScale, stats,
+                                             grid, tile_of, order, s));
+  } else {
+    E2F_TIMED("tile_plan", launch_plan_grid(stats, ynorm ? dmin : nullptr, side, kYnormTileScale, grid, s));
+    E2F_TIMED("tile_plan", launch_plan_order(pos, graph_id, n, grid, tile_of, (uint64_t*)(ws + f.keys),
+                                             (uint64_t*)(ws + f.keys_out), (int32_t*)(ws + f.vals), order,
+                                             ws + f.sort_tmp, f.sort_b, s));
+  }
   E2F_TIMED("sh", launch_plan_sh(t, pos, erows, col_idx, n, n_edges, tile_of, grid, Rr, Re, s));
   // ---- aggregation and recouple per slice of receivers (S of one slice
   // at a time in the workspace)

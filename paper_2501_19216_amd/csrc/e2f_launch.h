@@ -19,9 +19,9 @@ constexpr int kEdgePad = 128;
 hipError_t launch_bbox(const float* pos, const int32_t* graph_id, int n, int* stats, hipStream_t s);
 
 // ---- device-side plan of the factorised forward (plan.hip)
-// Tile grid on the 2^-16 A lattice: cell (cx, cy, cz) of a graph covers
-// lo + [c span / dim, (c+1) span / dim) per axis; its centre is the local
-// origin of the receivers in it.
+// Tile grid on the 2^-16 A lattice, shared by every graph: cell (cx, cy, cz)
+// covers lo + [c span / dim, (c+1) span / dim) per axis; its centre is the
+// local origin of the receivers in it.
 struct TileGridDev {
   int lo[3];
   int dim[3];
@@ -38,10 +38,20 @@ hipError_t launch_plan_dmin(const float* pos, const int32_t* rows, const int32_t
 // origin [3] float64 = the centre of the bounding box in stats
 hipError_t launch_plan_centre(const int* stats, double* origin, hipStream_t s);
 // side in grid units; with dmin, side = min(side, dmin_scale * shortest edge)
-hipError_t launch_plan_grid(const int* stats, const unsigned* dmin, double side, double dmin_scale, bool graphs,
+hipError_t launch_plan_grid(const int* stats, const unsigned* dmin, double side, double dmin_scale,
                             TileGridDev* grid, hipStream_t s);
 size_t plan_sort_tmp_bytes(int n);
-// tile_of [n]; order [n] = receivers sorted by (graph, Morton index of 4 A cells)
+// stats and *dmin initialised alone (the small plan computes the box itself)
+hipError_t launch_plan_init(int* stats, unsigned* dmin, hipStream_t s);
+// The whole plan of a graph of at most kPlanSmallMax atoms in one workgroup:
+// stats, grid, tile_of and order as launch_plan_bbox + launch_plan_grid +
+// launch_plan_order give them (dmin as for launch_plan_grid)
+constexpr int kPlanSmallMax = 8192;
+hipError_t launch_plan_small(const float* pos, const int32_t* graph_id, int n, const unsigned* dmin, double side,
+                             double dmin_scale, int* stats, TileGridDev* grid, int32_t* tile_of, int32_t* order,
+                             hipStream_t s);
+// tile_of [n] = the grid cell of every atom; order [n] = receivers sorted by
+// (graph, Morton index of 4 A cells)
 hipError_t launch_plan_order(const float* pos, const int32_t* graph_id, int n, const TileGridDev* grid,
                              int32_t* tile_of, uint64_t* keys, uint64_t* keys_out, int32_t* vals, int32_t* order,
                              void* tmp, size_t tmp_bytes, hipStream_t s);

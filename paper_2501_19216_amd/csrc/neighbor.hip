@@ -18,23 +18,68 @@ namespace {
 
 __device__ __forceinline__ int grid_coord(float x) { return __float2int_rn(x * 65536.0f); }
 
-__global__ void k_bbox(const float* __restrict__ pos, const int32_t* __restrict__ gid, int n, int* __restrict__ st) {
+// Bounding box on the grid (stats as in launch_bbox): each lane's atom, a
+// reduction over the wave and the workgroup, then one atomic per workgroup
+// and value.  An atom with a coordinate that is not finite or beyond
+// +-16384 A sets bit 1 and stays out of the box; a negative graph id sets
+// bit 2.
+__global__ __launch_bounds__(256) void k_bbox(const float* __restrict__ pos, const int32_t* __restrict__ gid, int n,
+                                              int* __restrict__ st) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  for (int k = 0; k < 3; ++k) {
-    const float x = pos[3 * i + k];
-    if (!(fabsf(x) < 16384.0f)) {  // also catches NaN
-      atomicOr(&st[7], 1);
-      return;
+  int lo[3] = {INT_MAX, INT_MAX, INT_MAX}, hi[3] = {INT_MIN, INT_MIN, INT_MIN}, gmax = 0, bad = 0;
+  if (i < n) {
+    float x[3];
+    bool ok = true;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      x[k] = pos[3 * i + k];
+      ok = ok && fabsf(x[k]) < 16384.0f;  // also false for NaN
     }
-    const int X = grid_coord(x);
-    atomicMin(&st[k], X);
-    atomicMax(&st[3 + k], X);
+    if (ok) {
+#pragma unroll
+      for (int k = 0; k < 3; ++k) lo[k] = hi[k] = grid_coord(x[k]);
+    } else {
+      bad |= 1;
+    }
+    if (gid) {
+      const int g = gid[i];
+      if (g < 0) bad |= 2;
+      else gmax = g;
+    }
   }
-  if (gid) {
-    const int g = gid[i];
-    if (g < 0) atomicOr(&st[7], 2);
-    else atomicMax(&st[6], g);
+  for (int o = 32; o > 0; o >>= 1) {  // every lane takes part
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      lo[k] = min(lo[k], __shfl_xor(lo[k], o));
+      hi[k] = max(hi[k], __shfl_xor(hi[k], o));
+    }
+    gmax = max(gmax, __shfl_xor(gmax, o));
+    bad |= __shfl_xor(bad, o);
+  }
+  __shared__ int part[4][8];  // the waves' results, then one atomic per workgroup and value
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+    for (int k = 0; k < 3; ++k) part[wave][k] = lo[k], part[wave][3 + k] = hi[k];
+    part[wave][6] = gmax, part[wave][7] = bad;
+  }
+  __syncthreads();
+  if (threadIdx.x < 8) {
+    const int q = threadIdx.x;
+    int v = part[0][q];
+    for (int w = 1; w < (int)(blockDim.x >> 6); ++w) {
+      const int u = part[w][q];
+      v = q < 3 ? min(v, u) : (q < 7 ? max(v, u) : (v | u));
+    }
+    if (q < 3) {
+      if (v != INT_MAX) atomicMin(&st[q], v);
+    } else if (q < 6) {
+      if (v != INT_MIN) atomicMax(&st[q], v);
+    } else if (q == 6) {
+      if (v > 0) atomicMax(&st[6], v);
+    } else if (v) {
+      atomicOr(&st[7], v);
+    }
   }
 }
 

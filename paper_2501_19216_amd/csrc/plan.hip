@@ -13,6 +13,7 @@
 #include <hip/hip_runtime.h>
 #include <hipcub/hipcub.hpp>
 
+#include <algorithm>
 #include <climits>
 
 #include "e2f_launch.h"
@@ -41,7 +42,12 @@ __device__ __forceinline__ void tile_centre(const TileGridDev& g, int cell, doub
   double o[3];
 #pragma unroll
   for (int k = 0; k < 3; ++k)
-    o[k] = (double)(g.lo[k] + ((2 * (int64_t)c[k] + 1) * g.span[k]) / (2 * (int64_t)g.dim[k])) / kGrid;
+    // floor((2c + 1) span / (2 dim)): the product is below 2^43 and the
+    // divisor at most 2048, so the double quotient (below 2^32, error below
+    // 2^-21) truncates to the integer division's result, which is at least
+    // 1/2048 from the next integer
+    o[k] = (double)(g.lo[k] + (int64_t)((double)((2 * (int64_t)c[k] + 1) * g.span[k]) / (double)(2 * g.dim[k]))) /
+           kGrid;
   ox = o[0], oy = o[1], oz = o[2];
 }
 
@@ -72,24 +78,76 @@ __global__ void k_plan_init(int* __restrict__ st, unsigned* __restrict__ dmin) {
   if (threadIdx.x == 0 && dmin) *dmin = 0x7f800000u;  // +inf
 }
 
-__global__ void k_plan_bbox(const float* __restrict__ pos, const int32_t* __restrict__ gid, int n,
-                            int* __restrict__ st) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  for (int k = 0; k < 3; ++k) {
-    const float x = pos[3 * i + k];
-    if (!(fabsf(x) < 16384.0f)) {  // also catches NaN; the atom is then kept out of the box
-      atomicOr(&st[7], 1);
-      return;
-    }
-    const int X = __float2int_rn(x * 65536.0f);
-    atomicMin(&st[k], X);
-    atomicMax(&st[3 + k], X);
+// One atom's part of the bounding box: its grid coordinates (lo = hi), or
+// the empty box and error bit 1 when a coordinate is not finite or outside
+// +-16384 A (the atom is then kept out of the box); its graph id g (or -1
+// without graphs), or error bit 2 when negative.
+__device__ __forceinline__ void atom_box(const float x[3], int g, bool has_graph, int lo[3], int hi[3], int& gmax,
+                                         int& bad) {
+  lo[0] = lo[1] = lo[2] = INT_MAX;
+  hi[0] = hi[1] = hi[2] = INT_MIN;
+  gmax = 0;
+  bad = 0;
+  const bool ok = fabsf(x[0]) < 16384.0f && fabsf(x[1]) < 16384.0f && fabsf(x[2]) < 16384.0f;  // false for NaN
+  if (ok) {
+#pragma unroll
+    for (int k = 0; k < 3; ++k) lo[k] = hi[k] = __float2int_rn(x[k] * 65536.0f);
+  } else {
+    bad |= 1;
   }
-  if (gid) {
-    const int g = gid[i];
-    if (g < 0) atomicOr(&st[7], 2);
-    else atomicMax(&st[6], g);
+  if (has_graph) {
+    if (g < 0) bad |= 2;
+    else gmax = g;
+  }
+}
+
+// Reduction of atom_box over a wave (every lane takes part).
+__device__ __forceinline__ void wave_box(int lo[3], int hi[3], int& gmax, int& bad) {
+  for (int o = 32; o > 0; o >>= 1) {
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      lo[k] = min(lo[k], __shfl_xor(lo[k], o));
+      hi[k] = max(hi[k], __shfl_xor(hi[k], o));
+    }
+    gmax = max(gmax, __shfl_xor(gmax, o));
+    bad |= __shfl_xor(bad, o);
+  }
+}
+
+// The bounding box on the grid: a wave reduction, the workgroup's waves
+// through LDS, then one atomic per workgroup and value.
+__global__ __launch_bounds__(256) void k_plan_bbox(const float* __restrict__ pos, const int32_t* __restrict__ gid,
+                                                   int n, int* __restrict__ st) {
+  __shared__ int part[4][8];
+  const int i = blockIdx.x * blockDim.x + threadIdx.x, wave = threadIdx.x >> 6;
+  int lo[3] = {INT_MAX, INT_MAX, INT_MAX}, hi[3] = {INT_MIN, INT_MIN, INT_MIN}, gmax = 0, bad = 0;
+  if (i < n) {
+    const float x[3] = {pos[3 * i], pos[3 * i + 1], pos[3 * i + 2]};
+    atom_box(x, gid ? gid[i] : 0, gid != nullptr, lo, hi, gmax, bad);
+  }
+  wave_box(lo, hi, gmax, bad);  // every lane takes part
+  if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+    for (int k = 0; k < 3; ++k) part[wave][k] = lo[k], part[wave][3 + k] = hi[k];
+    part[wave][6] = gmax, part[wave][7] = bad;
+  }
+  __syncthreads();
+  if (threadIdx.x < 8) {
+    const int q = threadIdx.x;
+    int v = part[0][q];
+    for (int w = 1; w < (int)(blockDim.x >> 6); ++w) {
+      const int u = part[w][q];
+      v = q < 3 ? min(v, u) : (q < 7 ? max(v, u) : (v | u));
+    }
+    if (q < 3) {
+      if (v != INT_MAX) atomicMin(&st[q], v);
+    } else if (q < 6) {
+      if (v != INT_MIN) atomicMax(&st[q], v);
+    } else if (q == 6) {
+      if (v > 0) atomicMax(&st[6], v);
+    } else if (v) {
+      atomicOr(&st[7], v);
+    }
   }
 }
 
@@ -109,60 +167,54 @@ __global__ void k_plan_dmin(const float* __restrict__ pos, const int32_t* __rest
   if ((threadIdx.x & 63) == 0 && v != 0x7f800000u) atomicMin(dmin, v);
 }
 
-// One thread: the tile grid from the bounding box.  The side is `side`
-// grid units, or, when dmin is given, at most dmin_scale times the shortest
-// edge; at least 1/64 A, at most 1024 tiles per axis, and graphs x tiles
-// below 2^31.
-__global__ void k_plan_grid(const int* __restrict__ st, const unsigned* __restrict__ dmin, double side,
-                            double dmin_scale, bool graphs, TileGridDev* __restrict__ g) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  int lo[3], hi[3];
-  for (int k = 0; k < 3; ++k) {
-    lo[k] = st[k], hi[k] = st[3 + k];
-    if (lo[k] > hi[k]) lo[k] = hi[k] = 0;  // no finite position
-  }
+// The tile grid from the bounding box st (as k_plan_bbox leaves it).  The
+// side is `side` grid units, or, when dmin is given, at most dmin_scale
+// times the shortest edge; at least 1/64 A and at most 1024 tiles per axis
+// (so at most 2^30 tiles).  The tiles of every graph share the grid: a tile
+// only places the local origin of the receivers in it.
+__device__ void grid_from_box(const int* st, const unsigned* __restrict__ dmin, double side, double dmin_scale,
+                              TileGridDev& g) {
   if (dmin) {
     const float d = __uint_as_float(*dmin);
     if (d < INFINITY) side = fmin(side, dmin_scale * (double)d * kGrid);
   }
   side = fmax(side, kGrid / 64.0);
-  const int64_t ngraph = graphs ? (int64_t)st[6] + 1 : 1;
-  for (;;) {
-    int64_t ncell = 1;
-    for (int k = 0; k < 3; ++k) {
-      g->lo[k] = lo[k];
-      g->span[k] = (int64_t)hi[k] - lo[k] + 1;
-      int64_t d = (int64_t)ceil((double)g->span[k] / side);
-      d = d < 1 ? 1 : (d > 1024 ? 1024 : d);
-      g->dim[k] = (int)d;
-      ncell *= d;
-    }
-    if (ncell * ngraph < ((int64_t)1 << 31) || side > 1e18) {
-      g->ncell = (int)ncell;
-      break;
-    }
-    side *= 2.0;
+  int64_t ncell = 1;
+  for (int k = 0; k < 3; ++k) {
+    int lo = st[k], hi = st[3 + k];
+    if (lo > hi) lo = hi = 0;  // no finite position
+    g.lo[k] = lo;
+    g.span[k] = (int64_t)hi - lo + 1;
+    int64_t d = (int64_t)ceil((double)g.span[k] / side);
+    d = d < 1 ? 1 : (d > 1024 ? 1024 : d);
+    g.dim[k] = (int)d;
+    ncell *= d;
   }
+  g.ncell = (int)ncell;
+  g.pad = 0;
+}
+
+__global__ void k_plan_grid(const int* __restrict__ st, const unsigned* __restrict__ dmin, double side,
+                            double dmin_scale, TileGridDev* __restrict__ g) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  TileGridDev v;
+  grid_from_box(st, dmin, side, dmin_scale, v);
+  *g = v;
 }
 
 __device__ __forceinline__ int tile_axis(float x, const TileGridDev& g, int k) {
   const int64_t X = __float2int_rn(x * 65536.0f);
-  int64_t q = (X - g.lo[k]) * g.dim[k] / g.span[k];
+  const int64_t q = (int64_t)((double)(X - g.lo[k]) * (double)g.dim[k] / (double)g.span[k]);
   return (int)(q < 0 ? 0 : (q > g.dim[k] - 1 ? g.dim[k] - 1 : q));
 }
 
-// tile_of[i] = graph * ncell + cell; keys for the receiver order: graph in
-// the high 32 bits, then the Morton index of 4 A cells of the box.
-__global__ void k_plan_tiles(const float* __restrict__ pos, const int32_t* __restrict__ gid, int n,
-                             const TileGridDev* __restrict__ gp, int32_t* __restrict__ tile_of,
-                             uint64_t* __restrict__ keys, int32_t* __restrict__ vals) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const TileGridDev g = *gp;
-  const float p[3] = {pos[3 * i], pos[3 * i + 1], pos[3 * i + 2]};
+// Tile of an atom at p (its cell of the grid) and its key in the receiver
+// order: the graph in the high 32 bits, then the Morton index of 4 A cells
+// of the box.
+__device__ __forceinline__ void tile_key(const float p[3], int graph, const TileGridDev& g, int32_t& tile,
+                                         uint64_t& key) {
   const int c0 = tile_axis(p[0], g, 0), c1 = tile_axis(p[1], g, 1), c2 = tile_axis(p[2], g, 2);
-  const int graph = gid ? max(gid[i], 0) : 0;
-  tile_of[i] = graph * g.ncell + (c2 * g.dim[1] + c1) * g.dim[0] + c0;
+  tile = (c2 * g.dim[1] + c1) * g.dim[0] + c0;
   uint32_t m = 0;
   for (int k = 0; k < 3; ++k) {
     int64_t c = ((int64_t)__float2int_rn(p[k] * 65536.0f) - g.lo[k]) / (int64_t)(4.0 * kGrid);
@@ -174,8 +226,199 @@ __global__ void k_plan_tiles(const float* __restrict__ pos, const int32_t* __res
     v = (v | (v << 2)) & 0x09249249;
     m |= v << k;
   }
-  keys[i] = ((uint64_t)(uint32_t)graph << 32) | m;
+  key = ((uint64_t)(uint32_t)graph << 32) | m;
+}
+
+__global__ void k_plan_tiles(const float* __restrict__ pos, const int32_t* __restrict__ gid, int n,
+                             const TileGridDev* __restrict__ gp, int32_t* __restrict__ tile_of,
+                             uint64_t* __restrict__ keys, int32_t* __restrict__ vals) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const TileGridDev g = *gp;
+  const float p[3] = {pos[3 * i], pos[3 * i + 1], pos[3 * i + 2]};
+  tile_key(p, gid ? max(gid[i], 0) : 0, g, tile_of[i], keys[i]);
   vals[i] = i;
+}
+
+// The whole plan of a small graph (n <= kPlanSmallMax) in one workgroup of
+// T threads (8 T >= n): bounding box, grid, tiles and keys (each thread
+// loads its atoms tid + u T, u < 8, once, all loads in flight together),
+// then the receivers sorted by key with a least-significant-digit radix sort
+// in LDS.  A slot is one 64-bit word, Morton index << 13 | atom index; the
+// passes take four bits at a time, first of the Morton index, then (with
+// graphs) of the graph id, read through the slot's atom index (graph ids are
+// more significant, as in the key of the large path), and a pass is skipped
+// where every atom has the same digit.  Each pass is stable: thread t holds
+// slots 8t .. 8t+7, and the slot of its u-th item with digit d is the count
+// of smaller digits, plus the count of d in threads below t, plus the count
+// of d in its own items before u.  So the order is the one the stable radix
+// sort of the large path gives.  The slots past n hold the largest key and
+// follow every atom.  st and *gout are written as by k_plan_bbox and
+// k_plan_grid.
+// LDS: slots [9 NS/8] u64 (slot s at s + s/8, so the eight consecutive slots
+// of a lane start 72 bytes after the previous lane's), per-thread offset
+// rows [T][17] u32, per-wave digit counts and their prefix over the waves
+// [33][8] u32.
+constexpr int kPlanIpt = 8;
+constexpr int kPlanIdxBits = 13;  // atom index bits of a slot: kPlanSmallMax <= 2^13
+constexpr int kPlanThreads = 1024;
+
+__device__ __forceinline__ int plan_slot(int s) { return s + s / kPlanIpt; }
+
+__global__ __launch_bounds__(kPlanThreads) void k_plan_small(const float* __restrict__ pos,
+                                                             const int32_t* __restrict__ gid, int n,
+                                                             const unsigned* __restrict__ dmin, double side,
+                                                             double dmin_scale, int* __restrict__ st,
+                                                             TileGridDev* __restrict__ gout,
+                                                             int32_t* __restrict__ tile_of,
+                                                             int32_t* __restrict__ order) {
+  extern __shared__ uint64_t slot[];
+  __shared__ int box[kStatsInts];
+  __shared__ unsigned bits[4];  // OR and AND of the Morton indices, then of the graph ids
+  __shared__ TileGridDev g;
+  const int T = blockDim.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, NW = T / 64, NS = kPlanIpt * T;
+  unsigned* offs = (unsigned*)(slot + plan_slot(NS));
+  unsigned* wcnt = offs + 17 * T;  // [wave][8]: the wave's digit counts; [16 + wave][8]: those of the waves below
+  if (tid < kStatsInts) box[tid] = tid < 3 ? INT_MAX : (tid < 6 ? INT_MIN : 0);
+  if (tid < 4) bits[tid] = (tid & 1) ? ~0u : 0u;
+  float x[kPlanIpt][3];
+  int gv[kPlanIpt];
+#pragma unroll
+  for (int u = 0; u < kPlanIpt; ++u) {
+    const int i = tid + u * T;
+    const int c = i < n ? i : 0;  // unconditional loads (n >= 1), masked below
+    x[u][0] = pos[3 * c], x[u][1] = pos[3 * c + 1], x[u][2] = pos[3 * c + 2];
+    gv[u] = gid ? gid[c] : 0;
+  }
+  int lo[3] = {INT_MAX, INT_MAX, INT_MAX}, hi[3] = {INT_MIN, INT_MIN, INT_MIN}, gmax = 0, bad = 0;
+#pragma unroll
+  for (int u = 0; u < kPlanIpt; ++u) {
+    if (tid + u * T >= n) continue;
+    int l[3], h[3], gm, b;
+    atom_box(x[u], gv[u], gid != nullptr, l, h, gm, b);
+#pragma unroll
+    for (int k = 0; k < 3; ++k) lo[k] = min(lo[k], l[k]), hi[k] = max(hi[k], h[k]);
+    gmax = max(gmax, gm);
+    bad |= b;
+  }
+  __syncthreads();  // box initialised
+  wave_box(lo, hi, gmax, bad);
+  if (lane == 0) {
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      atomicMin(&box[k], lo[k]);
+      atomicMax(&box[3 + k], hi[k]);
+    }
+    atomicMax(&box[6], gmax);
+    atomicOr(&box[7], bad);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    TileGridDev v;
+    grid_from_box(box, dmin, side, dmin_scale, v);
+    g = v;
+    *gout = v;
+  }
+  if (tid < kStatsInts) st[tid] = box[tid];
+  __syncthreads();
+  unsigned mor = 0, mand = ~0u, gor = 0, gand = ~0u;
+#pragma unroll
+  for (int u = 0; u < kPlanIpt; ++u) {
+    const int i = tid + u * T;
+    uint64_t w = (uint64_t)0x3fffffff << kPlanIdxBits | (uint64_t)i;  // past n: the largest Morton index
+    if (i < n) {
+      int32_t t;
+      uint64_t key;
+      tile_key(x[u], gid ? max(gv[u], 0) : 0, g, t, key);
+      tile_of[i] = t;
+      const unsigned m = (unsigned)key, gr = (unsigned)(key >> 32);
+      mor |= m, mand &= m, gor |= gr, gand &= gr;
+      w = (uint64_t)m << kPlanIdxBits | (uint64_t)i;
+    }
+    slot[plan_slot(i)] = w;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    mor |= __shfl_xor(mor, o), mand &= __shfl_xor(mand, o);
+    gor |= __shfl_xor(gor, o), gand &= __shfl_xor(gand, o);
+  }
+  if (lane == 0) {
+    atomicOr(&bits[0], mor);
+    atomicAnd(&bits[1], mand);
+    atomicOr(&bits[2], gor);
+    atomicAnd(&bits[3], gand);
+  }
+  __syncthreads();
+  const unsigned mdiff = bits[0] ^ bits[1], gdiff = gid ? bits[2] ^ bits[3] : 0u;
+  // passes: digit p < 8 of the Morton index, then digit p - 8 of the graph id
+  for (int p = 0; p < 16; ++p) {
+    const unsigned dm = p < 8 ? mdiff : gdiff;
+    const int sh = 4 * (p & 7);
+    if (((dm >> sh) & 15u) == 0) continue;  // every atom has this digit: the pass keeps the order
+    uint64_t w[kPlanIpt];
+    int d[kPlanIpt], r[kPlanIpt];
+    uint64_t c64 = 0;  // the thread's count of each digit, four bits each (at most 8)
+#pragma unroll
+    for (int u = 0; u < kPlanIpt; ++u) w[u] = slot[plan_slot(kPlanIpt * tid + u)];
+#pragma unroll
+    for (int u = 0; u < kPlanIpt; ++u) {
+      if (p < 8) {
+        d[u] = (int)(w[u] >> (kPlanIdxBits + sh)) & 15;
+      } else {
+        const int i = (int)(w[u] & ((1u << kPlanIdxBits) - 1));
+        const unsigned gr = i < n ? (unsigned)max(gid[i], 0) : 0x7fffffffu;
+        d[u] = (int)(gr >> sh) & 15;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kPlanIpt; ++u) {
+      r[u] = (int)(c64 >> (4 * d[u])) & 15;
+      c64 += (uint64_t)1 << (4 * d[u]);
+    }
+    // counts of digits 2q and 2q+1 in the halves of word q, then an
+    // inclusive scan over the wave (totals stay below 2^16)
+    unsigned cw[8], inc[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      cw[q] = (unsigned)((c64 >> (8 * q)) & 15) | (unsigned)((c64 >> (8 * q + 4)) & 15) << 16;
+      inc[q] = cw[q];
+    }
+    for (int o = 1; o < 64; o <<= 1) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const unsigned y = __shfl_up(inc[q], o);
+        if (lane >= o) inc[q] += y;
+      }
+    }
+    if (lane == 63) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) wcnt[wave * 8 + q] = inc[q];
+    }
+    __syncthreads();  // every slot loaded (the scatter below overwrites them) and the wave counts stored
+    if (tid < 8) {    // prefix of the counts over the waves; entry NW holds the totals
+      unsigned c[kPlanThreads / 64], a = 0;
+#pragma unroll
+      for (int wv = 0; wv < kPlanThreads / 64; ++wv) c[wv] = wv < NW ? wcnt[wv * 8 + tid] : 0u;
+#pragma unroll
+      for (int wv = 0; wv < kPlanThreads / 64; ++wv) {
+        if (wv < NW) wcnt[(16 + wv) * 8 + tid] = a;
+        a += c[wv];
+      }
+      wcnt[(16 + NW) * 8 + tid] = a;
+    }
+    __syncthreads();
+    unsigned start = 0;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int sq = 16 * (q & 1);
+      const unsigned own = (inc[q >> 1] - cw[q >> 1] + wcnt[(16 + wave) * 8 + (q >> 1)]) >> sq & 0xffffu;
+      offs[17 * tid + q] = start + own;
+      start += wcnt[(16 + NW) * 8 + (q >> 1)] >> sq & 0xffffu;
+    }
+#pragma unroll
+    for (int u = 0; u < kPlanIpt; ++u) slot[plan_slot((int)offs[17 * tid + d[u]] + r[u])] = w[u];
+    __syncthreads();  // slots placed; the wave counts are free again
+  }
+  for (int i = tid; i < n; i += T) order[i] = (int32_t)(slot[plan_slot(i)] & ((1u << kPlanIdxBits) - 1));
 }
 
 // Solid harmonics of every receiver about its tile centre, fp64 [n][nk].
@@ -188,7 +431,7 @@ __global__ __launch_bounds__(256) void k_plan_node_sh(DevTables t, const float* 
   if (i >= n) return;
   const TileGridDev g = *gp;
   double ox, oy, oz;
-  tile_centre(g, tile_of[i] % g.ncell, ox, oy, oz);
+  tile_centre(g, tile_of[i], ox, oy, oz);
   double* Ri = R + (size_t)i * NK;
   sh_all<L>(t, (double)pos[3 * i] - ox, (double)pos[3 * i + 1] - oy, (double)pos[3 * i + 2] - oz,
             [&](int k, double v) { Ri[k] = v; });
@@ -212,7 +455,7 @@ __global__ __launch_bounds__(256) void k_plan_edge_sh(DevTables t, const float* 
     const TileGridDev g = *gp;
     const int i = clamp_node(rows[e], n), j = clamp_node(col[e], n);
     double ox, oy, oz;
-    tile_centre(g, tile_of[i] % g.ncell, ox, oy, oz);
+    tile_centre(g, tile_of[i], ox, oy, oz);
     float* b = buf + threadIdx.x * NKP;
     sh_all<L>(t, (double)pos[3 * j] - ox, (double)pos[3 * j + 1] - oy, (double)pos[3 * j + 2] - oz,
               [&](int k, double v) { b[k] = (float)v; });
@@ -275,6 +518,31 @@ hipError_t launch_plan_bbox(const float* pos, const int32_t* graph_id, int n, in
   return hipGetLastError();
 }
 
+hipError_t launch_plan_init(int* stats, unsigned* dmin, hipStream_t s) {
+  k_plan_init<<<1, 64, 0, s>>>(stats, dmin);
+  return hipGetLastError();
+}
+
+hipError_t launch_plan_small(const float* pos, const int32_t* graph_id, int n, const unsigned* dmin, double side,
+                             double dmin_scale, int* stats, TileGridDev* grid, int32_t* tile_of, int32_t* order,
+                             hipStream_t s) {
+  if (n <= 0 || n > kPlanSmallMax) return hipErrorInvalidValue;
+  static_assert(kPlanSmallMax <= kPlanIpt * kPlanThreads, "one workgroup holds the small plan");
+  static_assert(kPlanSmallMax <= (1 << kPlanIdxBits), "a slot holds the atom index");
+  static_assert(kPlanThreads / 64 + 17 <= 33, "wave counts and their prefix fit 33 rows of 8");
+  // 16 T >= n, whole waves
+  const int T = std::max(64, (n + 64 * kPlanIpt - 1) / (64 * kPlanIpt) * 64);
+  const int ns = kPlanIpt * T;
+  const size_t lds = sizeof(uint64_t) * (size_t)(ns + ns / kPlanIpt) + sizeof(unsigned) * (17 * (size_t)T + 33 * 8);
+  if (lds > 32768)
+    if (hipError_t e = hipFuncSetAttribute((const void*)k_plan_small, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)lds);
+        e != hipSuccess)
+      return e;
+  k_plan_small<<<1, T, lds, s>>>(pos, graph_id, n, dmin, side, dmin_scale, stats, grid, tile_of, order);
+  return hipGetLastError();
+}
+
 hipError_t launch_plan_centre(const int* stats, double* origin, hipStream_t s) {
   k_plan_centre<<<1, 64, 0, s>>>(stats, origin);
   return hipGetLastError();
@@ -288,9 +556,9 @@ hipError_t launch_plan_dmin(const float* pos, const int32_t* rows, const int32_t
   return hipGetLastError();
 }
 
-hipError_t launch_plan_grid(const int* stats, const unsigned* dmin, double side, double dmin_scale, bool graphs,
+hipError_t launch_plan_grid(const int* stats, const unsigned* dmin, double side, double dmin_scale,
                             TileGridDev* grid, hipStream_t s) {
-  k_plan_grid<<<1, 64, 0, s>>>(stats, dmin, side, dmin_scale, graphs, grid);
+  k_plan_grid<<<1, 64, 0, s>>>(stats, dmin, side, dmin_scale, grid);
   return hipGetLastError();
 }
 

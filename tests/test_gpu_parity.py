@@ -187,6 +187,33 @@ def test_conv_edge_cases(e2f, ctx):
         assert np.all(got == 0)
 
 
+@pytest.mark.parametrize("copies", [1, 2])
+def test_conv_graph_ids_sparse_and_interleaved(e2f, ctx, copies):
+    # the receiver order's keys with graph ids near 2^31, not contiguous in
+    # the atom order: one copy of the 256 molecules (7,680 atoms, the plan of
+    # one workgroup, whose sort then runs over the id's digits) and two
+    # copies side by side (15,360 atoms, the plan's large path)
+    base, _, _, _ = case("molecules256x30_L3")
+    wl = base.workload
+    n0 = base.pos.shape[0]
+    pos = np.concatenate([base.pos + np.float32(40.0 * c) for c in range(copies)])
+    old = np.concatenate([base.graph_id + 256 * c for c in range(copies)]).astype(np.int64)
+    gid = (2_147_000_000 - old * 4_000_001).astype(np.int32)
+    feat = np.concatenate([base.feat] * copies)
+    species = np.concatenate([base.species] * copies)
+    perm = np.random.default_rng(77).permutation(n0 * copies)
+    pos, gid, feat, species = pos[perm], gid[perm], feat[perm], species[perm]
+    rp, ci = o.neighbor_list(pos, wl.cutoff, gid)
+    alpha = syn.attention_weights(pos, species, rp, ci, wl.heads, wl.cutoff, wl.species, wl.seed)
+    r = sample_rows(pos.shape[0], 128, seed=copies)
+    ref = o.conv_edge(wl.lmax, wl.heads, pos, feat, rp, ci, alpha, base.path_w, rows=r)
+    got = e2f.e2f_wigner6j_conv_forward(ctx, gpu(pos), gpu(feat), gpu(rp), gpu(ci), gpu(alpha), wl.lmax, wl.heads,
+                                        wl.cutoff, path_w=base.path_w, graph_id=gpu(gid)).cpu().numpy()
+    err = o.max_rel_err(got[r], ref, wl.lmax)
+    print("sparse graph ids, %d atoms: err %.3e" % (pos.shape[0], err))
+    assert err <= TOL_F32
+
+
 @pytest.mark.parametrize("C,H", [(12, 3), (48, 4), (256, 8)])
 def test_mixing_channel_counts(e2f, ctx, C, H):
     # channel mixing on both kernels: MFMA (C a multiple of 16 up to 128) and
