@@ -697,12 +697,13 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
   const bool small_plan = n <= kPlanSmallMax;
   if (!small_plan) E2F_TIMED("bbox", launch_plan_bbox(pos, graph_id, n, stats, ynorm ? dmin : nullptr, s));
   else if (ynorm) E2F_TIMED("bbox", launch_plan_init(stats, dmin, s));
-  E2F_TIMED("tile_plan", launch_plan_edge_rows(row_ptr, n, n_edges, erows, s));
+  // (the receiver of every edge, and in the same launch the weights
+  // head-major unless y_norm scales them per filter degree)
+  E2F_TIMED("tile_plan", launch_plan_edge_rows(row_ptr, n, n_edges, erows, ynorm ? nullptr : alpha, H,
+                                               ynorm ? nullptr : alpha_hm, s));
   if (ynorm) {
     E2F_TIMED("alpha_hm", launch_plan_dmin(pos, erows, col_idx, n, n_edges, dmin, s));
     E2F_TIMED("alpha_hm", launch_alpha_dnorm(pos, nullptr, col_idx, alpha, n, n_edges, H, L, erows, alpha_hm, s));
-  } else if (alpha) {
-    E2F_TIMED("alpha_hm", launch_alpha_head_major(alpha, n_edges, H, alpha_hm, s));
   }
   const double side = (p->tile_side > 0.0f ? (double)p->tile_side : kTileCutoffs[L] * (double)p->cutoff) * kGrid;
   if (small_plan) {

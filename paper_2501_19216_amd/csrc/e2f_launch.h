@@ -61,7 +61,10 @@ hipError_t launch_plan_order(const float* pos, const int32_t* graph_id, int n, c
 hipError_t launch_plan_sh(const DevTables& t, const float* pos, const int32_t* rows, const int32_t* col, int n,
                           int64_t n_edges, const int32_t* tile_of, const TileGridDev* grid, double* Rr, float* Re,
                           hipStream_t s);
-hipError_t launch_plan_edge_rows(const int64_t* row_ptr, int n, int64_t n_edges, int32_t* rows, hipStream_t s);
+// rows [E] = the receiver of every edge; with alpha (and alpha_hm), the same
+// launch copies the weights [E][H] head-major into alpha_hm [H][E]
+hipError_t launch_plan_edge_rows(const int64_t* row_ptr, int n, int64_t n_edges, int32_t* rows, const float* alpha,
+                                 int H, float* alpha_hm, hipStream_t s);
 hipError_t launch_fill(float* p, int64_t count, float v, hipStream_t s);
 // *bad (device int) = 0, or the bits of k_validate_*: 1 row_ptr[0] != 0,
 // 2 a decreasing row_ptr, 4 row_ptr[n] != n_edges, 8 a sender outside [0, n)

@@ -421,40 +421,36 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_small(const float* __rest
   for (int i = tid; i < n; i += T) order[i] = (int32_t)(slot[plan_slot(i)] & ((1u << kPlanIdxBits) - 1));
 }
 
-// Solid harmonics of every receiver about its tile centre, fp64 [n][nk].
+// Solid harmonics about each receiver's tile centre, in one launch: blocks
+// below eblocks take 256 consecutive edges each, the harmonics of the
+// edge's sender in fp32, Re [E][nk] in CSR order (rows: the receiver of
+// every edge; a thread per edge, whose values pass through LDS so that the
+// workgroup stores its 256 rows as one contiguous block); the blocks after
+// take 256 receivers each, their own harmonics in fp64, R [n][nk].
 template <int L>
-__global__ __launch_bounds__(256) void k_plan_node_sh(DevTables t, const float* __restrict__ pos, int n,
-                                                      const int32_t* __restrict__ tile_of,
-                                                      const TileGridDev* __restrict__ gp, double* __restrict__ R) {
-  constexpr int NK = (L + 1) * (L + 1);
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const TileGridDev g = *gp;
-  double ox, oy, oz;
-  tile_centre(g, tile_of[i], ox, oy, oz);
-  double* Ri = R + (size_t)i * NK;
-  sh_all<L>(t, (double)pos[3 * i] - ox, (double)pos[3 * i + 1] - oy, (double)pos[3 * i + 2] - oz,
-            [&](int k, double v) { Ri[k] = v; });
-}
-
-// Solid harmonics of every edge's sender about its receiver's tile centre,
-// fp32 [E][nk] in CSR order.  A thread per edge (rows: the receiver of every
-// edge), 256 consecutive edges per workgroup; the values pass through LDS so
-// that the workgroup stores its 256 rows as one contiguous block.
-template <int L>
-__global__ __launch_bounds__(256) void k_plan_edge_sh(DevTables t, const float* __restrict__ pos,
-                                                      const int32_t* __restrict__ rows,
-                                                      const int32_t* __restrict__ col, int n, int64_t n_edges,
-                                                      const int32_t* __restrict__ tile_of,
-                                                      const TileGridDev* __restrict__ gp, float* __restrict__ Re) {
+__global__ __launch_bounds__(256) void k_plan_sh(DevTables t, const float* __restrict__ pos,
+                                                 const int32_t* __restrict__ rows, const int32_t* __restrict__ col,
+                                                 int n, int64_t n_edges, int64_t eblocks,
+                                                 const int32_t* __restrict__ tile_of,
+                                                 const TileGridDev* __restrict__ gp, float* __restrict__ Re,
+                                                 double* __restrict__ R) {
   constexpr int NK = (L + 1) * (L + 1), NKP = NK | 1;  // odd row stride: conflict-free LDS stores
   __shared__ float buf[256 * NKP];
+  const TileGridDev g = *gp;
+  double ox, oy, oz;
+  if (blockIdx.x >= eblocks) {  // a receiver's own harmonics (uniform over the workgroup)
+    const int i = (int)((blockIdx.x - eblocks) * 256) + threadIdx.x;
+    if (i >= n) return;
+    tile_centre(g, tile_of[i], ox, oy, oz);
+    double* Ri = R + (size_t)i * NK;
+    sh_all<L>(t, (double)pos[3 * i] - ox, (double)pos[3 * i + 1] - oy, (double)pos[3 * i + 2] - oz,
+              [&](int k, double v) { Ri[k] = v; });
+    return;
+  }
   const int64_t e0 = (int64_t)blockIdx.x * 256, e = e0 + threadIdx.x;
   const int cnt = (int)min((int64_t)256, n_edges - e0);
   if (e < n_edges) {
-    const TileGridDev g = *gp;
     const int i = clamp_node(rows[e], n), j = clamp_node(col[e], n);
-    double ox, oy, oz;
     tile_centre(g, tile_of[i], ox, oy, oz);
     float* b = buf + threadIdx.x * NKP;
     sh_all<L>(t, (double)pos[3 * j] - ox, (double)pos[3 * j + 1] - oy, (double)pos[3 * j + 2] - oz,
@@ -465,10 +461,20 @@ __global__ __launch_bounds__(256) void k_plan_edge_sh(DevTables t, const float* 
   for (int q = threadIdx.x; q < cnt * NK; q += 256) dst[q] = buf[(q / NK) * NKP + q % NK];
 }
 
-// The receiver of every edge (rows [E]), clamped like every CSR read.
-// A wave per receiver, its lanes over the receiver's edges.
+// The receiver of every edge (rows [E]), clamped like every CSR read: a
+// wave per receiver, its lanes over the receiver's edges, in the blocks
+// below rblocks; with alpha, the blocks after copy the attention weights
+// [E][H] head-major, alpha_hm [H][E] (a thread per edge).
 __global__ __launch_bounds__(256) void k_plan_edge_rows(const int64_t* __restrict__ row_ptr, int n, int64_t n_edges,
-                                                        int32_t* __restrict__ rows) {
+                                                        int32_t* __restrict__ rows, int64_t rblocks,
+                                                        const float* __restrict__ alpha, int H,
+                                                        float* __restrict__ alpha_hm) {
+  if (blockIdx.x >= rblocks) {
+    const int64_t e = (blockIdx.x - rblocks) * 256 + threadIdx.x;
+    if (e >= n_edges) return;
+    for (int h = 0; h < H; ++h) alpha_hm[(int64_t)h * n_edges + e] = alpha[e * H + h];
+    return;
+  }
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (i >= n) return;
   int64_t e0, e1;
@@ -582,14 +588,12 @@ hipError_t launch_plan_sh(const DevTables& t, const float* pos, const int32_t* r
                           int64_t n_edges, const int32_t* tile_of, const TileGridDev* grid, double* Rr, float* Re,
                           hipStream_t s) {
   if (n == 0) return hipSuccess;
-  const int64_t eblocks = (n_edges + 255) / 256;
-  if (eblocks > 0x7fffffff) return hipErrorInvalidValue;
+  const int64_t eblocks = (n_edges + 255) / 256, blocks = eblocks + (n + 255) / 256;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
   switch (t.L) {
-#define E2F_SH(LL)                                                                                          \
-  case LL:                                                                                                  \
-    k_plan_node_sh<LL><<<(n + 255) / 256, 256, 0, s>>>(t, pos, n, tile_of, grid, Rr);                       \
-    if (eblocks > 0)                                                                                        \
-      k_plan_edge_sh<LL><<<(unsigned)eblocks, 256, 0, s>>>(t, pos, rows, col, n, n_edges, tile_of, grid, Re); \
+#define E2F_SH(LL)                                                                                             \
+  case LL:                                                                                                     \
+    k_plan_sh<LL><<<(unsigned)blocks, 256, 0, s>>>(t, pos, rows, col, n, n_edges, eblocks, tile_of, grid, Re, Rr); \
     break;
     E2F_SH(0) E2F_SH(1) E2F_SH(2) E2F_SH(3) E2F_SH(4) E2F_SH(5) E2F_SH(6)
 #undef E2F_SH
@@ -598,8 +602,13 @@ hipError_t launch_plan_sh(const DevTables& t, const float* pos, const int32_t* r
   return hipGetLastError();
 }
 
-hipError_t launch_plan_edge_rows(const int64_t* row_ptr, int n, int64_t n_edges, int32_t* rows, hipStream_t s) {
-  if (n > 0) k_plan_edge_rows<<<(n + 3) / 4, 256, 0, s>>>(row_ptr, n, n_edges, rows);
+hipError_t launch_plan_edge_rows(const int64_t* row_ptr, int n, int64_t n_edges, int32_t* rows, const float* alpha,
+                                 int H, float* alpha_hm, hipStream_t s) {
+  const int64_t rblocks = (n + 3) / 4, ablocks = alpha && alpha_hm ? (n_edges + 255) / 256 : 0;
+  if (rblocks + ablocks > 0x7fffffff) return hipErrorInvalidValue;
+  if (rblocks + ablocks > 0)
+    k_plan_edge_rows<<<(unsigned)(rblocks + ablocks), 256, 0, s>>>(row_ptr, n, n_edges, rows, rblocks,
+                                                                  ablocks ? alpha : nullptr, H, alpha_hm);
   return hipGetLastError();
 }
 
