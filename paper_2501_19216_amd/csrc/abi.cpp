@@ -299,6 +299,7 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
   push_array(blob, o, t.ag_ptr);          // oag
   push_array(blob, o, t.ag_idx);          // oag + 1
   push_array(blob, o, t.ag_coef);         // oag + 2
+  push_array(blob, o, t.sh_dense);        // oag + 3
   void* mem = nullptr;
   E2F_HIP(hipMalloc(&mem, blob.size()));
   ctx->table_mem[L] = mem;
@@ -335,6 +336,7 @@ e2f_status upload_tables(e2f_ctx* ctx, int L) {
   d.ag_ptr = (const int*)(b + o[oag]);
   d.ag_idx = (const int*)(b + o[oag + 1]);
   d.ag_coef = (const float*)(b + o[oag + 2]);
+  d.sh_dense = (const double*)(b + o[oag + 3]);
   ctx->rcf_k[L].assign(L + 1, nullptr);
   ctx->rcf_off[L].assign(L + 1, nullptr);
   ctx->rcf_meta[L].assign(L + 1, nullptr);

@@ -43,6 +43,11 @@ constexpr int rc_qstride(int nk) {
 // thread t walks entries k = 0..k[c]-1 at index off[c] + k*256 + t, each
 // adding coef * R[ridx] and, on the last entry of a slot, storing the sum to
 // LDS position dest.  meta packs dest (bits 0-19), ridx (20-26), last (31).
+// Monomials of degree l, and the offset of degree l's block in the dense
+// solid-harmonic table (rows 2l'+1 by columns sh_monos(l') for every l' < l).
+constexpr int sh_monos(int l) { return (l + 1) * (l + 2) / 2; }
+constexpr int sh_dense_off(int l) { return l <= 0 ? 0 : sh_dense_off(l - 1) + (2 * l - 1) * sh_monos(l - 1); }
+
 struct Schedule {
   std::vector<int> k, off;
   std::vector<int> meta;
@@ -62,6 +67,10 @@ struct LayerTables {
   std::vector<int> sh_ptr;          // [nk+1]
   std::vector<int> sh_pow;          // packed ex | ey<<4 | ez<<8
   std::vector<double> sh_coef;
+  // the same polynomials dense per degree l: rows m < 2l+1, columns the
+  // monomials x^ex y^ey z^(l-ex-ey) in (ex, ey) order, ex and ey ascending;
+  // the block of degree l starts at sh_dense_off(l)
+  std::vector<double> sh_dense;
   // j-side per-node matrix M: row r of T has (2a+1) slots starting at m_rowoff[r]
   std::vector<int> m_rowoff;        // [dimT+1]
   std::vector<int> m_ptr;           // [nslots+1] entries of each slot
@@ -199,6 +208,7 @@ struct DevTables {
   int L, nk, dimT;
   const int* a_row_start;
   const int* sh_ptr; const int* sh_pow; const double* sh_coef;
+  const double* sh_dense;  // LayerTables::sh_dense
   const int* m_rowoff; const int* m_ptr; const int* m_ridx; const double* m_coef;
   const int* q_ncol; const int* q_coloff; const int* q_cols; const int* q_slotoff;
   const int* q_ptr; const int* q_ridx; const double* q_coef; // q_coef includes path weights

@@ -71,6 +71,38 @@ __device__ __forceinline__ void sh_all(const DevTables& t, double x, double y, d
   }
 }
 
+// The same harmonics from the dense per-degree table: the powers of x, y
+// and z once, then per degree l the monomials x^ex y^ey z^(l-ex-ey) at fixed
+// register positions and each component as their dot product with its row
+// (the table's loads are uniform over the wave).  Every loop bound is a
+// constant of L, so the whole evaluation unrolls into straight-line fp64
+// multiply-adds.
+template <int L, typename Sink>
+__device__ __forceinline__ void sh_dense(const DevTables& t, double x, double y, double z, Sink sink) {
+  double px[L + 1], py[L + 1], pz[L + 1];
+  px[0] = py[0] = pz[0] = 1.0;
+#pragma unroll
+  for (int a = 1; a <= L; ++a) px[a] = px[a - 1] * x, py[a] = py[a - 1] * y, pz[a] = pz[a - 1] * z;
+  const double* __restrict__ c = t.sh_dense;
+#pragma unroll
+  for (int l = 0; l <= L; ++l) {
+    double mono[sh_monos(L)];
+    int q = 0;
+#pragma unroll
+    for (int ex = 0; ex <= l; ++ex)
+#pragma unroll
+      for (int ey = 0; ey <= l - ex; ++ey) mono[q++] = px[ex] * py[ey] * pz[l - ex - ey];
+    const int M = sh_monos(l), off = sh_dense_off(l);
+#pragma unroll
+    for (int m = 0; m < 2 * l + 1; ++m) {
+      double acc = 0.0;
+#pragma unroll
+      for (int k = 0; k < M; ++k) acc = fma(c[off + m * M + k], mono[k], acc);
+      sink(l * l + m, acc);
+    }
+  }
+}
+
 __global__ void k_plan_init(int* __restrict__ st, unsigned* __restrict__ dmin) {
   if (threadIdx.x < 3) st[threadIdx.x] = INT_MAX;
   else if (threadIdx.x < 6) st[threadIdx.x] = INT_MIN;
@@ -443,8 +475,8 @@ __global__ __launch_bounds__(256) void k_plan_sh(DevTables t, const float* __res
     if (i >= n) return;
     tile_centre(g, tile_of[i], ox, oy, oz);
     double* Ri = R + (size_t)i * NK;
-    sh_all<L>(t, (double)pos[3 * i] - ox, (double)pos[3 * i + 1] - oy, (double)pos[3 * i + 2] - oz,
-              [&](int k, double v) { Ri[k] = v; });
+    sh_dense<L>(t, (double)pos[3 * i] - ox, (double)pos[3 * i + 1] - oy, (double)pos[3 * i + 2] - oz,
+                [&](int k, double v) { Ri[k] = v; });
     return;
   }
   const int64_t e0 = (int64_t)blockIdx.x * 256, e = e0 + threadIdx.x;
@@ -453,8 +485,8 @@ __global__ __launch_bounds__(256) void k_plan_sh(DevTables t, const float* __res
     const int i = clamp_node(rows[e], n), j = clamp_node(col[e], n);
     tile_centre(g, tile_of[i], ox, oy, oz);
     float* b = buf + threadIdx.x * NKP;
-    sh_all<L>(t, (double)pos[3 * j] - ox, (double)pos[3 * j + 1] - oy, (double)pos[3 * j + 2] - oz,
-              [&](int k, double v) { b[k] = (float)v; });
+    sh_dense<L>(t, (double)pos[3 * j] - ox, (double)pos[3 * j + 1] - oy, (double)pos[3 * j + 2] - oz,
+                [&](int k, double v) { b[k] = (float)v; });
   }
   __syncthreads();
   float* dst = Re + e0 * NK;

@@ -245,6 +245,17 @@ LayerTables build_layer_tables(int L) {
     }
     t.sh_ptr.push_back((int)t.sh_coef.size());
   }
+  t.sh_dense.assign(sh_dense_off(L + 1), 0.0);
+  for (int l = 0; l <= L; ++l)
+    for (int m = 0; m < 2 * l + 1; ++m)
+      for (auto& kv : R[l * l + m]) {
+        auto [ex, ey, ez] = kv.first;
+        if (ex + ey + ez != l) continue;  // never: R^(l) is homogeneous of degree l by its construction
+        int q = 0;  // column of (ex, ey): the monomials of smaller ex, then ey
+        for (int a = 0; a < ex; ++a) q += l - a + 1;
+        q += ey;
+        t.sh_dense[sh_dense_off(l) + m * sh_monos(l) + q] += kv.second;
+      }
 
   // ---- j-side blocks, sorted by (a, b, d)
   int toff = 0;
