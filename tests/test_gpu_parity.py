@@ -214,6 +214,29 @@ def test_conv_graph_ids_sparse_and_interleaved(e2f, ctx, copies):
     assert err <= TOL_F32
 
 
+@pytest.mark.parametrize("n", [2, 3, 511, 512, 8192, 8193])
+def test_conv_plan_sizes(e2f, ctx, n):
+    # the forward's plan at the sizes that change its shape: the one-workgroup
+    # plan (up to 8,192 atoms; 64 threads below 512 atoms, 1,024 at 8,192) and
+    # the multi-kernel plan above it, on random positions at 0.1 per A^3
+    rng = np.random.default_rng(500 + n)
+    L, C, H, cut = 2, 16, 2, 4.5
+    box = max((n / 0.1) ** (1.0 / 3.0), 3.0)
+    pos = syn.quantize(rng.uniform(0, box, size=(n, 3)))
+    rp, ci = o.neighbor_list(pos, cut)
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    alpha = rng.uniform(0.05, 1.0, size=(len(ci), H)).astype(np.float32)
+    w = rng.uniform(0.2, 1.0, size=(L + 1) ** 3)
+    r = sample_rows(n, 64, seed=n)
+    ref = o.conv_edge(L, H, pos, feat, rp, ci, alpha, w, rows=r)
+    got = e2f.e2f_wigner6j_conv_forward(ctx, gpu(pos), gpu(feat), gpu(rp), gpu(ci), gpu(alpha), L, H, cut,
+                                        path_w=w).cpu().numpy()
+    scale = max(float(np.max(np.abs(ref))), 1e-30)
+    err = o.max_rel_err(got[r], ref, L) if len(ci) else float(np.max(np.abs(got))) / scale
+    print("plan sizes: n %d edges %d err %.3e" % (n, len(ci), err))
+    assert err <= TOL_F32
+
+
 @pytest.mark.parametrize("C,H", [(12, 3), (48, 4), (256, 8)])
 def test_mixing_channel_counts(e2f, ctx, C, H):
     # channel mixing on both kernels: MFMA (C a multiple of 16 up to 128) and
