@@ -358,7 +358,7 @@ def main():
     ap.add_argument("--fig2-panels", default="", help="comma-separated subset of the panels b.i,b.ii,b.iii,c,d")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path (no sharding, no collectives).",
+        print("bench.py runs on one GPU only: the library has no multi-GPU path (no sharding, no collectives).",
               file=sys.stderr)
         sys.exit(2)
 
