@@ -30,8 +30,9 @@ double wigner6j(int j1, int j2, int j3, int j4, int j5, int j6);
 constexpr int kSchedThreads = 256;
 // Rows of T per chunk of the recouple's per-node matrix: 192 at L <= 4 (a
 // 37 KB tile, four workgroups per CU: 1.18 vs 1.20 ms with 256 rows and three),
-// 128 above (two workgroups per CU).
-constexpr int rc_rows(int nk) { return nk > 25 ? 128 : 192; }
+// 128 at L = 5, 120 at L = 6 (a 38.4 KB tile: four workgroups per CU instead
+// of three with 128 rows, 46.9 vs 49.7 ms at 200k atoms).
+constexpr int rc_rows(int nk) { return nk > 36 ? 120 : (nk > 25 ? 128 : 192); }
 // Row stride (floats) of the recouple's per-node matrix tile in LDS: the
 // 16*ceil(nk/16) used columns padded to 16 mod 32, so the MFMA operand reads
 // of 4 rows x 16 columns fall in distinct banks.
