@@ -593,37 +593,39 @@ __device__ __forceinline__ void stage_chunk(const float* __restrict__ Re, const 
 // The j-side coupling of one receiver's G (in LDS, rows of GS floats) into
 // its S rows of one head (Sr, rows of dh floats), from a thread-balanced
 // schedule: group g walks its entries k*cgroups + g, four channels per
-// thread (tq), four entries at a time (their schedule reads, then their G
+// thread (tq), CB entries at a time (their schedule reads, then their G
 // reads, then the sums; past ck: entry 0 with coefficient 0, never the last
 // of a row).  Packed entries (PK) hold a 9-bit row and the index of their
 // coefficient in coef; otherwise coef runs beside meta and the row has 12
-// bits.
-template <bool PK>
+// bits.  CB = 8 above L = 4, where the schedule (120 KB at L = 6) is read
+// from L2 by every receiver and head: half the round trips (234.4 vs 237.7
+// ms at 200k atoms, L = 6); 4 below (no gain there).
+template <bool PK, int CB>
 __device__ __forceinline__ void couple_rows(const int* __restrict__ meta, const float* __restrict__ coef, int ck,
                                             int cgroups, int g, int tq, const float* G, int GS, int dh,
                                             float* __restrict__ Sr) {
   float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int k0 = 0; k0 < ck; k0 += 4) {
-    int m[4];
-    float c[4];
-    float4 gv[4];
+  for (int k0 = 0; k0 < ck; k0 += CB) {
+    int m[CB];
+    float c[CB];
+    float4 gv[CB];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < CB; ++u) {
       const bool ok = k0 + u < ck;
       m[u] = ok ? meta[(k0 + u) * cgroups + g] : 0;
       if (!PK) c[u] = ok ? coef[(k0 + u) * cgroups + g] : 0.0f;
     }
     if (PK) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < CB; ++u) {
         const float cv = coef[(m[u] >> 21) & 1023];
         c[u] = k0 + u < ck ? cv : 0.0f;
       }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) gv[u] = *(const float4*)(G + ((m[u] >> 6) & 63) * GS + (m[u] & 63) * dh + 4 * tq);
+    for (int u = 0; u < CB; ++u) gv[u] = *(const float4*)(G + ((m[u] >> 6) & 63) * GS + (m[u] & 63) * dh + 4 * tq);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < CB; ++u) {
       v.x += c[u] * gv[u].x, v.y += c[u] * gv[u].y, v.z += c[u] * gv[u].z, v.w += c[u] * gv[u].w;
       if (m[u] < 0) {
         *(float4*)(Sr + ((m[u] >> 12) & (PK ? 511 : 4095)) * dh + 4 * tq) = v;
@@ -774,15 +776,16 @@ __global__ __launch_bounds__(LB) void k_outer_agg(DevTables t, const float* __re
   // j-side coupling: S[row][tt] = sum over the row's entries of C * G[be][q dh + tt]
   float* Sr = S + (size_t)r * t.dimT * C + (size_t)h * t.dimT * dh;
   const int dq = dh >> 2, g = threadIdx.x / dq, tq = threadIdx.x % dq;
+  constexpr int CB = L > 4 ? 8 : 4;  // schedule entries per batch
   if (g < cgroups) {
     if (work_floats > 0 && ntab > 0)
-      couple_rows<true>((const int*)(sm + work_floats), sm + work_floats + ck * cgroups, ck, cgroups, g, tq, G, GS,
-                        dh, Sr);
+      couple_rows<true, CB>((const int*)(sm + work_floats), sm + work_floats + ck * cgroups, ck, cgroups, g, tq, G,
+                            GS, dh, Sr);
     else if (work_floats > 0)
-      couple_rows<false>((const int*)(sm + work_floats), sm + work_floats + ck * cgroups, ck, cgroups, g, tq, G,
-                         GS, dh, Sr);
+      couple_rows<false, CB>((const int*)(sm + work_floats), sm + work_floats + ck * cgroups, ck, cgroups, g, tq,
+                             G, GS, dh, Sr);
     else
-      couple_rows<false>(cmeta, ccoef, ck, cgroups, g, tq, G, GS, dh, Sr);
+      couple_rows<false, CB>(cmeta, ccoef, ck, cgroups, g, tq, G, GS, dh, Sr);
   }
   }  // receivers of the workgroup
 }
