@@ -90,6 +90,11 @@ struct e2f_ctx {
   };
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
+  // a second stream of the context's device and the events that fork work
+  // onto it and join it back (the forward re-lays the features there while
+  // the plan runs on the caller's stream)
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
   // coupling schedules of the aggregation of uncoupled products, per (L, groups)
   struct Couple {
     int k = 0, ntab = 0;
@@ -697,6 +702,20 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
   // (a graph of at most kPlanSmallMax atoms takes the whole plan in one
   // workgroup: box, grid, tiles and the sorted order in one launch)
   const bool small_plan = n <= kPlanSmallMax;
+  // the fused form's copy of the features needs only the features: it is
+  // made on the context's second stream while the plan runs on this one
+  // (the fork waits for the work already queued here; the join comes before
+  // the aggregation)
+  float* featq = (float*)(ws + f.featq);
+  if (fsplit > 0) {
+    E2F_HIP(hipEventRecord(ctx->fork, s));
+    E2F_HIP(hipStreamWaitEvent(ctx->side, ctx->fork, 0));
+    {
+      hipStream_t s = ctx->side;  // (E2F_TIMED records on s)
+      E2F_TIMED("feat_qmajor", launch_feat_qmajor(L, feat, n, C, featq, s));
+    }
+    E2F_HIP(hipEventRecord(ctx->join, ctx->side));
+  }
   if (!small_plan) E2F_TIMED("bbox", launch_plan_bbox(pos, graph_id, n, stats, ynorm ? dmin : nullptr, s));
   else if (ynorm) E2F_TIMED("bbox", launch_plan_init(stats, dmin, s));
   // (the receiver of every edge, and in the same launch the weights
@@ -722,8 +741,7 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
   // at a time in the workspace)
   const int64_t slice = std::min<int64_t>(n, (int64_t)((workspace_bytes - f.fixed) / f.s_row));
   int64_t slices = 0;
-  float* featq = (float*)(ws + f.featq);
-  if (fsplit > 0) E2F_TIMED("feat_qmajor", launch_feat_qmajor(L, feat, n, C, featq, s));
+  if (fsplit > 0) E2F_HIP(hipStreamWaitEvent(s, ctx->join, 0));
   for (int64_t q0 = 0; q0 < n; q0 += slice, ++slices) {
     const int nb = (int)std::min<int64_t>(slice, n - q0);
     const int32_t* ord = order + q0;
@@ -798,6 +816,10 @@ e2f_status e2f_create(int lmax_max, int device, e2f_ctx** out) {
         st = fail(E2F_EDEVICE, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
       }
     }
+    if (st == E2F_OK && (hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking) != hipSuccess ||
+                         hipEventCreateWithFlags(&ctx->fork, hipEventDisableTiming) != hipSuccess ||
+                         hipEventCreateWithFlags(&ctx->join, hipEventDisableTiming) != hipSuccess))
+      st = fail(E2F_EDEVICE, "side stream or its events: %s", hipGetErrorString(hipGetLastError()));
     if (st != E2F_OK) {
       e2f_destroy(ctx);
       return st;
@@ -835,6 +857,9 @@ void e2f_destroy(e2f_ctx* ctx) {
       ctx->pool.push_back(r.stop);
     }
     for (hipEvent_t e : ctx->pool) (void)hipEventDestroy(e);
+    if (ctx->fork) (void)hipEventDestroy(ctx->fork);
+    if (ctx->join) (void)hipEventDestroy(ctx->join);
+    if (ctx->side) (void)hipStreamDestroy(ctx->side);
     if (ctx->stats) (void)hipFree(ctx->stats);
     if (ctx->pinned) (void)hipHostFree(ctx->pinned);
     if (ctx->pinned_plan) (void)hipHostFree(ctx->pinned_plan);
