@@ -69,6 +69,9 @@ struct e2f_ctx {
     const int* f_ptr = nullptr;
     const int* f_idx = nullptr;
     const double* f_coef = nullptr;
+    // the same per filter degree f (alpha / D^f), L + 1 tables
+    std::vector<const int*> ff_ptr, ff_idx;
+    std::vector<const double*> ff_coef;
   };
   std::vector<std::vector<CoefSet>> coefs;
   // per L and filter degree f: the recouple schedule restricted to b + u = f
@@ -414,6 +417,13 @@ e2f_status coef_of(e2f_ctx* ctx, int L, const std::vector<double>& w, bool allow
   push_array(blob, o, ft.ptr);
   push_array(blob, o, ft.idx);
   push_array(blob, o, ft.coef);
+  std::vector<FuseTable> ftf;  // o[8 + L + 3f] .. o[10 + L + 3f]
+  for (int f = 0; f <= L && !ft.coef.empty(); ++f) {
+    ftf.push_back(fuse_table(t, w, f));
+    push_array(blob, o, ftf.back().ptr);
+    push_array(blob, o, ftf.back().idx);
+    push_array(blob, o, ftf.back().coef);
+  }
   if (sets.size() >= kMaxCoefSets) {  // the oldest set may still be read by queued work
     E2F_HIP(hipDeviceSynchronize());
     E2F_HIP(hipFree(sets.front().mem));
@@ -437,6 +447,11 @@ e2f_status coef_of(e2f_ctx* ctx, int L, const std::vector<double>& w, bool allow
     c.f_ptr = (const int*)((char*)mem + o[5 + L]);
     c.f_idx = (const int*)((char*)mem + o[6 + L]);
     c.f_coef = (const double*)((char*)mem + o[7 + L]);
+    for (int f = 0; f <= L; ++f) {
+      c.ff_ptr.push_back((const int*)((char*)mem + o[8 + L + 3 * f]));
+      c.ff_idx.push_back((const int*)((char*)mem + o[9 + L + 3 * f]));
+      c.ff_coef.push_back((const double*)((char*)mem + o[10 + L + 3 * f]));
+    }
   }
   sets.push_back(std::move(c));
   out = &sets.back();
@@ -576,7 +591,7 @@ struct FwdLayout {
 
 // The split of each head into channel groups of 16 with which the
 // aggregation applies the recouple itself (L <= 4, head width a multiple of
-// 16, one attention weight per edge and head); 0 where the forward writes S.
+// 16; with y_norm one pass per filter degree); 0 where the forward writes S.
 // The automatic choice takes the fused form at L = 4 once S would outgrow
 // the 256 MiB on-die cache (measured: 1,000 atoms with 32 neighbours at L =
 // 4, S 232 MB, 0.31 ms split vs 0.34 fused; 2,000 atoms with 72, S 465 MB,
@@ -584,7 +599,7 @@ struct FwdLayout {
 // fast or faster at every size).
 int fused_split(const e2f_conv_params* p, int64_t n) {
   const int dh = p->channels / p->heads;
-  if (p->y_norm != 0 || p->form == E2F_FORM_SPLIT || dh % 16 != 0) return 0;
+  if (p->form == E2F_FORM_SPLIT || dh % 16 != 0) return 0;
   if (!outer_fused_supported(p->lmax, p->channels, p->channels / 16, n)) return 0;
   if (p->form == E2F_FORM_FUSED) return dh / 16;
   const double s_bytes = 4.0 * (double)n * (double)node_tp_dim(p->lmax) * p->channels;
@@ -665,7 +680,7 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
     if (!allow_upload && ctx->couple.find(std::make_pair(L, cgroups)) == ctx->couple.end())
       return fail(E2F_EINVAL, "the coupling schedule is not resident on the context; call e2f_wigner6j_prepare first");
     if ((rs = couple_of(ctx, L, cgroups, cpl)) != E2F_OK) return rs;
-  } else if (!cs->f_ptr) {
+  } else if (!cs->f_ptr || (p->y_norm && (int)cs->ff_ptr.size() != L + 1)) {
     return fail(E2F_EDEVICE, "the fused recouple table of L = %d is missing", L);
   }
   if (n == 0) return E2F_OK;
@@ -745,10 +760,19 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
   for (int64_t q0 = 0; q0 < n; q0 += slice, ++slices) {
     const int nb = (int)std::min<int64_t>(slice, n - q0);
     const int32_t* ord = order + q0;
-    if (fsplit > 0) {  // F of the slice, then the aggregation with the recouple applied
+    if (fsplit > 0 && !ynorm) {  // F of the slice, then the aggregation with the recouple applied
       E2F_TIMED("fuse_build", launch_fuse_build(L, cs->f_ptr, cs->f_idx, cs->f_coef, Rr, ord, nb, S, s));
       E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, alpha_hm, n_edges, featq, ord, S, nb, C,
-                                                Hv, hdiv, n, y, s));
+                                                Hv, hdiv, n, false, y, s));
+      continue;
+    }
+    if (fsplit > 0) {  // per filter degree f: F^(f) (the terms b + u = f) and the weights alpha / D^f; f > 0 adds
+      for (int fd = 0; fd <= L; ++fd) {
+        E2F_TIMED("fuse_build", launch_fuse_build(L, cs->ff_ptr[fd], cs->ff_idx[fd], cs->ff_coef[fd], Rr, ord, nb, S,
+                                                  s));
+        E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, alpha_hm + (size_t)fd * H * n_edges,
+                                                  n_edges, featq, ord, S, nb, C, Hv, hdiv, n, fd > 0, y, s));
+      }
       continue;
     }
     if (!ynorm) {

@@ -925,7 +925,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
                                                     const uint4* __restrict__ fhm, const uint2* __restrict__ flo,
                                                     const int32_t* __restrict__ order, const float* __restrict__ F,
                                                     int n, int nrx, int rpw, int C, int H, int hdiv, int n_nodes,
-                                                    float* __restrict__ y) {
+                                                    bool accumulate, float* __restrict__ y) {
   constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
   constexpr int EC = kOuterEdges;
   // staging row stride in words: two words per component (a 64-bit read per
@@ -1218,7 +1218,8 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
         const int row = idx >> 4, t = idx & 15;
         float sum = 0.0f;
         for (int wv = 0; wv < NG; ++wv) sum += yp[(wv * MP + row) * 16 + t];
-        y[((size_t)i * NK + row) * C + h * 16 + t] = sum;
+        float* yo = y + ((size_t)i * NK + row) * C + h * 16 + t;
+        *yo = accumulate ? *yo + sum : sum;  // (accumulate: the sum over the filter degrees of alpha / D^f)
       }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -2273,7 +2274,8 @@ hipError_t launch_feat_qmajor(int L, const float* feat, int n, int C, float* fea
 
 hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, const int32_t* col,
                               const float* alpha_hm, int64_t n_edges, const float* featq, const int32_t* order,
-                              const float* F, int n, int C, int H, int hdiv, int n_nodes, float* y, hipStream_t s) {
+                              const float* F, int n, int C, int H, int hdiv, int n_nodes, bool accumulate, float* y,
+                              hipStream_t s) {
   if (n == 0) return hipSuccess;
   if (!outer_fused_supported(L, C, H, n_nodes)) return hipErrorInvalidValue;
   const int nk = (L + 1) * (L + 1), mp = 16 * ((nk + 15) / 16);
@@ -2295,7 +2297,8 @@ hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, co
   case LL:                                                                                                    \
     if (hipError_t e = allow_lds(k_outer_fused<LL, 512>, lds); e != hipSuccess) return e;                     \
     k_outer_fused<LL, 512><<<(unsigned)blocks, 64 * nw, lds, s>>>(Re, row_ptr, col, alpha_hm, n_edges, fhm, flo, \
-                                                                  order, F, n, nrx, rpw, C, H, hdiv, n_nodes, y); \
+                                                                  order, F, n, nrx, rpw, C, H, hdiv, n_nodes,  \
+                                                                  accumulate, y);                              \
     break;
     E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4)
 #undef E2F_CASE

@@ -201,7 +201,10 @@ struct FuseTable {
   std::vector<int> idx;
   std::vector<double> coef;
 };
-FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w);
+// f >= 0: only the terms of filter degree f (the T rows of j-side degree b
+// with the receiver's harmonics of degree u = f - b), for the per-degree
+// weights alpha / D^f
+FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, int f = -1);
 
 // ---------------------------------------------------------------- device side
 // Device copies of one LayerTables (pointers into one allocation).

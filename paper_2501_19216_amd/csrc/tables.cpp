@@ -543,10 +543,13 @@ GeomSchedule geom_schedule(const LayerTables& t, int qc) {
   return gs;
 }
 
-FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w) {
+FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, int f) {
   const int nk = t.nk;
   FuseTable ft;
   if (t.L > kFuseMaxL) return ft;
+  std::vector<int> row_b(t.dimT, 0);  // j-side degree of every T row
+  for (const Block& B : t.blocks)
+    for (int de = 0; de < 2 * B.d + 1; ++de) row_b[B.toff + de] = B.b;
   // dense K[pos][x], accumulated over the T rows r that link a recouple entry
   // (k, r) with a coupling entry (r, be, q)
   const int np = fuse_stride(nk);
@@ -563,6 +566,9 @@ FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w) {
         for (int e = t.q_ptr[s]; e < t.q_ptr[s + 1]; ++e) {
           const double cq = t.q_unit[e] * w[t.q_path[e]];
           const int x = t.q_ridx[e];
+          int u = 0;  // x = u^2 + gamma: the degree of the receiver's harmonic
+          while ((u + 1) * (u + 1) <= x) ++u;
+          if (f >= 0 && row_b[r] + u != f) continue;
           for (int sl = s0; sl < s1; ++sl)
             for (int e2 = t.m_ptr[sl]; e2 < t.m_ptr[sl + 1]; ++e2) {
               const size_t at = (size_t)fuse_pos(nk, k, t.m_ridx[e2], a * a + sl - s0) * nk + x;

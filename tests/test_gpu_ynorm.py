@@ -64,6 +64,23 @@ def test_y_norm_workloads(e2f, ctx, name, rows, mix):
     assert o.max_rel_err(ref[:8], plain, wl.lmax) > 1e-2
 
 
+@pytest.mark.parametrize("form", ["split", "fused"])
+def test_y_norm_both_forms(e2f, ctx, form):
+    # alpha / D^f in both forms of the aggregation: the two-kernel form (S^(f)
+    # per degree, recoupled by its terms b + u = f) and the fused form (one
+    # pass per degree with F^(f) of the same terms)
+    inp, rp, ci, alpha = case("water2000_L4")
+    wl = inp.workload
+    r = sample_rows(inp.pos.shape[0], 64, seed=21)
+    ref = o.layer(wl.lmax, wl.heads, inp.pos, inp.feat, rp, ci, alpha, inp.path_w, rows=r, y_norm=True)
+    got = e2f.e2f_wigner6j_conv_forward(ctx, gpu(inp.pos), gpu(inp.feat), gpu(rp), gpu(ci), gpu(alpha), wl.lmax,
+                                        wl.heads, wl.cutoff, path_w=inp.path_w, y_norm=True,
+                                        form=form).cpu().numpy()
+    err = o.max_rel_err(got[r], ref, wl.lmax)
+    print("water2000 y_norm %s: err %.3e" % (form, err))
+    assert err <= TOL_F32
+
+
 def test_y_norm_short_contacts_and_slices(e2f, ctx):
     # L = 6 on uniform random positions (no minimum distance: the closest
     # pairs are about 0.1 A apart), where the weights 1/D^f of the short edges
