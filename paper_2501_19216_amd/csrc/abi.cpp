@@ -72,6 +72,9 @@ struct e2f_ctx {
     // the same per filter degree f (alpha / D^f), L + 1 tables
     std::vector<const int*> ff_ptr, ff_idx;
     std::vector<const double*> ff_coef;
+    // at L = 4: the degree pairs (3, 2) and (1, 0) in one table each
+    std::vector<const int*> fp_ptr, fp_idx;
+    std::vector<const double*> fp_coef;
   };
   std::vector<std::vector<CoefSet>> coefs;
   // per L and filter degree f: the recouple schedule restricted to b + u = f
@@ -424,6 +427,13 @@ e2f_status coef_of(e2f_ctx* ctx, int L, const std::vector<double>& w, bool allow
     push_array(blob, o, ftf.back().idx);
     push_array(blob, o, ftf.back().coef);
   }
+  const bool pairs = !ft.coef.empty() && L == 4;  // o[11 + 4L + 3q] .. o[13 + 4L + 3q]
+  for (int q = 0; q < (pairs ? 2 : 0); ++q) {
+    const FuseTable fp = fuse_table(t, w, 3 - 2 * q, 2 - 2 * q);
+    push_array(blob, o, fp.ptr);
+    push_array(blob, o, fp.idx);
+    push_array(blob, o, fp.coef);
+  }
   if (sets.size() >= kMaxCoefSets) {  // the oldest set may still be read by queued work
     E2F_HIP(hipDeviceSynchronize());
     E2F_HIP(hipFree(sets.front().mem));
@@ -451,6 +461,11 @@ e2f_status coef_of(e2f_ctx* ctx, int L, const std::vector<double>& w, bool allow
       c.ff_ptr.push_back((const int*)((char*)mem + o[8 + L + 3 * f]));
       c.ff_idx.push_back((const int*)((char*)mem + o[9 + L + 3 * f]));
       c.ff_coef.push_back((const double*)((char*)mem + o[10 + L + 3 * f]));
+    }
+    for (int q = 0; q < (pairs ? 2 : 0); ++q) {
+      c.fp_ptr.push_back((const int*)((char*)mem + o[11 + 4 * L + 3 * q]));
+      c.fp_idx.push_back((const int*)((char*)mem + o[12 + 4 * L + 3 * q]));
+      c.fp_coef.push_back((const double*)((char*)mem + o[13 + 4 * L + 3 * q]));
     }
   }
   sets.push_back(std::move(c));
@@ -762,16 +777,33 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
     const int32_t* ord = order + q0;
     if (fsplit > 0 && !ynorm) {  // F of the slice, then the aggregation with the recouple applied
       E2F_TIMED("fuse_build", launch_fuse_build(L, cs->f_ptr, cs->f_idx, cs->f_coef, Rr, ord, nb, S, s));
-      E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, alpha_hm, n_edges, featq, ord, S, nb, C,
-                                                Hv, hdiv, n, false, y, s));
+      E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, alpha_hm, nullptr, n_edges, featq, ord, S,
+                                                nb, C, Hv, hdiv, n, false, y, s));
       continue;
     }
-    if (fsplit > 0) {  // per filter degree f: F^(f) (the terms b + u = f) and the weights alpha / D^f; f > 0 adds
+    if (fsplit > 0) {  // per filter degree f: F^(f) (the terms b + u = f) and the weights alpha / D^f; later passes add
+      const float* afd[kMaxL + 1];
+      for (int fd = 0; fd <= L; ++fd) afd[fd] = alpha_hm + (size_t)fd * H * n_edges;
+      if (L == 4 && cs->fp_ptr.size() == 2) {
+        // three passes: the degree pairs (3, 2) and (1, 0), each in the two
+        // K tiles of one pass (16 and 9 rows: (f+1)^2 components of degree
+        // f), then degree 4 on both tiles
+        for (int q = 0; q < 2; ++q) {
+          E2F_TIMED("fuse_build", launch_fuse_build(L, cs->fp_ptr[q], cs->fp_idx[q], cs->fp_coef[q], Rr, ord, nb, S,
+                                                    s));
+          E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, afd[3 - 2 * q], afd[2 - 2 * q], n_edges,
+                                                    featq, ord, S, nb, C, Hv, hdiv, n, q > 0, y, s));
+        }
+        E2F_TIMED("fuse_build", launch_fuse_build(L, cs->ff_ptr[4], cs->ff_idx[4], cs->ff_coef[4], Rr, ord, nb, S, s));
+        E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, afd[4], nullptr, n_edges, featq, ord, S, nb,
+                                                  C, Hv, hdiv, n, true, y, s));
+        continue;
+      }
       for (int fd = 0; fd <= L; ++fd) {
         E2F_TIMED("fuse_build", launch_fuse_build(L, cs->ff_ptr[fd], cs->ff_idx[fd], cs->ff_coef[fd], Rr, ord, nb, S,
                                                   s));
-        E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, alpha_hm + (size_t)fd * H * n_edges,
-                                                  n_edges, featq, ord, S, nb, C, Hv, hdiv, n, fd > 0, y, s));
+        E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, afd[fd], nullptr, n_edges, featq, ord, S,
+                                                  nb, C, Hv, hdiv, n, fd > 0, y, s));
       }
       continue;
     }

@@ -921,7 +921,8 @@ constexpr int kFuseRows = kOuterEdges + 4 * (2 * kFuseStages - 2);  // staging r
 template <int L, int LB>
 __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re, const int64_t* __restrict__ row_ptr,
                                                     const int32_t* __restrict__ col,
-                                                    const float* __restrict__ alpha_hm, int64_t n_edges,
+                                                    const float* __restrict__ alpha_hm,
+                                                    const float* __restrict__ alpha_hm2, int64_t n_edges,
                                                     const uint4* __restrict__ fhm, const uint2* __restrict__ flo,
                                                     const int32_t* __restrict__ order, const float* __restrict__ F,
                                                     int n, int nrx, int rpw, int C, int H, int hdiv, int n_nodes,
@@ -949,6 +950,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
   float* Alb = sm;                        // [2][SR][AS] alpha R of the chunk's edges, split (zero past its rows)
   int* job = (int*)(sm + 2 * SB);         // [2][SR] the senders' offsets in the re-laid features
   float* sa = sm + 2 * SB + 2 * SR;       // [EC] the staging wave's copy of the chunk's weights
+  float* sa2 = sa + EC;                   // [EC] with alpha_hm2: the second tile's weights
   const int bid = blockIdx.x, xcd = bid % 8, local = bid / 8;
   const int h = local % H, rfirst = xcd * nrx + (local / H) * rpw;
   const int rlast = min(min(rfirst + rpw, (xcd + 1) * nrx), n);  // uniform over the workgroup
@@ -963,6 +965,10 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
   const unsigned fstride = (unsigned)(H * NG * 16);
   const unsigned foff = (unsigned)((h * NG + min(wave, NG - 1)) * 16 + l16);
   const float* ah = alpha_hm ? alpha_hm + (int64_t)(h / hdiv) * n_edges : nullptr;
+  // alpha_hm2 (NK = 25): the rows of the second K tile (positions 16 ..) take
+  // the harmonics' components 0 .. 8 with these weights instead, so that one
+  // pass aggregates two filter degrees (their terms in one F table)
+  const float* ah2 = alpha_hm2 && NK == 25 ? alpha_hm2 + (int64_t)(h / hdiv) * n_edges : nullptr;
   for (int q = threadIdx.x; q < 2 * (SR - EC) * AS; q += blockDim.x) {
     const int b = q / ((SR - EC) * AS);
     Alb[b * SB + EC * AS + q % ((SR - EC) * AS)] = 0.0f;
@@ -1000,19 +1006,22 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
     // missing weight array reads the harmonics instead); the caller's senders
     // are read at a clamped index.  Rows past ne are masked by selects.
     const float* ap = ah ? ah : Re;
-    float av[EC / 64];
+    float av[EC / 64], av2[EC / 64];
     int jv[EC / 64];
 #pragma unroll
     for (int u = 0; u < EC / 64; ++u) {
       const int nb = lane + 64 * u;
       const float a = ap[c0 + nb];
+      const float a2 = ah2 ? ah2[c0 + nb] : 0.0f;
       const int j = col[c0 + min(nb, ne - 1)];
       av[u] = nb < ne ? (ah ? a : 1.0f) : 0.0f;
+      av2[u] = nb < ne ? a2 : 0.0f;
       jv[u] = nb < ne && (unsigned)j < (unsigned)n_nodes ? j : 0;
     }
 #pragma unroll
     for (int u = 0; u < EC / 64; ++u) {
       sa[lane + 64 * u] = av[u];
+      if (ah2) sa2[lane + 64 * u] = av2[u];
       jo[lane + 64 * u] = (int)((unsigned)jv[u] * fstride);
     }
     __builtin_amdgcn_wave_barrier();
@@ -1024,7 +1033,9 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
     const int pt = p / 16, pk4 = (p % 16) / 4, ps = p % 4, ks = fuse_ks(NK, pt);
     const int pj = pk4 * ks + ps;
     const bool bok = pt * 16 < NK && ps < ks && pj < fuse_rows(NK, pt);
-    const int be = bok ? 16 * pt + pj : 0;
+    const bool second = ah2 && pt == 1;  // (uniform per lane) the second degree's row
+    const int be = bok ? (second ? pj : 16 * pt + pj) : 0;  // the harmonics' component
+    const float* wsrc = second ? sa2 : sa;
     // the lane's rows rs + RPI (BT bt + k): one base per batch, immediate
     // offsets within it
     const float* src = Re + (size_t)(c0 + rs) * NK + be;
@@ -1045,7 +1056,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
 #pragma unroll
       for (int k = 0; k < BT; ++k) {
         const int nb = (bt * BT + k) * RPI + rs;
-        const float w = cur[k] * sa[nb];
+        const float w = cur[k] * wsrc[nb];
         const float v = bok && nb < ne ? w : 0.0f;
         if (nb < nrow) {
           // A of the split products: words hi | mid << 16 and hi | lo << 16
@@ -2273,14 +2284,16 @@ hipError_t launch_feat_qmajor(int L, const float* feat, int n, int C, float* fea
 }
 
 hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, const int32_t* col,
-                              const float* alpha_hm, int64_t n_edges, const float* featq, const int32_t* order,
+                              const float* alpha_hm, const float* alpha_hm2, int64_t n_edges, const float* featq,
+                              const int32_t* order,
                               const float* F, int n, int C, int H, int hdiv, int n_nodes, bool accumulate, float* y,
                               hipStream_t s) {
   if (n == 0) return hipSuccess;
   if (!outer_fused_supported(L, C, H, n_nodes)) return hipErrorInvalidValue;
   const int nk = (L + 1) * (L + 1), mp = 16 * ((nk + 15) / 16);
   const int nw = (nk + 3) / 4 + 1;  // a product wave per group of four components, and the staging wave
-  const size_t lds = sizeof(float) * (2 * (size_t)kFuseRows * 2 * mp + 2 * (size_t)kFuseRows + kOuterEdges);
+  const size_t lds = sizeof(float) * (2 * (size_t)kFuseRows * 2 * mp + 2 * (size_t)kFuseRows + 2 * kOuterEdges);
+  if (alpha_hm2 && L != 4) return hipErrorInvalidValue;
   const size_t nq = (size_t)n_nodes * H * fuse_groups(L) * 16;  // entries of the re-laid features
   const uint4* fhm = (const uint4*)featq;
   const uint2* flo = (const uint2*)(fhm + nq);
@@ -2296,7 +2309,8 @@ hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, co
 #define E2F_CASE(LL)                                                                                          \
   case LL:                                                                                                    \
     if (hipError_t e = allow_lds(k_outer_fused<LL, 512>, lds); e != hipSuccess) return e;                     \
-    k_outer_fused<LL, 512><<<(unsigned)blocks, 64 * nw, lds, s>>>(Re, row_ptr, col, alpha_hm, n_edges, fhm, flo, \
+    k_outer_fused<LL, 512><<<(unsigned)blocks, 64 * nw, lds, s>>>(Re, row_ptr, col, alpha_hm, alpha_hm2,   \
+                                                                  n_edges, fhm, flo,                           \
                                                                   order, F, n, nrx, rpw, C, H, hdiv, n_nodes,  \
                                                                   accumulate, y);                              \
     break;

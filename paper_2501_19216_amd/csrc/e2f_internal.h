@@ -203,8 +203,11 @@ struct FuseTable {
 };
 // f >= 0: only the terms of filter degree f (the T rows of j-side degree b
 // with the receiver's harmonics of degree u = f - b), for the per-degree
-// weights alpha / D^f
-FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, int f = -1);
+// weights alpha / D^f.  f2 >= 0 (L = 4): two degrees in one table, those of
+// f at the j-side components be (f <= 3: be < 16, the first K tile) and those
+// of f2 at 16 + be (f2 <= 2: be < 9, the second tile's nine rows), for one
+// aggregation pass whose A rows carry the two degrees' weights
+FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, int f = -1, int f2 = -1);
 
 // ---------------------------------------------------------------- device side
 // Device copies of one LayerTables (pointers into one allocation).

@@ -177,8 +177,11 @@ int fuse_groups(int L);
 hipError_t launch_feat_qmajor(int L, const float* feat, int n, int C, float* featq, hipStream_t s);
 // accumulate: the result is added to y (the sum over the filter degrees of
 // alpha / D^f), else stored
+// alpha_hm2 (L = 4, else NULL): the weights of a second filter degree for
+// the rows of the second K tile (components 0 .. 8), F from a paired table
 hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, const int32_t* col,
-                              const float* alpha_hm, int64_t n_edges, const float* featq, const int32_t* order,
+                              const float* alpha_hm, const float* alpha_hm2, int64_t n_edges, const float* featq,
+                              const int32_t* order,
                               const float* F, int n, int C, int H, int hdiv, int n_nodes, bool accumulate, float* y,
                               hipStream_t s);
 // y[order[r]] from S row r (head-major like T), r < n; shared_s: every r

@@ -543,7 +543,7 @@ GeomSchedule geom_schedule(const LayerTables& t, int qc) {
   return gs;
 }
 
-FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, int f) {
+FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, int f, int f2) {
   const int nk = t.nk;
   FuseTable ft;
   if (t.L > kFuseMaxL) return ft;
@@ -568,10 +568,17 @@ FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, int f) 
           const int x = t.q_ridx[e];
           int u = 0;  // x = u^2 + gamma: the degree of the receiver's harmonic
           while ((u + 1) * (u + 1) <= x) ++u;
-          if (f >= 0 && row_b[r] + u != f) continue;
+          const int deg = row_b[r] + u;
+          int shift = 0;  // K row of a j-side component be: be + shift
+          if (f2 >= 0) {
+            if (deg == f2) shift = 16;
+            else if (deg != f) continue;
+          } else if (f >= 0 && deg != f) {
+            continue;
+          }
           for (int sl = s0; sl < s1; ++sl)
             for (int e2 = t.m_ptr[sl]; e2 < t.m_ptr[sl + 1]; ++e2) {
-              const size_t at = (size_t)fuse_pos(nk, k, t.m_ridx[e2], a * a + sl - s0) * nk + x;
+              const size_t at = (size_t)fuse_pos(nk, k, t.m_ridx[e2] + shift, a * a + sl - s0) * nk + x;
               K[at] += cq * t.m_coef[e2];
               mag[at] += std::fabs(cq * t.m_coef[e2]);
             }
