@@ -66,15 +66,18 @@ struct e2f_ctx {
     std::vector<const double*> rcf_coef;  // per filter degree f
     const float* w_f = nullptr;
     // fused recouple tensor (L <= kFuseMaxL): CSR over the positions of F
-    const int* f_ptr = nullptr;
-    const int* f_idx = nullptr;
-    const double* f_coef = nullptr;
+    // in the layout of nkr K rows
+    struct FuseTab {
+      const int* ptr = nullptr;
+      const int* idx = nullptr;
+      const double* coef = nullptr;
+      int nkr = 0;
+    };
+    FuseTab f;
     // the same per filter degree f (alpha / D^f), L + 1 tables
-    std::vector<const int*> ff_ptr, ff_idx;
-    std::vector<const double*> ff_coef;
-    // at L = 4: the degree pairs (3, 2) and (1, 0) in one table each
-    std::vector<const int*> fp_ptr, fp_idx;
-    std::vector<const double*> fp_coef;
+    std::vector<FuseTab> ff;
+    // at L = 4: the passes of kYnormPass4, their degrees stacked in the K rows
+    std::vector<FuseTab> fy;
   };
   std::vector<std::vector<CoefSet>> coefs;
   // per L and filter degree f: the recouple schedule restricted to b + u = f
@@ -416,20 +419,22 @@ e2f_status coef_of(e2f_ctx* ctx, int L, const std::vector<double>& w, bool allow
   }
   std::vector<float> wf(w.begin(), w.end());  // o[4 + L]
   push_array(blob, o, wf);
-  const FuseTable ft = fuse_table(t, w);  // o[5 + L] .. o[7 + L] (empty above kFuseMaxL)
+  const int all_degs[1] = {-1};
+  const FuseTable ft = fuse_table(t, w, all_degs, 1, t.nk);  // o[5 + L] .. o[7 + L] (empty above kFuseMaxL)
   push_array(blob, o, ft.ptr);
   push_array(blob, o, ft.idx);
   push_array(blob, o, ft.coef);
   std::vector<FuseTable> ftf;  // o[8 + L + 3f] .. o[10 + L + 3f]
   for (int f = 0; f <= L && !ft.coef.empty(); ++f) {
-    ftf.push_back(fuse_table(t, w, f));
+    ftf.push_back(fuse_table(t, w, &f, 1, t.nk));
     push_array(blob, o, ftf.back().ptr);
     push_array(blob, o, ftf.back().idx);
     push_array(blob, o, ftf.back().coef);
   }
-  const bool pairs = !ft.coef.empty() && L == 4;  // o[11 + 4L + 3q] .. o[13 + 4L + 3q]
-  for (int q = 0; q < (pairs ? 2 : 0); ++q) {
-    const FuseTable fp = fuse_table(t, w, 3 - 2 * q, 2 - 2 * q);
+  const bool stacked = !ft.coef.empty() && L == kFuseMaxL;  // o[11 + 4L + 3q] .. o[13 + 4L + 3q]
+  for (int q = 0; q < (stacked ? kYnormPasses4 : 0); ++q) {
+    const YnormPass& yp = kYnormPass4[q];
+    const FuseTable fp = fuse_table(t, w, yp.degs, yp.nd, fuse_krows(t.nk, yp.degs, yp.nd));
     push_array(blob, o, fp.ptr);
     push_array(blob, o, fp.idx);
     push_array(blob, o, fp.coef);
@@ -454,19 +459,14 @@ e2f_status coef_of(e2f_ctx* ctx, int L, const std::vector<double>& w, bool allow
   for (int f = 0; f <= L; ++f) c.rcf_coef.push_back((const double*)((char*)mem + o[3 + f]));
   c.w_f = (const float*)((char*)mem + o[4 + L]);
   if (!ft.coef.empty()) {
-    c.f_ptr = (const int*)((char*)mem + o[5 + L]);
-    c.f_idx = (const int*)((char*)mem + o[6 + L]);
-    c.f_coef = (const double*)((char*)mem + o[7 + L]);
-    for (int f = 0; f <= L; ++f) {
-      c.ff_ptr.push_back((const int*)((char*)mem + o[8 + L + 3 * f]));
-      c.ff_idx.push_back((const int*)((char*)mem + o[9 + L + 3 * f]));
-      c.ff_coef.push_back((const double*)((char*)mem + o[10 + L + 3 * f]));
-    }
-    for (int q = 0; q < (pairs ? 2 : 0); ++q) {
-      c.fp_ptr.push_back((const int*)((char*)mem + o[11 + 4 * L + 3 * q]));
-      c.fp_idx.push_back((const int*)((char*)mem + o[12 + 4 * L + 3 * q]));
-      c.fp_coef.push_back((const double*)((char*)mem + o[13 + 4 * L + 3 * q]));
-    }
+    auto tab = [&](size_t k, int nkr) {
+      return e2f_ctx::CoefSet::FuseTab{(const int*)((char*)mem + o[k]), (const int*)((char*)mem + o[k + 1]),
+                                       (const double*)((char*)mem + o[k + 2]), nkr};
+    };
+    c.f = tab(5 + L, t.nk);
+    for (int f = 0; f <= L; ++f) c.ff.push_back(tab(8 + L + 3 * f, t.nk));
+    for (int q = 0; q < (stacked ? kYnormPasses4 : 0); ++q)
+      c.fy.push_back(tab(11 + 4 * L + 3 * q, fuse_krows(t.nk, kYnormPass4[q].degs, kYnormPass4[q].nd)));
   }
   sets.push_back(std::move(c));
   out = &sets.back();
@@ -621,6 +621,18 @@ int fused_split(const e2f_conv_params* p, int64_t n) {
   return p->lmax == kFuseMaxL && s_bytes > 256.0 * 1024 * 1024 ? dh / 16 : 0;
 }
 
+// Floats of one receiver's F in the fused form: the largest layout among
+// the forward's passes (the alpha / D^f passes at L = 4 stack degrees in
+// more K rows).
+int fused_row_floats(const e2f_conv_params* p) {
+  const int L = p->lmax, nk = nk_of(L);
+  int fl = fuse_stride(nk, nk);
+  if (p->y_norm && L == kFuseMaxL)
+    for (int q = 0; q < kYnormPasses4; ++q)
+      fl = std::max(fl, fuse_stride(nk, fuse_krows(nk, kYnormPass4[q].degs, kYnormPass4[q].nd)));
+  return fl;
+}
+
 FwdLayout fwd_layout(const e2f_conv_params* p, int n, int64_t E, bool have_alpha) {
   const int L = p->lmax, nk = nk_of(L), C = p->channels, H = p->heads;
   const bool ynorm = p->y_norm != 0;
@@ -652,8 +664,9 @@ FwdLayout fwd_layout(const e2f_conv_params* p, int n, int64_t E, bool have_alpha
   f.featq = take(fused_split(p, n) > 0 ? sizeof(float) * (size_t)n * C * 6 * fuse_groups(L) : 0);
   f.S = off;
   f.fixed = off;
-  // per receiver of a slice: F_i (fused) or S_i
-  f.s_row = fused_split(p, n) > 0 ? sizeof(float) * (size_t)fuse_stride(nk) : al256(sizeof(float) * (size_t)node_tp_dim(L) * C);
+  // per receiver of a slice: F_i (fused; the largest layout of its passes) or S_i
+  f.s_row = fused_split(p, n) > 0 ? sizeof(float) * (size_t)fused_row_floats(p)
+                                  : al256(sizeof(float) * (size_t)node_tp_dim(L) * C);
   return f;
 }
 
@@ -695,7 +708,8 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
     if (!allow_upload && ctx->couple.find(std::make_pair(L, cgroups)) == ctx->couple.end())
       return fail(E2F_EINVAL, "the coupling schedule is not resident on the context; call e2f_wigner6j_prepare first");
     if ((rs = couple_of(ctx, L, cgroups, cpl)) != E2F_OK) return rs;
-  } else if (!cs->f_ptr || (p->y_norm && (int)cs->ff_ptr.size() != L + 1)) {
+  } else if (!cs->f.ptr ||
+             (p->y_norm && ((int)cs->ff.size() != L + 1 || (L == kFuseMaxL && (int)cs->fy.size() != kYnormPasses4)))) {
     return fail(E2F_EDEVICE, "the fused recouple table of L = %d is missing", L);
   }
   if (n == 0) return E2F_OK;
@@ -775,35 +789,36 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
   for (int64_t q0 = 0; q0 < n; q0 += slice, ++slices) {
     const int nb = (int)std::min<int64_t>(slice, n - q0);
     const int32_t* ord = order + q0;
-    if (fsplit > 0 && !ynorm) {  // F of the slice, then the aggregation with the recouple applied
-      E2F_TIMED("fuse_build", launch_fuse_build(L, cs->f_ptr, cs->f_idx, cs->f_coef, Rr, ord, nb, S, s));
-      E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, alpha_hm, nullptr, n_edges, featq, ord, S,
-                                                nb, C, Hv, hdiv, n, false, y, s));
-      continue;
-    }
-    if (fsplit > 0) {  // per filter degree f: F^(f) (the terms b + u = f) and the weights alpha / D^f; later passes add
-      const float* afd[kMaxL + 1];
-      for (int fd = 0; fd <= L; ++fd) afd[fd] = alpha_hm + (size_t)fd * H * n_edges;
-      if (L == 4 && cs->fp_ptr.size() == 2) {
-        // three passes: the degree pairs (3, 2) and (1, 0), each in the two
-        // K tiles of one pass (16 and 9 rows: (f+1)^2 components of degree
-        // f), then degree 4 on both tiles
-        for (int q = 0; q < 2; ++q) {
-          E2F_TIMED("fuse_build", launch_fuse_build(L, cs->fp_ptr[q], cs->fp_idx[q], cs->fp_coef[q], Rr, ord, nb, S,
-                                                    s));
-          E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, afd[3 - 2 * q], afd[2 - 2 * q], n_edges,
-                                                    featq, ord, S, nb, C, Hv, hdiv, n, q > 0, y, s));
+    if (fsplit > 0) {
+      // per pass: F of the slice (from a table whose K rows stack the pass's
+      // filter degrees), then the aggregation with the recouple applied; the
+      // passes after the first add to y.  The plain layer: one pass.  With
+      // y_norm the weights alpha / D^f and the terms b + u = f of each degree
+      // f: at L = 4 two passes, the degrees of kYnormPass4 (3 and 2, then 4,
+      // 1 and 0), each degree in (f+1)^2 K rows; below, one pass per degree.
+      int npass = 0;
+      const int all_degs[1] = {-1};
+      auto pass = [&](const e2f_ctx::CoefSet::FuseTab& tab, const int* degs, int nd) -> e2f_status {
+        FusedSegs sg{};
+        sg.n = nd;
+        for (int q = 0, r = 0; q < nd; ++q) {
+          sg.alpha_hm[q] = degs[q] < 0 ? alpha_hm : alpha_hm + (size_t)degs[q] * H * n_edges;
+          sg.start[q] = r;
+          r += degs[q] < 0 || nd == 1 ? nk : (degs[q] + 1) * (degs[q] + 1);
         }
-        E2F_TIMED("fuse_build", launch_fuse_build(L, cs->ff_ptr[4], cs->ff_idx[4], cs->ff_coef[4], Rr, ord, nb, S, s));
-        E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, afd[4], nullptr, n_edges, featq, ord, S, nb,
-                                                  C, Hv, hdiv, n, true, y, s));
-        continue;
-      }
-      for (int fd = 0; fd <= L; ++fd) {
-        E2F_TIMED("fuse_build", launch_fuse_build(L, cs->ff_ptr[fd], cs->ff_idx[fd], cs->ff_coef[fd], Rr, ord, nb, S,
-                                                  s));
-        E2F_TIMED("aggregate", launch_outer_fused(L, Re, row_ptr, col_idx, afd[fd], nullptr, n_edges, featq, ord, S,
-                                                  nb, C, Hv, hdiv, n, fd > 0, y, s));
+        E2F_TIMED("fuse_build", launch_fuse_build(L, tab.nkr, tab.ptr, tab.idx, tab.coef, Rr, ord, nb, S, s));
+        E2F_TIMED("aggregate", launch_outer_fused(L, tab.nkr, Re, row_ptr, col_idx, sg, n_edges, featq, ord, S, nb, C,
+                                                  Hv, hdiv, n, npass++ > 0, y, s));
+        return E2F_OK;
+      };
+      if (!ynorm) {
+        if ((rs = pass(cs->f, all_degs, 1)) != E2F_OK) return rs;
+      } else if (L == kFuseMaxL) {
+        for (int q = 0; q < kYnormPasses4; ++q)
+          if ((rs = pass(cs->fy[q], kYnormPass4[q].degs, kYnormPass4[q].nd)) != E2F_OK) return rs;
+      } else {
+        for (int fd = 0; fd <= L; ++fd)
+          if ((rs = pass(cs->ff[fd], &fd, 1)) != E2F_OK) return rs;
       }
       continue;
     }

@@ -914,28 +914,32 @@ __global__ void k_feat_qmajor3(const float* __restrict__ feat, int n, int nk, in
 // the products never wait for a chunk's loads.  One barrier per chunk (two
 // more after a receiver's last chunk, for the shares of y, which reuse the
 // finished buffer).
+// The K rows of G and F (KR of them; the plain layer: KR = NK, row be the
+// component be of R(p_j)) may stack several filter degrees of alpha / D^f:
+// segment s of the K rows (from sg.start[s]) holds the components be =
+// row - start of R(p_j) weighted by alpha_hm[s], so that one gather of the
+// senders serves several degrees.
 // register pipeline of the fused products: kFuseStages - 1 steps ahead
 constexpr int kFuseStages = 3;
 constexpr int kFuseRows = kOuterEdges + 4 * (2 * kFuseStages - 2);  // staging rows with the prefetch padding
 
-template <int L, int LB>
+template <int L, int LB, int KR>
 __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re, const int64_t* __restrict__ row_ptr,
-                                                    const int32_t* __restrict__ col,
-                                                    const float* __restrict__ alpha_hm,
-                                                    const float* __restrict__ alpha_hm2, int64_t n_edges,
+                                                    const int32_t* __restrict__ col, FusedSegs sg, int64_t n_edges,
                                                     const uint4* __restrict__ fhm, const uint2* __restrict__ flo,
                                                     const int32_t* __restrict__ order, const float* __restrict__ F,
                                                     int n, int nrx, int rpw, int C, int H, int hdiv, int n_nodes,
                                                     bool accumulate, float* __restrict__ y) {
-  constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;
+  constexpr int NK = (L + 1) * (L + 1), MT = (NK + 15) / 16, MP = 16 * MT;  // rows k of y and F
+  constexpr int MK = (KR + 15) / 16, MPK = 16 * MK;                         // K rows of G and F
   constexpr int EC = kOuterEdges;
   // staging row stride in words: two words per component (a 64-bit read per
   // lane), odd rows rotated by 16 components where 2 MP is a multiple of 64,
   // so rows 4 st + k4 of one step alternate between the two halves of the
   // banks
-  constexpr int AS = 2 * MP;
-  constexpr int ROT = (2 * MP) % 64 == 0 ? 16 : 0;
-  constexpr int QB = fuse_qblock(NK), FS = fuse_stride(NK);
+  constexpr int AS = 2 * MPK;
+  constexpr int ROT = (2 * MPK) % 64 == 0 ? 16 : 0;
+  constexpr int QB = fuse_qblock(NK, KR), FS = fuse_stride(NK, KR);
   constexpr int NG = (NK + 3) / 4;  // groups of at most four components (fuse_gn): one product wave each
   // rows EC .. SR-1 of a buffer are padding (zero weights, sender offset 0):
   // the last iteration of the step loop starts at a step st <= ns - 1 and
@@ -944,13 +948,12 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
   constexpr int SR = kFuseRows, SB = SR * AS;
   static_assert(SR - EC >= 8 * kFuseStages - 8, "padding rows must cover the prefetch past a full chunk");
   static_assert(NG * MP * 16 <= SB, "the shares of y must fit one staging buffer");
-  constexpr int RPI = 64 / MP;            // rows the staging wave covers per pass (lane: be = lane % MP)
+  constexpr int RPI = 64 / MPK;           // rows the staging wave covers per pass (lane: K row lane % MPK)
   constexpr int ITER = EC / RPI;          // passes over a full chunk
   extern __shared__ float sm[];
   float* Alb = sm;                        // [2][SR][AS] alpha R of the chunk's edges, split (zero past its rows)
   int* job = (int*)(sm + 2 * SB);         // [2][SR] the senders' offsets in the re-laid features
-  float* sa = sm + 2 * SB + 2 * SR;       // [EC] the staging wave's copy of the chunk's weights
-  float* sa2 = sa + EC;                   // [EC] with alpha_hm2: the second tile's weights
+  float* sa = sm + 2 * SB + 2 * SR;       // [sg.n][EC] the staging wave's copy of the chunk's weights
   const int bid = blockIdx.x, xcd = bid % 8, local = bid / 8;
   const int h = local % H, rfirst = xcd * nrx + (local / H) * rpw;
   const int rlast = min(min(rfirst + rpw, (xcd + 1) * nrx), n);  // uniform over the workgroup
@@ -964,11 +967,6 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
   const int q0 = stager ? 0 : fuse_g0(NK, wave);
   const unsigned fstride = (unsigned)(H * NG * 16);
   const unsigned foff = (unsigned)((h * NG + min(wave, NG - 1)) * 16 + l16);
-  const float* ah = alpha_hm ? alpha_hm + (int64_t)(h / hdiv) * n_edges : nullptr;
-  // alpha_hm2 (NK = 25): the rows of the second K tile (positions 16 ..) take
-  // the harmonics' components 0 .. 8 with these weights instead, so that one
-  // pass aggregates two filter degrees (their terms in one F table)
-  const float* ah2 = alpha_hm2 && NK == 25 ? alpha_hm2 + (int64_t)(h / hdiv) * n_edges : nullptr;
   for (int q = threadIdx.x; q < 2 * (SR - EC) * AS; q += blockDim.x) {
     const int b = q / ((SR - EC) * AS);
     Alb[b * SB + EC * AS + q % ((SR - EC) * AS)] = 0.0f;
@@ -995,7 +993,9 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
     if (ne == 0) {  // an isolated receiver: zero weights, sender offsets 0
 #pragma unroll
       for (int u = 0; u < EC / 64; ++u) {
-        sa[lane + 64 * u] = 0.0f;
+#pragma unroll
+        for (int sgm = 0; sgm < kFusedSegs; ++sgm)
+          if (sgm < sg.n) sa[sgm * EC + lane + 64 * u] = 0.0f;
         jo[lane + 64 * u] = 0;
       }
       return;
@@ -1005,37 +1005,49 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
     // arrays, which carry kEdgePad rows of padding past the last edge (a
     // missing weight array reads the harmonics instead); the caller's senders
     // are read at a clamped index.  Rows past ne are masked by selects.
-    const float* ap = ah ? ah : Re;
-    float av[EC / 64], av2[EC / 64];
+    float av[kFusedSegs][EC / 64];
     int jv[EC / 64];
 #pragma unroll
     for (int u = 0; u < EC / 64; ++u) {
       const int nb = lane + 64 * u;
-      const float a = ap[c0 + nb];
-      const float a2 = ah2 ? ah2[c0 + nb] : 0.0f;
+#pragma unroll
+      for (int sgm = 0; sgm < kFusedSegs; ++sgm) {
+        if (sgm >= sg.n) break;
+        const float* ah = sg.alpha_hm[sgm] ? sg.alpha_hm[sgm] + (int64_t)(h / hdiv) * n_edges : nullptr;
+        const float a = (ah ? ah : Re)[c0 + nb];
+        av[sgm][u] = nb < ne ? (ah ? a : 1.0f) : 0.0f;
+      }
       const int j = col[c0 + min(nb, ne - 1)];
-      av[u] = nb < ne ? (ah ? a : 1.0f) : 0.0f;
-      av2[u] = nb < ne ? a2 : 0.0f;
       jv[u] = nb < ne && (unsigned)j < (unsigned)n_nodes ? j : 0;
     }
 #pragma unroll
     for (int u = 0; u < EC / 64; ++u) {
-      sa[lane + 64 * u] = av[u];
-      if (ah2) sa2[lane + 64 * u] = av2[u];
+#pragma unroll
+      for (int sgm = 0; sgm < kFusedSegs; ++sgm)
+        if (sgm < sg.n) sa[sgm * EC + lane + 64 * u] = av[sgm][u];
       jo[lane + 64 * u] = (int)((unsigned)jv[u] * fstride);
     }
     __builtin_amdgcn_wave_barrier();
     const int nrow = 4 * ((ne + 3) / 4);
-    // the lane's position p = lane % MP of the row holds component be (the
-    // K order of F: within tile p / 16, component j at 4 (j / ks) + j % ks),
-    // or nothing (zeros) where no component takes it
-    const int p = lane % MP, rs = lane / MP;
-    const int pt = p / 16, pk4 = (p % 16) / 4, ps = p % 4, ks = fuse_ks(NK, pt);
+    // the lane's position p = lane % MPK of the row holds K row kr (the K
+    // order of F: within tile p / 16, row 16 (p / 16) + j at 4 (j / ks) +
+    // j % ks), or nothing (zeros) where no row takes it; K row kr of segment
+    // sgm is the harmonics' component kr - sg.start[sgm] with that segment's
+    // weights
+    const int p = lane % MPK, rs = lane / MPK;
+    const int pt = p / 16, pk4 = (p % 16) / 4, ps = p % 4, ks = fuse_ks(KR, pt);
     const int pj = pk4 * ks + ps;
-    const bool bok = pt * 16 < NK && ps < ks && pj < fuse_rows(NK, pt);
-    const bool second = ah2 && pt == 1;  // (uniform per lane) the second degree's row
-    const int be = bok ? (second ? pj : 16 * pt + pj) : 0;  // the harmonics' component
-    const float* wsrc = second ? sa2 : sa;
+    const bool bok = pt * 16 < KR && ps < ks && pj < fuse_rows(KR, pt);
+    const int kr = 16 * pt + pj;
+    int seg = 0, s0 = 0;
+#pragma unroll
+    for (int sgm = 1; sgm < kFusedSegs; ++sgm)
+      if (sgm < sg.n && kr >= sg.start[sgm]) {
+        seg = sgm;
+        s0 = sg.start[sgm];
+      }
+    const int be = bok ? kr - s0 : 0;  // the harmonics' component (< NK: checked by the launcher)
+    const float* wsrc = sa + seg * EC;
     // the lane's rows rs + RPI (BT bt + k): one base per batch, immediate
     // offsets within it
     const float* src = Re + (size_t)(c0 + rs) * NK + be;
@@ -1062,7 +1074,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
           // A of the split products: words hi | mid << 16 and hi | lo << 16
           unsigned hi, mid, lo;
           split_bf16x3(v, hi, mid, lo);
-          ((uint2*)(Al + nb * AS))[(p + (nb & 1) * ROT) % MP] = make_uint2(hi | mid << 16, hi | lo << 16);
+          ((uint2*)(Al + nb * AS))[(p + (nb & 1) * ROT) % MPK] = make_uint2(hi | mid << 16, hi | lo << 16);
         }
       }
       if (more_rows) {
@@ -1077,9 +1089,9 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
   int64_t c0 = e0;
   if (stager) stage(c0, (int)min((int64_t)EC, e1 - c0), 0);
   __syncthreads();
-  v4f acc[MT][4];
+  v4f acc[MK][4];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+  for (int mt = 0; mt < MK; ++mt)
 #pragma unroll
     for (int w = 0; w < 4; ++w) acc[mt][w] = (v4f){0.f, 0.f, 0.f, 0.f};
   for (int kb = 0;; kb ^= 1) {
@@ -1113,7 +1125,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
       // operations per tile and NL MT MFMAs of half the fp32 cost.
       auto products = [&](auto nlc) {
         constexpr int NL = decltype(nlc)::value;
-        uint2 aq[kFuseStages][MT];
+        uint2 aq[kFuseStages][MK];
         uint4 bh[kFuseStages];
         uint2 bl[kFuseStages];
         auto loadb = [&](int st, uint2* a, uint4& h4, uint2& l2) {
@@ -1123,7 +1135,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
           l2 = flo[o];
           const uint2* row = (const uint2*)(Al + nb * AS);
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) a[mt] = row[(mt * 16 + l16 + (nb & 1) * ROT) % MP];
+          for (int mt = 0; mt < MK; ++mt) a[mt] = row[(mt * 16 + l16 + (nb & 1) * ROT) % MPK];
         };
         auto mma = [&](const uint2* a, const uint4& h4, const uint2& l2) {
           const unsigned hw[4] = {h4.x, h4.y, h4.z, h4.w};
@@ -1133,7 +1145,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
             const v8bf bv =
                 __builtin_bit_cast(v8bf, (v4u){hw[w], (hw[w] >> 16) | (hw[w] << 16), lw[w] | (hw[w] << 16), 0u});
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
+            for (int mt = 0; mt < MK; ++mt) {
               const v8bf av = __builtin_bit_cast(v8bf, (v4u){a[mt].x, a[mt].y, a[mt].x, 0u});
               acc[mt][w] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc[mt][w], 0, 0, 0);
             }
@@ -1158,8 +1170,8 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
       else if (nl == 1) products(std::integral_constant<int, 1>{});
     }
     if (last) {
-      // this wave's share of y_i: A = F_i (rows k, K = be in the step order
-      // above, zero past NK), B = the accumulators.  The F loads are
+      // this wave's share of y_i: A = F_i (rows k, K = the K rows in the step
+      // order above, zero past KR), B = the accumulators.  The F loads are
       // unconditional (lanes past a sub-block's rows or K values read a
       // valid element and take zero), so the wait counts stay exact; the
       // next component's values load while this one's MFMAs run.
@@ -1169,18 +1181,18 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
       for (int rt = 0; rt < MT; ++rt) ya[rt] = (v4f){0.f, 0.f, 0.f, 0.f};
       auto recouple = [&](auto nlc) {
         constexpr int NL = decltype(nlc)::value;
-        float4 fv[2][MT][MT];
+        float4 fv[2][MT][MK];
         auto loadf = [&](int w, float4 (*f)[MT]) {
           const int q = q0 + w;  // < NK for w < NL
 #pragma unroll
           for (int rt = 0; rt < MT; ++rt)
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
+            for (int mt = 0; mt < MK; ++mt) {
               // (a 0/1 factor rather than a select: a value every lane uses
               // keeps the compiler from predicating the load)
-              const bool ok = l16 < fuse_rows(NK, rt) && k4 < fuse_kc(NK, mt);
+              const bool ok = l16 < fuse_rows(NK, rt) && k4 < fuse_kc(KR, mt);
               const float z = ok ? 1.0f : 0.0f;
-              const float4 v = *(const float4*)(Fr + q * QB + fuse_blk(NK, rt, mt) +
+              const float4 v = *(const float4*)(Fr + q * QB + fuse_blk(NK, KR, rt, mt) +
                                                 (ok ? (k4 * fuse_rows(NK, rt) + l16) * 4 : 0));
               f[rt][mt] = make_float4(v.x * z, v.y * z, v.z * z, v.w * z);
             }
@@ -1194,18 +1206,18 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
           if (w + 1 < NL) loadf(w + 1, fv[(w + 1) & 1]);
           __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
+          for (int mt = 0; mt < MK; ++mt)
 #pragma unroll
             for (int rt = 0; rt < MT; ++rt) {
-              // K steps s >= fuse_ks(NK, mt) hold no component (zero F and
-              // G): skipped (mt is a constant of the unrolled loop)
+              // K steps s >= fuse_ks(KR, mt) hold no K row (zero F and G):
+              // skipped (mt is a constant of the unrolled loop)
               const float4 f = fv[w & 1][rt][mt];
               ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.x, acc[mt][w][0], ya[rt], 0, 0, 0);
-              if (fuse_ks(NK, mt) > 1)
+              if (fuse_ks(KR, mt) > 1)
                 ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.y, acc[mt][w][1], ya[rt], 0, 0, 0);
-              if (fuse_ks(NK, mt) > 2)
+              if (fuse_ks(KR, mt) > 2)
                 ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.z, acc[mt][w][2], ya[rt], 0, 0, 0);
-              if (fuse_ks(NK, mt) > 3)
+              if (fuse_ks(KR, mt) > 3)
                 ya[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.w, acc[mt][w][3], ya[rt], 0, 0, 0);
             }
           __builtin_amdgcn_sched_barrier(0);
@@ -1233,7 +1245,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
         *yo = accumulate ? *yo + sum : sum;  // (accumulate: the sum over the filter degrees of alpha / D^f)
       }
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MK; ++mt)
 #pragma unroll
         for (int w = 0; w < 4; ++w) acc[mt][w] = (v4f){0.f, 0.f, 0.f, 0.f};
     }
@@ -2263,13 +2275,13 @@ bool outer_fused_supported(int L, int C, int H, int64_t n_nodes) {
          (uint64_t)n_nodes * H * fuse_groups(L) * 16 <= 0xffffffffull;
 }
 
-hipError_t launch_fuse_build(int L, const int* fptr, const int* fidx, const double* fcoef, const double* R,
-                             const int32_t* order, int n, float* F, hipStream_t s) {
+hipError_t launch_fuse_build(int L, int nkr, const int* fptr, const int* fidx, const double* fcoef,
+                             const double* R, const int32_t* order, int n, float* F, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  if (L < 0 || L > kFuseMaxL) return hipErrorInvalidValue;
+  if (L < 0 || L > kFuseMaxL || nkr < 1) return hipErrorInvalidValue;
   const int nk = (L + 1) * (L + 1);
-  k_fuse_build<<<(n + kFuseRecv - 1) / kFuseRecv, 256, 0, s>>>(fptr, fidx, fcoef, fuse_stride(nk), nk, R, order, n,
-                                                                 F);
+  k_fuse_build<<<(n + kFuseRecv - 1) / kFuseRecv, 256, 0, s>>>(fptr, fidx, fcoef, fuse_stride(nk, nkr), nk, R, order,
+                                                                 n, F);
   return hipGetLastError();
 }
 
@@ -2283,17 +2295,28 @@ hipError_t launch_feat_qmajor(int L, const float* feat, int n, int C, float* fea
   return hipGetLastError();
 }
 
-hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, const int32_t* col,
-                              const float* alpha_hm, const float* alpha_hm2, int64_t n_edges, const float* featq,
-                              const int32_t* order,
+bool fused_krows_supported(int L, int nkr) {
+  const int nk = (L + 1) * (L + 1);
+  return L >= 0 && L <= kFuseMaxL && (nkr == nk || (L == 4 && nkr == 30));
+}
+
+hipError_t launch_outer_fused(int L, int nkr, const float* Re, const int64_t* row_ptr, const int32_t* col,
+                              const FusedSegs& sg, int64_t n_edges, const float* featq, const int32_t* order,
                               const float* F, int n, int C, int H, int hdiv, int n_nodes, bool accumulate, float* y,
                               hipStream_t s) {
   if (n == 0) return hipSuccess;
-  if (!outer_fused_supported(L, C, H, n_nodes)) return hipErrorInvalidValue;
-  const int nk = (L + 1) * (L + 1), mp = 16 * ((nk + 15) / 16);
+  if (!outer_fused_supported(L, C, H, n_nodes) || !fused_krows_supported(L, nkr)) return hipErrorInvalidValue;
+  const int nk = (L + 1) * (L + 1), mpk = 16 * ((nkr + 15) / 16);
+  // segments: start[0] = 0, increasing, each at most nk rows (the harmonics'
+  // component kr - start stays below nk)
+  if (sg.n < 1 || sg.n > kFusedSegs || sg.start[0] != 0) return hipErrorInvalidValue;
+  for (int q = 0; q < sg.n; ++q) {
+    const int end = q + 1 < sg.n ? sg.start[q + 1] : nkr;
+    if (end <= sg.start[q] || end - sg.start[q] > nk) return hipErrorInvalidValue;
+  }
   const int nw = (nk + 3) / 4 + 1;  // a product wave per group of four components, and the staging wave
-  const size_t lds = sizeof(float) * (2 * (size_t)kFuseRows * 2 * mp + 2 * (size_t)kFuseRows + 2 * kOuterEdges);
-  if (alpha_hm2 && L != 4) return hipErrorInvalidValue;
+  const size_t lds =
+      sizeof(float) * (2 * (size_t)kFuseRows * 2 * mpk + 2 * (size_t)kFuseRows + (size_t)sg.n * kOuterEdges);
   const size_t nq = (size_t)n_nodes * H * fuse_groups(L) * 16;  // entries of the re-laid features
   const uint4* fhm = (const uint4*)featq;
   const uint2* flo = (const uint2*)(fhm + nq);
@@ -2305,19 +2328,26 @@ hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, co
   const int nrx = (n + kXcds - 1) / kXcds;
   const int64_t blocks = (int64_t)kXcds * ((nrx + rpw - 1) / rpw) * H;
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  switch (L) {
-#define E2F_CASE(LL)                                                                                          \
-  case LL:                                                                                                    \
-    if (hipError_t e = allow_lds(k_outer_fused<LL, 512>, lds); e != hipSuccess) return e;                     \
-    k_outer_fused<LL, 512><<<(unsigned)blocks, 64 * nw, lds, s>>>(Re, row_ptr, col, alpha_hm, alpha_hm2,   \
-                                                                  n_edges, fhm, flo,                           \
-                                                                  order, F, n, nrx, rpw, C, H, hdiv, n_nodes,  \
-                                                                  accumulate, y);                              \
-    break;
-    E2F_CASE(0) E2F_CASE(1) E2F_CASE(2) E2F_CASE(3) E2F_CASE(4)
-#undef E2F_CASE
-    default: return hipErrorInvalidValue;
+#define E2F_LAUNCH(LL, KK)                                                                                     \
+  do {                                                                                                         \
+    if (hipError_t e = allow_lds(k_outer_fused<LL, 512, KK>, lds); e != hipSuccess) return e;                  \
+    k_outer_fused<LL, 512, KK><<<(unsigned)blocks, 64 * nw, lds, s>>>(Re, row_ptr, col, sg, n_edges, fhm, flo,  \
+                                                                      order, F, n, nrx, rpw, C, H, hdiv,       \
+                                                                      n_nodes, accumulate, y);                 \
+  } while (0)
+  if (nkr != nk) {
+    E2F_LAUNCH(4, 30);
+  } else {
+    switch (L) {
+      case 0: E2F_LAUNCH(0, 1); break;
+      case 1: E2F_LAUNCH(1, 4); break;
+      case 2: E2F_LAUNCH(2, 9); break;
+      case 3: E2F_LAUNCH(3, 16); break;
+      case 4: E2F_LAUNCH(4, 25); break;
+      default: return hipErrorInvalidValue;
+    }
   }
+#undef E2F_LAUNCH
   return hipGetLastError();
 }
 

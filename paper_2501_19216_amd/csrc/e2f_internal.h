@@ -175,24 +175,45 @@ constexpr int fuse_kpos(int nk, int be) {
 static_assert(fuse_ks(25, 1) == 3 && fuse_kpos(25, 24) == 10 && fuse_kpos(25, 19) == 4 && fuse_kpos(25, 7) == 7 &&
                   fuse_ks(16, 0) == 4 && fuse_ks(1, 0) == 1 && fuse_ks(9, 0) == 3,
               "K positions of the fused layout");
+// The K rows of F may stack several filter degrees (alpha / D^f, one pass
+// over the edges for several degrees): nkr rows, in segments of (f+1)^2 rows
+// per degree f, the j-side component be of degree f's segment at row
+// start + be (the plain layer: one segment, nkr = nk).  Rows k stay the nk
+// output components; the functions below with nk take rows k or, with nkr,
+// K rows.
 // offset (floats) of sub-block (rt, mt) inside a q block, rt-major
-constexpr int fuse_blk(int nk, int rt, int mt) {
+constexpr int fuse_blk(int nk, int nkr, int rt, int mt) {
   int off = 0;
   for (int a = 0; a < fuse_tiles(nk); ++a)
-    for (int b = 0; b < fuse_tiles(nk); ++b) {
+    for (int b = 0; b < fuse_tiles(nkr); ++b) {
       if (a == rt && b == mt) return off;
-      off += 4 * fuse_kc(nk, b) * fuse_rows(nk, a);
+      off += 4 * fuse_kc(nkr, b) * fuse_rows(nk, a);
     }
   return off;
 }
-constexpr int fuse_qblock(int nk) { return fuse_blk(nk, fuse_tiles(nk), 0); }
+constexpr int fuse_qblock(int nk, int nkr) { return fuse_blk(nk, nkr, fuse_tiles(nk), 0); }
 // floats of one receiver's F, rounded up to 64 (256-byte rows)
-constexpr int fuse_stride(int nk) { return (nk * fuse_qblock(nk) + 63) / 64 * 64; }
-// position of F[k][be][q] in a receiver's row
-constexpr int fuse_pos(int nk, int k, int be, int q) {
-  return q * fuse_qblock(nk) + fuse_blk(nk, k / 16, be / 16) +
-         (fuse_kpos(nk, be) / 4 * fuse_rows(nk, k / 16) + k % 16) * 4 + fuse_kpos(nk, be) % 4;
+constexpr int fuse_stride(int nk, int nkr) { return (nk * fuse_qblock(nk, nkr) + 63) / 64 * 64; }
+// position of F[k][kr][q] (kr a K row) in a receiver's row
+constexpr int fuse_pos(int nk, int nkr, int k, int kr, int q) {
+  return q * fuse_qblock(nk, nkr) + fuse_blk(nk, nkr, k / 16, kr / 16) +
+         (fuse_kpos(nkr, kr) / 4 * fuse_rows(nk, k / 16) + k % 16) * 4 + fuse_kpos(nkr, kr) % 4;
 }
+// K rows of the stacked degrees degs[0 .. nd) (a degree -1: every filter
+// degree in one segment of nk rows)
+inline int fuse_krows(int nk, const int* degs, int nd) {
+  int r = 0;
+  for (int s = 0; s < nd; ++s) r += degs[s] < 0 ? nk : (degs[s] + 1) * (degs[s] + 1);
+  return r;
+}
+// the alpha / D^f passes at L = 4: degrees 3 and 2 (25 K rows), then 4, 1
+// and 0 (30 K rows)
+struct YnormPass {
+  int nd;       // segments
+  int degs[3];  // their filter degrees
+};
+constexpr int kYnormPasses4 = 2;
+constexpr YnormPass kYnormPass4[kYnormPasses4] = {{2, {3, 2, 0}}, {3, {4, 1, 0}}};
 // K_x by position of F (CSR over the positions 0 .. fuse_stride - 1): the
 // entries of position p are idx[e] (the component x) and coef[e] (float64,
 // path weights w[a][f][o] included) for e in ptr[p] .. ptr[p+1] - 1.
@@ -201,13 +222,13 @@ struct FuseTable {
   std::vector<int> idx;
   std::vector<double> coef;
 };
-// f >= 0: only the terms of filter degree f (the T rows of j-side degree b
-// with the receiver's harmonics of degree u = f - b), for the per-degree
-// weights alpha / D^f.  f2 >= 0 (L = 4): two degrees in one table, those of
-// f at the j-side components be (f <= 3: be < 16, the first K tile) and those
-// of f2 at 16 + be (f2 <= 2: be < 9, the second tile's nine rows), for one
-// aggregation pass whose A rows carry the two degrees' weights
-FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, int f = -1, int f2 = -1);
+// degs[0 .. nd): the segments of K rows (fuse_krows): a degree f >= 0 takes
+// only the terms of filter degree f (the T rows of j-side degree b with the
+// receiver's harmonics of degree u = f - b), for the per-degree weights
+// alpha / D^f, at rows start + be of its segment; -1 takes every term (the
+// plain layer).  nkr >= fuse_krows: the K rows of the layout (rows past the
+// segments hold zeros), so that one degree alone can use the plain layout.
+FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, const int* degs, int nd, int nkr);
 
 // ---------------------------------------------------------------- device side
 // Device copies of one LayerTables (pointers into one allocation).

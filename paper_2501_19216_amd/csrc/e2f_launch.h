@@ -167,21 +167,34 @@ hipError_t launch_outer_agg(const DevTables& t, const float* Re, const int64_t* 
 // (L <= kFuseMaxL, C = 16 H, and the re-laid features of n_nodes atoms
 // addressable with 32-bit entry offsets)
 bool outer_fused_supported(int L, int C, int H, int64_t n_nodes);
-hipError_t launch_fuse_build(int L, const int* fptr, const int* fidx, const double* fcoef, const double* R,
-                             const int32_t* order, int n, float* F, hipStream_t s);
+// nkr: the K rows of the table's layout (fuse_stride(nk, nkr) floats a row)
+hipError_t launch_fuse_build(int L, int nkr, const int* fptr, const int* fidx, const double* fcoef,
+                             const double* R, const int32_t* order, int n, float* F, hipStream_t s);
 // featq: the features re-laid and split into bfloat16 parts by
 // launch_feat_qmajor, n_nodes * C * 6 * fuse_groups(L) floats of space (a
 // 16-byte and an 8-byte array of n_nodes * C / 16 * fuse_groups(L) * 16
 // entries each)
 int fuse_groups(int L);
 hipError_t launch_feat_qmajor(int L, const float* feat, int n, int C, float* featq, hipStream_t s);
+// The segments of the K rows of one fused aggregation (nkr rows, F from a
+// table of that layout): segment q, from K row start[q] to the next start
+// (or nkr), holds the components 0 .. of R(p_j) weighted by alpha_hm[q]
+// ([H / hdiv][n_edges] head-major, NULL: weight 1).  The plain layer: one
+// segment of nk rows; alpha / D^f: a segment per filter degree f of the
+// table, (f+1)^2 rows with the weights alpha / D^f.
+constexpr int kFusedSegs = 5;
+struct FusedSegs {
+  const float* alpha_hm[kFusedSegs];
+  int start[kFusedSegs];  // start[0] = 0, increasing; no segment longer than nk
+  int n;                  // 1 .. kFusedSegs
+};
+// K row counts the fused aggregation is built for: nk, and 30 at L = 4
+// (degrees 4, 1 and 0 of alpha / D^f)
+bool fused_krows_supported(int L, int nkr);
 // accumulate: the result is added to y (the sum over the filter degrees of
 // alpha / D^f), else stored
-// alpha_hm2 (L = 4, else NULL): the weights of a second filter degree for
-// the rows of the second K tile (components 0 .. 8), F from a paired table
-hipError_t launch_outer_fused(int L, const float* Re, const int64_t* row_ptr, const int32_t* col,
-                              const float* alpha_hm, const float* alpha_hm2, int64_t n_edges, const float* featq,
-                              const int32_t* order,
+hipError_t launch_outer_fused(int L, int nkr, const float* Re, const int64_t* row_ptr, const int32_t* col,
+                              const FusedSegs& sg, int64_t n_edges, const float* featq, const int32_t* order,
                               const float* F, int n, int C, int H, int hdiv, int n_nodes, bool accumulate, float* y,
                               hipStream_t s);
 // y[order[r]] from S row r (head-major like T), r < n; shared_s: every r

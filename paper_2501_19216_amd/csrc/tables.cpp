@@ -543,16 +543,25 @@ GeomSchedule geom_schedule(const LayerTables& t, int qc) {
   return gs;
 }
 
-FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, int f, int f2) {
+FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, const int* degs, int nd, int nkr) {
   const int nk = t.nk;
   FuseTable ft;
-  if (t.L > kFuseMaxL) return ft;
+  if (t.L > kFuseMaxL || nkr < fuse_krows(nk, degs, nd)) return ft;
+  // first K row of each filter degree's segment (-1: not in this table),
+  // and of the segment that takes every term (the plain layer: b + u up to 2L)
+  int start[kFuseMaxL + 1], start_all = -1;
+  for (int f = 0; f <= kFuseMaxL; ++f) start[f] = -1;
+  for (int s = 0, r = 0; s < nd; ++s) {
+    if (degs[s] < 0) start_all = r;
+    else start[degs[s]] = r;
+    r += degs[s] < 0 ? nk : (degs[s] + 1) * (degs[s] + 1);
+  }
   std::vector<int> row_b(t.dimT, 0);  // j-side degree of every T row
   for (const Block& B : t.blocks)
     for (int de = 0; de < 2 * B.d + 1; ++de) row_b[B.toff + de] = B.b;
   // dense K[pos][x], accumulated over the T rows r that link a recouple entry
   // (k, r) with a coupling entry (r, be, q)
-  const int np = fuse_stride(nk);
+  const int np = fuse_stride(nk, nkr);
   std::vector<double> K((size_t)np * nk, 0.0), mag((size_t)np * nk, 0.0);
   for (int o = 0; o <= t.L; ++o) {
     const int ncol = t.q_ncol[o];
@@ -569,16 +578,14 @@ FuseTable fuse_table(const LayerTables& t, const std::vector<double>& w, int f, 
           int u = 0;  // x = u^2 + gamma: the degree of the receiver's harmonic
           while ((u + 1) * (u + 1) <= x) ++u;
           const int deg = row_b[r] + u;
-          int shift = 0;  // K row of a j-side component be: be + shift
-          if (f2 >= 0) {
-            if (deg == f2) shift = 16;
-            else if (deg != f) continue;
-          } else if (f >= 0 && deg != f) {
-            continue;
+          int shift = start_all;  // K row of a j-side component be: shift + be
+          if (shift < 0) {
+            if (deg > kFuseMaxL || start[deg] < 0) continue;
+            shift = start[deg];
           }
           for (int sl = s0; sl < s1; ++sl)
             for (int e2 = t.m_ptr[sl]; e2 < t.m_ptr[sl + 1]; ++e2) {
-              const size_t at = (size_t)fuse_pos(nk, k, t.m_ridx[e2] + shift, a * a + sl - s0) * nk + x;
+              const size_t at = (size_t)fuse_pos(nk, nkr, k, t.m_ridx[e2] + shift, a * a + sl - s0) * nk + x;
               K[at] += cq * t.m_coef[e2];
               mag[at] += std::fabs(cq * t.m_coef[e2]);
             }
