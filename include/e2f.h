@@ -192,7 +192,7 @@ typedef struct {
                             E2F_FORM_FUSED: up to L = 4, with heads whose width is a multiple of 16,
                             the aggregation applies the i-side recouple itself (with y_norm, per
                             filter degree f with the weights alpha / D^f and the terms b + u = f,
-                            at L = 4 the degrees 3 and 2, and 1 and 0, in one pass each) (the
+                            at L = 4 in two passes: degrees 3 and 2, then 4, 1 and 0) (the
                             j-side coupling and the recouple of Thm. 3.3 composed into one
                             (L+1)^2 x (L+1)^4 matrix per receiver), so S is never stored;
                             elsewhere the split form.  E2F_FORM_SPLIT: S is written and recoupled
