@@ -74,9 +74,8 @@ struct e2f_ctx {
       int nkr = 0;
     };
     FuseTab f;
-    // the same per filter degree f (alpha / D^f), L + 1 tables
-    std::vector<FuseTab> ff;
-    // at L = 4: the passes of kYnormPass4, their degrees stacked in the K rows
+    // the passes of alpha / D^f (ynorm_passes), their degrees stacked in the
+    // K rows
     std::vector<FuseTab> fy;
   };
   std::vector<std::vector<CoefSet>> coefs;
@@ -424,17 +423,10 @@ e2f_status coef_of(e2f_ctx* ctx, int L, const std::vector<double>& w, bool allow
   push_array(blob, o, ft.ptr);
   push_array(blob, o, ft.idx);
   push_array(blob, o, ft.coef);
-  std::vector<FuseTable> ftf;  // o[8 + L + 3f] .. o[10 + L + 3f]
-  for (int f = 0; f <= L && !ft.coef.empty(); ++f) {
-    ftf.push_back(fuse_table(t, w, &f, 1, t.nk));
-    push_array(blob, o, ftf.back().ptr);
-    push_array(blob, o, ftf.back().idx);
-    push_array(blob, o, ftf.back().coef);
-  }
-  const bool stacked = !ft.coef.empty() && L == kFuseMaxL;  // o[11 + 4L + 3q] .. o[13 + 4L + 3q]
-  for (int q = 0; q < (stacked ? kYnormPasses4 : 0); ++q) {
-    const YnormPass& yp = kYnormPass4[q];
-    const FuseTable fp = fuse_table(t, w, yp.degs, yp.nd, fuse_krows(t.nk, yp.degs, yp.nd));
+  YnormPass yps[kYnormMaxPasses];  // o[8 + L + 3q] .. o[10 + L + 3q]
+  const int nyp = ft.coef.empty() ? 0 : ynorm_passes(L, yps);
+  for (int q = 0; q < nyp; ++q) {
+    const FuseTable fp = fuse_table(t, w, yps[q].degs, yps[q].nd, fuse_krows(t.nk, yps[q].degs, yps[q].nd));
     push_array(blob, o, fp.ptr);
     push_array(blob, o, fp.idx);
     push_array(blob, o, fp.coef);
@@ -464,9 +456,7 @@ e2f_status coef_of(e2f_ctx* ctx, int L, const std::vector<double>& w, bool allow
                                        (const double*)((char*)mem + o[k + 2]), nkr};
     };
     c.f = tab(5 + L, t.nk);
-    for (int f = 0; f <= L; ++f) c.ff.push_back(tab(8 + L + 3 * f, t.nk));
-    for (int q = 0; q < (stacked ? kYnormPasses4 : 0); ++q)
-      c.fy.push_back(tab(11 + 4 * L + 3 * q, fuse_krows(t.nk, kYnormPass4[q].degs, kYnormPass4[q].nd)));
+    for (int q = 0; q < nyp; ++q) c.fy.push_back(tab(8 + L + 3 * q, fuse_krows(t.nk, yps[q].degs, yps[q].nd)));
   }
   sets.push_back(std::move(c));
   out = &sets.back();
@@ -622,14 +612,14 @@ int fused_split(const e2f_conv_params* p, int64_t n) {
 }
 
 // Floats of one receiver's F in the fused form: the largest layout among
-// the forward's passes (the alpha / D^f passes at L = 4 stack degrees in
-// more K rows).
+// the forward's passes (the alpha / D^f passes stack degrees in more K
+// rows).
 int fused_row_floats(const e2f_conv_params* p) {
   const int L = p->lmax, nk = nk_of(L);
   int fl = fuse_stride(nk, nk);
-  if (p->y_norm && L == kFuseMaxL)
-    for (int q = 0; q < kYnormPasses4; ++q)
-      fl = std::max(fl, fuse_stride(nk, fuse_krows(nk, kYnormPass4[q].degs, kYnormPass4[q].nd)));
+  YnormPass yps[kYnormMaxPasses];
+  const int nyp = p->y_norm && L <= kFuseMaxL ? ynorm_passes(L, yps) : 0;
+  for (int q = 0; q < nyp; ++q) fl = std::max(fl, fuse_stride(nk, fuse_krows(nk, yps[q].degs, yps[q].nd)));
   return fl;
 }
 
@@ -708,8 +698,7 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
     if (!allow_upload && ctx->couple.find(std::make_pair(L, cgroups)) == ctx->couple.end())
       return fail(E2F_EINVAL, "the coupling schedule is not resident on the context; call e2f_wigner6j_prepare first");
     if ((rs = couple_of(ctx, L, cgroups, cpl)) != E2F_OK) return rs;
-  } else if (!cs->f.ptr ||
-             (p->y_norm && ((int)cs->ff.size() != L + 1 || (L == kFuseMaxL && (int)cs->fy.size() != kYnormPasses4)))) {
+  } else if (!cs->f.ptr || (p->y_norm && cs->fy.empty())) {
     return fail(E2F_EDEVICE, "the fused recouple table of L = %d is missing", L);
   }
   if (n == 0) return E2F_OK;
@@ -794,8 +783,8 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
       // filter degrees), then the aggregation with the recouple applied; the
       // passes after the first add to y.  The plain layer: one pass.  With
       // y_norm the weights alpha / D^f and the terms b + u = f of each degree
-      // f: at L = 4 two passes, the degrees of kYnormPass4 (3 and 2, then 4,
-      // 1 and 0), each degree in (f+1)^2 K rows; below, one pass per degree.
+      // f, in (f+1)^2 K rows: the passes of ynorm_passes (one below L = 4;
+      // at L = 4 degrees 3 and 2, then 4, 1 and 0).
       int npass = 0;
       const int all_degs[1] = {-1};
       auto pass = [&](const e2f_ctx::CoefSet::FuseTab& tab, const int* degs, int nd) -> e2f_status {
@@ -804,7 +793,7 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
         for (int q = 0, r = 0; q < nd; ++q) {
           sg.alpha_hm[q] = degs[q] < 0 ? alpha_hm : alpha_hm + (size_t)degs[q] * H * n_edges;
           sg.start[q] = r;
-          r += degs[q] < 0 || nd == 1 ? nk : (degs[q] + 1) * (degs[q] + 1);
+          r += degs[q] < 0 ? nk : (degs[q] + 1) * (degs[q] + 1);
         }
         E2F_TIMED("fuse_build", launch_fuse_build(L, tab.nkr, tab.ptr, tab.idx, tab.coef, Rr, ord, nb, S, s));
         E2F_TIMED("aggregate", launch_outer_fused(L, tab.nkr, Re, row_ptr, col_idx, sg, n_edges, featq, ord, S, nb, C,
@@ -813,12 +802,12 @@ e2f_status forward_impl(e2f_ctx* ctx, const e2f_conv_params* p, const float* pos
       };
       if (!ynorm) {
         if ((rs = pass(cs->f, all_degs, 1)) != E2F_OK) return rs;
-      } else if (L == kFuseMaxL) {
-        for (int q = 0; q < kYnormPasses4; ++q)
-          if ((rs = pass(cs->fy[q], kYnormPass4[q].degs, kYnormPass4[q].nd)) != E2F_OK) return rs;
       } else {
-        for (int fd = 0; fd <= L; ++fd)
-          if ((rs = pass(cs->ff[fd], &fd, 1)) != E2F_OK) return rs;
+        YnormPass yps[kYnormMaxPasses];
+        const int nyp = ynorm_passes(L, yps);
+        if (nyp != (int)cs->fy.size()) return fail(E2F_EDEVICE, "the alpha / D^f tables of L = %d are missing", L);
+        for (int q = 0; q < nyp; ++q)
+          if ((rs = pass(cs->fy[q], yps[q].degs, yps[q].nd)) != E2F_OK) return rs;
       }
       continue;
     }

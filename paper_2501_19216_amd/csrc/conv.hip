@@ -1182,7 +1182,7 @@ __global__ __launch_bounds__(LB) void k_outer_fused(const float* __restrict__ Re
       auto recouple = [&](auto nlc) {
         constexpr int NL = decltype(nlc)::value;
         float4 fv[2][MT][MK];
-        auto loadf = [&](int w, float4 (*f)[MT]) {
+        auto loadf = [&](int w, float4 (*f)[MK]) {
           const int q = q0 + w;  // < NK for w < NL
 #pragma unroll
           for (int rt = 0; rt < MT; ++rt)
@@ -2295,9 +2295,11 @@ hipError_t launch_feat_qmajor(int L, const float* feat, int n, int C, float* fea
   return hipGetLastError();
 }
 
+// (the stacked alpha / D^f passes: 5, 14 and 30 K rows at L = 1, 2, 3, and
+// 30 at L = 4)
 bool fused_krows_supported(int L, int nkr) {
   const int nk = (L + 1) * (L + 1);
-  return L >= 0 && L <= kFuseMaxL && (nkr == nk || (L == 4 && nkr == 30));
+  return L >= 0 && L <= kFuseMaxL && (nkr == nk || (L == 1 && nkr == 5) || (L == 2 && nkr == 14) || (L >= 3 && nkr == 30));
 }
 
 hipError_t launch_outer_fused(int L, int nkr, const float* Re, const int64_t* row_ptr, const int32_t* col,
@@ -2336,7 +2338,13 @@ hipError_t launch_outer_fused(int L, int nkr, const float* Re, const int64_t* ro
                                                                       n_nodes, accumulate, y);                 \
   } while (0)
   if (nkr != nk) {
-    E2F_LAUNCH(4, 30);
+    switch (L) {
+      case 1: E2F_LAUNCH(1, 5); break;
+      case 2: E2F_LAUNCH(2, 14); break;
+      case 3: E2F_LAUNCH(3, 30); break;
+      case 4: E2F_LAUNCH(4, 30); break;
+      default: return hipErrorInvalidValue;
+    }
   } else {
     switch (L) {
       case 0: E2F_LAUNCH(0, 1); break;

@@ -206,14 +206,25 @@ inline int fuse_krows(int nk, const int* degs, int nd) {
   for (int s = 0; s < nd; ++s) r += degs[s] < 0 ? nk : (degs[s] + 1) * (degs[s] + 1);
   return r;
 }
-// the alpha / D^f passes at L = 4: degrees 3 and 2 (25 K rows), then 4, 1
-// and 0 (30 K rows)
+// The alpha / D^f passes of the fused aggregation, each a set of filter
+// degrees stacked in the K rows: below L = 4 one pass of every degree (L, L-1,
+// .. 0: 30 K rows at L = 3); at L = 4 (55 rows in all) two passes within two
+// K tiles, degrees 3 and 2 (25 rows), then 4, 1 and 0 (30 rows).
 struct YnormPass {
-  int nd;       // segments
-  int degs[3];  // their filter degrees
+  int nd;                   // segments
+  int degs[kFuseMaxL + 1];  // their filter degrees
 };
-constexpr int kYnormPasses4 = 2;
-constexpr YnormPass kYnormPass4[kYnormPasses4] = {{2, {3, 2, 0}}, {3, {4, 1, 0}}};
+constexpr int kYnormMaxPasses = 2;
+inline int ynorm_passes(int L, YnormPass* out) {
+  if (L == 4) {
+    out[0] = YnormPass{2, {3, 2, 0, 0, 0}};
+    out[1] = YnormPass{3, {4, 1, 0, 0, 0}};
+    return 2;
+  }
+  out[0] = YnormPass{L + 1, {0, 0, 0, 0, 0}};
+  for (int s = 0; s <= L; ++s) out[0].degs[s] = L - s;
+  return 1;
+}
 // K_x by position of F (CSR over the positions 0 .. fuse_stride - 1): the
 // entries of position p are idx[e] (the component x) and coef[e] (float64,
 // path weights w[a][f][o] included) for e in ptr[p] .. ptr[p+1] - 1.

@@ -188,8 +188,8 @@ struct FusedSegs {
   int start[kFusedSegs];  // start[0] = 0, increasing; no segment longer than nk
   int n;                  // 1 .. kFusedSegs
 };
-// K row counts the fused aggregation is built for: nk, and 30 at L = 4
-// (degrees 4, 1 and 0 of alpha / D^f)
+// K row counts the fused aggregation is built for: nk, and those of the
+// stacked alpha / D^f passes (5, 14, 30 at L = 1, 2, 3; 30 at L = 4)
 bool fused_krows_supported(int L, int nkr);
 // accumulate: the result is added to y (the sum over the filter degrees of
 // alpha / D^f), else stored

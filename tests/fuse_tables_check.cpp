@@ -6,9 +6,9 @@
 //     b <= f);
 //   * the per-degree tables sum to the plain layer's table (the degrees f =
 //     0 .. L partition its terms);
-//   * at L = 4 each stacked pass (its degrees in segments of (f+1)^2 K rows)
+//   * each pass of ynorm_passes (its degrees in segments of (f+1)^2 K rows)
 //     equals the per-degree tables moved to the segment's rows, entry by
-//     entry, with nothing else in it.
+//     entry, with nothing else in it, and the passes cover every degree once.
 // Prints one line per check, "ok" or "FAIL", and exits 1 on a failure.
 #include <cmath>
 #include <cstdio>
@@ -61,9 +61,17 @@ int main() {
     std::printf("L=%d per-degree rows and sum: %s (entries outside %zu, |sum - plain| %.3e of %.3e)\n", L,
                 ok1 ? "ok" : "FAIL", outside, dsum, fmax);
     all_ok = all_ok && ok1;
-    if (L != kFuseMaxL) continue;
-    for (int q = 0; q < kYnormPasses4; ++q) {
-      const YnormPass& yp = kYnormPass4[q];
+    YnormPass yps[kYnormMaxPasses];
+    const int nyp = ynorm_passes(L, yps);
+    std::vector<int> seen(L + 1, 0);
+    for (int q = 0; q < nyp; ++q)
+      for (int s = 0; s < yps[q].nd; ++s) ++seen[yps[q].degs[s]];
+    bool cover = true;
+    for (int f = 0; f <= L; ++f) cover = cover && seen[f] == 1;
+    std::printf("L=%d passes cover every degree once: %s\n", L, cover ? "ok" : "FAIL");
+    all_ok = all_ok && cover;
+    for (int q = 0; q < nyp; ++q) {
+      const YnormPass& yp = yps[q];
       const int nkr = fuse_krows(nk, yp.degs, yp.nd);
       bool okp = true;
       const std::vector<double> P = dense(fuse_table(t, w, yp.degs, yp.nd, nkr), fuse_stride(nk, nkr), nk, okp);

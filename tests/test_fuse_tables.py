@@ -24,4 +24,5 @@ def test_fuse_tables_stacked_and_per_degree(tmp_path):
     print(r.stdout)
     lines = [l for l in r.stdout.splitlines() if l.strip()]
     assert r.returncode == 0, r.stdout + r.stderr
-    assert len(lines) == 5 + 2 and all(": ok" in l for l in lines), r.stdout
+    # per L: the per-degree check, the cover check and one line per pass (two at L = 4)
+    assert len(lines) == 5 * 2 + 6 and all(": ok" in l for l in lines), r.stdout

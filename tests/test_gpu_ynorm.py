@@ -1,7 +1,9 @@
 """Alg. 1's per-degree attention weights alpha / D^f (Y-based filters, the
 y_norm flag): both forms of the layer on the GPU against the oracle's
-definition of the variant.  The factorised forward aggregates once per
-filter degree f and recouples the terms of degree b + u = f from S^(f).
+definition of the variant.  The factorised forward weights the terms of
+filter degree b + u = f by alpha / D^f: the two-kernel form aggregates once
+per degree and recouples those terms from S^(f); the fused form stacks
+degrees in the K rows of one pass (one pass below L = 4, two at L = 4).
 
 Run with -m gpu."""
 import numpy as np
@@ -67,8 +69,8 @@ def test_y_norm_workloads(e2f, ctx, name, rows, mix):
 @pytest.mark.parametrize("form", ["split", "fused"])
 def test_y_norm_both_forms(e2f, ctx, form):
     # alpha / D^f in both forms of the aggregation: the two-kernel form (S^(f)
-    # per degree, recoupled by its terms b + u = f) and the fused form (one
-    # pass per degree with F^(f) of the same terms)
+    # per degree, recoupled by its terms b + u = f) and the fused form (two
+    # passes at L = 4, each with the terms of the degrees its K rows stack)
     inp, rp, ci, alpha = case("water2000_L4")
     wl = inp.workload
     r = sample_rows(inp.pos.shape[0], 64, seed=21)
@@ -79,6 +81,32 @@ def test_y_norm_both_forms(e2f, ctx, form):
     err = o.max_rel_err(got[r], ref, wl.lmax)
     print("water2000 y_norm %s: err %.3e" % (form, err))
     assert err <= TOL_F32
+
+
+@pytest.mark.parametrize("L", [1, 2, 3])
+def test_y_norm_fused_below_l4(e2f, ctx, L):
+    # below L = 4 the fused form runs alpha / D^f in one pass whose K rows
+    # stack every filter degree (L, .., 0; 5, 14 and 30 rows at L = 1, 2, 3);
+    # heads of 16 channels, random positions (contacts down to about 0.1 A),
+    # rows of up to about 250 edges (two staging chunks); both forms against
+    # the oracle
+    rng = np.random.default_rng(70 + L)
+    C, H, cutoff = 32, 2, 5.0
+    pos = syn.quantize(rng.uniform(0.0, 11.0, size=(600, 3)))  # about half the rows longer than 128
+    n = pos.shape[0]
+    rp, ci = o.neighbor_list(pos, cutoff)
+    feat = rng.standard_normal((n, (L + 1) ** 2, C)).astype(np.float32)
+    alpha = rng.uniform(0.1, 1.0, size=(len(ci), H)).astype(np.float32)
+    w = rng.uniform(0.5, 1.5, size=(L + 1) ** 3)
+    r = sample_rows(n, 48, seed=L)
+    ref = o.layer(L, H, pos, feat, rp, ci, alpha, w, rows=r, y_norm=True)
+    print("L%d y_norm: %d atoms, %d edges, longest row %d" % (L, n, len(ci), np.diff(rp).max()), flush=True)
+    for form in ("fused", "split"):
+        got = e2f.e2f_wigner6j_conv_forward(ctx, gpu(pos), gpu(feat), gpu(rp), gpu(ci), gpu(alpha), L, H, cutoff,
+                                            path_w=w, y_norm=True, form=form).cpu().numpy()
+        err = o.max_rel_err(got[r], ref, L)
+        print("L%d y_norm %s: err %.3e" % (L, form, err), flush=True)
+        assert err <= TOL_F32
 
 
 def test_y_norm_short_contacts_and_slices(e2f, ctx):
