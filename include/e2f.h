@@ -196,10 +196,11 @@ typedef struct {
                             j-side coupling and the recouple of Thm. 3.3 composed into one
                             (L+1)^2 x (L+1)^4 matrix per receiver), so S is never stored;
                             elsewhere the split form.  E2F_FORM_SPLIT: S is written and recoupled
-                            by a second kernel.  E2F_FORM_AUTO (0): fused at L = 4 where the split
-                            form's S (n dimT C floats) would exceed 256 MiB (beyond the on-die
-                            cache its round trip through HBM outweighs the fused form's extra
-                            matrix-core work per receiver), else split.  All forms give the same
+                            by a second kernel.  E2F_FORM_AUTO (0): fused wherever it applies with
+                            y_norm (the split form then aggregates once per degree), and at L = 4
+                            where the split form's S (n dimT C floats) would exceed 256 MiB
+                            (beyond the on-die cache its round trip through HBM outweighs the
+                            fused form's extra matrix-core work per receiver), else split.  All forms give the same
                             result up to rounding order: the fused form multiplies on the bf16
                             matrix cores with each float operand split into three bf16 parts
                             (x = hi + mid + lo exactly) and the six cross products that reach

@@ -596,17 +596,21 @@ struct FwdLayout {
 
 // The split of each head into channel groups of 16 with which the
 // aggregation applies the recouple itself (L <= 4, head width a multiple of
-// 16; with y_norm one pass per filter degree); 0 where the forward writes S.
-// The automatic choice takes the fused form at L = 4 once S would outgrow
-// the 256 MiB on-die cache (measured: 1,000 atoms with 32 neighbours at L =
-// 4, S 232 MB, 0.31 ms split vs 0.34 fused; 2,000 atoms with 72, S 465 MB,
-// 0.90 vs 0.84; 20,000 with 80, 7.17 vs 6.27; at L = 3 the split form was as
-// fast or faster at every size).
+// 16; with y_norm the filter degrees stacked in the K rows of one or two
+// passes); 0 where the forward writes S.  The automatic choice takes the
+// fused form with y_norm (the two-kernel form then aggregates once per
+// degree: 20,000 atoms, L = 1 .. 4, 1.47 ms fused vs 2.16, 2.04 vs 4.74,
+// 4.79 vs 9.77, 10.6 vs 34.5),
+// and otherwise at L = 4 once S would outgrow the 256 MiB on-die cache
+// (measured: 1,000 atoms with 32 neighbours at L = 4, S 232 MB, 0.31 ms
+// split vs 0.34 fused; 2,000 atoms with 72, S 465 MB, 0.90 vs 0.84; 20,000
+// with 80, 7.17 vs 6.27; at L = 3 the split form was as fast or faster at
+// every size).
 int fused_split(const e2f_conv_params* p, int64_t n) {
   const int dh = p->channels / p->heads;
   if (p->form == E2F_FORM_SPLIT || dh % 16 != 0) return 0;
   if (!outer_fused_supported(p->lmax, p->channels, p->channels / 16, n)) return 0;
-  if (p->form == E2F_FORM_FUSED) return dh / 16;
+  if (p->form == E2F_FORM_FUSED || p->y_norm) return dh / 16;
   const double s_bytes = 4.0 * (double)n * (double)node_tp_dim(p->lmax) * p->channels;
   return p->lmax == kFuseMaxL && s_bytes > 256.0 * 1024 * 1024 ? dh / 16 : 0;
 }
