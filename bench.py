@@ -472,6 +472,25 @@ def main():
                                                              out=glob_out)
     glob_only()
     ms_glob = timed(glob_only, args.steps)
+    # Alg. 1's per-degree weights alpha / D^f (the y_norm flag): both forms of
+    # the factorised forward and the per-edge baseline
+    yn_out = torch.empty_like(feat)
+    yn = {}
+    for form in ("fused", "split"):
+        def fy(form=form):
+            e2f.e2f_wigner6j_conv_forward(ctx, pos, feat, row_ptr, col, alpha, L, H, wl.cutoff, mix_w=mix_w,
+                                          graph_id=gid, out=yn_out, y_norm=True, form=form)
+        fy()
+        yn[form + "_ms"] = timed(fy, args.steps)
+
+    def fy_edge():
+        e2f.e2f_edge_tp_conv_forward(ctx, pos, feat, row_ptr, col, alpha, L, H, wl.cutoff, mix_w=mix_w,
+                                     graph_id=gid, out=yn_out, y_norm=True)
+
+    fy_edge()
+    yn["edge_tp_ms"] = timed(fy_edge, args.steps)
+    yn["speedup_vs_edge_tp"] = yn["edge_tp_ms"] / yn["fused_ms"]
+    del yn_out
     # the backward of the timed forward (fp32 mixing): both products, then each alone
     g_out = torch.randn(out.shape, device=dev, generator=g)
 
@@ -652,6 +671,7 @@ def main():
         "backward": {"ms": ms_bwd, "grad_feat_ms": ms_bwd_feat, "grad_alpha_ms": ms_bwd_alpha,
                      "grad_pos_ms": ms_bwd_pos},
         "global_moment": {"ms": ms_glob, "pairs": n * n, "atoms_per_s": n / (ms_glob * 1e-3)},
+        "y_norm": yn,
         "attention": {"ms": ms_att, "dk": 16, "n_rbf": 8, "bytes_GBps": (E * (4 + 4 * H) + 12.0 * n) / (ms_att * 1e-3) / 1e9},
         "aggregate_alone": a3,
         "counts": {"dimT": counts["dimT"], "coupling_entries": counts["coupling_entries"],
