@@ -184,19 +184,32 @@ __global__ __launch_bounds__(256) void k_plan_bbox(const float* __restrict__ pos
 }
 
 // Shortest nonzero edge length (fp32 bits; positive floats order like their
-// bits), one atomic per wave.
-__global__ void k_plan_dmin(const float* __restrict__ pos, const int32_t* __restrict__ rows,
-                            const int32_t* __restrict__ col, int n, int64_t n_edges, unsigned* __restrict__ dmin) {
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// bits): each thread takes a grid-stride share of the edges, the minimum is
+// reduced over the wave and the workgroup, and one atomic per workgroup
+// meets the others (one per wave made a 1.6 M-edge graph wait on 25,000
+// atomics to a single word).
+constexpr int kDminThreads = 256, kDminMaxBlocks = 2048;
+__global__ __launch_bounds__(kDminThreads) void k_plan_dmin(const float* __restrict__ pos,
+                                                            const int32_t* __restrict__ rows,
+                                                            const int32_t* __restrict__ col, int n, int64_t n_edges,
+                                                            unsigned* __restrict__ dmin) {
+  __shared__ unsigned part[kDminThreads / 64];
   unsigned v = 0x7f800000u;
-  if (e < n_edges) {
+  for (int64_t e = (int64_t)blockIdx.x * kDminThreads + threadIdx.x; e < n_edges;
+       e += (int64_t)gridDim.x * kDminThreads) {
     const int i = clamp_node(rows[e], n), j = clamp_node(col[e], n);
     const float dx = pos[3 * i] - pos[3 * j], dy = pos[3 * i + 1] - pos[3 * j + 1], dz = pos[3 * i + 2] - pos[3 * j + 2];
     const float d = sqrtf(dx * dx + dy * dy + dz * dz);
-    if (d > 0.0f && d < INFINITY) v = __float_as_uint(d);
+    if (d > 0.0f && d < INFINITY) v = min(v, __float_as_uint(d));
   }
   for (int o = 32; o > 0; o >>= 1) v = min(v, (unsigned)__shfl_xor((int)v, o));
-  if ((threadIdx.x & 63) == 0 && v != 0x7f800000u) atomicMin(dmin, v);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned m = part[0];
+    for (int w = 1; w < kDminThreads / 64; ++w) m = min(m, part[w]);
+    if (m != 0x7f800000u) atomicMin(dmin, m);
+  }
 }
 
 // The tile grid from the bounding box st (as k_plan_bbox leaves it).  The
@@ -588,9 +601,8 @@ hipError_t launch_plan_centre(const int* stats, double* origin, hipStream_t s) {
 
 hipError_t launch_plan_dmin(const float* pos, const int32_t* rows, const int32_t* col, int n, int64_t n_edges,
                             unsigned* dmin, hipStream_t s) {
-  const int64_t blocks = (n_edges + 255) / 256;
-  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  if (blocks > 0) k_plan_dmin<<<(unsigned)blocks, 256, 0, s>>>(pos, rows, col, n, n_edges, dmin);
+  const int64_t blocks = std::min<int64_t>((n_edges + kDminThreads - 1) / kDminThreads, kDminMaxBlocks);
+  if (blocks > 0) k_plan_dmin<<<(unsigned)blocks, kDminThreads, 0, s>>>(pos, rows, col, n, n_edges, dmin);
   return hipGetLastError();
 }
 
